@@ -1,0 +1,10 @@
+"""CPU oracle for Sparse Feature Attention -- test infrastructure only.
+
+Only `tests/`, `__graft_entry__.smoke()` and `bench.py`'s `cpu_baseline` leg
+may import this package.  It shares no code with the HIP library.
+"""
+from .sfa_oracle import (  # noqa: F401
+    widen, topk_select, topk_encode, bf16_rne, topk_encode_bf16, densify,
+    softmax_attention, attn_fwd, attn_fwd_rows, attn_decode, overlap_count,
+    csr_bytes,
+)
