@@ -1,0 +1,337 @@
+#!/usr/bin/env python3
+"""Benchmark of the SFA hot path on one MI355X.
+
+Default workload (the headline metric): Qwen3-like long-context forward,
+B=1, 32 query heads over 8 KV heads, n=32768, d=128, k=16, causal, bf16 V and
+output.  One step = Top-k coding of the dense fp32 Q and K
+(sfa_topk_encode x2) + the fused forward (sfa_attn_fwd), with every input
+already resident in HBM.  `--workload decode_64k` times the decode step
+(sfa_attn_decode) over the 64-sequence x 64K sparse-code KV cache instead.
+
+Prints ONE JSON line.  Besides the contract fields it carries
+  roofline      the dominant kernel's algorithmic rate (from HIP events
+                around its own launches) against the MI355X peak, and HBM
+                traffic from rocprofv3 counters when a matching summary
+                exists under profiles/;
+  cpu_baseline  the CPU oracle timed on a bounded sample of the same
+                workload on this host, scaled to the metric's unit.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2603_22300_amd as sfa  # noqa: E402
+import sfa_inputs as si  # noqa: E402
+
+METRIC = "SFA fwd tokens/s at n=32K,d=128,k=16; % of HBM/MFMA roofline"
+PEAK_MFMA_BF16 = 2.5e15      # dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12            # bytes/s
+DEV = "cuda"
+
+
+def _src_hash(name: str) -> str:
+    p = os.path.join(ROOT, "paper_2603_22300_amd", "csrc", name)
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def _traffic(kernel_file: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 PMC summary, if it was
+    taken on the current kernel source; else None."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        t = json.load(open(p))
+    except Exception:
+        return None
+    if t.get("src_sha256_16") != _src_hash(kernel_file):
+        return None
+    return t.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------
+# forward workload
+# ----------------------------------------------------------------------------
+
+def _fwd_inputs(w):
+    q = torch.empty((w.B, w.Hq, w.n, w.d), device=DEV)
+    k = torch.empty((w.B, w.Hkv, w.n, w.d), device=DEV)
+    v = torch.empty((w.B, w.Hkv, w.n, w.d), device=DEV, dtype=torch.bfloat16)
+    for b in range(w.B):
+        for h in range(w.Hq):
+            if w.zipf_s:
+                perm = si.zipf_feature_perm(w.d, w.seed, h // w.G)
+                i_, v_ = si.zipf_codes(w.n, w.d, w.k, w.zipf_s, perm, w.seed, "q", b, h, device=DEV)
+                q[b, h] = si.dense_from_codes(i_, v_, w.d)
+            else:
+                q[b, h] = si.normal((w.n, w.d), w.seed, "q", b, h, device=DEV)
+        for h in range(w.Hkv):
+            if w.zipf_s:
+                perm = si.zipf_feature_perm(w.d, w.seed, h)
+                i_, v_ = si.zipf_codes(w.n, w.d, w.k, w.zipf_s, perm, w.seed, "k", b, h, device=DEV)
+                k[b, h] = si.dense_from_codes(i_, v_, w.d)
+            else:
+                k[b, h] = si.normal((w.n, w.d), w.seed, "k", b, h, device=DEV)
+            v[b, h] = si.normal((w.n, w.d), w.seed, "v", b, h, device=DEV).to(torch.bfloat16)
+    return q, k, v
+
+
+def _overlap_count(qi: torch.Tensor, ki: torch.Tensor, d: int, G: int, causal: bool) -> int:
+    """Exact E = sum over allowed (i, j) of |S_i cap S_j| (accounting only):
+    per coordinate, the number of keys j <= i holding it, summed over the
+    query's coordinates."""
+    B, Hq, n, k = qi.shape
+    E = 0
+    for b in range(B):
+        for g in range(ki.shape[1]):
+            km = torch.zeros((n, d), dtype=torch.int32, device=qi.device)
+            km.scatter_(1, ki[b, g].long(), 1)
+            kc = torch.cumsum(km, 0) if causal else km.sum(0, keepdim=True).expand(n, d)
+            for h in range(g * G, (g + 1) * G):
+                E += int(torch.gather(kc, 1, qi[b, h].long()).sum().item())
+    return E
+
+
+def bench_fwd(w, steps, warmup, want_cpu):
+    q, k, v = _fwd_inputs(w)
+    B, Hq, Hkv, n, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
+    qi = torch.empty((B, Hq, n, kk), dtype=torch.int32, device=DEV)
+    qv = torch.empty((B, Hq, n, kk), dtype=torch.float32, device=DEV)
+    ki = torch.empty((B, Hkv, n, kk), dtype=torch.int32, device=DEV)
+    kv = torch.empty((B, Hkv, n, kk), dtype=torch.float32, device=DEV)
+    o = torch.empty((B, Hq, n, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((B, Hq, n), dtype=torch.float32, device=DEV)
+
+    def step(ev=None):
+        sfa.sfa_topk_encode(q, kk, idx=qi, val=qv)
+        sfa.sfa_topk_encode(k, kk, idx=ki, val=kv)
+        if ev is not None:
+            ev[0].record()
+        sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse)
+        if ev is not None:
+            ev[1].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    for s in range(steps):
+        step(evs[s])
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / steps
+    fwd_ms = [a.elapsed_time(b_) for a, b_ in evs]
+    fwd_avg = float(np.mean(fwd_ms))
+
+    pairs_per_head = n * (n + 1) // 2 if w.causal else n * n
+    pairs = B * Hq * pairs_per_head
+    pv_flops = 2.0 * d * pairs
+    E = _overlap_count(qi, ki, d, w.G, w.causal)
+    achieved = pv_flops / (fwd_avg * 1e-3)
+    tokens = B * n
+    out = {
+        "metric": METRIC,
+        "value": tokens / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "n": n, "d": d, "k": kk,
+            "causal": w.causal, "seed": w.seed,
+            "step": "sfa_topk_encode(Q) + sfa_topk_encode(K) + sfa_attn_fwd",
+            "precision": "codes fp32; scores and softmax fp32; P.V bf16 MFMA, fp32 accumulate; O bf16",
+        },
+        "roofline": {
+            "kernel": "sfa_fwd_kernel",
+            "bound": "mfma",
+            "achieved": achieved / 1e12,
+            "peak": PEAK_MFMA_BF16 / 1e12,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_MFMA_BF16,
+            "traffic": _traffic("sfa_fwd.hip", w.name),
+            "algorithmic_flops_per_launch": pv_flops,
+            "fwd_ms_avg": fwd_avg,
+            "fwd_ms_min": float(np.min(fwd_ms)),
+            "allowed_pairs": pairs,
+            "overlap_products_E": E,
+            "algorithmic_hbm_bytes_per_launch": _fwd_bytes(w),
+            "hbm_frac": _fwd_bytes(w) / (fwd_avg * 1e-3) / PEAK_HBM,
+        },
+        "wall_s_timed": wall,
+    }
+    if want_cpu:
+        out["cpu_baseline"] = cpu_baseline_fwd(w, q, k, v)
+    return out
+
+
+def _fwd_bytes(w):
+    """Compulsory HBM bytes of one forward launch: codes in (int32 + fp32),
+    V in (bf16), O out (bf16), LSE out (fp32)."""
+    codes = (w.B * w.Hq * w.n + w.B * w.Hkv * w.n) * w.k * 8
+    return codes + w.B * w.Hkv * w.n * w.d * 2 + w.B * w.Hq * w.n * w.d * 2 + w.B * w.Hq * w.n * 4
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        return 1
+
+
+def cpu_baseline_fwd(w, q, k, v, budget_rows=256, seed=0):
+    """The oracle on a bounded sample of the same workload, extrapolated to
+    the whole step: Top-k of every key row (timed in full), Top-k of a sample
+    of query rows (scaled by the row count), and the attention of `budget_rows`
+    random positions for every query head (scaled by the causal row cost,
+    proportional to i+1)."""
+    import oracle
+    rng = np.random.default_rng(seed)
+    # key coding, every key row
+    kn = k.cpu().numpy()
+    t = time.perf_counter()
+    kc = [[oracle.topk_encode(kn[b, g], w.k) for g in range(w.Hkv)] for b in range(w.B)]
+    t_enck = time.perf_counter() - t
+    # query coding, sampled rows
+    rows = np.sort(rng.choice(w.n, size=budget_rows, replace=False))
+    qs = q[:, :, torch.from_numpy(rows).to(q.device)].cpu().numpy()   # [B,Hq,R,d]
+    t = time.perf_counter()
+    qc = oracle.topk_encode(qs, w.k)
+    t_encq = (time.perf_counter() - t) * (w.n / budget_rows)
+    # attention on the sampled rows, all heads
+    vn = v.view(torch.int16).cpu().numpy().view(np.uint16)
+    t = time.perf_counter()
+    for b in range(w.B):
+        for h in range(w.Hq):
+            g = h // w.G
+            qi_full = np.zeros((w.n, w.k), np.int64)
+            qv_full = np.zeros((w.n, w.k), np.float32)
+            qi_full[rows], qv_full[rows] = qc[0][b, h], qc[1][b, h]
+            oracle.attn_fwd_rows(qi_full, qv_full, kc[b][g][0], kc[b][g][1], vn[b, g], w.d,
+                                 w.scale, w.causal, rows)
+    t_att = time.perf_counter() - t
+    if w.causal:
+        scale_rows = (w.n * (w.n + 1) / 2) / float(np.sum(rows + 1))
+    else:
+        scale_rows = w.n / budget_rows
+    total = t_enck + t_encq + t_att * scale_rows
+    return {
+        "value": w.B * w.n / total,
+        "unit": "tokens/s",
+        "cores": _blas_threads(),
+        "kind": "oracle",
+        "sample": (f"{w.name}: oracle Top-k of all {w.B * w.Hkv * w.n} key rows ({t_enck:.1f} s), "
+                   f"of {budget_rows} query rows x {w.Hq} heads (x{w.n / budget_rows:.0f}), "
+                   f"float64 attention of those {budget_rows} random positions x {w.Hq} heads "
+                   f"({t_att:.1f} s, scaled x{scale_rows:.1f} by the causal row cost i+1); "
+                   f"extrapolated step {total:.0f} s"),
+        "host_cpu_count": os.cpu_count(),
+    }
+
+
+# ----------------------------------------------------------------------------
+# decode workload
+# ----------------------------------------------------------------------------
+
+def bench_decode(w, steps, warmup, want_cpu):
+    B, Hq, Hkv, L, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
+    ci = torch.empty((B, Hkv, L, kk), dtype=torch.int16, device=DEV)
+    cv = torch.empty((B, Hkv, L, kk), dtype=torch.bfloat16, device=DEV)
+    vc = torch.empty((B, Hkv, L, d), dtype=torch.bfloat16, device=DEV)
+    for b in range(B):
+        for h in range(Hkv):
+            kd = si.normal((L, d), w.seed, "k", b, h, device=DEV)
+            sfa.sfa_topk_encode(kd, kk, idx=ci[b, h], val=cv[b, h])
+            vc[b, h] = si.normal((L, d), w.seed, "v", b, h, device=DEV).to(torch.bfloat16)
+    del kd
+    qd = si.normal((B, Hq, d), w.seed, "q", device=DEV)
+    qi, qv = sfa.sfa_topk_encode(qd, kk)
+    o = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=DEV)
+    ws = torch.empty(sfa.sfa_attn_decode_workspace(B, Hq, L, d), dtype=torch.uint8, device=DEV)
+
+    def step():
+        sfa.sfa_attn_decode(qi, qv, ci, cv, vc, scale=w.scale, o=o, lse=lse, ws=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        step()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    algo_bytes = B * Hkv * L * (kk * 4 + d * 2) + B * Hq * (kk * 8 + d * 2 + 4)
+    achieved = algo_bytes / (ms * 1e-3)
+    out = {
+        "metric": "SFA decode tokens/s, 64 seqs x 64K sparse-code cache (k=16 int16/bf16, d=128), 32/8 heads",
+        "value": B / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "L": L, "d": d, "k": kk,
+                   "step": "sfa_attn_decode (split context + LSE merge)"},
+        "roofline": {"kernel": "sfa_decode_kernel + combine", "bound": "hbm",
+                     "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM, "traffic": _traffic("sfa_decode.hip", w.name),
+                     "algorithmic_bytes_per_launch": algo_bytes},
+    }
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen3_32k", choices=sorted(si.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: the SFA hot path here is built and measured "
+              "on a single MI355X (no multi-GPU path); rerun with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    w = si.workload(args.workload)
+    if w.kind == "decode":
+        out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline)
+    else:
+        out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

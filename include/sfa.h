@@ -1,0 +1,153 @@
+/*
+ * sfa.h -- C ABI of libsfa, a gfx950 (AMD Instinct MI355X) implementation of
+ * Sparse Feature Attention (SFA): attention in which every query and key is a
+ * k-sparse code, the Top-k of its d-dimensional projection.
+ *
+ * Paper: "Scaling Attention via Feature Sparsity" (arXiv 2603.22300).
+ *   - Top-k coding: Sec. 3.1, Eq. (1) and the case definition under it.
+ *   - Overlap scores s_ij = scale * sum_{u in S_i cap S_j} q_iu k_ju: Sec. 3.1.
+ *   - Masked softmax and value aggregation: Sec. 2 (attention equations);
+ *     the tiled kernel's result equals softmax(Q~ K~^T / sqrt(d)) V: Sec. 3.2.
+ *   - Decode against a cache of sparse key codes and dense V: App. B
+ *     ("KV-cache latency") and App. J (code storage).
+ *
+ * Conventions shared by every entry point
+ *   - All array pointers are DEVICE pointers to dense, row-major, contiguous
+ *     arrays owned by the caller.  The library never allocates device memory
+ *     and keeps no state across calls apart from cached device properties.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Every call only enqueues work on `stream` and returns; results are
+ *     ready when the stream reaches that point.
+ *   - Arguments are validated on the host before anything is launched.  On
+ *     any error nothing is launched and no output is touched.  No exception
+ *     crosses the ABI.
+ *   - Codes: a code row is k (index, value) pairs.  Indices lie in [0, d) and
+ *     are distinct within a row; sfa_topk_encode writes them in ascending
+ *     order (the attention entry points accept any order).  Values and V must
+ *     be finite.  Violating these device-side preconditions gives undefined
+ *     results (no fault: indices are masked into range before any access).
+ *   - Grouped heads: query head h reads KV head h / (Hq / Hkv).
+ *   - dtype codes below: index arrays are SFA_I32 or SFA_I16; value arrays
+ *     are SFA_F32 or SFA_BF16 (bfloat16 bit patterns, 2 bytes).
+ */
+#ifndef SFA_H
+#define SFA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SFA_OK = 0,
+  SFA_EINVAL = 1,  /* bad argument: null pointer, size out of range, k > d,
+                      Hq not a multiple of Hkv, bad dtype code             */
+  SFA_ENOTSUP = 2, /* valid but unsupported: head dim or dtype combination
+                      without a kernel, or a shape whose tiles exceed LDS  */
+  SFA_EHIP = 3,    /* the HIP runtime reported an error at launch          */
+  SFA_ENOSPC = 4   /* the caller's workspace is smaller than required      */
+} sfa_status;
+
+typedef enum { SFA_I32 = 0, SFA_I16 = 1, SFA_F32 = 2, SFA_BF16 = 3 } sfa_dtype;
+
+/* Version of this ABI (incremented on any incompatible change). */
+int sfa_abi_version(void);
+
+/* Static, human-readable text for a status code. */
+const char* sfa_strerror(int status);
+
+/*
+ * Row-wise Top-k coding (Sec. 3.1, Eq. (1)).
+ *
+ * x    [rows, d] float32.  For each row, keeps the k coordinates of largest
+ *      |x_u|; ties go to the lower index (the paper leaves ties open).
+ *      Magnitudes are compared as exact float32 values: subnormals are
+ *      ordered, never flushed; +0 and -0 tie.
+ * idx  [rows, k] of idx_t (SFA_I32 or SFA_I16; SFA_I16 needs d <= 32767):
+ *      the kept coordinates in ascending order.
+ * val  [rows, k] of val_t: SFA_F32 copies x_u bit for bit; SFA_BF16 stores
+ *      x_u rounded to nearest-even bfloat16 (selection still uses the
+ *      float32 magnitudes).
+ * Limits: 1 <= d <= 256, 1 <= k <= d, rows >= 0 (rows == 0 is a no-op).
+ * Errors: SFA_EINVAL (null pointer with rows > 0, k or d out of range,
+ *         bad dtype), SFA_ENOTSUP (d > 256), SFA_EHIP.
+ */
+sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
+                           void* idx, int idx_t, void* val, int val_t,
+                           void* stream);
+
+/*
+ * SFA forward (Sec. 3.1-3.2): for every batch b, query head h and position i
+ *   s_ij  = scale * sum_{u in S_i cap S_j} q_iu k_ju            (allowed j)
+ *   O_i   = sum_j exp(s_ij - m_i) v_j / l_i,  l_i = sum_j exp(s_ij - m_i)
+ *   LSE_i = m_i + ln(l_i),  m_i = max_j s_ij
+ * where the allowed keys are j <= i if `causal`, else all j < n.  An allowed
+ * key whose support does not overlap the query's enters with s_ij = 0.
+ * No n x n matrix is ever stored.
+ *
+ * q_idx, q_val  [B, Hq, n, k]   query codes (idx_t, qk_val_t)
+ * k_idx, k_val  [B, Hkv, n, k]  key codes   (idx_t, qk_val_t)
+ * v             [B, Hkv, n, d]  values (v_t: SFA_BF16 or SFA_F32)
+ * o             [B, Hq, n, d]   output (o_t: SFA_F32 or SFA_BF16, the latter
+ *                               rounded to nearest-even from float32)
+ * lse           [B, Hq, n] float32 natural-log LSE, or NULL to skip it.
+ * Arithmetic: scores, softmax and accumulation in float32.  With bf16 V the
+ * probabilities enter the P.V product as bfloat16 (MFMA, float32
+ * accumulate); with float32 V the product is float32 throughout.
+ * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0; d in {64, 128}; 1 <= k <= d
+ *         (k * d bounded by LDS capacity: SFA_ENOTSUP beyond it).
+ * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_EHIP.
+ */
+sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,
+                        const void* k_idx, const void* k_val,
+                        const void* v,
+                        int B, int Hq, int Hkv, int n, int d, int k,
+                        int causal, float scale,
+                        int idx_t, int qk_val_t, int v_t, int o_t,
+                        void* o, float* lse, void* stream);
+
+/*
+ * Bytes of device workspace sfa_attn_decode needs for these sizes.
+ */
+size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d);
+
+/*
+ * SFA decode step (App. B, KV-cache attention with one new query per
+ * sequence): each query code attends to the first seq_len[b] cached keys
+ * (all of them allowed), with the same s, O and LSE definitions as
+ * sfa_attn_fwd.  The context is split into chunks processed in parallel and
+ * the partial (max, sum, output) triples are merged by their LSE.
+ *
+ * q_idx, q_val    [B, Hq, k]          query codes (q_idx_t, q_val_t)
+ * kc_idx, kc_val  [B, Hkv, Lmax, k]   cached key codes (kc_idx_t, kc_val_t)
+ * v_cache         [B, Hkv, Lmax, d]   cached values (v_t)
+ * seq_len         [B] int32 on the device, each in [1, Lmax]; NULL means
+ *                 every sequence holds Lmax keys.  Values outside the range
+ *                 are clamped into [0, Lmax]; a sequence with 0 keys gets
+ *                 O = 0 and LSE = -inf.
+ * o               [B, Hq, d] (o_t);  lse [B, Hq] float32 or NULL.
+ * ws, ws_bytes    caller-owned device workspace of at least
+ *                 sfa_attn_decode_workspace(B, Hq, Lmax, d) bytes; its
+ *                 contents need no initialisation and are scratch after the
+ *                 call.  Concurrent calls must use distinct workspaces.
+ * Limits: B, Hq, Hkv, Lmax >= 1; Hq % Hkv == 0; Hq / Hkv <= 8;
+ *         d in {64, 128}; 1 <= k <= d.
+ * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (ws_bytes too small), SFA_EHIP.
+ */
+sfa_status sfa_attn_decode(const void* q_idx, const void* q_val,
+                           const void* kc_idx, const void* kc_val,
+                           const void* v_cache, const int32_t* seq_len,
+                           int B, int Hq, int Hkv, int Lmax, int d, int k,
+                           float scale,
+                           int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t,
+                           int v_t, int o_t,
+                           void* o, float* lse,
+                           void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SFA_H */

@@ -1,0 +1,193 @@
+"""Python binding of libsfa (Sparse Feature Attention on gfx950).
+
+Argument marshalling only: every function here checks tensor placement,
+shapes and dtypes, allocates outputs with torch when the caller passes none,
+and calls the C entry point of the same name in libsfa.so on torch's current
+stream.  All arithmetic happens in the HIP kernels.  There is no fallback:
+if libsfa.so is missing or the device is not a GPU, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+__all__ = [
+    "SfaError", "lib", "library_path", "sfa_abi_version", "sfa_strerror",
+    "sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_decode_workspace", "sfa_attn_decode",
+    "SFA_OK", "SFA_EINVAL", "SFA_ENOTSUP", "SFA_EHIP", "SFA_ENOSPC",
+    "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16",
+]
+
+SFA_OK, SFA_EINVAL, SFA_ENOTSUP, SFA_EHIP, SFA_ENOSPC = 0, 1, 2, 3, 4
+SFA_I32, SFA_I16, SFA_F32, SFA_BF16 = 0, 1, 2, 3
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libsfa.so")
+
+_lib = None
+
+
+class SfaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {sfa_strerror(status)} (status {status})")
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libsfa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(library_path):
+            raise RuntimeError(
+                f"{library_path} is missing: build it with `python -m paper_2603_22300_amd.build`")
+        L = ctypes.CDLL(library_path)
+        vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+        L.sfa_abi_version.restype = i32
+        L.sfa_abi_version.argtypes = []
+        L.sfa_strerror.restype = ctypes.c_char_p
+        L.sfa_strerror.argtypes = [i32]
+        L.sfa_topk_encode.restype = i32
+        L.sfa_topk_encode.argtypes = [vp, i64, i32, i32, vp, i32, vp, i32, vp]
+        L.sfa_attn_fwd.restype = i32
+        L.sfa_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
+                                   i32, i32, i32, i32, vp, vp, vp]
+        L.sfa_attn_decode_workspace.restype = sz
+        L.sfa_attn_decode_workspace.argtypes = [i32, i32, i32, i32]
+        L.sfa_attn_decode.restype = i32
+        L.sfa_attn_decode.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, f32,
+                                      i32, i32, i32, i32, i32, i32, vp, vp, vp, sz, vp]
+        _lib = L
+    return _lib
+
+
+def sfa_abi_version() -> int:
+    return lib().sfa_abi_version()
+
+
+def sfa_strerror(status: int) -> str:
+    return lib().sfa_strerror(status).decode()
+
+
+_IDX = {torch.int32: SFA_I32, torch.int16: SFA_I16}
+_VAL = {torch.float32: SFA_F32, torch.bfloat16: SFA_BF16}
+
+
+def _check(t: torch.Tensor, name: str, table) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.dtype not in table:
+        raise TypeError(f"{name}: unsupported dtype {t.dtype}")
+    return table[t.dtype]
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _call(status: int, where: str):
+    if status != SFA_OK:
+        raise SfaError(status, where)
+
+
+def sfa_topk_encode(x: torch.Tensor, k: int, idx_dtype=torch.int32, val_dtype=torch.float32,
+                    idx: torch.Tensor | None = None, val: torch.Tensor | None = None):
+    """Row Top-k codes of x [..., d] float32: (idx [..., k], val [..., k])."""
+    _check(x, "x", {torch.float32: SFA_F32})
+    d = x.shape[-1]
+    rows = x.numel() // d if d else 0
+    if idx is None:
+        idx = torch.empty(x.shape[:-1] + (k,), dtype=idx_dtype, device=x.device)
+    if val is None:
+        val = torch.empty(x.shape[:-1] + (k,), dtype=val_dtype, device=x.device)
+    it = _check(idx, "idx", _IDX)
+    vt = _check(val, "val", _VAL)
+    if idx.numel() != rows * k or val.numel() != rows * k:
+        raise ValueError("idx/val must hold rows * k elements")
+    _call(lib().sfa_topk_encode(x.data_ptr(), rows, d, k, idx.data_ptr(), it, val.data_ptr(), vt,
+                                _stream(x)), "sfa_topk_encode")
+    return idx, val
+
+
+def sfa_attn_fwd(q_idx, q_val, k_idx, k_val, v, causal: bool = True, scale: float | None = None,
+                 o_dtype=None, o: torch.Tensor | None = None, lse: torch.Tensor | None = None,
+                 want_lse: bool = True):
+    """SFA forward on codes.  q_* [B, Hq, n, k], k_* [B, Hkv, n, k], v [B, Hkv, n, d].
+    Returns (o [B, Hq, n, d], lse [B, Hq, n] float32 or None)."""
+    B, Hq, n, k = q_idx.shape
+    Hkv, d = k_idx.shape[1], v.shape[-1]
+    if tuple(q_val.shape) != (B, Hq, n, k) or tuple(k_idx.shape) != (B, Hkv, n, k) \
+            or tuple(k_val.shape) != (B, Hkv, n, k) or tuple(v.shape) != (B, Hkv, n, d):
+        raise ValueError("inconsistent shapes")
+    if q_idx.dtype != k_idx.dtype or q_val.dtype != k_val.dtype:
+        raise TypeError("query and key codes must share index and value dtypes")
+    it = _check(q_idx, "q_idx", _IDX); _check(k_idx, "k_idx", _IDX)
+    qt = _check(q_val, "q_val", _VAL); _check(k_val, "k_val", _VAL)
+    vt = _check(v, "v", _VAL)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if o is None:
+        o = torch.empty((B, Hq, n, d), dtype=o_dtype or v.dtype, device=v.device)
+    ot = _check(o, "o", _VAL)
+    if tuple(o.shape) != (B, Hq, n, d):
+        raise ValueError("o has the wrong shape")
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, n), dtype=torch.float32, device=v.device)
+    lp = 0
+    if lse is not None:
+        _check(lse, "lse", {torch.float32: SFA_F32})
+        lp = lse.data_ptr()
+    _call(lib().sfa_attn_fwd(q_idx.data_ptr(), q_val.data_ptr(), k_idx.data_ptr(), k_val.data_ptr(),
+                             v.data_ptr(), B, Hq, Hkv, n, d, k, int(bool(causal)), float(scale),
+                             it, qt, vt, ot, o.data_ptr(), lp, _stream(v)), "sfa_attn_fwd")
+    return o, lse
+
+
+def sfa_attn_decode_workspace(B: int, Hq: int, Lmax: int, d: int) -> int:
+    return int(lib().sfa_attn_decode_workspace(B, Hq, Lmax, d))
+
+
+def sfa_attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len=None, scale: float | None = None,
+                    o_dtype=None, o=None, lse=None, want_lse: bool = True, ws=None):
+    """SFA decode step.  q_* [B, Hq, k], kc_* [B, Hkv, Lmax, k], v_cache [B, Hkv, Lmax, d],
+    seq_len int32 [B] on the GPU or None.  Returns (o [B, Hq, d], lse [B, Hq] or None)."""
+    B, Hq, k = q_idx.shape
+    Hkv, Lmax, d = kc_idx.shape[1], kc_idx.shape[2], v_cache.shape[-1]
+    if tuple(q_val.shape) != (B, Hq, k) or tuple(kc_idx.shape) != (B, Hkv, Lmax, k) \
+            or tuple(kc_val.shape) != (B, Hkv, Lmax, k) or tuple(v_cache.shape) != (B, Hkv, Lmax, d):
+        raise ValueError("inconsistent shapes")
+    qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _VAL)
+    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _VAL)
+    vt = _check(v_cache, "v_cache", _VAL)
+    sp = 0
+    if seq_len is not None:
+        _check(seq_len, "seq_len", {torch.int32: SFA_I32})
+        if seq_len.numel() != B:
+            raise ValueError("seq_len must hold B entries")
+        sp = seq_len.data_ptr()
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if o is None:
+        o = torch.empty((B, Hq, d), dtype=o_dtype or v_cache.dtype, device=v_cache.device)
+    ot = _check(o, "o", _VAL)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=v_cache.device)
+    lp = 0
+    if lse is not None:
+        _check(lse, "lse", {torch.float32: SFA_F32})
+        lp = lse.data_ptr()
+    need = sfa_attn_decode_workspace(B, Hq, Lmax, d)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=v_cache.device)
+    _call(lib().sfa_attn_decode(q_idx.data_ptr(), q_val.data_ptr(), kc_idx.data_ptr(),
+                                kc_val.data_ptr(), v_cache.data_ptr(), sp, B, Hq, Hkv, Lmax, d, k,
+                                float(scale), qit, qvt, cit, cvt, vt, ot, o.data_ptr(), lp,
+                                ws.data_ptr(), ws.numel() * ws.element_size(), _stream(v_cache)),
+          "sfa_attn_decode")
+    return o, lse

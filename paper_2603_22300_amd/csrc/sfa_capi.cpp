@@ -1,0 +1,98 @@
+// C ABI of libsfa: argument validation, dtype dispatch, launch, error codes.
+// Every check runs on the host before anything is enqueued.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "../../include/sfa.h"
+#include "sfa_launch.h"
+
+namespace {
+
+constexpr int kAbiVersion = 1;
+constexpr int kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
+
+bool is_idx(int t) { return t == SFA_I32 || t == SFA_I16; }
+bool is_val(int t) { return t == SFA_F32 || t == SFA_BF16; }
+bool pow2_le(int g, int maxg) { return g >= 1 && g <= maxg && (g & (g - 1)) == 0; }
+
+sfa_status from_hip(hipError_t e) { return e == hipSuccess ? SFA_OK : SFA_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+int sfa_abi_version(void) { return kAbiVersion; }
+
+const char* sfa_strerror(int status) {
+  switch (status) {
+    case SFA_OK: return "ok";
+    case SFA_EINVAL: return "invalid argument";
+    case SFA_ENOTSUP: return "unsupported shape or dtype";
+    case SFA_EHIP: return "HIP runtime error";
+    case SFA_ENOSPC: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k, void* idx, int idx_t,
+                           void* val, int val_t, void* stream) {
+  if (rows < 0 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
+  if (!is_idx(idx_t) || !is_val(val_t)) return SFA_EINVAL;
+  if (d > 256) return SFA_ENOTSUP;
+  if (rows == 0) return SFA_OK;
+  if (!x || !idx || !val) return SFA_EINVAL;
+  if ((rows + 3) / 4 > 0x7fffffffLL) return SFA_ENOTSUP;
+  return from_hip(sfa::launch_topk_encode(x, rows, d, k, idx, idx_t == SFA_I16, val,
+                                          val_t == SFA_BF16, (hipStream_t)stream));
+}
+
+sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
+                        const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
+                        int k, int causal, float scale, int idx_t, int qk_val_t, int v_t,
+                        int o_t, void* o, float* lse, void* stream) {
+  if (!q_idx || !q_val || !k_idx || !k_val || !v || !o) return SFA_EINVAL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || n < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
+  if (Hq % Hkv != 0) return SFA_EINVAL;
+  if (!is_idx(idx_t) || !is_val(qk_val_t) || !is_val(v_t) || !is_val(o_t)) return SFA_EINVAL;
+  if (!isfinite(scale)) return SFA_EINVAL;
+  if (d != 64 && d != 128) return SFA_ENOTSUP;
+  const int G = Hq / Hkv;
+  if (!pow2_le(G, sfa::fwd_rows_per_block())) return SFA_ENOTSUP;
+  if (k > sfa::fwd_max_k()) return SFA_ENOTSUP;
+  if (sfa::fwd_lds_bytes(d, k, v_t == SFA_BF16) > kMaxLds) return SFA_ENOTSUP;
+  if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  return from_hip(sfa::launch_attn_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
+                                       causal != 0, scale, idx_t == SFA_I16,
+                                       qk_val_t == SFA_BF16, v_t == SFA_BF16, o_t == SFA_BF16,
+                                       o, lse, (hipStream_t)stream));
+}
+
+size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d) {
+  if (B < 1 || Hq < 1 || Lmax < 1 || d < 1) return 0;
+  return sfa::decode_workspace_bytes(B, Hq, Lmax, d);
+}
+
+sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
+                           const void* kc_val, const void* v_cache, const int32_t* seq_len,
+                           int B, int Hq, int Hkv, int Lmax, int d, int k, float scale,
+                           int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t, int v_t,
+                           int o_t, void* o, float* lse, void* ws, size_t ws_bytes,
+                           void* stream) {
+  if (!q_idx || !q_val || !kc_idx || !kc_val || !v_cache || !o || !ws) return SFA_EINVAL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || Lmax < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
+  if (Hq % Hkv != 0) return SFA_EINVAL;
+  if (!is_idx(q_idx_t) || !is_val(q_val_t) || !is_idx(kc_idx_t) || !is_val(kc_val_t) ||
+      !is_val(v_t) || !is_val(o_t))
+    return SFA_EINVAL;
+  if (!isfinite(scale)) return SFA_EINVAL;
+  if (d != 64 && d != 128) return SFA_ENOTSUP;
+  if (!pow2_le(Hq / Hkv, sfa::decode_max_group())) return SFA_ENOTSUP;
+  if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
+  return from_hip(sfa::launch_attn_decode(
+      q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, B, Hq, Hkv, Lmax, d, k, scale,
+      q_idx_t == SFA_I16, q_val_t == SFA_BF16, kc_idx_t == SFA_I16, kc_val_t == SFA_BF16,
+      v_t == SFA_BF16, o_t == SFA_BF16, o, lse, ws, (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,276 @@
+// SFA decode step (App. B, KV-cache attention) on gfx950.
+//
+// The cache holds sparse key codes (k index/value pairs per key) and dense V.
+// Grid = (context chunks, B * Hkv): a workgroup streams one chunk of one KV
+// head and serves all G query heads of the group from each load.
+//   scores: lane = key.  The G query codes are densified once into an LDS
+//           table qd[u][h]; a key's score for head h is
+//           scale * sum_t kval_t * qd[kidx_t][h] -- zero-cost for coordinates
+//           the query does not hold, which is exactly the overlap sum.
+//   softmax: online, base 2, the running max kept wave-uniform per head.
+//   P.V:    lanes over (8 dims, key subset); float32 FMAs.
+// Each workgroup writes one partial (max, sum, unnormalised output) per query
+// head; a second kernel merges the chunks by their LSE.
+#include "sfa_device.h"
+#include "sfa_launch.h"
+
+namespace sfa {
+
+constexpr int kDecWaves = 4;
+constexpr int kDecThreads = 64 * kDecWaves;
+constexpr int kDecChunk = 2048;  // keys per workgroup
+constexpr int kDecMaxG = 8;
+
+struct DecParams {
+  const void* q_idx;
+  const void* q_val;
+  const void* kc_idx;
+  const void* kc_val;
+  const void* v;
+  const int32_t* seq_len;
+  float* ws_m;  // [B*Hq, nch]
+  float* ws_l;  // [B*Hq, nch]
+  float* ws_o;  // [B*Hq, nch, D]
+  int Hq, Hkv, Lmax, k, nch;
+  float scale_log2;
+  int qidx16, qvalbf16, kidx16, kvalbf16;
+};
+
+__device__ __forceinline__ int seq_len_of(const int32_t* seq_len, int b, int Lmax) {
+  if (!seq_len) return Lmax;
+  int L = seq_len[b];
+  return L < 0 ? 0 : (L > Lmax ? Lmax : L);
+}
+
+template <int D, int G, bool VBF16>
+__global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
+  constexpr int DL = D / 8;     // lanes covering one key's D values (8 each)
+  constexpr int KPL = 64 / DL;  // keys per wave-wide V load
+  __shared__ float qd[D][G];
+  __shared__ float pbuf[kDecWaves][64][G];
+  __shared__ float red_m[kDecWaves][G], red_l[kDecWaves][G];
+  __shared__ float red_o[kDecWaves][G][D];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int chunk = blockIdx.x;
+  const int bh = blockIdx.y;
+  const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+  const int L = seq_len_of(p.seq_len, b, p.Lmax);
+  const int c0 = chunk * kDecChunk;
+  const int c1 = min(L, c0 + kDecChunk);
+  const int k = p.k;
+  const int dmask = D - 1;
+
+  // densify the G query codes: qd[u][h]
+  for (int x = tid; x < D * G; x += kDecThreads) (&qd[0][0])[x] = 0.f;
+  __syncthreads();
+  for (int x = tid; x < G * k; x += kDecThreads) {
+    const int h = x / k, t = x - h * k;
+    const int64_t qi = ((int64_t)b * p.Hq + hkv * G + h) * k + t;
+    const int u = load_idx(p.q_idx, qi, p.qidx16, dmask);
+    qd[u][h] = load_val(p.q_val, qi, p.qvalbf16);
+  }
+  __syncthreads();
+
+  float m_run[G], l_lane[G], o[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m_run[h] = -INFINITY;
+    l_lane[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+  }
+
+  const int64_t kv_row0 = ((int64_t)b * p.Hkv + hkv) * p.Lmax;
+  const int dsub = lane % DL;  // 8-dim group of this lane in the P.V phase
+  const int ksub = lane / DL;  // key offset within a wave-wide V load
+  const int per_wave = kDecChunk / kDecWaves;
+  const int w0 = c0 + wave * per_wave;
+  const int w1 = min(c1, w0 + per_wave);
+
+  for (int sb = w0; sb < w1; sb += 64) {
+    // ---- scores, lane = key ----
+    const int j = sb + lane;
+    const bool ok = j < w1;
+    float s[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) s[h] = 0.f;
+    if (ok) {
+      const int64_t cbase = (kv_row0 + j) * k;
+      for (int t = 0; t < k; ++t) {
+        const int u = load_idx(p.kc_idx, cbase + t, p.kidx16, dmask);
+        const float kv = load_val(p.kc_val, cbase + t, p.kvalbf16);
+#pragma unroll
+        for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
+      }
+    }
+    // ---- online softmax, per head ----
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float tt = ok ? s[h] * p.scale_log2 : -INFINITY;
+      const float mb = wave_max(tt);
+      const float m_new = fmaxf(m_run[h], mb);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = exp2f(m_run[h] - m_use);
+      const float pj = exp2f(tt - m_use);
+      l_lane[h] = l_lane[h] * alpha + pj;
+      m_run[h] = m_new;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] *= alpha;
+      pbuf[wave][lane][h] = pj;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    // ---- P.V: lanes over (8 dims, key subset) ----
+    for (int r = 0; r < 64; r += KPL) {
+      const int jj = r + ksub;
+      const int jg = sb + jj;
+      if (jg < w1) {
+        float vv[8];
+        if constexpr (VBF16) {
+          const uint4 raw = *(const uint4*)((const uint16_t*)p.v + (kv_row0 + jg) * D + dsub * 8);
+          vv[0] = __uint_as_float(raw.x << 16); vv[1] = __uint_as_float(raw.x & 0xffff0000u);
+          vv[2] = __uint_as_float(raw.y << 16); vv[3] = __uint_as_float(raw.y & 0xffff0000u);
+          vv[4] = __uint_as_float(raw.z << 16); vv[5] = __uint_as_float(raw.z & 0xffff0000u);
+          vv[6] = __uint_as_float(raw.w << 16); vv[7] = __uint_as_float(raw.w & 0xffff0000u);
+        } else {
+          const float4* src = (const float4*)((const float*)p.v + (kv_row0 + jg) * D + dsub * 8);
+          const float4 a = src[0], c = src[1];
+          vv[0] = a.x; vv[1] = a.y; vv[2] = a.z; vv[3] = a.w;
+          vv[4] = c.x; vv[5] = c.y; vv[6] = c.z; vv[7] = c.w;
+        }
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float ph = pbuf[wave][jj][h];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[h][e] = fmaf(ph, vv[e], o[h][e]);
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  // ---- reduce within the wave: sums over lanes, outputs over key subsets ----
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    l_lane[h] = wave_sum(l_lane[h]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int off = DL; off < 64; off <<= 1) o[h][e] += __shfl_xor(o[h][e], off, 64);
+  }
+  if (lane < DL) {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red_o[wave][h][lane * 8 + e] = o[h][e];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) { red_m[wave][h] = m_run[h]; red_l[wave][h] = l_lane[h]; }
+  }
+  __syncthreads();
+  // ---- merge the waves and write this chunk's partial ----
+  for (int x = tid; x < G * D; x += kDecThreads) {
+    const int h = x / D, dd = x - h * D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, red_m[w][h]);
+    const float Mu = (M == -INFINITY) ? 0.f : M;
+    float lsum = 0.f, osum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+      const float sc = exp2f(red_m[w][h] - Mu);
+      lsum += sc * red_l[w][h];
+      osum += sc * red_o[w][h][dd];
+    }
+    const int64_t slot = ((int64_t)b * p.Hq + hkv * G + h) * p.nch + chunk;
+    p.ws_o[slot * D + dd] = osum;
+    if (dd == 0) { p.ws_m[slot] = M; p.ws_l[slot] = lsum; }
+  }
+}
+
+// Merge the chunk partials of each (b, h): O = sum_c w_c o_c / sum_c w_c l_c,
+// w_c = 2^(m_c - M), LSE = (M + log2 sum_c w_c l_c) ln 2.
+template <int D>
+__global__ __launch_bounds__(D) void sfa_decode_combine_kernel(
+    const float* __restrict__ ws_m, const float* __restrict__ ws_l, const float* __restrict__ ws_o,
+    const int32_t* seq_len, int Hq, int Lmax, int nch, void* o, int obf16, float* lse) {
+  const int bh = blockIdx.x;
+  const int b = bh / Hq;
+  const int dd = threadIdx.x;
+  const int L = seq_len_of(seq_len, b, Lmax);
+  const int nc = (L + kDecChunk - 1) / kDecChunk;
+  const int64_t s0 = (int64_t)bh * nch;
+  float M = -INFINITY;
+  for (int c = 0; c < nc; ++c) M = fmaxf(M, ws_m[s0 + c]);
+  const float Mu = (M == -INFINITY) ? 0.f : M;
+  float lsum = 0.f, osum = 0.f;
+  for (int c = 0; c < nc; ++c) {
+    const float w = exp2f(ws_m[s0 + c] - Mu);
+    lsum += w * ws_l[s0 + c];
+    osum += w * ws_o[(s0 + c) * D + dd];
+  }
+  const float out = lsum > 0.f ? osum / lsum : 0.f;
+  if (obf16) ((uint16_t*)o)[(int64_t)bh * D + dd] = (uint16_t)f32_to_bf16_rne(out);
+  else ((float*)o)[(int64_t)bh * D + dd] = out;
+  if (lse && dd == 0) lse[bh] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+}
+
+size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d) {
+  const size_t nch = (size_t)((Lmax + kDecChunk - 1) / kDecChunk);
+  return (size_t)B * Hq * nch * (size_t)(d + 2) * sizeof(float);
+}
+
+template <int D, int G, bool VBF16>
+static void launch_dec_t(const DecParams& p, int B, hipStream_t stream) {
+  dim3 grid(p.nch, B * p.Hkv), block(kDecThreads);
+  hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16>), grid, block, 0, stream, p);
+}
+
+template <int D, bool VBF16>
+static void launch_dec_g(const DecParams& p, int G, int B, hipStream_t stream) {
+  switch (G) {
+    case 1: launch_dec_t<D, 1, VBF16>(p, B, stream); break;
+    case 2: launch_dec_t<D, 2, VBF16>(p, B, stream); break;
+    case 4: launch_dec_t<D, 4, VBF16>(p, B, stream); break;
+    default: launch_dec_t<D, 8, VBF16>(p, B, stream); break;
+  }
+}
+
+int decode_max_group() { return kDecMaxG; }
+
+hipError_t launch_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
+                              const void* kc_val, const void* v, const int32_t* seq_len, int B,
+                              int Hq, int Hkv, int Lmax, int d, int k, float scale, int qidx16,
+                              int qvalbf16, int kidx16, int kvalbf16, int vbf16, int obf16,
+                              void* o, float* lse, void* ws, hipStream_t stream) {
+  DecParams p;
+  p.q_idx = q_idx; p.q_val = q_val; p.kc_idx = kc_idx; p.kc_val = kc_val; p.v = v;
+  p.seq_len = seq_len;
+  p.Hq = Hq; p.Hkv = Hkv; p.Lmax = Lmax; p.k = k;
+  p.nch = (Lmax + kDecChunk - 1) / kDecChunk;
+  const size_t nslot = (size_t)B * Hq * p.nch;
+  p.ws_m = (float*)ws;
+  p.ws_l = p.ws_m + nslot;
+  p.ws_o = p.ws_l + nslot;
+  p.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  p.qidx16 = qidx16; p.qvalbf16 = qvalbf16; p.kidx16 = kidx16; p.kvalbf16 = kvalbf16;
+  const int G = Hq / Hkv;
+  if (d == 64) {
+    if (vbf16) launch_dec_g<64, true>(p, G, B, stream); else launch_dec_g<64, false>(p, G, B, stream);
+  } else {
+    if (vbf16) launch_dec_g<128, true>(p, G, B, stream); else launch_dec_g<128, false>(p, G, B, stream);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (d == 64)
+    hipLaunchKernelGGL(sfa_decode_combine_kernel<64>, dim3(B * Hq), dim3(64), 0, stream,
+                       p.ws_m, p.ws_l, p.ws_o, seq_len, Hq, Lmax, p.nch, o, obf16, lse);
+  else
+    hipLaunchKernelGGL(sfa_decode_combine_kernel<128>, dim3(B * Hq), dim3(128), 0, stream,
+                       p.ws_m, p.ws_l, p.ws_o, seq_len, Hq, Lmax, p.nch, o, obf16, lse);
+  return hipGetLastError();
+}
+
+}  // namespace sfa

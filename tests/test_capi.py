@@ -1,0 +1,97 @@
+"""The C-ABI library: loads, exports every entry point include/sfa.h declares,
+and rejects bad arguments on the host, before anything is launched (so these
+run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sfa.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sfa_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2603_22300_amd as sfa
+    if not os.path.exists(sfa.library_path):
+        from paper_2603_22300_amd.build import build
+        build()
+    return sfa.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared()
+    assert {"sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_decode",
+            "sfa_attn_decode_workspace", "sfa_abi_version", "sfa_strerror"} <= set(names)
+    for nm in names:
+        assert hasattr(L, nm), nm
+
+
+def test_version_and_strerror(L):
+    assert L.sfa_abi_version() == 1
+    for s in range(5):
+        assert L.sfa_strerror(s)
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+
+
+def _fwd(L, **kw):
+    a = dict(q_idx=FAKE, q_val=FAKE, k_idx=FAKE, k_val=FAKE, v=FAKE, B=1, Hq=4, Hkv=2, n=16, d=64,
+             k=8, causal=1, scale=0.125, idx_t=0, qk_val_t=2, v_t=3, o_t=2, o=FAKE, lse=None,
+             stream=None)
+    a.update(kw)
+    return L.sfa_attn_fwd(*a.values())
+
+
+def test_fwd_validation(L):
+    assert _fwd(L, q_idx=None) == 1
+    assert _fwd(L, o=None) == 1
+    assert _fwd(L, k=0) == 1
+    assert _fwd(L, k=65, d=64) == 1
+    assert _fwd(L, Hq=3, Hkv=2) == 1
+    assert _fwd(L, n=0) == 1
+    assert _fwd(L, idx_t=2) == 1            # a value dtype as index dtype
+    assert _fwd(L, v_t=0) == 1
+    assert _fwd(L, scale=float("nan")) == 1
+    assert _fwd(L, d=96, k=8) == 2           # no kernel for this head dim
+    assert _fwd(L, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
+    assert _fwd(L, d=128, k=128) == 2        # beyond the supported k
+
+
+def test_encode_validation(L):
+    enc = L.sfa_topk_encode
+    assert enc(FAKE, 10, 64, 0, FAKE, 0, FAKE, 2, None) == 1
+    assert enc(FAKE, 10, 64, 65, FAKE, 0, FAKE, 2, None) == 1
+    assert enc(None, 10, 64, 8, FAKE, 0, FAKE, 2, None) == 1
+    assert enc(FAKE, -1, 64, 8, FAKE, 0, FAKE, 2, None) == 1
+    assert enc(FAKE, 10, 64, 8, FAKE, 3, FAKE, 2, None) == 1
+    assert enc(FAKE, 10, 300, 8, FAKE, 0, FAKE, 2, None) == 2
+    assert enc(None, 0, 64, 8, None, 0, None, 2, None) == 0     # empty: no-op
+
+
+def _dec(L, **kw):
+    a = dict(q_idx=FAKE, q_val=FAKE, kc_idx=FAKE, kc_val=FAKE, v=FAKE, seq_len=None, B=2, Hq=8,
+             Hkv=2, Lmax=100, d=128, k=16, scale=0.088, q_idx_t=0, q_val_t=2, kc_idx_t=1,
+             kc_val_t=3, v_t=3, o_t=2, o=FAKE, lse=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return L.sfa_attn_decode(*a.values())
+
+
+def test_decode_validation_and_workspace(L):
+    need = L.sfa_attn_decode_workspace(2, 8, 100, 128)
+    assert need > 0
+    assert L.sfa_attn_decode_workspace(0, 8, 100, 128) == 0
+    assert _dec(L, ws_bytes=need - 1) == 4
+    assert _dec(L, ws=None) == 1
+    assert _dec(L, Hq=6, Hkv=4) == 1
+    assert _dec(L, Hq=32, Hkv=2) == 2       # group of 16 heads: unsupported
+    assert _dec(L, d=80, k=8) == 2
+    assert _dec(L, kc_idx_t=3) == 1

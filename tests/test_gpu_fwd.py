@@ -1,0 +1,164 @@
+"""GPU parity: sfa_attn_fwd (fed by sfa_topk_encode) against the oracle.
+
+The GPU path codes dense Q and K with its own encoder; the oracle codes the
+same dense inputs with its own Top-k and evaluates the plain definition in
+float64.  Tolerances: helpers.TOL_* (O 1e-5 float32 path, 5e-3 bf16-V path,
+LSE 1e-4)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_22300_amd as sfa
+import sfa_inputs as si
+from helpers import (TOL_O_BF16V, TOL_O_F32, check_lse, check_o, np_vals, sample_rows)
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _gpu_codes(x, k, idx_dtype=torch.int32, val_dtype=torch.float32):
+    return sfa.sfa_topk_encode(x, k, idx_dtype=idx_dtype, val_dtype=val_dtype)
+
+
+def _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, idx_dtype=torch.int32,
+              val_dtype=torch.float32, zipf_s=0.0):
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed,
+                            v_dtype=torch.bfloat16 if v_bf16 else torch.float32, device=DEV)
+    if zipf_s:
+        for b in range(B):
+            for h in range(Hq):
+                perm = si.zipf_feature_perm(d, seed, h // (Hq // Hkv))
+                i_, v_ = si.zipf_codes(n, d, k, zipf_s, perm, seed, "q", b, h, device=DEV)
+                q[b, h] = si.dense_from_codes(i_, v_, d)
+            for h in range(Hkv):
+                perm = si.zipf_feature_perm(d, seed, h)
+                i_, v_ = si.zipf_codes(n, d, k, zipf_s, perm, seed, "k", b, h, device=DEV)
+                kk[b, h] = si.dense_from_codes(i_, v_, d)
+    qi, qv = _gpu_codes(q, k, idx_dtype, val_dtype)
+    ki, kv = _gpu_codes(kk, k, idx_dtype, val_dtype)
+    scale = 1.0 / math.sqrt(d)
+    o32, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=torch.float32)
+    ob16 = None
+    if v_bf16:
+        ob16, _ = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale,
+                                   o_dtype=torch.bfloat16, want_lse=False)
+    torch.cuda.synchronize()
+    # oracle: its own codes of the same dense inputs
+    qn, kn, vn = q.cpu().numpy(), kk.cpu().numpy(), np_vals(v)
+    if val_dtype == torch.bfloat16:
+        oqi, oqv = oracle.topk_encode_bf16(qn, k)
+        oki, okv = oracle.topk_encode_bf16(kn, k)
+    else:
+        oqi, oqv = oracle.topk_encode(qn, k)
+        oki, okv = oracle.topk_encode(kn, k)
+    O, L = oracle.attn_fwd(oqi, oqv, oki, okv, vn, d, scale, causal)
+    tol = TOL_O_BF16V if v_bf16 else TOL_O_F32
+    eo = check_o(o32, O, tol, "O (float32 output)")
+    el = check_lse(lse, L, "LSE")
+    if ob16 is not None:
+        check_o(ob16, O, tol, "O (bf16 output)")
+    return eo, el
+
+
+def test_tiny_workload_fp32():
+    w = si.workload("tiny")
+    _run_case(w.B, w.Hq, w.Hkv, w.n, w.d, w.k, w.causal, w.v_bf16, w.seed)
+
+
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,v_bf16",
+    [
+        (1, 1, 1, 1, 64, 8, True, False),      # n = 1
+        (1, 1, 1, 37, 64, 8, True, False),     # one ragged tile
+        (2, 2, 2, 130, 64, 16, True, True),    # ragged tail past two tiles
+        (1, 4, 1, 200, 128, 16, True, True),   # GQA 4:1, d = 128
+        (1, 8, 1, 100, 128, 16, True, True),   # GQA 8:1 (two heads per wave)
+        (1, 2, 1, 257, 128, 8, False, True),   # non-causal
+        (1, 1, 1, 300, 64, 1, True, True),     # k = 1
+        (1, 2, 2, 150, 64, 64, True, False),   # k = d: dense attention
+        (1, 2, 1, 129, 128, 64, True, True),   # largest supported k at d = 128
+        (2, 4, 2, 96, 128, 16, False, False),  # float32 V, GQA 2:1
+        (1, 16, 1, 70, 64, 8, True, True),     # 16 heads per KV head
+    ])
+def test_shapes(B, Hq, Hkv, n, d, k, causal, v_bf16):
+    _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=B * 1000 + Hq * 100 + n)
+
+
+def test_int16_indices_bf16_values():
+    _run_case(1, 4, 2, 190, 128, 16, True, True, seed=77, idx_dtype=torch.int16,
+              val_dtype=torch.bfloat16)
+
+
+def test_zipf_small():
+    _run_case(1, 2, 2, 260, 128, 8, True, True, seed=4, zipf_s=1.1)
+
+
+def test_gpt2s_workload_full():
+    # every output of the GPT-2-small-shaped workload, against the oracle
+    w = si.workload("gpt2s")
+    _run_case(w.B, w.Hq, w.Hkv, w.n, w.d, w.k, w.causal, w.v_bf16, w.seed)
+
+
+def _big_case_sampled(w, heads, zipf=False):
+    """Full-size workload on the GPU (encode + forward), oracle on sampled rows."""
+    G = w.G
+    q = torch.empty((1, w.Hq, w.n, w.d), device=DEV)
+    kk = torch.empty((1, w.Hkv, w.n, w.d), device=DEV)
+    v = torch.empty((1, w.Hkv, w.n, w.d), device=DEV, dtype=torch.bfloat16)
+    for h in range(w.Hq):
+        if zipf:
+            perm = si.zipf_feature_perm(w.d, w.seed, h // G)
+            i_, v_ = si.zipf_codes(w.n, w.d, w.k, w.zipf_s, perm, w.seed, "q", 0, h, device=DEV)
+            q[0, h] = si.dense_from_codes(i_, v_, w.d)
+        else:
+            q[0, h] = si.normal((w.n, w.d), w.seed, "q", 0, h, device=DEV)
+    for h in range(w.Hkv):
+        if zipf:
+            perm = si.zipf_feature_perm(w.d, w.seed, h)
+            i_, v_ = si.zipf_codes(w.n, w.d, w.k, w.zipf_s, perm, w.seed, "k", 0, h, device=DEV)
+            kk[0, h] = si.dense_from_codes(i_, v_, w.d)
+        else:
+            kk[0, h] = si.normal((w.n, w.d), w.seed, "k", 0, h, device=DEV)
+        v[0, h] = si.normal((w.n, w.d), w.seed, "v", 0, h, device=DEV).to(torch.bfloat16)
+    qi, qv = _gpu_codes(q, w.k)
+    ki, kv = _gpu_codes(kk, w.k)
+    o32, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale,
+                                o_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = sample_rows(w.n, extra=(127, 128, 4095, 4096, w.n // 2), count=16, seed=w.seed)
+    for h in heads:
+        g = h // G
+        kn = kk[0, g, : rows.max() + 1].cpu().numpy()
+        oki, okv = oracle.topk_encode(kn, w.k)
+        oqi, oqv = oracle.topk_encode(q[0, h, torch.from_numpy(rows).to(DEV)].cpu().numpy(), w.k)
+        qi_full = np.zeros((w.n, w.k), np.int64); qv_full = np.zeros((w.n, w.k), np.float32)
+        qi_full[rows], qv_full[rows] = oqi, oqv
+        O, L = oracle.attn_fwd_rows(qi_full, qv_full, oki, okv,
+                                    np_vals(v[0, g, : rows.max() + 1]), w.d, w.scale, w.causal, rows)
+        sel = torch.from_numpy(rows).to(DEV)
+        check_o(o32[0, h, sel], O, TOL_O_BF16V, f"O head {h}")
+        check_lse(lse[0, h, sel], L, f"LSE head {h}")
+
+
+def test_qwen3_32k_full_size_sampled():
+    _big_case_sampled(si.workload("qwen3_32k"), heads=(0, 5, 31))
+
+
+def test_zipf_128k_full_size_sampled():
+    _big_case_sampled(si.workload("zipf_128k"), heads=(0, 7), zipf=True)
+
+
+def test_repeatable():
+    # the score accumulation order may vary between runs (LDS float atomics);
+    # two runs must agree far inside the tolerance
+    q, kk, v = si.dense_qkv(1, 4, 1, 500, 128, 9, device=DEV)
+    qi, qv = _gpu_codes(q, 16)
+    ki, kv = _gpu_codes(kk, 16)
+    o1, l1 = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.float32)
+    o2, l2 = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert (o1 - o2).abs().max().item() < 1e-5
+    assert (l1 - l2).abs().max().item() < 1e-5
