@@ -93,11 +93,14 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * o             [B, Hq, n, d]   output (o_t: SFA_F32 or SFA_BF16, the latter
  *                               rounded to nearest-even from float32)
  * lse           [B, Hq, n] float32 natural-log LSE, or NULL to skip it.
- * Arithmetic: scores, softmax and accumulation in float32.  With bf16 V the
- * probabilities enter the P.V product as bfloat16 (MFMA, float32
- * accumulate); with float32 V the product is float32 throughout.
- * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0; d in {64, 128}; 1 <= k <= d
- *         (k * d bounded by LDS capacity: SFA_ENOTSUP beyond it).
+ * Arithmetic: the scores are the product of the densified codes on the
+ * matrix cores, each value split into bfloat16 pieces whose products are
+ * exact in float32 (bf16 V: three piece products, relative error ~2^-16 of
+ * sum |q_u k_u|; float32 V: six, ~2^-24); softmax and accumulation in
+ * float32.  With bf16 V the probabilities enter the P.V product as bfloat16
+ * (MFMA, float32 accumulate); with float32 V that product is float32.
+ * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0 with Hq / Hkv a power of two
+ *         <= 128; d in {64, 128}; 1 <= k <= d; B * Hkv <= 65535.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_EHIP.
  */
 sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,
@@ -107,6 +110,25 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,
                         int causal, float scale,
                         int idx_t, int qk_val_t, int v_t, int o_t,
                         void* o, float* lse, void* stream);
+
+/*
+ * The same forward with the overlap scores accumulated through a per-key-tile
+ * inverted index in LDS (Sec. 3.2's feature-intersection formulation): the
+ * tile's key codes are counting-sorted by coordinate and each query nonzero
+ * adds q_u * k_u into the score tile for exactly the keys holding its
+ * coordinate.  Same arguments, definitions and results as sfa_attn_fwd (up
+ * to float32 summation order); slower on this hardware, kept as the direct
+ * realisation of the overlap formulation.
+ * Limits: as sfa_attn_fwd, plus k <= 64, Hq / Hkv <= 128, and the per-tile
+ * tables must fit LDS (SFA_ENOTSUP otherwise).
+ */
+sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
+                              const void* k_idx, const void* k_val,
+                              const void* v,
+                              int B, int Hq, int Hkv, int n, int d, int k,
+                              int causal, float scale,
+                              int idx_t, int qk_val_t, int v_t, int o_t,
+                              void* o, float* lse, void* stream);
 
 /*
  * Bytes of device workspace sfa_attn_decode needs for these sizes.

@@ -46,25 +46,51 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k, void* idx
                                           val_t == SFA_BF16, (hipStream_t)stream));
 }
 
-sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
-                        const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
-                        int k, int causal, float scale, int idx_t, int qk_val_t, int v_t,
-                        int o_t, void* o, float* lse, void* stream) {
+namespace {
+
+sfa_status check_fwd(const void* q_idx, const void* q_val, const void* k_idx, const void* k_val,
+                     const void* v, int B, int Hq, int Hkv, int n, int d, int k, float scale,
+                     int idx_t, int qk_val_t, int v_t, int o_t, const void* o) {
   if (!q_idx || !q_val || !k_idx || !k_val || !v || !o) return SFA_EINVAL;
   if (B < 1 || Hq < 1 || Hkv < 1 || n < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
   if (Hq % Hkv != 0) return SFA_EINVAL;
   if (!is_idx(idx_t) || !is_val(qk_val_t) || !is_val(v_t) || !is_val(o_t)) return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
   if (d != 64 && d != 128) return SFA_ENOTSUP;
-  const int G = Hq / Hkv;
-  if (!pow2_le(G, sfa::fwd_rows_per_block())) return SFA_ENOTSUP;
-  if (k > sfa::fwd_max_k()) return SFA_ENOTSUP;
-  if (sfa::fwd_lds_bytes(d, k, v_t == SFA_BF16) > kMaxLds) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  return SFA_OK;
+}
+
+}  // namespace
+
+sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
+                        const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
+                        int k, int causal, float scale, int idx_t, int qk_val_t, int v_t,
+                        int o_t, void* o, float* lse, void* stream) {
+  sfa_status st = check_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k, scale, idx_t,
+                            qk_val_t, v_t, o_t, o);
+  if (st != SFA_OK) return st;
+  if (!pow2_le(Hq / Hkv, sfa::fwd_max_group())) return SFA_ENOTSUP;
   return from_hip(sfa::launch_attn_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
                                        causal != 0, scale, idx_t == SFA_I16,
                                        qk_val_t == SFA_BF16, v_t == SFA_BF16, o_t == SFA_BF16,
                                        o, lse, (hipStream_t)stream));
+}
+
+sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,
+                              const void* k_val, const void* v, int B, int Hq, int Hkv, int n,
+                              int d, int k, int causal, float scale, int idx_t, int qk_val_t,
+                              int v_t, int o_t, void* o, float* lse, void* stream) {
+  sfa_status st = check_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k, scale, idx_t,
+                            qk_val_t, v_t, o_t, o);
+  if (st != SFA_OK) return st;
+  if (!pow2_le(Hq / Hkv, sfa::fwd_index_rows_per_block())) return SFA_ENOTSUP;
+  if (k > sfa::fwd_index_max_k()) return SFA_ENOTSUP;
+  if (sfa::fwd_index_lds_bytes(d, k, v_t == SFA_BF16) > kMaxLds) return SFA_ENOTSUP;
+  return from_hip(sfa::launch_attn_fwd_index(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
+                                             causal != 0, scale, idx_t == SFA_I16,
+                                             qk_val_t == SFA_BF16, v_t == SFA_BF16,
+                                             o_t == SFA_BF16, o, lse, (hipStream_t)stream));
 }
 
 size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d) {

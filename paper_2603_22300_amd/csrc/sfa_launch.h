@@ -15,9 +15,15 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
                            int k, int causal, float scale, int idx16, int valbf16, int vbf16,
                            int obf16, void* o, float* lse, hipStream_t stream);
-int fwd_lds_bytes(int d, int k, int vbf16);
-int fwd_max_k();
-int fwd_rows_per_block();
+int fwd_max_group();
+
+hipError_t launch_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,
+                                 const void* k_val, const void* v, int B, int Hq, int Hkv, int n,
+                                 int d, int k, int causal, float scale, int idx16, int valbf16,
+                                 int vbf16, int obf16, void* o, float* lse, hipStream_t stream);
+int fwd_index_lds_bytes(int d, int k, int vbf16);
+int fwd_index_max_k();
+int fwd_index_rows_per_block();
 
 hipError_t launch_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
                               const void* kc_val, const void* v, const int32_t* seq_len, int B,

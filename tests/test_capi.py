@@ -28,7 +28,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = _declared()
-    assert {"sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_decode",
+    assert {"sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_fwd_index", "sfa_attn_decode",
             "sfa_attn_decode_workspace", "sfa_abi_version", "sfa_strerror"} <= set(names)
     for nm in names:
         assert hasattr(L, nm), nm
@@ -43,27 +43,32 @@ def test_version_and_strerror(L):
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
 
 
-def _fwd(L, **kw):
+def _fwd(L, fn="sfa_attn_fwd", **kw):
     a = dict(q_idx=FAKE, q_val=FAKE, k_idx=FAKE, k_val=FAKE, v=FAKE, B=1, Hq=4, Hkv=2, n=16, d=64,
              k=8, causal=1, scale=0.125, idx_t=0, qk_val_t=2, v_t=3, o_t=2, o=FAKE, lse=None,
              stream=None)
     a.update(kw)
-    return L.sfa_attn_fwd(*a.values())
+    return getattr(L, fn)(*a.values())
 
 
-def test_fwd_validation(L):
-    assert _fwd(L, q_idx=None) == 1
-    assert _fwd(L, o=None) == 1
-    assert _fwd(L, k=0) == 1
-    assert _fwd(L, k=65, d=64) == 1
-    assert _fwd(L, Hq=3, Hkv=2) == 1
-    assert _fwd(L, n=0) == 1
-    assert _fwd(L, idx_t=2) == 1            # a value dtype as index dtype
-    assert _fwd(L, v_t=0) == 1
-    assert _fwd(L, scale=float("nan")) == 1
-    assert _fwd(L, d=96, k=8) == 2           # no kernel for this head dim
-    assert _fwd(L, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
-    assert _fwd(L, d=128, k=128) == 2        # beyond the supported k
+@pytest.mark.parametrize("fn", ["sfa_attn_fwd", "sfa_attn_fwd_index"])
+def test_fwd_validation(L, fn):
+    assert _fwd(L, fn, q_idx=None) == 1
+    assert _fwd(L, fn, o=None) == 1
+    assert _fwd(L, fn, k=0) == 1
+    assert _fwd(L, fn, k=65, d=64) == 1
+    assert _fwd(L, fn, Hq=3, Hkv=2) == 1
+    assert _fwd(L, fn, n=0) == 1
+    assert _fwd(L, fn, idx_t=2) == 1            # a value dtype as index dtype
+    assert _fwd(L, fn, v_t=0) == 1
+    assert _fwd(L, fn, scale=float("nan")) == 1
+    assert _fwd(L, fn, d=96, k=8) == 2           # no kernel for this head dim
+    assert _fwd(L, fn, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
+    assert _fwd(L, fn, B=70000, Hkv=1, Hq=1) == 2  # grid limit
+
+
+def test_fwd_index_limits(L):
+    assert _fwd(L, "sfa_attn_fwd_index", d=128, k=128) == 2   # index tables exceed LDS
 
 
 def test_encode_validation(L):

@@ -24,7 +24,8 @@ def _gpu_codes(x, k, idx_dtype=torch.int32, val_dtype=torch.float32):
 
 
 def _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, idx_dtype=torch.int32,
-              val_dtype=torch.float32, zipf_s=0.0):
+              val_dtype=torch.float32, zipf_s=0.0, fwd=None):
+    fwd = fwd or sfa.sfa_attn_fwd
     q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed,
                             v_dtype=torch.bfloat16 if v_bf16 else torch.float32, device=DEV)
     if zipf_s:
@@ -40,11 +41,11 @@ def _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, idx_dtype=torch.int32,
     qi, qv = _gpu_codes(q, k, idx_dtype, val_dtype)
     ki, kv = _gpu_codes(kk, k, idx_dtype, val_dtype)
     scale = 1.0 / math.sqrt(d)
-    o32, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=torch.float32)
+    o32, lse = fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=torch.float32)
     ob16 = None
     if v_bf16:
-        ob16, _ = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale,
-                                   o_dtype=torch.bfloat16, want_lse=False)
+        ob16, _ = fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=torch.bfloat16,
+                      want_lse=False)
     torch.cuda.synchronize()
     # oracle: its own codes of the same dense inputs
     qn, kn, vn = q.cpu().numpy(), kk.cpu().numpy(), np_vals(v)
@@ -82,9 +83,27 @@ def test_tiny_workload_fp32():
         (1, 2, 1, 129, 128, 64, True, True),   # largest supported k at d = 128
         (2, 4, 2, 96, 128, 16, False, False),  # float32 V, GQA 2:1
         (1, 16, 1, 70, 64, 8, True, True),     # 16 heads per KV head
+        (1, 2, 2, 140, 128, 128, True, True),  # k = d = 128
+        (1, 8, 2, 700, 128, 16, True, True),   # GQA 4:1 over eleven key tiles
+        (1, 2, 2, 333, 128, 16, True, False),  # float32 V, causal, ragged
     ])
 def test_shapes(B, Hq, Hkv, n, d, k, causal, v_bf16):
     _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=B * 1000 + Hq * 100 + n)
+
+
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,v_bf16",
+    [
+        (1, 1, 1, 37, 64, 8, True, False),
+        (2, 2, 2, 130, 64, 16, True, True),
+        (1, 4, 1, 200, 128, 16, True, True),
+        (1, 2, 1, 257, 128, 8, False, True),
+        (1, 2, 2, 150, 64, 64, True, False),
+        (1, 16, 1, 70, 64, 8, True, True),
+    ])
+def test_index_variant(B, Hq, Hkv, n, d, k, causal, v_bf16):
+    _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=B * 1000 + Hq * 100 + n + 7,
+              fwd=sfa.sfa_attn_fwd_index)
 
 
 def test_int16_indices_bf16_values():
@@ -151,14 +170,25 @@ def test_zipf_128k_full_size_sampled():
     _big_case_sampled(si.workload("zipf_128k"), heads=(0, 7), zipf=True)
 
 
-def test_repeatable():
-    # the score accumulation order may vary between runs (LDS float atomics);
-    # two runs must agree far inside the tolerance
+def test_deterministic():
+    # the matrix-core forward has a fixed summation order: bitwise repeatable
     q, kk, v = si.dense_qkv(1, 4, 1, 500, 128, 9, device=DEV)
     qi, qv = _gpu_codes(q, 16)
     ki, kv = _gpu_codes(kk, 16)
     o1, l1 = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.float32)
     o2, l2 = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_index_variant_repeatable():
+    # the inverted-index variant accumulates with LDS float atomics, whose
+    # order may vary between runs; two runs agree far inside the tolerance
+    q, kk, v = si.dense_qkv(1, 4, 1, 500, 128, 9, device=DEV)
+    qi, qv = _gpu_codes(q, 16)
+    ki, kv = _gpu_codes(kk, 16)
+    o1, l1 = sfa.sfa_attn_fwd_index(qi, qv, ki, kv, v, o_dtype=torch.float32)
+    o2, l2 = sfa.sfa_attn_fwd_index(qi, qv, ki, kv, v, o_dtype=torch.float32)
     torch.cuda.synchronize()
     assert (o1 - o2).abs().max().item() < 1e-5
     assert (l1 - l2).abs().max().item() < 1e-5
