@@ -316,6 +316,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3_32k", choices=sorted(si.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, run a plain 1 GiB device copy twice (reference for "
+                         "the FETCH_SIZE / WRITE_SIZE counters of a profiling run)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the SFA hot path here is built and measured "
@@ -330,6 +333,13 @@ def main():
         out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline)
     else:
         out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=DEV)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = src.numel() * 4
     print(json.dumps(out), flush=True)
 
 

@@ -52,21 +52,36 @@ struct FwdParams {
   float inv_k;
 };
 
-template <int D>
+template <int D, int NP>
 struct Geo {
-  static constexpr int KP = D + 8;    // bf16 pitch of a densified row
-  static constexpr int VP = kBC + 8;  // bf16 pitch of a transposed V row
-  static constexpr int NKB = D / 16;  // 16-coordinate blocks of the score MFMA
-  static constexpr int NDB = D / 32;  // 32-wide output blocks
+  static constexpr int QP = D + 8;           // bf16 pitch of a densified query row (setup)
+  static constexpr int KR = NP * D + 8;      // bf16 pitch of a key row: [piece][coordinate] + pad
+  static constexpr int VP = kBC + 4;         // bf16 pitch of a transposed V row
+  static constexpr int NKB = D / 16;         // 16-coordinate blocks of the score MFMA
+  static constexpr int NDB = D / 32;         // 32-wide output blocks
 };
+// Pitches: a key row of KR bf16 is 4 dwords past a multiple of 32 banks, so
+// the 16-byte A-operand reads of consecutive keys hit disjoint banks; a V row
+// of 68 bf16 is 2 dwords past, for the 8-byte operand reads.
+
+template <int D, bool VBF16>
+__host__ __device__ constexpr int stage_bytes() {
+  constexpr int NP = VBF16 ? 2 : 3;
+  return kBC * Geo<D, NP>::KR * 2 + (VBF16 ? D * Geo<D, NP>::VP * 2 : kBC * D * 4);
+}
+
+// Two LDS stages (next tile written while the current one is read) when they
+// fit; the float32-V path (three pieces, float32 V tile) uses one.
+template <int D, bool VBF16>
+__host__ __device__ constexpr int n_stages() {
+  return 2 * stage_bytes<D, VBF16>() <= 160 * 1024 ? 2 : 1;
+}
 
 template <int D, bool VBF16, int NW>
 __host__ __device__ constexpr int lds_bytes() {
-  constexpr int NP = VBF16 ? 2 : 3;
-  constexpr int kd = NP * kBC * Geo<D>::KP * 2;
-  constexpr int vt = VBF16 ? D * Geo<D>::VP * 2 : kBC * D * 4;
-  constexpr int qs = NW * 32 * Geo<D>::KP * 2;
-  return (kd + vt) > qs ? (kd + vt) : qs;
+  constexpr int st = n_stages<D, VBF16>() * stage_bytes<D, VBF16>();
+  constexpr int qs = NW * 32 * Geo<D, 2>::QP * 2;
+  return st > qs ? st : qs;
 }
 
 // bf16 piece `pc` of x (0: nearest bf16; 1, 2: bf16 of the remaining error).
@@ -79,17 +94,30 @@ __device__ __forceinline__ uint16_t bf16_piece(float x, int pc) {
   return (uint16_t)f32_to_bf16_rne(r1 - bf16_bits_to_f32(m));
 }
 
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// The running row maximum is raised only when a tile's maximum exceeds it by
+// more than this (log2 units), so probabilities stay below 2^kLazyMax and the
+// accumulators are rescaled rarely; O and LSE use the same stale maximum.
+constexpr float kLazyMax = 8.f;
+
 template <int D, bool VBF16, int NW, int KM>
 __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   constexpr int NT = NW * 64;
   constexpr int R = NW * 32;
   constexpr int NP = VBF16 ? 2 : 3;
-  constexpr int KP = Geo<D>::KP, VP = Geo<D>::VP, NKB = Geo<D>::NKB, NDB = Geo<D>::NDB;
-  constexpr int KE = (kBC * KM + NT - 1) / NT;  // key-code entries per thread and tile
+  using Gm = Geo<D, NP>;
+  constexpr int QP = Gm::QP, KR = Gm::KR, VP = Gm::VP, NKB = Gm::NKB, NDB = Gm::NDB;
+  constexpr int NS = n_stages<D, VBF16>();
+  constexpr int SB = stage_bytes<D, VBF16>();
+  constexpr int KW = kBC / NW;                 // key rows owned (zeroed, filled) by a wave
+  constexpr int KEL = (KW * KM + 63) / 64;     // key-code entries per lane and tile
+  constexpr int NDP = D / 2;
+  constexpr int VITEMS = VBF16 ? NDP * (kBC / 8) : kBC * D / 4;
+  constexpr int VI = (VITEMS + NT - 1) / NT;   // V items per thread and tile
+  constexpr int VW = VBF16 ? 8 : 4;            // registers per V item
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t* Kd = (uint16_t*)smem;                    // [NP][kBC][KP]
-  unsigned char* vt = smem + NP * kBC * KP * 2;      // V tile
-  uint16_t* Qs = (uint16_t*)smem;                    // setup only: [R][KP]
+  uint16_t* Qs = (uint16_t*)smem;              // setup only: [R][QP]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -116,7 +144,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   bf16x8 qB[NP][NKB];
 #pragma unroll
   for (int pc = 0; pc < NP; ++pc) {
-    for (int x = tid; x < R * KP / 8; x += NT) ((uint4*)Qs)[x] = make_uint4(0u, 0u, 0u, 0u);
+    for (int x = tid; x < R * QP / 8; x += NT) ((uint4*)Qs)[x] = make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
     for (int e = tid; e < R * k; e += NT) {
       const int r = (int)(((float)e + 0.5f) * p.inv_k);
@@ -126,17 +154,14 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
         const int hq = hkv * p.G + r / p.BR;
         const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
         const int f = load_idx(p.q_idx, gi, p.idx16, dmask);
-        Qs[r * KP + f] = bf16_piece(load_val(p.q_val, gi, p.valbf16), pc);
+        Qs[r * QP + f] = bf16_piece(load_val(p.q_val, gi, p.valbf16), pc);
       }
     }
     __syncthreads();
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) qB[pc][kb] = *(const bf16x8*)(Qs + rho * KP + kb * 16 + 8 * hh);
+    for (int kb = 0; kb < NKB; ++kb) qB[pc][kb] = *(const bf16x8*)(Qs + rho * QP + kb * 16 + 8 * hh);
     __syncthreads();
   }
-  // the dense key tile starts (and is kept) all-zero between tiles
-  for (int x = tid; x < NP * kBC * KP / 8; x += NT) ((uint4*)Kd)[x] = make_uint4(0u, 0u, 0u, 0u);
-  __syncthreads();
 
   float m_run = -INFINITY, l_run = 0.f;
   floatx16 acc[NDB];
@@ -146,151 +171,264 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
   const int wave_i_max = i0 + (wave * 32 + 31) % p.BR;  // largest position in this wave
+  const int wave_i_min = p.BR >= 32 ? i0 + (wave * 32) % p.BR : i0;
   const int blk_last = min(n, i0 + p.BR) - 1;
   const int n_keys = p.causal ? blk_last + 1 : n;
   const int ntiles = (n_keys + kBC - 1) / kBC;
   const int64_t kv_base = ((int64_t)b * p.Hkv + hkv) * n;
-  const int nke = kBC * k;
+  const float c = p.scale_log2;
 
-  uint32_t ent[KE];  // (key << 8) | coordinate of this thread's scattered entries
-  for (int jt = 0; jt < ntiles; ++jt) {
+  // ---- global -> registers for one tile ----
+  // Per-lane offsets are loop-invariant; loads are unconditional (indices
+  // clamped into the arrays on the last tile only) and the dtype branches are
+  // uniform, so nothing waits on them until write_tile.
+  int k_off[KEL], k_row[KEL];
+#pragma unroll
+  for (int r = 0; r < KEL; ++r) {
+    int el = lane + 64 * r;
+    const bool ok = el < KW * k;
+    el = ok ? el : KW * k - 1;
+    const int cl = (int)(((float)el + 0.5f) * p.inv_k);
+    k_row[r] = ok ? wave * KW + cl : -1;
+    k_off[r] = (wave * KW + cl) * k + (el - cl * k);
+  }
+  int kf[KEL];
+  float kx[KEL];
+  uint32_t vr[VI][VW];
+  auto load_tile = [&](int jt) {
     const int j0 = jt * kBC;
-
-    // ---- [A] key codes -> dense bf16 pieces; V tile -> LDS ----
+    const bool full = j0 + kBC <= n;
+    int64_t gi[KEL];
 #pragma unroll
-    for (int r = 0; r < KE; ++r) {
-      const int e = tid + r * NT;
-      ent[r] = 0xffffffffu;
-      if (e < nke) {
-        const int c = (int)(((float)e + 0.5f) * p.inv_k);
-        const int t = e - c * k;
-        const int j = j0 + c;
-        if (j < n) {
-          const int64_t gi = (kv_base + j) * k + t;
-          const int f = load_idx(p.k_idx, gi, p.idx16, dmask);
-          const float x = load_val(p.k_val, gi, p.valbf16);
-          ent[r] = ((uint32_t)c << 8) | (uint32_t)f;
-#pragma unroll
-          for (int pc = 0; pc < NP; ++pc) Kd[(pc * kBC + c) * KP + f] = bf16_piece(x, pc);
-        }
+    for (int r = 0; r < KEL; ++r) {
+      if (full) {
+        gi[r] = (kv_base + j0) * k + k_off[r];
+      } else {
+        const int row = k_row[r] < 0 ? 0 : k_row[r];
+        const int j = min(j0 + row, n - 1);
+        gi[r] = (kv_base + j) * k + (k_off[r] - row * k);
       }
     }
-    if constexpr (VBF16) {
-      uint16_t* Vt = (uint16_t*)vt;
-      const uint16_t* Vg = (const uint16_t*)p.v;
-      constexpr int NDP = D / 2;
-      constexpr int ITEMS = NDP * (kBC / 8);
-      for (int it = tid; it < ITEMS; it += NT) {
-        const int dp = it % NDP;
-        const int kg = it / NDP;
+    if (p.idx16) {
+#pragma unroll
+      for (int r = 0; r < KEL; ++r) kf[r] = ((const int16_t*)p.k_idx)[gi[r]];
+    } else {
+#pragma unroll
+      for (int r = 0; r < KEL; ++r) kf[r] = ((const int32_t*)p.k_idx)[gi[r]];
+    }
+    if (p.valbf16) {
+#pragma unroll
+      for (int r = 0; r < KEL; ++r) kx[r] = __uint_as_float((uint32_t)((const uint16_t*)p.k_val)[gi[r]] << 16);
+    } else {
+#pragma unroll
+      for (int r = 0; r < KEL; ++r) kx[r] = ((const float*)p.k_val)[gi[r]];
+    }
+#pragma unroll
+    for (int r = 0; r < VI; ++r) {
+      const int it = min(tid + r * NT, VITEMS - 1);
+      if constexpr (VBF16) {
+        const int dp = it % NDP, kg = it / NDP;
+        const uint16_t* src = (const uint16_t*)p.v + (kv_base + j0 + kg * 8) * D + 2 * dp;
+        if (full) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) vr[r][e] = *(const uint32_t*)(src + e * D);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int j = min(j0 + kg * 8 + e, n - 1);
+            vr[r][e] = *(const uint32_t*)((const uint16_t*)p.v + (kv_base + j) * D + 2 * dp);
+          }
+        }
+      } else {
+        const float* Vg = (const float*)p.v;
+        const int j = min(j0 + it / (D / 4), n - 1), c4 = it % (D / 4);
+        const uint4 val = *(const uint4*)(Vg + (kv_base + j) * D + 4 * c4);
+        vr[r][0] = val.x; vr[r][1] = val.y; vr[r][2] = val.z; vr[r][3] = val.w;
+      }
+    }
+  };
+  // ---- registers -> LDS stage: zero own key rows, scatter own codes, V ----
+  // Stage layout: Kd[key][piece][coordinate] (pitch KR), then the V tile.
+  auto write_tile = [&](int stage, int jt) {
+    const int j0 = jt * kBC;
+    uint16_t* Kd = (uint16_t*)(smem + stage * SB);
+    unsigned char* vt = smem + stage * SB + kBC * KR * 2;
+    uint4* zrow = (uint4*)(Kd + wave * KW * KR);  // this wave's KW contiguous key rows
+    constexpr int NZ = KW * KR / 8;
+#pragma unroll
+    for (int x = lane; x < NZ; x += 64) zrow[x] = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int r = 0; r < KEL; ++r) {
+      if (k_row[r] >= 0 && j0 + k_row[r] < n) {
+        const int f = kf[r] & dmask;
+#pragma unroll
+        for (int pc = 0; pc < NP; ++pc) Kd[k_row[r] * KR + pc * D + f] = bf16_piece(kx[r], pc);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < VI; ++r) {
+      const int it = tid + r * NT;
+      if (it >= VITEMS) break;
+      if constexpr (VBF16) {
+        uint16_t* Vt = (uint16_t*)vt;
+        const int dp = it % NDP, kg = it / NDP;
         uint32_t w[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int j = j0 + kg * 8 + e;
-          w[e] = (j < n) ? *(const uint32_t*)(Vg + (kv_base + j) * D + 2 * dp) : 0u;
-        }
-        uint4 lo, hi;
-        lo.x = (w[0] & 0xffffu) | (w[1] << 16); hi.x = (w[0] >> 16) | (w[1] & 0xffff0000u);
-        lo.y = (w[2] & 0xffffu) | (w[3] << 16); hi.y = (w[2] >> 16) | (w[3] & 0xffff0000u);
-        lo.z = (w[4] & 0xffffu) | (w[5] << 16); hi.z = (w[4] >> 16) | (w[5] & 0xffff0000u);
-        lo.w = (w[6] & 0xffffu) | (w[7] << 16); hi.w = (w[6] >> 16) | (w[7] & 0xffff0000u);
-        *(uint4*)(Vt + (2 * dp) * VP + kg * 8) = lo;
-        *(uint4*)(Vt + (2 * dp + 1) * VP + kg * 8) = hi;
-      }
-    } else {
-      float* Vs = (float*)vt;
-      const float* Vg = (const float*)p.v;
-      constexpr int N4 = kBC * D / 4;
-      for (int it = tid; it < N4; it += NT) {
-        const int j = it / (D / 4);
-        const int c4 = it % (D / 4);
-        float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (j0 + j < n) val = *(const float4*)(Vg + (kv_base + j0 + j) * D + 4 * c4);
-        *(float4*)(Vs + j * D + 4 * c4) = val;
+        for (int e = 0; e < 8; ++e) w[e] = (j0 + kg * 8 + e < n) ? vr[r][e] : 0u;
+        uint2 lo0, lo1, hi0, hi1;
+        lo0.x = (w[0] & 0xffffu) | (w[1] << 16); hi0.x = (w[0] >> 16) | (w[1] & 0xffff0000u);
+        lo0.y = (w[2] & 0xffffu) | (w[3] << 16); hi0.y = (w[2] >> 16) | (w[3] & 0xffff0000u);
+        lo1.x = (w[4] & 0xffffu) | (w[5] << 16); hi1.x = (w[4] >> 16) | (w[5] & 0xffff0000u);
+        lo1.y = (w[6] & 0xffffu) | (w[7] << 16); hi1.y = (w[6] >> 16) | (w[7] & 0xffff0000u);
+        uint16_t* r0 = Vt + (2 * dp) * VP + kg * 8;
+        uint16_t* r1 = r0 + VP;
+        *(uint2*)r0 = lo0; *(uint2*)(r0 + 4) = lo1;
+        *(uint2*)r1 = hi0; *(uint2*)(r1 + 4) = hi1;
+      } else {
+        float* Vs = (float*)vt;
+        const int j = it / (D / 4), c4 = it % (D / 4);
+        const bool ok = j0 + j < n;
+        *(uint4*)(Vs + j * D + 4 * c4) = ok ? make_uint4(vr[r][0], vr[r][1], vr[r][2], vr[r][3])
+                                            : make_uint4(0u, 0u, 0u, 0u);
       }
     }
-    __syncthreads();
+  };
 
-    // ---- [B] scores on MFMA, online softmax, P.V on MFMA ----
+  if (ntiles > 0 && NS == 2) {
+    load_tile(0);
+    write_tile(0, 0);
+  }
+  __syncthreads();
+
+  for (int jt = 0; jt < ntiles; ++jt) {
+    const int j0 = jt * kBC;
+    const int stage = NS == 2 ? (jt & 1) : 0;
+    if constexpr (NS == 1) {
+      load_tile(jt);
+      write_tile(0, jt);
+      __syncthreads();
+    } else {
+      if (jt + 1 < ntiles) load_tile(jt + 1);  // in flight during this tile's compute
+    }
+    const uint16_t* Kd = (const uint16_t*)(smem + stage * SB);
+    const unsigned char* vt = smem + stage * SB + kBC * KR * 2;
+
+    // ---- scores on MFMA, online softmax, P.V on MFMA ----
     const bool act0 = !p.causal || wave_i_max >= j0;
     const bool act1 = !p.causal || wave_i_max >= j0 + 32;
     if (act0) {
       floatx16 sc[2];
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
+      for (int s = 0; s < 2; ++s)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sc[s][r] = 0.f;
-        if (s == 0 || act1) {
+      const int nsub = act1 ? 2 : 1;
 #pragma unroll
-          for (int kb = 0; kb < NKB; ++kb) {
-            bf16x8 ka[NP];
+      for (int kb = 0; kb < NKB; ++kb) {
+        bf16x8 ka[2][NP];
 #pragma unroll
-            for (int pc = 0; pc < NP; ++pc)
-              ka[pc] = *(const bf16x8*)(Kd + (pc * kBC + s * 32 + l32) * KP + kb * 16 + 8 * hh);
-            // smaller terms first
-            if constexpr (NP == 3) {
-              sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[2], qB[0][kb], sc[s], 0, 0, 0);
-              sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[1][kb], sc[s], 0, 0, 0);
-              sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[2][kb], sc[s], 0, 0, 0);
-            }
-            sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[0][kb], sc[s], 0, 0, 0);
-            sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[1][kb], sc[s], 0, 0, 0);
-            sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], sc[s], 0, 0, 0);
-          }
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+          for (int pc = 0; pc < NP; ++pc)
+            if (s < nsub) ka[s][pc] = *(const bf16x8*)(Kd + (s * 32 + l32) * KR + pc * D + kb * 16 + 8 * hh);
+        // smaller terms first; the two sub-tiles alternate so that consecutive
+        // MFMAs never accumulate into the same registers
+#define SFA_TERM(ia, ib)                                                                  \
+  _Pragma("unroll") for (int s = 0; s < 2; ++s) if (s < nsub)                             \
+      sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s][ia], qB[ib][kb], sc[s], 0, 0, 0);
+        if constexpr (NP == 3) {
+          SFA_TERM(2, 0)
+          SFA_TERM(1, 1)
+          SFA_TERM(0, 2)
         }
+        SFA_TERM(1, 0)
+        SFA_TERM(0, 1)
+        SFA_TERM(0, 0)
+#undef SFA_TERM
       }
       // lane: query row rho; register r of sub-tile s holds key
-      // j0 + 32 s + 8 (r / 4) + 4 hh + (r % 4)
-      float mt = -INFINITY;
+      // j0 + 32 s + 8 (r / 4) + 4 hh + (r % 4).  Scores become base-2
+      // exponents t = s * c; masked keys get t = -inf.
+      const bool need_mask = !row_ok || j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min);
+      float mt;
+      if (need_mask) {
+        mt = -INFINITY;
 #pragma unroll
-      for (int s = 0; s < 2; ++s)
+        for (int s = 0; s < 2; ++s)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
-          sc[s][r] = ok ? sc[s][r] * p.scale_log2 : -INFINITY;
-          mt = fmaxf(mt, sc[s][r]);
-        }
+          for (int r = 0; r < 16; ++r) {
+            const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
+            const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
+            sc[s][r] = ok ? sc[s][r] * c : -INFINITY;
+            mt = fmaxf(mt, sc[s][r]);
+          }
+      } else {
+        // no mask: the extreme raw score scales to the extreme exponent
+        float hi = sc[0][0], lo = sc[0][0];
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) { hi = fmaxf(hi, sc[s][r]); lo = fminf(lo, sc[s][r]); }
+        mt = (c >= 0.f ? hi : lo) * c;
+      }
       mt = fmaxf(mt, swap_halves(mt));
-      const float m_new = fmaxf(m_run, mt);
+      const bool upd = mt > m_run + kLazyMax;
+      const float m_new = upd ? mt : m_run;
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_use);
-      float rs = 0.f;
+      if (__builtin_amdgcn_ballot_w64(upd)) {
+        const float alpha = upd ? fast_exp2(m_run - m_use) : 1.f;
+        l_run *= alpha;
 #pragma unroll
-      for (int s = 0; s < 2; ++s)
+        for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          sc[s][r] = exp2f(sc[s][r] - m_use);
-          rs += sc[s][r];
-        }
-      rs += swap_halves(rs);
-      l_run = l_run * alpha + rs;
+          for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
+      }
       m_run = m_new;
+      float rs = 0.f;
+      if (need_mask) {
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+        for (int s = 0; s < 2; ++s)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
+          for (int r = 0; r < 16; ++r) { sc[s][r] = fast_exp2(sc[s][r] - m_use); rs += sc[s][r]; }
+      } else {
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) { sc[s][r] = fast_exp2(fmaf(sc[s][r], c, -m_use)); rs += sc[s][r]; }
+      }
+      rs += swap_halves(rs);
+      l_run += rs;
 
       if constexpr (VBF16) {
+        // P = Ph + Pl, both bfloat16 (Pl = bf16(P - Ph)): two MFMAs, so the
+        // probabilities enter P.V with ~2^-17 relative error.
         const uint16_t* Vt = (const uint16_t*)vt;
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
           if (s == 1 && !act1) break;
 #pragma unroll
           for (int kk = 0; kk < 2; ++kk) {
-            bf16x8 pb;
+            bf16x8 ph, pl;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) pb[e] = (__bf16)sc[s][8 * kk + e];
+            for (int e = 0; e < 8; ++e) ph[e] = (__bf16)sc[s][8 * kk + e];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pl[e] = (__bf16)(sc[s][8 * kk + e] - (float)ph[e]);
             const int kbase = 32 * s + 16 * kk + 4 * hh;  // keys kbase+0..3, kbase+8..11
+            bf16x8 va[NDB];
 #pragma unroll
             for (int db = 0; db < NDB; ++db) {
               const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
               const uint2 v0 = *(const uint2*)row;
               const uint2 v1 = *(const uint2*)(row + 8);
               const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
-              const bf16x8 va = __builtin_bit_cast(bf16x8, vw);
-              acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc[db], 0, 0, 0);
+              va[db] = __builtin_bit_cast(bf16x8, vw);
             }
+#pragma unroll
+            for (int db = 0; db < NDB; ++db)
+              acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pl, acc[db], 0, 0, 0);
+#pragma unroll
+            for (int db = 0; db < NDB; ++db)
+              acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], ph, acc[db], 0, 0, 0);
           }
         }
       } else {
@@ -309,16 +447,8 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
         }
       }
     }
-    __syncthreads();
-
-    // ---- [C] clear the scattered key entries ----
-#pragma unroll
-    for (int r = 0; r < KE; ++r) {
-      if (ent[r] != 0xffffffffu) {
-        const int c = (int)(ent[r] >> 8), f = (int)(ent[r] & 0xffu);
-#pragma unroll
-        for (int pc = 0; pc < NP; ++pc) Kd[(pc * kBC + c) * KP + f] = 0;
-      }
+    if constexpr (NS == 2) {
+      if (jt + 1 < ntiles) write_tile(stage ^ 1, jt + 1);
     }
     __syncthreads();
   }
