@@ -249,26 +249,37 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   };
   // ---- registers -> LDS stage: zero own key rows, scatter own codes, V ----
   // Stage layout: Kd[key][piece][coordinate] (pitch KR), then the V tile.
-  auto write_tile = [&](int stage, int jt) {
+  auto write_tile_keys = [&](int stage, int jt) {
     const int j0 = jt * kBC;
     uint16_t* Kd = (uint16_t*)(smem + stage * SB);
-    unsigned char* vt = smem + stage * SB + kBC * KR * 2;
-    uint4* zrow = (uint4*)(Kd + wave * KW * KR);  // this wave's KW contiguous key rows
-    constexpr int NZ = KW * KR / 8;
+    // zero the coordinate part of this wave's KW key rows (straight-line)
+    constexpr int RU4 = NP * D / 8;  // uint4 per row, padding excluded
+    static_assert((KW * RU4) % 64 == 0, "row zeroing must be whole wave steps");
 #pragma unroll
-    for (int x = lane; x < NZ; x += 64) zrow[x] = make_uint4(0u, 0u, 0u, 0u);
+    for (int i = 0; i < KW * RU4 / 64; ++i) {
+      const int x = lane + 64 * i;
+      const int row = x / RU4, col = x - row * RU4;
+      *(uint4*)(Kd + (wave * KW + row) * KR + col * 8) = make_uint4(0u, 0u, 0u, 0u);
+    }
+    // scatter this lane's codes; entries outside the sequence write into the
+    // row padding (never read), so the code stays branch-free
 #pragma unroll
     for (int r = 0; r < KEL; ++r) {
-      if (k_row[r] >= 0 && j0 + k_row[r] < n) {
-        const int f = kf[r] & dmask;
+      const bool ok = k_row[r] >= 0 && j0 + k_row[r] < n;
+      const int row = k_row[r] < 0 ? 0 : k_row[r];
+      const int f = kf[r] & dmask;
 #pragma unroll
-        for (int pc = 0; pc < NP; ++pc) Kd[k_row[r] * KR + pc * D + f] = bf16_piece(kx[r], pc);
-      }
+      for (int pc = 0; pc < NP; ++pc)
+        Kd[row * KR + (ok ? pc * D + f : NP * D + pc)] = bf16_piece(kx[r], pc);
     }
+  };
+  auto write_tile_v = [&](int stage, int jt) {
+    const int j0 = jt * kBC;
+    unsigned char* vt = smem + stage * SB + kBC * KR * 2;
 #pragma unroll
     for (int r = 0; r < VI; ++r) {
       const int it = tid + r * NT;
-      if (it >= VITEMS) break;
+      if (VITEMS % NT != 0 && it >= VITEMS) break;
       if constexpr (VBF16) {
         uint16_t* Vt = (uint16_t*)vt;
         const int dp = it % NDP, kg = it / NDP;
@@ -294,11 +305,257 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     }
   };
 
+  auto write_tile = [&](int stage, int jt) {
+    write_tile_keys(stage, jt);
+    write_tile_v(stage, jt);
+  };
   if (ntiles > 0 && NS == 2) {
     load_tile(0);
     write_tile(0, 0);
   }
   __syncthreads();
+
+  // ---- building blocks of a key tile -------------------------------------
+  // S^T for keys 32 s .. 32 s + 31 of the tile, this wave's 32 rows: lane
+  // (row rho) register r holds key 32 s + 8 (r / 4) + 4 hh + (r % 4).
+  auto score_sub = [&](floatx16& o, int s, const uint16_t* Kd) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[r] = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+      bf16x8 ka[NP];
+#pragma unroll
+      for (int pc = 0; pc < NP; ++pc)
+        ka[pc] = *(const bf16x8*)(Kd + (s * 32 + l32) * KR + pc * D + kb * 16 + 8 * hh);
+      // smaller terms first
+      if constexpr (NP == 3) {
+        o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[2], qB[0][kb], o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[1][kb], o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[2][kb], o, 0, 0, 0);
+      }
+      o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[0][kb], o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[1][kb], o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
+    }
+  };
+  // largest base-2 exponent s * c of a sub-tile (no mask), combined over the
+  // two lanes of the row
+  auto sub_max = [&](const floatx16& o) {
+    float hi = o[0], lo = o[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) { hi = fmaxf(hi, o[r]); lo = fminf(lo, o[r]); }
+    const float mt = (c >= 0.f ? hi : lo) * c;
+    return fmaxf(mt, swap_halves(mt));
+  };
+  // probabilities 2^(s c - m) in place; returns their (lane-partial) sum
+  auto sub_exp = [&](floatx16& o) {
+    float rs = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) { o[r] = fast_exp2(fmaf(o[r], c, -m_run)); rs += o[r]; }
+    return rs;
+  };
+  // P = Ph + Pl in bfloat16 (Pl = bf16(P - Ph)), per 16-key PV block kk
+  auto split_p = [&](const floatx16& pr, bf16x8 (&ph)[2], bf16x8 (&pl)[2]) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        ph[kk][e] = (__bf16)pr[8 * kk + e];
+        pl[kk][e] = (__bf16)(pr[8 * kk + e] - (float)ph[kk][e]);
+      }
+  };
+  // O^T += V^T P^T for the 32 keys of sub-tile s (bf16 V)
+  auto pv_sub = [&](int s, const bf16x8 (&ph)[2], const bf16x8 (&pl)[2], const uint16_t* Vt) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int kbase = 32 * s + 16 * kk + 4 * hh;  // keys kbase+0..3, kbase+8..11
+      bf16x8 va[NDB];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
+        const uint2 v0 = *(const uint2*)row;
+        const uint2 v1 = *(const uint2*)(row + 8);
+        const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
+        va[db] = __builtin_bit_cast(bf16x8, vw);
+      }
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pl[kk], acc[db], 0, 0, 0);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], ph[kk], acc[db], 0, 0, 0);
+    }
+  };
+  auto rescale = [&](float alpha) {
+    l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
+  };
+
+  // ---- generic tile: any mask, first tile, large jumps of the maximum -----
+  auto generic_tile = [&](int j0, bool act1, const uint16_t* Kd, const unsigned char* vt) {
+    floatx16 sc[2];
+    score_sub(sc[0], 0, Kd);
+    if (act1) score_sub(sc[1], 1, Kd);
+    else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[1][r] = 0.f;
+    }
+    // base-2 exponents t = s * c; masked keys get t = -inf
+    float mt = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
+        const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
+        sc[s][r] = ok ? sc[s][r] * c : -INFINITY;
+        mt = fmaxf(mt, sc[s][r]);
+      }
+    mt = fmaxf(mt, swap_halves(mt));
+    const bool upd = mt > m_run + kLazyMax;
+    const float m_new = upd ? mt : m_run;
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    if (__builtin_amdgcn_ballot_w64(upd)) rescale(upd ? fast_exp2(m_run - m_use) : 1.f);
+    m_run = m_new;
+    float rs = 0.f;
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { sc[s][r] = fast_exp2(sc[s][r] - m_use); rs += sc[s][r]; }
+    l_run += rs;
+    if constexpr (VBF16) {
+      const uint16_t* Vt = (const uint16_t*)vt;
+      bf16x8 ph[2], pl[2];
+      split_p(sc[0], ph, pl);
+      pv_sub(0, ph, pl, Vt);
+      if (act1) {
+        split_p(sc[1], ph, pl);
+        pv_sub(1, ph, pl, Vt);
+      }
+    } else {
+      const float* Vs = (const float*)vt;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        if (s == 1 && !act1) break;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int jj = 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
+#pragma unroll
+          for (int db = 0; db < NDB; ++db)
+            acc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(Vs[jj * D + db * 32 + l32], sc[s][r],
+                                                           acc[db], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  // ---- interior tile, software-pipelined by 32-key sub-tile ---------------
+  // A: scores(0)  B: scores(1) || softmax(0)  C: P.V(0) || softmax(1)
+  // D: P.V(1) || next tile's LDS writes.  Within B, C and D the source is
+  // sliced by hand (one MFMA group plus its share of independent VALU work,
+  // operands read one slice ahead) and sched_barrier fences keep that order,
+  // so the matrix pipe and the VALU work side by side.  The maximum stays
+  // fixed unless a sub-tile exceeds it by 2^kLazyMax: after A that hands the
+  // tile to generic_tile (returns false); after B it is fixed up in place.
+  auto ka_load = [&](bf16x8 (&ka)[NP], int s, int kb, const uint16_t* Kd) {
+#pragma unroll
+    for (int pc = 0; pc < NP; ++pc)
+      ka[pc] = *(const bf16x8*)(Kd + (s * 32 + l32) * KR + pc * D + kb * 16 + 8 * hh);
+  };
+  auto score_terms = [&](floatx16& o, const bf16x8 (&ka)[NP], int kb) {
+    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[0][kb], o, 0, 0, 0);
+    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[1][kb], o, 0, 0, 0);
+    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
+  };
+  // probability of value r (exp of the lane's score), its split into ph/pl
+  auto exp_split = [&](floatx16& o, int r, float& rs, bf16x8 (&ph)[2], bf16x8 (&pl)[2]) {
+    const float pr = fast_exp2(fmaf(o[r], c, -m_run));
+    rs += pr;
+    const __bf16 h = (__bf16)pr;
+    ph[r >> 3][r & 7] = h;
+    pl[r >> 3][r & 7] = (__bf16)(pr - (float)h);
+  };
+  auto va_load = [&](bf16x8 (&va)[NDB], int s, int kk, const uint16_t* Vt) {
+    const int kbase = 32 * s + 16 * kk + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
+      const uint2 v0 = *(const uint2*)row;
+      const uint2 v1 = *(const uint2*)(row + 8);
+      const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
+      va[db] = __builtin_bit_cast(bf16x8, vw);
+    }
+  };
+  auto pv_terms = [&](const bf16x8 (&va)[NDB], const bf16x8& ph, const bf16x8& pl) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pl, acc[db], 0, 0, 0);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], ph, acc[db], 0, 0, 0);
+  };
+
+  auto fast_tile = [&](const uint16_t* Kd, const uint16_t* Vt, int jt_next, int stage_next) {
+    // ---- A ----
+    floatx16 s0, s1;
+    score_sub(s0, 0, Kd);
+    if (__builtin_amdgcn_ballot_w64(sub_max(s0) > m_run + kLazyMax)) return false;
+    // ---- B: scores(1) || softmax(0) ----
+    bf16x8 ph0[2], pl0[2];
+    float rs = 0.f;
+    {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s1[r] = 0.f;
+      bf16x8 ka[2][NP];
+      ka_load(ka[0], 1, 0, Kd);
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        if (kb + 1 < NKB) ka_load(ka[(kb + 1) & 1], 1, kb + 1, Kd);
+        score_terms(s1, ka[kb & 1], kb);
+        // 16 probabilities of sub-tile 0 spread over the NKB slices
+#pragma unroll
+        for (int q = 0; q < 16 / NKB; ++q) exp_split(s0, kb * (16 / NKB) + q, rs, ph0, pl0);
+      }
+    }
+    l_run += rs;
+    const float mt1 = sub_max(s1);
+    const bool up1 = mt1 > m_run + kLazyMax;
+    if (__builtin_amdgcn_ballot_w64(up1)) {
+      const float m_new = up1 ? mt1 : m_run;
+      const float alpha = fast_exp2(m_run - m_new);
+      rescale(alpha);
+      floatx16 p0;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p0[8 * kk + e] = ((float)ph0[kk][e] + (float)pl0[kk][e]) * alpha;
+      split_p(p0, ph0, pl0);
+      m_run = m_new;
+    }
+    // ---- C: P.V(0) || softmax(1) ----
+    bf16x8 ph1[2], pl1[2];
+    rs = 0.f;
+    bf16x8 va[2][NDB];
+    va_load(va[0], 0, 0, Vt);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      va_load(va[(kk + 1) & 1], kk == 0 ? 0 : 1, kk == 0 ? 1 : 0, Vt);  // next PV block
+      pv_terms(va[kk & 1], ph0[kk], pl0[kk]);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) exp_split(s1, 8 * kk + q, rs, ph1, pl1);
+    }
+    l_run += rs;
+    // ---- D: P.V(1) || next tile's LDS writes ----
+    va_load(va[1], 1, 1, Vt);
+    pv_terms(va[0], ph1[0], pl1[0]);
+    write_tile_keys(stage_next, jt_next);
+    pv_terms(va[1], ph1[1], pl1[1]);
+    write_tile_v(stage_next, jt_next);
+    return true;
+  };
 
   for (int jt = 0; jt < ntiles; ++jt) {
     const int j0 = jt * kBC;
@@ -308,150 +565,25 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
       write_tile(0, jt);
       __syncthreads();
     } else {
-      if (jt + 1 < ntiles) load_tile(jt + 1);  // in flight during this tile's compute
+      load_tile(jt + 1);  // past the end it reads clamped, valid addresses; unused
     }
     const uint16_t* Kd = (const uint16_t*)(smem + stage * SB);
     const unsigned char* vt = smem + stage * SB + kBC * KR * 2;
-
-    // ---- scores on MFMA, online softmax, P.V on MFMA ----
     const bool act0 = !p.causal || wave_i_max >= j0;
     const bool act1 = !p.causal || wave_i_max >= j0 + 32;
-    if (act0) {
-      floatx16 sc[2];
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sc[s][r] = 0.f;
-      const int nsub = act1 ? 2 : 1;
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        bf16x8 ka[2][NP];
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int pc = 0; pc < NP; ++pc)
-            if (s < nsub) ka[s][pc] = *(const bf16x8*)(Kd + (s * 32 + l32) * KR + pc * D + kb * 16 + 8 * hh);
-        // smaller terms first; the two sub-tiles alternate so that consecutive
-        // MFMAs never accumulate into the same registers
-#define SFA_TERM(ia, ib)                                                                  \
-  _Pragma("unroll") for (int s = 0; s < 2; ++s) if (s < nsub)                             \
-      sc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s][ia], qB[ib][kb], sc[s], 0, 0, 0);
-        if constexpr (NP == 3) {
-          SFA_TERM(2, 0)
-          SFA_TERM(1, 1)
-          SFA_TERM(0, 2)
-        }
-        SFA_TERM(1, 0)
-        SFA_TERM(0, 1)
-        SFA_TERM(0, 0)
-#undef SFA_TERM
-      }
-      // lane: query row rho; register r of sub-tile s holds key
-      // j0 + 32 s + 8 (r / 4) + 4 hh + (r % 4).  Scores become base-2
-      // exponents t = s * c; masked keys get t = -inf.
-      const bool need_mask = !row_ok || j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min);
-      float mt;
-      if (need_mask) {
-        mt = -INFINITY;
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
-            const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
-            sc[s][r] = ok ? sc[s][r] * c : -INFINITY;
-            mt = fmaxf(mt, sc[s][r]);
-          }
-      } else {
-        // no mask: the extreme raw score scales to the extreme exponent
-        float hi = sc[0][0], lo = sc[0][0];
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) { hi = fmaxf(hi, sc[s][r]); lo = fminf(lo, sc[s][r]); }
-        mt = (c >= 0.f ? hi : lo) * c;
-      }
-      mt = fmaxf(mt, swap_halves(mt));
-      const bool upd = mt > m_run + kLazyMax;
-      const float m_new = upd ? mt : m_run;
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      if (__builtin_amdgcn_ballot_w64(upd)) {
-        const float alpha = upd ? fast_exp2(m_run - m_use) : 1.f;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
-      }
-      m_run = m_new;
-      float rs = 0.f;
-      if (need_mask) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) { sc[s][r] = fast_exp2(sc[s][r] - m_use); rs += sc[s][r]; }
-      } else {
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) { sc[s][r] = fast_exp2(fmaf(sc[s][r], c, -m_use)); rs += sc[s][r]; }
-      }
-      rs += swap_halves(rs);
-      l_run += rs;
-
-      if constexpr (VBF16) {
-        // P = Ph + Pl, both bfloat16 (Pl = bf16(P - Ph)): two MFMAs, so the
-        // probabilities enter P.V with ~2^-17 relative error.
-        const uint16_t* Vt = (const uint16_t*)vt;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          if (s == 1 && !act1) break;
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
-            bf16x8 ph, pl;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) ph[e] = (__bf16)sc[s][8 * kk + e];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) pl[e] = (__bf16)(sc[s][8 * kk + e] - (float)ph[e]);
-            const int kbase = 32 * s + 16 * kk + 4 * hh;  // keys kbase+0..3, kbase+8..11
-            bf16x8 va[NDB];
-#pragma unroll
-            for (int db = 0; db < NDB; ++db) {
-              const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
-              const uint2 v0 = *(const uint2*)row;
-              const uint2 v1 = *(const uint2*)(row + 8);
-              const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
-              va[db] = __builtin_bit_cast(bf16x8, vw);
-            }
-#pragma unroll
-            for (int db = 0; db < NDB; ++db)
-              acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pl, acc[db], 0, 0, 0);
-#pragma unroll
-            for (int db = 0; db < NDB; ++db)
-              acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], ph, acc[db], 0, 0, 0);
-          }
-        }
-      } else {
-        const float* Vs = (const float*)vt;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          if (s == 1 && !act1) break;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int jj = 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
-#pragma unroll
-            for (int db = 0; db < NDB; ++db)
-              acc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(Vs[jj * D + db * 32 + l32], sc[s][r],
-                                                             acc[db], 0, 0, 0);
-          }
-        }
-      }
+    const bool need_mask = j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min) ||
+                           __builtin_amdgcn_ballot_w64(!row_ok || m_run == -INFINITY) != 0;
+    bool done = false;
+    if constexpr (NS == 2 && VBF16) {
+      if (act1 && !need_mask) done = fast_tile(Kd, (const uint16_t*)vt, jt + 1, stage ^ 1);
     }
-    if constexpr (NS == 2) {
-      if (jt + 1 < ntiles) write_tile(stage ^ 1, jt + 1);
+    if (!done) {
+      if (act0) generic_tile(j0, act1, Kd, vt);
+      if constexpr (NS == 2) write_tile(stage ^ 1, jt + 1);
     }
     __syncthreads();
   }
+  l_run += swap_halves(l_run);  // lane-partial row sums -> row sums
 
   // ---------------- epilogue: O = acc / l, LSE = ln(l) + m ln 2 -------------
   if (row_ok) {
