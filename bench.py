@@ -144,9 +144,10 @@ def bench_fwd(w, steps, warmup, want_cpu):
 
     pairs_per_head = n * (n + 1) // 2 if w.causal else n * n
     pairs = B * Hq * pairs_per_head
-    pv_flops = 2.0 * d * pairs
+    pv_flops = 2.0 * d * pairs          # P.V: 2 d flops per allowed pair
     E = _overlap_count(qi, ki, d, w.G, w.causal)
-    achieved = pv_flops / (fwd_avg * 1e-3)
+    algo_flops = pv_flops + 2.0 * E     # + one multiply-add per overlapping coordinate
+    achieved = algo_flops / (fwd_avg * 1e-3)
     tokens = B * n
     out = {
         "metric": METRIC,
@@ -175,7 +176,8 @@ def bench_fwd(w, steps, warmup, want_cpu):
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_MFMA_BF16,
             "traffic": _traffic("sfa_fwd.hip", w.name),
-            "algorithmic_flops_per_launch": pv_flops,
+            "algorithmic_flops_per_launch": algo_flops,
+            "pv_flops_per_launch": pv_flops,
             "fwd_ms_avg": fwd_avg,
             "fwd_ms_min": float(np.min(fwd_ms)),
             "allowed_pairs": pairs,

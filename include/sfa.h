@@ -4,9 +4,9 @@
  * k-sparse code, the Top-k of its d-dimensional projection.
  *
  * Paper: "Scaling Attention via Feature Sparsity" (arXiv 2603.22300).
- *   - Top-k coding: Sec. 3.1, Eq. (1) and the case definition under it.
- *   - Overlap scores s_ij = scale * sum_{u in S_i cap S_j} q_iu k_ju: Sec. 3.1.
- *   - Masked softmax and value aggregation: Sec. 2 (attention equations);
+ *   - Top-k coding: Sec. 3.1, Eqs. (3)-(4).
+ *   - Overlap scores s_ij = scale * sum_{u in S_i cap S_j} q_iu k_ju: Sec. 3.1, Eq. (5).
+ *   - Masked softmax and value aggregation: Sec. 2, Eqs. (1)-(2);
  *     the tiled kernel's result equals softmax(Q~ K~^T / sqrt(d)) V: Sec. 3.2.
  *   - Decode against a cache of sparse key codes and dense V: App. B
  *     ("KV-cache latency") and App. J (code storage).
@@ -59,7 +59,7 @@ int sfa_abi_version(void);
 const char* sfa_strerror(int status);
 
 /*
- * Row-wise Top-k coding (Sec. 3.1, Eq. (1)).
+ * Row-wise Top-k coding (Sec. 3.1, Eqs. (3)-(4)).
  *
  * x    [rows, d] float32.  For each row, keeps the k coordinates of largest
  *      |x_u|; ties go to the lower index (the paper leaves ties open).

@@ -7,15 +7,15 @@ its Python binding) never does, and shares no code with it.
 Everything here is the plain definition of what the method computes, written
 out in float64 with numpy:
 
-* Top-k coding of a row (Sec. 3.1, Eq. (1) and the case definition under it):
+* Top-k coding of a row (Sec. 3.1, Eqs. (3)-(4)):
   keep the k entries of largest magnitude, zero the rest.  The paper leaves
   ties open; this oracle orders by larger |x| first, then lower index, and
   lists the kept pairs by ascending index.
-* Sparse scores (Sec. 3.1, overlap-score equation): s_ij = scale * sum over
+* Sparse scores (Sec. 3.1, Eq. (5)): s_ij = scale * sum over
   coordinates shared by the supports of q_i and k_j of q_iu * k_ju.  On the
   densified codes this is exactly the dense product Q~ K~^T (Sec. 3.1:
   "S = Q~ K~^T"), which is what is computed here.
-* Softmax and value aggregation (Sec. 2, attention equations; Sec. 3.2: the
+* Softmax and value aggregation (Sec. 2, Eqs. (1)-(2); Sec. 3.2: the
   tiled result equals softmax(Q~ K~^T / sqrt(d)) V).  Allowed keys under the
   causal mask are j <= i; an allowed key whose support does not overlap the
   query's still enters the softmax with score 0.
@@ -49,7 +49,7 @@ def widen(a) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
-# Top-k coding, Sec. 3.1 Eq. (1)
+# Top-k coding, Sec. 3.1 Eqs. (3)-(4)
 # --------------------------------------------------------------------------
 
 

@@ -1,4 +1,4 @@
-// Row-wise Top-k coding (Sec. 3.1, Eq. (1)) on gfx950.
+// Row-wise Top-k coding (Sec. 3.1, Eqs. (3)-(4)) on gfx950.
 //
 // One wavefront codes one row held in registers (lane l holds coordinates
 // l, l+64, ...).  Selection is an exact radix select on integer magnitude

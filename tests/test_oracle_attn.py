@@ -1,4 +1,4 @@
-"""Pins of the oracle's attention on codes (Sec. 2 attention equations;
+"""Pins of the oracle's attention on codes (Sec. 2, Eqs. (1)-(2);
 Sec. 3.1 overlap scores; Sec. 3.2 exactness of the tiled result; App. B
 decode).
 

@@ -1,4 +1,4 @@
-"""Pins of the oracle's Top-k coding (Sec. 3.1, Eq. (1)) and bf16 rounding.
+"""Pins of the oracle's Top-k coding (Sec. 3.1, Eqs. (3)-(4)) and bf16 rounding.
 
 Each test checks the oracle against something other than itself: a
 hand-worked fixture, a brute-force enumeration of subsets, a library routine
