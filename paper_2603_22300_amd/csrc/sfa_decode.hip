@@ -42,10 +42,15 @@ __device__ __forceinline__ int seq_len_of(const int32_t* seq_len, int b, int Lma
   return L < 0 ? 0 : (L > Lmax ? Lmax : L);
 }
 
-template <int D, int G, bool VBF16>
+// KC8 > 0: cache codes are int16 indices and bf16 values with k = 8 * KC8,
+// loaded as 16-byte vectors and prefetched one 64-key sub-block ahead, with
+// the sub-block's V (bf16) in flight during its score phase.  KC8 = 0: any
+// format and k, element loads issued as a batch per sub-block.
+template <int D, int G, bool VBF16, int KC8>
 __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   constexpr int DL = D / 8;     // lanes covering one key's D values (8 each)
   constexpr int KPL = 64 / DL;  // keys per wave-wide V load
+  constexpr int NR = 64 / KPL;  // V loads per lane per 64-key sub-block
   __shared__ float qd[D][G];
   __shared__ float pbuf[kDecWaves][64][G];
   __shared__ float red_m[kDecWaves][G], red_l[kDecWaves][G];
@@ -88,31 +93,17 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   const int w0 = c0 + wave * per_wave;
   const int w1 = min(c1, w0 + per_wave);
 
-  for (int sb = w0; sb < w1; sb += 64) {
-    // ---- scores, lane = key ----
-    const int j = sb + lane;
-    const bool ok = j < w1;
-    float s[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) s[h] = 0.f;
-    if (ok) {
-      const int64_t cbase = (kv_row0 + j) * k;
-      for (int t = 0; t < k; ++t) {
-        const int u = load_idx(p.kc_idx, cbase + t, p.kidx16, dmask);
-        const float kv = load_val(p.kc_val, cbase + t, p.kvalbf16);
-#pragma unroll
-        for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
-      }
-    }
-    // ---- online softmax, per head ----
+  // ---- per-sub-block pieces ----
+  // online softmax of the lane's key scores s[h] (valid: ok); writes P to pbuf
+  auto softmax_block = [&](float (&s)[G], bool ok) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       const float tt = ok ? s[h] * p.scale_log2 : -INFINITY;
       const float mb = wave_max(tt);
       const float m_new = fmaxf(m_run[h], mb);
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = exp2f(m_run[h] - m_use);
-      const float pj = exp2f(tt - m_use);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[h] - m_use);
+      const float pj = __builtin_amdgcn_exp2f(tt - m_use);
       l_lane[h] = l_lane[h] * alpha + pj;
       m_run[h] = m_new;
 #pragma unroll
@@ -121,11 +112,84 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    // ---- P.V: lanes over (8 dims, key subset) ----
-    for (int r = 0; r < 64; r += KPL) {
-      const int jj = r + ksub;
-      const int jg = sb + jj;
-      if (jg < w1) {
+  };
+  auto pv_accum = [&](int jj, const float (&vv)[8]) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float ph = pbuf[wave][jj][h];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] = fmaf(ph, vv[e], o[h][e]);
+    }
+  };
+
+  if constexpr (KC8 > 0) {
+    // ---------------- vectorized, prefetched path ----------------
+    uint4 cidx[KC8], cval[KC8];
+    auto load_codes = [&](int sb) {
+      const int j = min(sb + lane, w1 - 1);
+      const uint4* pi = (const uint4*)((const int16_t*)p.kc_idx + (kv_row0 + j) * (8 * KC8));
+      const uint4* pv = (const uint4*)((const uint16_t*)p.kc_val + (kv_row0 + j) * (8 * KC8));
+#pragma unroll
+      for (int c = 0; c < KC8; ++c) { cidx[c] = pi[c]; cval[c] = pv[c]; }
+    };
+    if (w0 < w1) load_codes(w0);
+    for (int sb = w0; sb < w1; sb += 64) {
+      // V of this sub-block: in flight during the score phase
+      uint4 vraw[NR];
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        const int jg = min(sb + r * KPL + ksub, w1 - 1);
+        vraw[r] = *(const uint4*)((const uint16_t*)p.v + (kv_row0 + jg) * D + dsub * 8);
+      }
+      // scores, lane = key
+      float s[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) s[h] = 0.f;
+#pragma unroll
+      for (int c = 0; c < KC8; ++c) {
+        const uint32_t iw[4] = {cidx[c].x, cidx[c].y, cidx[c].z, cidx[c].w};
+        const uint32_t vw[4] = {cval[c].x, cval[c].y, cval[c].z, cval[c].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int u = (int)((iw[e >> 1] >> (16 * (e & 1))) & 0xffffu) & dmask;
+          const float kv = __uint_as_float((e & 1) ? (vw[e >> 1] & 0xffff0000u) : (vw[e >> 1] << 16));
+#pragma unroll
+          for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
+        }
+      }
+      softmax_block(s, sb + lane < w1);
+      if (sb + 64 < w1) load_codes(sb + 64);  // next sub-block's codes during P.V
+      // P.V: lanes over (8 dims, key subset)
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        float vv[8];
+        vv[0] = __uint_as_float(vraw[r].x << 16); vv[1] = __uint_as_float(vraw[r].x & 0xffff0000u);
+        vv[2] = __uint_as_float(vraw[r].y << 16); vv[3] = __uint_as_float(vraw[r].y & 0xffff0000u);
+        vv[4] = __uint_as_float(vraw[r].z << 16); vv[5] = __uint_as_float(vraw[r].z & 0xffff0000u);
+        vv[6] = __uint_as_float(vraw[r].w << 16); vv[7] = __uint_as_float(vraw[r].w & 0xffff0000u);
+        pv_accum(r * KPL + ksub, vv);
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+    // ---------------- generic path: any code format and k ----------------
+    for (int sb = w0; sb < w1; sb += 64) {
+      const int j = min(sb + lane, w1 - 1);
+      const bool ok = sb + lane < w1;
+      float s[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) s[h] = 0.f;
+      const int64_t cbase = (kv_row0 + j) * k;
+      for (int t = 0; t < k; ++t) {
+        const int u = load_idx(p.kc_idx, cbase + t, p.kidx16, dmask);
+        const float kv = load_val(p.kc_val, cbase + t, p.kvalbf16);
+#pragma unroll
+        for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
+      }
+      softmax_block(s, ok);
+      for (int r = 0; r < 64; r += KPL) {
+        const int jj = r + ksub;
+        const int jg = min(sb + jj, w1 - 1);
         float vv[8];
         if constexpr (VBF16) {
           const uint4 raw = *(const uint4*)((const uint16_t*)p.v + (kv_row0 + jg) * D + dsub * 8);
@@ -139,15 +203,10 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
           vv[0] = a.x; vv[1] = a.y; vv[2] = a.z; vv[3] = a.w;
           vv[4] = c.x; vv[5] = c.y; vv[6] = c.z; vv[7] = c.w;
         }
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float ph = pbuf[wave][jj][h];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) o[h][e] = fmaf(ph, vv[e], o[h][e]);
-        }
+        pv_accum(jj, vv);
       }
+      __builtin_amdgcn_wave_barrier();
     }
-    __builtin_amdgcn_wave_barrier();
   }
 
   // ---- reduce within the wave: sums over lanes, outputs over key subsets ----
@@ -222,19 +281,30 @@ size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d) {
   return (size_t)B * Hq * nch * (size_t)(d + 2) * sizeof(float);
 }
 
-template <int D, int G, bool VBF16>
+template <int D, int G, bool VBF16, int KC8>
 static void launch_dec_t(const DecParams& p, int B, hipStream_t stream) {
   dim3 grid(p.nch, B * p.Hkv), block(kDecThreads);
-  hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16>), grid, block, 0, stream, p);
+  hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8>), grid, block, 0, stream, p);
+}
+
+template <int D, int G, bool VBF16>
+static void launch_dec_kc(const DecParams& p, int B, hipStream_t stream) {
+  const bool vec = VBF16 && p.kidx16 && p.kvalbf16;
+  if constexpr (VBF16) {
+    if (vec && p.k == 8) return launch_dec_t<D, G, VBF16, 1>(p, B, stream);
+    if (vec && p.k == 16) return launch_dec_t<D, G, VBF16, 2>(p, B, stream);
+    if (vec && p.k == 32) return launch_dec_t<D, G, VBF16, 4>(p, B, stream);
+  }
+  launch_dec_t<D, G, VBF16, 0>(p, B, stream);
 }
 
 template <int D, bool VBF16>
 static void launch_dec_g(const DecParams& p, int G, int B, hipStream_t stream) {
   switch (G) {
-    case 1: launch_dec_t<D, 1, VBF16>(p, B, stream); break;
-    case 2: launch_dec_t<D, 2, VBF16>(p, B, stream); break;
-    case 4: launch_dec_t<D, 4, VBF16>(p, B, stream); break;
-    default: launch_dec_t<D, 8, VBF16>(p, B, stream); break;
+    case 1: launch_dec_kc<D, 1, VBF16>(p, B, stream); break;
+    case 2: launch_dec_kc<D, 2, VBF16>(p, B, stream); break;
+    case 4: launch_dec_kc<D, 4, VBF16>(p, B, stream); break;
+    default: launch_dec_kc<D, 8, VBF16>(p, B, stream); break;
   }
 }
 

@@ -51,6 +51,9 @@ def _case(B, Hq, Hkv, Lmax, d, k, v_bf16, seq, seed, cache_bf16=True):
         (2, 8, 1, 4097, 128, 16, True, [4097, 2049]),  # chunk boundaries, 8:1 groups
         (1, 2, 1, 64, 64, 64, False, None),           # k = d
         (2, 2, 2, 100, 128, 1, True, [100, 63]),      # k = 1
+        (2, 4, 1, 3000, 128, 8, True, [3000, 1]),     # vectorized codes, k = 8
+        (1, 8, 4, 2500, 64, 32, True, [2500]),        # vectorized codes, k = 32, d = 64
+        (3, 2, 2, 777, 128, 16, True, [5, 777, 64]),  # vectorized codes, short sequences
     ])
 def test_shapes(B, Hq, Hkv, Lmax, d, k, v_bf16, seq):
     _case(B, Hq, Hkv, Lmax, d, k, v_bf16, seq, seed=Lmax + k)
