@@ -18,15 +18,17 @@
 // Workgroup = NW wavefronts = 32*NW query rows: the G query heads of one KV
 // head times BR = 32*NW/G positions, so all G heads share each key tile.
 // Per tile of 64 keys:
-//   [A] scatter the tile's key codes (bf16 pieces) into a zeroed dense LDS
-//       tile Kd[piece][key][coordinate]; stage V, transposed, into LDS;
+//   [A] each wave zeroes its 64/NW rows of a dense LDS key tile
+//       Kd[key][piece][coordinate] and scatters those keys' codes (bf16
+//       pieces) into them; V is staged, transposed, beside it;
 //   [B] per wavefront, two 32-key sub-tiles: S^T = K~ Q~^T on
 //       v_mfma_f32_32x32x16_bf16 (the query pieces live in registers for the
 //       whole kernel), leaving each lane with one query row and 16 keys;
 //       scale, causal mask and the online-softmax update (base 2) run on those
 //       registers; the bf16 probabilities are already in the B-operand layout
-//       of O^T += V^T P^T, the second MFMA;
-//   [C] clear the scattered entries.
+//       of O^T += V^T P^T, the second MFMA.
+// The next tile is loaded into registers during the current one and written
+// to the other LDS stage, with one barrier per tile.
 // Keys whose support does not overlap a query keep score 0 and still enter
 // the softmax: the result is exactly softmax(Q~ K~^T * scale) V.
 #include "sfa_device.h"
