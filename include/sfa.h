@@ -97,10 +97,16 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * matrix cores, each value split into bfloat16 pieces whose products are
  * exact in float32 (bf16 V: three piece products, relative error ~2^-16 of
  * sum |q_u k_u|; float32 V: six, ~2^-24); softmax and accumulation in
- * float32.  With bf16 V the probabilities enter the P.V product as bfloat16
- * (MFMA, float32 accumulate); with float32 V that product is float32.
+ * float32.  With bf16 V, V is converted to float16 (exact for normal values
+ * up to 65504) and the probabilities (at most 2^8) enter P.V as float16,
+ * relative rounding 2^-11 per weight (MFMA, float32 accumulate).  Workgroups
+ * whose keys reach a V value of magnitude >= 65536 (or inf / NaN) are
+ * recomputed by a second kernel launched on the same stream, with bf16 V and
+ * the probabilities split into two bfloat16 terms (~2^-17).  With float32 V
+ * the P.V product is float32.
  * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0 with Hq / Hkv a power of two
- *         <= 128; d in {64, 128}; 1 <= k <= d; B * Hkv <= 65535.
+ *         <= 128; d in {64, 128}; 1 <= k <= d; B * Hkv <= 65535;
+ *         n * d <= 2^29 and n * k <= 2^29 (SFA_ENOTSUP otherwise).
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_EHIP.
  */
 sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,

@@ -58,6 +58,8 @@ sfa_status check_fwd(const void* q_idx, const void* q_val, const void* k_idx, co
   if (!isfinite(scale)) return SFA_EINVAL;
   if (d != 64 && d != 128) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  // per-head code and value offsets are 32-bit byte offsets in the kernels
+  if ((long long)n * d > (1LL << 29) || (long long)n * k > (1LL << 29)) return SFA_ENOTSUP;
   return SFA_OK;
 }
 

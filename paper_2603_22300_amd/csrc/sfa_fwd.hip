@@ -14,6 +14,11 @@
 // score keeps the terms q0k0 + q0k1 + q1k0 (relative error ~2^-16 of
 // sum|q_u k_u|); with float32 V it keeps every term of order <= 2
 // (q0k0 + q0k1 + q1k0 + q0k2 + q1k1 + q2k0, ~2^-24).
+// P.V with bf16 V: V is staged into LDS as float16 (exact for normal values up
+// to 65504) and P enters as float16 (P <= 2^8, relative rounding 2^-11), one
+// MFMA per block.  A tile holding a V value outside the float16 range is
+// flagged while staged and runs with V read as bf16 from global memory and
+// P = Ph + Pl in bf16.  With float32 V, P.V runs on the float32 MFMA.
 //
 // Workgroup = NW wavefronts = 32*NW query rows: the G query heads of one KV
 // head times BR = 32*NW/G positions, so all G heads share each key tile.
@@ -81,7 +86,8 @@ __host__ __device__ constexpr int n_stages() {
 
 template <int D, bool VBF16, int NW>
 __host__ __device__ constexpr int lds_bytes() {
-  constexpr int st = n_stages<D, VBF16>() * stage_bytes<D, VBF16>();
+  // stages, then one V range flag per stage and wavefront
+  constexpr int st = n_stages<D, VBF16>() * (stage_bytes<D, VBF16>() + NW * 4);
   constexpr int qs = NW * 32 * Geo<D, 2>::QP * 2;
   return st > qs ? st : qs;
 }
@@ -98,13 +104,34 @@ __device__ __forceinline__ uint16_t bf16_piece(float x, int pc) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// two float32 (given as bits) -> packed float16, round to nearest even
+__device__ __forceinline__ uint32_t f16_pair(uint32_t a, uint32_t b) {
+  const f16x2 h = {(_Float16)__uint_as_float(a), (_Float16)__uint_as_float(b)};
+  return __builtin_bit_cast(uint32_t, h);
+}
+
 // The running row maximum is raised only when a tile's maximum exceeds it by
 // more than this (log2 units), so probabilities stay below 2^kLazyMax and the
 // accumulators are rescaled rarely; O and LSE use the same stale maximum.
 constexpr float kLazyMax = 8.f;
 
-template <int D, bool VBF16, int NW, int KM>
-__global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
+// Bits written into the first output element of a workgroup's rows when the
+// float16 path meets a V tile outside the float16 range: a NaN payload that
+// the arithmetic does not produce (it yields the default NaN).  Should a
+// computed NaN carry it anyway, the rerun only recomputes the same result.
+constexpr uint16_t kHandBack16 = 0x7fa5u;
+constexpr uint32_t kHandBack32 = 0x7fa5a5a5u;
+
+// One workgroup: query block qb of (batch, KV head) bh.
+// SAFE (bf16 V only): V is staged as bf16 and P.V uses P = Ph + Pl on the
+// bf16 MFMA, every tile on the generic path; it reruns the workgroups that the
+// float16 path handed back.
+template <int D, bool VBF16, int NW, int KM, bool SAFE>
+__device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, const int bh) {
+  static_assert(VBF16 || !SAFE, "the rerun is for bf16 V");
   constexpr int NT = NW * 64;
   constexpr int R = NW * 32;
   constexpr int NP = VBF16 ? 2 : 3;
@@ -120,6 +147,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   constexpr int VW = VBF16 ? 8 : 4;            // registers per V item
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* Qs = (uint16_t*)smem;              // setup only: [R][QP]
+  int* vflag_lds = (int*)(smem + NS * SB);     // [NS][NW] V range flags
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -130,8 +158,6 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   const int n = p.n;
   const int dmask = D - 1;
 
-  const int qb = p.nqb - 1 - (int)blockIdx.x;  // longest causal blocks first
-  const int bh = blockIdx.y;
   const int b = bh / p.Hkv;
   const int hkv = bh - b * p.Hkv;
   const int i0 = qb * p.BR;
@@ -143,6 +169,9 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   const bool row_ok = my_i < n;
 
   // ---------------- query operand: NP bf16 pieces of the densified rows ----
+  // A negative scale is carried by the query values (s * c = (-s) * |c|), so
+  // the softmax below only ever needs row maxima of the raw scores.
+  const float qsign = p.scale_log2 < 0.f ? -1.f : 1.f;
   bf16x8 qB[NP][NKB];
 #pragma unroll
   for (int pc = 0; pc < NP; ++pc) {
@@ -156,7 +185,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
         const int hq = hkv * p.G + r / p.BR;
         const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
         const int f = load_idx(p.q_idx, gi, p.idx16, dmask);
-        Qs[r * QP + f] = bf16_piece(load_val(p.q_val, gi, p.valbf16), pc);
+        Qs[r * QP + f] = bf16_piece(qsign * load_val(p.q_val, gi, p.valbf16), pc);
       }
     }
     __syncthreads();
@@ -178,7 +207,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   const int n_keys = p.causal ? blk_last + 1 : n;
   const int ntiles = (n_keys + kBC - 1) / kBC;
   const int64_t kv_base = ((int64_t)b * p.Hkv + hkv) * n;
-  const float c = p.scale_log2;
+  const float c = fabsf(p.scale_log2);
 
   // ---- global -> registers for one tile ----
   // Per-lane offsets are loop-invariant; loads are unconditional (indices
@@ -197,54 +226,60 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   int kf[KEL];
   float kx[KEL];
   uint32_t vr[VI][VW];
+  // Uniform per-(batch, KV head) bases; per-lane offsets fit 32 bits (n*d and
+  // n*k are at most 2^29, checked on the host), so the loads take the form
+  // scalar base + 32-bit vector offset.
+  const unsigned isz = p.idx16 ? 2u : 4u, ksz = p.valbf16 ? 2u : 4u;
+  const unsigned char* kidx_b = (const unsigned char*)p.k_idx + kv_base * k * isz;
+  const unsigned char* kval_b = (const unsigned char*)p.k_val + kv_base * k * ksz;
+  const unsigned char* v_b = (const unsigned char*)p.v + kv_base * D * (VBF16 ? 2 : 4);
   auto load_tile = [&](int jt) {
     const int j0 = jt * kBC;
     const bool full = j0 + kBC <= n;
-    int64_t gi[KEL];
+    uint32_t ge[KEL];  // code element within this KV head
 #pragma unroll
     for (int r = 0; r < KEL; ++r) {
       if (full) {
-        gi[r] = (kv_base + j0) * k + k_off[r];
+        ge[r] = (uint32_t)(j0 * k + k_off[r]);
       } else {
         const int row = k_row[r] < 0 ? 0 : k_row[r];
         const int j = min(j0 + row, n - 1);
-        gi[r] = (kv_base + j) * k + (k_off[r] - row * k);
+        ge[r] = (uint32_t)(j * k + (k_off[r] - row * k));
       }
     }
     if (p.idx16) {
 #pragma unroll
-      for (int r = 0; r < KEL; ++r) kf[r] = ((const int16_t*)p.k_idx)[gi[r]];
+      for (int r = 0; r < KEL; ++r) kf[r] = *(const int16_t*)(kidx_b + ge[r] * 2u);
     } else {
 #pragma unroll
-      for (int r = 0; r < KEL; ++r) kf[r] = ((const int32_t*)p.k_idx)[gi[r]];
+      for (int r = 0; r < KEL; ++r) kf[r] = *(const int32_t*)(kidx_b + ge[r] * 4u);
     }
     if (p.valbf16) {
 #pragma unroll
-      for (int r = 0; r < KEL; ++r) kx[r] = __uint_as_float((uint32_t)((const uint16_t*)p.k_val)[gi[r]] << 16);
+      for (int r = 0; r < KEL; ++r) kx[r] = __uint_as_float((uint32_t)*(const uint16_t*)(kval_b + ge[r] * 2u) << 16);
     } else {
 #pragma unroll
-      for (int r = 0; r < KEL; ++r) kx[r] = ((const float*)p.k_val)[gi[r]];
+      for (int r = 0; r < KEL; ++r) kx[r] = *(const float*)(kval_b + ge[r] * 4u);
     }
 #pragma unroll
     for (int r = 0; r < VI; ++r) {
       const int it = min(tid + r * NT, VITEMS - 1);
       if constexpr (VBF16) {
         const int dp = it % NDP, kg = it / NDP;
-        const uint16_t* src = (const uint16_t*)p.v + (kv_base + j0 + kg * 8) * D + 2 * dp;
         if (full) {
+          const uint32_t off = (uint32_t)((j0 + kg * 8) * D + 2 * dp) * 2u;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) vr[r][e] = *(const uint32_t*)(src + e * D);
+          for (int e = 0; e < 8; ++e) vr[r][e] = *(const uint32_t*)(v_b + off + e * D * 2);
         } else {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int j = min(j0 + kg * 8 + e, n - 1);
-            vr[r][e] = *(const uint32_t*)((const uint16_t*)p.v + (kv_base + j) * D + 2 * dp);
+            vr[r][e] = *(const uint32_t*)(v_b + (uint32_t)(j * D + 2 * dp) * 2u);
           }
         }
       } else {
-        const float* Vg = (const float*)p.v;
         const int j = min(j0 + it / (D / 4), n - 1), c4 = it % (D / 4);
-        const uint4 val = *(const uint4*)(Vg + (kv_base + j) * D + 4 * c4);
+        const uint4 val = *(const uint4*)(v_b + (uint32_t)(j * D + 4 * c4) * 4u);
         vr[r][0] = val.x; vr[r][1] = val.y; vr[r][2] = val.z; vr[r][3] = val.w;
       }
     }
@@ -278,11 +313,42 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   auto write_tile_v = [&](int stage, int jt) {
     const int j0 = jt * kBC;
     unsigned char* vt = smem + stage * SB + kBC * KR * 2;
+    uint32_t v_over = 0u;
 #pragma unroll
     for (int r = 0; r < VI; ++r) {
       const int it = tid + r * NT;
       if (VITEMS % NT != 0 && it >= VITEMS) break;
-      if constexpr (VBF16) {
+      if constexpr (VBF16 && !SAFE) {
+        // bf16 -> fp16 is exact for 2^-14 <= |v| <= 65504 (below that to
+        // within 2^-25); a finite |v| >= 65536 (bf16 magnitude bits >=
+        // 0x4780) would overflow, and so would inf / NaN: such a tile is
+        // flagged.
+        uint16_t* Vt = (uint16_t*)vt;
+        const int dp = it % NDP, kg = it / NDP;
+        uint32_t w[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w[e] = vr[r][e];
+        if (j0 + kBC > n) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) w[e] = (j0 + kg * 8 + e < n) ? w[e] : 0u;
+        }
+        u16x2 mx = {0, 0};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2, w[e] & 0x7fff7fffu));
+        v_over |= (uint32_t)(mx.x >= 0x4780u) | (uint32_t)(mx.y >= 0x4780u);
+        // dimension 2dp (low halves) and 2dp+1 (high halves), keys in pairs
+        uint32_t lo[4], hi[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          lo[e] = f16_pair(w[2 * e] << 16, w[2 * e + 1] << 16);
+          hi[e] = f16_pair(w[2 * e] & 0xffff0000u, w[2 * e + 1] & 0xffff0000u);
+        }
+        uint16_t* r0 = Vt + (2 * dp) * VP + kg * 8;
+        uint16_t* r1 = r0 + VP;
+        *(uint2*)r0 = make_uint2(lo[0], lo[1]); *(uint2*)(r0 + 4) = make_uint2(lo[2], lo[3]);
+        *(uint2*)r1 = make_uint2(hi[0], hi[1]); *(uint2*)(r1 + 4) = make_uint2(hi[2], hi[3]);
+      } else if constexpr (VBF16) {
         uint16_t* Vt = (uint16_t*)vt;
         const int dp = it % NDP, kg = it / NDP;
         uint32_t w[8];
@@ -304,6 +370,10 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
         *(uint4*)(Vs + j * D + 4 * c4) = ok ? make_uint4(vr[r][0], vr[r][1], vr[r][2], vr[r][3])
                                             : make_uint4(0u, 0u, 0u, 0u);
       }
+    }
+    if constexpr (VBF16 && !SAFE) {
+      const bool any = __builtin_amdgcn_ballot_w64(v_over != 0u) != 0;
+      if (lane == 0) vflag_lds[stage * NW + wave] = any ? 1 : 0;
     }
   };
 
@@ -343,10 +413,10 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   // largest base-2 exponent s * c of a sub-tile (no mask), combined over the
   // two lanes of the row
   auto sub_max = [&](const floatx16& o) {
-    float hi = o[0], lo = o[0];
+    float hi = o[0];
 #pragma unroll
-    for (int r = 1; r < 16; ++r) { hi = fmaxf(hi, o[r]); lo = fminf(lo, o[r]); }
-    const float mt = (c >= 0.f ? hi : lo) * c;
+    for (int r = 1; r < 16; ++r) hi = fmaxf(hi, o[r]);
+    const float mt = hi * c;  // c >= 0
     return fmaxf(mt, swap_halves(mt));
   };
   // probabilities 2^(s c - m) in place; returns their (lane-partial) sum
@@ -356,36 +426,61 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     for (int r = 0; r < 16; ++r) { o[r] = fast_exp2(fmaf(o[r], c, -m_run)); rs += o[r]; }
     return rs;
   };
-  // P = Ph + Pl in bfloat16 (Pl = bf16(P - Ph)), per 16-key PV block kk
-  auto split_p = [&](const floatx16& pr, bf16x8 (&ph)[2], bf16x8 (&pl)[2]) {
+  // P in float16 for the fp16 V tile (values <= 2^kLazyMax, 11-bit mantissa)
+  auto to_f16 = [&](const floatx16& pr, f16x8 (&pf)[2]) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        ph[kk][e] = (__bf16)pr[8 * kk + e];
-        pl[kk][e] = (__bf16)(pr[8 * kk + e] - (float)ph[kk][e]);
-      }
+      for (int e = 0; e < 8; ++e) pf[kk][e] = (_Float16)pr[8 * kk + e];
   };
-  // O^T += V^T P^T for the 32 keys of sub-tile s (bf16 V)
-  auto pv_sub = [&](int s, const bf16x8 (&ph)[2], const bf16x8 (&pl)[2], const uint16_t* Vt) {
+  // V^T operand of the 16-key PV block kk of sub-tile s from the fp16 LDS tile
+  // (keys kbase+0..3 and kbase+8..11 of this lane half)
+  auto va_load = [&](f16x8 (&va)[NDB], int s, int kk, const uint16_t* Vt) {
+    const int kbase = 32 * s + 16 * kk + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
+      const uint2 v0 = *(const uint2*)row;
+      const uint2 v1 = *(const uint2*)(row + 8);
+      const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
+      va[db] = __builtin_bit_cast(f16x8, vw);
+    }
+  };
+  auto pv_terms = [&](const f16x8 (&va)[NDB], const f16x8& pf) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va[db], pf, acc[db], 0, 0, 0);
+  };
+  auto pv16_sub = [&](int s, const f16x8 (&pf)[2], const uint16_t* Vt) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      const int kbase = 32 * s + 16 * kk + 4 * hh;  // keys kbase+0..3, kbase+8..11
-      bf16x8 va[NDB];
+      f16x8 va[NDB];
+      va_load(va, s, kk, Vt);
+      pv_terms(va, pf[kk]);
+    }
+  };
+  // bf16 V tile (rerun): O^T += V^T P^T with P = Ph + Pl in bfloat16,
+  // Pl = bf16(P - Ph), relative error ~2^-17 per weight.
+  auto pv_sub_bf16 = [&](int s, const floatx16& pr, const uint16_t* Vt) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int kbase = 32 * s + 16 * kk + 4 * hh;
+      bf16x8 ph, pl;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        ph[e] = (__bf16)pr[8 * kk + e];
+        pl[e] = (__bf16)(pr[8 * kk + e] - (float)ph[e]);
+      }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
         const uint2 v0 = *(const uint2*)row;
         const uint2 v1 = *(const uint2*)(row + 8);
         const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
-        va[db] = __builtin_bit_cast(bf16x8, vw);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, vw);
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pl, acc[db], 0, 0, 0);
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ph, acc[db], 0, 0, 0);
       }
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pl[kk], acc[db], 0, 0, 0);
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], ph[kk], acc[db], 0, 0, 0);
     }
   };
   auto rescale = [&](float alpha) {
@@ -396,26 +491,21 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
       for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
   };
 
-  // ---- generic tile: any mask, first tile, large jumps of the maximum -----
-  auto generic_tile = [&](int j0, bool act1, const uint16_t* Kd, const unsigned char* vt) {
-    floatx16 sc[2];
-    score_sub(sc[0], 0, Kd);
-    if (act1) score_sub(sc[1], 1, Kd);
-    else {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sc[1][r] = 0.f;
-    }
+  // ---- generic sub-tile: any mask, first tile, large jumps of the maximum --
+  // One 32-key sub-tile s with its own online-softmax update (keeps a single
+  // score tile live).
+  auto generic_sub = [&](int j0, int s, const uint16_t* Kd, const unsigned char* vt) {
+    floatx16 sc;
+    score_sub(sc, s, Kd);
     // base-2 exponents t = s * c; masked keys get t = -inf
     float mt = -INFINITY;
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
-        const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
-        sc[s][r] = ok ? sc[s][r] * c : -INFINITY;
-        mt = fmaxf(mt, sc[s][r]);
-      }
+    for (int r = 0; r < 16; ++r) {
+      const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
+      const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
+      sc[r] = ok ? sc[r] * c : -INFINITY;
+      mt = fmaxf(mt, sc[r]);
+    }
     mt = fmaxf(mt, swap_halves(mt));
     const bool upd = mt > m_run + kLazyMax;
     const float m_new = upd ? mt : m_run;
@@ -424,32 +514,26 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     m_run = m_new;
     float rs = 0.f;
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { sc[s][r] = fast_exp2(sc[s][r] - m_use); rs += sc[s][r]; }
+    for (int r = 0; r < 16; ++r) { sc[r] = fast_exp2(sc[r] - m_use); rs += sc[r]; }
     l_run += rs;
     if constexpr (VBF16) {
       const uint16_t* Vt = (const uint16_t*)vt;
-      bf16x8 ph[2], pl[2];
-      split_p(sc[0], ph, pl);
-      pv_sub(0, ph, pl, Vt);
-      if (act1) {
-        split_p(sc[1], ph, pl);
-        pv_sub(1, ph, pl, Vt);
+      if constexpr (!SAFE) {
+        f16x8 pf[2];
+        to_f16(sc, pf);
+        pv16_sub(s, pf, Vt);
+      } else {
+        pv_sub_bf16(s, sc, Vt);
       }
     } else {
       const float* Vs = (const float*)vt;
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        if (s == 1 && !act1) break;
+      for (int r = 0; r < 16; ++r) {
+        const int jj = 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int jj = 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
-#pragma unroll
-          for (int db = 0; db < NDB; ++db)
-            acc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(Vs[jj * D + db * 32 + l32], sc[s][r],
-                                                           acc[db], 0, 0, 0);
-        }
+        for (int db = 0; db < NDB; ++db)
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(Vs[jj * D + db * 32 + l32], sc[r],
+                                                         acc[db], 0, 0, 0);
       }
     }
   };
@@ -472,32 +556,11 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[1][kb], o, 0, 0, 0);
     o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
   };
-  // probability of value r (exp of the lane's score), its split into ph/pl
-  auto exp_split = [&](floatx16& o, int r, float& rs, bf16x8 (&ph)[2], bf16x8 (&pl)[2]) {
+  // probability of value r (exp of the lane's score), as float16 into pf
+  auto exp_h = [&](const floatx16& o, int r, float& rs, f16x8 (&pf)[2]) {
     const float pr = fast_exp2(fmaf(o[r], c, -m_run));
     rs += pr;
-    const __bf16 h = (__bf16)pr;
-    ph[r >> 3][r & 7] = h;
-    pl[r >> 3][r & 7] = (__bf16)(pr - (float)h);
-  };
-  auto va_load = [&](bf16x8 (&va)[NDB], int s, int kk, const uint16_t* Vt) {
-    const int kbase = 32 * s + 16 * kk + 4 * hh;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
-      const uint2 v0 = *(const uint2*)row;
-      const uint2 v1 = *(const uint2*)(row + 8);
-      const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
-      va[db] = __builtin_bit_cast(bf16x8, vw);
-    }
-  };
-  auto pv_terms = [&](const bf16x8 (&va)[NDB], const bf16x8& ph, const bf16x8& pl) {
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pl, acc[db], 0, 0, 0);
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], ph, acc[db], 0, 0, 0);
+    pf[r >> 3][r & 7] = (_Float16)pr;
   };
 
   auto fast_tile = [&](const uint16_t* Kd, const uint16_t* Vt, int jt_next, int stage_next) {
@@ -506,7 +569,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     score_sub(s0, 0, Kd);
     if (__builtin_amdgcn_ballot_w64(sub_max(s0) > m_run + kLazyMax)) return false;
     // ---- B: scores(1) || softmax(0) ----
-    bf16x8 ph0[2], pl0[2];
+    f16x8 p0[2];
     float rs = 0.f;
     {
 #pragma unroll
@@ -519,7 +582,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
         score_terms(s1, ka[kb & 1], kb);
         // 16 probabilities of sub-tile 0 spread over the NKB slices
 #pragma unroll
-        for (int q = 0; q < 16 / NKB; ++q) exp_split(s0, kb * (16 / NKB) + q, rs, ph0, pl0);
+        for (int q = 0; q < 16 / NKB; ++q) exp_h(s0, kb * (16 / NKB) + q, rs, p0);
       }
     }
     l_run += rs;
@@ -527,34 +590,29 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     const bool up1 = mt1 > m_run + kLazyMax;
     if (__builtin_amdgcn_ballot_w64(up1)) {
       const float m_new = up1 ? mt1 : m_run;
-      const float alpha = fast_exp2(m_run - m_new);
-      rescale(alpha);
-      floatx16 p0;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) p0[8 * kk + e] = ((float)ph0[kk][e] + (float)pl0[kk][e]) * alpha;
-      split_p(p0, ph0, pl0);
+      rescale(fast_exp2(m_run - m_new));  // also rescales sub-tile 0's share of l
       m_run = m_new;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) p0[r >> 3][r & 7] = (_Float16)fast_exp2(fmaf(s0[r], c, -m_run));
     }
     // ---- C: P.V(0) || softmax(1) ----
-    bf16x8 ph1[2], pl1[2];
+    f16x8 p1[2];
     rs = 0.f;
-    bf16x8 va[2][NDB];
+    f16x8 va[2][NDB];
     va_load(va[0], 0, 0, Vt);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       va_load(va[(kk + 1) & 1], kk == 0 ? 0 : 1, kk == 0 ? 1 : 0, Vt);  // next PV block
-      pv_terms(va[kk & 1], ph0[kk], pl0[kk]);
+      pv_terms(va[kk & 1], p0[kk]);
 #pragma unroll
-      for (int q = 0; q < 8; ++q) exp_split(s1, 8 * kk + q, rs, ph1, pl1);
+      for (int q = 0; q < 8; ++q) exp_h(s1, 8 * kk + q, rs, p1);
     }
     l_run += rs;
     // ---- D: P.V(1) || next tile's LDS writes ----
     va_load(va[1], 1, 1, Vt);
-    pv_terms(va[0], ph1[0], pl1[0]);
+    pv_terms(va[0], p1[0]);
     write_tile_keys(stage_next, jt_next);
-    pv_terms(va[1], ph1[1], pl1[1]);
+    pv_terms(va[1], p1[1]);
     write_tile_v(stage_next, jt_next);
     return true;
   };
@@ -575,12 +633,29 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     const bool act1 = !p.causal || wave_i_max >= j0 + 32;
     const bool need_mask = j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min) ||
                            __builtin_amdgcn_ballot_w64(!row_ok || m_run == -INFINITY) != 0;
+    if constexpr (VBF16 && !SAFE) {
+      // Some V of this tile does not fit float16: every wave sees the same
+      // flags after the same barrier, so the whole workgroup hands its rows
+      // back to the bf16 rerun here.
+      bool vflag = false;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) vflag |= vflag_lds[stage * NW + w] != 0;
+      if (vflag) {
+        if (tid == 0) {
+          const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;  // row rho = 0
+          if (p.obf16) ((uint16_t*)p.o)[orow0 * D] = kHandBack16;
+          else ((uint32_t*)p.o)[orow0 * D] = kHandBack32;
+        }
+        return;
+      }
+    }
     bool done = false;
-    if constexpr (NS == 2 && VBF16) {
+    if constexpr (NS == 2 && VBF16 && !SAFE) {
       if (act1 && !need_mask) done = fast_tile(Kd, (const uint16_t*)vt, jt + 1, stage ^ 1);
     }
     if (!done) {
-      if (act0) generic_tile(j0, act1, Kd, vt);
+      if (act0) generic_sub(j0, 0, Kd, vt);
+      if (act1) generic_sub(j0, 1, Kd, vt);
       if constexpr (NS == 2) write_tile(stage ^ 1, jt + 1);
     }
     __syncthreads();
@@ -612,17 +687,63 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
 }
 
 template <int D, bool VBF16, int NW, int KM>
+__global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
+  // longest causal blocks first
+  fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - (int)blockIdx.x, (int)blockIdx.y);
+}
+
+// Whether workgroup t = bh * nqb + qb was handed back (its first output
+// element holds the hand-back bits).
+__device__ __forceinline__ bool handed_back(const FwdParams& p, int t, int D) {
+  const int qb = t % p.nqb, bh = t / p.nqb;
+  const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+  const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * p.n + (int64_t)qb * p.BR;
+  return p.obf16 ? ((const uint16_t*)p.o)[orow0 * D] == kHandBack16
+                 : ((const uint32_t*)p.o)[orow0 * D] == kHandBack32;
+}
+
+// bf16-V rerun, launched after sfa_fwd_kernel on the same stream: a
+// persistent grid checks every workgroup's hand-back mark (one load per
+// thread) and recomputes only the marked ones.
+template <int D, int NW, int KM>
+__global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int nbh) {
+  constexpr int NT = NW * 64;
+  const int total = p.nqb * nbh;
+  const int stride = (int)gridDim.x;
+  for (int base = (int)blockIdx.x; base < total; base += stride * NT) {
+    const int t = base + (int)threadIdx.x * stride;
+    if (!__syncthreads_or(t < total && handed_back(p, t, D))) continue;
+    for (int c = 0; c < NT; ++c) {
+      const int tc = base + c * stride;
+      if (tc >= total) break;
+      if (!__syncthreads_or(threadIdx.x == 0 && handed_back(p, tc, D))) continue;
+      fwd_block<D, true, NW, KM, true>(p, tc % p.nqb, tc / p.nqb);
+      __syncthreads();  // LDS is reused by the next workgroup
+    }
+  }
+}
+
+template <int D, bool VBF16, int NW, int KM>
 hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
   constexpr int bytes = lds_bytes<D, VBF16, NW>();
   static bool configured = false;  // per instantiation
   if (bytes > 65536 && !configured) {
     hipError_t e = hipFuncSetAttribute((const void*)sfa_fwd_kernel<D, VBF16, NW, KM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess && VBF16)
+      e = hipFuncSetAttribute((const void*)sfa_fwd_rerun_kernel<D, NW, KM>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
     configured = true;
   }
   dim3 grid(p.nqb, B * p.Hkv), block(NW * 64);
   hipLaunchKernelGGL((sfa_fwd_kernel<D, VBF16, NW, KM>), grid, block, bytes, stream, p);
+  if constexpr (VBF16) {
+    // one resident workgroup per compute unit (LDS-bound)
+    const int total = p.nqb * B * p.Hkv;
+    dim3 rgrid(total < 256 ? total : 256);
+    hipLaunchKernelGGL((sfa_fwd_rerun_kernel<D, NW, KM>), rgrid, block, bytes, stream, p, B * p.Hkv);
+  }
   return hipGetLastError();
 }
 

@@ -65,6 +65,7 @@ def test_fwd_validation(L, fn):
     assert _fwd(L, fn, d=96, k=8) == 2           # no kernel for this head dim
     assert _fwd(L, fn, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
     assert _fwd(L, fn, B=70000, Hkv=1, Hq=1) == 2  # grid limit
+    assert _fwd(L, fn, n=(1 << 22) + 1, d=128, k=16) == 2  # 32-bit per-head offsets
 
 
 def test_fwd_index_limits(L):

@@ -115,6 +115,52 @@ def test_zipf_small():
     _run_case(1, 2, 2, 260, 128, 8, True, True, seed=4, zipf_s=1.1)
 
 
+@pytest.mark.parametrize("where", ["some_tiles", "every_tile"])
+def test_v_beyond_float16_range(where):
+    """bf16 V values of magnitude >= 65536 do not fit the float16 P.V path;
+    the workgroups whose keys reach them are recomputed with bf16 V (P split
+    hi + lo).  Some workgroups keep the float16 path, the others are redone:
+    every output must match the oracle, to an error bound that scales with
+    max|V| (2^-17 per weight, plus the bf16-output half-ulp)."""
+    B, Hq, Hkv, n, d, k = 1, 8, 2, 700, 128, 16
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, 91, v_dtype=torch.bfloat16, device=DEV)
+    big = [65536.0, -1.0e6, 3.0e5, 2.0e30]
+    if where == "some_tiles":
+        # KV head 0: key 70 (second tile); KV head 1: key 650 (last tile)
+        v[0, 0, 70, 5] = big[0]
+        v[0, 0, 70, 77] = big[1]
+        v[0, 1, 650, 100] = big[2]
+    else:
+        for j in range(0, n, 64):
+            v[0, j // 64 % Hkv, j, (7 * j) % d] = big[(j // 64) % len(big)]
+    qi, qv = _gpu_codes(q, k)
+    ki, kv = _gpu_codes(kk, k)
+    scale = 1.0 / math.sqrt(d)
+    o32, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=scale, o_dtype=torch.float32)
+    ob16, _ = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=scale, o_dtype=torch.bfloat16,
+                               want_lse=False)
+    torch.cuda.synchronize()
+    oqi, oqv = oracle.topk_encode(q.cpu().numpy(), k)
+    oki, okv = oracle.topk_encode(kk.cpu().numpy(), k)
+    vn = np_vals(v)
+    O, L = oracle.attn_fwd(oqi, oqv, oki, okv, vn, d, scale, True)
+    vmax = float(np.abs(oracle.widen(vn)).max())
+    tol = TOL_O_BF16V + 2.0 ** -16 * vmax
+    got = o32.double().cpu().numpy()
+    assert np.isfinite(got).all()
+    err = np.abs(got - O).max()
+    print(f"[parity] O with max|V| = {vmax:.3g}: max|O-O_oracle| = {err:.3e} (bound {tol:.3e})", flush=True)
+    assert err <= tol
+    check_o(ob16, O, tol, "O (bf16 output, large V)")
+    check_lse(lse, L, "LSE (large V)")
+    # rows whose keys hold no large value are held to the ordinary tolerance
+    if where == "some_tiles":
+        small = np.abs(O).max(axis=-1) < 100.0
+        e_small = np.abs(got - O)[small].max()
+        print(f"[parity] rows away from the large values: max|O-O_oracle| = {e_small:.3e}", flush=True)
+        assert e_small <= TOL_O_BF16V
+
+
 def test_gpt2s_workload_full():
     # every output of the GPT-2-small-shaped workload, against the oracle
     w = si.workload("gpt2s")
