@@ -93,6 +93,12 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * o             [B, Hq, n, d]   output (o_t: SFA_F32 or SFA_BF16, the latter
  *                               rounded to nearest-even from float32)
  * lse           [B, Hq, n] float32 natural-log LSE, or NULL to skip it.
+ * ws, ws_bytes  caller-owned device workspace of at least
+ *               sfa_attn_fwd_workspace(B, Hkv, n, d, v_t) bytes (0 for float32
+ *               V, where ws may be NULL).  With bf16 V it receives, on the
+ *               stream, V converted once to float16 and laid out as the
+ *               kernel's key tiles, and a range flag per tile.  Calls that
+ *               overlap in time need separate workspaces.
  * Arithmetic: the scores are the product of the densified codes on the
  * matrix cores, each value split into bfloat16 pieces whose products are
  * exact in float32 (bf16 V: three piece products, relative error ~2^-16 of
@@ -107,7 +113,8 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0 with Hq / Hkv a power of two
  *         <= 128; d in {64, 128}; 1 <= k <= d; B * Hkv <= 65535;
  *         n * d <= 2^29 and n * k <= 2^29 (SFA_ENOTSUP otherwise).
- * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_EHIP.
+ * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (workspace missing or too
+ *         small), SFA_EHIP.
  */
 sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,
                         const void* k_idx, const void* k_val,
@@ -115,16 +122,25 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,
                         int B, int Hq, int Hkv, int n, int d, int k,
                         int causal, float scale,
                         int idx_t, int qk_val_t, int v_t, int o_t,
-                        void* o, float* lse, void* stream);
+                        void* o, float* lse, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/*
+ * Bytes of device workspace sfa_attn_fwd needs for these sizes: 0 for
+ * float32 V (v_t == SFA_F32), and for an unsupported d or invalid sizes.
+ */
+size_t sfa_attn_fwd_workspace(int B, int Hkv, int n, int d, int v_t);
 
 /*
  * The same forward with the overlap scores accumulated through a per-key-tile
  * inverted index in LDS (Sec. 3.2's feature-intersection formulation): the
  * tile's key codes are counting-sorted by coordinate and each query nonzero
  * adds q_u * k_u into the score tile for exactly the keys holding its
- * coordinate.  Same arguments, definitions and results as sfa_attn_fwd (up
- * to float32 summation order); slower on this hardware, kept as the direct
- * realisation of the overlap formulation.
+ * coordinate.  Same arguments (without the workspace) and definitions as
+ * sfa_attn_fwd; the scores agree up to float32 summation order, and with bf16
+ * V the probabilities enter P.V as a single bfloat16 (relative rounding 2^-9
+ * per weight).  Slower on this hardware; kept as the direct realisation of
+ * the overlap formulation.
  * Limits: as sfa_attn_fwd, plus k <= 64, Hq / Hkv <= 128, and the per-tile
  * tables must fit LDS (SFA_ENOTSUP otherwise).
  */

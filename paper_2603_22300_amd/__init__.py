@@ -16,7 +16,8 @@ import torch
 
 __all__ = [
     "SfaError", "lib", "library_path", "sfa_abi_version", "sfa_strerror",
-    "sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_fwd_index", "sfa_attn_decode_workspace", "sfa_attn_decode",
+    "sfa_topk_encode", "sfa_attn_fwd_workspace", "sfa_attn_fwd", "sfa_attn_fwd_index",
+    "sfa_attn_decode_workspace", "sfa_attn_decode",
     "SFA_OK", "SFA_EINVAL", "SFA_ENOTSUP", "SFA_EHIP", "SFA_ENOSPC",
     "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16",
 ]
@@ -53,9 +54,12 @@ def lib() -> ctypes.CDLL:
         L.sfa_topk_encode.argtypes = [vp, i64, i32, i32, vp, i32, vp, i32, vp]
         L.sfa_attn_fwd.restype = i32
         L.sfa_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
-                                   i32, i32, i32, i32, vp, vp, vp]
+                                   i32, i32, i32, i32, vp, vp, vp, sz, vp]
+        L.sfa_attn_fwd_workspace.restype = sz
+        L.sfa_attn_fwd_workspace.argtypes = [i32, i32, i32, i32, i32]
         L.sfa_attn_fwd_index.restype = i32
-        L.sfa_attn_fwd_index.argtypes = L.sfa_attn_fwd.argtypes
+        L.sfa_attn_fwd_index.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
+                                         f32, i32, i32, i32, i32, vp, vp, vp]
         L.sfa_attn_decode_workspace.restype = sz
         L.sfa_attn_decode_workspace.argtypes = [i32, i32, i32, i32]
         L.sfa_attn_decode.restype = i32
@@ -117,13 +121,19 @@ def sfa_topk_encode(x: torch.Tensor, k: int, idx_dtype=torch.int32, val_dtype=to
     return idx, val
 
 
+def sfa_attn_fwd_workspace(B: int, Hkv: int, n: int, d: int, v_dtype=torch.bfloat16) -> int:
+    """Bytes of device workspace sfa_attn_fwd needs (0 for float32 V)."""
+    return int(lib().sfa_attn_fwd_workspace(B, Hkv, n, d, _VAL[v_dtype]))
+
+
 def sfa_attn_fwd(q_idx, q_val, k_idx, k_val, v, causal: bool = True, scale: float | None = None,
                  o_dtype=None, o: torch.Tensor | None = None, lse: torch.Tensor | None = None,
-                 want_lse: bool = True):
+                 want_lse: bool = True, ws: torch.Tensor | None = None):
     """SFA forward on codes.  q_* [B, Hq, n, k], k_* [B, Hkv, n, k], v [B, Hkv, n, d].
-    Returns (o [B, Hq, n, d], lse [B, Hq, n] float32 or None)."""
+    ws: uint8 device workspace of sfa_attn_fwd_workspace(...) bytes, allocated
+    here when None.  Returns (o [B, Hq, n, d], lse [B, Hq, n] float32 or None)."""
     return _fwd("sfa_attn_fwd", q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse,
-                want_lse)
+                want_lse, ws)
 
 
 def sfa_attn_fwd_index(q_idx, q_val, k_idx, k_val, v, causal: bool = True,
@@ -131,10 +141,10 @@ def sfa_attn_fwd_index(q_idx, q_val, k_idx, k_val, v, causal: bool = True,
                        lse: torch.Tensor | None = None, want_lse: bool = True):
     """The inverted-index variant of sfa_attn_fwd (same arguments and results)."""
     return _fwd("sfa_attn_fwd_index", q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o,
-                lse, want_lse)
+                lse, want_lse, None)
 
 
-def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, want_lse):
+def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, want_lse, ws):
     B, Hq, n, k = q_idx.shape
     Hkv, d = k_idx.shape[1], v.shape[-1]
     if tuple(q_val.shape) != (B, Hq, n, k) or tuple(k_idx.shape) != (B, Hkv, n, k) \
@@ -158,10 +168,19 @@ def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, wa
     if lse is not None:
         _check(lse, "lse", {torch.float32: SFA_F32})
         lp = lse.data_ptr()
-    _call(getattr(lib(), name)(q_idx.data_ptr(), q_val.data_ptr(), k_idx.data_ptr(),
-                               k_val.data_ptr(), v.data_ptr(), B, Hq, Hkv, n, d, k,
-                               int(bool(causal)), float(scale), it, qt, vt, ot, o.data_ptr(), lp,
-                               _stream(v)), name)
+    args = [q_idx.data_ptr(), q_val.data_ptr(), k_idx.data_ptr(), k_val.data_ptr(), v.data_ptr(),
+            B, Hq, Hkv, n, d, k, int(bool(causal)), float(scale), it, qt, vt, ot, o.data_ptr(), lp]
+    if name == "sfa_attn_fwd":
+        need = int(lib().sfa_attn_fwd_workspace(B, Hkv, n, d, vt))
+        if ws is None and need > 0:
+            ws = torch.empty(need, dtype=torch.uint8, device=v.device)
+        if ws is not None:
+            if ws.device.type != "cuda" or not ws.is_contiguous():
+                raise ValueError("ws must be a contiguous GPU tensor")
+            args += [ws.data_ptr(), ws.numel() * ws.element_size()]
+        else:
+            args += [0, 0]
+    _call(getattr(lib(), name)(*args, _stream(v)), name)
     return o, lse
 
 

@@ -8,7 +8,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 1;
+constexpr int kAbiVersion = 2;
 constexpr int kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
 
 bool is_idx(int t) { return t == SFA_I32 || t == SFA_I16; }
@@ -65,18 +65,25 @@ sfa_status check_fwd(const void* q_idx, const void* q_val, const void* k_idx, co
 
 }  // namespace
 
+size_t sfa_attn_fwd_workspace(int B, int Hkv, int n, int d, int v_t) {
+  if (B < 1 || Hkv < 1 || n < 1 || (d != 64 && d != 128) || !is_val(v_t)) return 0;
+  return sfa::fwd_workspace_bytes(B, Hkv, n, d, v_t == SFA_BF16);
+}
+
 sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                         const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
                         int k, int causal, float scale, int idx_t, int qk_val_t, int v_t,
-                        int o_t, void* o, float* lse, void* stream) {
+                        int o_t, void* o, float* lse, void* ws, size_t ws_bytes, void* stream) {
   sfa_status st = check_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k, scale, idx_t,
                             qk_val_t, v_t, o_t, o);
   if (st != SFA_OK) return st;
   if (!pow2_le(Hq / Hkv, sfa::fwd_max_group())) return SFA_ENOTSUP;
+  const size_t need = sfa::fwd_workspace_bytes(B, Hkv, n, d, v_t == SFA_BF16);
+  if (need > 0 && (ws == nullptr || ws_bytes < need)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
                                        causal != 0, scale, idx_t == SFA_I16,
                                        qk_val_t == SFA_BF16, v_t == SFA_BF16, o_t == SFA_BF16,
-                                       o, lse, (hipStream_t)stream));
+                                       o, lse, ws, (hipStream_t)stream));
 }
 
 sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,

@@ -57,6 +57,11 @@ struct FwdParams {
   int idx16, valbf16, obf16;
   int G, BR, nqb;
   float inv_k;
+  // bf16 V, prepared once per call (sfa_fwd_vprep_kernel): float16 V^T tiles
+  // in the staged LDS layout and a range flag per tile
+  const unsigned char* ws_v;
+  const int* ws_flag;
+  int vtiles;  // tiles per (batch, KV head): ceil(n / 64)
 };
 
 template <int D, int NP>
@@ -71,10 +76,17 @@ struct Geo {
 // the 16-byte A-operand reads of consecutive keys hit disjoint banks; a V row
 // of 68 bf16 is 2 dwords past, for the 8-byte operand reads.
 
+// The 16-bit V tile in LDS: [dimension][key], pitch VP, padded to whole
+// 1 KB blocks so that it is copied by whole-wave 16-byte direct-to-LDS loads.
+template <int D>
+__host__ __device__ constexpr int vtile_bytes() {
+  return (D * (kBC + 4) * 2 + 1023) / 1024 * 1024;
+}
+
 template <int D, bool VBF16>
 __host__ __device__ constexpr int stage_bytes() {
   constexpr int NP = VBF16 ? 2 : 3;
-  return kBC * Geo<D, NP>::KR * 2 + (VBF16 ? D * Geo<D, NP>::VP * 2 : kBC * D * 4);
+  return kBC * Geo<D, NP>::KR * 2 + (VBF16 ? vtile_bytes<D>() : kBC * D * 4);
 }
 
 // Two LDS stages (next tile written while the current one is read) when they
@@ -86,8 +98,7 @@ __host__ __device__ constexpr int n_stages() {
 
 template <int D, bool VBF16, int NW>
 __host__ __device__ constexpr int lds_bytes() {
-  // stages, then one V range flag per stage and wavefront
-  constexpr int st = n_stages<D, VBF16>() * (stage_bytes<D, VBF16>() + NW * 4);
+  constexpr int st = n_stages<D, VBF16>() * stage_bytes<D, VBF16>();
   constexpr int qs = NW * 32 * Geo<D, 2>::QP * 2;
   return st > qs ? st : qs;
 }
@@ -147,11 +158,10 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   constexpr int VW = VBF16 ? 8 : 4;            // registers per V item
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* Qs = (uint16_t*)smem;              // setup only: [R][QP]
-  int* vflag_lds = (int*)(smem + NS * SB);     // [NS][NW] V range flags
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hh = lane >> 5;
   const int l32 = lane & 31;
   const int k = p.k;
@@ -167,6 +177,25 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   const int my_i = i0 + rho % p.BR;
   const int my_hq = hkv * p.G + rho / p.BR;
   const bool row_ok = my_i < n;
+
+  const int blk_last = min(n, i0 + p.BR) - 1;
+  const int n_keys = p.causal ? blk_last + 1 : n;
+  const int ntiles = (n_keys + kBC - 1) / kBC;
+
+  if constexpr (VBF16 && !SAFE) {
+    // A V tile of this workgroup's key range outside the float16 range: hand
+    // the rows back to the bf16 rerun before doing any work.
+    bool over = false;
+    for (int t = tid; t < ntiles; t += NT) over |= p.ws_flag[(int64_t)bh * p.vtiles + t] != 0;
+    if (__syncthreads_or(over)) {
+      if (tid == 0) {
+        const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;  // row rho = 0
+        if (p.obf16) ((uint16_t*)p.o)[orow0 * D] = kHandBack16;
+        else ((uint32_t*)p.o)[orow0 * D] = kHandBack32;
+      }
+      return;
+    }
+  }
 
   // ---------------- query operand: NP bf16 pieces of the densified rows ----
   // A negative scale is carried by the query values (s * c = (-s) * |c|), so
@@ -203,9 +232,6 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
 
   const int wave_i_max = i0 + (wave * 32 + 31) % p.BR;  // largest position in this wave
   const int wave_i_min = p.BR >= 32 ? i0 + (wave * 32) % p.BR : i0;
-  const int blk_last = min(n, i0 + p.BR) - 1;
-  const int n_keys = p.causal ? blk_last + 1 : n;
-  const int ntiles = (n_keys + kBC - 1) / kBC;
   const int64_t kv_base = ((int64_t)b * p.Hkv + hkv) * n;
   const float c = fabsf(p.scale_log2);
 
@@ -263,6 +289,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     }
 #pragma unroll
     for (int r = 0; r < VI; ++r) {
+      if constexpr (VBF16 && !SAFE) break;  // V arrives by direct-to-LDS copies
       const int it = min(tid + r * NT, VITEMS - 1);
       if constexpr (VBF16) {
         const int dp = it % NDP, kg = it / NDP;
@@ -313,41 +340,12 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   auto write_tile_v = [&](int stage, int jt) {
     const int j0 = jt * kBC;
     unsigned char* vt = smem + stage * SB + kBC * KR * 2;
-    uint32_t v_over = 0u;
 #pragma unroll
     for (int r = 0; r < VI; ++r) {
       const int it = tid + r * NT;
       if (VITEMS % NT != 0 && it >= VITEMS) break;
       if constexpr (VBF16 && !SAFE) {
-        // bf16 -> fp16 is exact for 2^-14 <= |v| <= 65504 (below that to
-        // within 2^-25); a finite |v| >= 65536 (bf16 magnitude bits >=
-        // 0x4780) would overflow, and so would inf / NaN: such a tile is
-        // flagged.
-        uint16_t* Vt = (uint16_t*)vt;
-        const int dp = it % NDP, kg = it / NDP;
-        uint32_t w[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) w[e] = vr[r][e];
-        if (j0 + kBC > n) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) w[e] = (j0 + kg * 8 + e < n) ? w[e] : 0u;
-        }
-        u16x2 mx = {0, 0};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2, w[e] & 0x7fff7fffu));
-        v_over |= (uint32_t)(mx.x >= 0x4780u) | (uint32_t)(mx.y >= 0x4780u);
-        // dimension 2dp (low halves) and 2dp+1 (high halves), keys in pairs
-        uint32_t lo[4], hi[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          lo[e] = f16_pair(w[2 * e] << 16, w[2 * e + 1] << 16);
-          hi[e] = f16_pair(w[2 * e] & 0xffff0000u, w[2 * e + 1] & 0xffff0000u);
-        }
-        uint16_t* r0 = Vt + (2 * dp) * VP + kg * 8;
-        uint16_t* r1 = r0 + VP;
-        *(uint2*)r0 = make_uint2(lo[0], lo[1]); *(uint2*)(r0 + 4) = make_uint2(lo[2], lo[3]);
-        *(uint2*)r1 = make_uint2(hi[0], hi[1]); *(uint2*)(r1 + 4) = make_uint2(hi[2], hi[3]);
+        break;  // V arrives by direct-to-LDS copies
       } else if constexpr (VBF16) {
         uint16_t* Vt = (uint16_t*)vt;
         const int dp = it % NDP, kg = it / NDP;
@@ -371,19 +369,33 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
                                             : make_uint4(0u, 0u, 0u, 0u);
       }
     }
-    if constexpr (VBF16 && !SAFE) {
-      const bool any = __builtin_amdgcn_ballot_w64(v_over != 0u) != 0;
-      if (lane == 0) vflag_lds[stage * NW + wave] = any ? 1 : 0;
-    }
   };
 
   auto write_tile = [&](int stage, int jt) {
     write_tile_keys(stage, jt);
     write_tile_v(stage, jt);
   };
+  // bf16 V: the prepared float16 tile is copied global -> LDS by the memory
+  // unit (16 bytes per lane, 1 KB per wave instruction); completion is
+  // awaited with vmcnt before the barrier that publishes the stage.
+  auto dma_v = [&](int stage, int jt) {
+    constexpr int VTB = vtile_bytes<D>();
+    const unsigned char* src = p.ws_v + ((int64_t)bh * p.vtiles + jt) * VTB + lane * 16;
+    unsigned char* dst = smem + stage * SB + kBC * KR * 2;
+#pragma unroll
+    for (int i = wave; i < VTB / 1024; i += NW)
+      __builtin_amdgcn_global_load_lds(src + i * 1024,
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                       16, 0, 0);
+  };
+  auto wait_dma = [&]() {
+    if constexpr (VBF16 && !SAFE) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+  };
   if (ntiles > 0 && NS == 2) {
     load_tile(0);
+    if constexpr (VBF16 && !SAFE) dma_v(0, 0);
     write_tile(0, 0);
+    wait_dma();
   }
   __syncthreads();
 
@@ -626,6 +638,9 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       __syncthreads();
     } else {
       load_tile(jt + 1);  // past the end it reads clamped, valid addresses; unused
+      if constexpr (VBF16 && !SAFE) {
+        if (jt + 1 < ntiles) dma_v(stage ^ 1, jt + 1);
+      }
     }
     const uint16_t* Kd = (const uint16_t*)(smem + stage * SB);
     const unsigned char* vt = smem + stage * SB + kBC * KR * 2;
@@ -633,22 +648,6 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     const bool act1 = !p.causal || wave_i_max >= j0 + 32;
     const bool need_mask = j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min) ||
                            __builtin_amdgcn_ballot_w64(!row_ok || m_run == -INFINITY) != 0;
-    if constexpr (VBF16 && !SAFE) {
-      // Some V of this tile does not fit float16: every wave sees the same
-      // flags after the same barrier, so the whole workgroup hands its rows
-      // back to the bf16 rerun here.
-      bool vflag = false;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) vflag |= vflag_lds[stage * NW + w] != 0;
-      if (vflag) {
-        if (tid == 0) {
-          const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;  // row rho = 0
-          if (p.obf16) ((uint16_t*)p.o)[orow0 * D] = kHandBack16;
-          else ((uint32_t*)p.o)[orow0 * D] = kHandBack32;
-        }
-        return;
-      }
-    }
     bool done = false;
     if constexpr (NS == 2 && VBF16 && !SAFE) {
       if (act1 && !need_mask) done = fast_tile(Kd, (const uint16_t*)vt, jt + 1, stage ^ 1);
@@ -658,6 +657,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       if (act1) generic_sub(j0, 1, Kd, vt);
       if constexpr (NS == 2) write_tile(stage ^ 1, jt + 1);
     }
+    wait_dma();
     __syncthreads();
   }
   l_run += swap_halves(l_run);  // lane-partial row sums -> row sums
@@ -723,6 +723,43 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
   }
 }
 
+// bf16 V -> float16 V^T tiles in the staged LDS layout, once per call: tile t
+// of (batch, KV head) bh holds [dimension][key 64t .. 64t+63] with pitch
+// kBC + 4 (keys past n and the padding are zero), and flag t is set when a V
+// value of the tile lies outside the float16 range (|v| >= 65536, inf, NaN).
+// bf16 -> float16 is exact for 2^-14 <= |v| <= 65504; below that it rounds
+// to the float16 subnormal grid (absolute error <= 2^-25).
+template <int D>
+__global__ __launch_bounds__(256) void sfa_fwd_vprep_kernel(const uint16_t* __restrict__ v, int n,
+                                                            int vtiles,
+                                                            unsigned char* __restrict__ ws_v,
+                                                            int* __restrict__ ws_flag) {
+  constexpr int VP = kBC + 4, VTB = vtile_bytes<D>();
+  __shared__ __attribute__((aligned(16))) uint16_t T[VTB / 2];
+  const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int j0 = t * kBC;
+  for (int i = tid; i < VTB / 16; i += 256) ((uint4*)T)[i] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
+  bool over = false;
+  for (int c = tid; c < kBC * D / 8; c += 256) {  // 16-byte chunks: key j, dims d0..d0+7
+    const int j = c / (D / 8), d0 = (c % (D / 8)) * 8;
+    if (j0 + j >= n) continue;
+    const uint4 w4 = *(const uint4*)(src + (int64_t)j * D + d0);
+    const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      over |= (w[e] & 0x7fffu) >= 0x4780u || ((w[e] >> 16) & 0x7fffu) >= 0x4780u;
+      T[(d0 + 2 * e) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] & 0xffffu));
+      T[(d0 + 2 * e + 1) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] >> 16));
+    }
+  }
+  const int any = __syncthreads_or(over);
+  uint4* dst = (uint4*)(ws_v + ((int64_t)bh * vtiles + t) * VTB);
+  for (int i = tid; i < VTB / 16; i += 256) dst[i] = ((const uint4*)T)[i];
+  if (tid == 0) ws_flag[(int64_t)bh * vtiles + t] = any ? 1 : 0;
+}
+
 template <int D, bool VBF16, int NW, int KM>
 hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
   constexpr int bytes = lds_bytes<D, VBF16, NW>();
@@ -768,10 +805,17 @@ hipError_t launch_t(const FwdParams& p, int B, hipStream_t stream) {
 
 int fwd_max_group() { return 128; }
 
+size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16) {
+  if (!vbf16) return 0;
+  const size_t tiles = (size_t)B * Hkv * (size_t)((n + kBC - 1) / kBC);
+  const size_t vtb = d == 64 ? vtile_bytes<64>() : vtile_bytes<128>();
+  return tiles * vtb + (tiles * 4 + 255) / 256 * 256;
+}
+
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
                            int k, int causal, float scale, int idx16, int valbf16, int vbf16,
-                           int obf16, void* o, float* lse, hipStream_t stream) {
+                           int obf16, void* o, float* lse, void* ws, hipStream_t stream) {
   FwdParams p;
   p.q_idx = q_idx; p.q_val = q_val; p.k_idx = k_idx; p.k_val = k_val; p.v = v;
   p.o = o; p.lse = lse;
@@ -781,6 +825,22 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
   p.G = Hq / Hkv;
   p.BR = 0; p.nqb = 0;
   p.inv_k = 1.0f / (float)k;
+  p.vtiles = (n + kBC - 1) / kBC;
+  p.ws_v = (const unsigned char*)ws;
+  p.ws_flag = nullptr;
+  if (vbf16) {
+    const size_t tiles = (size_t)B * Hkv * p.vtiles;
+    p.ws_flag = (const int*)((unsigned char*)ws + tiles * (d == 64 ? vtile_bytes<64>() : vtile_bytes<128>()));
+    dim3 grid(p.vtiles, B * Hkv), block(256);
+    if (d == 64)
+      hipLaunchKernelGGL(sfa_fwd_vprep_kernel<64>, grid, block, 0, stream, (const uint16_t*)v, n,
+                         p.vtiles, (unsigned char*)ws, (int*)p.ws_flag);
+    else
+      hipLaunchKernelGGL(sfa_fwd_vprep_kernel<128>, grid, block, 0, stream, (const uint16_t*)v, n,
+                         p.vtiles, (unsigned char*)ws, (int*)p.ws_flag);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (d == 64) return vbf16 ? launch_t<64, true>(p, B, stream) : launch_t<64, false>(p, B, stream);
   return vbf16 ? launch_t<128, true>(p, B, stream) : launch_t<128, false>(p, B, stream);
 }

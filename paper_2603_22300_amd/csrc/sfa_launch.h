@@ -14,8 +14,9 @@ hipError_t launch_topk_encode(const float* x, int64_t rows, int d, int k, void* 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
                            int k, int causal, float scale, int idx16, int valbf16, int vbf16,
-                           int obf16, void* o, float* lse, hipStream_t stream);
+                           int obf16, void* o, float* lse, void* ws, hipStream_t stream);
 int fwd_max_group();
+size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16);
 
 hipError_t launch_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,
                                  const void* k_val, const void* v, int B, int Hq, int Hkv, int n,

@@ -28,14 +28,15 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = _declared()
-    assert {"sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_fwd_index", "sfa_attn_decode",
-            "sfa_attn_decode_workspace", "sfa_abi_version", "sfa_strerror"} <= set(names)
+    assert {"sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_fwd_workspace", "sfa_attn_fwd_index",
+            "sfa_attn_decode", "sfa_attn_decode_workspace", "sfa_abi_version",
+            "sfa_strerror"} <= set(names)
     for nm in names:
         assert hasattr(L, nm), nm
 
 
 def test_version_and_strerror(L):
-    assert L.sfa_abi_version() == 1
+    assert L.sfa_abi_version() == 2
     for s in range(5):
         assert L.sfa_strerror(s)
 
@@ -45,8 +46,10 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails val
 
 def _fwd(L, fn="sfa_attn_fwd", **kw):
     a = dict(q_idx=FAKE, q_val=FAKE, k_idx=FAKE, k_val=FAKE, v=FAKE, B=1, Hq=4, Hkv=2, n=16, d=64,
-             k=8, causal=1, scale=0.125, idx_t=0, qk_val_t=2, v_t=3, o_t=2, o=FAKE, lse=None,
-             stream=None)
+             k=8, causal=1, scale=0.125, idx_t=0, qk_val_t=2, v_t=3, o_t=2, o=FAKE, lse=None)
+    if fn == "sfa_attn_fwd":
+        a.update(ws=FAKE, ws_bytes=ctypes.c_size_t(1 << 40))
+    a["stream"] = None
     a.update(kw)
     return getattr(L, fn)(*a.values())
 
@@ -66,6 +69,18 @@ def test_fwd_validation(L, fn):
     assert _fwd(L, fn, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
     assert _fwd(L, fn, B=70000, Hkv=1, Hq=1) == 2  # grid limit
     assert _fwd(L, fn, n=(1 << 22) + 1, d=128, k=16) == 2  # 32-bit per-head offsets
+
+
+def test_fwd_workspace(L):
+    need = L.sfa_attn_fwd_workspace(1, 2, 16, 64, 3)
+    assert need > 0                                          # bf16 V: float16 V tiles + flags
+    assert L.sfa_attn_fwd_workspace(1, 2, 16, 64, 2) == 0    # float32 V needs none
+    assert L.sfa_attn_fwd_workspace(1, 2, 16, 96, 3) == 0    # unsupported head dim
+    assert L.sfa_attn_fwd_workspace(0, 2, 16, 64, 3) == 0
+    big = L.sfa_attn_fwd_workspace(2, 8, 32768, 128, 3)
+    assert big >= 2 * 8 * 512 * 128 * 68 * 2                # one float16 V^T tile per key tile
+    assert _fwd(L, ws_bytes=ctypes.c_size_t(need - 1)) == 4
+    assert _fwd(L, ws=None) == 4
 
 
 def test_fwd_index_limits(L):
