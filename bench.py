@@ -113,13 +113,14 @@ def bench_fwd(w, steps, warmup, want_cpu):
     kv = torch.empty((B, Hkv, n, kk), dtype=torch.float32, device=DEV)
     o = torch.empty((B, Hq, n, d), dtype=torch.bfloat16, device=DEV)
     lse = torch.empty((B, Hq, n), dtype=torch.float32, device=DEV)
+    ws = torch.empty(sfa.sfa_attn_fwd_workspace(B, Hkv, n, d, v.dtype), dtype=torch.uint8, device=DEV)
 
     def step(ev=None):
         sfa.sfa_topk_encode(q, kk, idx=qi, val=qv)
         sfa.sfa_topk_encode(k, kk, idx=ki, val=kv)
         if ev is not None:
             ev[0].record()
-        sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse)
+        sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse, ws=ws)
         if ev is not None:
             ev[1].record()
 
@@ -166,7 +167,8 @@ def bench_fwd(w, steps, warmup, want_cpu):
             "workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "n": n, "d": d, "k": kk,
             "causal": w.causal, "seed": w.seed,
             "step": "sfa_topk_encode(Q) + sfa_topk_encode(K) + sfa_attn_fwd",
-            "precision": "codes fp32; scores and softmax fp32; P.V bf16 MFMA, fp32 accumulate; O bf16",
+            "precision": ("codes fp32; scores fp32 (three bf16 piece products on MFMA); softmax fp32; "
+                          "P.V fp16 MFMA on V converted exactly to fp16, fp32 accumulate; O bf16"),
         },
         "roofline": {
             "kernel": "sfa_fwd_kernel",

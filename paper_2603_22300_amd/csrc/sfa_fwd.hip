@@ -57,9 +57,10 @@ struct FwdParams {
   int idx16, valbf16, obf16;
   int G, BR, nqb;
   float inv_k;
-  // bf16 V, prepared once per call (sfa_fwd_vprep_kernel): float16 V^T tiles
-  // in the staged LDS layout and a range flag per tile
-  const unsigned char* ws_v;
+  // bf16 V, prepared once per call (sfa_fwd_prep_kernel): every key tile as
+  // its LDS stage image (dense bf16 key pieces, float16 V^T) and a V range
+  // flag per tile
+  const unsigned char* ws_tiles;
   const int* ws_flag;
   int vtiles;  // tiles per (batch, KV head): ceil(n / 64)
 };
@@ -259,7 +260,10 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   const unsigned char* kidx_b = (const unsigned char*)p.k_idx + kv_base * k * isz;
   const unsigned char* kval_b = (const unsigned char*)p.k_val + kv_base * k * ksz;
   const unsigned char* v_b = (const unsigned char*)p.v + kv_base * D * (VBF16 ? 2 : 4);
+  // bf16 V: key tiles arrive as prepared stage images (dma_stage below)
+  constexpr bool kDMA = VBF16 && !SAFE;
   auto load_tile = [&](int jt) {
+    if constexpr (kDMA) return;
     const int j0 = jt * kBC;
     const bool full = j0 + kBC <= n;
     uint32_t ge[KEL];  // code element within this KV head
@@ -289,7 +293,6 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     }
 #pragma unroll
     for (int r = 0; r < VI; ++r) {
-      if constexpr (VBF16 && !SAFE) break;  // V arrives by direct-to-LDS copies
       const int it = min(tid + r * NT, VITEMS - 1);
       if constexpr (VBF16) {
         const int dp = it % NDP, kg = it / NDP;
@@ -314,6 +317,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // ---- registers -> LDS stage: zero own key rows, scatter own codes, V ----
   // Stage layout: Kd[key][piece][coordinate] (pitch KR), then the V tile.
   auto write_tile_keys = [&](int stage, int jt) {
+    if constexpr (kDMA) return;
     const int j0 = jt * kBC;
     uint16_t* Kd = (uint16_t*)(smem + stage * SB);
     // zero the coordinate part of this wave's KW key rows (straight-line)
@@ -344,8 +348,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     for (int r = 0; r < VI; ++r) {
       const int it = tid + r * NT;
       if (VITEMS % NT != 0 && it >= VITEMS) break;
-      if constexpr (VBF16 && !SAFE) {
-        break;  // V arrives by direct-to-LDS copies
+      if constexpr (kDMA) {
+        break;
       } else if constexpr (VBF16) {
         uint16_t* Vt = (uint16_t*)vt;
         const int dp = it % NDP, kg = it / NDP;
@@ -375,27 +379,30 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     write_tile_keys(stage, jt);
     write_tile_v(stage, jt);
   };
-  // bf16 V: the prepared float16 tile is copied global -> LDS by the memory
-  // unit (16 bytes per lane, 1 KB per wave instruction); completion is
-  // awaited with vmcnt before the barrier that publishes the stage.
-  auto dma_v = [&](int stage, int jt) {
-    constexpr int VTB = vtile_bytes<D>();
-    const unsigned char* src = p.ws_v + ((int64_t)bh * p.vtiles + jt) * VTB + lane * 16;
-    unsigned char* dst = smem + stage * SB + kBC * KR * 2;
+  // bf16 V: the prepared stage image of a key tile is copied global -> LDS
+  // by the memory unit (16 bytes per lane, 1 KB per wave instruction);
+  // completion is awaited with vmcnt before the barrier that publishes it.
+  auto dma_stage = [&](int stage, int jt) {
+    static_assert(SB % 1024 == 0, "stage images are whole 1 KB blocks");
+    const unsigned char* src = p.ws_tiles + ((int64_t)bh * p.vtiles + jt) * SB + lane * 16;
+    unsigned char* dst = smem + stage * SB;
 #pragma unroll
-    for (int i = wave; i < VTB / 1024; i += NW)
+    for (int i = wave; i < SB / 1024; i += NW)
       __builtin_amdgcn_global_load_lds(src + i * 1024,
                                        (__attribute__((address_space(3))) void*)(dst + i * 1024),
                                        16, 0, 0);
   };
   auto wait_dma = [&]() {
-    if constexpr (VBF16 && !SAFE) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+    if constexpr (kDMA) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   };
   if (ntiles > 0 && NS == 2) {
-    load_tile(0);
-    if constexpr (VBF16 && !SAFE) dma_v(0, 0);
-    write_tile(0, 0);
-    wait_dma();
+    if constexpr (kDMA) {
+      dma_stage(0, 0);
+      wait_dma();
+    } else {
+      load_tile(0);
+      write_tile(0, 0);
+    }
   }
   __syncthreads();
 
@@ -638,8 +645,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       __syncthreads();
     } else {
       load_tile(jt + 1);  // past the end it reads clamped, valid addresses; unused
-      if constexpr (VBF16 && !SAFE) {
-        if (jt + 1 < ntiles) dma_v(stage ^ 1, jt + 1);
+      if constexpr (kDMA) {
+        if (jt + 1 < ntiles) dma_stage(stage ^ 1, jt + 1);
       }
     }
     const uint16_t* Kd = (const uint16_t*)(smem + stage * SB);
@@ -723,40 +730,54 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
   }
 }
 
-// bf16 V -> float16 V^T tiles in the staged LDS layout, once per call: tile t
-// of (batch, KV head) bh holds [dimension][key 64t .. 64t+63] with pitch
-// kBC + 4 (keys past n and the padding are zero), and flag t is set when a V
-// value of the tile lies outside the float16 range (|v| >= 65536, inf, NaN).
-// bf16 -> float16 is exact for 2^-14 <= |v| <= 65504; below that it rounds
-// to the float16 subnormal grid (absolute error <= 2^-25).
+// Stage images for bf16 V, built once per call: image t of (batch, KV head) bh
+// is exactly what the forward kernel holds in LDS for keys 64t .. 64t+63:
+//   - the dense key tile [key][piece][coordinate] (pitch KR) with the codes'
+//     values as bf16 pieces x0 = bf16(x), x1 = bf16(x - x0) at their
+//     coordinates and zeros elsewhere;
+//   - V^T as float16, [dimension][key] (pitch kBC + 4).
+// Keys past n and all padding are zero.  flag t is set when a V value of the
+// tile lies outside the float16 range (|v| >= 65536, inf, NaN).  bf16 ->
+// float16 is exact for 2^-14 <= |v| <= 65504; below that it rounds to the
+// float16 subnormal grid (absolute error <= 2^-25).
 template <int D>
-__global__ __launch_bounds__(256) void sfa_fwd_vprep_kernel(const uint16_t* __restrict__ v, int n,
-                                                            int vtiles,
-                                                            unsigned char* __restrict__ ws_v,
-                                                            int* __restrict__ ws_flag) {
-  constexpr int VP = kBC + 4, VTB = vtile_bytes<D>();
-  __shared__ __attribute__((aligned(16))) uint16_t T[VTB / 2];
+__global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
+    const void* __restrict__ k_idx, const void* __restrict__ k_val, const uint16_t* __restrict__ v,
+    int n, int k, int idx16, int valbf16, int vtiles, unsigned char* __restrict__ ws_tiles,
+    int* __restrict__ ws_flag) {
+  constexpr int KR = Geo<D, 2>::KR, VP = kBC + 4, SB = stage_bytes<D, true>();
+  __shared__ __attribute__((aligned(16))) uint16_t T[SB / 2];
+  uint16_t* Vt = T + kBC * KR;
   const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const int j0 = t * kBC;
-  for (int i = tid; i < VTB / 16; i += 256) ((uint4*)T)[i] = make_uint4(0u, 0u, 0u, 0u);
+  for (int i = tid; i < SB / 16; i += 256) ((uint4*)T)[i] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
+  const int64_t c0 = ((int64_t)bh * n + j0) * k;  // first code element of the tile
+  for (int e = tid; e < kBC * k; e += 256) {
+    const int j = e / k;
+    if (j0 + j >= n) break;
+    const int f = load_idx(k_idx, c0 + e, idx16, D - 1);
+    const float x = load_val(k_val, c0 + e, valbf16);
+    T[j * KR + f] = bf16_piece(x, 0);
+    T[j * KR + D + f] = bf16_piece(x, 1);
+  }
   const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
   bool over = false;
   for (int c = tid; c < kBC * D / 8; c += 256) {  // 16-byte chunks: key j, dims d0..d0+7
     const int j = c / (D / 8), d0 = (c % (D / 8)) * 8;
-    if (j0 + j >= n) continue;
+    if (j0 + j >= n) break;
     const uint4 w4 = *(const uint4*)(src + (int64_t)j * D + d0);
     const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       over |= (w[e] & 0x7fffu) >= 0x4780u || ((w[e] >> 16) & 0x7fffu) >= 0x4780u;
-      T[(d0 + 2 * e) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] & 0xffffu));
-      T[(d0 + 2 * e + 1) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] >> 16));
+      Vt[(d0 + 2 * e) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] & 0xffffu));
+      Vt[(d0 + 2 * e + 1) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] >> 16));
     }
   }
   const int any = __syncthreads_or(over);
-  uint4* dst = (uint4*)(ws_v + ((int64_t)bh * vtiles + t) * VTB);
-  for (int i = tid; i < VTB / 16; i += 256) dst[i] = ((const uint4*)T)[i];
+  uint4* dst = (uint4*)(ws_tiles + ((int64_t)bh * vtiles + t) * SB);
+  for (int i = tid; i < SB / 16; i += 256) dst[i] = ((const uint4*)T)[i];
   if (tid == 0) ws_flag[(int64_t)bh * vtiles + t] = any ? 1 : 0;
 }
 
@@ -808,8 +829,8 @@ int fwd_max_group() { return 128; }
 size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16) {
   if (!vbf16) return 0;
   const size_t tiles = (size_t)B * Hkv * (size_t)((n + kBC - 1) / kBC);
-  const size_t vtb = d == 64 ? vtile_bytes<64>() : vtile_bytes<128>();
-  return tiles * vtb + (tiles * 4 + 255) / 256 * 256;
+  const size_t sb = d == 64 ? stage_bytes<64, true>() : stage_bytes<128, true>();
+  return tiles * sb + (tiles * 4 + 255) / 256 * 256;
 }
 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
@@ -826,18 +847,21 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
   p.BR = 0; p.nqb = 0;
   p.inv_k = 1.0f / (float)k;
   p.vtiles = (n + kBC - 1) / kBC;
-  p.ws_v = (const unsigned char*)ws;
+  p.ws_tiles = (const unsigned char*)ws;
   p.ws_flag = nullptr;
   if (vbf16) {
     const size_t tiles = (size_t)B * Hkv * p.vtiles;
-    p.ws_flag = (const int*)((unsigned char*)ws + tiles * (d == 64 ? vtile_bytes<64>() : vtile_bytes<128>()));
+    const size_t sb = d == 64 ? stage_bytes<64, true>() : stage_bytes<128, true>();
+    p.ws_flag = (const int*)((unsigned char*)ws + tiles * sb);
     dim3 grid(p.vtiles, B * Hkv), block(256);
     if (d == 64)
-      hipLaunchKernelGGL(sfa_fwd_vprep_kernel<64>, grid, block, 0, stream, (const uint16_t*)v, n,
-                         p.vtiles, (unsigned char*)ws, (int*)p.ws_flag);
+      hipLaunchKernelGGL(sfa_fwd_prep_kernel<64>, grid, block, 0, stream, k_idx, k_val,
+                         (const uint16_t*)v, n, k, idx16, valbf16, p.vtiles, (unsigned char*)ws,
+                         (int*)p.ws_flag);
     else
-      hipLaunchKernelGGL(sfa_fwd_vprep_kernel<128>, grid, block, 0, stream, (const uint16_t*)v, n,
-                         p.vtiles, (unsigned char*)ws, (int*)p.ws_flag);
+      hipLaunchKernelGGL(sfa_fwd_prep_kernel<128>, grid, block, 0, stream, k_idx, k_val,
+                         (const uint16_t*)v, n, k, idx16, valbf16, p.vtiles, (unsigned char*)ws,
+                         (int*)p.ws_flag);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
