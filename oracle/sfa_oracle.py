@@ -22,6 +22,11 @@ out in float64 with numpy:
 * LSE_i = m_i + ln(l_i), natural log (the paper does not define it; this is
   the standard log-sum-exp of the row's scaled scores).
 * Decode (App. B, KV-cache latency): one query row against all cached keys.
+* Backward with the straight-through estimator (Sec. 3.1, Eq. (6)): the
+  chain rule of softmax attention on the densified codes, with the gradient
+  of a query or key coordinate equal to that of its code value on the
+  support and zero elsewhere, i.e. the dense gradient read at the code's
+  coordinates.
 * bf16 storage of code values (round to nearest, ties to even) for the
   KV-cache codes.
 
@@ -216,6 +221,114 @@ def attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, d: int, scale: float, seq
 # --------------------------------------------------------------------------
 # accounting (Sec. 3.1 efficiency analysis; App. J memory formula)
 # --------------------------------------------------------------------------
+
+
+# --------------------------------------------------------------------------
+# backward (straight-through estimator, Sec. 3.1, Eq. (6))
+# --------------------------------------------------------------------------
+
+
+def softmax_attention_grad(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, do: np.ndarray,
+                           scale: float, causal: bool):
+    """Gradients of O = softmax(scale * qd kd^T, causal mask) v for one head,
+    dense float64, queries at positions 0..r-1 and keys at 0..n_k-1.
+
+    With P the row-normalised weights: dV = P^T dO, dP = dO V^T,
+    dS = P * (dP - rowsum(dP * P)), dQ = scale dS K, dK = scale dS^T Q.
+    Returns (dQ [r, d], dK [n_k, d], dV [n_k, dv])."""
+    S = scale * (qd @ kd.T)
+    if causal:
+        allowed = np.arange(kd.shape[0])[None, :] <= np.arange(qd.shape[0])[:, None]
+        S = np.where(allowed, S, -np.inf)
+    P = np.exp(S - S.max(axis=1, keepdims=True))
+    P /= P.sum(axis=1, keepdims=True)
+    dV = P.T @ do
+    dP = do @ v.T
+    dS = P * (dP - (dP * P).sum(axis=1, keepdims=True))
+    return scale * (dS @ kd), scale * (dS.T @ qd), dV
+
+
+def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bool):
+    """SFA backward on codes (Sec. 3.1, Eq. (6)).
+
+    Inputs as attn_fwd, plus do [B, Hq, n, dv] (float32, or uint16 bf16
+    bits).  The gradient of query i's coordinate u is the dense dQ~[i, u] on
+    its support and 0 elsewhere, so it is returned in code form:
+    dq_val [B, Hq, n, k] with dq_val[..., t] the gradient at q_idx[..., t];
+    likewise dk_val [B, Hkv, n, k].  dv [B, Hkv, n, dv].  A KV head's
+    gradients sum over the query heads that read it.  float64."""
+    B, Hq, n, k = np.shape(q_idx)
+    Hkv = np.shape(k_idx)[1]
+    G = Hq // Hkv
+    vv, dd = widen(v), widen(do)
+    dq = np.empty((B, Hq, n, k), dtype=np.float64)
+    dk = np.zeros((B, Hkv, n, k), dtype=np.float64)
+    dv = np.zeros((B, Hkv, n, vv.shape[-1]), dtype=np.float64)
+    for b in range(B):
+        for g in range(Hkv):
+            kd = densify(k_idx[b, g], k_val[b, g], d)
+            dkd = np.zeros_like(kd)
+            for h in range(g * G, (g + 1) * G):
+                qd = densify(q_idx[b, h], q_val[b, h], d)
+                gq, gk, gv = softmax_attention_grad(qd, kd, vv[b, g], dd[b, h], scale, causal)
+                dq[b, h] = np.take_along_axis(gq, np.asarray(q_idx[b, h], dtype=np.int64), 1)
+                dkd += gk
+                dv[b, g] += gv
+            dk[b, g] = np.take_along_axis(dkd, np.asarray(k_idx[b, g], dtype=np.int64), 1)
+    return dq, dk, dv
+
+
+def attn_bwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, do_bh, d: int, scale: float,
+                  causal: bool, rows):
+    """dq_val (Eq. (6)) of the selected query rows of one head, each row on
+    its own: p = softmax over the row's allowed keys, dp = V do_i,
+    ds = p * (dp - p.dp), dq~ = scale ds K~, read at the row's support.
+    Returns [len(rows), k], float64."""
+    kd = densify(k_idx_bg, k_val_bg, d)
+    vv, dd = widen(v_bg), widen(do_bh)
+    out = np.empty((len(rows), np.shape(q_idx_bh)[1]), dtype=np.float64)
+    for r, i in enumerate(rows):
+        qd = densify(q_idx_bh[i][None], q_val_bh[i][None], d)[0]
+        last = int(i) + 1 if causal else kd.shape[0]
+        s = scale * (kd[:last] @ qd)
+        p = np.exp(s - s.max())
+        p /= p.sum()
+        dp = vv[:last] @ dd[i]
+        ds = p * (dp - p @ dp)
+        out[r] = (scale * (ds @ kd[:last]))[np.asarray(q_idx_bh[i], dtype=np.int64)]
+    return out
+
+
+def attn_bwd_cols(q_idx_bg, q_val_bg, k_idx_bg, k_val_bg, v_bg, do_bg, d: int, scale: float,
+                  causal: bool, cols, row_chunk: int = 1024):
+    """dk_val and dv (Eq. (6)) of the selected keys of one KV head, summed
+    over its query heads: q_*_bg [G, n, k], do_bg [G, n, dv].  Each query
+    row's LSE_i and D_i = dO_i . O_i come from the plain forward
+    (softmax_attention); then for key j and every query i that sees it,
+    P_ij = exp(s_ij - LSE_i), dS_ij = P_ij (dO_i . v_j - D_i),
+    dv_j = sum_i P_ij dO_i and dk~_j = scale sum_i dS_ij q~_i.
+    Returns (dk [len(cols), k], dv [len(cols), dv]), float64."""
+    kd = densify(k_idx_bg, k_val_bg, d)
+    vv, dd = widen(v_bg), widen(do_bg)
+    n = kd.shape[0]
+    cols = np.asarray(cols, dtype=np.int64)
+    dk = np.zeros((len(cols), np.shape(k_idx_bg)[1]), dtype=np.float64)
+    dv = np.zeros((len(cols), vv.shape[1]), dtype=np.float64)
+    dkd = np.zeros((len(cols), d), dtype=np.float64)
+    for h in range(np.shape(q_idx_bg)[0]):
+        qd = densify(q_idx_bg[h], q_val_bg[h], d)
+        O, L = softmax_attention(qd, kd, vv, scale, causal, row_chunk=row_chunk)
+        D = (dd[h] * O).sum(axis=1)
+        S = scale * (qd @ kd[cols].T)                      # [n, len(cols)]
+        if causal:
+            S = np.where(np.arange(n)[:, None] >= cols[None, :], S, -np.inf)
+        P = np.exp(S - L[:, None])
+        dS = P * (dd[h] @ vv[cols].T - D[:, None])
+        dv += P.T @ dd[h]
+        dkd += scale * (dS.T @ qd)
+    for c, j in enumerate(cols):
+        dk[c] = dkd[c][np.asarray(k_idx_bg[j], dtype=np.int64)]
+    return dk, dv
 
 
 def overlap_count(q_idx_bh, k_idx_bg, causal: bool, d: int) -> int:
