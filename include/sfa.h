@@ -153,6 +153,50 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
                               void* o, float* lse, void* stream);
 
 /*
+ * SFA backward with the straight-through estimator (Sec. 3.1, Eq. (6)).
+ * With the forward's weights P_ij = exp(s_ij - LSE_i) over the allowed keys
+ * (s_ij as in sfa_attn_fwd) and D_i = dO_i . O_i:
+ *   dV_j  = sum_i P_ij dO_i
+ *   dS_ij = P_ij (dO_i . v_j - D_i)
+ *   dQ~_i = scale sum_j dS_ij k~_j,   dK~_j = scale sum_i dS_ij q~_i
+ * and, by Eq. (6), the gradient of a query coordinate u is dQ~_iu on the
+ * query's support and 0 elsewhere (likewise for keys).  The results come in
+ * code form, aligned with the codes: dq_val[..., t] is the gradient at
+ * q_idx[..., t].  A KV head's dk_val and dv sum over the query heads that
+ * read it.
+ *
+ * q_*, k_*, v, B ... o_t   as sfa_attn_fwd (o and dout share o_t)
+ * o             [B, Hq, n, d]   the forward's output
+ * lse           [B, Hq, n] float32, the forward's LSE (natural log)
+ * dout          [B, Hq, n, d]   dL/dO
+ * dq_val        [B, Hq, n, k]  float32 out
+ * dk_val        [B, Hkv, n, k] float32 out
+ * dv            [B, Hkv, n, d] float32 out
+ * ws, ws_bytes  caller-owned device workspace of at least
+ *               sfa_attn_bwd_workspace(B, Hq, Hkv, n, d) bytes: tile images of
+ *               the codes, V and dO written and read on the stream.  Calls
+ *               that overlap in time need separate workspaces.
+ * Arithmetic: every product on the matrix cores with both operands split
+ * into two bfloat16 pieces and three piece products kept (relative error
+ * ~2^-16 of the sum of |terms|), float32 accumulation; P recomputed as
+ * exp2(s log2(e) - LSE log2(e)) in float32.
+ * Limits: as sfa_attn_fwd, plus Hq / Hkv a power of two <= 4.
+ * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC, SFA_EHIP.
+ */
+sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val,
+                        const void* k_idx, const void* k_val,
+                        const void* v, const void* o, const float* lse,
+                        const void* dout,
+                        int B, int Hq, int Hkv, int n, int d, int k,
+                        int causal, float scale,
+                        int idx_t, int qk_val_t, int v_t, int o_t,
+                        float* dq_val, float* dk_val, float* dv,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* Bytes of device workspace sfa_attn_bwd needs (0 for invalid sizes or d). */
+size_t sfa_attn_bwd_workspace(int B, int Hq, int Hkv, int n, int d);
+
+/*
  * Bytes of device workspace sfa_attn_decode needs for these sizes.
  */
 size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d);

@@ -17,6 +17,7 @@ import torch
 __all__ = [
     "SfaError", "lib", "library_path", "sfa_abi_version", "sfa_strerror",
     "sfa_topk_encode", "sfa_attn_fwd_workspace", "sfa_attn_fwd", "sfa_attn_fwd_index",
+    "sfa_attn_bwd_workspace", "sfa_attn_bwd",
     "sfa_attn_decode_workspace", "sfa_attn_decode",
     "SFA_OK", "SFA_EINVAL", "SFA_ENOTSUP", "SFA_EHIP", "SFA_ENOSPC",
     "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16",
@@ -60,6 +61,11 @@ def lib() -> ctypes.CDLL:
         L.sfa_attn_fwd_index.restype = i32
         L.sfa_attn_fwd_index.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
                                          f32, i32, i32, i32, i32, vp, vp, vp]
+        L.sfa_attn_bwd.restype = i32
+        L.sfa_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                   i32, f32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
+        L.sfa_attn_bwd_workspace.restype = sz
+        L.sfa_attn_bwd_workspace.argtypes = [i32, i32, i32, i32, i32]
         L.sfa_attn_decode_workspace.restype = sz
         L.sfa_attn_decode_workspace.argtypes = [i32, i32, i32, i32]
         L.sfa_attn_decode.restype = i32
@@ -182,6 +188,58 @@ def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, wa
             args += [0, 0]
     _call(getattr(lib(), name)(*args, _stream(v)), name)
     return o, lse
+
+
+def sfa_attn_bwd_workspace(B: int, Hq: int, Hkv: int, n: int, d: int) -> int:
+    """Bytes of device workspace sfa_attn_bwd needs."""
+    return int(lib().sfa_attn_bwd_workspace(B, Hq, Hkv, n, d))
+
+
+def sfa_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, causal: bool = True,
+                 scale: float | None = None, dq: torch.Tensor | None = None,
+                 dk: torch.Tensor | None = None, dv: torch.Tensor | None = None,
+                 ws: torch.Tensor | None = None):
+    """SFA backward (straight-through estimator).  Shapes as sfa_attn_fwd;
+    o, dout [B, Hq, n, d] (same dtype), lse [B, Hq, n] float32.  Returns
+    (dq_val [B, Hq, n, k], dk_val [B, Hkv, n, k], dv [B, Hkv, n, d]), float32:
+    the gradients of the code values (Eq. (6): zero off the supports)."""
+    B, Hq, n, k = q_idx.shape
+    Hkv, d = k_idx.shape[1], v.shape[-1]
+    if tuple(q_val.shape) != (B, Hq, n, k) or tuple(k_idx.shape) != (B, Hkv, n, k) \
+            or tuple(k_val.shape) != (B, Hkv, n, k) or tuple(v.shape) != (B, Hkv, n, d) \
+            or tuple(o.shape) != (B, Hq, n, d) or tuple(dout.shape) != (B, Hq, n, d) \
+            or tuple(lse.shape) != (B, Hq, n):
+        raise ValueError("inconsistent shapes")
+    if q_idx.dtype != k_idx.dtype or q_val.dtype != k_val.dtype or o.dtype != dout.dtype:
+        raise TypeError("query/key codes, and o/dout, must share dtypes")
+    it = _check(q_idx, "q_idx", _IDX); _check(k_idx, "k_idx", _IDX)
+    qt = _check(q_val, "q_val", _VAL); _check(k_val, "k_val", _VAL)
+    vt = _check(v, "v", _VAL)
+    ot = _check(o, "o", _VAL); _check(dout, "dout", _VAL)
+    _check(lse, "lse", {torch.float32: SFA_F32})
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    f32 = dict(dtype=torch.float32, device=v.device)
+    dq = torch.empty((B, Hq, n, k), **f32) if dq is None else dq
+    dk = torch.empty((B, Hkv, n, k), **f32) if dk is None else dk
+    dv = torch.empty((B, Hkv, n, d), **f32) if dv is None else dv
+    for t, name, shape in ((dq, "dq", (B, Hq, n, k)), (dk, "dk", (B, Hkv, n, k)),
+                           (dv, "dv", (B, Hkv, n, d))):
+        _check(t, name, {torch.float32: SFA_F32})
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} has the wrong shape")
+    if ws is None:
+        ws = torch.empty(sfa_attn_bwd_workspace(B, Hq, Hkv, n, d), dtype=torch.uint8,
+                         device=v.device)
+    if ws.device.type != "cuda" or not ws.is_contiguous():
+        raise ValueError("ws must be a contiguous GPU tensor")
+    _call(lib().sfa_attn_bwd(q_idx.data_ptr(), q_val.data_ptr(), k_idx.data_ptr(),
+                             k_val.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                             dout.data_ptr(), B, Hq, Hkv, n, d, k, int(bool(causal)),
+                             float(scale), it, qt, vt, ot, dq.data_ptr(), dk.data_ptr(),
+                             dv.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
+                             _stream(v)), "sfa_attn_bwd")
+    return dq, dk, dv
 
 
 def sfa_attn_decode_workspace(B: int, Hq: int, Lmax: int, d: int) -> int:

@@ -17,7 +17,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsfa.so")
-SOURCES = ["sfa_encode.hip", "sfa_fwd.hip", "sfa_fwd_index.hip", "sfa_decode.hip", "sfa_capi.cpp"]
+SOURCES = ["sfa_encode.hip", "sfa_fwd.hip", "sfa_fwd_index.hip", "sfa_bwd.hip", "sfa_decode.hip",
+           "sfa_capi.cpp"]
 ARCH = "gfx950"
 
 

@@ -1,0 +1,555 @@
+// SFA backward with the straight-through estimator (Sec. 3.1, Eq. (6)) on
+// gfx950.
+//
+// With P the attention weights of the forward (recomputed from its LSE),
+//   dV = P^T dO,  dP = dO V^T,  dS = P o (dP - D),  D_i = dO_i . O_i,
+//   dQ~ = scale dS K~,  dK~ = scale dS^T Q~,
+// and Eq. (6) makes the gradient of a query (key) coordinate that of its code
+// value on the support and zero elsewhere: the outputs are dQ~ and dK~ read
+// at the codes' coordinates (dq_val, dk_val), plus dV.  As in the forward,
+// the products run on the matrix cores on densified codes; every operand is
+// split into two bf16 pieces x = x0 + x1 and each product keeps the three
+// terms a0 b0 + a0 b1 + a1 b0 (relative error ~2^-16 of sum |a b|), with
+// float32 accumulation.
+//
+// Kernels (all on the caller's stream):
+//   sfa_bwd_qprep_kernel  per (batch, query head, 32-row tile): an image of
+//       Q~ and dO as bf16 pieces, row-major and transposed, plus
+//       log2(e) * LSE and D for the 32 rows;
+//   sfa_bwd_kprep_kernel  per (batch, KV head, 32-key tile): K~ row-major and
+//       transposed, V row-major;
+//   sfa_bwd_dq_kernel     query-parallel (like the forward): S^T = K~ Q~^T,
+//       dP^T = V dO^T, dS^T, dQ~^T += K~^T dS^T over the allowed key tiles;
+//   sfa_bwd_dkv_kernel    key-parallel: S = Q~ K~^T, dP = dO V^T, dS,
+//       dV^T += dO^T P and dK~^T += Q~^T dS over the query tiles of every
+//       query head of the KV head.
+// Every output element is owned by one wavefront: no atomics.  The tile
+// images are copied global -> LDS with direct-to-LDS loads.
+#include "sfa_device.h"
+#include "sfa_launch.h"
+
+namespace sfa {
+namespace {
+
+constexpr int kT = 32;         // rows (queries or keys) per tile image
+constexpr int kNW = 4;         // wavefronts per workgroup (one per SIMD)
+constexpr int kTP = kT + 4;    // bf16 pitch of a transposed row: 72 B, conflict-free 8-byte reads
+constexpr float kLog2e = 1.44269504088896340736f;
+
+template <int D>
+struct Img {
+  static constexpr int RP = 2 * D + 8;                 // bf16 pitch of a row-major row: [piece][col]
+  static constexpr int RMB = kT * RP * 2;              // row-major array bytes
+  static constexpr int TRB = 2 * D * kTP * 2;          // transposed array bytes: [piece][col][row]
+  // query image: Q~ rm | Q~ tr | dO rm | dO tr | L2[32] | D[32]
+  static constexpr int Q_RMQ = 0, Q_TRQ = RMB, Q_RMO = RMB + TRB, Q_TRO = 2 * RMB + TRB;
+  static constexpr int Q_L2 = 2 * RMB + 2 * TRB, Q_D = Q_L2 + kT * 4;
+  static constexpr int QB = (Q_D + kT * 4 + 1023) / 1024 * 1024;
+  // key image: K~ rm | K~ tr | V rm
+  static constexpr int K_RMK = 0, K_TRK = RMB, K_RMV = RMB + TRB;
+  static constexpr int KB = (2 * RMB + TRB + 1023) / 1024 * 1024;
+  static constexpr int NKB = D / 16, NDB = D / 32;
+};
+
+struct BwdParams {
+  const void* q_idx;
+  const void* q_val;
+  const void* k_idx;
+  const void* k_val;
+  const void* v;
+  const void* o;
+  const float* lse;
+  const void* dout;
+  float* dq;
+  float* dk;
+  float* dv;
+  unsigned char* qimg;
+  unsigned char* kimg;
+  int Hq, Hkv, G, n, k, causal;
+  int idx16, valbf16, vbf16, obf16;
+  int nt;    // tiles per head: ceil(n / 32)
+  int BR;    // query positions per dq workgroup: 128 / G
+  int nqb;   // dq workgroups per (batch, KV head)
+  float scale, c;  // c = scale * log2(e)
+};
+
+__device__ __forceinline__ void split2(float x, uint16_t& h, uint16_t& l) {
+  const uint32_t hb = f32_to_bf16_rne(x);
+  h = (uint16_t)hb;
+  l = (uint16_t)f32_to_bf16_rne(x - bf16_bits_to_f32(hb));
+}
+
+__device__ __forceinline__ float load_f(const void* p, int64_t i, int bf16) {
+  return bf16 ? bf16_bits_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
+}
+
+// c += a1 b0 + a0 b1 + a0 b0 (smaller terms first)
+__device__ __forceinline__ void mfma3(floatx16& c, const bf16x8 (&a)[2], const bf16x8 (&b)[2]) {
+  c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1], b[0], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[1], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[0], c, 0, 0, 0);
+}
+
+// Copy `bytes` (a multiple of 1 KB) global -> LDS, whole-wave 16-byte
+// direct-to-LDS loads spread over the workgroup's waves.
+__device__ __forceinline__ void dma(const unsigned char* src, unsigned char* dst, int bytes, int wave,
+                                    int lane) {
+  for (int i = wave; i < bytes / 1024; i += kNW)
+    __builtin_amdgcn_global_load_lds(src + i * 1024 + lane * 16,
+                                     (__attribute__((address_space(3))) void*)(dst + i * 1024), 16,
+                                     0, 0);
+}
+
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
+
+// A-operand slice of a transposed array: row `row` (a coordinate / dimension),
+// columns kbase + 0..3 and kbase + 8..11 (the key / query order of the MFMA
+// output layout).
+__device__ __forceinline__ bf16x8 tr_load(const uint16_t* tr, int row, int kbase) {
+  const uint16_t* p = tr + row * kTP + kbase;
+  const uint2 v0 = *(const uint2*)p;
+  const uint2 v1 = *(const uint2*)(p + 8);
+  const u32x4 w = {v0.x, v0.y, v1.x, v1.y};
+  return __builtin_bit_cast(bf16x8, w);
+}
+
+// ---------------------------------------------------------------------------
+// images
+// ---------------------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
+  using I = Img<D>;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  uint16_t* rmq = (uint16_t*)(smem + I::Q_RMQ);
+  uint16_t* trq = (uint16_t*)(smem + I::Q_TRQ);
+  uint16_t* rmo = (uint16_t*)(smem + I::Q_RMO);
+  uint16_t* tro = (uint16_t*)(smem + I::Q_TRO);
+  float* l2 = (float*)(smem + I::Q_L2);
+  float* dd = (float*)(smem + I::Q_D);
+  const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;  // bh = b * Hq + hq
+  const int n = p.n, k = p.k;
+  const int64_t r0 = (int64_t)bh * n + (int64_t)t * kT;  // first row of the tile
+  for (int i = tid; i < I::QB / 16; i += 256) ((uint4*)smem)[i] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  for (int e = tid; e < kT * k; e += 256) {
+    const int r = e / k;
+    if (t * kT + r >= n) break;
+    const int f = load_idx(p.q_idx, r0 * k + e, p.idx16, D - 1);
+    uint16_t h, l;
+    split2(load_val(p.q_val, r0 * k + e, p.valbf16), h, l);
+    rmq[r * I::RP + f] = h;
+    rmq[r * I::RP + D + f] = l;
+    trq[f * kTP + r] = h;
+    trq[(D + f) * kTP + r] = l;
+  }
+  // dO pieces, and D = dO . O with 8 threads per row (fixed reduction order)
+  {
+    const int r = tid >> 3, part = tid & 7;
+    const bool ok = t * kT + r < n;
+    float acc = 0.f;
+    for (int x = 0; x < D / 8; ++x) {
+      const int dim = part * (D / 8) + x;
+      float g = 0.f, o = 0.f;
+      if (ok) {
+        g = load_f(p.dout, (r0 + r) * D + dim, p.obf16);
+        o = load_f(p.o, (r0 + r) * D + dim, p.obf16);
+      }
+      acc = fmaf(g, o, acc);
+      uint16_t h, l;
+      split2(g, h, l);
+      rmo[r * I::RP + dim] = h;
+      rmo[r * I::RP + D + dim] = l;
+      tro[dim * kTP + r] = h;
+      tro[(D + dim) * kTP + r] = l;
+    }
+    acc += __shfl_xor(acc, 1, 64);
+    acc += __shfl_xor(acc, 2, 64);
+    acc += __shfl_xor(acc, 4, 64);
+    if (part == 0) {
+      // rows past n: P = exp2(s c - inf) = 0 and D = 0, so they add nothing
+      l2[r] = ok ? p.lse[r0 + r] * kLog2e : INFINITY;
+      dd[r] = ok ? acc : 0.f;
+    }
+  }
+  __syncthreads();
+  uint4* dst = (uint4*)(p.qimg + ((int64_t)bh * p.nt + t) * I::QB);
+  for (int i = tid; i < I::QB / 16; i += 256) dst[i] = ((const uint4*)smem)[i];
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void sfa_bwd_kprep_kernel(BwdParams p) {
+  using I = Img<D>;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  uint16_t* rmk = (uint16_t*)(smem + I::K_RMK);
+  uint16_t* trk = (uint16_t*)(smem + I::K_TRK);
+  uint16_t* rmv = (uint16_t*)(smem + I::K_RMV);
+  const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;  // bh = b * Hkv + hkv
+  const int n = p.n, k = p.k;
+  const int64_t r0 = (int64_t)bh * n + (int64_t)t * kT;
+  for (int i = tid; i < I::KB / 16; i += 256) ((uint4*)smem)[i] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  for (int e = tid; e < kT * k; e += 256) {
+    const int r = e / k;
+    if (t * kT + r >= n) break;
+    const int f = load_idx(p.k_idx, r0 * k + e, p.idx16, D - 1);
+    uint16_t h, l;
+    split2(load_val(p.k_val, r0 * k + e, p.valbf16), h, l);
+    rmk[r * I::RP + f] = h;
+    rmk[r * I::RP + D + f] = l;
+    trk[f * kTP + r] = h;
+    trk[(D + f) * kTP + r] = l;
+  }
+  for (int e = tid; e < kT * D; e += 256) {
+    const int r = e / D, dim = e - r * D;
+    if (t * kT + r >= n) break;
+    uint16_t h, l;
+    split2(load_f(p.v, (r0 + r) * D + dim, p.vbf16), h, l);
+    rmv[r * I::RP + dim] = h;
+    rmv[r * I::RP + D + dim] = l;
+  }
+  __syncthreads();
+  uint4* dst = (uint4*)(p.kimg + ((int64_t)bh * p.nt + t) * I::KB);
+  for (int i = tid; i < I::KB / 16; i += 256) dst[i] = ((const uint4*)smem)[i];
+}
+
+// Row-major B operand (lane = row l32, coordinates 16 kb + 8 hh ..) of both
+// pieces, straight from an image in global memory.
+template <int D>
+__device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, int l32, int hh,
+                                            bf16x8 (&b)[2][D / 16]) {
+  const uint16_t* rm = (const uint16_t*)(img + off);
+#pragma unroll
+  for (int pc = 0; pc < 2; ++pc)
+#pragma unroll
+    for (int kb = 0; kb < D / 16; ++kb)
+      b[pc][kb] = *(const bf16x8*)(rm + l32 * Img<D>::RP + pc * D + kb * 16 + 8 * hh);
+}
+
+// ---------------------------------------------------------------------------
+// dq: query-parallel
+// ---------------------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(256) void sfa_bwd_dq_kernel(BwdParams p) {
+  using I = Img<D>;
+  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = p.n;
+  const int qb = p.nqb - 1 - (int)blockIdx.x;  // longest causal blocks first
+  const int bh = blockIdx.y, b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+  const int i0 = qb * p.BR;
+  // wave: 32 consecutive positions of one query head (BR is a multiple of 32)
+  const int hq = hkv * p.G + (wave * kT) / p.BR;
+  const int pos0 = i0 + (wave * kT) % p.BR;
+  const int my_i = pos0 + l32;
+  const bool wave_ok = pos0 < n;
+  const bool row_ok = my_i < n;
+  const int wave_i_max = min(pos0 + kT - 1, n - 1);
+
+  bf16x8 qB[2][NKB], dB[2][NKB];
+  float L2 = INFINITY, Dq = 0.f;
+  if (wave_ok) {
+    const unsigned char* qimg = p.qimg + ((int64_t)(b * p.Hq + hq) * p.nt + pos0 / kT) * I::QB;
+    load_rows_b<D>(qimg, I::Q_RMQ, l32, hh, qB);
+    load_rows_b<D>(qimg, I::Q_RMO, l32, hh, dB);
+    L2 = ((const float*)(qimg + I::Q_L2))[l32];
+    Dq = ((const float*)(qimg + I::Q_D))[l32];
+  } else {
+#pragma unroll
+    for (int pc = 0; pc < 2; ++pc)
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        qB[pc][kb] = bf16x8{};
+        dB[pc][kb] = bf16x8{};
+      }
+  }
+  floatx16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
+
+  const int blk_last = min(n, i0 + p.BR) - 1;
+  const int nkt = ((p.causal ? blk_last + 1 : n) + kT - 1) / kT;
+  const unsigned char* kimg0 = p.kimg + (int64_t)bh * p.nt * I::KB;
+  dma(kimg0, smem, I::KB, wave, lane);
+  wait_vm();
+  __syncthreads();
+  for (int jt = 0; jt < nkt; ++jt) {
+    const int stage = jt & 1;
+    if (jt + 1 < nkt) dma(kimg0 + (int64_t)(jt + 1) * I::KB, smem + (stage ^ 1) * I::KB, I::KB, wave, lane);
+    const int j0 = jt * kT;
+    if (wave_ok && (!p.causal || wave_i_max >= j0)) {
+      const unsigned char* K = smem + stage * I::KB;
+      const uint16_t* rmk = (const uint16_t*)(K + I::K_RMK);
+      const uint16_t* trk = (const uint16_t*)(K + I::K_TRK);
+      const uint16_t* rmv = (const uint16_t*)(K + I::K_RMV);
+      floatx16 s, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        bf16x8 a[2], v[2];
+#pragma unroll
+        for (int pc = 0; pc < 2; ++pc) {
+          a[pc] = *(const bf16x8*)(rmk + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          v[pc] = *(const bf16x8*)(rmv + l32 * RP + pc * D + kb * 16 + 8 * hh);
+        }
+        const bf16x8 qq[2] = {qB[0][kb], qB[1][kb]};
+        const bf16x8 gg[2] = {dB[0][kb], dB[1][kb]};
+        mfma3(s, a, qq);   // S^T = K~ Q~^T   (keys x queries)
+        mfma3(dp, v, gg);  // dP^T = V dO^T
+      }
+      // dS^T = P^T o (dP^T - D); lane = query my_i, register r = key j0 + 8(r/4) + 4hh + r%4
+      bf16x8 dsb[2][2];  // [kk][piece]
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = j0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
+        const float pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -L2)) : 0.f;
+        uint16_t h, l;
+        split2(pr * (dp[r] - Dq), h, l);
+        dsb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h);
+        dsb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l);
+      }
+      // dQ~^T += K~^T dS^T   (coordinates x queries)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int kbase = 16 * kk + 4 * hh;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8 a[2] = {tr_load(trk, db * 32 + l32, kbase), tr_load(trk, D + db * 32 + l32, kbase)};
+          mfma3(acc[db], a, dsb[kk]);
+        }
+      }
+    }
+    wait_vm();
+    __syncthreads();
+  }
+
+  // dq_val = scale * dQ~ at the row's support: stage dQ~ through LDS
+  // (the key stages are free now): [wave][query][coordinate], pitch D + 4.
+  float* L = (float*)smem + wave * kT * (D + 4);
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
+  __syncthreads();
+  if (row_ok) {
+    const int64_t row = ((int64_t)b * p.Hq + hq) * n + my_i;
+    for (int t = hh; t < p.k; t += 2) {
+      const int u = load_idx(p.q_idx, row * p.k + t, p.idx16, D - 1);
+      p.dq[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dk, dv: key-parallel
+// ---------------------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
+  using I = Img<D>;
+  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = p.n;
+  const int bh = blockIdx.y, b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+  const int j0b = (int)blockIdx.x * (kNW * kT);  // most key tiles first: smallest j0 first
+  const int jw0 = j0b + wave * kT;
+  const int my_j = jw0 + l32;
+  const bool wave_ok = jw0 < n;
+  const bool key_ok = my_j < n;
+
+  bf16x8 kB[2][NKB], vB[2][NKB];
+  if (wave_ok) {
+    const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
+    load_rows_b<D>(kimg, I::K_RMK, l32, hh, kB);
+    load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
+  } else {
+#pragma unroll
+    for (int pc = 0; pc < 2; ++pc)
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        kB[pc][kb] = bf16x8{};
+        vB[pc][kb] = bf16x8{};
+      }
+  }
+  floatx16 accv[NDB], acck[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) { accv[db][r] = 0.f; acck[db][r] = 0.f; }
+
+  // query tiles of all G heads that see some key of the block
+  const int t0 = p.causal ? j0b / kT : 0;
+  const int per_head = p.nt - t0;
+  const int total = p.G * per_head;
+  auto qimg_of = [&](int it) {
+    const int h = it / per_head, t = t0 + it - h * per_head;
+    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + h) * p.nt + t) * I::QB;
+  };
+  if (total > 0) {
+    dma(qimg_of(0), smem, I::QB, wave, lane);
+    wait_vm();
+  }
+  __syncthreads();
+  for (int it = 0; it < total; ++it) {
+    const int stage = it & 1;
+    if (it + 1 < total) dma(qimg_of(it + 1), smem + (stage ^ 1) * I::QB, I::QB, wave, lane);
+    const int h = it / per_head, t = t0 + it - h * per_head;
+    const int q0 = t * kT;
+    (void)h;
+    if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0)) {
+      const unsigned char* Q = smem + stage * I::QB;
+      const uint16_t* rmq = (const uint16_t*)(Q + I::Q_RMQ);
+      const uint16_t* trq = (const uint16_t*)(Q + I::Q_TRQ);
+      const uint16_t* rmo = (const uint16_t*)(Q + I::Q_RMO);
+      const uint16_t* tro = (const uint16_t*)(Q + I::Q_TRO);
+      const float* l2 = (const float*)(Q + I::Q_L2);
+      const float* dd = (const float*)(Q + I::Q_D);
+      floatx16 s, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        bf16x8 a[2], g[2];
+#pragma unroll
+        for (int pc = 0; pc < 2; ++pc) {
+          a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
+        }
+        const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
+        const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
+        mfma3(s, a, kk2);   // S = Q~ K~^T   (queries x keys)
+        mfma3(dp, g, vv2);  // dP = dO V^T
+      }
+      // lane = key my_j; register r = query row q0 + 8(r/4) + 4hh + r%4
+      bf16x8 pb[2][2], dsb[2][2];  // [kk][piece]
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
+        const float4 d4 = *(const float4*)(dd + 8 * g4 + 4 * hh);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const int r = 4 * g4 + x;
+          const int i = q0 + 8 * g4 + 4 * hh + x;
+          const bool ok = key_ok && (!p.causal || i >= my_j);
+          const float pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x])) : 0.f;
+          uint16_t h1, l1, h2, l2b;
+          split2(pr, h1, l1);
+          split2(pr * (dp[r] - dv4[x]), h2, l2b);
+          pb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h1);
+          pb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l1);
+          dsb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h2);
+          dsb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l2b);
+        }
+      }
+      // dV^T += dO^T P,  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int kbase = 16 * kk + 4 * hh;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8 ao[2] = {tr_load(tro, db * 32 + l32, kbase), tr_load(tro, D + db * 32 + l32, kbase)};
+          mfma3(accv[db], ao, pb[kk]);
+          const bf16x8 aq[2] = {tr_load(trq, db * 32 + l32, kbase), tr_load(trq, D + db * 32 + l32, kbase)};
+          mfma3(acck[db], aq, dsb[kk]);
+        }
+      }
+    }
+    wait_vm();
+    __syncthreads();
+  }
+
+  // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
+  if (key_ok) {
+    float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *(float4*)(dvr + db * 32 + 8 * g4 + 4 * hh) =
+            make_float4(accv[db][4 * g4], accv[db][4 * g4 + 1], accv[db][4 * g4 + 2], accv[db][4 * g4 + 3]);
+  }
+  // dk_val = scale * dK~ at the key's support, through LDS
+  float* L = (float*)smem + wave * kT * (D + 4);
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acck[db][r];
+  __syncthreads();
+  if (key_ok) {
+    const int64_t row = (int64_t)bh * n + my_j;
+    for (int t = hh; t < p.k; t += 2) {
+      const int u = load_idx(p.k_idx, row * p.k + t, p.idx16, D - 1);
+      p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+    }
+  }
+}
+
+template <int D>
+hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
+  using I = Img<D>;
+  static bool configured = false;
+  if (!configured) {
+    hipError_t e = hipSuccess;
+    const void* fns[4] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
+                          (const void*)sfa_bwd_dq_kernel<D>, (const void*)sfa_bwd_dkv_kernel<D>};
+    const int bytes[4] = {I::QB, I::KB, 2 * I::KB, 2 * I::QB};
+    for (int f = 0; f < 4 && e == hipSuccess; ++f)
+      if (bytes[f] > 65536) e = hipFuncSetAttribute(fns[f], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[f]);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  static_assert(2 * I::KB >= kNW * kT * (D + 4) * 4, "dq gather fits the stages");
+  static_assert(2 * I::QB >= kNW * kT * (D + 4) * 4, "dk gather fits the stages");
+  const dim3 blk(256);
+  hipLaunchKernelGGL(sfa_bwd_qprep_kernel<D>, dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
+  hipLaunchKernelGGL(sfa_bwd_kprep_kernel<D>, dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
+  hipLaunchKernelGGL(sfa_bwd_dq_kernel<D>, dim3(p.nqb, B * p.Hkv), blk, 2 * I::KB, stream, p);
+  const int nkb = (p.n + kNW * kT - 1) / (kNW * kT);
+  hipLaunchKernelGGL(sfa_bwd_dkv_kernel<D>, dim3(nkb, B * p.Hkv), blk, 2 * I::QB, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int bwd_max_group() { return (kNW * kT) / kT; }
+
+size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d) {
+  const size_t nt = (size_t)((n + kT - 1) / kT);
+  const size_t qb = d == 64 ? Img<64>::QB : Img<128>::QB;
+  const size_t kb = d == 64 ? Img<64>::KB : Img<128>::KB;
+  return (size_t)B * Hq * nt * qb + (size_t)B * Hkv * nt * kb;
+}
+
+hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
+                           const void* k_val, const void* v, const void* o, const float* lse,
+                           const void* dout, int B, int Hq, int Hkv, int n, int d, int k,
+                           int causal, float scale, int idx16, int valbf16, int vbf16, int obf16,
+                           float* dq, float* dk, float* dv, void* ws, hipStream_t stream) {
+  BwdParams p;
+  p.q_idx = q_idx; p.q_val = q_val; p.k_idx = k_idx; p.k_val = k_val; p.v = v; p.o = o;
+  p.lse = lse; p.dout = dout; p.dq = dq; p.dk = dk; p.dv = dv;
+  p.Hq = Hq; p.Hkv = Hkv; p.G = Hq / Hkv; p.n = n; p.k = k; p.causal = causal;
+  p.idx16 = idx16; p.valbf16 = valbf16; p.vbf16 = vbf16; p.obf16 = obf16;
+  p.nt = (n + kT - 1) / kT;
+  p.BR = kNW * kT / p.G;
+  p.nqb = (n + p.BR - 1) / p.BR;
+  p.scale = scale;
+  p.c = (float)((double)scale * 1.4426950408889634);
+  const size_t qbytes = (size_t)B * Hq * p.nt * (d == 64 ? Img<64>::QB : Img<128>::QB);
+  p.qimg = (unsigned char*)ws;
+  p.kimg = (unsigned char*)ws + qbytes;
+  return d == 64 ? launch_d<64>(p, B, stream) : launch_d<128>(p, B, stream);
+}
+
+}  // namespace sfa

@@ -8,7 +8,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 2;
+constexpr int kAbiVersion = 3;
 constexpr int kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
 
 bool is_idx(int t) { return t == SFA_I32 || t == SFA_I16; }
@@ -84,6 +84,28 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                                        causal != 0, scale, idx_t == SFA_I16,
                                        qk_val_t == SFA_BF16, v_t == SFA_BF16, o_t == SFA_BF16,
                                        o, lse, ws, (hipStream_t)stream));
+}
+
+size_t sfa_attn_bwd_workspace(int B, int Hq, int Hkv, int n, int d) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || n < 1 || (d != 64 && d != 128)) return 0;
+  return sfa::bwd_workspace_bytes(B, Hq, Hkv, n, d);
+}
+
+sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
+                        const void* k_val, const void* v, const void* o, const float* lse,
+                        const void* dout, int B, int Hq, int Hkv, int n, int d, int k, int causal,
+                        float scale, int idx_t, int qk_val_t, int v_t, int o_t, float* dq_val,
+                        float* dk_val, float* dv, void* ws, size_t ws_bytes, void* stream) {
+  sfa_status st = check_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k, scale, idx_t,
+                            qk_val_t, v_t, o_t, o);
+  if (st != SFA_OK) return st;
+  if (!lse || !dout || !dq_val || !dk_val || !dv) return SFA_EINVAL;
+  if (!pow2_le(Hq / Hkv, sfa::bwd_max_group())) return SFA_ENOTSUP;
+  if (ws == nullptr || ws_bytes < sfa::bwd_workspace_bytes(B, Hq, Hkv, n, d)) return SFA_ENOSPC;
+  return from_hip(sfa::launch_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n,
+                                       d, k, causal != 0, scale, idx_t == SFA_I16,
+                                       qk_val_t == SFA_BF16, v_t == SFA_BF16, o_t == SFA_BF16,
+                                       dq_val, dk_val, dv, ws, (hipStream_t)stream));
 }
 
 sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,

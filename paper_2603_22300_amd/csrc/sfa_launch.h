@@ -18,6 +18,14 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
 int fwd_max_group();
 size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16);
 
+hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
+                           const void* k_val, const void* v, const void* o, const float* lse,
+                           const void* dout, int B, int Hq, int Hkv, int n, int d, int k,
+                           int causal, float scale, int idx16, int valbf16, int vbf16, int obf16,
+                           float* dq, float* dk, float* dv, void* ws, hipStream_t stream);
+size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d);
+int bwd_max_group();
+
 hipError_t launch_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,
                                  const void* k_val, const void* v, int B, int Hq, int Hkv, int n,
                                  int d, int k, int causal, float scale, int idx16, int valbf16,

@@ -12,6 +12,14 @@ TOL_O_F32 = 1e-5
 TOL_O_BF16V = 5e-3
 TOL_LSE = 1e-4
 
+# Backward (no tolerance is fixed by the method): max |g - g_oracle| as a
+# fraction of max |g_oracle| of the same tensor, keyed by (bf16 V, bf16 O and
+# dO).  The products themselves carry ~2^-16; the error that dominates enters
+# through D_i = dO_i . O_i, computed from the forward's O: ~1e-6 relative on
+# the float32 path, ~1e-4 with bf16 V (float16 P in the forward), 2^-9 when
+# O and dO are stored in bf16.  Each bound leaves a factor of ~10 over that.
+TOL_GRAD = {(False, False): 1e-4, (True, False): 2e-3, (True, True): 2e-2}
+
 
 def np_vals(t: torch.Tensor) -> np.ndarray:
     """float32 tensors -> float32 numpy; bf16 tensors -> uint16 bit patterns."""
@@ -60,3 +68,15 @@ def sample_rows(n: int, extra=(), count: int = 24, seed: int = 0, tile: int = 64
     rows |= {r for r in extra if 0 <= r < n}
     rows |= set(rng.integers(0, n, size=count).tolist())
     return np.array(sorted(rows), dtype=np.int64)
+
+
+def check_grad(g_gpu: torch.Tensor, g_ref: np.ndarray, tol: float, what: str):
+    got = np_f64(g_gpu)
+    scale = float(np.abs(g_ref).max()) if g_ref.size else 0.0
+    err = float(np.abs(got - g_ref).max()) if got.size else 0.0
+    rel = err / scale if scale > 0 else err
+    print(f"[parity] {what}: max|g-g_oracle| = {err:.3e}, {rel:.2e} of max|g| = {scale:.3e} "
+          f"(tol {tol:.0e})", flush=True)
+    assert np.isfinite(got).all(), f"{what}: non-finite gradient"
+    assert rel <= tol, f"{what}: max |g - g_oracle| / max |g| = {rel:.3e} > {tol:.1e}"
+    return rel

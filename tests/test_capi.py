@@ -29,6 +29,7 @@ def L():
 def test_exports_every_declared_symbol(L):
     names = _declared()
     assert {"sfa_topk_encode", "sfa_attn_fwd", "sfa_attn_fwd_workspace", "sfa_attn_fwd_index",
+            "sfa_attn_bwd", "sfa_attn_bwd_workspace",
             "sfa_attn_decode", "sfa_attn_decode_workspace", "sfa_abi_version",
             "sfa_strerror"} <= set(names)
     for nm in names:
@@ -36,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_strerror(L):
-    assert L.sfa_abi_version() == 2
+    assert L.sfa_abi_version() == 3
     for s in range(5):
         assert L.sfa_strerror(s)
 
@@ -116,3 +117,27 @@ def test_decode_validation_and_workspace(L):
     assert _dec(L, Hq=32, Hkv=2) == 2       # group of 16 heads: unsupported
     assert _dec(L, d=80, k=8) == 2
     assert _dec(L, kc_idx_t=3) == 1
+
+
+def _bwd(L, **kw):
+    a = dict(q_idx=FAKE, q_val=FAKE, k_idx=FAKE, k_val=FAKE, v=FAKE, o=FAKE, lse=FAKE, dout=FAKE,
+             B=1, Hq=4, Hkv=2, n=16, d=64, k=8, causal=1, scale=0.125, idx_t=0, qk_val_t=2,
+             v_t=3, o_t=3, dq=FAKE, dk=FAKE, dv=FAKE, ws=FAKE, ws_bytes=ctypes.c_size_t(1 << 40),
+             stream=None)
+    a.update(kw)
+    return L.sfa_attn_bwd(*a.values())
+
+
+def test_bwd_validation_and_workspace(L):
+    need = L.sfa_attn_bwd_workspace(1, 4, 2, 16, 64)
+    assert need > 0
+    assert L.sfa_attn_bwd_workspace(1, 4, 2, 16, 96) == 0
+    assert _bwd(L, ws_bytes=ctypes.c_size_t(need - 1)) == 4
+    assert _bwd(L, ws=None) == 4
+    assert _bwd(L, lse=None) == 1
+    assert _bwd(L, dout=None) == 1
+    assert _bwd(L, dq=None) == 1
+    assert _bwd(L, k=0) == 1
+    assert _bwd(L, Hq=3, Hkv=2) == 1
+    assert _bwd(L, Hq=16, Hkv=2) == 2      # group of 8 heads: not supported by the backward
+    assert _bwd(L, d=96, k=8) == 2

@@ -1,0 +1,84 @@
+"""GPU parity: sfa_attn_bwd (straight-through estimator, Sec. 3.1 Eq. (6))
+against the oracle's backward.
+
+The GPU path codes the dense Q, K with its own encoder, runs its own forward
+for O and LSE, and then the backward; the oracle codes the same dense inputs
+with its own Top-k and evaluates the plain chain rule in float64.  dO is a
+seeded input shared by both.  Gradients are compared as a fraction of the
+largest oracle gradient of the same tensor (helpers.TOL_GRAD)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_22300_amd as sfa
+import sfa_inputs as si
+from helpers import TOL_GRAD, check_grad, np_vals
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, o_bf16=False):
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed,
+                            v_dtype=torch.bfloat16 if v_bf16 else torch.float32, device=DEV)
+    odt = torch.bfloat16 if o_bf16 else torch.float32
+    dout = torch.empty((B, Hq, n, d), device=DEV)
+    for b in range(B):
+        for h in range(Hq):
+            dout[b, h] = si.normal((n, d), seed, "dout", b, h, device=DEV)
+    dout = dout.to(odt)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    scale = 1.0 / math.sqrt(d)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=odt)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    oqi, oqv = oracle.topk_encode(q.cpu().numpy(), k)
+    oki, okv = oracle.topk_encode(kk.cpu().numpy(), k)
+    # the GPU and oracle codes are bit-identical (encoder parity), so the
+    # gradients line up entry by entry
+    assert np.array_equal(qi.cpu().numpy(), oqi) and np.array_equal(ki.cpu().numpy(), oki)
+    gq, gk, gv = oracle.attn_bwd(oqi, oqv, oki, okv, np_vals(v), np_vals(dout), d, scale, causal)
+    tol = TOL_GRAD[(v_bf16, o_bf16)]
+    e = (check_grad(dq, gq, tol, "dq_val"), check_grad(dk, gk, tol, "dk_val"),
+         check_grad(dv, gv, tol, "dv"))
+    return e
+
+
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,v_bf16",
+    [
+        (1, 1, 1, 1, 64, 8, True, False),       # n = 1: every gradient but dv is zero
+        (1, 1, 1, 37, 64, 8, True, False),      # one ragged tile
+        (1, 4, 2, 100, 128, 16, True, True),    # GQA 2:1, ragged
+        (2, 4, 1, 161, 128, 16, True, True),    # GQA 4:1, several key blocks
+        (1, 2, 2, 130, 64, 16, False, True),    # non-causal
+        (1, 1, 1, 70, 64, 1, True, True),       # k = 1
+        (1, 2, 2, 96, 64, 64, True, False),     # k = d: dense attention gradients
+        (1, 2, 1, 257, 128, 8, True, False),    # float32 V, past two key blocks
+        (1, 4, 4, 64, 128, 32, True, True),     # exact tiles, G = 1
+    ])
+def test_shapes(B, Hq, Hkv, n, d, k, causal, v_bf16):
+    _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=7 * n + k + Hq)
+
+
+def test_bf16_output_and_grad():
+    _run(1, 4, 2, 150, 128, 16, True, True, seed=21, o_bf16=True)
+
+
+def test_deterministic():
+    torch.manual_seed(0)
+    B, Hq, Hkv, n, d, k = 1, 4, 2, 200, 128, 16
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, 5, v_dtype=torch.bfloat16, device=DEV)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.float32)
+    dout = si.normal((B, Hq, n, d), 5, "dout", device=DEV)
+    a = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout)
+    b = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
