@@ -6,7 +6,9 @@ B=1, 32 query heads over 8 KV heads, n=32768, d=128, k=16, causal, bf16 V and
 output.  One step = Top-k coding of the dense fp32 Q and K
 (sfa_topk_encode x2) + the fused forward (sfa_attn_fwd), with every input
 already resident in HBM.  `--workload decode_64k` times the decode step
-(sfa_attn_decode) over the 64-sequence x 64K sparse-code KV cache instead.
+(sfa_attn_decode) over the 64-sequence x 64K sparse-code KV cache instead, and
+`--pass bwd` the backward with the straight-through estimator (sfa_attn_bwd on
+the workload's codes, forward O / LSE and a seeded dO).
 
 Prints ONE JSON line.  Besides the contract fields it carries
   roofline      the dominant kernel's algorithmic rate (from HIP events
@@ -194,6 +196,118 @@ def bench_fwd(w, steps, warmup, want_cpu):
     return out
 
 
+def bench_bwd(w, steps, warmup, want_cpu):
+    """One step = sfa_attn_bwd (codes, O, LSE and dO resident in HBM)."""
+    q, k, v = _fwd_inputs(w)
+    B, Hq, Hkv, n, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
+    qi, qv = sfa.sfa_topk_encode(q, kk)
+    ki, kv = sfa.sfa_topk_encode(k, kk)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale,
+                              o_dtype=torch.bfloat16)
+    dout = torch.empty((B, Hq, n, d), dtype=torch.bfloat16, device=DEV)
+    for b in range(B):
+        for h in range(Hq):
+            dout[b, h] = si.normal((n, d), w.seed, "dout", b, h, device=DEV).to(torch.bfloat16)
+    dq = torch.empty((B, Hq, n, kk), dtype=torch.float32, device=DEV)
+    dk = torch.empty((B, Hkv, n, kk), dtype=torch.float32, device=DEV)
+    dv = torch.empty((B, Hkv, n, d), dtype=torch.float32, device=DEV)
+    ws = torch.empty(sfa.sfa_attn_bwd_workspace(B, Hq, Hkv, n, d), dtype=torch.uint8, device=DEV)
+
+    def step():
+        sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=w.causal, scale=w.scale,
+                         dq=dq, dk=dk, dv=dv, ws=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    wall0 = time.perf_counter()
+    for s_ in range(steps):
+        evs[s_][0].record()
+        step()
+        evs[s_][1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = [a.elapsed_time(b_) for a, b_ in evs]
+    ms_step = float(np.mean(ms))
+    pairs_per_head = n * (n + 1) // 2 if w.causal else n * n
+    pairs = B * Hq * pairs_per_head
+    E = _overlap_count(qi, ki, d, w.G, w.causal)
+    # dV and dP: 2d flops per allowed pair each; S, dq~ and dk~ on the
+    # supports: 2 flops per shared coordinate each
+    algo = 4.0 * d * pairs + 6.0 * E
+    out = {
+        "metric": "SFA bwd (straight-through estimator) tokens/s at n=32K,d=128,k=16",
+        "value": B * n / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "n": n, "d": d, "k": kk,
+            "causal": w.causal, "seed": w.seed, "step": "sfa_attn_bwd",
+            "precision": "O and dO bf16; products on MFMA with bf16 hi/lo pieces (3 terms), "
+                         "fp32 accumulate; gradients fp32",
+        },
+        "roofline": {
+            "kernel": "sfa_bwd_dq_kernel + sfa_bwd_dkv_kernel (+ tile images)",
+            "bound": "mfma",
+            "achieved": algo / (ms_step * 1e-3) / 1e12,
+            "peak": PEAK_MFMA_BF16 / 1e12,
+            "unit": "TFLOP/s",
+            "frac": algo / (ms_step * 1e-3) / PEAK_MFMA_BF16,
+            "traffic": None,
+            "algorithmic_flops_per_launch": algo,
+            "allowed_pairs": pairs,
+            "overlap_products_E": E,
+            "ms_min": float(np.min(ms)),
+        },
+        "wall_s_timed": wall,
+    }
+    if want_cpu:
+        out["cpu_baseline"] = cpu_baseline_bwd(w, q, k, v, dout)
+    return out
+
+
+def cpu_baseline_bwd(w, q, k, v, dout, n_sub=3072):
+    """The oracle backward (oracle.attn_bwd, float64) on the first n_sub
+    positions of one KV head group -- a causal prefix is a sub-problem of the
+    same workload -- scaled by the ratio of allowed pairs."""
+    import oracle
+    G = w.G
+    sl = slice(0, n_sub)
+    qn = q[:1, :G, sl].cpu().numpy()
+    kn = k[:1, :1, sl].cpu().numpy()
+    vn = v[:1, :1, sl].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    dn = dout[:1, :G, sl].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    t = time.perf_counter()
+    qi, qv = oracle.topk_encode(qn, w.k)
+    ki, kv = oracle.topk_encode(kn, w.k)
+    oracle.attn_bwd(qi, qv, ki, kv, vn, dn, w.d, w.scale, w.causal)
+    dt = time.perf_counter() - t
+    sub_pairs = G * (n_sub * (n_sub + 1) // 2 if w.causal else n_sub * n_sub)
+    all_pairs = w.B * w.Hq * (w.n * (w.n + 1) // 2 if w.causal else w.n * w.n)
+    total = dt * all_pairs / sub_pairs
+    return {
+        "value": w.B * w.n / total,
+        "unit": "tokens/s",
+        "cores": _blas_threads(),
+        "kind": "oracle",
+        "sample": (f"{w.name}: oracle backward (codes, softmax, chain rule in float64) of the "
+                   f"first {n_sub} positions of one KV head group ({G} query heads), {dt:.1f} s, "
+                   f"scaled x{all_pairs / sub_pairs:.0f} by allowed pairs; extrapolated step "
+                   f"{total:.0f} s"),
+        "host_cpu_count": os.cpu_count(),
+    }
+
+
 def _fwd_bytes(w):
     """Compulsory HBM bytes of one forward launch: codes in (int32 + fp32),
     V in (bf16), O out (bf16), LSE out (fp32)."""
@@ -319,6 +433,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3_32k", choices=sorted(si.WORKLOADS))
+    ap.add_argument("--pass", dest="which", default="fwd", choices=["fwd", "bwd"],
+                    help="forward (default, the headline metric) or the backward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 1 GiB device copy twice (reference for "
@@ -335,6 +451,8 @@ def main():
     w = si.workload(args.workload)
     if w.kind == "decode":
         out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline)
+    elif args.which == "bwd":
+        out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
     else:
         out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
     if args.copy_calibration:

@@ -83,10 +83,12 @@ __device__ __forceinline__ float load_f(const void* p, int64_t i, int bf16) {
   return bf16 ? bf16_bits_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
 }
 
-// c += a1 b0 + a0 b1 + a0 b0 (smaller terms first)
+// c += a1 b0 + a0 b1 + a0 b0 (smaller terms first).  A1 / B1 false: that
+// operand is exact in bf16 (its low piece is zero), so its term is skipped.
+template <bool A1 = true, bool B1 = true>
 __device__ __forceinline__ void mfma3(floatx16& c, const bf16x8 (&a)[2], const bf16x8 (&b)[2]) {
-  c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1], b[0], c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[1], c, 0, 0, 0);
+  if constexpr (A1) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1], b[0], c, 0, 0, 0);
+  if constexpr (B1) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[1], c, 0, 0, 0);
   c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[0], c, 0, 0, 0);
 }
 
@@ -230,7 +232,8 @@ __device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, i
 // dq: query-parallel
 // ---------------------------------------------------------------------------
 
-template <int D>
+// VEX / OEX: V / dO are stored in bf16, so their low pieces are zero.
+template <int D, bool VEX, bool OEX>
 __global__ __launch_bounds__(256) void sfa_bwd_dq_kernel(BwdParams p) {
   using I = Img<D>;
   constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
@@ -300,8 +303,8 @@ __global__ __launch_bounds__(256) void sfa_bwd_dq_kernel(BwdParams p) {
         }
         const bf16x8 qq[2] = {qB[0][kb], qB[1][kb]};
         const bf16x8 gg[2] = {dB[0][kb], dB[1][kb]};
-        mfma3(s, a, qq);   // S^T = K~ Q~^T   (keys x queries)
-        mfma3(dp, v, gg);  // dP^T = V dO^T
+        mfma3(s, a, qq);               // S^T = K~ Q~^T   (keys x queries)
+        mfma3<!VEX, !OEX>(dp, v, gg);  // dP^T = V dO^T
       }
       // dS^T = P^T o (dP^T - D); lane = query my_i, register r = key j0 + 8(r/4) + 4hh + r%4
       bf16x8 dsb[2][2];  // [kk][piece]
@@ -351,7 +354,7 @@ __global__ __launch_bounds__(256) void sfa_bwd_dq_kernel(BwdParams p) {
 // dk, dv: key-parallel
 // ---------------------------------------------------------------------------
 
-template <int D>
+template <int D, bool VEX, bool OEX>
 __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
   using I = Img<D>;
   constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
@@ -426,8 +429,8 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
         }
         const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
         const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
-        mfma3(s, a, kk2);   // S = Q~ K~^T   (queries x keys)
-        mfma3(dp, g, vv2);  // dP = dO V^T
+        mfma3(s, a, kk2);                // S = Q~ K~^T   (queries x keys)
+        mfma3<!OEX, !VEX>(dp, g, vv2);   // dP = dO V^T
       }
       // lane = key my_j; register r = query row q0 + 8(r/4) + 4hh + r%4
       bf16x8 pb[2][2], dsb[2][2];  // [kk][piece]
@@ -459,7 +462,7 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           const bf16x8 ao[2] = {tr_load(tro, db * 32 + l32, kbase), tr_load(tro, D + db * 32 + l32, kbase)};
-          mfma3(accv[db], ao, pb[kk]);
+          mfma3<!OEX, true>(accv[db], ao, pb[kk]);
           const bf16x8 aq[2] = {tr_load(trq, db * 32 + l32, kbase), tr_load(trq, D + db * 32 + l32, kbase)};
           mfma3(acck[db], aq, dsb[kk]);
         }
@@ -495,14 +498,15 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
   }
 }
 
-template <int D>
+template <int D, bool VEX, bool OEX>
 hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   using I = Img<D>;
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipSuccess;
     const void* fns[4] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
-                          (const void*)sfa_bwd_dq_kernel<D>, (const void*)sfa_bwd_dkv_kernel<D>};
+                          (const void*)sfa_bwd_dq_kernel<D, VEX, OEX>,
+                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX>};
     const int bytes[4] = {I::QB, I::KB, 2 * I::KB, 2 * I::QB};
     for (int f = 0; f < 4 && e == hipSuccess; ++f)
       if (bytes[f] > 65536) e = hipFuncSetAttribute(fns[f], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[f]);
@@ -514,9 +518,9 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   const dim3 blk(256);
   hipLaunchKernelGGL(sfa_bwd_qprep_kernel<D>, dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
   hipLaunchKernelGGL(sfa_bwd_kprep_kernel<D>, dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
-  hipLaunchKernelGGL(sfa_bwd_dq_kernel<D>, dim3(p.nqb, B * p.Hkv), blk, 2 * I::KB, stream, p);
+  hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX>), dim3(p.nqb, B * p.Hkv), blk, 2 * I::KB, stream, p);
   const int nkb = (p.n + kNW * kT - 1) / (kNW * kT);
-  hipLaunchKernelGGL(sfa_bwd_dkv_kernel<D>, dim3(nkb, B * p.Hkv), blk, 2 * I::QB, stream, p);
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX>), dim3(nkb, B * p.Hkv), blk, 2 * I::QB, stream, p);
   return hipGetLastError();
 }
 
@@ -549,7 +553,12 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
   const size_t qbytes = (size_t)B * Hq * p.nt * (d == 64 ? Img<64>::QB : Img<128>::QB);
   p.qimg = (unsigned char*)ws;
   p.kimg = (unsigned char*)ws + qbytes;
-  return d == 64 ? launch_d<64>(p, B, stream) : launch_d<128>(p, B, stream);
+  if (d == 64) {
+    if (vbf16) return obf16 ? launch_d<64, true, true>(p, B, stream) : launch_d<64, true, false>(p, B, stream);
+    return obf16 ? launch_d<64, false, true>(p, B, stream) : launch_d<64, false, false>(p, B, stream);
+  }
+  if (vbf16) return obf16 ? launch_d<128, true, true>(p, B, stream) : launch_d<128, true, false>(p, B, stream);
+  return obf16 ? launch_d<128, false, true>(p, B, stream) : launch_d<128, false, false>(p, B, stream);
 }
 
 }  // namespace sfa
