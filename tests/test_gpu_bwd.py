@@ -82,3 +82,44 @@ def test_deterministic():
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+def test_qwen3_32k_full_size_sampled():
+    """The 32K GQA workload in the bench's configuration (bf16 V, O and dO):
+    all gradients computed on the GPU; the oracle rebuilds dq for sampled
+    query rows of two heads and dk, dv for sampled keys of one KV head (its
+    forward over all 32768 rows of the four query heads supplies LSE and O)."""
+    w = si.workload("qwen3_32k")
+    B, Hq, Hkv, n, d, k, G = w.B, w.Hq, w.Hkv, w.n, w.d, w.k, w.G
+    q = torch.empty((B, Hq, n, d), device=DEV)
+    kk = torch.empty((B, Hkv, n, d), device=DEV)
+    v = torch.empty((B, Hkv, n, d), device=DEV, dtype=torch.bfloat16)
+    dout = torch.empty((B, Hq, n, d), device=DEV, dtype=torch.bfloat16)
+    for h in range(Hq):
+        q[0, h] = si.normal((n, d), w.seed, "q", 0, h, device=DEV)
+        dout[0, h] = si.normal((n, d), w.seed, "dout", 0, h, device=DEV).to(torch.bfloat16)
+    for h in range(Hkv):
+        kk[0, h] = si.normal((n, d), w.seed, "k", 0, h, device=DEV)
+        v[0, h] = si.normal((n, d), w.seed, "v", 0, h, device=DEV).to(torch.bfloat16)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=w.scale, o_dtype=torch.bfloat16)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=True, scale=w.scale)
+    torch.cuda.synchronize()
+    tol = TOL_GRAD[(True, True)]
+    g = 5  # KV head under test; query heads 20..23 read it
+    oki, okv = oracle.topk_encode(kk[0, g].cpu().numpy(), k)
+    vn, dn = np_vals(v[0, g]), np_vals(dout[0])
+    rng = np.random.default_rng(1)
+    rows = np.unique(np.concatenate([[0, 1, 31, 32, 4095, 16383, n - 1], rng.integers(0, n, 9)]))
+    for h in (G * g, G * g + 3):
+        oqi, oqv = oracle.topk_encode(q[0, h].cpu().numpy(), k)
+        ref = oracle.attn_bwd_rows(oqi, oqv, oki, okv, vn, dn[h], d, w.scale, True, rows)
+        check_grad(dq[0, h, torch.from_numpy(rows).to(DEV)], ref, tol, f"dq_val head {h}")
+    cols = np.unique(np.concatenate([[0, 1, 63, 127, 128, 20000, n - 1], rng.integers(0, n, 9)]))
+    qc = [oracle.topk_encode(q[0, h].cpu().numpy(), k) for h in range(G * g, G * g + G)]
+    gk, gv = oracle.attn_bwd_cols(np.stack([c[0] for c in qc]), np.stack([c[1] for c in qc]),
+                                  oki, okv, vn, dn[G * g:G * g + G], d, w.scale, True, cols)
+    sel = torch.from_numpy(cols).to(DEV)
+    check_grad(dk[0, g, sel], gk, tol, f"dk_val KV head {g}")
+    check_grad(dv[0, g, sel], gv, tol, f"dv KV head {g}")
