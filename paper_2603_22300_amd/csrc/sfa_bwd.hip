@@ -389,13 +389,15 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) { accv[db][r] = 0.f; acck[db][r] = 0.f; }
 
-  // query tiles of all G heads that see some key of the block
+  // Query tiles of all G heads that see some key of the block, swept from
+  // the last tile down, the G heads of a tile together: every workgroup of a
+  // KV head starts on the same tile and moves at the same rate, so the
+  // resident workgroups read each tile image while it is in L2.
   const int t0 = p.causal ? j0b / kT : 0;
-  const int per_head = p.nt - t0;
-  const int total = p.G * per_head;
+  const int total = p.G * (p.nt - t0);
+  auto tile_of = [&](int it) { return p.nt - 1 - it / p.G; };
   auto qimg_of = [&](int it) {
-    const int h = it / per_head, t = t0 + it - h * per_head;
-    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + h) * p.nt + t) * I::QB;
+    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + it % p.G) * p.nt + tile_of(it)) * I::QB;
   };
   if (total > 0) {
     dma(qimg_of(0), smem, I::QB, wave, lane);
@@ -405,9 +407,7 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
   for (int it = 0; it < total; ++it) {
     const int stage = it & 1;
     if (it + 1 < total) dma(qimg_of(it + 1), smem + (stage ^ 1) * I::QB, I::QB, wave, lane);
-    const int h = it / per_head, t = t0 + it - h * per_head;
-    const int q0 = t * kT;
-    (void)h;
+    const int q0 = tile_of(it) * kT;
     if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0)) {
       const unsigned char* Q = smem + stage * I::QB;
       const uint16_t* rmq = (const uint16_t*)(Q + I::Q_RMQ);
