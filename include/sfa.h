@@ -180,7 +180,7 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
  * into two bfloat16 pieces and three piece products kept (relative error
  * ~2^-16 of the sum of |terms|), float32 accumulation; P recomputed as
  * exp2(s log2(e) - LSE log2(e)) in float32.
- * Limits: as sfa_attn_fwd, plus Hq / Hkv a power of two <= 4.
+ * Limits: as sfa_attn_fwd, plus Hq / Hkv a power of two <= 8.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC, SFA_EHIP.
  */
 sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val,

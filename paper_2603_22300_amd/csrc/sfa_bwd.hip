@@ -32,7 +32,8 @@ namespace sfa {
 namespace {
 
 constexpr int kT = 32;         // rows (queries or keys) per tile image
-constexpr int kNW = 4;         // wavefronts per workgroup (one per SIMD)
+constexpr int kNW = 8;         // dk, dv: wavefronts per workgroup (two per SIMD)
+constexpr int kNWQ = 8;        // dq: wavefronts per workgroup (two per SIMD)
 constexpr int kTP = kT + 4;    // bf16 pitch of a transposed row: 72 B, conflict-free 8-byte reads
 constexpr float kLog2e = 1.44269504088896340736f;
 
@@ -41,10 +42,15 @@ struct Img {
   static constexpr int RP = 2 * D + 8;                 // bf16 pitch of a row-major row: [piece][col]
   static constexpr int RMB = kT * RP * 2;              // row-major array bytes
   static constexpr int TRB = 2 * D * kTP * 2;          // transposed array bytes: [piece][col][row]
-  // query image: Q~ rm | Q~ tr | dO rm | dO tr | L2[32] | D[32]
-  static constexpr int Q_RMQ = 0, Q_TRQ = RMB, Q_RMO = RMB + TRB, Q_TRO = 2 * RMB + TRB;
-  static constexpr int Q_L2 = 2 * RMB + 2 * TRB, Q_D = Q_L2 + kT * 4;
-  static constexpr int QB = (Q_D + kT * 4 + 1023) / 1024 * 1024;
+  // query image: dO tr | Q~ rm | L2[32] | D[32] | Q~ tr | dO rm, ordered so
+  // that the dV kernel's part (dO tr, Q~ rm, L2) and the dK kernel's part
+  // (Q~ rm .. dO rm) are each one contiguous range of whole 1 KB blocks
+  static constexpr int Q_TRO = 0, Q_RMQ = TRB, Q_L2 = TRB + RMB, Q_D = Q_L2 + kT * 4;
+  static constexpr int Q_TRQ = Q_D + kT * 4, Q_RMO = Q_TRQ + TRB;
+  static constexpr int QB = (Q_RMO + RMB + 1023) / 1024 * 1024;
+  static constexpr int DV_OFF = 0, DV_LEN = (Q_D + 1023) / 1024 * 1024;
+  static constexpr int DK_OFF = Q_RMQ, DK_LEN = QB - Q_RMQ;
+  static_assert(Q_RMQ % 1024 == 0, "the dK range starts on a 1 KB block");
   // key image: K~ rm | K~ tr | V rm
   static constexpr int K_RMK = 0, K_TRK = RMB, K_RMV = RMB + TRB;
   static constexpr int KB = (2 * RMB + TRB + 1023) / 1024 * 1024;
@@ -68,7 +74,7 @@ struct BwdParams {
   int Hq, Hkv, G, n, k, causal;
   int idx16, valbf16, vbf16, obf16;
   int nt;    // tiles per head: ceil(n / 32)
-  int BR;    // query positions per dq workgroup: 128 / G
+  int BR;    // query positions per dq workgroup: 256 / G
   int nqb;   // dq workgroups per (batch, KV head)
   float scale, c;  // c = scale * log2(e)
 };
@@ -94,15 +100,27 @@ __device__ __forceinline__ void mfma3(floatx16& c, const bf16x8 (&a)[2], const b
 
 // Copy `bytes` (a multiple of 1 KB) global -> LDS, whole-wave 16-byte
 // direct-to-LDS loads spread over the workgroup's waves.
+template <int NW>
 __device__ __forceinline__ void dma(const unsigned char* src, unsigned char* dst, int bytes, int wave,
                                     int lane) {
-  for (int i = wave; i < bytes / 1024; i += kNW)
+  for (int i = wave; i < bytes / 1024; i += NW)
     __builtin_amdgcn_global_load_lds(src + i * 1024 + lane * 16,
                                      (__attribute__((address_space(3))) void*)(dst + i * 1024), 16,
                                      0, 0);
 }
 
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
+
+constexpr int kQS = 3;  // query-image stages of the key-parallel kernels
+
+// vmcnt(N): at most N of this wave's loads outstanding.  Loads retire in issue
+// order, so with N no larger than the number of copies this wave issued for
+// the most recent image, every earlier image is complete.
+template <int N>
+__device__ __forceinline__ void wait_vm_n() {
+  static_assert(N >= 0 && N < 16, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt(0x0f70 | N);
+}
 
 // A-operand slice of a transposed array: row `row` (a coordinate / dimension),
 // columns kbase + 0..3 and kbase + 8..11 (the key / query order of the MFMA
@@ -234,7 +252,7 @@ __device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, i
 
 // VEX / OEX: V / dO are stored in bf16, so their low pieces are zero.
 template <int D, bool VEX, bool OEX>
-__global__ __launch_bounds__(256) void sfa_bwd_dq_kernel(BwdParams p) {
+__global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
   using I = Img<D>;
   constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -278,15 +296,18 @@ __global__ __launch_bounds__(256) void sfa_bwd_dq_kernel(BwdParams p) {
   const int blk_last = min(n, i0 + p.BR) - 1;
   const int nkt = ((p.causal ? blk_last + 1 : n) + kT - 1) / kT;
   const unsigned char* kimg0 = p.kimg + (int64_t)bh * p.nt * I::KB;
-  dma(kimg0, smem, I::KB, wave, lane);
+  dma<kNWQ>(kimg0, smem, I::KB, wave, lane);
   wait_vm();
   __syncthreads();
   for (int jt = 0; jt < nkt; ++jt) {
     const int stage = jt & 1;
-    if (jt + 1 < nkt) dma(kimg0 + (int64_t)(jt + 1) * I::KB, smem + (stage ^ 1) * I::KB, I::KB, wave, lane);
+    // reads through `cur`, the copy of the next tile through `nxt` (restrict:
+    // no compiler wait on the copy before the reads)
+    auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
+    if (jt + 1 < nkt) dma<kNWQ>(kimg0 + (int64_t)(jt + 1) * I::KB, nxt, I::KB, wave, lane);
     const int j0 = jt * kT;
     if (wave_ok && (!p.causal || wave_i_max >= j0)) {
-      const unsigned char* K = smem + stage * I::KB;
+      const unsigned char* K = cur;
       const uint16_t* rmk = (const uint16_t*)(K + I::K_RMK);
       const uint16_t* trk = (const uint16_t*)(K + I::K_TRK);
       const uint16_t* rmv = (const uint16_t*)(K + I::K_RMV);
@@ -329,33 +350,47 @@ __global__ __launch_bounds__(256) void sfa_bwd_dq_kernel(BwdParams p) {
         }
       }
     }
+    };
+    tile(smem + stage * I::KB, smem + (stage ^ 1) * I::KB);
     wait_vm();
     __syncthreads();
   }
 
   // dq_val = scale * dQ~ at the row's support: stage dQ~ through LDS
-  // (the key stages are free now): [wave][query][coordinate], pitch D + 4.
-  float* L = (float*)smem + wave * kT * (D + 4);
+  // (the key stages are free now), four waves at a time:
+  // [wave % 4][query][coordinate], pitch D + 4.
+  float* L = (float*)smem + (wave & 3) * kT * (D + 4);
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int round = 0; round < kNWQ / 4; ++round) {
+    if (wave / 4 == round) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
-  __syncthreads();
-  if (row_ok) {
-    const int64_t row = ((int64_t)b * p.Hq + hq) * n + my_i;
-    for (int t = hh; t < p.k; t += 2) {
-      const int u = load_idx(p.q_idx, row * p.k + t, p.idx16, D - 1);
-      p.dq[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
     }
+    __syncthreads();
+    if (wave / 4 == round && row_ok) {
+      const int64_t row = ((int64_t)b * p.Hq + hq) * n + my_i;
+      for (int t = hh; t < p.k; t += 2) {
+        const int u = load_idx(p.q_idx, row * p.k + t, p.idx16, D - 1);
+        p.dq[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+      }
+    }
+    __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// dk, dv: key-parallel
+// dk, dv: key-parallel, one kernel each
 // ---------------------------------------------------------------------------
+// PART kDV: S, P, dV^T += dO^T P.   PART kDK: S, dP, dS, dK~^T += Q~^T dS.
+// Split in two so that each fits two wavefronts per SIMD (256 VGPRs); both
+// recompute S.
+constexpr int kDV = 0, kDK = 1;
 
-template <int D, bool VEX, bool OEX>
-__global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
+template <int D, bool VEX, bool OEX, int PART>
+__global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   using I = Img<D>;
   constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -373,7 +408,7 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
   if (wave_ok) {
     const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
     load_rows_b<D>(kimg, I::K_RMK, l32, hh, kB);
-    load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
+    if constexpr (PART == kDK) load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
   } else {
 #pragma unroll
     for (int pc = 0; pc < 2; ++pc)
@@ -383,11 +418,11 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
         vB[pc][kb] = bf16x8{};
       }
   }
-  floatx16 accv[NDB], acck[NDB];
+  floatx16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) { accv[db][r] = 0.f; acck[db][r] = 0.f; }
+    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
   // Query tiles of all G heads that see some key of the block, swept from
   // the last tile down, the G heads of a tile together: every workgroup of a
@@ -396,20 +431,30 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
   const int t0 = p.causal ? j0b / kT : 0;
   const int total = p.G * (p.nt - t0);
   auto tile_of = [&](int it) { return p.nt - 1 - it / p.G; };
+  // only this kernel's part of each image is copied; LDS holds it from
+  // image offset ROFF on
+  constexpr int ROFF = PART == kDV ? I::DV_OFF : I::DK_OFF;
+  constexpr int RLEN = PART == kDV ? I::DV_LEN : I::DK_LEN;
   auto qimg_of = [&](int it) {
-    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + it % p.G) * p.nt + tile_of(it)) * I::QB;
+    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + it % p.G) * p.nt + tile_of(it)) * I::QB + ROFF;
   };
-  if (total > 0) {
-    dma(qimg_of(0), smem, I::QB, wave, lane);
-    wait_vm();
-  }
+  // three stages: the image two tiles ahead is in flight while a tile is
+  // consumed (vmcnt waits only for the one needed next)
+  // every wave copies at least RLEN / 1024 / kNW blocks of an image
+  constexpr int kMinCopies = RLEN / 1024 / kNW;
+  if (total > 0) dma<kNW>(qimg_of(0), smem, RLEN, wave, lane);
+  if (total > 1) dma<kNW>(qimg_of(1), smem + RLEN, RLEN, wave, lane);
+  if (total > 1) wait_vm_n<kMinCopies>(); else wait_vm();
   __syncthreads();
   for (int it = 0; it < total; ++it) {
-    const int stage = it & 1;
-    if (it + 1 < total) dma(qimg_of(it + 1), smem + (stage ^ 1) * I::QB, I::QB, wave, lane);
+    // The tile's LDS reads go through `cur` and the copy two tiles ahead
+    // through `nxt`, both restrict: the compiler then knows the copy cannot
+    // alias those reads and does not wait for it before them.
+    auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
+    if (it + 2 < total) dma<kNW>(qimg_of(it + 2), nxt, RLEN, wave, lane);
     const int q0 = tile_of(it) * kT;
     if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0)) {
-      const unsigned char* Q = smem + stage * I::QB;
+      const unsigned char* Q = cur - ROFF;  // image offsets apply as is
       const uint16_t* rmq = (const uint16_t*)(Q + I::Q_RMQ);
       const uint16_t* trq = (const uint16_t*)(Q + I::Q_TRQ);
       const uint16_t* rmo = (const uint16_t*)(Q + I::Q_RMO);
@@ -421,79 +466,96 @@ __global__ __launch_bounds__(256) void sfa_bwd_dkv_kernel(BwdParams p) {
       for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
-        bf16x8 a[2], g[2];
+        bf16x8 a[2];
 #pragma unroll
-        for (int pc = 0; pc < 2; ++pc) {
-          a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
-          g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
-        }
+        for (int pc = 0; pc < 2; ++pc) a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
         const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
-        const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
-        mfma3(s, a, kk2);                // S = Q~ K~^T   (queries x keys)
-        mfma3<!OEX, !VEX>(dp, g, vv2);   // dP = dO V^T
+        mfma3(s, a, kk2);  // S = Q~ K~^T   (queries x keys)
+        if constexpr (PART == kDK) {
+          bf16x8 g[2];
+#pragma unroll
+          for (int pc = 0; pc < 2; ++pc) g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
+          mfma3<!OEX, !VEX>(dp, g, vv2);  // dP = dO V^T
+        }
       }
       // lane = key my_j; register r = query row q0 + 8(r/4) + 4hh + r%4
-      bf16x8 pb[2][2], dsb[2][2];  // [kk][piece]
+      bf16x8 xb[2][2];  // [kk][piece]: P (dV) or dS (dK)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
-        const float4 d4 = *(const float4*)(dd + 8 * g4 + 4 * hh);
         const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+        float dv4[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (PART == kDK) {
+          const float4 d4 = *(const float4*)(dd + 8 * g4 + 4 * hh);
+          dv4[0] = d4.x; dv4[1] = d4.y; dv4[2] = d4.z; dv4[3] = d4.w;
+        }
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
           const int r = 4 * g4 + x;
           const int i = q0 + 8 * g4 + 4 * hh + x;
           const bool ok = key_ok && (!p.causal || i >= my_j);
           const float pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x])) : 0.f;
-          uint16_t h1, l1, h2, l2b;
-          split2(pr, h1, l1);
-          split2(pr * (dp[r] - dv4[x]), h2, l2b);
-          pb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h1);
-          pb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l1);
-          dsb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h2);
-          dsb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l2b);
+          const float val = PART == kDV ? pr : pr * (dp[r] - dv4[x]);
+          uint16_t h, l;
+          split2(val, h, l);
+          xb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h);
+          xb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l);
         }
       }
-      // dV^T += dO^T P,  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
+      // dV^T += dO^T P  or  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
+      const uint16_t* tra = PART == kDV ? tro : trq;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         const int kbase = 16 * kk + 4 * hh;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const bf16x8 ao[2] = {tr_load(tro, db * 32 + l32, kbase), tr_load(tro, D + db * 32 + l32, kbase)};
-          mfma3<!OEX, true>(accv[db], ao, pb[kk]);
-          const bf16x8 aq[2] = {tr_load(trq, db * 32 + l32, kbase), tr_load(trq, D + db * 32 + l32, kbase)};
-          mfma3(acck[db], aq, dsb[kk]);
+          const bf16x8 at[2] = {tr_load(tra, db * 32 + l32, kbase), tr_load(tra, D + db * 32 + l32, kbase)};
+          if constexpr (PART == kDV) mfma3<!OEX, true>(acc[db], at, xb[kk]);
+          else mfma3(acc[db], at, xb[kk]);
         }
       }
     }
-    wait_vm();
+    };
+    tile(smem + (it % kQS) * RLEN, smem + ((it + 2) % kQS) * RLEN);
+    // the next tile's copies must be complete; the one after may still run
+    if (it + 2 < total) wait_vm_n<kMinCopies>(); else wait_vm();
     __syncthreads();
   }
 
-  // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
-  if (key_ok) {
-    float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
+  if constexpr (PART == kDV) {
+    // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
+    if (key_ok) {
+      float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4)
-        *(float4*)(dvr + db * 32 + 8 * g4 + 4 * hh) =
-            make_float4(accv[db][4 * g4], accv[db][4 * g4 + 1], accv[db][4 * g4 + 2], accv[db][4 * g4 + 3]);
-  }
-  // dk_val = scale * dK~ at the key's support, through LDS
-  float* L = (float*)smem + wave * kT * (D + 4);
+        for (int g4 = 0; g4 < 4; ++g4)
+          *(float4*)(dvr + db * 32 + 8 * g4 + 4 * hh) =
+              make_float4(acc[db][4 * g4], acc[db][4 * g4 + 1], acc[db][4 * g4 + 2], acc[db][4 * g4 + 3]);
+    }
+  } else {
+    // dk_val = scale * dK~ at the key's support, through LDS, four waves at
+    // a time: [wave % 4][key][coordinate], pitch D + 4
+    float* L = (float*)smem + (wave & 3) * kT * (D + 4);
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+    for (int round = 0; round < kNW / 4; ++round) {
+      if (wave / 4 == round) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acck[db][r];
-  __syncthreads();
-  if (key_ok) {
-    const int64_t row = (int64_t)bh * n + my_j;
-    for (int t = hh; t < p.k; t += 2) {
-      const int u = load_idx(p.k_idx, row * p.k + t, p.idx16, D - 1);
-      p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
+      }
+      __syncthreads();
+      if (wave / 4 == round && key_ok) {
+        const int64_t row = (int64_t)bh * n + my_j;
+        for (int t = hh; t < p.k; t += 2) {
+          const int u = load_idx(p.k_idx, row * p.k + t, p.idx16, D - 1);
+          p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+        }
+      }
+      __syncthreads();
     }
   }
 }
@@ -504,29 +566,37 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipSuccess;
-    const void* fns[4] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
+    const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
                           (const void*)sfa_bwd_dq_kernel<D, VEX, OEX>,
-                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX>};
-    const int bytes[4] = {I::QB, I::KB, 2 * I::KB, 2 * I::QB};
-    for (int f = 0; f < 4 && e == hipSuccess; ++f)
+                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, kDV>,
+                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, kDK>};
+    const int bytes[5] = {I::QB, I::KB, 2 * I::KB, kQS * I::DV_LEN, kQS * I::DK_LEN};
+    for (int f = 0; f < 5 && e == hipSuccess; ++f)
       if (bytes[f] > 65536) e = hipFuncSetAttribute(fns[f], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[f]);
     if (e != hipSuccess) return e;
     configured = true;
   }
-  static_assert(2 * I::KB >= kNW * kT * (D + 4) * 4, "dq gather fits the stages");
-  static_assert(2 * I::QB >= kNW * kT * (D + 4) * 4, "dk gather fits the stages");
+  static_assert(2 * I::KB >= 4 * kT * (D + 4) * 4, "dq gather (four waves at a time) fits the stages");
+  static_assert(kQS * I::DK_LEN >= 4 * kT * (D + 4) * 4, "dk gather (four waves at a time) fits the stages");
+  static_assert(kQS * I::DK_LEN <= 160 * 1024 - 512, "three dK stages fit LDS");
+  static_assert(I::DV_LEN / 1024 / kNW >= 1 && I::DK_LEN / 1024 / kNW >= 1, "each wave copies part of each image");
   const dim3 blk(256);
   hipLaunchKernelGGL(sfa_bwd_qprep_kernel<D>, dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
   hipLaunchKernelGGL(sfa_bwd_kprep_kernel<D>, dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
-  hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX>), dim3(p.nqb, B * p.Hkv), blk, 2 * I::KB, stream, p);
+  hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX>), dim3(p.nqb, B * p.Hkv), dim3(kNWQ * 64),
+                     2 * I::KB, stream, p);
   const int nkb = (p.n + kNW * kT - 1) / (kNW * kT);
-  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX>), dim3(nkb, B * p.Hkv), blk, 2 * I::QB, stream, p);
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, kDV>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
+                     kQS * I::DV_LEN, stream, p);
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, kDK>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
+                     kQS * I::DK_LEN, stream, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int bwd_max_group() { return (kNW * kT) / kT; }
+// a dq wave's 32 rows must be one query head: G <= 8 (and <= 4 would do for dk/dv)
+int bwd_max_group() { return kNWQ; }
 
 size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d) {
   const size_t nt = (size_t)((n + kT - 1) / kT);
@@ -546,7 +616,7 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
   p.Hq = Hq; p.Hkv = Hkv; p.G = Hq / Hkv; p.n = n; p.k = k; p.causal = causal;
   p.idx16 = idx16; p.valbf16 = valbf16; p.vbf16 = vbf16; p.obf16 = obf16;
   p.nt = (n + kT - 1) / kT;
-  p.BR = kNW * kT / p.G;
+  p.BR = kNWQ * kT / p.G;
   p.nqb = (n + p.BR - 1) / p.BR;
   p.scale = scale;
   p.c = (float)((double)scale * 1.4426950408889634);

@@ -139,5 +139,5 @@ def test_bwd_validation_and_workspace(L):
     assert _bwd(L, dq=None) == 1
     assert _bwd(L, k=0) == 1
     assert _bwd(L, Hq=3, Hkv=2) == 1
-    assert _bwd(L, Hq=16, Hkv=2) == 2      # group of 8 heads: not supported by the backward
+    assert _bwd(L, Hq=32, Hkv=2) == 2      # group of 16 heads: not supported by the backward
     assert _bwd(L, d=96, k=8) == 2
