@@ -7,4 +7,5 @@ from .sfa_oracle import (  # noqa: F401
     widen, topk_select, topk_encode, bf16_rne, topk_encode_bf16, densify,
     softmax_attention, attn_fwd, attn_fwd_rows, attn_decode, overlap_count,
     csr_bytes, softmax_attention_grad, attn_bwd, attn_bwd_rows, attn_bwd_cols,
+    cache_location, cache_capacity, kv_append, cache_gather, attn_decode_paged,
 )

@@ -22,6 +22,10 @@ out in float64 with numpy:
 * LSE_i = m_i + ln(l_i), natural log (the paper does not define it; this is
   the standard log-sum-exp of the row's scaled scores).
 * Decode (App. B, KV-cache latency): one query row against all cached keys.
+* KV-cache maintenance: coded keys and their values appended at a
+  sequence's next positions, in a contiguous or paged cache (a block table
+  maps each run of page_size positions of a sequence to a page of the
+  pool), and decode reading each position through that map.
 * Backward with the straight-through estimator (Sec. 3.1, Eq. (6)): the
   chain rule of softmax attention on the densified codes, with the gradient
   of a query or key coordinate equal to that of its code value on the
@@ -215,6 +219,108 @@ def attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, d: int, scale: float, seq
                 qd = densify(np.asarray(q_idx)[b, h][None], np.asarray(q_val)[b, h][None], d)
                 O1, L1 = softmax_attention(qd, kd, vv, scale, causal=False)
                 O[b, h], L[b, h] = O1[0], L1[0]
+    return O, L
+
+
+# --------------------------------------------------------------------------
+# KV-cache maintenance (App. B: decode against a cache of sparse key codes
+# and dense V that grows by one coded key per generated token)
+# --------------------------------------------------------------------------
+
+
+def cache_location(block_table, page_size, b: int, j: int):
+    """(page, slot) that holds position j of sequence b.
+
+    Paged cache: arrays [num_pages, Hkv, page_size, ...]; position j of
+    sequence b sits in page block_table[b][j // page_size] at slot
+    j % page_size.  block_table None is the contiguous cache
+    [B, Hkv, Lmax, ...]: page b, slot j."""
+    if block_table is None:
+        return b, j
+    return int(np.asarray(block_table)[b][j // page_size]), j % page_size
+
+
+def cache_capacity(kc_idx, block_table, page_size) -> int:
+    """Positions a sequence can hold: Lmax, or max_pages * page_size."""
+    if block_table is None:
+        return int(np.shape(kc_idx)[2])
+    return int(np.shape(block_table)[1]) * int(page_size)
+
+
+def kv_append(kc_idx, kc_val, v_cache, k_new, v_new, seq_len, k: int, block_table=None,
+              page_size=None, n_new=None):
+    """Append coded keys and their values to a KV cache, in place.
+
+    For each sequence b and t < n_new[b] (all T when n_new is None), the key
+    row k_new[b, h, t] (float32, d wide) is coded by Top-k (Sec. 3.1): kept
+    coordinates ascending, values stored as bf16 bits when kc_val holds
+    uint16, else as float32 copies.  Code and value row v_new[b, h, t] go to
+    position seq_len[b] + t of sequence b in every KV head h; a bf16 V cache
+    stores bf16_rne of float32 values, a float32 one widens bf16 bits
+    exactly.  Positions at or past the capacity, and pages outside the pool,
+    are not written.  Returns the new lengths, min(seq_len + n_new,
+    capacity)."""
+    k_new = np.asarray(k_new, dtype=np.float32)
+    B, Hkv, T, _ = k_new.shape
+    cap = cache_capacity(kc_idx, block_table, page_size)
+    npages = np.shape(kc_idx)[0]
+    lens = np.asarray(seq_len).astype(np.int64)
+    cnt = np.full(B, T) if n_new is None else np.clip(np.asarray(n_new), 0, T)
+    bf16_codes = np.asarray(kc_val).dtype == np.uint16
+    v_new = np.asarray(v_new)
+    for b in range(B):
+        for t in range(int(cnt[b])):
+            j = int(lens[b]) + t
+            if j >= cap:
+                break
+            page, slot = cache_location(block_table, page_size, b, j)
+            if not 0 <= page < npages:
+                continue
+            for h in range(Hkv):
+                if bf16_codes:
+                    ci, cv = topk_encode_bf16(k_new[b, h, t], k)
+                else:
+                    ci, cv = topk_encode(k_new[b, h, t], k)
+                kc_idx[page, h, slot] = ci
+                kc_val[page, h, slot] = cv
+                row = v_new[b, h, t]
+                if v_cache.dtype == np.uint16:
+                    v_cache[page, h, slot] = row if row.dtype == np.uint16 else bf16_rne(row)
+                else:
+                    v_cache[page, h, slot] = widen(row).astype(v_cache.dtype)
+    return np.minimum(lens + cnt, cap)
+
+
+def cache_gather(kc_idx, kc_val, v_cache, b: int, L: int, block_table=None, page_size=None):
+    """Contiguous copies [Hkv, L, ...] of positions 0..L-1 of sequence b."""
+    Hkv = np.shape(kc_idx)[1]
+    gi = np.empty((Hkv, L) + np.shape(kc_idx)[3:], dtype=np.asarray(kc_idx).dtype)
+    gv = np.empty((Hkv, L) + np.shape(kc_val)[3:], dtype=np.asarray(kc_val).dtype)
+    gvv = np.empty((Hkv, L) + np.shape(v_cache)[3:], dtype=np.asarray(v_cache).dtype)
+    for j in range(L):
+        page, slot = cache_location(block_table, page_size, b, j)
+        gi[:, j] = kc_idx[page, :, slot]
+        gv[:, j] = kc_val[page, :, slot]
+        gvv[:, j] = v_cache[page, :, slot]
+    return gi, gv, gvv
+
+
+def attn_decode_paged(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, d: int, scale: float,
+                      block_table=None, page_size=None):
+    """Decode (App. B) over a paged cache: each sequence's first seq_len[b]
+    positions, read through its block table, then the plain decode."""
+    B, Hq, _ = np.shape(q_idx)
+    dv = np.shape(v_cache)[-1]
+    O = np.zeros((B, Hq, dv))
+    L = np.full((B, Hq), -np.inf)
+    for b in range(B):
+        Lb = int(seq_len[b])
+        if Lb == 0:
+            continue
+        gi, gv, gvv = cache_gather(kc_idx, kc_val, v_cache, b, Lb, block_table, page_size)
+        Ob, Lsb = attn_decode(np.asarray(q_idx)[b:b + 1], np.asarray(q_val)[b:b + 1],
+                              gi[None], gv[None], gvv[None], d, scale)
+        O[b], L[b] = Ob[0], Lsb[0]
     return O, L
 
 
