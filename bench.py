@@ -8,7 +8,10 @@ output.  One step = Top-k coding of the dense fp32 Q and K
 already resident in HBM.  `--workload decode_64k` times the decode step
 (sfa_attn_decode) over the 64-sequence x 64K sparse-code KV cache instead, and
 `--pass bwd` the backward with the straight-through estimator (sfa_attn_bwd on
-the workload's codes, forward O / LSE and a seeded dO).
+the workload's codes, forward O / LSE and a seeded dO).  `--workload
+decode_64k --cache paged` times a serving step over a paged cache: append of
+the new token (sfa_kv_append) + decode of the dense query
+(sfa_attn_decode_paged), after filling the cache by appends.
 
 Prints ONE JSON line.  Besides the contract fields it carries
   roofline      the dominant kernel's algorithmic rate (from HIP events
@@ -427,6 +430,98 @@ def bench_decode(w, steps, warmup, want_cpu):
     return out
 
 
+def bench_decode_paged(w, steps, warmup):
+    """Serving step over a paged cache: append each sequence's new key (coded on
+    append) and value, then decode the new dense query (coded inside the decode
+    kernel) over the grown cache.  The cache is first filled by sfa_kv_append,
+    one 64K-token prefill per sequence, which is timed as the append rate."""
+    B, Hq, Hkv, L, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
+    P = 256
+    if warmup + steps > P:
+        raise SystemExit("--cache paged grows each sequence by one token per step: "
+                         f"warmup + steps must be <= {P}")
+    max_pages = L // P + 1  # one spare page per sequence for the generated tokens
+    num_pages = B * max_pages
+    g = torch.Generator(device="cpu")
+    g.manual_seed(si.slice_seed(w.seed, "block_table"))
+    table = torch.randperm(num_pages, generator=g).reshape(B, max_pages).to(torch.int32).to(DEV)
+    ci = torch.empty((num_pages, Hkv, P, kk), dtype=torch.int16, device=DEV)
+    cv = torch.empty((num_pages, Hkv, P, kk), dtype=torch.bfloat16, device=DEV)
+    vc = torch.empty((num_pages, Hkv, P, d), dtype=torch.bfloat16, device=DEV)
+    lens = torch.zeros(B, dtype=torch.int32, device=DEV)
+    kb = torch.empty((1, Hkv, L, d), device=DEV)
+    vb = torch.empty((1, Hkv, L, d), device=DEV, dtype=torch.bfloat16)
+    app_ms = 0.0
+    for b in range(B):
+        for h in range(Hkv):
+            kb[0, h] = si.normal((L, d), w.seed, "k", b, h, device=DEV)
+            vb[0, h] = si.normal((L, d), w.seed, "v", b, h, device=DEV).to(torch.bfloat16)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        sfa.sfa_kv_append(kb, vb, lens[b:b + 1], ci, cv, vc, k=kk, block_table=table[b:b + 1])
+        e1.record()
+        torch.cuda.synchronize()
+        if b > 0:  # the first call pays the module load
+            app_ms += e0.elapsed_time(e1)
+    del kb, vb
+    app_bytes = Hkv * L * (d * 4 + d * 2 + kk * 4 + d * 2)  # per prefill call
+    app_rate = app_bytes / (app_ms / (B - 1) * 1e-3)
+    # per-step inputs: one new token per sequence, the new dense queries
+    kn = si.normal((B, Hkv, 1, d), w.seed, "k_step", device=DEV)
+    vn = si.normal((B, Hkv, 1, d), w.seed, "v_step", device=DEV).to(torch.bfloat16)
+    qd = si.normal((B, Hq, d), w.seed, "q", device=DEV)
+    o = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=DEV)
+    ws = torch.empty(sfa.sfa_attn_decode_workspace(B, Hq, max_pages * P, d), dtype=torch.uint8,
+                     device=DEV)
+
+    def step(ev=None):
+        sfa.sfa_kv_append(kn, vn, lens, ci, cv, vc, k=kk, block_table=table)
+        if ev is not None:
+            ev[0].record()
+        sfa.sfa_attn_decode_paged(ci, cv, vc, table, seq_len=lens, q=qd, scale=w.scale, o=o,
+                                  lse=lse, ws=ws)
+        if ev is not None:
+            ev[1].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for s_ in range(steps):
+        step(evs[s_])
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    dec_ms = sum(a.elapsed_time(b) for a, b in evs) / steps
+    ctx = L + warmup + (steps + 1) / 2.0  # mean context length over the timed steps
+    dec_bytes = B * Hkv * ctx * (kk * 4 + d * 2) + B * Hq * (d * 4 + d * 2 + 4)
+    achieved = dec_bytes / (dec_ms * 1e-3)
+    return {
+        "metric": "SFA decode tokens/s, 64 seqs x 64K sparse-code cache (k=16 int16/bf16, d=128), 32/8 heads",
+        "value": B / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name + "_paged", "B": B, "Hq": Hq, "Hkv": Hkv, "L": L, "d": d,
+                   "k": kk, "page_size": P,
+                   "step": "sfa_kv_append (new token) + sfa_attn_decode_paged (dense query "
+                           "coded in-kernel, split context + LSE merge)"},
+        "roofline": {"kernel": "sfa_decode_kernel (paged) + combine", "bound": "hbm",
+                     "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM, "traffic": None,
+                     "algorithmic_bytes_per_launch": dec_bytes, "ms_per_launch": dec_ms},
+        "append_prefill": {"kernel": "sfa_kv_append_kernel", "tokens_per_call": L,
+                           "ms_per_call": app_ms / (B - 1), "bytes_per_call": app_bytes,
+                           "achieved_GBps": app_rate / 1e9, "frac": app_rate / PEAK_HBM},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -435,6 +530,9 @@ def main():
     ap.add_argument("--workload", default="qwen3_32k", choices=sorted(si.WORKLOADS))
     ap.add_argument("--pass", dest="which", default="fwd", choices=["fwd", "bwd"],
                     help="forward (default, the headline metric) or the backward")
+    ap.add_argument("--cache", default="contiguous", choices=["contiguous", "paged"],
+                    help="decode workloads: contiguous cache (decode only) or paged cache "
+                         "(append of the new token + decode with in-kernel query coding)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 1 GiB device copy twice (reference for "
@@ -449,7 +547,9 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     w = si.workload(args.workload)
-    if w.kind == "decode":
+    if w.kind == "decode" and args.cache == "paged":
+        out = bench_decode_paged(w, args.steps, args.warmup)
+    elif w.kind == "decode":
         out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline)
     elif args.which == "bwd":
         out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline)

@@ -9,7 +9,8 @@
  *   - Masked softmax and value aggregation: Sec. 2, Eqs. (1)-(2);
  *     the tiled kernel's result equals softmax(Q~ K~^T / sqrt(d)) V: Sec. 3.2.
  *   - Decode against a cache of sparse key codes and dense V: App. B
- *     ("KV-cache latency") and App. J (code storage).
+ *     ("KV-cache latency") and App. J (code storage); appending coded keys
+ *     to a contiguous or paged cache, and decode through its block table.
  *
  * Conventions shared by every entry point
  *   - All array pointers are DEVICE pointers to dense, row-major, contiguous
@@ -233,6 +234,84 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val,
                            int v_t, int o_t,
                            void* o, float* lse,
                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * KV-cache maintenance for decode (App. B: generation extends the cache by
+ * one coded key and its value per token; App. J: keys are stored as codes).
+ *
+ * Paged cache.  A pool of num_pages pages, each holding page_size
+ * consecutive positions of one sequence for all Hkv heads:
+ *     kc_idx, kc_val  [num_pages, Hkv, page_size, k]
+ *     v_cache         [num_pages, Hkv, page_size, d]
+ * block_table [B, max_pages] int32 on the device: position j of sequence b
+ * lives in page block_table[b * max_pages + j / page_size] at slot
+ * j % page_size.  A sequence holds at most max_pages * page_size positions.
+ * The caller owns the pool and the table and decides which pages a sequence
+ * gets; pages shared by two sequences must not be appended to by both.
+ */
+
+/*
+ * Append new tokens to a contiguous or paged cache (Top-k coding of the keys,
+ * Sec. 3.1, Eqs. (3)-(4), fused with the cache write).
+ *
+ * k_new    [B, Hkv, T, d] float32 dense keys; coded like sfa_topk_encode
+ *          (k coordinates of largest |x|, ties to the lower index, ascending)
+ *          into kc_idx_t (SFA_I16 | SFA_I32) / kc_val_t (SFA_BF16: round to
+ *          nearest even | SFA_F32: bit copy).
+ * v_new    [B, Hkv, T, d] values (v_new_t), stored as v_t (float32 to bf16
+ *          rounds to nearest even; bf16 to float32 is exact).
+ * n_new    [B] int32 on the device, tokens of sequence b to append (clamped
+ *          into [0, T]); NULL means T for every sequence.
+ * seq_len  [B] int32 on the device, in/out: on entry each sequence's length,
+ *          which is the position of its first new token; on return (in
+ *          stream order) min(length + appended, capacity).
+ * block_table, max_pages, page_size, num_pages: the paged layout above
+ *          (page_size a power of two); with block_table NULL the cache is
+ *          contiguous [B, Hkv, page_size, ...] (page_size = Lmax, any value;
+ *          max_pages and num_pages ignored).
+ * Tokens whose position reaches the capacity, or whose page id lies outside
+ * [0, num_pages), are not written.  With T == 0 only the clamping of seq_len
+ * into [0, capacity] happens.
+ * Limits: 1 <= d <= 256; 1 <= k <= d; B * Hkv * T <= 2^31;
+ *         max_pages * page_size <= 2^30.
+ * Errors: SFA_EINVAL, SFA_ENOTSUP (d > 256), SFA_EHIP.
+ */
+sfa_status sfa_kv_append(const float* k_new, const void* v_new, const int32_t* n_new,
+                         int32_t* seq_len, int B, int Hkv, int T, int d, int k,
+                         const int32_t* block_table, int max_pages, int page_size,
+                         int num_pages, void* kc_idx, void* kc_val, void* v_cache,
+                         int kc_idx_t, int kc_val_t, int v_new_t, int v_t, void* stream);
+
+/*
+ * SFA decode step over a paged cache (App. B), optionally coding the query
+ * inside the decode kernel.
+ *
+ * q               [B, Hq, d] float32 dense query, coded in the kernel exactly
+ *                 as sfa_topk_encode codes it (float32 values); q_idx and
+ *                 q_val must then be NULL.  Or q NULL and q_idx, q_val
+ *                 [B, Hq, k] query codes (q_idx_t, q_val_t), as in
+ *                 sfa_attn_decode.
+ * kc_idx, kc_val, v_cache, block_table, max_pages, page_size, num_pages:
+ *                 the paged layout above; page_size a power of two >= 16.
+ *                 Page ids outside [0, num_pages) are clamped into range
+ *                 (undefined results, no fault).
+ * seq_len         [B] int32 on the device (clamped into
+ *                 [0, max_pages * page_size]) or NULL for full sequences.
+ * o, lse, ws, ws_bytes, scale, dtypes: as sfa_attn_decode, with the
+ *                 workspace sized by
+ *                 sfa_attn_decode_workspace(B, Hq, max_pages * page_size, d).
+ * The result equals sfa_attn_decode on the gathered contiguous cache (same
+ * chunking and summation order, hence the same bits).
+ * Limits: as sfa_attn_decode; max_pages * page_size <= 2^30.
+ * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC, SFA_EHIP.
+ */
+sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* q_val,
+                                 const void* kc_idx, const void* kc_val, const void* v_cache,
+                                 const int32_t* block_table, int max_pages, int page_size,
+                                 int num_pages, const int32_t* seq_len, int B, int Hq, int Hkv,
+                                 int d, int k, float scale, int q_idx_t, int q_val_t,
+                                 int kc_idx_t, int kc_val_t, int v_t, int o_t, void* o,
+                                 float* lse, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

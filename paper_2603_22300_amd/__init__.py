@@ -18,7 +18,7 @@ __all__ = [
     "SfaError", "lib", "library_path", "sfa_abi_version", "sfa_strerror",
     "sfa_topk_encode", "sfa_attn_fwd_workspace", "sfa_attn_fwd", "sfa_attn_fwd_index",
     "sfa_attn_bwd_workspace", "sfa_attn_bwd",
-    "sfa_attn_decode_workspace", "sfa_attn_decode",
+    "sfa_attn_decode_workspace", "sfa_attn_decode", "sfa_attn_decode_paged", "sfa_kv_append",
     "SFA_OK", "SFA_EINVAL", "SFA_ENOTSUP", "SFA_EHIP", "SFA_ENOSPC",
     "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16",
 ]
@@ -71,6 +71,13 @@ def lib() -> ctypes.CDLL:
         L.sfa_attn_decode.restype = i32
         L.sfa_attn_decode.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, f32,
                                       i32, i32, i32, i32, i32, i32, vp, vp, vp, sz, vp]
+        L.sfa_attn_decode_paged.restype = i32
+        L.sfa_attn_decode_paged.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, i32, i32,
+                                            i32, i32, i32, f32, i32, i32, i32, i32, i32, i32, vp,
+                                            vp, vp, sz, vp]
+        L.sfa_kv_append.restype = i32
+        L.sfa_kv_append.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp, i32, i32, i32,
+                                    vp, vp, vp, i32, i32, i32, i32, vp]
         _lib = L
     return _lib
 
@@ -283,4 +290,109 @@ def sfa_attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len=None, scale: 
                                 float(scale), qit, qvt, cit, cvt, vt, ot, o.data_ptr(), lp,
                                 ws.data_ptr(), ws.numel() * ws.element_size(), _stream(v_cache)),
           "sfa_attn_decode")
+    return o, lse
+
+
+def _i32_vec(t, name: str, n: int) -> int:
+    _check(t, name, {torch.int32: SFA_I32})
+    if t.numel() != n:
+        raise ValueError(f"{name} must hold {n} entries")
+    return t.data_ptr()
+
+
+def sfa_kv_append(k_new, v_new, seq_len, kc_idx, kc_val, v_cache, k: int, block_table=None,
+                  n_new=None):
+    """Append coded keys and values to a KV cache, in place, and advance seq_len.
+
+    k_new float32 [B, Hkv, T, d]; v_new [B, Hkv, T, d] (float32 or bf16);
+    seq_len int32 [B] (in/out).  Contiguous cache (block_table None):
+    kc_* [B, Hkv, Lmax, k], v_cache [B, Hkv, Lmax, d].  Paged cache:
+    kc_* [num_pages, Hkv, page_size, k], v_cache [num_pages, Hkv, page_size, d],
+    block_table int32 [B, max_pages].  n_new int32 [B] or None (= T)."""
+    B, Hkv, T, d = k_new.shape
+    _check(k_new, "k_new", {torch.float32: SFA_F32})
+    vnt = _check(v_new, "v_new", _VAL)
+    if tuple(v_new.shape) != (B, Hkv, T, d):
+        raise ValueError("v_new must match k_new")
+    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _VAL)
+    vt = _check(v_cache, "v_cache", _VAL)
+    npg, P = kc_idx.shape[0], kc_idx.shape[2]
+    if tuple(kc_idx.shape) != (npg, Hkv, P, k) or tuple(kc_val.shape) != (npg, Hkv, P, k) \
+            or tuple(v_cache.shape) != (npg, Hkv, P, d):
+        raise ValueError("inconsistent cache shapes")
+    sp = _i32_vec(seq_len, "seq_len", B)
+    tp, maxp = 0, 1
+    if block_table is not None:
+        _check(block_table, "block_table", {torch.int32: SFA_I32})
+        if block_table.dim() != 2 or block_table.shape[0] != B:
+            raise ValueError("block_table must be [B, max_pages]")
+        tp, maxp = block_table.data_ptr(), block_table.shape[1]
+    elif npg != B:
+        raise ValueError("a contiguous cache holds B sequences")
+    npp = 0 if n_new is None else _i32_vec(n_new, "n_new", B)
+    _call(lib().sfa_kv_append(k_new.data_ptr(), v_new.data_ptr(), npp, sp, B, Hkv, T, d, k, tp,
+                              maxp, P, npg, kc_idx.data_ptr(), kc_val.data_ptr(),
+                              v_cache.data_ptr(), cit, cvt, vnt, vt, _stream(k_new)),
+          "sfa_kv_append")
+    return seq_len
+
+
+def sfa_attn_decode_paged(kc_idx, kc_val, v_cache, block_table, seq_len=None, q=None, q_idx=None,
+                          q_val=None, scale: float | None = None, o_dtype=None, o=None, lse=None,
+                          want_lse: bool = True, ws=None):
+    """SFA decode step over a paged cache.  Give either the dense query q
+    (float32 [B, Hq, d], coded inside the kernel) or its codes q_idx, q_val
+    [B, Hq, k].  kc_* [num_pages, Hkv, page_size, k], v_cache
+    [num_pages, Hkv, page_size, d], block_table int32 [B, max_pages],
+    seq_len int32 [B] or None.  Returns (o [B, Hq, d], lse [B, Hq] or None)."""
+    npg, Hkv, P, k = kc_idx.shape
+    d = v_cache.shape[-1]
+    if tuple(kc_val.shape) != (npg, Hkv, P, k) or tuple(v_cache.shape) != (npg, Hkv, P, d):
+        raise ValueError("inconsistent cache shapes")
+    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _VAL)
+    vt = _check(v_cache, "v_cache", _VAL)
+    _check(block_table, "block_table", {torch.int32: SFA_I32})
+    if block_table.dim() != 2:
+        raise ValueError("block_table must be [B, max_pages]")
+    B, maxp = block_table.shape
+    qp = qip = qvp = 0
+    qit = qvt = 0
+    if q is not None:
+        if q_idx is not None or q_val is not None:
+            raise ValueError("give either q or (q_idx, q_val)")
+        _check(q, "q", {torch.float32: SFA_F32})
+        if q.dim() != 3 or q.shape[0] != B or q.shape[2] != d:
+            raise ValueError("q must be [B, Hq, d]")
+        Hq = q.shape[1]
+        qp = q.data_ptr()
+    else:
+        qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _VAL)
+        if q_idx.dim() != 3 or tuple(q_idx.shape) != (B, q_idx.shape[1], k) \
+                or tuple(q_val.shape) != tuple(q_idx.shape):
+            raise ValueError("q codes must be [B, Hq, k]")
+        Hq = q_idx.shape[1]
+        qip, qvp = q_idx.data_ptr(), q_val.data_ptr()
+    sp = 0 if seq_len is None else _i32_vec(seq_len, "seq_len", B)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if o is None:
+        o = torch.empty((B, Hq, d), dtype=o_dtype or v_cache.dtype, device=v_cache.device)
+    ot = _check(o, "o", _VAL)
+    if tuple(o.shape) != (B, Hq, d):
+        raise ValueError("o has the wrong shape")
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=v_cache.device)
+    lp = 0
+    if lse is not None:
+        _check(lse, "lse", {torch.float32: SFA_F32})
+        lp = lse.data_ptr()
+    if ws is None:
+        ws = torch.empty(sfa_attn_decode_workspace(B, Hq, maxp * P, d), dtype=torch.uint8,
+                         device=v_cache.device)
+    _call(lib().sfa_attn_decode_paged(qp, qip, qvp, kc_idx.data_ptr(), kc_val.data_ptr(),
+                                      v_cache.data_ptr(), block_table.data_ptr(), maxp, P, npg,
+                                      sp, B, Hq, Hkv, d, k, float(scale), qit, qvt, cit, cvt, vt,
+                                      ot, o.data_ptr(), lp, ws.data_ptr(),
+                                      ws.numel() * ws.element_size(), _stream(v_cache)),
+          "sfa_attn_decode_paged")
     return o, lse

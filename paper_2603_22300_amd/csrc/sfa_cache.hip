@@ -1,0 +1,141 @@
+// KV-cache maintenance for SFA decode (App. B: generation appends one coded
+// key and its value per token to a cache of sparse key codes and dense V).
+//
+// sfa_kv_append_kernel: one wavefront per new (sequence, KV head, token) row
+// at a time.
+// The key row is coded with the same exact Top-k selection as the coding
+// kernel (Sec. 3.1, Eqs. (3)-(4)) and written, with the value row, at the
+// token's position seq_len[b] + t: in a contiguous cache [B, Hkv, P, ...] at
+// row (b, h, position), in a paged one through the block table (page
+// table[b][position / P], slot position % P).  Positions past the capacity
+// and pages outside the pool are not written.
+// sfa_kv_advance_kernel: seq_len[b] += appended count, clamped to the
+// capacity; it runs after the append on the same stream, so every append
+// wave reads the old length.
+#include "sfa_device.h"
+#include "sfa_launch.h"
+#include "sfa_topk.h"
+
+namespace sfa {
+
+__device__ __forceinline__ int appended_count(const int32_t* n_new, int b, int T) {
+  if (!n_new) return T;
+  const int c = n_new[b];
+  return c < 0 ? 0 : (c > T ? T : c);
+}
+
+// Grid: y strides over the B * Hkv (sequence, KV head) pairs, x over the
+// pair's tokens, one wavefront per token row, the next row's key and value
+// loads in flight while the current one is selected and stored.  Everything
+// that depends only on the pair (its length, count, capacity) is read once;
+// a token's page and slot are a shift and a mask (power-of-two pages).
+template <int E>  // coordinates per lane: d <= 64 * E
+__global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int tw = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tstride = gridDim.x * 4;
+  const int64_t cap = a.table ? (int64_t)a.max_pages * a.page_size : a.page_size;
+  for (int bh = blockIdx.y; bh < a.B * a.Hkv; bh += gridDim.y) {
+    const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+    int64_t L0 = a.seq_len[b];
+    L0 = L0 < 0 ? 0 : (L0 > cap ? cap : L0);
+    // tokens written: t < count, and positions below the capacity
+    const int tend = (int)min((int64_t)appended_count(a.n_new, b, a.T), cap - L0);
+    if (tw >= tend) continue;  // uniform per wave
+    const float* kbase = a.k_new + (int64_t)bh * a.T * a.d;
+    const unsigned char* vbase =
+        (const unsigned char*)a.v_new + (int64_t)bh * a.T * a.d * (a.vin_bf16 ? 2 : 4);
+
+    // raw 32-bit words: key bits, and value bits (bf16 zero-extended or float)
+    uint32_t nk[E], nv[E];
+    auto load_row = [&](int t) {
+      const int64_t o = (int64_t)t * a.d;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int c = min(lane + 64 * e, a.d - 1);
+        nk[e] = __float_as_uint(kbase[o + c]);
+        nv[e] = a.vin_bf16 ? (uint32_t)((const uint16_t*)vbase)[o + c]
+                           : ((const uint32_t*)vbase)[o + c];
+      }
+    };
+    load_row(tw);
+    for (int t = tw; t < tend; t += tstride) {
+      uint32_t bits[E], vb[E], key[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        bits[e] = nk[e];
+        vb[e] = nv[e];
+        key[e] = topk_key(bits[e], lane + 64 * e < a.d);
+      }
+      if (t + tstride < tend) load_row(t + tstride);
+      const int64_t pos = L0 + t;
+      int64_t page = b, slot = pos;
+      if (a.table) {
+        page = a.table[(int64_t)b * a.max_pages + (pos >> a.log2P)];
+        slot = pos & (a.page_size - 1);
+        if (page < 0 || page >= a.num_pages) continue;  // uniform per wave
+      }
+      const int64_t crow = (page * a.Hkv + h) * a.page_size + slot;
+
+      bool sel[E];
+      topk_select<E>(key, a.k, sel);
+      int sl[E];
+      topk_slots<E>(sel, sl);
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (sel[e] && sl[e] < a.k)
+          store_code(a.kc_idx, a.kc_val, crow * a.k + sl[e], lane + 64 * e, bits[e], a.idx16,
+                     a.valbf16);
+      // value row (bf16 cache from float32 values: round to nearest even)
+      const int64_t vo = crow * a.d;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int c = lane + 64 * e;
+        if (c < a.d) {
+          if (a.vc_bf16)
+            ((uint16_t*)a.v_cache)[vo + c] =
+                a.vin_bf16 ? (uint16_t)vb[e] : (uint16_t)f32_to_bf16_rne(__uint_as_float(vb[e]));
+          else
+            ((uint32_t*)a.v_cache)[vo + c] = a.vin_bf16 ? vb[e] << 16 : vb[e];
+        }
+      }
+    }
+  }
+}
+
+__global__ void sfa_kv_advance_kernel(int32_t* seq_len, const int32_t* n_new, int B, int T,
+                                      int64_t cap) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int64_t L = seq_len[b];
+  L = L < 0 ? 0 : (L > cap ? cap : L);
+  L += appended_count(n_new, b, T);
+  seq_len[b] = (int32_t)(L > cap ? cap : L);
+}
+
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.B * a.Hkv * a.T;
+  if (rows > 0) {
+    // about 2048 workgroups of 4 waves (8 per compute unit) over the pairs
+    const int pairs = a.B * a.Hkv;
+    const int gy = pairs < 65535 ? pairs : 65535;
+    int gx = (2048 + gy - 1) / gy;
+    const int gx_need = (a.T + 3) / 4;
+    if (gx > gx_need) gx = gx_need;
+    dim3 grid(gx, gy), block(256);
+    if (a.d <= 64)
+      hipLaunchKernelGGL(sfa_kv_append_kernel<1>, grid, block, 0, stream, a);
+    else if (a.d <= 128)
+      hipLaunchKernelGGL(sfa_kv_append_kernel<2>, grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL(sfa_kv_append_kernel<4>, grid, block, 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int64_t cap = a.table ? (int64_t)a.max_pages * a.page_size : a.page_size;
+  hipLaunchKernelGGL(sfa_kv_advance_kernel, dim3((a.B + 255) / 256), dim3(256), 0, stream,
+                     a.seq_len, a.n_new, a.B, a.T, cap);
+  return hipGetLastError();
+}
+
+}  // namespace sfa

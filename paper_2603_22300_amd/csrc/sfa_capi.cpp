@@ -146,10 +146,81 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
   if (!pow2_le(Hq / Hkv, sfa::decode_max_group())) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
   if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
-  return from_hip(sfa::launch_attn_decode(
-      q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, B, Hq, Hkv, Lmax, d, k, scale,
-      q_idx_t == SFA_I16, q_val_t == SFA_BF16, kc_idx_t == SFA_I16, kc_val_t == SFA_BF16,
-      v_t == SFA_BF16, o_t == SFA_BF16, o, lse, ws, (hipStream_t)stream));
+  sfa::DecodeArgs a = {};
+  a.q_idx = q_idx; a.q_val = q_val; a.kc_idx = kc_idx; a.kc_val = kc_val; a.v = v_cache;
+  a.seq_len = seq_len;
+  a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lmax = Lmax; a.d = d; a.k = k; a.scale = scale;
+  a.qidx16 = q_idx_t == SFA_I16; a.qvalbf16 = q_val_t == SFA_BF16;
+  a.kidx16 = kc_idx_t == SFA_I16; a.kvalbf16 = kc_val_t == SFA_BF16;
+  a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;
+  a.o = o; a.lse = lse; a.ws = ws;
+  return from_hip(sfa::launch_attn_decode(a, (hipStream_t)stream));
+}
+
+sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* q_val,
+                                 const void* kc_idx, const void* kc_val, const void* v_cache,
+                                 const int32_t* block_table, int max_pages, int page_size,
+                                 int num_pages, const int32_t* seq_len, int B, int Hq, int Hkv,
+                                 int d, int k, float scale, int q_idx_t, int q_val_t,
+                                 int kc_idx_t, int kc_val_t, int v_t, int o_t, void* o,
+                                 float* lse, void* ws, size_t ws_bytes, void* stream) {
+  const bool dense_q = q != nullptr;
+  if (dense_q ? (q_idx || q_val) : (!q_idx || !q_val)) return SFA_EINVAL;
+  if (!kc_idx || !kc_val || !v_cache || !block_table || !o || !ws) return SFA_EINVAL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
+  if (max_pages < 1 || num_pages < 1) return SFA_EINVAL;
+  if (page_size < 16 || (page_size & (page_size - 1)) != 0) return SFA_EINVAL;
+  if ((long long)max_pages * page_size > (1LL << 30)) return SFA_EINVAL;
+  if (Hq % Hkv != 0) return SFA_EINVAL;
+  if ((!dense_q && (!is_idx(q_idx_t) || !is_val(q_val_t))) || !is_idx(kc_idx_t) ||
+      !is_val(kc_val_t) || !is_val(v_t) || !is_val(o_t))
+    return SFA_EINVAL;
+  if (!isfinite(scale)) return SFA_EINVAL;
+  if (d != 64 && d != 128) return SFA_ENOTSUP;
+  if (!pow2_le(Hq / Hkv, sfa::decode_max_group())) return SFA_ENOTSUP;
+  if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  const int Lmax = max_pages * page_size;
+  if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
+  int log2P = 0;
+  while ((1 << log2P) < page_size) ++log2P;
+  sfa::DecodeArgs a = {};
+  a.q_dense = q; a.q_idx = q_idx; a.q_val = q_val;
+  a.kc_idx = kc_idx; a.kc_val = kc_val; a.v = v_cache;
+  a.seq_len = seq_len; a.table = block_table;
+  a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lmax = Lmax; a.d = d; a.k = k; a.scale = scale;
+  a.max_pages = max_pages; a.log2P = log2P; a.num_pages = num_pages;
+  a.qidx16 = !dense_q && q_idx_t == SFA_I16; a.qvalbf16 = !dense_q && q_val_t == SFA_BF16;
+  a.kidx16 = kc_idx_t == SFA_I16; a.kvalbf16 = kc_val_t == SFA_BF16;
+  a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;
+  a.o = o; a.lse = lse; a.ws = ws;
+  return from_hip(sfa::launch_attn_decode(a, (hipStream_t)stream));
+}
+
+sfa_status sfa_kv_append(const float* k_new, const void* v_new, const int32_t* n_new,
+                         int32_t* seq_len, int B, int Hkv, int T, int d, int k,
+                         const int32_t* block_table, int max_pages, int page_size,
+                         int num_pages, void* kc_idx, void* kc_val, void* v_cache,
+                         int kc_idx_t, int kc_val_t, int v_new_t, int v_t, void* stream) {
+  if (!seq_len || !kc_idx || !kc_val || !v_cache) return SFA_EINVAL;
+  if (B < 1 || Hkv < 1 || T < 0 || d < 1 || k < 1 || k > d || page_size < 1) return SFA_EINVAL;
+  if (T > 0 && (!k_new || !v_new)) return SFA_EINVAL;
+  if (block_table && (max_pages < 1 || num_pages < 1)) return SFA_EINVAL;
+  if (block_table && (long long)max_pages * page_size > (1LL << 30)) return SFA_EINVAL;
+  if (block_table && (page_size & (page_size - 1)) != 0) return SFA_EINVAL;
+  if (!is_idx(kc_idx_t) || !is_val(kc_val_t) || !is_val(v_new_t) || !is_val(v_t))
+    return SFA_EINVAL;
+  if (kc_idx_t == SFA_I16 && d > 32767) return SFA_EINVAL;
+  if (d > 256) return SFA_ENOTSUP;
+  if ((long long)B * Hkv * T > (1LL << 31)) return SFA_ENOTSUP;
+  sfa::AppendArgs a = {};
+  a.k_new = k_new; a.v_new = v_new; a.n_new = n_new; a.seq_len = seq_len;
+  a.table = block_table; a.kc_idx = kc_idx; a.kc_val = kc_val; a.v_cache = v_cache;
+  a.B = B; a.Hkv = Hkv; a.T = T; a.d = d; a.k = k;
+  a.page_size = page_size; a.max_pages = max_pages; a.num_pages = num_pages;
+  while ((1 << a.log2P) < page_size) ++a.log2P;
+  a.idx16 = kc_idx_t == SFA_I16; a.valbf16 = kc_val_t == SFA_BF16;
+  a.vin_bf16 = v_new_t == SFA_BF16; a.vc_bf16 = v_t == SFA_BF16;
+  return from_hip(sfa::launch_kv_append(a, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -11,8 +11,19 @@
 //   P.V:    lanes over (8 dims, key subset); float32 FMAs.
 // Each workgroup writes one partial (max, sum, unnormalised output) per query
 // head; a second kernel merges the chunks by their LSE.
+//
+// Cache layouts: contiguous [B, Hkv, Lmax, ...], or paged -- a pool of pages
+// [num_pages, Hkv, P, ...] with a block table mapping each run of P
+// positions of a sequence to a page (P a power of two >= 16).  A wave's
+// 512-position range spans at most 32 pages; their ids are loaded once into
+// one register (lane l: the range's l-th page) and read back by lane shuffle
+// for the codes (lane = key) and by readlane for V, whose keys within one
+// wide load always share a page.
+// Query: codes, or the dense float32 query coded in the prologue with the
+// same Top-k selection as the coding kernel (one wavefront per head).
 #include "sfa_device.h"
 #include "sfa_launch.h"
+#include "sfa_topk.h"
 
 namespace sfa {
 
@@ -34,6 +45,9 @@ struct DecParams {
   int Hq, Hkv, Lmax, k, nch;
   float scale_log2;
   int qidx16, qvalbf16, kidx16, kvalbf16;
+  const float* q_dense;   // [B, Hq, D] or null (then q_idx / q_val)
+  const int32_t* table;   // paged: [B, max_pages]
+  int max_pages, log2P, num_pages;
 };
 
 __device__ __forceinline__ int seq_len_of(const int32_t* seq_len, int b, int Lmax) {
@@ -46,7 +60,7 @@ __device__ __forceinline__ int seq_len_of(const int32_t* seq_len, int b, int Lma
 // loaded as 16-byte vectors and prefetched one 64-key sub-block ahead, with
 // the sub-block's V (bf16) in flight during its score phase.  KC8 = 0: any
 // format and k, element loads issued as a batch per sub-block.
-template <int D, int G, bool VBF16, int KC8>
+template <int D, int G, bool VBF16, int KC8, bool PAGED>
 __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   constexpr int DL = D / 8;     // lanes covering one key's D values (8 each)
   constexpr int KPL = 64 / DL;  // keys per wave-wide V load
@@ -67,13 +81,32 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   const int dmask = D - 1;
 
   // densify the G query codes: qd[u][h]
-  for (int x = tid; x < D * G; x += kDecThreads) (&qd[0][0])[x] = 0.f;
-  __syncthreads();
-  for (int x = tid; x < G * k; x += kDecThreads) {
-    const int h = x / k, t = x - h * k;
-    const int64_t qi = ((int64_t)b * p.Hq + hkv * G + h) * k + t;
-    const int u = load_idx(p.q_idx, qi, p.qidx16, dmask);
-    qd[u][h] = load_val(p.q_val, qi, p.qvalbf16);
+  if (p.q_dense) {
+    // code each dense query row here: one wavefront per head, kept
+    // coordinates keep their float32 value, the rest are zero
+    constexpr int E = D / 64;
+    for (int h = __builtin_amdgcn_readfirstlane(wave); h < G; h += kDecWaves) {
+      const float* qr = p.q_dense + ((int64_t)b * p.Hq + hkv * G + h) * D;
+      uint32_t bits[E], key[E];
+      bool sel[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        bits[e] = __float_as_uint(qr[lane + 64 * e]);
+        key[e] = topk_key(bits[e], true);
+      }
+      topk_select<E>(key, k, sel);
+#pragma unroll
+      for (int e = 0; e < E; ++e) qd[lane + 64 * e][h] = sel[e] ? __uint_as_float(bits[e]) : 0.f;
+    }
+  } else {
+    for (int x = tid; x < D * G; x += kDecThreads) (&qd[0][0])[x] = 0.f;
+    __syncthreads();
+    for (int x = tid; x < G * k; x += kDecThreads) {
+      const int h = x / k, t = x - h * k;
+      const int64_t qi = ((int64_t)b * p.Hq + hkv * G + h) * k + t;
+      const int u = load_idx(p.q_idx, qi, p.qidx16, dmask);
+      qd[u][h] = load_val(p.q_val, qi, p.qvalbf16);
+    }
   }
   __syncthreads();
 
@@ -92,6 +125,34 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   const int per_wave = kDecChunk / kDecWaves;
   const int w0 = c0 + wave * per_wave;
   const int w1 = min(c1, w0 + per_wave);
+
+  // Row of key j in the cache arrays.  Paged: lane l of `tblv` holds the
+  // page of the wave's l-th page-sized run (ids clamped into the pool).
+  int tblv = 0;
+  const int pg0 = PAGED ? (w0 >> p.log2P) : 0;
+  if constexpr (PAGED) {
+    if (w0 < w1) {
+      const int npg = ((w1 - 1) >> p.log2P) - pg0 + 1;  // <= 32 (P >= 16)
+      if (lane < npg) {
+        const int pg = p.table[(int64_t)b * p.max_pages + pg0 + lane];
+        tblv = min(max(pg, 0), p.num_pages - 1);
+      }
+    }
+  }
+  const int pmask = (1 << (PAGED ? p.log2P : 0)) - 1;
+  auto paged_row = [&](int pg, int j) -> int64_t {
+    return (((int64_t)pg * p.Hkv + hkv) << p.log2P) + (j & pmask);
+  };
+  // j may differ across lanes (w0 <= j < w1)
+  auto row_of = [&](int j) -> int64_t {
+    if constexpr (PAGED) return paged_row(__shfl(tblv, (j >> p.log2P) - pg0, 64), j);
+    else return kv_row0 + j;
+  };
+  // jb wave-uniform (w0 <= jb < w1), j on the same page as jb
+  auto row_near = [&](int jb, int j) -> int64_t {
+    if constexpr (PAGED) return paged_row(__builtin_amdgcn_readlane(tblv, (jb >> p.log2P) - pg0), j);
+    else return kv_row0 + j;
+  };
 
   // ---- per-sub-block pieces ----
   // online softmax of the lane's key scores s[h] (valid: ok); writes P to pbuf
@@ -126,9 +187,9 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
     // ---------------- vectorized, prefetched path ----------------
     uint4 cidx[KC8], cval[KC8];
     auto load_codes = [&](int sb) {
-      const int j = min(sb + lane, w1 - 1);
-      const uint4* pi = (const uint4*)((const int16_t*)p.kc_idx + (kv_row0 + j) * (8 * KC8));
-      const uint4* pv = (const uint4*)((const uint16_t*)p.kc_val + (kv_row0 + j) * (8 * KC8));
+      const int64_t row = row_of(min(sb + lane, w1 - 1));
+      const uint4* pi = (const uint4*)((const int16_t*)p.kc_idx + row * (8 * KC8));
+      const uint4* pv = (const uint4*)((const uint16_t*)p.kc_val + row * (8 * KC8));
 #pragma unroll
       for (int c = 0; c < KC8; ++c) { cidx[c] = pi[c]; cval[c] = pv[c]; }
     };
@@ -139,7 +200,8 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
 #pragma unroll
       for (int r = 0; r < NR; ++r) {
         const int jg = min(sb + r * KPL + ksub, w1 - 1);
-        vraw[r] = *(const uint4*)((const uint16_t*)p.v + (kv_row0 + jg) * D + dsub * 8);
+        const int64_t row = row_near(min(sb + r * KPL, w1 - 1), jg);
+        vraw[r] = *(const uint4*)((const uint16_t*)p.v + row * D + dsub * 8);
       }
       // scores, lane = key
       float s[G];
@@ -179,7 +241,7 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
       float s[G];
 #pragma unroll
       for (int h = 0; h < G; ++h) s[h] = 0.f;
-      const int64_t cbase = (kv_row0 + j) * k;
+      const int64_t cbase = row_of(j) * k;
       for (int t = 0; t < k; ++t) {
         const int u = load_idx(p.kc_idx, cbase + t, p.kidx16, dmask);
         const float kv = load_val(p.kc_val, cbase + t, p.kvalbf16);
@@ -190,15 +252,16 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
       for (int r = 0; r < 64; r += KPL) {
         const int jj = r + ksub;
         const int jg = min(sb + jj, w1 - 1);
+        const int64_t row = row_near(min(sb + r, w1 - 1), jg);
         float vv[8];
         if constexpr (VBF16) {
-          const uint4 raw = *(const uint4*)((const uint16_t*)p.v + (kv_row0 + jg) * D + dsub * 8);
+          const uint4 raw = *(const uint4*)((const uint16_t*)p.v + row * D + dsub * 8);
           vv[0] = __uint_as_float(raw.x << 16); vv[1] = __uint_as_float(raw.x & 0xffff0000u);
           vv[2] = __uint_as_float(raw.y << 16); vv[3] = __uint_as_float(raw.y & 0xffff0000u);
           vv[4] = __uint_as_float(raw.z << 16); vv[5] = __uint_as_float(raw.z & 0xffff0000u);
           vv[6] = __uint_as_float(raw.w << 16); vv[7] = __uint_as_float(raw.w & 0xffff0000u);
         } else {
-          const float4* src = (const float4*)((const float*)p.v + (kv_row0 + jg) * D + dsub * 8);
+          const float4* src = (const float4*)((const float*)p.v + row * D + dsub * 8);
           const float4 a = src[0], c = src[1];
           vv[0] = a.x; vv[1] = a.y; vv[2] = a.z; vv[3] = a.w;
           vv[4] = c.x; vv[5] = c.y; vv[6] = c.z; vv[7] = c.w;
@@ -284,7 +347,10 @@ size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d) {
 template <int D, int G, bool VBF16, int KC8>
 static void launch_dec_t(const DecParams& p, int B, hipStream_t stream) {
   dim3 grid(p.nch, B * p.Hkv), block(kDecThreads);
-  hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8>), grid, block, 0, stream, p);
+  if (p.table)
+    hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8, true>), grid, block, 0, stream, p);
+  else
+    hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8, false>), grid, block, 0, stream, p);
 }
 
 template <int D, int G, bool VBF16>
@@ -310,36 +376,35 @@ static void launch_dec_g(const DecParams& p, int G, int B, hipStream_t stream) {
 
 int decode_max_group() { return kDecMaxG; }
 
-hipError_t launch_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
-                              const void* kc_val, const void* v, const int32_t* seq_len, int B,
-                              int Hq, int Hkv, int Lmax, int d, int k, float scale, int qidx16,
-                              int qvalbf16, int kidx16, int kvalbf16, int vbf16, int obf16,
-                              void* o, float* lse, void* ws, hipStream_t stream) {
+hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   DecParams p;
-  p.q_idx = q_idx; p.q_val = q_val; p.kc_idx = kc_idx; p.kc_val = kc_val; p.v = v;
-  p.seq_len = seq_len;
-  p.Hq = Hq; p.Hkv = Hkv; p.Lmax = Lmax; p.k = k;
-  p.nch = (Lmax + kDecChunk - 1) / kDecChunk;
-  const size_t nslot = (size_t)B * Hq * p.nch;
-  p.ws_m = (float*)ws;
+  p.q_idx = a.q_idx; p.q_val = a.q_val; p.kc_idx = a.kc_idx; p.kc_val = a.kc_val; p.v = a.v;
+  p.seq_len = a.seq_len;
+  p.Hq = a.Hq; p.Hkv = a.Hkv; p.Lmax = a.Lmax; p.k = a.k;
+  p.nch = (a.Lmax + kDecChunk - 1) / kDecChunk;
+  const size_t nslot = (size_t)a.B * a.Hq * p.nch;
+  p.ws_m = (float*)a.ws;
   p.ws_l = p.ws_m + nslot;
   p.ws_o = p.ws_l + nslot;
-  p.scale_log2 = (float)((double)scale * 1.4426950408889634);
-  p.qidx16 = qidx16; p.qvalbf16 = qvalbf16; p.kidx16 = kidx16; p.kvalbf16 = kvalbf16;
-  const int G = Hq / Hkv;
-  if (d == 64) {
-    if (vbf16) launch_dec_g<64, true>(p, G, B, stream); else launch_dec_g<64, false>(p, G, B, stream);
+  p.scale_log2 = (float)((double)a.scale * 1.4426950408889634);
+  p.qidx16 = a.qidx16; p.qvalbf16 = a.qvalbf16; p.kidx16 = a.kidx16; p.kvalbf16 = a.kvalbf16;
+  p.q_dense = a.q_dense;
+  p.table = a.table;
+  p.max_pages = a.max_pages; p.log2P = a.log2P; p.num_pages = a.num_pages;
+  const int G = a.Hq / a.Hkv, B = a.B;
+  if (a.d == 64) {
+    if (a.vbf16) launch_dec_g<64, true>(p, G, B, stream); else launch_dec_g<64, false>(p, G, B, stream);
   } else {
-    if (vbf16) launch_dec_g<128, true>(p, G, B, stream); else launch_dec_g<128, false>(p, G, B, stream);
+    if (a.vbf16) launch_dec_g<128, true>(p, G, B, stream); else launch_dec_g<128, false>(p, G, B, stream);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (d == 64)
-    hipLaunchKernelGGL(sfa_decode_combine_kernel<64>, dim3(B * Hq), dim3(64), 0, stream,
-                       p.ws_m, p.ws_l, p.ws_o, seq_len, Hq, Lmax, p.nch, o, obf16, lse);
+  if (a.d == 64)
+    hipLaunchKernelGGL(sfa_decode_combine_kernel<64>, dim3(B * a.Hq), dim3(64), 0, stream,
+                       p.ws_m, p.ws_l, p.ws_o, a.seq_len, a.Hq, a.Lmax, p.nch, a.o, a.obf16, a.lse);
   else
-    hipLaunchKernelGGL(sfa_decode_combine_kernel<128>, dim3(B * Hq), dim3(128), 0, stream,
-                       p.ws_m, p.ws_l, p.ws_o, seq_len, Hq, Lmax, p.nch, o, obf16, lse);
+    hipLaunchKernelGGL(sfa_decode_combine_kernel<128>, dim3(B * a.Hq), dim3(128), 0, stream,
+                       p.ws_m, p.ws_l, p.ws_o, a.seq_len, a.Hq, a.Lmax, p.nch, a.o, a.obf16, a.lse);
   return hipGetLastError();
 }
 

@@ -34,12 +34,41 @@ int fwd_index_lds_bytes(int d, int k, int vbf16);
 int fwd_index_max_k();
 int fwd_index_rows_per_block();
 
-hipError_t launch_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
-                              const void* kc_val, const void* v, const int32_t* seq_len, int B,
-                              int Hq, int Hkv, int Lmax, int d, int k, float scale, int qidx16,
-                              int qvalbf16, int kidx16, int kvalbf16, int vbf16, int obf16,
-                              void* o, float* lse, void* ws, hipStream_t stream);
+// Decode over a contiguous (table == nullptr: [B, Hkv, Lmax, ...]) or paged
+// (pages [num_pages, Hkv, 1 << log2P, ...], table [B, max_pages],
+// Lmax = max_pages << log2P) cache; query codes, or q_dense coded in-kernel.
+struct DecodeArgs {
+  const float* q_dense;
+  const void *q_idx, *q_val, *kc_idx, *kc_val, *v;
+  const int32_t* seq_len;
+  const int32_t* table;
+  int B, Hq, Hkv, Lmax, d, k;
+  int max_pages, log2P, num_pages;
+  float scale;
+  int qidx16, qvalbf16, kidx16, kvalbf16, vbf16, obf16;
+  void* o;
+  float* lse;
+  void* ws;
+};
+hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream);
 size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d);
 int decode_max_group();
+
+// KV-cache append: Top-k coding of new keys and copy of their values into a
+// contiguous (table == nullptr: [B, Hkv, P, ...]) or paged cache, then
+// seq_len[b] += the appended count (clamped to the capacity).
+struct AppendArgs {
+  const float* k_new;
+  const void* v_new;
+  const int32_t* n_new;
+  int32_t* seq_len;
+  const int32_t* table;
+  void *kc_idx, *kc_val, *v_cache;
+  int B, Hkv, T, d, k;
+  int page_size, max_pages, num_pages;
+  int log2P;  // paged: page_size == 1 << log2P
+  int idx16, valbf16, vin_bf16, vc_bf16;
+};
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
 
 }  // namespace sfa

@@ -141,3 +141,56 @@ def test_bwd_validation_and_workspace(L):
     assert _bwd(L, Hq=3, Hkv=2) == 1
     assert _bwd(L, Hq=32, Hkv=2) == 2      # group of 16 heads: not supported by the backward
     assert _bwd(L, d=96, k=8) == 2
+
+
+def _paged(L, **kw):
+    a = dict(q=None, q_idx=FAKE, q_val=FAKE, kc_idx=FAKE, kc_val=FAKE, v_cache=FAKE,
+             block_table=FAKE, max_pages=4, page_size=64, num_pages=16, seq_len=None, B=2, Hq=8,
+             Hkv=2, d=128, k=16, scale=0.1, q_idx_t=0, q_val_t=2, kc_idx_t=1, kc_val_t=3, v_t=3,
+             o_t=2, o=FAKE, lse=None, ws=FAKE, ws_bytes=ctypes.c_size_t(1), stream=None)
+    a.update(kw)
+    return L.sfa_attn_decode_paged(*a.values())
+
+
+def test_decode_paged_validation(L):
+    need = L.sfa_attn_decode_workspace(2, 8, 4 * 64, 128)
+    assert _paged(L) == 4                            # workspace too small, checked last
+    assert _paged(L, ws_bytes=ctypes.c_size_t(need - 1)) == 4
+    ok = dict(ws_bytes=ctypes.c_size_t(need))
+    assert _paged(L, q=FAKE, **ok) == 1              # dense query and codes both given
+    assert _paged(L, q_idx=None, **ok) == 1          # neither complete
+    assert _paged(L, block_table=None, **ok) == 1
+    assert _paged(L, page_size=48, **ok) == 1        # not a power of two
+    assert _paged(L, page_size=8, **ok) == 1         # below 16
+    assert _paged(L, max_pages=0, **ok) == 1
+    assert _paged(L, num_pages=0, **ok) == 1
+    assert _paged(L, max_pages=1 << 25, page_size=64, **ok) == 1  # capacity beyond 2^30
+    assert _paged(L, Hq=6, Hkv=4, **ok) == 1
+    assert _paged(L, Hq=32, Hkv=2, **ok) == 2
+    assert _paged(L, d=96, k=8, **ok) == 2
+    assert _paged(L, kc_val_t=1, **ok) == 1
+    assert _paged(L, q=FAKE, q_idx=None, q_val=None, q_idx_t=7, o=None, **ok) == 1  # o missing
+
+
+def _append(L, **kw):
+    a = dict(k_new=FAKE, v_new=FAKE, n_new=None, seq_len=FAKE, B=2, Hkv=2, T=3, d=128, k=16,
+             block_table=None, max_pages=0, page_size=100, num_pages=0, kc_idx=FAKE, kc_val=FAKE,
+             v_cache=FAKE, kc_idx_t=1, kc_val_t=3, v_new_t=3, v_t=3, stream=None)
+    a.update(kw)
+    return L.sfa_kv_append(*a.values())
+
+
+def test_kv_append_validation(L):
+    assert _append(L, seq_len=None) == 1
+    assert _append(L, k_new=None) == 1
+    assert _append(L, kc_idx=None) == 1
+    assert _append(L, k=0) == 1
+    assert _append(L, k=129) == 1
+    assert _append(L, T=-1) == 1
+    assert _append(L, page_size=0) == 1
+    assert _append(L, block_table=FAKE, max_pages=0, num_pages=4) == 1
+    assert _append(L, block_table=FAKE, max_pages=1 << 21, num_pages=4, page_size=1024) == 1
+    assert _append(L, block_table=FAKE, max_pages=4, num_pages=4, page_size=48) == 1  # paged: power of two
+    assert _append(L, kc_idx_t=2) == 1
+    assert _append(L, v_new_t=0) == 1
+    assert _append(L, d=300, k=8) == 2

@@ -1,0 +1,256 @@
+"""GPU parity of KV-cache maintenance: sfa_kv_append (coded append into a
+contiguous or paged cache) and sfa_attn_decode_paged (decode through a block
+table, with the query given as codes or coded inside the kernel).
+
+Append is integer / bit work: the whole cache pool after a series of ragged
+appends must equal, bit for bit, the pool the oracle writes from the same
+inputs, sentinel slots included.  Paged decode must equal the contiguous
+decode on the same positions bit for bit (same chunks, same order), the
+in-kernel query coding the decode of sfa_topk_encode's codes, and both the
+oracle within the decode tolerances."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_22300_amd as sfa
+import sfa_inputs as si
+from helpers import TOL_O_BF16V, TOL_O_F32, check_lse, check_o, np_vals
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+IDX_NP = {torch.int16: np.int16, torch.int32: np.int32}
+
+
+def _pool(num_pages, Hkv, P, k, d, idx_dt, val_dt, v_dt):
+    """GPU pool filled with sentinels and its numpy twin for the oracle."""
+    ci = torch.full((num_pages, Hkv, P, k), -1, dtype=idx_dt, device=DEV)
+    cv = torch.full((num_pages, Hkv, P, k), -7.0, dtype=val_dt, device=DEV)
+    vc = torch.full((num_pages, Hkv, P, d), -7.0, dtype=v_dt, device=DEV)
+    return (ci, cv, vc), (ci.cpu().numpy(), np_vals(cv).copy(), np_vals(vc).copy())
+
+
+def _assert_pool_equal(gpu, ref, what):
+    for g, r, nm in zip(gpu, ref, ("kc_idx", "kc_val", "v_cache")):
+        got = g.cpu().numpy() if g.dtype not in (torch.bfloat16,) else np_vals(g)
+        bad = got != r
+        assert not bad.any(), f"{what} {nm}: {int(bad.sum())} entries differ, first at " \
+                              f"{np.argwhere(bad)[:3].tolist()}"
+
+
+@pytest.mark.parametrize("paged,idx_dt,val_dt,v_dt,vin_dt,d,k,P", [
+    (True, torch.int16, torch.bfloat16, torch.bfloat16, torch.bfloat16, 128, 16, 16),
+    (True, torch.int16, torch.bfloat16, torch.bfloat16, torch.float32, 128, 16, 64),
+    (True, torch.int32, torch.float32, torch.float32, torch.bfloat16, 64, 8, 32),
+    (True, torch.int16, torch.bfloat16, torch.bfloat16, torch.bfloat16, 200, 7, 8),  # d > 128
+    (False, torch.int16, torch.bfloat16, torch.bfloat16, torch.bfloat16, 128, 16, 300),
+    (False, torch.int32, torch.float32, torch.float32, torch.float32, 64, 64, 50),   # k = d
+])
+def test_append_matches_oracle(paged, idx_dt, val_dt, v_dt, vin_dt, d, k, P):
+    B, Hkv = 3, 2
+    max_pages = 5
+    rng = np.random.default_rng(d + k + P)
+    if paged:
+        num_pages = B * max_pages + 3
+        table_np = rng.permutation(num_pages)[:B * max_pages].reshape(B, max_pages).astype(np.int32)
+        table = torch.from_numpy(table_np).to(DEV)
+        cap = max_pages * P
+    else:
+        num_pages, table_np, table, cap = B, None, None, P
+    gpu, ref = _pool(num_pages, Hkv, P, k, d, idx_dt, val_dt, v_dt)
+    lens = torch.zeros(B, dtype=torch.int32, device=DEV)
+    lens_np = np.zeros(B, dtype=np.int64)
+    seed = 100 + d
+    for step, T in enumerate((37, 1, 0, 64, 5, 1, 90)):
+        kn = si.normal((B, Hkv, T, d), seed, "k_new", step, device=DEV)
+        vn = si.normal((B, Hkv, T, d), seed, "v_new", step, device=DEV).to(vin_dt)
+        n_new_np = rng.integers(0, T + 1, B).astype(np.int32)
+        n_new = torch.from_numpy(n_new_np).to(DEV)
+        sfa.sfa_kv_append(kn, vn, lens, *gpu, k=k, block_table=table, n_new=n_new)
+        lens_np = oracle.kv_append(*ref, kn.cpu().numpy(), np_vals(vn), lens_np, k,
+                                   table_np, P if paged else None, n_new_np)
+    torch.cuda.synchronize()
+    assert np.array_equal(lens.cpu().numpy(), lens_np), (lens.cpu().numpy(), lens_np)
+    assert (lens_np <= cap).all() and lens_np.max() > 0
+    _assert_pool_equal(gpu, ref, f"append paged={paged}")
+
+
+def test_append_capacity_and_pages_outside_the_pool():
+    B, Hkv, d, k, P = 2, 1, 128, 16, 16
+    table_np = np.array([[0, 1], [2, 9]], dtype=np.int32)  # page 9 lies outside a 3-page pool
+    gpu, ref = _pool(3, Hkv, P, k, d, torch.int16, torch.bfloat16, torch.bfloat16)
+    lens_np = np.array([20, -5], dtype=np.int64)
+    lens = torch.tensor(lens_np, dtype=torch.int32, device=DEV)
+    kn = si.normal((B, Hkv, 40, d), 9, "k_new", device=DEV)
+    vn = si.normal((B, Hkv, 40, d), 9, "v_new", device=DEV).to(torch.bfloat16)
+    sfa.sfa_kv_append(kn, vn, lens, *gpu, k=k, block_table=torch.from_numpy(table_np).to(DEV))
+    torch.cuda.synchronize()
+    want = oracle.kv_append(*ref, kn.cpu().numpy(), np_vals(vn), np.clip(lens_np, 0, None), k,
+                            table_np, P)
+    assert list(lens.cpu().numpy()) == [32, 32] == list(want)
+    _assert_pool_equal(gpu, ref, "append at capacity")
+
+
+def _paged_copy(ci, cv, vc, P, rng, spare=3):
+    """Scatter a contiguous cache [B, Hkv, Lmax, ...] into a shuffled page pool."""
+    B, Hkv, Lmax = ci.shape[:3]
+    max_pages = (Lmax + P - 1) // P
+    num_pages = B * max_pages + spare
+    table = rng.permutation(num_pages)[:B * max_pages].reshape(B, max_pages).astype(np.int32)
+    pools = []
+    for a in (ci, cv, vc):
+        pool = torch.zeros((num_pages, Hkv, P) + tuple(a.shape[3:]), dtype=a.dtype, device=DEV)
+        pad = max_pages * P - Lmax
+        src = torch.nn.functional.pad(a.float(), (0, 0, 0, pad)).to(a.dtype) if pad else a
+        src = src.reshape(B, Hkv, max_pages, P, -1).permute(0, 2, 1, 3, 4)
+        pool[torch.from_numpy(table.reshape(-1).astype(np.int64)).to(DEV)] = \
+            src.reshape(B * max_pages, Hkv, P, -1)
+        pools.append(pool)
+    return pools, torch.from_numpy(table).to(DEV)
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,Lmax,d,k,P,v_bf16,seq", [
+    (3, 8, 2, 300, 128, 16, 16, True, [300, 1, 157]),
+    (2, 4, 4, 5000, 64, 8, 64, False, None),          # several context chunks
+    (2, 8, 1, 4097, 128, 16, 256, True, [4097, 2049]),  # chunk boundaries, 8:1 groups
+    (2, 4, 1, 3000, 128, 8, 1024, True, [3000, 0]),   # an empty sequence; page > wave range
+    (1, 8, 4, 2500, 64, 32, 32, True, [2500]),
+    (3, 2, 2, 777, 128, 1, 16, True, [5, 777, 64]),   # k = 1, generic code path
+])
+def test_paged_decode(B, Hq, Hkv, Lmax, d, k, P, v_bf16, seq):
+    seed = Lmax + P
+    kd = torch.empty((B, Hkv, Lmax, d), device=DEV)
+    vdt = torch.bfloat16 if v_bf16 else torch.float32
+    vc = torch.empty((B, Hkv, Lmax, d), device=DEV, dtype=vdt)
+    for b in range(B):
+        for h in range(Hkv):
+            kd[b, h] = si.normal((Lmax, d), seed, "k", b, h, device=DEV)
+            vc[b, h] = si.normal((Lmax, d), seed, "v", b, h, device=DEV).to(vdt)
+    ci, cv = sfa.sfa_topk_encode(kd, k, idx_dtype=torch.int16, val_dtype=torch.bfloat16)
+    qd = si.normal((B, Hq, d), seed, "q", device=DEV)
+    qi, qv = sfa.sfa_topk_encode(qd, k)
+    seq_t = None if seq is None else torch.tensor(seq, dtype=torch.int32, device=DEV)
+    scale = 1.0 / math.sqrt(d)
+    rng = np.random.default_rng(seed)
+    (pi, pv, pvc), table = _paged_copy(ci, cv, vc, P, rng)
+    o_c, l_c = sfa.sfa_attn_decode(qi, qv, ci, cv, vc, seq_len=seq_t, scale=scale,
+                                   o_dtype=torch.float32)
+    # the paged pool's capacity rounds Lmax up to whole pages: give lengths
+    seq_p = seq_t if seq is not None else torch.full((B,), Lmax, dtype=torch.int32, device=DEV)
+    o_p, l_p = sfa.sfa_attn_decode_paged(pi, pv, pvc, table, seq_len=seq_p, q_idx=qi, q_val=qv,
+                                         scale=scale, o_dtype=torch.float32)
+    o_f, l_f = sfa.sfa_attn_decode_paged(pi, pv, pvc, table, seq_len=seq_p, q=qd, scale=scale,
+                                         o_dtype=torch.float32)
+    torch.cuda.synchronize()
+    # paged == contiguous and in-kernel query coding == separate coding, bit for bit
+    assert torch.equal(o_p, o_c) and torch.equal(l_p, l_c)
+    assert torch.equal(o_f, o_p) and torch.equal(l_f, l_p)
+    lens = np.full(B, Lmax) if seq is None else np.array(seq)
+    oqi, oqv = oracle.topk_encode(qd.cpu().numpy(), k)
+    oci, ocv = oracle.topk_encode_bf16(kd.cpu().numpy(), k)
+    O, L = oracle.attn_decode_paged(oqi, oqv, oci, ocv, np_vals(vc), lens, d, scale)
+    check_o(o_f, O, TOL_O_BF16V if v_bf16 else TOL_O_F32, "paged decode O")
+    live = lens > 0
+    check_lse(l_f[torch.from_numpy(live).to(DEV)], L[live], "paged decode LSE")
+    if not live.all():
+        assert (o_f[torch.from_numpy(~live).to(DEV)] == 0).all()
+        assert torch.isneginf(l_f[torch.from_numpy(~live).to(DEV)]).all()
+
+
+def test_generation_loop():
+    """Prefill a paged cache by one append, then decode token by token: each
+    step appends the new key and value and decodes the new dense query over the
+    grown cache, coded inside the kernel.  Every step equals the oracle's
+    causal forward row of that token (the token sees its own key)."""
+    B, Hq, Hkv, d, k, P, max_pages = 2, 8, 2, 128, 16, 16, 8
+    prompt, steps = 70, 6
+    n = prompt + steps
+    rng = np.random.default_rng(5)
+    num_pages = B * max_pages
+    table_np = rng.permutation(num_pages).reshape(B, max_pages).astype(np.int32)
+    table = torch.from_numpy(table_np).to(DEV)
+    (ci, cv, vc), _ = _pool(num_pages, Hkv, P, k, d, torch.int16, torch.bfloat16, torch.bfloat16)
+    kd = si.normal((B, Hkv, n, d), 5, "k", device=DEV)
+    vd = si.normal((B, Hkv, n, d), 5, "v", device=DEV).to(torch.bfloat16)
+    qd = si.normal((B, Hq, n, d), 5, "q", device=DEV)
+    lens = torch.zeros(B, dtype=torch.int32, device=DEV)
+    sfa.sfa_kv_append(kd[:, :, :prompt].contiguous(), vd[:, :, :prompt].contiguous(), lens,
+                      ci, cv, vc, k=k, block_table=table)
+    outs = []
+    for t in range(prompt, n):
+        sfa.sfa_kv_append(kd[:, :, t:t + 1].contiguous(), vd[:, :, t:t + 1].contiguous(), lens,
+                          ci, cv, vc, k=k, block_table=table)
+        o, lse = sfa.sfa_attn_decode_paged(ci, cv, vc, table, seq_len=lens,
+                                           q=qd[:, :, t].contiguous(), o_dtype=torch.float32)
+        outs.append((o.clone(), lse.clone()))
+    torch.cuda.synchronize()
+    assert list(lens.cpu().numpy()) == [n] * B
+    oqi, oqv = oracle.topk_encode(qd.cpu().numpy(), k)
+    oki, okv = oracle.topk_encode_bf16(kd.cpu().numpy(), k)
+    O, L = oracle.attn_fwd(oqi, oqv, oki, okv, np_vals(vd), d, 1 / math.sqrt(d), causal=True)
+    for s, (o, lse) in enumerate(outs):
+        t = prompt + s
+        check_o(o, O[:, :, t], TOL_O_BF16V, f"generation step {s} O")
+        check_lse(lse, L[:, :, t], f"generation step {s} LSE")
+
+
+def test_decode_64k_paged_full_size():
+    """The 64-sequence x 64K-token workload in a paged cache (256-token pages,
+    shuffled), filled by sfa_kv_append one sequence at a time from the dense
+    keys, decoded with in-kernel query coding.  The pool holds exactly what
+    sfa_topk_encode writes into the contiguous cache, and the decode equals the
+    contiguous decode bit for bit; the oracle checks sampled (sequence, head)
+    outputs."""
+    w = si.workload("decode_64k")
+    B, Hq, Hkv, L, d, k = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
+    P = 256
+    max_pages = L // P
+    rng = np.random.default_rng(64)
+    num_pages = B * max_pages
+    table_np = rng.permutation(num_pages).reshape(B, max_pages).astype(np.int32)
+    table = torch.from_numpy(table_np).to(DEV)
+    pi = torch.empty((num_pages, Hkv, P, k), dtype=torch.int16, device=DEV)
+    pv = torch.empty((num_pages, Hkv, P, k), dtype=torch.bfloat16, device=DEV)
+    pvc = torch.empty((num_pages, Hkv, P, d), dtype=torch.bfloat16, device=DEV)
+    ci = torch.empty((B, Hkv, L, k), dtype=torch.int16, device=DEV)
+    cv = torch.empty((B, Hkv, L, k), dtype=torch.bfloat16, device=DEV)
+    vc = torch.empty((B, Hkv, L, d), dtype=torch.bfloat16, device=DEV)
+    lens = torch.zeros(B, dtype=torch.int32, device=DEV)
+    kb = torch.empty((1, Hkv, L, d), device=DEV)
+    for b in range(B):
+        for h in range(Hkv):
+            kb[0, h] = si.normal((L, d), w.seed, "k", b, h, device=DEV)
+            vc[b, h] = si.normal((L, d), w.seed, "v", b, h, device=DEV).to(torch.bfloat16)
+        sfa.sfa_topk_encode(kb[0], k, idx=ci[b], val=cv[b])
+        sfa.sfa_kv_append(kb, vc[b:b + 1], lens[b:b + 1], pi, pv, pvc, k=k,
+                          block_table=table[b:b + 1])
+    del kb
+    torch.cuda.synchronize()
+    assert (lens == L).all()
+    tbl = table.long()
+    for b in (0, 31, 63):
+        got = pi[tbl[b]].permute(1, 0, 2, 3).reshape(Hkv, L, k)
+        assert torch.equal(got, ci[b]), f"appended codes of sequence {b}"
+        got = pv[tbl[b]].permute(1, 0, 2, 3).reshape(Hkv, L, k)
+        assert torch.equal(got, cv[b])
+        got = pvc[tbl[b]].permute(1, 0, 2, 3).reshape(Hkv, L, d)
+        assert torch.equal(got, vc[b])
+    qd = si.normal((B, Hq, d), w.seed, "q", device=DEV)
+    qi, qv = sfa.sfa_topk_encode(qd, k)
+    o_c, l_c = sfa.sfa_attn_decode(qi, qv, ci, cv, vc, scale=w.scale, o_dtype=torch.float32)
+    o_p, l_p = sfa.sfa_attn_decode_paged(pi, pv, pvc, table, seq_len=lens, q=qd, scale=w.scale,
+                                         o_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(o_p, o_c) and torch.equal(l_p, l_c)
+    oqi, oqv = oracle.topk_encode(qd.cpu().numpy(), k)
+    for (b, h) in [(0, 0), (17, 5), (63, 30)]:
+        g = h // w.G
+        kd = si.normal((L, d), w.seed, "k", b, g, device=DEV).cpu().numpy()
+        oci, ocv = oracle.topk_encode_bf16(kd, k)
+        qd1 = oracle.densify(oqi[b, h][None], oqv[b, h][None], d)
+        O, Lse = oracle.softmax_attention(qd1, oracle.densify(oci, ocv, d),
+                                          oracle.widen(np_vals(vc[b, g])), w.scale, False)
+        check_o(o_p[b, h][None], O, TOL_O_BF16V, f"paged decode O ({b},{h})")
+        check_lse(l_p[b, h].reshape(1), Lse, f"paged decode LSE ({b},{h})")
