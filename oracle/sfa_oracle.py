@@ -31,8 +31,10 @@ out in float64 with numpy:
   of a query or key coordinate equal to that of its code value on the
   support and zero elsewhere, i.e. the dense gradient read at the code's
   coordinates.
-* bf16 storage of code values (round to nearest, ties to even) for the
-  KV-cache codes.
+* bf16 and binary16 storage of code values (round to nearest, ties to even)
+  for the KV-cache codes and the compact format of App. J (8-bit indices,
+  fp16 values), and CSR rows of variable length (Sec. 2 sparse formats)
+  brought to fixed width.
 
 Parity pins for every function live in tests/test_oracle_*.py.
 """
@@ -50,10 +52,13 @@ def widen(a) -> np.ndarray:
 
     float32 / float64 arrays widen as usual; uint16 arrays are taken as
     bfloat16 bit patterns (sign, 8 exponent bits, 7 mantissa bits), whose
-    value is that of the float32 with the same high 16 bits."""
+    value is that of the float32 with the same high 16 bits; float16 arrays
+    are binary16 values, widened from their bits by definition."""
     a = np.asarray(a)
     if a.dtype == np.uint16:
         return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if a.dtype == np.float16:
+        return widen_f16(a.view(np.uint16))
     return a.astype(np.float64)
 
 
@@ -114,6 +119,59 @@ def bf16_rne(x: np.ndarray) -> np.ndarray:
     return out
 
 
+def f16_rne(x: np.ndarray) -> np.ndarray:
+    """IEEE binary16 bit patterns (uint16) of float32 values, rounded to nearest
+    with ties to even -- written from the definition.  binary16 has a 10-bit
+    fraction, exponents -14..15 for normal numbers and subnormals in steps of
+    2^-24.  Of the two representable values that bracket x, take the nearer; on
+    a tie the one whose last fraction bit is 0.  Magnitudes from
+    65504 + 16 (half an ulp past the largest finite value) on round to inf.
+    Finite inputs only."""
+    x = np.asarray(x, dtype=np.float32)
+    xv = np.abs(x.astype(np.float64))
+    sign = (x.view(np.uint32) >> 31).astype(np.uint16) << 15
+    # spacing of binary16 values at |x|: 2^(e - 10) for e = floor(log2|x|) >= -14,
+    # else the subnormal step 2^-24
+    with np.errstate(divide="ignore"):
+        e = np.floor(np.log2(np.where(xv > 0, xv, 1.0)))
+    e = np.maximum(e, -14.0)
+    step = np.exp2(e - 10)
+    lo = np.floor(xv / step) * step                  # exact: both are powers of two times integers
+    hi = lo + step
+    d_lo, d_hi = xv - lo, hi - xv
+    lo_units = np.round(lo / step).astype(np.int64)  # last fraction bit parity
+    take_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (lo_units % 2 == 1))
+    mag = np.where(take_hi, hi, lo)
+    # encode the magnitude: subnormal (mag < 2^-14) or normal
+    sub = mag < 2.0**-14
+    frac_sub = np.round(mag / 2.0**-24).astype(np.int64)
+    with np.errstate(divide="ignore"):
+        em = np.floor(np.log2(np.where(mag > 0, mag, 1.0)))
+    frac_n = np.round((mag / np.exp2(em) - 1.0) * 1024).astype(np.int64)
+    bits_n = ((em + 15).astype(np.int64) << 10) | frac_n
+    bits = np.where(sub, frac_sub, bits_n)
+    bits = np.where(mag > 65504.0, 0x7C00, bits)     # overflow to inf
+    return (bits.astype(np.uint16) | sign).astype(np.uint16)
+
+
+def widen_f16(bits: np.ndarray) -> np.ndarray:
+    """Exact float64 value of binary16 bit patterns, from the definition."""
+    b = np.asarray(bits).astype(np.int64)
+    sign = np.where(b & 0x8000, -1.0, 1.0)
+    ex = (b >> 10) & 0x1F
+    fr = (b & 0x3FF).astype(np.float64)
+    val = np.where(ex == 0, fr * 2.0**-24, (1.0 + fr / 1024.0) * np.exp2(ex - 15.0))
+    val = np.where(ex == 0x1F, np.where(fr == 0, np.inf, np.nan), val)
+    return sign * val
+
+
+def topk_encode_f16(x: np.ndarray, k: int):
+    """Top-k coding with the kept values stored as binary16 (selection on the
+    float32 magnitudes): (idx int64 [..., k], val float16 array)."""
+    idx, val = topk_encode(x, k)
+    return idx, f16_rne(val).view(np.float16)
+
+
 def topk_encode_bf16(x: np.ndarray, k: int):
     """Top-k coding with the kept values stored as bfloat16 (selection still on
     the float32 magnitudes): (idx int64 [..., k], val uint16 bf16 bits)."""
@@ -124,6 +182,47 @@ def topk_encode_bf16(x: np.ndarray, k: int):
 # --------------------------------------------------------------------------
 # attention on codes, Sec. 2 and Sec. 3.1-3.2
 # --------------------------------------------------------------------------
+
+
+# --------------------------------------------------------------------------
+# CSR code storage (Sec. 2 sparse formats; App. J memory formula): row r holds
+# the entries indptr[r] .. indptr[r+1]-1 of indices / values
+# --------------------------------------------------------------------------
+
+
+def csr_densify(indptr, indices, values, d: int) -> np.ndarray:
+    """float64 [rows, d] from a CSR matrix (values widened exactly)."""
+    indptr = np.asarray(indptr).astype(np.int64)
+    rows = indptr.size - 1
+    vals = widen(values)
+    out = np.zeros((rows, d))
+    for r in range(rows):
+        for t in range(indptr[r], indptr[r + 1]):
+            out[r, int(indices[t])] = vals[t]
+    return out
+
+
+def csr_to_fixed(indptr, indices, values, d: int, kmax: int):
+    """Fixed-width codes [rows, kmax] holding the same matrix as a CSR one whose
+    rows have at most kmax entries: each row's own entries, then zero-valued
+    entries at the lowest coordinates the row does not hold (the fewer-than-k
+    reading of Top-k coding), all sorted by ascending index.  Values keep their
+    storage type."""
+    indptr = np.asarray(indptr).astype(np.int64)
+    rows = indptr.size - 1
+    values = np.asarray(values)
+    idx = np.empty((rows, kmax), dtype=np.int64)
+    val = np.zeros((rows, kmax), dtype=values.dtype)
+    for r in range(rows):
+        own = [(int(indices[t]), values[t]) for t in range(indptr[r], indptr[r + 1])]
+        if len(own) > kmax:
+            raise ValueError("row longer than kmax")
+        held = {u for u, _ in own}
+        pad = [(u, values.dtype.type(0)) for u in range(d) if u not in held][:kmax - len(own)]
+        ent = sorted(own + pad, key=lambda e: e[0])
+        idx[r] = [u for u, _ in ent]
+        val[r] = [v for _, v in ent]
+    return idx, val
 
 
 def densify(idx: np.ndarray, val, d: int) -> np.ndarray:
