@@ -28,8 +28,12 @@
  *     be finite.  Violating these device-side preconditions gives undefined
  *     results (no fault: indices are masked into range before any access).
  *   - Grouped heads: query head h reads KV head h / (Hq / Hkv).
- *   - dtype codes below: index arrays are SFA_I32 or SFA_I16; value arrays
- *     are SFA_F32 or SFA_BF16 (bfloat16 bit patterns, 2 bytes).
+ *   - dtype codes below: code index arrays are SFA_I32, SFA_I16 or SFA_U8;
+ *     code value arrays are SFA_F32, SFA_BF16 (bfloat16 bit patterns) or
+ *     SFA_F16 (binary16); V and O are SFA_F32 or SFA_BF16.  Narrow formats
+ *     are written with round-to-nearest-even.
+ *   - Device pointers are at least 16-byte aligned (any torch allocation is);
+ *     the decode entry points check this for the cache arrays.
  */
 #ifndef SFA_H
 #define SFA_H
@@ -51,7 +55,12 @@ typedef enum {
   SFA_ENOSPC = 4   /* the caller's workspace is smaller than required      */
 } sfa_status;
 
-typedef enum { SFA_I32 = 0, SFA_I16 = 1, SFA_F32 = 2, SFA_BF16 = 3 } sfa_dtype;
+/* SFA_U8 (8-bit unsigned indices) and SFA_F16 (IEEE binary16 values) are the
+ * compact code storage of App. J (int8 indices, fp16 values): for code arrays
+ * only, not for V or O. */
+typedef enum {
+  SFA_I32 = 0, SFA_I16 = 1, SFA_F32 = 2, SFA_BF16 = 3, SFA_U8 = 4, SFA_F16 = 5
+} sfa_dtype;
 
 /* Version of this ABI (incremented on any incompatible change). */
 int sfa_abi_version(void);
@@ -66,11 +75,12 @@ const char* sfa_strerror(int status);
  *      |x_u|; ties go to the lower index (the paper leaves ties open).
  *      Magnitudes are compared as exact float32 values: subnormals are
  *      ordered, never flushed; +0 and -0 tie.
- * idx  [rows, k] of idx_t (SFA_I32 or SFA_I16; SFA_I16 needs d <= 32767):
+ * idx  [rows, k] of idx_t (SFA_I32, SFA_I16 or SFA_U8; d <= 256 fits all):
  *      the kept coordinates in ascending order.
- * val  [rows, k] of val_t: SFA_F32 copies x_u bit for bit; SFA_BF16 stores
- *      x_u rounded to nearest-even bfloat16 (selection still uses the
- *      float32 magnitudes).
+ * val  [rows, k] of val_t: SFA_F32 copies x_u bit for bit; SFA_BF16 and
+ *      SFA_F16 store x_u rounded to nearest-even bfloat16 / binary16
+ *      (selection still uses the float32 magnitudes; binary16 overflows to
+ *      +-inf beyond 65504 and keeps subnormals).
  * Limits: 1 <= d <= 256, 1 <= k <= d, rows >= 0 (rows == 0 is a no-op).
  * Errors: SFA_EINVAL (null pointer with rows > 0, k or d out of range,
  *         bad dtype), SFA_ENOTSUP (d > 256), SFA_EHIP.
@@ -234,6 +244,31 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val,
                            int v_t, int o_t,
                            void* o, float* lse,
                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * CSR code storage to fixed-width codes (Sec. 2, sparse formats; App. J: the
+ * paper stores codes as CSR with int32 indptr, int8 indices, fp16 values).
+ *
+ * indptr   [rows + 1] int32 on the device: row r holds entries
+ *          indptr[r] .. indptr[r+1]-1 of indices / values, at most kmax of
+ *          them, with distinct indices in [0, d) (any order).
+ * indices  [nnz] of indices_t (SFA_I32 | SFA_I16 | SFA_U8).
+ * values   [nnz] of values_t (SFA_F32 | SFA_BF16 | SFA_F16).
+ * idx, val [rows, kmax] of idx_t / values_t: each row's own entries plus
+ *          zero-valued entries at the lowest coordinates it does not hold,
+ *          kmax in all, in ascending index order.  Values are copied bit for
+ *          bit.  The result is the same matrix as the CSR input, in the form
+ *          every attention entry point takes (with k = kmax); rows shorter
+ *          than kmax are padded the way Top-k coding treats rows with fewer
+ *          than k nonzeros.
+ * Rows longer than kmax keep their first kmax entries; indices outside
+ * [0, d) are ignored (violated preconditions: undefined results, no fault).
+ * Limits: 1 <= kmax <= d <= 256; rows >= 0 (0 is a no-op).
+ * Errors: SFA_EINVAL, SFA_ENOTSUP (d > 256), SFA_EHIP.
+ */
+sfa_status sfa_csr_to_codes(const int32_t* indptr, const void* indices, int indices_t,
+                            const void* values, int values_t, int64_t rows, int d, int kmax,
+                            void* idx, int idx_t, void* val, void* stream);
 
 /*
  * KV-cache maintenance for decode (App. B: generation extends the cache by

@@ -353,7 +353,7 @@ def kv_append(kc_idx, kc_val, v_cache, k_new, v_new, seq_len, k: int, block_tabl
     For each sequence b and t < n_new[b] (all T when n_new is None), the key
     row k_new[b, h, t] (float32, d wide) is coded by Top-k (Sec. 3.1): kept
     coordinates ascending, values stored as bf16 bits when kc_val holds
-    uint16, else as float32 copies.  Code and value row v_new[b, h, t] go to
+    uint16, binary16 when it holds float16, else as float32 copies.  Code and value row v_new[b, h, t] go to
     position seq_len[b] + t of sequence b in every KV head h; a bf16 V cache
     stores bf16_rne of float32 values, a float32 one widens bf16 bits
     exactly.  Positions at or past the capacity, and pages outside the pool,
@@ -365,7 +365,7 @@ def kv_append(kc_idx, kc_val, v_cache, k_new, v_new, seq_len, k: int, block_tabl
     npages = np.shape(kc_idx)[0]
     lens = np.asarray(seq_len).astype(np.int64)
     cnt = np.full(B, T) if n_new is None else np.clip(np.asarray(n_new), 0, T)
-    bf16_codes = np.asarray(kc_val).dtype == np.uint16
+    code_dt = np.asarray(kc_val).dtype  # uint16: bf16 bits; float16: binary16
     v_new = np.asarray(v_new)
     for b in range(B):
         for t in range(int(cnt[b])):
@@ -376,8 +376,10 @@ def kv_append(kc_idx, kc_val, v_cache, k_new, v_new, seq_len, k: int, block_tabl
             if not 0 <= page < npages:
                 continue
             for h in range(Hkv):
-                if bf16_codes:
+                if code_dt == np.uint16:
                     ci, cv = topk_encode_bf16(k_new[b, h, t], k)
+                elif code_dt == np.float16:
+                    ci, cv = topk_encode_f16(k_new[b, h, t], k)
                 else:
                     ci, cv = topk_encode(k_new[b, h, t], k)
                 kc_idx[page, h, slot] = ci

@@ -19,12 +19,13 @@ __all__ = [
     "sfa_topk_encode", "sfa_attn_fwd_workspace", "sfa_attn_fwd", "sfa_attn_fwd_index",
     "sfa_attn_bwd_workspace", "sfa_attn_bwd",
     "sfa_attn_decode_workspace", "sfa_attn_decode", "sfa_attn_decode_paged", "sfa_kv_append",
+    "sfa_csr_to_codes",
     "SFA_OK", "SFA_EINVAL", "SFA_ENOTSUP", "SFA_EHIP", "SFA_ENOSPC",
-    "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16",
+    "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16", "SFA_U8", "SFA_F16",
 ]
 
 SFA_OK, SFA_EINVAL, SFA_ENOTSUP, SFA_EHIP, SFA_ENOSPC = 0, 1, 2, 3, 4
-SFA_I32, SFA_I16, SFA_F32, SFA_BF16 = 0, 1, 2, 3
+SFA_I32, SFA_I16, SFA_F32, SFA_BF16, SFA_U8, SFA_F16 = 0, 1, 2, 3, 4, 5
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 library_path = os.path.join(_HERE, "libsfa.so")
@@ -78,6 +79,8 @@ def lib() -> ctypes.CDLL:
         L.sfa_kv_append.restype = i32
         L.sfa_kv_append.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp, i32, i32, i32,
                                     vp, vp, vp, i32, i32, i32, i32, vp]
+        L.sfa_csr_to_codes.restype = i32
+        L.sfa_csr_to_codes.argtypes = [vp, vp, i32, vp, i32, i64, i32, i32, vp, i32, vp, vp]
         _lib = L
     return _lib
 
@@ -90,7 +93,9 @@ def sfa_strerror(status: int) -> str:
     return lib().sfa_strerror(status).decode()
 
 
-_IDX = {torch.int32: SFA_I32, torch.int16: SFA_I16}
+# code indices; code values; V and O
+_IDX = {torch.int32: SFA_I32, torch.int16: SFA_I16, torch.uint8: SFA_U8}
+_CVAL = {torch.float32: SFA_F32, torch.bfloat16: SFA_BF16, torch.float16: SFA_F16}
 _VAL = {torch.float32: SFA_F32, torch.bfloat16: SFA_BF16}
 
 
@@ -126,7 +131,7 @@ def sfa_topk_encode(x: torch.Tensor, k: int, idx_dtype=torch.int32, val_dtype=to
     if val is None:
         val = torch.empty(x.shape[:-1] + (k,), dtype=val_dtype, device=x.device)
     it = _check(idx, "idx", _IDX)
-    vt = _check(val, "val", _VAL)
+    vt = _check(val, "val", _CVAL)
     if idx.numel() != rows * k or val.numel() != rows * k:
         raise ValueError("idx/val must hold rows * k elements")
     _call(lib().sfa_topk_encode(x.data_ptr(), rows, d, k, idx.data_ptr(), it, val.data_ptr(), vt,
@@ -166,7 +171,7 @@ def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, wa
     if q_idx.dtype != k_idx.dtype or q_val.dtype != k_val.dtype:
         raise TypeError("query and key codes must share index and value dtypes")
     it = _check(q_idx, "q_idx", _IDX); _check(k_idx, "k_idx", _IDX)
-    qt = _check(q_val, "q_val", _VAL); _check(k_val, "k_val", _VAL)
+    qt = _check(q_val, "q_val", _CVAL); _check(k_val, "k_val", _CVAL)
     vt = _check(v, "v", _VAL)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
@@ -220,7 +225,7 @@ def sfa_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, causal: bool = Tru
     if q_idx.dtype != k_idx.dtype or q_val.dtype != k_val.dtype or o.dtype != dout.dtype:
         raise TypeError("query/key codes, and o/dout, must share dtypes")
     it = _check(q_idx, "q_idx", _IDX); _check(k_idx, "k_idx", _IDX)
-    qt = _check(q_val, "q_val", _VAL); _check(k_val, "k_val", _VAL)
+    qt = _check(q_val, "q_val", _CVAL); _check(k_val, "k_val", _CVAL)
     vt = _check(v, "v", _VAL)
     ot = _check(o, "o", _VAL); _check(dout, "dout", _VAL)
     _check(lse, "lse", {torch.float32: SFA_F32})
@@ -262,8 +267,8 @@ def sfa_attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len=None, scale: 
     if tuple(q_val.shape) != (B, Hq, k) or tuple(kc_idx.shape) != (B, Hkv, Lmax, k) \
             or tuple(kc_val.shape) != (B, Hkv, Lmax, k) or tuple(v_cache.shape) != (B, Hkv, Lmax, d):
         raise ValueError("inconsistent shapes")
-    qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _VAL)
-    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _VAL)
+    qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _CVAL)
+    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _CVAL)
     vt = _check(v_cache, "v_cache", _VAL)
     sp = 0
     if seq_len is not None:
@@ -314,7 +319,7 @@ def sfa_kv_append(k_new, v_new, seq_len, kc_idx, kc_val, v_cache, k: int, block_
     vnt = _check(v_new, "v_new", _VAL)
     if tuple(v_new.shape) != (B, Hkv, T, d):
         raise ValueError("v_new must match k_new")
-    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _VAL)
+    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _CVAL)
     vt = _check(v_cache, "v_cache", _VAL)
     npg, P = kc_idx.shape[0], kc_idx.shape[2]
     if tuple(kc_idx.shape) != (npg, Hkv, P, k) or tuple(kc_val.shape) != (npg, Hkv, P, k) \
@@ -349,7 +354,7 @@ def sfa_attn_decode_paged(kc_idx, kc_val, v_cache, block_table, seq_len=None, q=
     d = v_cache.shape[-1]
     if tuple(kc_val.shape) != (npg, Hkv, P, k) or tuple(v_cache.shape) != (npg, Hkv, P, d):
         raise ValueError("inconsistent cache shapes")
-    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _VAL)
+    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _CVAL)
     vt = _check(v_cache, "v_cache", _VAL)
     _check(block_table, "block_table", {torch.int32: SFA_I32})
     if block_table.dim() != 2:
@@ -366,7 +371,7 @@ def sfa_attn_decode_paged(kc_idx, kc_val, v_cache, block_table, seq_len=None, q=
         Hq = q.shape[1]
         qp = q.data_ptr()
     else:
-        qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _VAL)
+        qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _CVAL)
         if q_idx.dim() != 3 or tuple(q_idx.shape) != (B, q_idx.shape[1], k) \
                 or tuple(q_val.shape) != tuple(q_idx.shape):
             raise ValueError("q codes must be [B, Hq, k]")
@@ -396,3 +401,30 @@ def sfa_attn_decode_paged(kc_idx, kc_val, v_cache, block_table, seq_len=None, q=
                                       ws.numel() * ws.element_size(), _stream(v_cache)),
           "sfa_attn_decode_paged")
     return o, lse
+
+
+def sfa_csr_to_codes(indptr, indices, values, d: int, kmax: int, idx_dtype=None, idx=None,
+                     val=None):
+    """CSR codes (indptr int32 [rows + 1], indices [nnz], values [nnz]) to fixed
+    rows (idx [rows, kmax] of idx_dtype, default the indices' dtype; val
+    [rows, kmax] of the values' dtype), padded with zeros at the lowest free
+    coordinates.  Returns (idx, val)."""
+    _check(indptr, "indptr", {torch.int32: SFA_I32})
+    if indptr.dim() != 1 or indptr.numel() < 1:
+        raise ValueError("indptr must be 1-D with rows + 1 entries")
+    rows = indptr.numel() - 1
+    iit = _check(indices, "indices", _IDX)
+    vit = _check(values, "values", _CVAL)
+    if idx is None:
+        idx = torch.empty((rows, kmax), dtype=idx_dtype or indices.dtype, device=indptr.device)
+    if val is None:
+        val = torch.empty((rows, kmax), dtype=values.dtype, device=indptr.device)
+    it = _check(idx, "idx", _IDX)
+    if _check(val, "val", _CVAL) != vit:
+        raise TypeError("val must have the values' dtype")
+    if idx.numel() != rows * kmax or val.numel() != rows * kmax:
+        raise ValueError("idx and val must hold rows * kmax entries")
+    _call(lib().sfa_csr_to_codes(indptr.data_ptr(), indices.data_ptr(), iit, values.data_ptr(),
+                                 vit, rows, d, kmax, idx.data_ptr(), it, val.data_ptr(),
+                                 _stream(indptr)), "sfa_csr_to_codes")
+    return idx, val

@@ -72,7 +72,7 @@ struct BwdParams {
   unsigned char* qimg;
   unsigned char* kimg;
   int Hq, Hkv, G, n, k, causal;
-  int idx16, valbf16, vbf16, obf16;
+  int ifmt, vfmt, vbf16, obf16;
   int nt;    // tiles per head: ceil(n / 32)
   int BR;    // query positions per dq workgroup: 256 / G
   int nqb;   // dq workgroups per (batch, KV head)
@@ -155,9 +155,9 @@ __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
   for (int e = tid; e < kT * k; e += 256) {
     const int r = e / k;
     if (t * kT + r >= n) break;
-    const int f = load_idx(p.q_idx, r0 * k + e, p.idx16, D - 1);
+    const int f = load_idx(p.q_idx, r0 * k + e, p.ifmt, D - 1);
     uint16_t h, l;
-    split2(load_val(p.q_val, r0 * k + e, p.valbf16), h, l);
+    split2(load_val(p.q_val, r0 * k + e, p.vfmt), h, l);
     rmq[r * I::RP + f] = h;
     rmq[r * I::RP + D + f] = l;
     trq[f * kTP + r] = h;
@@ -212,9 +212,9 @@ __global__ __launch_bounds__(256) void sfa_bwd_kprep_kernel(BwdParams p) {
   for (int e = tid; e < kT * k; e += 256) {
     const int r = e / k;
     if (t * kT + r >= n) break;
-    const int f = load_idx(p.k_idx, r0 * k + e, p.idx16, D - 1);
+    const int f = load_idx(p.k_idx, r0 * k + e, p.ifmt, D - 1);
     uint16_t h, l;
-    split2(load_val(p.k_val, r0 * k + e, p.valbf16), h, l);
+    split2(load_val(p.k_val, r0 * k + e, p.vfmt), h, l);
     rmk[r * I::RP + f] = h;
     rmk[r * I::RP + D + f] = l;
     trk[f * kTP + r] = h;
@@ -373,7 +373,7 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
     if (wave / 4 == round && row_ok) {
       const int64_t row = ((int64_t)b * p.Hq + hq) * n + my_i;
       for (int t = hh; t < p.k; t += 2) {
-        const int u = load_idx(p.q_idx, row * p.k + t, p.idx16, D - 1);
+        const int u = load_idx(p.q_idx, row * p.k + t, p.ifmt, D - 1);
         p.dq[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
       }
     }
@@ -551,7 +551,7 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
       if (wave / 4 == round && key_ok) {
         const int64_t row = (int64_t)bh * n + my_j;
         for (int t = hh; t < p.k; t += 2) {
-          const int u = load_idx(p.k_idx, row * p.k + t, p.idx16, D - 1);
+          const int u = load_idx(p.k_idx, row * p.k + t, p.ifmt, D - 1);
           p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
         }
       }
@@ -608,13 +608,13 @@ size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d) {
 hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, const void* o, const float* lse,
                            const void* dout, int B, int Hq, int Hkv, int n, int d, int k,
-                           int causal, float scale, int idx16, int valbf16, int vbf16, int obf16,
+                           int causal, float scale, int ifmt, int vfmt, int vbf16, int obf16,
                            float* dq, float* dk, float* dv, void* ws, hipStream_t stream) {
   BwdParams p;
   p.q_idx = q_idx; p.q_val = q_val; p.k_idx = k_idx; p.k_val = k_val; p.v = v; p.o = o;
   p.lse = lse; p.dout = dout; p.dq = dq; p.dk = dk; p.dv = dv;
   p.Hq = Hq; p.Hkv = Hkv; p.G = Hq / Hkv; p.n = n; p.k = k; p.causal = causal;
-  p.idx16 = idx16; p.valbf16 = valbf16; p.vbf16 = vbf16; p.obf16 = obf16;
+  p.ifmt = ifmt; p.vfmt = vfmt; p.vbf16 = vbf16; p.obf16 = obf16;
   p.nt = (n + kT - 1) / kT;
   p.BR = kNWQ * kT / p.G;
   p.nqb = (n + p.BR - 1) / p.BR;

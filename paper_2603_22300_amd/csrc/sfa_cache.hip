@@ -84,8 +84,8 @@ __global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
 #pragma unroll
       for (int e = 0; e < E; ++e)
         if (sel[e] && sl[e] < a.k)
-          store_code(a.kc_idx, a.kc_val, crow * a.k + sl[e], lane + 64 * e, bits[e], a.idx16,
-                     a.valbf16);
+          store_code(a.kc_idx, a.kc_val, crow * a.k + sl[e], lane + 64 * e, bits[e], a.ifmt,
+                     a.vfmt);
       // value row (bf16 cache from float32 values: round to nearest even)
       const int64_t vo = crow * a.d;
 #pragma unroll

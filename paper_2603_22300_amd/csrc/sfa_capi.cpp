@@ -4,6 +4,7 @@
 #include <math.h>
 
 #include "../../include/sfa.h"
+#include "sfa_device.h"
 #include "sfa_launch.h"
 
 namespace {
@@ -11,8 +12,13 @@ namespace {
 constexpr int kAbiVersion = 3;
 constexpr int kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
 
-bool is_idx(int t) { return t == SFA_I32 || t == SFA_I16; }
+// index arrays of codes; values of codes; V and O
+bool is_idx(int t) { return t == SFA_I32 || t == SFA_I16 || t == SFA_U8; }
+bool is_cval(int t) { return t == SFA_F32 || t == SFA_BF16 || t == SFA_F16; }
 bool is_val(int t) { return t == SFA_F32 || t == SFA_BF16; }
+// kernel-side format codes (sfa_device.h)
+int ifmt_of(int t) { return t == SFA_I16 ? sfa::kIdxI16 : (t == SFA_U8 ? sfa::kIdxU8 : sfa::kIdxI32); }
+int vfmt_of(int t) { return t == SFA_BF16 ? sfa::kValBF16 : (t == SFA_F16 ? sfa::kValF16 : sfa::kValF32); }
 bool pow2_le(int g, int maxg) { return g >= 1 && g <= maxg && (g & (g - 1)) == 0; }
 
 sfa_status from_hip(hipError_t e) { return e == hipSuccess ? SFA_OK : SFA_EHIP; }
@@ -37,13 +43,13 @@ const char* sfa_strerror(int status) {
 sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k, void* idx, int idx_t,
                            void* val, int val_t, void* stream) {
   if (rows < 0 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
-  if (!is_idx(idx_t) || !is_val(val_t)) return SFA_EINVAL;
+  if (!is_idx(idx_t) || !is_cval(val_t)) return SFA_EINVAL;
   if (d > 256) return SFA_ENOTSUP;
   if (rows == 0) return SFA_OK;
   if (!x || !idx || !val) return SFA_EINVAL;
   if ((rows + 3) / 4 > 0x7fffffffLL) return SFA_ENOTSUP;
-  return from_hip(sfa::launch_topk_encode(x, rows, d, k, idx, idx_t == SFA_I16, val,
-                                          val_t == SFA_BF16, (hipStream_t)stream));
+  return from_hip(sfa::launch_topk_encode(x, rows, d, k, idx, ifmt_of(idx_t), val,
+                                          vfmt_of(val_t), (hipStream_t)stream));
 }
 
 namespace {
@@ -54,7 +60,7 @@ sfa_status check_fwd(const void* q_idx, const void* q_val, const void* k_idx, co
   if (!q_idx || !q_val || !k_idx || !k_val || !v || !o) return SFA_EINVAL;
   if (B < 1 || Hq < 1 || Hkv < 1 || n < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
   if (Hq % Hkv != 0) return SFA_EINVAL;
-  if (!is_idx(idx_t) || !is_val(qk_val_t) || !is_val(v_t) || !is_val(o_t)) return SFA_EINVAL;
+  if (!is_idx(idx_t) || !is_cval(qk_val_t) || !is_val(v_t) || !is_val(o_t)) return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
   if (d != 64 && d != 128) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
@@ -81,8 +87,8 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
   const size_t need = sfa::fwd_workspace_bytes(B, Hkv, n, d, v_t == SFA_BF16);
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
-                                       causal != 0, scale, idx_t == SFA_I16,
-                                       qk_val_t == SFA_BF16, v_t == SFA_BF16, o_t == SFA_BF16,
+                                       causal != 0, scale, ifmt_of(idx_t),
+                                       vfmt_of(qk_val_t), v_t == SFA_BF16, o_t == SFA_BF16,
                                        o, lse, ws, (hipStream_t)stream));
 }
 
@@ -103,8 +109,8 @@ sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
   if (!pow2_le(Hq / Hkv, sfa::bwd_max_group())) return SFA_ENOTSUP;
   if (ws == nullptr || ws_bytes < sfa::bwd_workspace_bytes(B, Hq, Hkv, n, d)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n,
-                                       d, k, causal != 0, scale, idx_t == SFA_I16,
-                                       qk_val_t == SFA_BF16, v_t == SFA_BF16, o_t == SFA_BF16,
+                                       d, k, causal != 0, scale, ifmt_of(idx_t),
+                                       vfmt_of(qk_val_t), v_t == SFA_BF16, o_t == SFA_BF16,
                                        dq_val, dk_val, dv, ws, (hipStream_t)stream));
 }
 
@@ -119,8 +125,8 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val, const void* 
   if (k > sfa::fwd_index_max_k()) return SFA_ENOTSUP;
   if (sfa::fwd_index_lds_bytes(d, k, v_t == SFA_BF16) > kMaxLds) return SFA_ENOTSUP;
   return from_hip(sfa::launch_attn_fwd_index(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
-                                             causal != 0, scale, idx_t == SFA_I16,
-                                             qk_val_t == SFA_BF16, v_t == SFA_BF16,
+                                             causal != 0, scale, ifmt_of(idx_t),
+                                             vfmt_of(qk_val_t), v_t == SFA_BF16,
                                              o_t == SFA_BF16, o, lse, (hipStream_t)stream));
 }
 
@@ -138,20 +144,21 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
   if (!q_idx || !q_val || !kc_idx || !kc_val || !v_cache || !o || !ws) return SFA_EINVAL;
   if (B < 1 || Hq < 1 || Hkv < 1 || Lmax < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
   if (Hq % Hkv != 0) return SFA_EINVAL;
-  if (!is_idx(q_idx_t) || !is_val(q_val_t) || !is_idx(kc_idx_t) || !is_val(kc_val_t) ||
+  if (!is_idx(q_idx_t) || !is_cval(q_val_t) || !is_idx(kc_idx_t) || !is_cval(kc_val_t) ||
       !is_val(v_t) || !is_val(o_t))
     return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
   if (d != 64 && d != 128) return SFA_ENOTSUP;
   if (!pow2_le(Hq / Hkv, sfa::decode_max_group())) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  if (((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0) return SFA_EINVAL;
   if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
   sfa::DecodeArgs a = {};
   a.q_idx = q_idx; a.q_val = q_val; a.kc_idx = kc_idx; a.kc_val = kc_val; a.v = v_cache;
   a.seq_len = seq_len;
   a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lmax = Lmax; a.d = d; a.k = k; a.scale = scale;
-  a.qidx16 = q_idx_t == SFA_I16; a.qvalbf16 = q_val_t == SFA_BF16;
-  a.kidx16 = kc_idx_t == SFA_I16; a.kvalbf16 = kc_val_t == SFA_BF16;
+  a.qifmt = ifmt_of(q_idx_t); a.qvfmt = vfmt_of(q_val_t);
+  a.kifmt = ifmt_of(kc_idx_t); a.kvfmt = vfmt_of(kc_val_t);
   a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;
   a.o = o; a.lse = lse; a.ws = ws;
   return from_hip(sfa::launch_attn_decode(a, (hipStream_t)stream));
@@ -172,14 +179,15 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
   if (page_size < 16 || (page_size & (page_size - 1)) != 0) return SFA_EINVAL;
   if ((long long)max_pages * page_size > (1LL << 30)) return SFA_EINVAL;
   if (Hq % Hkv != 0) return SFA_EINVAL;
-  if ((!dense_q && (!is_idx(q_idx_t) || !is_val(q_val_t))) || !is_idx(kc_idx_t) ||
-      !is_val(kc_val_t) || !is_val(v_t) || !is_val(o_t))
+  if ((!dense_q && (!is_idx(q_idx_t) || !is_cval(q_val_t))) || !is_idx(kc_idx_t) ||
+      !is_cval(kc_val_t) || !is_val(v_t) || !is_val(o_t))
     return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
   if (d != 64 && d != 128) return SFA_ENOTSUP;
   if (!pow2_le(Hq / Hkv, sfa::decode_max_group())) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
   const int Lmax = max_pages * page_size;
+  if (((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0) return SFA_EINVAL;
   if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
   int log2P = 0;
   while ((1 << log2P) < page_size) ++log2P;
@@ -189,8 +197,8 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
   a.seq_len = seq_len; a.table = block_table;
   a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lmax = Lmax; a.d = d; a.k = k; a.scale = scale;
   a.max_pages = max_pages; a.log2P = log2P; a.num_pages = num_pages;
-  a.qidx16 = !dense_q && q_idx_t == SFA_I16; a.qvalbf16 = !dense_q && q_val_t == SFA_BF16;
-  a.kidx16 = kc_idx_t == SFA_I16; a.kvalbf16 = kc_val_t == SFA_BF16;
+  a.qifmt = dense_q ? 0 : ifmt_of(q_idx_t); a.qvfmt = dense_q ? 0 : vfmt_of(q_val_t);
+  a.kifmt = ifmt_of(kc_idx_t); a.kvfmt = vfmt_of(kc_val_t);
   a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;
   a.o = o; a.lse = lse; a.ws = ws;
   return from_hip(sfa::launch_attn_decode(a, (hipStream_t)stream));
@@ -207,7 +215,7 @@ sfa_status sfa_kv_append(const float* k_new, const void* v_new, const int32_t* n
   if (block_table && (max_pages < 1 || num_pages < 1)) return SFA_EINVAL;
   if (block_table && (long long)max_pages * page_size > (1LL << 30)) return SFA_EINVAL;
   if (block_table && (page_size & (page_size - 1)) != 0) return SFA_EINVAL;
-  if (!is_idx(kc_idx_t) || !is_val(kc_val_t) || !is_val(v_new_t) || !is_val(v_t))
+  if (!is_idx(kc_idx_t) || !is_cval(kc_val_t) || !is_val(v_new_t) || !is_val(v_t))
     return SFA_EINVAL;
   if (kc_idx_t == SFA_I16 && d > 32767) return SFA_EINVAL;
   if (d > 256) return SFA_ENOTSUP;
@@ -218,9 +226,25 @@ sfa_status sfa_kv_append(const float* k_new, const void* v_new, const int32_t* n
   a.B = B; a.Hkv = Hkv; a.T = T; a.d = d; a.k = k;
   a.page_size = page_size; a.max_pages = max_pages; a.num_pages = num_pages;
   while ((1 << a.log2P) < page_size) ++a.log2P;
-  a.idx16 = kc_idx_t == SFA_I16; a.valbf16 = kc_val_t == SFA_BF16;
+  a.ifmt = ifmt_of(kc_idx_t); a.vfmt = vfmt_of(kc_val_t);
   a.vin_bf16 = v_new_t == SFA_BF16; a.vc_bf16 = v_t == SFA_BF16;
   return from_hip(sfa::launch_kv_append(a, (hipStream_t)stream));
+}
+
+sfa_status sfa_csr_to_codes(const int32_t* indptr, const void* indices, int indices_t,
+                            const void* values, int values_t, int64_t rows, int d, int kmax,
+                            void* idx, int idx_t, void* val, void* stream) {
+  if (rows < 0 || d < 1 || kmax < 1 || kmax > d) return SFA_EINVAL;
+  if (!is_idx(indices_t) || !is_idx(idx_t) || !is_cval(values_t)) return SFA_EINVAL;
+  if (d > 256) return SFA_ENOTSUP;
+  if (rows == 0) return SFA_OK;
+  if (!indptr || !indices || !values || !idx || !val) return SFA_EINVAL;
+  if ((rows + 3) / 4 > 0x7fffffffLL) return SFA_ENOTSUP;
+  sfa::CsrArgs a = {};
+  a.indptr = indptr; a.indices = indices; a.values = values; a.rows = rows; a.d = d;
+  a.kmax = kmax; a.ifmt_in = ifmt_of(indices_t); a.vbytes = values_t == SFA_F32 ? 4 : 2;
+  a.idx_out = idx; a.ifmt_out = ifmt_of(idx_t); a.val_out = val;
+  return from_hip(sfa::launch_csr_to_codes(a, (hipStream_t)stream));
 }
 
 }  // extern "C"

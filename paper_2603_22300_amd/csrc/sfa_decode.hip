@@ -44,7 +44,7 @@ struct DecParams {
   float* ws_o;  // [B*Hq, nch, D]
   int Hq, Hkv, Lmax, k, nch;
   float scale_log2;
-  int qidx16, qvalbf16, kidx16, kvalbf16;
+  int qifmt, qvfmt, kifmt, kvfmt;
   const float* q_dense;   // [B, Hq, D] or null (then q_idx / q_val)
   const int32_t* table;   // paged: [B, max_pages]
   int max_pages, log2P, num_pages;
@@ -56,11 +56,12 @@ __device__ __forceinline__ int seq_len_of(const int32_t* seq_len, int b, int Lma
   return L < 0 ? 0 : (L > Lmax ? Lmax : L);
 }
 
-// KC8 > 0: cache codes are int16 indices and bf16 values with k = 8 * KC8,
+// KC8 > 0: cache codes with k = 8 * KC8 in one of two compact formats --
+// int16 indices with bf16 values, or (C8) uint8 indices with float16 values --
 // loaded as 16-byte vectors and prefetched one 64-key sub-block ahead, with
 // the sub-block's V (bf16) in flight during its score phase.  KC8 = 0: any
 // format and k, element loads issued as a batch per sub-block.
-template <int D, int G, bool VBF16, int KC8, bool PAGED>
+template <int D, int G, bool VBF16, int KC8, bool C8, bool PAGED>
 __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   constexpr int DL = D / 8;     // lanes covering one key's D values (8 each)
   constexpr int KPL = 64 / DL;  // keys per wave-wide V load
@@ -104,8 +105,8 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
     for (int x = tid; x < G * k; x += kDecThreads) {
       const int h = x / k, t = x - h * k;
       const int64_t qi = ((int64_t)b * p.Hq + hkv * G + h) * k + t;
-      const int u = load_idx(p.q_idx, qi, p.qidx16, dmask);
-      qd[u][h] = load_val(p.q_val, qi, p.qvalbf16);
+      const int u = load_idx(p.q_idx, qi, p.qifmt, dmask);
+      qd[u][h] = load_val(p.q_val, qi, p.qvfmt);
     }
   }
   __syncthreads();
@@ -185,13 +186,28 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
 
   if constexpr (KC8 > 0) {
     // ---------------- vectorized, prefetched path ----------------
-    uint4 cidx[KC8], cval[KC8];
+    // a key's codes as 32-bit words: indices (2 or 4 per word), values (2 per word)
+    constexpr int NIW = C8 ? 2 * KC8 : 4 * KC8, NVW = 4 * KC8;
+    uint32_t cidx[NIW], cval[NVW];
     auto load_codes = [&](int sb) {
       const int64_t row = row_of(min(sb + lane, w1 - 1));
-      const uint4* pi = (const uint4*)((const int16_t*)p.kc_idx + row * (8 * KC8));
-      const uint4* pv = (const uint4*)((const uint16_t*)p.kc_val + row * (8 * KC8));
+      const uint32_t* pi = (const uint32_t*)((const unsigned char*)p.kc_idx + row * (4 * NIW));
+      const uint32_t* pv = (const uint32_t*)((const unsigned char*)p.kc_val + row * (4 * NVW));
+      if constexpr (NIW % 4 == 0) {
 #pragma unroll
-      for (int c = 0; c < KC8; ++c) { cidx[c] = pi[c]; cval[c] = pv[c]; }
+        for (int c = 0; c < NIW / 4; ++c) {
+          const uint4 w = ((const uint4*)pi)[c];
+          cidx[4 * c] = w.x; cidx[4 * c + 1] = w.y; cidx[4 * c + 2] = w.z; cidx[4 * c + 3] = w.w;
+        }
+      } else {
+        const uint2 w = *(const uint2*)pi;
+        cidx[0] = w.x; cidx[1] = w.y;
+      }
+#pragma unroll
+      for (int c = 0; c < NVW / 4; ++c) {
+        const uint4 w = ((const uint4*)pv)[c];
+        cval[4 * c] = w.x; cval[4 * c + 1] = w.y; cval[4 * c + 2] = w.z; cval[4 * c + 3] = w.w;
+      }
     };
     if (w0 < w1) load_codes(w0);
     for (int sb = w0; sb < w1; sb += 64) {
@@ -208,16 +224,13 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
 #pragma unroll
       for (int h = 0; h < G; ++h) s[h] = 0.f;
 #pragma unroll
-      for (int c = 0; c < KC8; ++c) {
-        const uint32_t iw[4] = {cidx[c].x, cidx[c].y, cidx[c].z, cidx[c].w};
-        const uint32_t vw[4] = {cval[c].x, cval[c].y, cval[c].z, cval[c].w};
+      for (int e = 0; e < 8 * KC8; ++e) {
+        const int u = (C8 ? (int)((cidx[e >> 2] >> (8 * (e & 3))) & 0xffu)
+                          : (int)((cidx[e >> 1] >> (16 * (e & 1))) & 0xffffu)) & dmask;
+        const uint32_t h16 = (e & 1) ? (cval[e >> 1] >> 16) : (cval[e >> 1] & 0xffffu);
+        const float kv = C8 ? f16_bits_to_f32(h16) : __uint_as_float(h16 << 16);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int u = (int)((iw[e >> 1] >> (16 * (e & 1))) & 0xffffu) & dmask;
-          const float kv = __uint_as_float((e & 1) ? (vw[e >> 1] & 0xffff0000u) : (vw[e >> 1] << 16));
-#pragma unroll
-          for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
-        }
+        for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
       }
       softmax_block(s, sb + lane < w1);
       if (sb + 64 < w1) load_codes(sb + 64);  // next sub-block's codes during P.V
@@ -243,8 +256,8 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
       for (int h = 0; h < G; ++h) s[h] = 0.f;
       const int64_t cbase = row_of(j) * k;
       for (int t = 0; t < k; ++t) {
-        const int u = load_idx(p.kc_idx, cbase + t, p.kidx16, dmask);
-        const float kv = load_val(p.kc_val, cbase + t, p.kvalbf16);
+        const int u = load_idx(p.kc_idx, cbase + t, p.kifmt, dmask);
+        const float kv = load_val(p.kc_val, cbase + t, p.kvfmt);
 #pragma unroll
         for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
       }
@@ -344,24 +357,30 @@ size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d) {
   return (size_t)B * Hq * nch * (size_t)(d + 2) * sizeof(float);
 }
 
-template <int D, int G, bool VBF16, int KC8>
+template <int D, int G, bool VBF16, int KC8, bool C8>
 static void launch_dec_t(const DecParams& p, int B, hipStream_t stream) {
   dim3 grid(p.nch, B * p.Hkv), block(kDecThreads);
   if (p.table)
-    hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8, true>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8, C8, true>), grid, block, 0, stream, p);
   else
-    hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8, false>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8, C8, false>), grid, block, 0, stream, p);
 }
 
 template <int D, int G, bool VBF16>
 static void launch_dec_kc(const DecParams& p, int B, hipStream_t stream) {
-  const bool vec = VBF16 && p.kidx16 && p.kvalbf16;
   if constexpr (VBF16) {
-    if (vec && p.k == 8) return launch_dec_t<D, G, VBF16, 1>(p, B, stream);
-    if (vec && p.k == 16) return launch_dec_t<D, G, VBF16, 2>(p, B, stream);
-    if (vec && p.k == 32) return launch_dec_t<D, G, VBF16, 4>(p, B, stream);
+    if (p.kifmt == kIdxI16 && p.kvfmt == kValBF16) {
+      if (p.k == 8) return launch_dec_t<D, G, VBF16, 1, false>(p, B, stream);
+      if (p.k == 16) return launch_dec_t<D, G, VBF16, 2, false>(p, B, stream);
+      if (p.k == 32) return launch_dec_t<D, G, VBF16, 4, false>(p, B, stream);
+    }
+    if (p.kifmt == kIdxU8 && p.kvfmt == kValF16) {
+      if (p.k == 8) return launch_dec_t<D, G, VBF16, 1, true>(p, B, stream);
+      if (p.k == 16) return launch_dec_t<D, G, VBF16, 2, true>(p, B, stream);
+      if (p.k == 32) return launch_dec_t<D, G, VBF16, 4, true>(p, B, stream);
+    }
   }
-  launch_dec_t<D, G, VBF16, 0>(p, B, stream);
+  launch_dec_t<D, G, VBF16, 0, false>(p, B, stream);
 }
 
 template <int D, bool VBF16>
@@ -387,7 +406,7 @@ hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   p.ws_l = p.ws_m + nslot;
   p.ws_o = p.ws_l + nslot;
   p.scale_log2 = (float)((double)a.scale * 1.4426950408889634);
-  p.qidx16 = a.qidx16; p.qvalbf16 = a.qvalbf16; p.kidx16 = a.kidx16; p.kvalbf16 = a.kvalbf16;
+  p.qifmt = a.qifmt; p.qvfmt = a.qvfmt; p.kifmt = a.kifmt; p.kvfmt = a.kvfmt;
   p.q_dense = a.q_dense;
   p.table = a.table;
   p.max_pages = a.max_pages; p.log2P = a.log2P; p.num_pages = a.num_pages;

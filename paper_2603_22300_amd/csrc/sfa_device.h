@@ -50,16 +50,31 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-// Loads of one code element by dtype flag (index: int32 / int16; value:
-// float32 / bfloat16).  Indices are masked into [0, dmask] so a violated
-// precondition cannot address outside the kernel's tables.
-__device__ __forceinline__ int load_idx(const void* p, int64_t i, int idx16, int dmask) {
-  int v = idx16 ? (int)((const int16_t*)p)[i] : ((const int32_t*)p)[i];
+// Storage formats of code arrays: indices int32 / int16 / uint8, values
+// float32 / bfloat16 / float16 (IEEE binary16).
+enum : int { kIdxI32 = 0, kIdxI16 = 1, kIdxU8 = 2 };
+enum : int { kValF32 = 0, kValBF16 = 1, kValF16 = 2 };
+
+__host__ __device__ constexpr int idx_bytes(int f) { return f == kIdxI32 ? 4 : (f == kIdxI16 ? 2 : 1); }
+__host__ __device__ constexpr int val_bytes(int f) { return f == kValF32 ? 4 : 2; }
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t h16) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h16);
+}
+
+// Loads of one code element by format.  Indices are masked into [0, dmask]
+// so a violated precondition cannot address outside the kernel's tables.
+__device__ __forceinline__ int load_idx(const void* p, int64_t i, int ifmt, int dmask) {
+  const int v = ifmt == kIdxI16 ? (int)((const int16_t*)p)[i]
+              : ifmt == kIdxU8 ? (int)((const uint8_t*)p)[i]
+                               : ((const int32_t*)p)[i];
   return v & dmask;
 }
 
-__device__ __forceinline__ float load_val(const void* p, int64_t i, int valbf16) {
-  return valbf16 ? bf16_bits_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
+__device__ __forceinline__ float load_val(const void* p, int64_t i, int vfmt) {
+  if (vfmt == kValBF16) return bf16_bits_to_f32(((const uint16_t*)p)[i]);
+  if (vfmt == kValF16) return f16_bits_to_f32(((const uint16_t*)p)[i]);
+  return ((const float*)p)[i];
 }
 
 }  // namespace sfa

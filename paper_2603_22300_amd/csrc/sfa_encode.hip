@@ -14,7 +14,7 @@ namespace sfa {
 template <int E>  // coordinates per lane: d <= 64 * E
 __global__ __launch_bounds__(256) void topk_encode_kernel(
     const float* __restrict__ x, int64_t rows, int d, int k,
-    void* __restrict__ idx_out, int idx16, void* __restrict__ val_out, int valbf16) {
+    void* __restrict__ idx_out, int ifmt, void* __restrict__ val_out, int vfmt) {
   const int lane = threadIdx.x & 63;
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   // the wave index is made visibly uniform so that the row walk and the
@@ -49,22 +49,22 @@ __global__ __launch_bounds__(256) void topk_encode_kernel(
 #pragma unroll
     for (int e = 0; e < E; ++e)
       if (sel[e] && slot[e] < k)  // exactly k are kept; the bound only hardens the store
-        store_code(idx_out, val_out, o0 + slot[e], lane + 64 * e, bits[e], idx16, valbf16);
+        store_code(idx_out, val_out, o0 + slot[e], lane + 64 * e, bits[e], ifmt, vfmt);
   }
 }
 
 hipError_t launch_topk_encode(const float* x, int64_t rows, int d, int k, void* idx,
-                              int idx16, void* val, int valbf16, hipStream_t stream) {
+                              int ifmt, void* val, int vfmt, hipStream_t stream) {
   // persistent waves: up to 32 per compute unit, 4 per workgroup
   const int64_t need = (rows + 3) / 4;
   const int64_t cap = 256 * 8;
   dim3 grid((unsigned)(need < cap ? need : cap)), block(256);
   if (d <= 64)
-    hipLaunchKernelGGL(topk_encode_kernel<1>, grid, block, 0, stream, x, rows, d, k, idx, idx16, val, valbf16);
+    hipLaunchKernelGGL(topk_encode_kernel<1>, grid, block, 0, stream, x, rows, d, k, idx, ifmt, val, vfmt);
   else if (d <= 128)
-    hipLaunchKernelGGL(topk_encode_kernel<2>, grid, block, 0, stream, x, rows, d, k, idx, idx16, val, valbf16);
+    hipLaunchKernelGGL(topk_encode_kernel<2>, grid, block, 0, stream, x, rows, d, k, idx, ifmt, val, vfmt);
   else
-    hipLaunchKernelGGL(topk_encode_kernel<4>, grid, block, 0, stream, x, rows, d, k, idx, idx16, val, valbf16);
+    hipLaunchKernelGGL(topk_encode_kernel<4>, grid, block, 0, stream, x, rows, d, k, idx, ifmt, val, vfmt);
   return hipGetLastError();
 }
 

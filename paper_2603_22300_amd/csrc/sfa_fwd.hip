@@ -54,7 +54,7 @@ struct FwdParams {
   float* lse;
   int Hq, Hkv, n, k, causal;
   float scale_log2;  // scale * log2(e)
-  int idx16, valbf16, obf16;
+  int ifmt, vfmt, obf16;
   int G, BR, nqb;
   float inv_k;
   // bf16 V, prepared once per call (sfa_fwd_prep_kernel): every key tile as
@@ -214,8 +214,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       if (i < n) {
         const int hq = hkv * p.G + r / p.BR;
         const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
-        const int f = load_idx(p.q_idx, gi, p.idx16, dmask);
-        Qs[r * QP + f] = bf16_piece(qsign * load_val(p.q_val, gi, p.valbf16), pc);
+        const int f = load_idx(p.q_idx, gi, p.ifmt, dmask);
+        Qs[r * QP + f] = bf16_piece(qsign * load_val(p.q_val, gi, p.vfmt), pc);
       }
     }
     __syncthreads();
@@ -256,7 +256,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // Uniform per-(batch, KV head) bases; per-lane offsets fit 32 bits (n*d and
   // n*k are at most 2^29, checked on the host), so the loads take the form
   // scalar base + 32-bit vector offset.
-  const unsigned isz = p.idx16 ? 2u : 4u, ksz = p.valbf16 ? 2u : 4u;
+  const unsigned isz = idx_bytes(p.ifmt), ksz = val_bytes(p.vfmt);
   const unsigned char* kidx_b = (const unsigned char*)p.k_idx + kv_base * k * isz;
   const unsigned char* kval_b = (const unsigned char*)p.k_val + kv_base * k * ksz;
   const unsigned char* v_b = (const unsigned char*)p.v + kv_base * D * (VBF16 ? 2 : 4);
@@ -277,16 +277,22 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
         ge[r] = (uint32_t)(j * k + (k_off[r] - row * k));
       }
     }
-    if (p.idx16) {
+    if (p.ifmt == kIdxI16) {
 #pragma unroll
       for (int r = 0; r < KEL; ++r) kf[r] = *(const int16_t*)(kidx_b + ge[r] * 2u);
+    } else if (p.ifmt == kIdxU8) {
+#pragma unroll
+      for (int r = 0; r < KEL; ++r) kf[r] = *(const uint8_t*)(kidx_b + ge[r]);
     } else {
 #pragma unroll
       for (int r = 0; r < KEL; ++r) kf[r] = *(const int32_t*)(kidx_b + ge[r] * 4u);
     }
-    if (p.valbf16) {
+    if (p.vfmt == kValBF16) {
 #pragma unroll
       for (int r = 0; r < KEL; ++r) kx[r] = __uint_as_float((uint32_t)*(const uint16_t*)(kval_b + ge[r] * 2u) << 16);
+    } else if (p.vfmt == kValF16) {
+#pragma unroll
+      for (int r = 0; r < KEL; ++r) kx[r] = f16_bits_to_f32(*(const uint16_t*)(kval_b + ge[r] * 2u));
     } else {
 #pragma unroll
       for (int r = 0; r < KEL; ++r) kx[r] = *(const float*)(kval_b + ge[r] * 4u);
@@ -743,7 +749,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
 template <int D>
 __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
     const void* __restrict__ k_idx, const void* __restrict__ k_val, const uint16_t* __restrict__ v,
-    int n, int k, int idx16, int valbf16, int vtiles, unsigned char* __restrict__ ws_tiles,
+    int n, int k, int ifmt, int vfmt, int vtiles, unsigned char* __restrict__ ws_tiles,
     int* __restrict__ ws_flag) {
   constexpr int KR = Geo<D, 2>::KR, VP = kBC + 4, SB = stage_bytes<D, true>();
   __shared__ __attribute__((aligned(16))) uint16_t T[SB / 2];
@@ -756,8 +762,8 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
   for (int e = tid; e < kBC * k; e += 256) {
     const int j = e / k;
     if (j0 + j >= n) break;
-    const int f = load_idx(k_idx, c0 + e, idx16, D - 1);
-    const float x = load_val(k_val, c0 + e, valbf16);
+    const int f = load_idx(k_idx, c0 + e, ifmt, D - 1);
+    const float x = load_val(k_val, c0 + e, vfmt);
     T[j * KR + f] = bf16_piece(x, 0);
     T[j * KR + D + f] = bf16_piece(x, 1);
   }
@@ -835,14 +841,14 @@ size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16) {
 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
-                           int k, int causal, float scale, int idx16, int valbf16, int vbf16,
+                           int k, int causal, float scale, int ifmt, int vfmt, int vbf16,
                            int obf16, void* o, float* lse, void* ws, hipStream_t stream) {
   FwdParams p;
   p.q_idx = q_idx; p.q_val = q_val; p.k_idx = k_idx; p.k_val = k_val; p.v = v;
   p.o = o; p.lse = lse;
   p.Hq = Hq; p.Hkv = Hkv; p.n = n; p.k = k; p.causal = causal;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
-  p.idx16 = idx16; p.valbf16 = valbf16; p.obf16 = obf16;
+  p.ifmt = ifmt; p.vfmt = vfmt; p.obf16 = obf16;
   p.G = Hq / Hkv;
   p.BR = 0; p.nqb = 0;
   p.inv_k = 1.0f / (float)k;
@@ -856,11 +862,11 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
     dim3 grid(p.vtiles, B * Hkv), block(256);
     if (d == 64)
       hipLaunchKernelGGL(sfa_fwd_prep_kernel<64>, grid, block, 0, stream, k_idx, k_val,
-                         (const uint16_t*)v, n, k, idx16, valbf16, p.vtiles, (unsigned char*)ws,
+                         (const uint16_t*)v, n, k, ifmt, vfmt, p.vtiles, (unsigned char*)ws,
                          (int*)p.ws_flag);
     else
       hipLaunchKernelGGL(sfa_fwd_prep_kernel<128>, grid, block, 0, stream, k_idx, k_val,
-                         (const uint16_t*)v, n, k, idx16, valbf16, p.vtiles, (unsigned char*)ws,
+                         (const uint16_t*)v, n, k, ifmt, vfmt, p.vtiles, (unsigned char*)ws,
                          (int*)p.ws_flag);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -44,7 +44,7 @@ struct FwdParams {
   float* lse;
   int Hq, Hkv, n, k, causal;
   float scale_log2;  // scale * log2(e)
-  int idx16, valbf16, obf16;
+  int ifmt, vfmt, obf16;
   int G, BR, nqb;
   float inv_k;
 };
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
       const int i = i0 + rho % p.BR;
       if (i < n) {
         const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
-        const int f = load_idx(p.q_idx, gi, p.idx16, dmask);
+        const int f = load_idx(p.q_idx, gi, p.ifmt, dmask);
         q_f[r] = f;
         q_slot[r] = (int)atomicAdd(&cnt[f], 1u);
       }
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
       const int hq = hkv * p.G + rho / p.BR;
       const int i = i0 + rho % p.BR;
       const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
-      const float qv = load_val(p.q_val, gi, p.valbf16);
+      const float qv = load_val(p.q_val, gi, p.vfmt);
       const uint32_t rowbyte = (uint32_t)(rho * kSP * 4);
       qent[koff[q_f[r]] + q_slot[r]] = make_uint2(rowbyte | ((uint32_t)q_f[r] << 16), __float_as_uint(qv));
     }
@@ -242,8 +242,8 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
         const int j = j0 + c;
         if (j < n) {
           const int64_t gi = (kv_base + j) * k + t;
-          k_f[r] = load_idx(p.k_idx, gi, p.idx16, dmask);
-          k_v[r] = load_val(p.k_val, gi, p.valbf16);
+          k_f[r] = load_idx(p.k_idx, gi, p.ifmt, dmask);
+          k_v[r] = load_val(p.k_val, gi, p.vfmt);
           k_slot[r] = (int)atomicAdd(&cnt[k_f[r]], 1u);
         }
       }
@@ -411,14 +411,14 @@ int fwd_index_max_k() { return kMaxK; }
 
 hipError_t launch_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n,
-                           int d, int k, int causal, float scale, int idx16, int valbf16,
+                           int d, int k, int causal, float scale, int ifmt, int vfmt,
                            int vbf16, int obf16, void* o, float* lse, hipStream_t stream) {
   FwdParams p;
   p.q_idx = q_idx; p.q_val = q_val; p.k_idx = k_idx; p.k_val = k_val; p.v = v;
   p.o = o; p.lse = lse;
   p.Hq = Hq; p.Hkv = Hkv; p.n = n; p.k = k; p.causal = causal;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
-  p.idx16 = idx16; p.valbf16 = valbf16; p.obf16 = obf16;
+  p.ifmt = ifmt; p.vfmt = vfmt; p.obf16 = obf16;
   p.G = Hq / Hkv;
   p.BR = kRows / p.G;
   p.nqb = (n + p.BR - 1) / p.BR;

@@ -8,12 +8,12 @@
 
 namespace sfa {
 
-hipError_t launch_topk_encode(const float* x, int64_t rows, int d, int k, void* idx, int idx16,
-                              void* val, int valbf16, hipStream_t stream);
+hipError_t launch_topk_encode(const float* x, int64_t rows, int d, int k, void* idx, int ifmt,
+                              void* val, int vfmt, hipStream_t stream);
 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
-                           int k, int causal, float scale, int idx16, int valbf16, int vbf16,
+                           int k, int causal, float scale, int ifmt, int vfmt, int vbf16,
                            int obf16, void* o, float* lse, void* ws, hipStream_t stream);
 int fwd_max_group();
 size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16);
@@ -21,14 +21,14 @@ size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16);
 hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, const void* o, const float* lse,
                            const void* dout, int B, int Hq, int Hkv, int n, int d, int k,
-                           int causal, float scale, int idx16, int valbf16, int vbf16, int obf16,
+                           int causal, float scale, int ifmt, int vfmt, int vbf16, int obf16,
                            float* dq, float* dk, float* dv, void* ws, hipStream_t stream);
 size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d);
 int bwd_max_group();
 
 hipError_t launch_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,
                                  const void* k_val, const void* v, int B, int Hq, int Hkv, int n,
-                                 int d, int k, int causal, float scale, int idx16, int valbf16,
+                                 int d, int k, int causal, float scale, int ifmt, int vfmt,
                                  int vbf16, int obf16, void* o, float* lse, hipStream_t stream);
 int fwd_index_lds_bytes(int d, int k, int vbf16);
 int fwd_index_max_k();
@@ -45,7 +45,7 @@ struct DecodeArgs {
   int B, Hq, Hkv, Lmax, d, k;
   int max_pages, log2P, num_pages;
   float scale;
-  int qidx16, qvalbf16, kidx16, kvalbf16, vbf16, obf16;
+  int qifmt, qvfmt, kifmt, kvfmt, vbf16, obf16;
   void* o;
   float* lse;
   void* ws;
@@ -67,8 +67,23 @@ struct AppendArgs {
   int B, Hkv, T, d, k;
   int page_size, max_pages, num_pages;
   int log2P;  // paged: page_size == 1 << log2P
-  int idx16, valbf16, vin_bf16, vc_bf16;
+  int ifmt, vfmt, vin_bf16, vc_bf16;
 };
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
+
+// CSR codes (row r: entries indptr[r] .. indptr[r+1]-1) to fixed rows of kmax
+// entries, padded with zero values at the lowest free coordinates.
+struct CsrArgs {
+  const int32_t* indptr;
+  const void* indices;
+  const void* values;
+  int64_t rows;
+  int d, kmax;
+  int ifmt_in, vbytes;  // index format; value storage bytes (copied bitwise)
+  void* idx_out;
+  int ifmt_out;
+  void* val_out;
+};
+hipError_t launch_csr_to_codes(const CsrArgs& a, hipStream_t stream);
 
 }  // namespace sfa

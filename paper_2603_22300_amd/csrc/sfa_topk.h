@@ -75,12 +75,15 @@ __device__ __forceinline__ void topk_slots(const bool (&sel)[E], int (&slot)[E])
   }
 }
 
-// Stores of one code entry in the requested formats.
+// Stores of one code entry in the requested formats (bf16 and float16
+// values round to nearest even).
 __device__ __forceinline__ void store_code(void* idx_out, void* val_out, int64_t pos, int u,
-                                           uint32_t bits, int idx16, int valbf16) {
-  if (idx16) ((int16_t*)idx_out)[pos] = (int16_t)u;
+                                           uint32_t bits, int ifmt, int vfmt) {
+  if (ifmt == kIdxI16) ((int16_t*)idx_out)[pos] = (int16_t)u;
+  else if (ifmt == kIdxU8) ((uint8_t*)idx_out)[pos] = (uint8_t)u;
   else ((int32_t*)idx_out)[pos] = u;
-  if (valbf16) ((uint16_t*)val_out)[pos] = (uint16_t)f32_to_bf16_rne(__uint_as_float(bits));
+  if (vfmt == kValBF16) ((uint16_t*)val_out)[pos] = (uint16_t)f32_to_bf16_rne(__uint_as_float(bits));
+  else if (vfmt == kValF16) ((_Float16*)val_out)[pos] = (_Float16)__uint_as_float(bits);
   else ((uint32_t*)val_out)[pos] = bits;
 }
 

@@ -23,5 +23,6 @@ from .gen import (  # noqa: F401
     zipf_codes,
     dense_from_codes,
     tie_rows,
+    random_csr,
 )
 from .configs import WORKLOADS, Workload, workload  # noqa: F401

@@ -129,3 +129,18 @@ def tie_rows(d: int, seed: int) -> np.ndarray:
         r[j[:, 0]] = np.where(rng.integers(0, 2, size=d // 4) == 1, 1, -1) * np.abs(r[j[:, 1]])
         rows.append(r.astype(np.float32))
     return np.stack(rows).astype(np.float32)
+
+
+def random_csr(rows: int, d: int, kmax: int, seed: int, *tags, min_len: int = 0):
+    """A random CSR sparsity structure with values: row lengths uniform in
+    [min_len, kmax] (row 0 empty and the last row full when rows > 1), distinct
+    coordinates per row in random order, N(0,1) float32 values.  Returns numpy
+    (indptr int32 [rows + 1], indices int64 [nnz], values float32 [nnz])."""
+    rng = np.random.default_rng(slice_seed(seed, "csr", *tags))
+    lens = rng.integers(min_len, kmax + 1, rows)
+    if rows > 1:
+        lens[0], lens[-1] = min_len, kmax
+    indptr = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    indices = np.concatenate([rng.permutation(d)[:m] for m in lens] or [np.zeros(0)])
+    values = rng.standard_normal(int(indptr[-1])).astype(np.float32)
+    return indptr, indices.astype(np.int64), values

@@ -194,3 +194,32 @@ def test_kv_append_validation(L):
     assert _append(L, kc_idx_t=2) == 1
     assert _append(L, v_new_t=0) == 1
     assert _append(L, d=300, k=8) == 2
+
+
+def _csr(L, **kw):
+    a = dict(indptr=FAKE, indices=FAKE, indices_t=4, values=FAKE, values_t=5, rows=10, d=128,
+             kmax=16, idx=FAKE, idx_t=4, val=FAKE, stream=None)
+    a.update(kw)
+    return L.sfa_csr_to_codes(*a.values())
+
+
+def test_csr_to_codes_validation(L):
+    assert _csr(L, rows=0, indptr=None) == 0      # empty: no-op before pointer checks
+    assert _csr(L, indptr=None) == 1
+    assert _csr(L, kmax=0) == 1
+    assert _csr(L, kmax=129) == 1                 # kmax > d
+    assert _csr(L, rows=-1) == 1
+    assert _csr(L, indices_t=2) == 1              # a value dtype as index dtype
+    assert _csr(L, values_t=0) == 1               # an index dtype as value dtype
+    assert _csr(L, idx_t=5) == 1
+    assert _csr(L, d=300, kmax=8) == 2
+
+
+def test_compact_dtypes_accepted_for_codes_only(L):
+    # U8 indices / F16 code values pass validation of the forward up to the
+    # workspace check; F16 is not a V or O dtype
+    assert _fwd(L, idx_t=4, qk_val_t=5, ws_bytes=ctypes.c_size_t(0)) == 4
+    assert _fwd(L, idx_t=4, qk_val_t=5, v_t=5) == 1
+    assert _fwd(L, o_t=5) == 1
+    assert _dec(L, kc_idx_t=4, kc_val_t=5, ws_bytes=1) == 4
+    assert _dec(L, v_t=5) == 1
