@@ -380,10 +380,16 @@ def cpu_baseline_fwd(w, q, k, v, budget_rows=256, seed=0):
 # decode workload
 # ----------------------------------------------------------------------------
 
-def bench_decode(w, steps, warmup, want_cpu):
+CODE_FORMATS = {"i16bf16": (torch.int16, torch.bfloat16), "u8f16": (torch.uint8, torch.float16)}
+_CODE_NAMES = {"i16bf16": "int16/bf16", "u8f16": "uint8/float16"}
+
+
+def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16"):
     B, Hq, Hkv, L, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
-    ci = torch.empty((B, Hkv, L, kk), dtype=torch.int16, device=DEV)
-    cv = torch.empty((B, Hkv, L, kk), dtype=torch.bfloat16, device=DEV)
+    idt, vdt = CODE_FORMATS[codes]
+    cbytes = kk * (idt.itemsize + vdt.itemsize)  # cache code bytes per key
+    ci = torch.empty((B, Hkv, L, kk), dtype=idt, device=DEV)
+    cv = torch.empty((B, Hkv, L, kk), dtype=vdt, device=DEV)
     vc = torch.empty((B, Hkv, L, d), dtype=torch.bfloat16, device=DEV)
     for b in range(B):
         for h in range(Hkv):
@@ -411,16 +417,18 @@ def bench_decode(w, steps, warmup, want_cpu):
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
-    algo_bytes = B * Hkv * L * (kk * 4 + d * 2) + B * Hq * (kk * 8 + d * 2 + 4)
+    algo_bytes = B * Hkv * L * (cbytes + d * 2) + B * Hq * (kk * 8 + d * 2 + 4)
     achieved = algo_bytes / (ms * 1e-3)
     out = {
-        "metric": "SFA decode tokens/s, 64 seqs x 64K sparse-code cache (k=16 int16/bf16, d=128), 32/8 heads",
+        "metric": f"SFA decode tokens/s, 64 seqs x 64K sparse-code cache (k=16 {_CODE_NAMES[codes]}, "
+                  "d=128), 32/8 heads",
         "value": B / (ms * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "L": L, "d": d, "k": kk,
+                   "cache_codes": codes,
                    "step": "sfa_attn_decode (split context + LSE merge)"},
         "roofline": {"kernel": "sfa_decode_kernel + combine", "bound": "hbm",
                      "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
@@ -430,7 +438,7 @@ def bench_decode(w, steps, warmup, want_cpu):
     return out
 
 
-def bench_decode_paged(w, steps, warmup):
+def bench_decode_paged(w, steps, warmup, codes="i16bf16"):
     """Serving step over a paged cache: append each sequence's new key (coded on
     append) and value, then decode the new dense query (coded inside the decode
     kernel) over the grown cache.  The cache is first filled by sfa_kv_append,
@@ -445,8 +453,10 @@ def bench_decode_paged(w, steps, warmup):
     g = torch.Generator(device="cpu")
     g.manual_seed(si.slice_seed(w.seed, "block_table"))
     table = torch.randperm(num_pages, generator=g).reshape(B, max_pages).to(torch.int32).to(DEV)
-    ci = torch.empty((num_pages, Hkv, P, kk), dtype=torch.int16, device=DEV)
-    cv = torch.empty((num_pages, Hkv, P, kk), dtype=torch.bfloat16, device=DEV)
+    idt, vdt = CODE_FORMATS[codes]
+    cbytes = kk * (idt.itemsize + vdt.itemsize)  # cache code bytes per key
+    ci = torch.empty((num_pages, Hkv, P, kk), dtype=idt, device=DEV)
+    cv = torch.empty((num_pages, Hkv, P, kk), dtype=vdt, device=DEV)
     vc = torch.empty((num_pages, Hkv, P, d), dtype=torch.bfloat16, device=DEV)
     lens = torch.zeros(B, dtype=torch.int32, device=DEV)
     kb = torch.empty((1, Hkv, L, d), device=DEV)
@@ -464,7 +474,7 @@ def bench_decode_paged(w, steps, warmup):
         if b > 0:  # the first call pays the module load
             app_ms += e0.elapsed_time(e1)
     del kb, vb
-    app_bytes = Hkv * L * (d * 4 + d * 2 + kk * 4 + d * 2)  # per prefill call
+    app_bytes = Hkv * L * (d * 4 + d * 2 + cbytes + d * 2)  # per prefill call
     app_rate = app_bytes / (app_ms / (B - 1) * 1e-3)
     # per-step inputs: one new token per sequence, the new dense queries
     kn = si.normal((B, Hkv, 1, d), w.seed, "k_step", device=DEV)
@@ -499,17 +509,18 @@ def bench_decode_paged(w, steps, warmup):
     ms = t0.elapsed_time(t1) / steps
     dec_ms = sum(a.elapsed_time(b) for a, b in evs) / steps
     ctx = L + warmup + (steps + 1) / 2.0  # mean context length over the timed steps
-    dec_bytes = B * Hkv * ctx * (kk * 4 + d * 2) + B * Hq * (d * 4 + d * 2 + 4)
+    dec_bytes = B * Hkv * ctx * (cbytes + d * 2) + B * Hq * (d * 4 + d * 2 + 4)
     achieved = dec_bytes / (dec_ms * 1e-3)
     return {
-        "metric": "SFA decode tokens/s, 64 seqs x 64K sparse-code cache (k=16 int16/bf16, d=128), 32/8 heads",
+        "metric": f"SFA decode tokens/s, 64 seqs x 64K sparse-code cache (k=16 {_CODE_NAMES[codes]}, "
+                  "d=128), 32/8 heads",
         "value": B / (ms * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.name + "_paged", "B": B, "Hq": Hq, "Hkv": Hkv, "L": L, "d": d,
-                   "k": kk, "page_size": P,
+                   "k": kk, "page_size": P, "cache_codes": codes,
                    "step": "sfa_kv_append (new token) + sfa_attn_decode_paged (dense query "
                            "coded in-kernel, split context + LSE merge)"},
         "roofline": {"kernel": "sfa_decode_kernel (paged) + combine", "bound": "hbm",
@@ -533,6 +544,9 @@ def main():
     ap.add_argument("--cache", default="contiguous", choices=["contiguous", "paged"],
                     help="decode workloads: contiguous cache (decode only) or paged cache "
                          "(append of the new token + decode with in-kernel query coding)")
+    ap.add_argument("--codes", default="i16bf16", choices=sorted(CODE_FORMATS),
+                    help="decode workloads: cache code storage (int16 indices + bf16 values, or "
+                         "the paper's compact uint8 indices + float16 values)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 1 GiB device copy twice (reference for "
@@ -548,9 +562,9 @@ def main():
     torch.cuda.set_device(0)
     w = si.workload(args.workload)
     if w.kind == "decode" and args.cache == "paged":
-        out = bench_decode_paged(w, args.steps, args.warmup)
+        out = bench_decode_paged(w, args.steps, args.warmup, args.codes)
     elif w.kind == "decode":
-        out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline)
+        out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline, args.codes)
     elif args.which == "bwd":
         out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
     else:
