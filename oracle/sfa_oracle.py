@@ -22,6 +22,9 @@ out in float64 with numpy:
 * LSE_i = m_i + ln(l_i), natural log (the paper does not define it; this is
   the standard log-sum-exp of the row's scaled scores).
 * Decode (App. B, KV-cache latency): one query row against all cached keys.
+* Composition with token sparsity (App. E: Longformer, SnapKV and others
+  combined with SFA): the causal mask and'ed with a sliding window plus
+  leading global tokens, in the forward and in decode.
 * KV-cache maintenance: coded keys and their values appended at a
   sequence's next positions, in a contiguous or paged cache (a block table
   maps each run of page_size positions of a sequence to a page of the
@@ -234,15 +237,35 @@ def densify(idx: np.ndarray, val, d: int) -> np.ndarray:
     return out
 
 
+def token_mask(pos, n_k: int, causal: bool, window: int = 0, n_global: int = 0) -> np.ndarray:
+    """allowed[a, j] for queries at positions pos[a] and keys 0..n_k-1.
+
+    The causal mask (j <= i) composed with a Longformer-style token pattern
+    (App. E): a sliding window |i - j| < window, plus n_global global tokens
+    at the start that every query sees and that see every key.  window 0
+    means no window (plain causal / full attention)."""
+    i = np.asarray(pos, dtype=np.int64)[:, None]
+    j = np.arange(n_k)[None, :]
+    allowed = (j <= i) if causal else np.ones((i.shape[0], n_k), dtype=bool)
+    if window > 0:
+        near = np.abs(i - j) < window
+        glob = (j < n_global) | (i < n_global)
+        allowed = allowed & (near | glob)
+    return allowed
+
+
 def softmax_attention(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, scale: float,
-                      causal: bool, pos=None, row_chunk: int = 1024):
+                      causal: bool, pos=None, row_chunk: int = 1024, window: int = 0,
+                      n_global: int = 0):
     """Plain softmax attention of one head on dense float64 inputs.
 
     qd [r, d] are query rows at sequence positions `pos` (default 0..r-1);
     kd [n_k, d] and v [n_k, dv] are the keys and values at positions
-    0..n_k-1.  A query at position i sees keys j <= i when causal, all keys
-    otherwise.  Rows are independent and are evaluated `row_chunk` at a time
-    only to bound memory.  Returns O [r, dv] and LSE [r] (natural log)."""
+    0..n_k-1.  A query at position i sees the keys token_mask allows: j <= i
+    when causal, all keys otherwise, further limited by a sliding window and
+    global tokens when window > 0.  Rows are independent and are evaluated
+    `row_chunk` at a time only to bound memory.  Returns O [r, dv] and LSE [r]
+    (natural log)."""
     r = qd.shape[0]
     pos = np.arange(r) if pos is None else np.asarray(pos, dtype=np.int64)
     O = np.empty((r, v.shape[1]), dtype=np.float64)
@@ -251,8 +274,8 @@ def softmax_attention(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, scale: floa
         pp = pos[s0:s0 + row_chunk]
         last = int(pp.max()) + 1 if causal else kd.shape[0]
         S = scale * (qd[s0:s0 + row_chunk] @ kd[:last].T)   # scores
-        if causal:
-            allowed = np.arange(last)[None, :] <= pp[:, None]
+        if causal or window > 0:
+            allowed = token_mask(pp, last, causal, window, n_global)
             S = np.where(allowed, S, -np.inf)
         m = S.max(axis=1)                                    # row max
         P = np.exp(S - m[:, None])                           # unnormalised weights
@@ -262,12 +285,14 @@ def softmax_attention(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, scale: floa
     return O, L
 
 
-def attn_fwd(q_idx, q_val, k_idx, k_val, v, d: int, scale: float, causal: bool):
+def attn_fwd(q_idx, q_val, k_idx, k_val, v, d: int, scale: float, causal: bool,
+             window: int = 0, n_global: int = 0):
     """SFA forward on codes.
 
     q_idx/q_val [B, Hq, n, k], k_idx/k_val [B, Hkv, n, k], v [B, Hkv, n, dv]
     (float32, or uint16 bfloat16 bits).  Query head h reads KV head
-    h // (Hq // Hkv).  Returns O [B, Hq, n, dv] and LSE [B, Hq, n], float64."""
+    h // (Hq // Hkv).  window / n_global: the token pattern of token_mask.
+    Returns O [B, Hq, n, dv] and LSE [B, Hq, n], float64."""
     B, Hq, n, _ = np.shape(q_idx)
     Hkv = np.shape(k_idx)[1]
     if Hq % Hkv:
@@ -281,12 +306,13 @@ def attn_fwd(q_idx, q_val, k_idx, k_val, v, d: int, scale: float, causal: bool):
             kd = densify(k_idx[b, g], k_val[b, g], d)
             for h in range(g * G, (g + 1) * G):
                 qd = densify(q_idx[b, h], q_val[b, h], d)
-                O[b, h], L[b, h] = softmax_attention(qd, kd, vv[b, g], scale, causal)
+                O[b, h], L[b, h] = softmax_attention(qd, kd, vv[b, g], scale, causal,
+                                                     window=window, n_global=n_global)
     return O, L
 
 
 def attn_fwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, d: int, scale: float,
-                  causal: bool, rows):
+                  causal: bool, rows, window: int = 0, n_global: int = 0):
     """SFA forward for chosen query rows of one (batch, query head), given the
     codes of that query head [n, k], of its KV head [n, k] and V [n, dv].
     Returns (O [len(rows), dv], LSE [len(rows)])."""
@@ -295,13 +321,17 @@ def attn_fwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, d: int, scale: f
     qd = densify(np.asarray(q_idx_bh)[rows], np.asarray(q_val_bh)[rows], d)
     kd = densify(np.asarray(k_idx_bg)[:last], np.asarray(k_val_bg)[:last], d)
     vv = widen(np.asarray(v_bg)[:last])
-    return softmax_attention(qd, kd, vv, scale, causal, pos=rows)
+    return softmax_attention(qd, kd, vv, scale, causal, pos=rows, window=window,
+                             n_global=n_global)
 
 
-def attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, d: int, scale: float, seq_len=None):
+def attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, d: int, scale: float, seq_len=None,
+                window: int = 0, n_global: int = 0):
     """SFA decode: each (b, h) query code [B, Hq, k] attends to all cached keys
     j < seq_len[b] of KV head h // G (cache codes [B, Hkv, Lmax, k], V cache
-    [B, Hkv, Lmax, dv]).  Returns O [B, Hq, dv] and LSE [B, Hq], float64."""
+    [B, Hkv, Lmax, dv]).  The query is the token at position seq_len[b] - 1;
+    with window > 0 it sees the keys token_mask allows from there.
+    Returns O [B, Hq, dv] and LSE [B, Hq], float64."""
     B, Hq, _ = np.shape(q_idx)
     Hkv, Lmax = np.shape(kc_idx)[1], np.shape(kc_idx)[2]
     G = Hq // Hkv
@@ -316,7 +346,8 @@ def attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, d: int, scale: float, seq
             vv = widen(np.asarray(v_cache)[b, g, :Lb])
             for h in range(g * G, (g + 1) * G):
                 qd = densify(np.asarray(q_idx)[b, h][None], np.asarray(q_val)[b, h][None], d)
-                O1, L1 = softmax_attention(qd, kd, vv, scale, causal=False)
+                O1, L1 = softmax_attention(qd, kd, vv, scale, causal=True, pos=[Lb - 1],
+                                           window=window, n_global=n_global)
                 O[b, h], L[b, h] = O1[0], L1[0]
     return O, L
 
@@ -407,7 +438,7 @@ def cache_gather(kc_idx, kc_val, v_cache, b: int, L: int, block_table=None, page
 
 
 def attn_decode_paged(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, d: int, scale: float,
-                      block_table=None, page_size=None):
+                      block_table=None, page_size=None, window: int = 0, n_global: int = 0):
     """Decode (App. B) over a paged cache: each sequence's first seq_len[b]
     positions, read through its block table, then the plain decode."""
     B, Hq, _ = np.shape(q_idx)
@@ -420,7 +451,8 @@ def attn_decode_paged(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, d: int, sc
             continue
         gi, gv, gvv = cache_gather(kc_idx, kc_val, v_cache, b, Lb, block_table, page_size)
         Ob, Lsb = attn_decode(np.asarray(q_idx)[b:b + 1], np.asarray(q_val)[b:b + 1],
-                              gi[None], gv[None], gvv[None], d, scale)
+                              gi[None], gv[None], gvv[None], d, scale, window=window,
+                              n_global=n_global)
         O[b], L[b] = Ob[0], Lsb[0]
     return O, L
 
