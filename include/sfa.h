@@ -97,6 +97,11 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * where the allowed keys are j <= i if `causal`, else all j < n.  An allowed
  * key whose support does not overlap the query's enters with s_ij = 0.
  * No n x n matrix is ever stored.
+ * Token sparsity (App. E: SFA composed with Longformer-style patterns): with
+ * window > 0 the allowed keys are further limited to |i - j| < window, plus
+ * the n_global leading tokens, which every query sees and which see every
+ * key; key tiles outside every row's window are skipped, not masked.
+ * window 0 (n_global ignored) is plain causal / full attention.
  *
  * q_idx, q_val  [B, Hq, n, k]   query codes (idx_t, qk_val_t)
  * k_idx, k_val  [B, Hkv, n, k]  key codes   (idx_t, qk_val_t)
@@ -123,7 +128,8 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * the P.V product is float32.
  * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0 with Hq / Hkv a power of two
  *         <= 128; d in {64, 128}; 1 <= k <= d; B * Hkv <= 65535;
- *         n * d <= 2^29 and n * k <= 2^29 (SFA_ENOTSUP otherwise).
+ *         n * d <= 2^29 and n * k <= 2^29 (SFA_ENOTSUP otherwise);
+ *         window, n_global >= 0.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (workspace missing or too
  *         small), SFA_EHIP.
  */
@@ -131,7 +137,7 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,
                         const void* k_idx, const void* k_val,
                         const void* v,
                         int B, int Hq, int Hkv, int n, int d, int k,
-                        int causal, float scale,
+                        int causal, int window, int n_global, float scale,
                         int idx_t, int qk_val_t, int v_t, int o_t,
                         void* o, float* lse, void* ws, size_t ws_bytes,
                         void* stream);
@@ -218,6 +224,10 @@ size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d);
  * (all of them allowed), with the same s, O and LSE definitions as
  * sfa_attn_fwd.  The context is split into chunks processed in parallel and
  * the partial (max, sum, output) triples are merged by their LSE.
+ * With window > 0 the query, the token at position L - 1 (L = seq_len[b]),
+ * sees only keys j > L - 1 - window and the n_global leading tokens (all
+ * keys if it is itself one of them), as row L - 1 of sfa_attn_fwd with the
+ * same window; context outside is skipped.
  *
  * q_idx, q_val    [B, Hq, k]          query codes (q_idx_t, q_val_t)
  * kc_idx, kc_val  [B, Hkv, Lmax, k]   cached key codes (kc_idx_t, kc_val_t)
@@ -232,14 +242,14 @@ size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d);
  *                 contents need no initialisation and are scratch after the
  *                 call.  Concurrent calls must use distinct workspaces.
  * Limits: B, Hq, Hkv, Lmax >= 1; Hq % Hkv == 0; Hq / Hkv <= 8;
- *         d in {64, 128}; 1 <= k <= d.
+ *         d in {64, 128}; 1 <= k <= d; window, n_global >= 0.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (ws_bytes too small), SFA_EHIP.
  */
 sfa_status sfa_attn_decode(const void* q_idx, const void* q_val,
                            const void* kc_idx, const void* kc_val,
                            const void* v_cache, const int32_t* seq_len,
                            int B, int Hq, int Hkv, int Lmax, int d, int k,
-                           float scale,
+                           float scale, int window, int n_global,
                            int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t,
                            int v_t, int o_t,
                            void* o, float* lse,
@@ -332,7 +342,8 @@ sfa_status sfa_kv_append(const float* k_new, const void* v_new, const int32_t* n
  *                 (undefined results, no fault).
  * seq_len         [B] int32 on the device (clamped into
  *                 [0, max_pages * page_size]) or NULL for full sequences.
- * o, lse, ws, ws_bytes, scale, dtypes: as sfa_attn_decode, with the
+ * o, lse, ws, ws_bytes, scale, window, n_global, dtypes: as
+ *                 sfa_attn_decode, with the
  *                 workspace sized by
  *                 sfa_attn_decode_workspace(B, Hq, max_pages * page_size, d).
  * The result equals sfa_attn_decode on the gathered contiguous cache (same
@@ -344,7 +355,8 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
                                  const void* kc_idx, const void* kc_val, const void* v_cache,
                                  const int32_t* block_table, int max_pages, int page_size,
                                  int num_pages, const int32_t* seq_len, int B, int Hq, int Hkv,
-                                 int d, int k, float scale, int q_idx_t, int q_val_t,
+                                 int d, int k, float scale, int window, int n_global,
+                                 int q_idx_t, int q_val_t,
                                  int kc_idx_t, int kc_val_t, int v_t, int o_t, void* o,
                                  float* lse, void* ws, size_t ws_bytes, void* stream);
 

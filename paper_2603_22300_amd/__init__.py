@@ -55,8 +55,8 @@ def lib() -> ctypes.CDLL:
         L.sfa_topk_encode.restype = i32
         L.sfa_topk_encode.argtypes = [vp, i64, i32, i32, vp, i32, vp, i32, vp]
         L.sfa_attn_fwd.restype = i32
-        L.sfa_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
-                                   i32, i32, i32, i32, vp, vp, vp, sz, vp]
+        L.sfa_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32,
+                                   i32, f32, i32, i32, i32, i32, vp, vp, vp, sz, vp]
         L.sfa_attn_fwd_workspace.restype = sz
         L.sfa_attn_fwd_workspace.argtypes = [i32, i32, i32, i32, i32]
         L.sfa_attn_fwd_index.restype = i32
@@ -71,11 +71,11 @@ def lib() -> ctypes.CDLL:
         L.sfa_attn_decode_workspace.argtypes = [i32, i32, i32, i32]
         L.sfa_attn_decode.restype = i32
         L.sfa_attn_decode.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, f32,
-                                      i32, i32, i32, i32, i32, i32, vp, vp, vp, sz, vp]
+                                      i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, sz, vp]
         L.sfa_attn_decode_paged.restype = i32
         L.sfa_attn_decode_paged.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, i32, i32,
-                                            i32, i32, i32, f32, i32, i32, i32, i32, i32, i32, vp,
-                                            vp, vp, sz, vp]
+                                            i32, i32, i32, f32, i32, i32, i32, i32, i32, i32,
+                                            i32, i32, vp, vp, vp, sz, vp]
         L.sfa_kv_append.restype = i32
         L.sfa_kv_append.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp, i32, i32, i32,
                                     vp, vp, vp, i32, i32, i32, i32, vp]
@@ -146,12 +146,15 @@ def sfa_attn_fwd_workspace(B: int, Hkv: int, n: int, d: int, v_dtype=torch.bfloa
 
 def sfa_attn_fwd(q_idx, q_val, k_idx, k_val, v, causal: bool = True, scale: float | None = None,
                  o_dtype=None, o: torch.Tensor | None = None, lse: torch.Tensor | None = None,
-                 want_lse: bool = True, ws: torch.Tensor | None = None):
+                 want_lse: bool = True, ws: torch.Tensor | None = None, window: int = 0,
+                 n_global: int = 0):
     """SFA forward on codes.  q_* [B, Hq, n, k], k_* [B, Hkv, n, k], v [B, Hkv, n, d].
     ws: uint8 device workspace of sfa_attn_fwd_workspace(...) bytes, allocated
-    here when None.  Returns (o [B, Hq, n, d], lse [B, Hq, n] float32 or None)."""
+    here when None.  window > 0: sliding window |i - j| < window plus n_global
+    leading global tokens.  Returns (o [B, Hq, n, d], lse [B, Hq, n] float32 or
+    None)."""
     return _fwd("sfa_attn_fwd", q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse,
-                want_lse, ws)
+                want_lse, ws, window, n_global)
 
 
 def sfa_attn_fwd_index(q_idx, q_val, k_idx, k_val, v, causal: bool = True,
@@ -159,10 +162,11 @@ def sfa_attn_fwd_index(q_idx, q_val, k_idx, k_val, v, causal: bool = True,
                        lse: torch.Tensor | None = None, want_lse: bool = True):
     """The inverted-index variant of sfa_attn_fwd (same arguments and results)."""
     return _fwd("sfa_attn_fwd_index", q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o,
-                lse, want_lse, None)
+                lse, want_lse, None, 0, 0)
 
 
-def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, want_lse, ws):
+def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, want_lse, ws,
+         window, n_global):
     B, Hq, n, k = q_idx.shape
     Hkv, d = k_idx.shape[1], v.shape[-1]
     if tuple(q_val.shape) != (B, Hq, n, k) or tuple(k_idx.shape) != (B, Hkv, n, k) \
@@ -186,8 +190,11 @@ def _fwd(name, q_idx, q_val, k_idx, k_val, v, causal, scale, o_dtype, o, lse, wa
     if lse is not None:
         _check(lse, "lse", {torch.float32: SFA_F32})
         lp = lse.data_ptr()
+    mask = [int(bool(causal))]
+    if name == "sfa_attn_fwd":
+        mask += [int(window), int(n_global)]
     args = [q_idx.data_ptr(), q_val.data_ptr(), k_idx.data_ptr(), k_val.data_ptr(), v.data_ptr(),
-            B, Hq, Hkv, n, d, k, int(bool(causal)), float(scale), it, qt, vt, ot, o.data_ptr(), lp]
+            B, Hq, Hkv, n, d, k] + mask + [float(scale), it, qt, vt, ot, o.data_ptr(), lp]
     if name == "sfa_attn_fwd":
         need = int(lib().sfa_attn_fwd_workspace(B, Hkv, n, d, vt))
         if ws is None and need > 0:
@@ -259,7 +266,8 @@ def sfa_attn_decode_workspace(B: int, Hq: int, Lmax: int, d: int) -> int:
 
 
 def sfa_attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len=None, scale: float | None = None,
-                    o_dtype=None, o=None, lse=None, want_lse: bool = True, ws=None):
+                    o_dtype=None, o=None, lse=None, want_lse: bool = True, ws=None,
+                    window: int = 0, n_global: int = 0):
     """SFA decode step.  q_* [B, Hq, k], kc_* [B, Hkv, Lmax, k], v_cache [B, Hkv, Lmax, d],
     seq_len int32 [B] on the GPU or None.  Returns (o [B, Hq, d], lse [B, Hq] or None)."""
     B, Hq, k = q_idx.shape
@@ -292,7 +300,8 @@ def sfa_attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len=None, scale: 
         ws = torch.empty(need, dtype=torch.uint8, device=v_cache.device)
     _call(lib().sfa_attn_decode(q_idx.data_ptr(), q_val.data_ptr(), kc_idx.data_ptr(),
                                 kc_val.data_ptr(), v_cache.data_ptr(), sp, B, Hq, Hkv, Lmax, d, k,
-                                float(scale), qit, qvt, cit, cvt, vt, ot, o.data_ptr(), lp,
+                                float(scale), int(window), int(n_global), qit, qvt, cit, cvt, vt,
+                                ot, o.data_ptr(), lp,
                                 ws.data_ptr(), ws.numel() * ws.element_size(), _stream(v_cache)),
           "sfa_attn_decode")
     return o, lse
@@ -344,7 +353,7 @@ def sfa_kv_append(k_new, v_new, seq_len, kc_idx, kc_val, v_cache, k: int, block_
 
 def sfa_attn_decode_paged(kc_idx, kc_val, v_cache, block_table, seq_len=None, q=None, q_idx=None,
                           q_val=None, scale: float | None = None, o_dtype=None, o=None, lse=None,
-                          want_lse: bool = True, ws=None):
+                          want_lse: bool = True, ws=None, window: int = 0, n_global: int = 0):
     """SFA decode step over a paged cache.  Give either the dense query q
     (float32 [B, Hq, d], coded inside the kernel) or its codes q_idx, q_val
     [B, Hq, k].  kc_* [num_pages, Hkv, page_size, k], v_cache
@@ -396,7 +405,8 @@ def sfa_attn_decode_paged(kc_idx, kc_val, v_cache, block_table, seq_len=None, q=
                          device=v_cache.device)
     _call(lib().sfa_attn_decode_paged(qp, qip, qvp, kc_idx.data_ptr(), kc_val.data_ptr(),
                                       v_cache.data_ptr(), block_table.data_ptr(), maxp, P, npg,
-                                      sp, B, Hq, Hkv, d, k, float(scale), qit, qvt, cit, cvt, vt,
+                                      sp, B, Hq, Hkv, d, k, float(scale), int(window),
+                                      int(n_global), qit, qvt, cit, cvt, vt,
                                       ot, o.data_ptr(), lp, ws.data_ptr(),
                                       ws.numel() * ws.element_size(), _stream(v_cache)),
           "sfa_attn_decode_paged")

@@ -9,7 +9,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 3;
+constexpr int kAbiVersion = 4;
 constexpr int kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
 
 // index arrays of codes; values of codes; V and O
@@ -78,16 +78,19 @@ size_t sfa_attn_fwd_workspace(int B, int Hkv, int n, int d, int v_t) {
 
 sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                         const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
-                        int k, int causal, float scale, int idx_t, int qk_val_t, int v_t,
-                        int o_t, void* o, float* lse, void* ws, size_t ws_bytes, void* stream) {
+                        int k, int causal, int window, int n_global, float scale, int idx_t,
+                        int qk_val_t, int v_t, int o_t, void* o, float* lse, void* ws,
+                        size_t ws_bytes, void* stream) {
   sfa_status st = check_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k, scale, idx_t,
                             qk_val_t, v_t, o_t, o);
   if (st != SFA_OK) return st;
+  if (window < 0 || n_global < 0) return SFA_EINVAL;
   if (!pow2_le(Hq / Hkv, sfa::fwd_max_group())) return SFA_ENOTSUP;
   const size_t need = sfa::fwd_workspace_bytes(B, Hkv, n, d, v_t == SFA_BF16);
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
-                                       causal != 0, scale, ifmt_of(idx_t),
+                                       causal != 0, window, window > 0 ? n_global : 0, scale,
+                                       ifmt_of(idx_t),
                                        vfmt_of(qk_val_t), v_t == SFA_BF16, o_t == SFA_BF16,
                                        o, lse, ws, (hipStream_t)stream));
 }
@@ -138,11 +141,13 @@ size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d) {
 sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
                            const void* kc_val, const void* v_cache, const int32_t* seq_len,
                            int B, int Hq, int Hkv, int Lmax, int d, int k, float scale,
+                           int window, int n_global,
                            int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t, int v_t,
                            int o_t, void* o, float* lse, void* ws, size_t ws_bytes,
                            void* stream) {
   if (!q_idx || !q_val || !kc_idx || !kc_val || !v_cache || !o || !ws) return SFA_EINVAL;
   if (B < 1 || Hq < 1 || Hkv < 1 || Lmax < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
+  if (window < 0 || n_global < 0) return SFA_EINVAL;
   if (Hq % Hkv != 0) return SFA_EINVAL;
   if (!is_idx(q_idx_t) || !is_cval(q_val_t) || !is_idx(kc_idx_t) || !is_cval(kc_val_t) ||
       !is_val(v_t) || !is_val(o_t))
@@ -157,6 +162,7 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
   a.q_idx = q_idx; a.q_val = q_val; a.kc_idx = kc_idx; a.kc_val = kc_val; a.v = v_cache;
   a.seq_len = seq_len;
   a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lmax = Lmax; a.d = d; a.k = k; a.scale = scale;
+  a.window = window; a.n_global = window > 0 ? n_global : 0;
   a.qifmt = ifmt_of(q_idx_t); a.qvfmt = vfmt_of(q_val_t);
   a.kifmt = ifmt_of(kc_idx_t); a.kvfmt = vfmt_of(kc_val_t);
   a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;
@@ -168,7 +174,8 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
                                  const void* kc_idx, const void* kc_val, const void* v_cache,
                                  const int32_t* block_table, int max_pages, int page_size,
                                  int num_pages, const int32_t* seq_len, int B, int Hq, int Hkv,
-                                 int d, int k, float scale, int q_idx_t, int q_val_t,
+                                 int d, int k, float scale, int window, int n_global,
+                                 int q_idx_t, int q_val_t,
                                  int kc_idx_t, int kc_val_t, int v_t, int o_t, void* o,
                                  float* lse, void* ws, size_t ws_bytes, void* stream) {
   const bool dense_q = q != nullptr;
@@ -176,6 +183,7 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
   if (!kc_idx || !kc_val || !v_cache || !block_table || !o || !ws) return SFA_EINVAL;
   if (B < 1 || Hq < 1 || Hkv < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
   if (max_pages < 1 || num_pages < 1) return SFA_EINVAL;
+  if (window < 0 || n_global < 0) return SFA_EINVAL;
   if (page_size < 16 || (page_size & (page_size - 1)) != 0) return SFA_EINVAL;
   if ((long long)max_pages * page_size > (1LL << 30)) return SFA_EINVAL;
   if (Hq % Hkv != 0) return SFA_EINVAL;
@@ -197,6 +205,7 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
   a.seq_len = seq_len; a.table = block_table;
   a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lmax = Lmax; a.d = d; a.k = k; a.scale = scale;
   a.max_pages = max_pages; a.log2P = log2P; a.num_pages = num_pages;
+  a.window = window; a.n_global = window > 0 ? n_global : 0;
   a.qifmt = dense_q ? 0 : ifmt_of(q_idx_t); a.qvfmt = dense_q ? 0 : vfmt_of(q_val_t);
   a.kifmt = ifmt_of(kc_idx_t); a.kvfmt = vfmt_of(kc_val_t);
   a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;

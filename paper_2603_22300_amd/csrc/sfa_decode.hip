@@ -48,6 +48,7 @@ struct DecParams {
   const float* q_dense;   // [B, Hq, D] or null (then q_idx / q_val)
   const int32_t* table;   // paged: [B, max_pages]
   int max_pages, log2P, num_pages;
+  int window, n_global;   // token pattern (window 0: all cached keys)
 };
 
 __device__ __forceinline__ int seq_len_of(const int32_t* seq_len, int b, int Lmax) {
@@ -124,8 +125,19 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   const int dsub = lane % DL;  // 8-dim group of this lane in the P.V phase
   const int ksub = lane / DL;  // key offset within a wave-wide V load
   const int per_wave = kDecChunk / kDecWaves;
-  const int w0 = c0 + wave * per_wave;
-  const int w1 = min(c1, w0 + per_wave);
+  int w0 = c0 + wave * per_wave;
+  int w1 = min(c1, w0 + per_wave);
+  // Token window: the query (position L - 1) sees keys [0, wg) and
+  // [wlo, L) only.  A wave range inside the gap does nothing; one that starts
+  // in it starts at the window (64-aligned; the keys before wlo are masked).
+  const bool winq = p.window > 0 && L - 1 >= p.n_global;
+  const int wlo = winq ? max(0, L - p.window) : 0;
+  const int wg = winq ? min(p.n_global, L) : 0;
+  if (winq && w0 >= wg) {
+    if (w1 <= wlo) w1 = w0;
+    else w0 = max(w0, wlo & ~63);
+  }
+  auto key_ok = [&](int j) { return j >= wlo || j < wg; };
 
   // Row of key j in the cache arrays.  Paged: lane l of `tblv` holds the
   // page of the wave's l-th page-sized run (ids clamped into the pool).
@@ -232,7 +244,7 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
 #pragma unroll
         for (int h = 0; h < G; ++h) s[h] = fmaf(kv, qd[u][h], s[h]);
       }
-      softmax_block(s, sb + lane < w1);
+      softmax_block(s, sb + lane < w1 && key_ok(sb + lane));
       if (sb + 64 < w1) load_codes(sb + 64);  // next sub-block's codes during P.V
       // P.V: lanes over (8 dims, key subset)
 #pragma unroll
@@ -250,7 +262,7 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
     // ---------------- generic path: any code format and k ----------------
     for (int sb = w0; sb < w1; sb += 64) {
       const int j = min(sb + lane, w1 - 1);
-      const bool ok = sb + lane < w1;
+      const bool ok = sb + lane < w1 && key_ok(sb + lane);
       float s[G];
 #pragma unroll
       for (int h = 0; h < G; ++h) s[h] = 0.f;
@@ -410,6 +422,7 @@ hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   p.q_dense = a.q_dense;
   p.table = a.table;
   p.max_pages = a.max_pages; p.log2P = a.log2P; p.num_pages = a.num_pages;
+  p.window = a.window; p.n_global = a.n_global;
   const int G = a.Hq / a.Hkv, B = a.B;
   if (a.d == 64) {
     if (a.vbf16) launch_dec_g<64, true>(p, G, B, stream); else launch_dec_g<64, false>(p, G, B, stream);

@@ -53,6 +53,7 @@ struct FwdParams {
   void* o;
   float* lse;
   int Hq, Hkv, n, k, causal;
+  int window, n_global;  // token pattern: |i - j| < window or a global token (window 0: none)
   float scale_log2;  // scale * log2(e)
   int ifmt, vfmt, obf16;
   int G, BR, nqb;
@@ -180,14 +181,28 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   const bool row_ok = my_i < n;
 
   const int blk_last = min(n, i0 + p.BR) - 1;
-  const int n_keys = p.causal ? blk_last + 1 : n;
-  const int ntiles = (n_keys + kBC - 1) / kBC;
+  // Key tiles this workgroup visits: all up to the causal limit, or with a
+  // token window (and no global row here) the global tiles [0, gt_end) and
+  // the window tiles [wt_begin, ntiles_all) -- tiles in the gap are skipped.
+  const bool win = p.window > 0;
+  int n_keys = p.causal ? blk_last + 1 : n;
+  int gt_end = 0, wt_begin = 0;
+  if (win && i0 >= p.n_global) {
+    if (!p.causal) n_keys = min(n, blk_last + p.window);
+    gt_end = (p.n_global + kBC - 1) / kBC;
+    wt_begin = max(0, i0 - p.window + 1) / kBC;
+    if (wt_begin <= gt_end) gt_end = wt_begin = 0;  // no gap
+  }
+  const int ntiles_all = (n_keys + kBC - 1) / kBC;
+  const int ntiles = gt_end + ntiles_all - wt_begin;
+  // key tile of list position t (t == ntiles gives ntiles_all: past the end)
+  auto tile_at = [&](int t) { return t < gt_end ? t : wt_begin + (t - gt_end); };
 
   if constexpr (VBF16 && !SAFE) {
     // A V tile of this workgroup's key range outside the float16 range: hand
     // the rows back to the bf16 rerun before doing any work.
     bool over = false;
-    for (int t = tid; t < ntiles; t += NT) over |= p.ws_flag[(int64_t)bh * p.vtiles + t] != 0;
+    for (int t = tid; t < ntiles; t += NT) over |= p.ws_flag[(int64_t)bh * p.vtiles + tile_at(t)] != 0;
     if (__syncthreads_or(over)) {
       if (tid == 0) {
         const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;  // row rho = 0
@@ -403,11 +418,11 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   };
   if (ntiles > 0 && NS == 2) {
     if constexpr (kDMA) {
-      dma_stage(0, 0);
+      dma_stage(0, tile_at(0));
       wait_dma();
     } else {
-      load_tile(0);
-      write_tile(0, 0);
+      load_tile(tile_at(0));
+      write_tile(0, tile_at(0));
     }
   }
   __syncthreads();
@@ -527,7 +542,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
-      const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
+      const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
+                      (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
       sc[r] = ok ? sc[r] * c : -INFINITY;
       mt = fmaxf(mt, sc[r]);
     }
@@ -642,33 +658,44 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     return true;
   };
 
-  for (int jt = 0; jt < ntiles; ++jt) {
+  // a 32-key sub-tile from key a on is seen by some row of this wave: it holds
+  // a global key, the wave a global row, or it meets some row's window
+  auto in_window = [&](int a) {
+    return !win || a < p.n_global || wave_i_min < p.n_global ||
+           (a + 31 > wave_i_min - p.window && a < wave_i_max + p.window);
+  };
+  for (int t = 0; t < ntiles; ++t) {
+    const int jt = tile_at(t), jt_next = tile_at(t + 1);
     const int j0 = jt * kBC;
-    const int stage = NS == 2 ? (jt & 1) : 0;
+    const int stage = NS == 2 ? (t & 1) : 0;
     if constexpr (NS == 1) {
       load_tile(jt);
       write_tile(0, jt);
       __syncthreads();
     } else {
-      load_tile(jt + 1);  // past the end it reads clamped, valid addresses; unused
+      load_tile(jt_next);  // past the end it reads clamped, valid addresses; unused
       if constexpr (kDMA) {
-        if (jt + 1 < ntiles) dma_stage(stage ^ 1, jt + 1);
+        if (t + 1 < ntiles) dma_stage(stage ^ 1, jt_next);
       }
     }
     const uint16_t* Kd = (const uint16_t*)(smem + stage * SB);
     const unsigned char* vt = smem + stage * SB + kBC * KR * 2;
-    const bool act0 = !p.causal || wave_i_max >= j0;
-    const bool act1 = !p.causal || wave_i_max >= j0 + 32;
-    const bool need_mask = j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min) ||
+    const bool act0 = (!p.causal || wave_i_max >= j0) && in_window(j0);
+    const bool act1 = (!p.causal || wave_i_max >= j0 + 32) && in_window(j0 + 32);
+    // the token window cuts into this tile for some row of the wave
+    const bool wcut = win && j0 + kBC > p.n_global &&
+                      (wave_i_min < p.n_global || wave_i_max - j0 >= p.window ||
+                       j0 + kBC - 1 - wave_i_min >= p.window);
+    const bool need_mask = j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min) || wcut ||
                            __builtin_amdgcn_ballot_w64(!row_ok || m_run == -INFINITY) != 0;
     bool done = false;
     if constexpr (NS == 2 && VBF16 && !SAFE) {
-      if (act1 && !need_mask) done = fast_tile(Kd, (const uint16_t*)vt, jt + 1, stage ^ 1);
+      if (act0 && act1 && !need_mask) done = fast_tile(Kd, (const uint16_t*)vt, jt_next, stage ^ 1);
     }
     if (!done) {
       if (act0) generic_sub(j0, 0, Kd, vt);
       if (act1) generic_sub(j0, 1, Kd, vt);
-      if constexpr (NS == 2) write_tile(stage ^ 1, jt + 1);
+      if constexpr (NS == 2) write_tile(stage ^ 1, jt_next);
     }
     wait_dma();
     __syncthreads();
@@ -841,12 +868,14 @@ size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16) {
 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
-                           int k, int causal, float scale, int ifmt, int vfmt, int vbf16,
-                           int obf16, void* o, float* lse, void* ws, hipStream_t stream) {
+                           int k, int causal, int window, int n_global, float scale, int ifmt,
+                           int vfmt, int vbf16, int obf16, void* o, float* lse, void* ws,
+                           hipStream_t stream) {
   FwdParams p;
   p.q_idx = q_idx; p.q_val = q_val; p.k_idx = k_idx; p.k_val = k_val; p.v = v;
   p.o = o; p.lse = lse;
   p.Hq = Hq; p.Hkv = Hkv; p.n = n; p.k = k; p.causal = causal;
+  p.window = window; p.n_global = n_global;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
   p.ifmt = ifmt; p.vfmt = vfmt; p.obf16 = obf16;
   p.G = Hq / Hkv;

@@ -13,8 +13,9 @@ hipError_t launch_topk_encode(const float* x, int64_t rows, int d, int k, void* 
 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, int B, int Hq, int Hkv, int n, int d,
-                           int k, int causal, float scale, int ifmt, int vfmt, int vbf16,
-                           int obf16, void* o, float* lse, void* ws, hipStream_t stream);
+                           int k, int causal, int window, int n_global, float scale, int ifmt,
+                           int vfmt, int vbf16, int obf16, void* o, float* lse, void* ws,
+                           hipStream_t stream);
 int fwd_max_group();
 size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16);
 
@@ -44,6 +45,7 @@ struct DecodeArgs {
   const int32_t* table;
   int B, Hq, Hkv, Lmax, d, k;
   int max_pages, log2P, num_pages;
+  int window, n_global;  // token pattern (window 0: none)
   float scale;
   int qifmt, qvfmt, kifmt, kvfmt, vbf16, obf16;
   void* o;

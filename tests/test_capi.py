@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_strerror(L):
-    assert L.sfa_abi_version() == 3
+    assert L.sfa_abi_version() == 4
     for s in range(5):
         assert L.sfa_strerror(s)
 
@@ -47,7 +47,10 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails val
 
 def _fwd(L, fn="sfa_attn_fwd", **kw):
     a = dict(q_idx=FAKE, q_val=FAKE, k_idx=FAKE, k_val=FAKE, v=FAKE, B=1, Hq=4, Hkv=2, n=16, d=64,
-             k=8, causal=1, scale=0.125, idx_t=0, qk_val_t=2, v_t=3, o_t=2, o=FAKE, lse=None)
+             k=8, causal=1)
+    if fn == "sfa_attn_fwd":
+        a.update(window=0, n_global=0)
+    a.update(scale=0.125, idx_t=0, qk_val_t=2, v_t=3, o_t=2, o=FAKE, lse=None)
     if fn == "sfa_attn_fwd":
         a.update(ws=FAKE, ws_bytes=ctypes.c_size_t(1 << 40))
     a["stream"] = None
@@ -70,6 +73,13 @@ def test_fwd_validation(L, fn):
     assert _fwd(L, fn, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
     assert _fwd(L, fn, B=70000, Hkv=1, Hq=1) == 2  # grid limit
     assert _fwd(L, fn, n=(1 << 22) + 1, d=128, k=16) == 2  # 32-bit per-head offsets
+
+
+def test_window_validation(L):
+    assert _fwd(L, window=-1) == 1
+    assert _fwd(L, window=4, n_global=-2) == 1
+    assert _dec(L, window=-3) == 1
+    assert _paged(L, n_global=-1, ws_bytes=ctypes.c_size_t(1 << 30)) == 1
 
 
 def test_fwd_workspace(L):
@@ -101,7 +111,8 @@ def test_encode_validation(L):
 
 def _dec(L, **kw):
     a = dict(q_idx=FAKE, q_val=FAKE, kc_idx=FAKE, kc_val=FAKE, v=FAKE, seq_len=None, B=2, Hq=8,
-             Hkv=2, Lmax=100, d=128, k=16, scale=0.088, q_idx_t=0, q_val_t=2, kc_idx_t=1,
+             Hkv=2, Lmax=100, d=128, k=16, scale=0.088, window=0, n_global=0, q_idx_t=0,
+             q_val_t=2, kc_idx_t=1,
              kc_val_t=3, v_t=3, o_t=2, o=FAKE, lse=None, ws=FAKE, ws_bytes=1 << 30, stream=None)
     a.update(kw)
     return L.sfa_attn_decode(*a.values())
@@ -146,7 +157,8 @@ def test_bwd_validation_and_workspace(L):
 def _paged(L, **kw):
     a = dict(q=None, q_idx=FAKE, q_val=FAKE, kc_idx=FAKE, kc_val=FAKE, v_cache=FAKE,
              block_table=FAKE, max_pages=4, page_size=64, num_pages=16, seq_len=None, B=2, Hq=8,
-             Hkv=2, d=128, k=16, scale=0.1, q_idx_t=0, q_val_t=2, kc_idx_t=1, kc_val_t=3, v_t=3,
+             Hkv=2, d=128, k=16, scale=0.1, window=0, n_global=0, q_idx_t=0, q_val_t=2,
+             kc_idx_t=1, kc_val_t=3, v_t=3,
              o_t=2, o=FAKE, lse=None, ws=FAKE, ws_bytes=ctypes.c_size_t(1), stream=None)
     a.update(kw)
     return L.sfa_attn_decode_paged(*a.values())

@@ -1,0 +1,113 @@
+"""GPU parity of SFA composed with token sparsity (App. E): a sliding window
+|i - j| < window plus n_global leading global tokens, in the forward (key
+tiles outside every row's window skipped) and in decode (context outside the
+window skipped), against the oracle's token_mask."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2603_22300_amd as sfa
+import sfa_inputs as si
+from helpers import TOL_O_BF16V, TOL_O_F32, check_lse, check_o, np_vals, sample_rows
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n,d,k,causal,v_bf16,w,g", [
+    (1, 4, 1, 700, 128, 16, True, True, 100, 0),     # window edge inside tiles
+    (1, 4, 2, 900, 128, 16, True, True, 128, 3),     # global tokens, gap of skipped tiles
+    (2, 2, 2, 333, 64, 8, True, False, 64, 70),      # globals past the first tile, float32 V
+    (1, 8, 1, 517, 128, 16, False, True, 50, 2),     # non-causal window
+    (1, 2, 1, 260, 128, 4, True, True, 1, 0),        # window 1: each query alone
+    (1, 4, 4, 300, 64, 16, True, True, 1000, 0),     # window beyond n: plain causal
+    (1, 4, 2, 1500, 128, 16, True, True, 257, 64),   # tile-aligned globals, odd window
+])
+def test_fwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
+    seed = n + w + g
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed, device=DEV,
+                            v_dtype=torch.bfloat16 if v_bf16 else torch.float32)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    scale = 1 / math.sqrt(d)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale,
+                              o_dtype=torch.float32, window=w, n_global=g)
+    torch.cuda.synchronize()
+    O, L = oracle.attn_fwd(qi.cpu().numpy(), qv.cpu().numpy(), ki.cpu().numpy(),
+                           kv.cpu().numpy(), np_vals(v), d, scale, causal, window=w, n_global=g)
+    check_o(o, O, TOL_O_BF16V if v_bf16 else TOL_O_F32, f"fwd window {w} global {g} O")
+    check_lse(lse, L, f"fwd window {w} global {g} LSE")
+
+
+def test_fwd_window_qwen3_32k_sampled():
+    """The 32K GQA workload with a 4096-token window and 4 global tokens: all
+    rows on the GPU, sampled rows of two heads by the oracle."""
+    w_ = si.workload("qwen3_32k")
+    B, Hq, Hkv, n, d, k, G = w_.B, w_.Hq, w_.Hkv, w_.n, w_.d, w_.k, w_.G
+    win, ng = 4096, 4
+    q = torch.empty((B, Hq, n, d), device=DEV)
+    kk = torch.empty((B, Hkv, n, d), device=DEV)
+    v = torch.empty((B, Hkv, n, d), device=DEV, dtype=torch.bfloat16)
+    for h in range(Hq):
+        q[0, h] = si.normal((n, d), w_.seed, "q", 0, h, device=DEV)
+    for h in range(Hkv):
+        kk[0, h] = si.normal((n, d), w_.seed, "k", 0, h, device=DEV)
+        v[0, h] = si.normal((n, d), w_.seed, "v", 0, h, device=DEV).to(torch.bfloat16)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=w_.scale,
+                              o_dtype=torch.float32, window=win, n_global=ng)
+    torch.cuda.synchronize()
+    rows = sample_rows(n, extra=[3, 4, win - 1, win, win + 63, 20000], count=12, seed=4)
+    for h in (0, 13):
+        g = h // G
+        ref = oracle.attn_fwd_rows(qi[0, h].cpu().numpy(), qv[0, h].cpu().numpy(),
+                                   ki[0, g].cpu().numpy(), kv[0, g].cpu().numpy(),
+                                   np_vals(v[0, g]), d, w_.scale, True, rows, window=win,
+                                   n_global=ng)
+        sel = torch.from_numpy(rows).to(DEV)
+        check_o(o[0, h, sel], ref[0], TOL_O_BF16V, f"qwen3_32k window head {h} O")
+        check_lse(lse[0, h, sel], ref[1], f"qwen3_32k window head {h} LSE")
+
+
+@pytest.mark.parametrize("w,g,seq", [(700, 0, [5000, 2500, 700]), (512, 4, [5000, 4097, 3]),
+                                     (1, 0, [5000, 10, 1]), (3000, 2049, [5000, 2100, 4999])])
+def test_decode_window(w, g, seq):
+    B, Hq, Hkv, L, d, k, P = 3, 8, 2, 5000, 128, 16, 64
+    seed = w + g
+    kd = torch.empty((B, Hkv, L, d), device=DEV)
+    vc = torch.empty((B, Hkv, L, d), device=DEV, dtype=torch.bfloat16)
+    for b in range(B):
+        for h in range(Hkv):
+            kd[b, h] = si.normal((L, d), seed, "k", b, h, device=DEV)
+            vc[b, h] = si.normal((L, d), seed, "v", b, h, device=DEV).to(torch.bfloat16)
+    ci, cv = sfa.sfa_topk_encode(kd, k, idx_dtype=torch.int16, val_dtype=torch.bfloat16)
+    qd = si.normal((B, Hq, d), seed, "q", device=DEV)
+    qi, qv = sfa.sfa_topk_encode(qd, k)
+    seq_t = torch.tensor(seq, dtype=torch.int32, device=DEV)
+    scale = 1 / math.sqrt(d)
+    o, lse = sfa.sfa_attn_decode(qi, qv, ci, cv, vc, seq_len=seq_t, scale=scale,
+                                 o_dtype=torch.float32, window=w, n_global=g)
+    mp = (L + P - 1) // P
+    pad = mp * P - L
+
+    def paged(a):
+        a = torch.cat([a, torch.zeros(a.shape[:2] + (pad,) + a.shape[3:], dtype=a.dtype,
+                                      device=DEV)], 2) if pad else a
+        return a.reshape(B, Hkv, mp, P, -1).permute(0, 2, 1, 3, 4).reshape(B * mp, Hkv, P, -1) \
+                .contiguous()
+    table = torch.arange(B * mp, dtype=torch.int32, device=DEV).reshape(B, mp)
+    op, lp = sfa.sfa_attn_decode_paged(paged(ci), paged(cv), paged(vc), table, seq_len=seq_t,
+                                       q=qd, scale=scale, o_dtype=torch.float32, window=w,
+                                       n_global=g)
+    torch.cuda.synchronize()
+    assert torch.equal(op, o) and torch.equal(lp, lse)
+    oci, ocv = oracle.topk_encode_bf16(kd.cpu().numpy(), k)
+    oqi, oqv = oracle.topk_encode(qd.cpu().numpy(), k)
+    O, Ls = oracle.attn_decode(oqi, oqv, oci, ocv, np_vals(vc), d, scale, seq_len=seq,
+                               window=w, n_global=g)
+    check_o(o, O, TOL_O_BF16V, f"decode window {w} global {g} O")
+    check_lse(lse, Ls, f"decode window {w} global {g} LSE")
