@@ -93,23 +93,48 @@ def _fwd_inputs(w):
     return q, k, v
 
 
-def _overlap_count(qi: torch.Tensor, ki: torch.Tensor, d: int, G: int, causal: bool) -> int:
+def _key_ranges(n: int, causal: bool, window: int, n_global: int, device):
+    """Per query position i, the keys it may see as two ranges: [lo, hi] and
+    the global keys below the window, [0, glob_end)."""
+    i = torch.arange(n, device=device)
+    hi = i.clone() if causal else torch.full_like(i, n - 1)
+    lo = torch.zeros_like(i)
+    glob_end = torch.zeros_like(i)
+    if window > 0:
+        isg = i < n_global
+        lo = torch.where(isg, lo, (i - window + 1).clamp(min=0))
+        if not causal:
+            hi = torch.where(isg, hi, (i + window - 1).clamp(max=n - 1))
+        glob_end = torch.where(isg, glob_end, torch.minimum(torch.full_like(i, n_global), lo))
+    return lo, hi, glob_end
+
+
+def _allowed_pairs(n: int, causal: bool, window: int = 0, n_global: int = 0) -> int:
+    lo, hi, ge = _key_ranges(n, causal, window, n_global, "cpu")
+    return int((hi - lo + 1 + ge).sum().item())
+
+
+def _overlap_count(qi: torch.Tensor, ki: torch.Tensor, d: int, G: int, causal: bool,
+                   window: int = 0, n_global: int = 0) -> int:
     """Exact E = sum over allowed (i, j) of |S_i cap S_j| (accounting only):
-    per coordinate, the number of keys j <= i holding it, summed over the
-    query's coordinates."""
+    per coordinate, the number of allowed keys holding it (prefix counts over
+    the key ranges), summed over the query's coordinates."""
     B, Hq, n, k = qi.shape
+    lo, hi, ge = _key_ranges(n, causal, window, n_global, qi.device)
     E = 0
     for b in range(B):
         for g in range(ki.shape[1]):
             km = torch.zeros((n, d), dtype=torch.int32, device=qi.device)
             km.scatter_(1, ki[b, g].long(), 1)
-            kc = torch.cumsum(km, 0) if causal else km.sum(0, keepdim=True).expand(n, d)
+            kc = torch.cat([torch.zeros((1, d), dtype=torch.int32, device=qi.device),
+                            torch.cumsum(km, 0, dtype=torch.int32)])  # kc[j] = keys < j
+            cnt = kc[hi + 1] - kc[lo] + kc[ge]
             for h in range(g * G, (g + 1) * G):
-                E += int(torch.gather(kc, 1, qi[b, h].long()).sum().item())
+                E += int(torch.gather(cnt, 1, qi[b, h].long()).sum().item())
     return E
 
 
-def bench_fwd(w, steps, warmup, want_cpu):
+def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     q, k, v = _fwd_inputs(w)
     B, Hq, Hkv, n, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
     qi = torch.empty((B, Hq, n, kk), dtype=torch.int32, device=DEV)
@@ -125,7 +150,8 @@ def bench_fwd(w, steps, warmup, want_cpu):
         sfa.sfa_topk_encode(k, kk, idx=ki, val=kv)
         if ev is not None:
             ev[0].record()
-        sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse, ws=ws)
+        sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse, ws=ws,
+                         window=window, n_global=n_global)
         if ev is not None:
             ev[1].record()
 
@@ -148,15 +174,15 @@ def bench_fwd(w, steps, warmup, want_cpu):
     fwd_ms = [a.elapsed_time(b_) for a, b_ in evs]
     fwd_avg = float(np.mean(fwd_ms))
 
-    pairs_per_head = n * (n + 1) // 2 if w.causal else n * n
-    pairs = B * Hq * pairs_per_head
+    pairs = B * Hq * _allowed_pairs(n, w.causal, window, n_global)
     pv_flops = 2.0 * d * pairs          # P.V: 2 d flops per allowed pair
-    E = _overlap_count(qi, ki, d, w.G, w.causal)
+    E = _overlap_count(qi, ki, d, w.G, w.causal, window, n_global)
     algo_flops = pv_flops + 2.0 * E     # + one multiply-add per overlapping coordinate
     achieved = algo_flops / (fwd_avg * 1e-3)
     tokens = B * n
     out = {
-        "metric": METRIC,
+        "metric": METRIC if window == 0 else
+        METRIC + f"; sliding window {window} + {n_global} global tokens",
         "value": tokens / (ms_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -170,7 +196,7 @@ def bench_fwd(w, steps, warmup, want_cpu):
         "data": "synthetic",
         "config": {
             "workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "n": n, "d": d, "k": kk,
-            "causal": w.causal, "seed": w.seed,
+            "causal": w.causal, "seed": w.seed, "window": window, "n_global": n_global,
             "step": "sfa_topk_encode(Q) + sfa_topk_encode(K) + sfa_attn_fwd",
             "precision": ("codes fp32; scores fp32 (three bf16 piece products on MFMA); softmax fp32; "
                           "P.V fp16 MFMA on V converted exactly to fp16, fp32 accumulate; O bf16"),
@@ -194,7 +220,7 @@ def bench_fwd(w, steps, warmup, want_cpu):
         },
         "wall_s_timed": wall,
     }
-    if want_cpu:
+    if want_cpu and window == 0:
         out["cpu_baseline"] = cpu_baseline_fwd(w, q, k, v)
     return out
 
@@ -384,7 +410,15 @@ CODE_FORMATS = {"i16bf16": (torch.int16, torch.bfloat16), "u8f16": (torch.uint8,
 _CODE_NAMES = {"i16bf16": "int16/bf16", "u8f16": "uint8/float16"}
 
 
-def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16"):
+def _decode_keys(L: int, window: int, n_global: int) -> int:
+    """Keys the decode query (position L - 1) may see."""
+    if window <= 0 or L - 1 < n_global:
+        return L
+    lo = max(0, L - window)
+    return (L - lo) + min(n_global, lo)
+
+
+def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16", window=0, n_global=0):
     B, Hq, Hkv, L, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
     idt, vdt = CODE_FORMATS[codes]
     cbytes = kk * (idt.itemsize + vdt.itemsize)  # cache code bytes per key
@@ -404,7 +438,8 @@ def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16"):
     ws = torch.empty(sfa.sfa_attn_decode_workspace(B, Hq, L, d), dtype=torch.uint8, device=DEV)
 
     def step():
-        sfa.sfa_attn_decode(qi, qv, ci, cv, vc, scale=w.scale, o=o, lse=lse, ws=ws)
+        sfa.sfa_attn_decode(qi, qv, ci, cv, vc, scale=w.scale, o=o, lse=lse, ws=ws, window=window,
+                            n_global=n_global)
 
     for _ in range(warmup):
         step()
@@ -417,7 +452,8 @@ def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16"):
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
-    algo_bytes = B * Hkv * L * (cbytes + d * 2) + B * Hq * (kk * 8 + d * 2 + 4)
+    algo_bytes = B * Hkv * _decode_keys(L, window, n_global) * (cbytes + d * 2) + \
+        B * Hq * (kk * 8 + d * 2 + 4)
     achieved = algo_bytes / (ms * 1e-3)
     out = {
         "metric": f"SFA decode tokens/s, 64 seqs x 64K sparse-code cache (k=16 {_CODE_NAMES[codes]}, "
@@ -428,7 +464,7 @@ def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16"):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "L": L, "d": d, "k": kk,
-                   "cache_codes": codes,
+                   "cache_codes": codes, "window": window, "n_global": n_global,
                    "step": "sfa_attn_decode (split context + LSE merge)"},
         "roofline": {"kernel": "sfa_decode_kernel + combine", "bound": "hbm",
                      "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
@@ -547,6 +583,10 @@ def main():
     ap.add_argument("--codes", default="i16bf16", choices=sorted(CODE_FORMATS),
                     help="decode workloads: cache code storage (int16 indices + bf16 values, or "
                          "the paper's compact uint8 indices + float16 values)")
+    ap.add_argument("--window", type=int, default=0,
+                    help="token sparsity composed with SFA: sliding window (0: none)")
+    ap.add_argument("--n-global", type=int, default=0,
+                    help="leading global tokens with --window")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 1 GiB device copy twice (reference for "
@@ -564,11 +604,13 @@ def main():
     if w.kind == "decode" and args.cache == "paged":
         out = bench_decode_paged(w, args.steps, args.warmup, args.codes)
     elif w.kind == "decode":
-        out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline, args.codes)
+        out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline, args.codes,
+                           args.window, args.n_global)
     elif args.which == "bwd":
         out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
     else:
-        out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
+        out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
+                        args.n_global)
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device=DEV)
         dst = torch.empty_like(src)

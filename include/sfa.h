@@ -241,7 +241,7 @@ size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d);
  *                 sfa_attn_decode_workspace(B, Hq, Lmax, d) bytes; its
  *                 contents need no initialisation and are scratch after the
  *                 call.  Concurrent calls must use distinct workspaces.
- * Limits: B, Hq, Hkv, Lmax >= 1; Hq % Hkv == 0; Hq / Hkv <= 8;
+ * Limits: B, Hq, Hkv, Lmax >= 1; Lmax <= 2^30; Hq % Hkv == 0; Hq / Hkv <= 8;
  *         d in {64, 128}; 1 <= k <= d; window, n_global >= 0.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (ws_bytes too small), SFA_EHIP.
  */

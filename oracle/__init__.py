@@ -8,5 +8,5 @@ from .sfa_oracle import (  # noqa: F401
     softmax_attention, attn_fwd, attn_fwd_rows, attn_decode, overlap_count,
     csr_bytes, softmax_attention_grad, attn_bwd, attn_bwd_rows, attn_bwd_cols,
     cache_location, cache_capacity, kv_append, cache_gather, attn_decode_paged,
-    f16_rne, widen_f16, topk_encode_f16, csr_densify, csr_to_fixed,
+    f16_rne, widen_f16, topk_encode_f16, csr_densify, csr_to_fixed, token_mask,
 )

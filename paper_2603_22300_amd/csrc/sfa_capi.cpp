@@ -148,6 +148,7 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
   if (!q_idx || !q_val || !kc_idx || !kc_val || !v_cache || !o || !ws) return SFA_EINVAL;
   if (B < 1 || Hq < 1 || Hkv < 1 || Lmax < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
   if (window < 0 || n_global < 0) return SFA_EINVAL;
+  if (Lmax > (1 << 30)) return SFA_ENOTSUP;
   if (Hq % Hkv != 0) return SFA_EINVAL;
   if (!is_idx(q_idx_t) || !is_cval(q_val_t) || !is_idx(kc_idx_t) || !is_cval(kc_val_t) ||
       !is_val(v_t) || !is_val(o_t))

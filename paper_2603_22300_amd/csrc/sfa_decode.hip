@@ -42,13 +42,14 @@ struct DecParams {
   float* ws_m;  // [B*Hq, nch]
   float* ws_l;  // [B*Hq, nch]
   float* ws_o;  // [B*Hq, nch, D]
-  int Hq, Hkv, Lmax, k, nch;
+  int Hq, Hkv, Lmax, k, nch;  // nch: partial slots per (b, h)
   float scale_log2;
   int qifmt, qvfmt, kifmt, kvfmt;
   const float* q_dense;   // [B, Hq, D] or null (then q_idx / q_val)
   const int32_t* table;   // paged: [B, max_pages]
   int max_pages, log2P, num_pages;
   int window, n_global;   // token pattern (window 0: all cached keys)
+  int nvc;                // window: workgroups per (b, KV head) (0: nch)
 };
 
 __device__ __forceinline__ int seq_len_of(const int32_t* seq_len, int b, int Lmax) {
@@ -73,11 +74,23 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   __shared__ float red_o[kDecWaves][G][D];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int chunk = blockIdx.x;
   const int bh = blockIdx.y;
   const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
   const int L = seq_len_of(p.seq_len, b, p.Lmax);
-  const int c0 = chunk * kDecChunk;
+  // Token window: the query (position L - 1) sees keys [0, wg) and [wlo, L)
+  // only.  The grid then covers only the chunks holding them: workgroup x
+  // takes the x-th of the global chunks followed by the window's chunks, and
+  // writes its partial to slot x (past the last such chunk: an empty one).
+  const bool winq = p.window > 0 && L - 1 >= p.n_global;
+  const int wlo = winq ? max(0, L - p.window) : 0;
+  const int wg = winq ? min(p.n_global, L) : 0;
+  int chunk = blockIdx.x;
+  if (winq) {
+    const int ngc = (wg + kDecChunk - 1) / kDecChunk;
+    const int wc0 = max(ngc, wlo / kDecChunk);
+    chunk = chunk < ngc ? chunk : wc0 + (chunk - ngc);
+  }
+  const int c0 = chunk * kDecChunk;  // at most Lmax + 2 chunks: no overflow
   const int c1 = min(L, c0 + kDecChunk);
   const int k = p.k;
   const int dmask = D - 1;
@@ -127,12 +140,8 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   const int per_wave = kDecChunk / kDecWaves;
   int w0 = c0 + wave * per_wave;
   int w1 = min(c1, w0 + per_wave);
-  // Token window: the query (position L - 1) sees keys [0, wg) and
-  // [wlo, L) only.  A wave range inside the gap does nothing; one that starts
-  // in it starts at the window (64-aligned; the keys before wlo are masked).
-  const bool winq = p.window > 0 && L - 1 >= p.n_global;
-  const int wlo = winq ? max(0, L - p.window) : 0;
-  const int wg = winq ? min(p.n_global, L) : 0;
+  // A wave range inside the window's gap does nothing; one that starts in it
+  // starts at the window (64-aligned; the keys before wlo are masked).
   if (winq && w0 >= wg) {
     if (w1 <= wlo) w1 = w0;
     else w0 = max(w0, wlo & ~63);
@@ -331,7 +340,7 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
       lsum += sc * red_l[w][h];
       osum += sc * red_o[w][h][dd];
     }
-    const int64_t slot = ((int64_t)b * p.Hq + hkv * G + h) * p.nch + chunk;
+    const int64_t slot = ((int64_t)b * p.Hq + hkv * G + h) * p.nch + blockIdx.x;
     p.ws_o[slot * D + dd] = osum;
     if (dd == 0) { p.ws_m[slot] = M; p.ws_l[slot] = lsum; }
   }
@@ -342,12 +351,13 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
 template <int D>
 __global__ __launch_bounds__(D) void sfa_decode_combine_kernel(
     const float* __restrict__ ws_m, const float* __restrict__ ws_l, const float* __restrict__ ws_o,
-    const int32_t* seq_len, int Hq, int Lmax, int nch, void* o, int obf16, float* lse) {
+    const int32_t* seq_len, int Hq, int Lmax, int nch, int nvc, void* o, int obf16, float* lse) {
   const int bh = blockIdx.x;
   const int b = bh / Hq;
   const int dd = threadIdx.x;
   const int L = seq_len_of(seq_len, b, Lmax);
-  const int nc = (L + kDecChunk - 1) / kDecChunk;
+  // slots written this call: the chunks up to L, or the nvc of a window grid
+  const int nc = nvc > 0 ? nvc : (L + kDecChunk - 1) / kDecChunk;
   const int64_t s0 = (int64_t)bh * nch;
   float M = -INFINITY;
   for (int c = 0; c < nc; ++c) M = fmaxf(M, ws_m[s0 + c]);
@@ -371,7 +381,7 @@ size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d) {
 
 template <int D, int G, bool VBF16, int KC8, bool C8>
 static void launch_dec_t(const DecParams& p, int B, hipStream_t stream) {
-  dim3 grid(p.nch, B * p.Hkv), block(kDecThreads);
+  dim3 grid(p.nvc > 0 ? p.nvc : p.nch, B * p.Hkv), block(kDecThreads);
   if (p.table)
     hipLaunchKernelGGL((sfa_decode_kernel<D, G, VBF16, KC8, C8, true>), grid, block, 0, stream, p);
   else
@@ -423,6 +433,14 @@ hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   p.table = a.table;
   p.max_pages = a.max_pages; p.log2P = a.log2P; p.num_pages = a.num_pages;
   p.window = a.window; p.n_global = a.n_global;
+  p.nvc = 0;
+  if (a.window > 0) {
+    // the global chunks, the window's chunks (one more when it straddles a
+    // chunk boundary), never more than the whole context
+    const int g = min(a.n_global, a.Lmax);
+    const int v = (g + kDecChunk - 1) / kDecChunk + (a.window + kDecChunk - 1) / kDecChunk + 1;
+    p.nvc = min(v, p.nch);
+  }
   const int G = a.Hq / a.Hkv, B = a.B;
   if (a.d == 64) {
     if (a.vbf16) launch_dec_g<64, true>(p, G, B, stream); else launch_dec_g<64, false>(p, G, B, stream);
@@ -433,10 +451,12 @@ hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream) {
   if (e != hipSuccess) return e;
   if (a.d == 64)
     hipLaunchKernelGGL(sfa_decode_combine_kernel<64>, dim3(B * a.Hq), dim3(64), 0, stream,
-                       p.ws_m, p.ws_l, p.ws_o, a.seq_len, a.Hq, a.Lmax, p.nch, a.o, a.obf16, a.lse);
+                       p.ws_m, p.ws_l, p.ws_o, a.seq_len, a.Hq, a.Lmax, p.nch, p.nvc, a.o,
+                       a.obf16, a.lse);
   else
     hipLaunchKernelGGL(sfa_decode_combine_kernel<128>, dim3(B * a.Hq), dim3(128), 0, stream,
-                       p.ws_m, p.ws_l, p.ws_o, a.seq_len, a.Hq, a.Lmax, p.nch, a.o, a.obf16, a.lse);
+                       p.ws_m, p.ws_l, p.ws_o, a.seq_len, a.Hq, a.Lmax, p.nch, p.nvc, a.o,
+                       a.obf16, a.lse);
   return hipGetLastError();
 }
 
