@@ -468,16 +468,17 @@ def attn_decode_paged(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, d: int, sc
 
 
 def softmax_attention_grad(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, do: np.ndarray,
-                           scale: float, causal: bool):
-    """Gradients of O = softmax(scale * qd kd^T, causal mask) v for one head,
-    dense float64, queries at positions 0..r-1 and keys at 0..n_k-1.
+                           scale: float, causal: bool, window: int = 0, n_global: int = 0):
+    """Gradients of O = softmax(scale * qd kd^T, mask) v for one head, dense
+    float64, queries at positions 0..r-1 and keys at 0..n_k-1; the mask is
+    token_mask (causal, window, global tokens).
 
     With P the row-normalised weights: dV = P^T dO, dP = dO V^T,
     dS = P * (dP - rowsum(dP * P)), dQ = scale dS K, dK = scale dS^T Q.
     Returns (dQ [r, d], dK [n_k, d], dV [n_k, dv])."""
     S = scale * (qd @ kd.T)
-    if causal:
-        allowed = np.arange(kd.shape[0])[None, :] <= np.arange(qd.shape[0])[:, None]
+    if causal or window > 0:
+        allowed = token_mask(np.arange(qd.shape[0]), kd.shape[0], causal, window, n_global)
         S = np.where(allowed, S, -np.inf)
     P = np.exp(S - S.max(axis=1, keepdims=True))
     P /= P.sum(axis=1, keepdims=True)
@@ -487,7 +488,8 @@ def softmax_attention_grad(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, do: np
     return scale * (dS @ kd), scale * (dS.T @ qd), dV
 
 
-def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bool):
+def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bool,
+             window: int = 0, n_global: int = 0):
     """SFA backward on codes (Sec. 3.1, Eq. (6)).
 
     Inputs as attn_fwd, plus do [B, Hq, n, dv] (float32, or uint16 bf16
@@ -509,7 +511,8 @@ def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bo
             dkd = np.zeros_like(kd)
             for h in range(g * G, (g + 1) * G):
                 qd = densify(q_idx[b, h], q_val[b, h], d)
-                gq, gk, gv = softmax_attention_grad(qd, kd, vv[b, g], dd[b, h], scale, causal)
+                gq, gk, gv = softmax_attention_grad(qd, kd, vv[b, g], dd[b, h], scale, causal,
+                                                    window, n_global)
                 dq[b, h] = np.take_along_axis(gq, np.asarray(q_idx[b, h], dtype=np.int64), 1)
                 dkd += gk
                 dv[b, g] += gv
@@ -518,7 +521,7 @@ def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bo
 
 
 def attn_bwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, do_bh, d: int, scale: float,
-                  causal: bool, rows):
+                  causal: bool, rows, window: int = 0, n_global: int = 0):
     """dq_val (Eq. (6)) of the selected query rows of one head, each row on
     its own: p = softmax over the row's allowed keys, dp = V do_i,
     ds = p * (dp - p.dp), dq~ = scale ds K~, read at the row's support.
@@ -528,18 +531,18 @@ def attn_bwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, do_bh, d: int, s
     out = np.empty((len(rows), np.shape(q_idx_bh)[1]), dtype=np.float64)
     for r, i in enumerate(rows):
         qd = densify(q_idx_bh[i][None], q_val_bh[i][None], d)[0]
-        last = int(i) + 1 if causal else kd.shape[0]
-        s = scale * (kd[:last] @ qd)
+        keys = np.flatnonzero(token_mask([int(i)], kd.shape[0], causal, window, n_global)[0])
+        s = scale * (kd[keys] @ qd)
         p = np.exp(s - s.max())
         p /= p.sum()
-        dp = vv[:last] @ dd[i]
+        dp = vv[keys] @ dd[i]
         ds = p * (dp - p @ dp)
-        out[r] = (scale * (ds @ kd[:last]))[np.asarray(q_idx_bh[i], dtype=np.int64)]
+        out[r] = (scale * (ds @ kd[keys]))[np.asarray(q_idx_bh[i], dtype=np.int64)]
     return out
 
 
 def attn_bwd_cols(q_idx_bg, q_val_bg, k_idx_bg, k_val_bg, v_bg, do_bg, d: int, scale: float,
-                  causal: bool, cols, row_chunk: int = 1024):
+                  causal: bool, cols, row_chunk: int = 1024, window: int = 0, n_global: int = 0):
     """dk_val and dv (Eq. (6)) of the selected keys of one KV head, summed
     over its query heads: q_*_bg [G, n, k], do_bg [G, n, dv].  Each query
     row's LSE_i and D_i = dO_i . O_i come from the plain forward
@@ -556,11 +559,13 @@ def attn_bwd_cols(q_idx_bg, q_val_bg, k_idx_bg, k_val_bg, v_bg, do_bg, d: int, s
     dkd = np.zeros((len(cols), d), dtype=np.float64)
     for h in range(np.shape(q_idx_bg)[0]):
         qd = densify(q_idx_bg[h], q_val_bg[h], d)
-        O, L = softmax_attention(qd, kd, vv, scale, causal, row_chunk=row_chunk)
+        O, L = softmax_attention(qd, kd, vv, scale, causal, row_chunk=row_chunk, window=window,
+                                 n_global=n_global)
         D = (dd[h] * O).sum(axis=1)
         S = scale * (qd @ kd[cols].T)                      # [n, len(cols)]
-        if causal:
-            S = np.where(np.arange(n)[:, None] >= cols[None, :], S, -np.inf)
+        if causal or window > 0:
+            allowed = token_mask(np.arange(n), n, causal, window, n_global)[:, cols]
+            S = np.where(allowed, S, -np.inf)
         P = np.exp(S - L[:, None])
         dS = P * (dd[h] @ vv[cols].T - D[:, None])
         dv += P.T @ dd[h]

@@ -119,3 +119,41 @@ def test_decode_window(w, g):
         Of, Lf = oracle.attn_fwd(qs, qsv, ki[b:b + 1, :, :Lb], kv[b:b + 1, :, :Lb],
                                  v[b:b + 1, :, :Lb], d, 0.4, True, window=w, n_global=g)
         assert np.abs(Of[0, :, -1] - O[b]).max() < 1e-12
+
+
+@pytest.mark.parametrize("causal,w,g", [(True, 6, 0), (True, 5, 3), (False, 4, 2)])
+def test_backward_with_window(causal, w, g):
+    """The oracle's backward under the token mask: torch autograd (float64)
+    through the dense formulation with the band mask built from tril / triu,
+    read at the supports (Eq. (6)), and the row / column forms."""
+    rng = np.random.default_rng(w + g)
+    B, Hq, Hkv, n, d, k = 1, 2, 1, 23, 16, 4
+    q = rng.standard_normal((B, Hq, n, d)).astype(np.float32)
+    kk = rng.standard_normal((B, Hkv, n, d)).astype(np.float32)
+    v = rng.standard_normal((B, Hkv, n, 10))
+    do = rng.standard_normal((B, Hq, n, 10))
+    qi, qv = oracle.topk_encode(q, k)
+    ki, kv = oracle.topk_encode(kk, k)
+    dq, dk, dv = oracle.attn_bwd(qi, qv, ki, kv, v, do, d, 0.3, causal, window=w, n_global=g)
+    ones = torch.ones(n, n, dtype=torch.bool)
+    band = torch.tril(ones, w - 1) & torch.triu(ones, -(w - 1))
+    band[:g, :] = True
+    band[:, :g] = True
+    mask = band & torch.tril(ones) if causal else band
+    Qd = torch.tensor(oracle.densify(qi, qv, d), requires_grad=True)
+    Kd = torch.tensor(oracle.densify(ki, kv, d), requires_grad=True)
+    V = torch.tensor(v, requires_grad=True)
+    S = 0.3 * torch.matmul(Qd, Kd.repeat_interleave(2, dim=1).transpose(-1, -2))
+    O = torch.matmul(torch.softmax(S.masked_fill(~mask, float("-inf")), -1),
+                     V.repeat_interleave(2, dim=1))
+    (O * torch.from_numpy(do)).sum().backward()
+    assert np.abs(np.take_along_axis(Qd.grad.numpy(), qi.astype(np.int64), -1) - dq).max() < 1e-12
+    assert np.abs(np.take_along_axis(Kd.grad.numpy(), ki.astype(np.int64), -1) - dk).max() < 1e-12
+    assert np.abs(V.grad.numpy() - dv).max() < 1e-12
+    rows, cols = [0, 5, 22], [0, 3, 17, 22]
+    got = oracle.attn_bwd_rows(qi[0, 1], qv[0, 1], ki[0, 0], kv[0, 0], v[0, 0], do[0, 1], d, 0.3,
+                               causal, rows, window=w, n_global=g)
+    assert np.abs(got - dq[0, 1, rows]).max() < 1e-12
+    gk, gv = oracle.attn_bwd_cols(qi[0], qv[0], ki[0, 0], kv[0, 0], v[0, 0], do[0], d, 0.3, causal,
+                                  cols, window=w, n_global=g)
+    assert np.abs(gk - dk[0, 0, cols]).max() < 1e-12 and np.abs(gv - dv[0, 0, cols]).max() < 1e-12
