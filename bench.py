@@ -225,14 +225,14 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     return out
 
 
-def bench_bwd(w, steps, warmup, want_cpu):
+def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     """One step = sfa_attn_bwd (codes, O, LSE and dO resident in HBM)."""
     q, k, v = _fwd_inputs(w)
     B, Hq, Hkv, n, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
     qi, qv = sfa.sfa_topk_encode(q, kk)
     ki, kv = sfa.sfa_topk_encode(k, kk)
     o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale,
-                              o_dtype=torch.bfloat16)
+                              o_dtype=torch.bfloat16, window=window, n_global=n_global)
     dout = torch.empty((B, Hq, n, d), dtype=torch.bfloat16, device=DEV)
     for b in range(B):
         for h in range(Hq):
@@ -244,7 +244,7 @@ def bench_bwd(w, steps, warmup, want_cpu):
 
     def step():
         sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=w.causal, scale=w.scale,
-                         dq=dq, dk=dk, dv=dv, ws=ws)
+                         dq=dq, dk=dk, dv=dv, ws=ws, window=window, n_global=n_global)
 
     for _ in range(warmup):
         step()
@@ -260,14 +260,14 @@ def bench_bwd(w, steps, warmup, want_cpu):
     wall = time.perf_counter() - wall0
     ms = [a.elapsed_time(b_) for a, b_ in evs]
     ms_step = float(np.mean(ms))
-    pairs_per_head = n * (n + 1) // 2 if w.causal else n * n
-    pairs = B * Hq * pairs_per_head
-    E = _overlap_count(qi, ki, d, w.G, w.causal)
+    pairs = B * Hq * _allowed_pairs(n, w.causal, window, n_global)
+    E = _overlap_count(qi, ki, d, w.G, w.causal, window, n_global)
     # dV and dP: 2d flops per allowed pair each; S, dq~ and dk~ on the
     # supports: 2 flops per shared coordinate each
     algo = 4.0 * d * pairs + 6.0 * E
     out = {
-        "metric": "SFA bwd (straight-through estimator) tokens/s at n=32K,d=128,k=16",
+        "metric": "SFA bwd (straight-through estimator) tokens/s at n=32K,d=128,k=16" +
+                  (f"; sliding window {window} + {n_global} global tokens" if window else ""),
         "value": B * n / (ms_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -281,7 +281,8 @@ def bench_bwd(w, steps, warmup, want_cpu):
         "data": "synthetic",
         "config": {
             "workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "n": n, "d": d, "k": kk,
-            "causal": w.causal, "seed": w.seed, "step": "sfa_attn_bwd",
+            "causal": w.causal, "seed": w.seed, "window": window, "n_global": n_global,
+            "step": "sfa_attn_bwd",
             "precision": "O and dO bf16; products on MFMA with bf16 hi/lo pieces (3 terms), "
                          "fp32 accumulate; gradients fp32",
         },
@@ -300,7 +301,7 @@ def bench_bwd(w, steps, warmup, want_cpu):
         },
         "wall_s_timed": wall,
     }
-    if want_cpu:
+    if want_cpu and window == 0:
         out["cpu_baseline"] = cpu_baseline_bwd(w, q, k, v, dout)
     return out
 
@@ -607,7 +608,8 @@ def main():
         out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline, args.codes,
                            args.window, args.n_global)
     elif args.which == "bwd":
-        out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline)
+        out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
+                        args.n_global)
     else:
         out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
                         args.n_global)

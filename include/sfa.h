@@ -182,7 +182,10 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
  * q_idx[..., t].  A KV head's dk_val and dv sum over the query heads that
  * read it.
  *
- * q_*, k_*, v, B ... o_t   as sfa_attn_fwd (o and dout share o_t)
+ * q_*, k_*, v, B ... o_t   as sfa_attn_fwd (o and dout share o_t), including
+ *               the token window: the allowed keys must be those of the
+ *               forward that produced o and lse; tiles outside every
+ *               row's (key's) window are skipped in each kernel.
  * o             [B, Hq, n, d]   the forward's output
  * lse           [B, Hq, n] float32, the forward's LSE (natural log)
  * dout          [B, Hq, n, d]   dL/dO
@@ -205,7 +208,7 @@ sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val,
                         const void* v, const void* o, const float* lse,
                         const void* dout,
                         int B, int Hq, int Hkv, int n, int d, int k,
-                        int causal, float scale,
+                        int causal, int window, int n_global, float scale,
                         int idx_t, int qk_val_t, int v_t, int o_t,
                         float* dq_val, float* dk_val, float* dv,
                         void* ws, size_t ws_bytes, void* stream);

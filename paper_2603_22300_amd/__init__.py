@@ -64,7 +64,7 @@ def lib() -> ctypes.CDLL:
                                          f32, i32, i32, i32, i32, vp, vp, vp]
         L.sfa_attn_bwd.restype = i32
         L.sfa_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
-                                   i32, f32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
+                                   i32, i32, i32, f32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]
         L.sfa_attn_bwd_workspace.restype = sz
         L.sfa_attn_bwd_workspace.argtypes = [i32, i32, i32, i32, i32]
         L.sfa_attn_decode_workspace.restype = sz
@@ -217,8 +217,9 @@ def sfa_attn_bwd_workspace(B: int, Hq: int, Hkv: int, n: int, d: int) -> int:
 def sfa_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, causal: bool = True,
                  scale: float | None = None, dq: torch.Tensor | None = None,
                  dk: torch.Tensor | None = None, dv: torch.Tensor | None = None,
-                 ws: torch.Tensor | None = None):
-    """SFA backward (straight-through estimator).  Shapes as sfa_attn_fwd;
+                 ws: torch.Tensor | None = None, window: int = 0, n_global: int = 0):
+    """SFA backward (straight-through estimator).  Shapes as sfa_attn_fwd, and
+    the same causal / window / n_global as the forward that gave o and lse;
     o, dout [B, Hq, n, d] (same dtype), lse [B, Hq, n] float32.  Returns
     (dq_val [B, Hq, n, k], dk_val [B, Hkv, n, k], dv [B, Hkv, n, d]), float32:
     the gradients of the code values (Eq. (6): zero off the supports)."""
@@ -255,7 +256,8 @@ def sfa_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, causal: bool = Tru
     _call(lib().sfa_attn_bwd(q_idx.data_ptr(), q_val.data_ptr(), k_idx.data_ptr(),
                              k_val.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
                              dout.data_ptr(), B, Hq, Hkv, n, d, k, int(bool(causal)),
-                             float(scale), it, qt, vt, ot, dq.data_ptr(), dk.data_ptr(),
+                             int(window), int(n_global), float(scale), it, qt, vt, ot,
+                             dq.data_ptr(), dk.data_ptr(),
                              dv.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
                              _stream(v)), "sfa_attn_bwd")
     return dq, dk, dv

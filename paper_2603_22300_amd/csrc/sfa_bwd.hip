@@ -72,6 +72,7 @@ struct BwdParams {
   unsigned char* qimg;
   unsigned char* kimg;
   int Hq, Hkv, G, n, k, causal;
+  int window, n_global;  // token pattern: |i - j| < window or a global token (window 0: none)
   int ifmt, vfmt, vbf16, obf16;
   int nt;    // tiles per head: ceil(n / 32)
   int BR;    // query positions per dq workgroup: 256 / G
@@ -294,19 +295,38 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
     for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
   const int blk_last = min(n, i0 + p.BR) - 1;
-  const int nkt = ((p.causal ? blk_last + 1 : n) + kT - 1) / kT;
+  // Key tiles of the block: all up to the causal limit, or with a token
+  // window (and no global row here) the global tiles [0, gt_end) and the
+  // window tiles [wt_begin, nkt_all); the gap between them is skipped.
+  const bool win = p.window > 0;
+  int kend = p.causal ? blk_last + 1 : n;
+  int gt_end = 0, wt_begin = 0;
+  if (win && i0 >= p.n_global) {
+    if (!p.causal) kend = min(n, blk_last + p.window);
+    gt_end = (p.n_global + kT - 1) / kT;
+    wt_begin = max(0, i0 - p.window + 1) / kT;
+    if (wt_begin <= gt_end) gt_end = wt_begin = 0;  // no gap
+  }
+  const int nkt = gt_end + (kend + kT - 1) / kT - wt_begin;
+  auto tile_at = [&](int t) { return t < gt_end ? t : wt_begin + (t - gt_end); };
+  // a key tile from j0 on meets the window of some row of this wave
+  auto in_window = [&](int j0) {
+    return !win || j0 < p.n_global || pos0 < p.n_global ||
+           (j0 + kT - 1 > pos0 - p.window && j0 < wave_i_max + p.window);
+  };
   const unsigned char* kimg0 = p.kimg + (int64_t)bh * p.nt * I::KB;
-  dma<kNWQ>(kimg0, smem, I::KB, wave, lane);
+  if (nkt > 0) dma<kNWQ>(kimg0 + (int64_t)tile_at(0) * I::KB, smem, I::KB, wave, lane);
   wait_vm();
   __syncthreads();
-  for (int jt = 0; jt < nkt; ++jt) {
-    const int stage = jt & 1;
+  for (int t = 0; t < nkt; ++t) {
+    const int stage = t & 1;
+    const int jt = tile_at(t);
     // reads through `cur`, the copy of the next tile through `nxt` (restrict:
     // no compiler wait on the copy before the reads)
     auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
-    if (jt + 1 < nkt) dma<kNWQ>(kimg0 + (int64_t)(jt + 1) * I::KB, nxt, I::KB, wave, lane);
+    if (t + 1 < nkt) dma<kNWQ>(kimg0 + (int64_t)tile_at(t + 1) * I::KB, nxt, I::KB, wave, lane);
     const int j0 = jt * kT;
-    if (wave_ok && (!p.causal || wave_i_max >= j0)) {
+    if (wave_ok && (!p.causal || wave_i_max >= j0) && in_window(j0)) {
       const unsigned char* K = cur;
       const uint16_t* rmk = (const uint16_t*)(K + I::K_RMK);
       const uint16_t* trk = (const uint16_t*)(K + I::K_TRK);
@@ -332,7 +352,8 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = j0 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        const bool ok = row_ok && j < n && (!p.causal || j <= my_i);
+        const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
+                        (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
         const float pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -L2)) : 0.f;
         uint16_t h, l;
         split2(pr * (dp[r] - Dq), h, l);
@@ -428,9 +449,30 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   // the last tile down, the G heads of a tile together: every workgroup of a
   // KV head starts on the same tile and moves at the same rate, so the
   // resident workgroups read each tile image while it is in L2.
-  const int t0 = p.causal ? j0b / kT : 0;
-  const int total = p.G * (p.nt - t0);
-  auto tile_of = [&](int it) { return p.nt - 1 - it / p.G; };
+  // Query tiles that see a key of the block, swept from the highest down: the
+  // range [t_lo, t_hi], and (non-causal window) the global query tiles below
+  // it, [0, gq_end).  Without a window t_hi is the last tile.
+  const bool win = p.window > 0;
+  int t_lo = p.causal ? j0b / kT : 0, t_hi = p.nt - 1, gq_end = 0;
+  if (win && j0b >= p.n_global) {
+    const int jlast = min(n, j0b + kNW * kT) - 1;
+    t_hi = min(p.nt - 1, (jlast + p.window - 1) / kT);
+    if (!p.causal) {
+      t_lo = max(0, j0b - p.window + 1) / kT;
+      gq_end = min(t_lo, (p.n_global + kT - 1) / kT);
+    }
+  }
+  const int nrange = t_hi - t_lo + 1;
+  const int total = p.G * (nrange + gq_end);
+  auto tile_of = [&](int it) {
+    const int x = it / p.G;
+    return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
+  };
+  // a query tile from q0 on meets the window of some key of this wave
+  auto in_window = [&](int q0) {
+    return !win || q0 < p.n_global || jw0 < p.n_global ||
+           (q0 < jw0 + kT - 1 + p.window && q0 + kT - 1 > jw0 - p.window);
+  };
   // only this kernel's part of each image is copied; LDS holds it from
   // image offset ROFF on
   constexpr int ROFF = PART == kDV ? I::DV_OFF : I::DK_OFF;
@@ -453,7 +495,7 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
     auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
     if (it + 2 < total) dma<kNW>(qimg_of(it + 2), nxt, RLEN, wave, lane);
     const int q0 = tile_of(it) * kT;
-    if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0)) {
+    if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
       const unsigned char* Q = cur - ROFF;  // image offsets apply as is
       const uint16_t* rmq = (const uint16_t*)(Q + I::Q_RMQ);
       const uint16_t* trq = (const uint16_t*)(Q + I::Q_TRQ);
@@ -494,7 +536,8 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
         for (int x = 0; x < 4; ++x) {
           const int r = 4 * g4 + x;
           const int i = q0 + 8 * g4 + 4 * hh + x;
-          const bool ok = key_ok && (!p.causal || i >= my_j);
+          const bool ok = key_ok && (!p.causal || i >= my_j) &&
+                          (!win || abs(i - my_j) < p.window || i < p.n_global || my_j < p.n_global);
           const float pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x])) : 0.f;
           const float val = PART == kDV ? pr : pr * (dp[r] - dv4[x]);
           uint16_t h, l;
@@ -608,12 +651,14 @@ size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d) {
 hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, const void* o, const float* lse,
                            const void* dout, int B, int Hq, int Hkv, int n, int d, int k,
-                           int causal, float scale, int ifmt, int vfmt, int vbf16, int obf16,
-                           float* dq, float* dk, float* dv, void* ws, hipStream_t stream) {
+                           int causal, int window, int n_global, float scale, int ifmt,
+                           int vfmt, int vbf16, int obf16, float* dq, float* dk, float* dv,
+                           void* ws, hipStream_t stream) {
   BwdParams p;
   p.q_idx = q_idx; p.q_val = q_val; p.k_idx = k_idx; p.k_val = k_val; p.v = v; p.o = o;
   p.lse = lse; p.dout = dout; p.dq = dq; p.dk = dk; p.dv = dv;
   p.Hq = Hq; p.Hkv = Hkv; p.G = Hq / Hkv; p.n = n; p.k = k; p.causal = causal;
+  p.window = window; p.n_global = n_global;
   p.ifmt = ifmt; p.vfmt = vfmt; p.vbf16 = vbf16; p.obf16 = obf16;
   p.nt = (n + kT - 1) / kT;
   p.BR = kNWQ * kT / p.G;

@@ -103,16 +103,19 @@ size_t sfa_attn_bwd_workspace(int B, int Hq, int Hkv, int n, int d) {
 sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
                         const void* k_val, const void* v, const void* o, const float* lse,
                         const void* dout, int B, int Hq, int Hkv, int n, int d, int k, int causal,
-                        float scale, int idx_t, int qk_val_t, int v_t, int o_t, float* dq_val,
+                        int window, int n_global, float scale, int idx_t, int qk_val_t, int v_t,
+                        int o_t, float* dq_val,
                         float* dk_val, float* dv, void* ws, size_t ws_bytes, void* stream) {
   sfa_status st = check_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k, scale, idx_t,
                             qk_val_t, v_t, o_t, o);
   if (st != SFA_OK) return st;
   if (!lse || !dout || !dq_val || !dk_val || !dv) return SFA_EINVAL;
+  if (window < 0 || n_global < 0) return SFA_EINVAL;
   if (!pow2_le(Hq / Hkv, sfa::bwd_max_group())) return SFA_ENOTSUP;
   if (ws == nullptr || ws_bytes < sfa::bwd_workspace_bytes(B, Hq, Hkv, n, d)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n,
-                                       d, k, causal != 0, scale, ifmt_of(idx_t),
+                                       d, k, causal != 0, window, window > 0 ? n_global : 0,
+                                       scale, ifmt_of(idx_t),
                                        vfmt_of(qk_val_t), v_t == SFA_BF16, o_t == SFA_BF16,
                                        dq_val, dk_val, dv, ws, (hipStream_t)stream));
 }

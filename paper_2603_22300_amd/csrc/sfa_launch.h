@@ -22,8 +22,9 @@ size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16);
 hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, const void* o, const float* lse,
                            const void* dout, int B, int Hq, int Hkv, int n, int d, int k,
-                           int causal, float scale, int ifmt, int vfmt, int vbf16, int obf16,
-                           float* dq, float* dk, float* dv, void* ws, hipStream_t stream);
+                           int causal, int window, int n_global, float scale, int ifmt,
+                           int vfmt, int vbf16, int obf16, float* dq, float* dk, float* dv,
+                           void* ws, hipStream_t stream);
 size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d);
 int bwd_max_group();
 

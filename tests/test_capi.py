@@ -79,6 +79,7 @@ def test_window_validation(L):
     assert _fwd(L, window=-1) == 1
     assert _fwd(L, window=4, n_global=-2) == 1
     assert _dec(L, window=-3) == 1
+    assert _bwd(L, window=-1) == 1
     assert _paged(L, n_global=-1, ws_bytes=ctypes.c_size_t(1 << 30)) == 1
 
 
@@ -132,7 +133,8 @@ def test_decode_validation_and_workspace(L):
 
 def _bwd(L, **kw):
     a = dict(q_idx=FAKE, q_val=FAKE, k_idx=FAKE, k_val=FAKE, v=FAKE, o=FAKE, lse=FAKE, dout=FAKE,
-             B=1, Hq=4, Hkv=2, n=16, d=64, k=8, causal=1, scale=0.125, idx_t=0, qk_val_t=2,
+             B=1, Hq=4, Hkv=2, n=16, d=64, k=8, causal=1, window=0, n_global=0, scale=0.125,
+             idx_t=0, qk_val_t=2,
              v_t=3, o_t=3, dq=FAKE, dk=FAKE, dv=FAKE, ws=FAKE, ws_bytes=ctypes.c_size_t(1 << 40),
              stream=None)
     a.update(kw)

@@ -1,7 +1,8 @@
 """GPU parity of SFA composed with token sparsity (App. E): a sliding window
 |i - j| < window plus n_global leading global tokens, in the forward (key
-tiles outside every row's window skipped) and in decode (context outside the
-window skipped), against the oracle's token_mask."""
+tiles outside every row's window skipped), the backward (the same in each
+kernel's tile loop) and decode (context outside the window skipped), against
+the oracle's token_mask."""
 import math
 
 import numpy as np
@@ -11,7 +12,8 @@ import torch
 import oracle
 import paper_2603_22300_amd as sfa
 import sfa_inputs as si
-from helpers import TOL_O_BF16V, TOL_O_F32, check_lse, check_o, np_vals, sample_rows
+from helpers import (TOL_GRAD, TOL_O_BF16V, TOL_O_F32, check_grad, check_lse, check_o, np_vals,
+                     sample_rows)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -111,3 +113,74 @@ def test_decode_window(w, g, seq):
                                window=w, n_global=g)
     check_o(o, O, TOL_O_BF16V, f"decode window {w} global {g} O")
     check_lse(lse, Ls, f"decode window {w} global {g} LSE")
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n,d,k,causal,v_bf16,w,g", [
+    (1, 4, 2, 700, 128, 16, True, True, 100, 0),
+    (1, 4, 1, 900, 128, 16, True, True, 200, 3),
+    (1, 2, 2, 400, 64, 8, False, False, 60, 40),
+    (1, 8, 1, 600, 128, 16, True, True, 1, 0),
+    (2, 2, 1, 333, 128, 16, False, True, 45, 0),
+])
+def test_bwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
+    seed = 3 * n + w + g
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed, device=DEV,
+                            v_dtype=torch.bfloat16 if v_bf16 else torch.float32)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    scale = 1 / math.sqrt(d)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=torch.float32,
+                              window=w, n_global=g)
+    dout = si.normal((B, Hq, n, d), seed, "dout", device=DEV)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale,
+                                  window=w, n_global=g)
+    torch.cuda.synchronize()
+    gq, gk, gv = oracle.attn_bwd(qi.cpu().numpy(), qv.cpu().numpy(), ki.cpu().numpy(),
+                                 kv.cpu().numpy(), np_vals(v), np_vals(dout), d, scale, causal,
+                                 window=w, n_global=g)
+    tol = TOL_GRAD[(v_bf16, False)]
+    check_grad(dq, gq, tol, f"dq_val window {w} global {g}")
+    check_grad(dk, gk, tol, f"dk_val window {w} global {g}")
+    check_grad(dv, gv, tol, f"dv window {w} global {g}")
+
+
+def test_bwd_window_qwen3_32k_sampled():
+    """Backward on the 32K GQA workload with a 4096-token window and 4 global
+    tokens (bf16 V, O, dO): dq rows of one head and dk, dv keys of one KV head
+    against the oracle."""
+    w_ = si.workload("qwen3_32k")
+    B, Hq, Hkv, n, d, k, G = w_.B, w_.Hq, w_.Hkv, w_.n, w_.d, w_.k, w_.G
+    win, ng = 4096, 4
+    q = torch.empty((B, Hq, n, d), device=DEV)
+    kk = torch.empty((B, Hkv, n, d), device=DEV)
+    v = torch.empty((B, Hkv, n, d), device=DEV, dtype=torch.bfloat16)
+    dout = torch.empty((B, Hq, n, d), device=DEV, dtype=torch.bfloat16)
+    for h in range(Hq):
+        q[0, h] = si.normal((n, d), w_.seed, "q", 0, h, device=DEV)
+        dout[0, h] = si.normal((n, d), w_.seed, "dout", 0, h, device=DEV).to(torch.bfloat16)
+    for h in range(Hkv):
+        kk[0, h] = si.normal((n, d), w_.seed, "k", 0, h, device=DEV)
+        v[0, h] = si.normal((n, d), w_.seed, "v", 0, h, device=DEV).to(torch.bfloat16)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=w_.scale,
+                              o_dtype=torch.bfloat16, window=win, n_global=ng)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=True, scale=w_.scale,
+                                  window=win, n_global=ng)
+    torch.cuda.synchronize()
+    tol = TOL_GRAD[(True, True)]
+    g = 2
+    oki, okv = ki[0, g].cpu().numpy(), kv[0, g].cpu().numpy()
+    vn, dn = np_vals(v[0, g]), np_vals(dout[0])
+    rows = np.array([0, 3, 4, 4095, 4096, 4160, 20000, n - 1])
+    h = G * g + 1
+    ref = oracle.attn_bwd_rows(qi[0, h].cpu().numpy(), qv[0, h].cpu().numpy(), oki, okv, vn,
+                               dn[h], d, w_.scale, True, rows, window=win, n_global=ng)
+    check_grad(dq[0, h, torch.from_numpy(rows).to(DEV)], ref, tol, f"dq_val window head {h}")
+    cols = np.array([0, 3, 4, 100, 4095, 4096, 30000, n - 1])
+    hs = slice(G * g, G * g + G)
+    gk, gv = oracle.attn_bwd_cols(qi[0, hs].cpu().numpy(), qv[0, hs].cpu().numpy(), oki, okv, vn,
+                                  dn[hs], d, w_.scale, True, cols, window=win, n_global=ng)
+    sel = torch.from_numpy(cols).to(DEV)
+    check_grad(dk[0, g, sel], gk, tol, f"dk_val window KV head {g}")
+    check_grad(dv[0, g, sel], gv, tol, f"dv window KV head {g}")
