@@ -126,6 +126,21 @@ __device__ __forceinline__ void wait_vm_n() {
 // A-operand slice of a transposed array: row `row` (a coordinate / dimension),
 // columns kbase + 0..3 and kbase + 8..11 (the key / query order of the MFMA
 // output layout).
+// Workgroup (x, y) of a grid (nx, nbh) -> (block, bh): workgroups go
+// round-robin over the 8 XCDs, each with its own L2; with nbh a multiple of 8,
+// XCD c runs the (batch, KV head) pairs congruent to c, so one L2 serves every
+// workgroup of a head.
+__device__ __forceinline__ void xcd_map(int nx, int& x, int& bh) {
+  x = (int)blockIdx.x;
+  bh = (int)blockIdx.y;
+  if (gridDim.y % 8 == 0) {
+    const int id = x + bh * nx;
+    const int j = id >> 3;
+    x = j % nx;
+    bh = (id & 7) + 8 * (j / nx);
+  }
+}
+
 __device__ __forceinline__ bf16x8 tr_load(const uint16_t* tr, int row, int kbase) {
   const uint16_t* p = tr + row * kTP + kbase;
   const uint2 v0 = *(const uint2*)p;
@@ -260,8 +275,10 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = p.n;
-  const int qb = p.nqb - 1 - (int)blockIdx.x;  // longest causal blocks first
-  const int bh = blockIdx.y, b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+  int xb, bh;
+  xcd_map(p.nqb, xb, bh);
+  const int qb = p.nqb - 1 - xb;  // longest causal blocks first
+  const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
   const int i0 = qb * p.BR;
   // wave: 32 consecutive positions of one query head (BR is a multiple of 32)
   const int hq = hkv * p.G + (wave * kT) / p.BR;
@@ -418,8 +435,10 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = p.n;
-  const int bh = blockIdx.y, b = bh / p.Hkv, hkv = bh - b * p.Hkv;
-  const int j0b = (int)blockIdx.x * (kNW * kT);  // most key tiles first: smallest j0 first
+  int xb, bh;
+  xcd_map((int)gridDim.x, xb, bh);
+  const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+  const int j0b = xb * (kNW * kT);  // most key tiles first: smallest j0 first
   const int jw0 = j0b + wave * kT;
   const int my_j = jw0 + l32;
   const bool wave_ok = jw0 < n;

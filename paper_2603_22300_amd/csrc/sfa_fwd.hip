@@ -729,7 +729,18 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
 template <int D, bool VBF16, int NW, int KM>
 __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   // longest causal blocks first
-  fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - (int)blockIdx.x, (int)blockIdx.y);
+  // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+  // L2): with the (batch, KV head) count a multiple of 8, XCD x runs the KV
+  // heads congruent to x, so one L2 serves all query blocks of a head, which
+  // sweep its key tiles together.  Longest causal blocks first either way.
+  const int nbh = (int)gridDim.y;
+  if (nbh % 8 == 0) {
+    const int id = (int)blockIdx.x + (int)blockIdx.y * p.nqb;
+    const int xcd = id & 7, j = id >> 3;
+    fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - j % p.nqb, xcd + 8 * (j / p.nqb));
+  } else {
+    fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - (int)blockIdx.x, (int)blockIdx.y);
+  }
 }
 
 // Whether workgroup t = bh * nqb + qb was handed back (its first output
