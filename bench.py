@@ -353,7 +353,7 @@ def _blas_threads():
         return 1
 
 
-def cpu_baseline_fwd(w, q, k, v, budget_rows=256, seed=0):
+def cpu_baseline_fwd(w, q, k, v, budget_rows=1536, seed=0):
     """The oracle on a bounded sample of the same workload, extrapolated to
     the whole step: Top-k of every key row (timed in full), Top-k of a sample
     of query rows (scaled by the row count), and the attention of `budget_rows`
