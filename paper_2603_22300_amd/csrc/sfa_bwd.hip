@@ -86,6 +86,19 @@ __device__ __forceinline__ void split2(float x, uint16_t& h, uint16_t& l) {
   l = (uint16_t)f32_to_bf16_rne(x - bf16_bits_to_f32(hb));
 }
 
+// The same split for two values at once, packed: word 0 holds the high
+// pieces of (x0, x1), word 1 the low pieces; the rounding to nearest-even is
+// the hardware conversion (v_cvt_pk_bf16_f32), identical to split2 for
+// finite values.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void split2_pair(float x0, float x1, uint32_t& hw, uint32_t& lw) {
+  const f32x2 v = {x0, x1};
+  hw = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+  const f32x2 r = {x0 - __uint_as_float(hw << 16), x1 - __uint_as_float(hw & 0xffff0000u)};
+  lw = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, bf16x2));
+}
+
 __device__ __forceinline__ float load_f(const void* p, int64_t i, int bf16) {
   return bf16 ? bf16_bits_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
 }
@@ -365,18 +378,39 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
         mfma3<!VEX, !OEX>(dp, v, gg);  // dP^T = V dO^T
       }
       // dS^T = P^T o (dP^T - D); lane = query my_i, register r = key j0 + 8(r/4) + 4hh + r%4
-      bf16x8 dsb[2][2];  // [kk][piece]
+      // every (row, key) pair of the tile allowed: no element mask (rows past
+      // n have L2 = +inf, hence P = 0, either way)
+      const bool wcut = win && j0 + kT > p.n_global && wave_i_max >= p.n_global &&
+                        (pos0 < p.n_global || wave_i_max - j0 >= p.window ||
+                         j0 + kT - 1 - pos0 >= p.window);
+      const bool full = j0 + kT <= n && (!p.causal || j0 + kT - 1 <= pos0) && !wcut;
+      u32x4 dsw[2][2];  // [kk][piece], as bf16 pairs
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = j0 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
-                        (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
-        const float pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -L2)) : 0.f;
-        uint16_t h, l;
-        split2(pr * (dp[r] - Dq), h, l);
-        dsb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h);
-        dsb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l);
+      for (int r = 0; r < 16; r += 2) {
+        float ds[2];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          const int j = j0 + 8 * ((r + x) >> 2) + 4 * hh + ((r + x) & 3);
+          float pr;
+          if (full) {
+            pr = __builtin_amdgcn_exp2f(fmaf(s[r + x], p.c, -L2));
+          } else {
+            const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
+                            (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
+            pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r + x], p.c, -L2)) : 0.f;
+          }
+          ds[x] = pr * (dp[r + x] - Dq);
+        }
+        uint32_t hw, lw;
+        split2_pair(ds[0], ds[1], hw, lw);
+        dsw[r >> 3][0][(r & 7) >> 1] = hw;
+        dsw[r >> 3][1][(r & 7) >> 1] = lw;
       }
+      bf16x8 dsb[2][2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int pc = 0; pc < 2; ++pc) dsb[kk][pc] = __builtin_bit_cast(bf16x8, dsw[kk][pc]);
       // dQ~^T += K~^T dS^T   (coordinates x queries)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
@@ -541,7 +575,13 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
         }
       }
       // lane = key my_j; register r = query row q0 + 8(r/4) + 4hh + r%4
-      bf16x8 xb[2][2];  // [kk][piece]: P (dV) or dS (dK)
+      // every (query, key) pair of the tile allowed: no element mask (queries
+      // past n have L2 = +inf, hence P = 0, either way)
+      const bool wcut = win && q0 + kT > p.n_global && jw0 + kT > p.n_global &&
+                        (q0 < p.n_global || jw0 < p.n_global || q0 + kT - 1 - jw0 >= p.window ||
+                         jw0 + kT - 1 - q0 >= p.window);
+      const bool full = jw0 + kT <= n && (!p.causal || q0 >= jw0 + kT - 1) && !wcut;
+      u32x4 xw[2][2];  // [kk][piece]: P (dV) or dS (dK), as bf16 pairs
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
@@ -551,20 +591,35 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
           const float4 d4 = *(const float4*)(dd + 8 * g4 + 4 * hh);
           dv4[0] = d4.x; dv4[1] = d4.y; dv4[2] = d4.z; dv4[3] = d4.w;
         }
+        float val[4];
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
           const int r = 4 * g4 + x;
           const int i = q0 + 8 * g4 + 4 * hh + x;
-          const bool ok = key_ok && (!p.causal || i >= my_j) &&
-                          (!win || abs(i - my_j) < p.window || i < p.n_global || my_j < p.n_global);
-          const float pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x])) : 0.f;
-          const float val = PART == kDV ? pr : pr * (dp[r] - dv4[x]);
-          uint16_t h, l;
-          split2(val, h, l);
-          xb[r >> 3][0][r & 7] = __builtin_bit_cast(__bf16, h);
-          xb[r >> 3][1][r & 7] = __builtin_bit_cast(__bf16, l);
+          float pr;
+          if (full) {
+            pr = __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x]));
+          } else {
+            const bool ok = key_ok && (!p.causal || i >= my_j) &&
+                            (!win || abs(i - my_j) < p.window || i < p.n_global || my_j < p.n_global);
+            pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x])) : 0.f;
+          }
+          val[x] = PART == kDV ? pr : pr * (dp[r] - dv4[x]);
+        }
+#pragma unroll
+        for (int x = 0; x < 4; x += 2) {
+          const int r = 4 * g4 + x;
+          uint32_t hw, lw;
+          split2_pair(val[x], val[x + 1], hw, lw);
+          xw[r >> 3][0][(r & 7) >> 1] = hw;
+          xw[r >> 3][1][(r & 7) >> 1] = lw;
         }
       }
+      bf16x8 xb[2][2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int pc = 0; pc < 2; ++pc) xb[kk][pc] = __builtin_bit_cast(bf16x8, xw[kk][pc]);
       // dV^T += dO^T P  or  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
       const uint16_t* tra = PART == kDV ? tro : trq;
 #pragma unroll
