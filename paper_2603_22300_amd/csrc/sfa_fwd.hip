@@ -8,14 +8,16 @@
 // clock), while the matrix cores take the densified product at 2.5 PFLOP/s;
 // so the codes are densified tile by tile into LDS and contracted there.
 //
-// Precision: each code value x is split into bfloat16 pieces x = x0 + x1 (+ x2),
+// Precision: each code value x (for queries: x = q * scale * log2(e), so the
+// scores come out as base-2 exponents) is split into bfloat16 pieces
+// x = x0 + x1 (+ x2),
 // x0 = bf16(x), x1 = bf16(x - x0), x2 = bf16(x - x0 - x1).  Products of
 // bf16 pieces are exact in float32 and accumulate in float32.  With bf16 V the
 // score keeps the terms q0k0 + q0k1 + q1k0 (relative error ~2^-16 of
 // sum|q_u k_u|); with float32 V it keeps every term of order <= 2
 // (q0k0 + q0k1 + q1k0 + q0k2 + q1k1 + q2k0, ~2^-24).
 // P.V with bf16 V: V is staged into LDS as float16 (exact for normal values up
-// to 65504) and P enters as float16 (P <= 2^8, relative rounding 2^-11), one
+// to 65504) and P enters as float16 (P < 2^15, relative rounding 2^-11), one
 // MFMA per block.  A tile holding a V value outside the float16 range is
 // flagged while staged and runs with V read as bf16 from global memory and
 // P = Ph + Pl in bf16.  With float32 V, P.V runs on the float32 MFMA.
@@ -127,9 +129,13 @@ __device__ __forceinline__ uint32_t f16_pair(uint32_t a, uint32_t b) {
 }
 
 // The running row maximum is raised only when a tile's maximum exceeds it by
-// more than this (log2 units), so probabilities stay below 2^kLazyMax and the
-// accumulators are rescaled rarely; O and LSE use the same stale maximum.
+// more than this (log2 units), so the accumulators are rescaled rarely; O and
+// LSE use the same stale maximum.
 constexpr float kLazyMax = 8.f;
+// An interior tile whose exponents are bounded (Cauchy-Schwarz on the code
+// norms) by m_run + kBoundMax skips the maxima: its probabilities stay below
+// 2^15, inside the float16 range of the P.V operand.
+constexpr float kBoundMax = 15.f;
 
 // Bits written into the first output element of a workgroup's rows when the
 // float16 path meets a V tile outside the float16 range: a NaN payload that
@@ -214,9 +220,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   }
 
   // ---------------- query operand: NP bf16 pieces of the densified rows ----
-  // A negative scale is carried by the query values (s * c = (-s) * |c|), so
-  // the softmax below only ever needs row maxima of the raw scores.
-  const float qsign = p.scale_log2 < 0.f ? -1.f : 1.f;
+  // The query values carry scale * log2(e): the score tiles come out as the
+  // base-2 exponents t = s * scale * log2(e) of the softmax, sign included.
   bf16x8 qB[NP][NKB];
 #pragma unroll
   for (int pc = 0; pc < NP; ++pc) {
@@ -230,7 +235,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
         const int hq = hkv * p.G + r / p.BR;
         const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
         const int f = load_idx(p.q_idx, gi, p.ifmt, dmask);
-        Qs[r * QP + f] = bf16_piece(qsign * load_val(p.q_val, gi, p.vfmt), pc);
+        Qs[r * QP + f] = bf16_piece(p.scale_log2 * load_val(p.q_val, gi, p.vfmt), pc);
       }
     }
     __syncthreads();
@@ -239,7 +244,35 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     __syncthreads();
   }
 
+  // Cauchy-Schwarz bound on this row's exponents: |t_ij| <= qn * |k_j| (the
+  // overlap sum runs over a subset of the coordinates), with a margin for the
+  // bf16 pieces and float32 rounding.
+  float qn = 0.f;
+  if constexpr (NP == 2) {
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = (float)qB[0][kb][e] + (float)qB[1][kb][e];
+        qn = fmaf(x, x, qn);
+      }
+    qn = sqrtf(pair_sum(qn)) * (1.f + 1.f / 256.f);
+  }
+
   float m_run = -INFINITY, l_run = 0.f;
+  // Interior tiles start their score accumulators at -m_run (the C operand of
+  // the first MFMA), so they come out as t - m_run, the argument of exp2.
+  constexpr bool kFast = NS == 2 && VBF16 && !SAFE;
+  floatx16 negm, zero16;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) zero16[r] = 0.f;
+  auto set_m = [&](float m) {
+    m_run = m;
+    if constexpr (kFast) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) negm[r] = -m;
+    }
+  };
   floatx16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
@@ -249,7 +282,6 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   const int wave_i_max = i0 + (wave * 32 + 31) % p.BR;  // largest position in this wave
   const int wave_i_min = p.BR >= 32 ? i0 + (wave * 32) % p.BR : i0;
   const int64_t kv_base = ((int64_t)b * p.Hkv + hkv) * n;
-  const float c = fabsf(p.scale_log2);
 
   // ---- global -> registers for one tile ----
   // Per-lane offsets are loop-invariant; loads are unconditional (indices
@@ -405,13 +437,18 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // completion is awaited with vmcnt before the barrier that publishes it.
   auto dma_stage = [&](int stage, int jt) {
     static_assert(SB % 1024 == 0, "stage images are whole 1 KB blocks");
-    const unsigned char* src = p.ws_tiles + ((int64_t)bh * p.vtiles + jt) * SB + lane * 16;
+    constexpr int NB = SB / 1024, NJ = (NB + NW - 1) / NW;
+    // wave-uniform base + 32-bit lane offset: the scalar-base address form
+    const unsigned char* src = p.ws_tiles + ((int64_t)bh * p.vtiles + jt) * SB;
     unsigned char* dst = smem + stage * SB;
 #pragma unroll
-    for (int i = wave; i < SB / 1024; i += NW)
-      __builtin_amdgcn_global_load_lds(src + i * 1024,
-                                       (__attribute__((address_space(3))) void*)(dst + i * 1024),
-                                       16, 0, 0);
+    for (int j = 0; j < NJ; ++j) {
+      const int i = wave + j * NW;  // 1 KB block of the image
+      if (j + 1 < NJ || i < NB)
+        __builtin_amdgcn_global_load_lds(src + (uint32_t)(i * 1024 + lane * 16),
+                                         (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                         16, 0, 0);
+    }
   };
   auto wait_dma = [&]() {
     if constexpr (kDMA) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
@@ -430,9 +467,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // ---- building blocks of a key tile -------------------------------------
   // S^T for keys 32 s .. 32 s + 31 of the tile, this wave's 32 rows: lane
   // (row rho) register r holds key 32 s + 8 (r / 4) + 4 hh + (r % 4).
-  auto score_sub = [&](floatx16& o, int s, const uint16_t* Kd) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[r] = 0.f;
+  auto score_sub = [&](floatx16& o, int s, const uint16_t* Kd, const floatx16& init) {
+    o = init;
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
       bf16x8 ka[NP];
@@ -450,23 +486,14 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
     }
   };
-  // largest base-2 exponent s * c of a sub-tile (no mask), combined over the
-  // two lanes of the row
+  // largest value of a sub-tile (no mask), combined over the two lanes of the row
   auto sub_max = [&](const floatx16& o) {
     float hi = o[0];
 #pragma unroll
     for (int r = 1; r < 16; ++r) hi = fmaxf(hi, o[r]);
-    const float mt = hi * c;  // c >= 0
-    return fmaxf(mt, swap_halves(mt));
+    return pair_max(hi);
   };
-  // probabilities 2^(s c - m) in place; returns their (lane-partial) sum
-  auto sub_exp = [&](floatx16& o) {
-    float rs = 0.f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) { o[r] = fast_exp2(fmaf(o[r], c, -m_run)); rs += o[r]; }
-    return rs;
-  };
-  // P in float16 for the fp16 V tile (values <= 2^kLazyMax, 11-bit mantissa)
+  // P in float16 for the fp16 V tile (values < 2^kBoundMax, 11-bit mantissa)
   auto to_f16 = [&](const floatx16& pr, f16x8 (&pf)[2]) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
@@ -536,23 +563,25 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // score tile live).
   auto generic_sub = [&](int j0, int s, const uint16_t* Kd, const unsigned char* vt) {
     floatx16 sc;
-    score_sub(sc, s, Kd);
-    // base-2 exponents t = s * c; masked keys get t = -inf
+    score_sub(sc, s, Kd, zero16);
+    // base-2 exponents t; masked keys get t = -inf
     float mt = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
       const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
                       (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
-      sc[r] = ok ? sc[r] * c : -INFINITY;
+      sc[r] = ok ? sc[r] : -INFINITY;
       mt = fmaxf(mt, sc[r]);
     }
-    mt = fmaxf(mt, swap_halves(mt));
+    mt = pair_max(mt);
     const bool upd = mt > m_run + kLazyMax;
     const float m_new = upd ? mt : m_run;
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    if (__builtin_amdgcn_ballot_w64(upd)) rescale(upd ? fast_exp2(m_run - m_use) : 1.f);
-    m_run = m_new;
+    if (__builtin_amdgcn_ballot_w64(upd)) {
+      rescale(upd ? fast_exp2(m_run - m_use) : 1.f);
+      set_m(m_new);
+    }
     float rs = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) { sc[r] = fast_exp2(sc[r] - m_use); rs += sc[r]; }
@@ -599,22 +628,29 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   };
   // probability of value r (exp of the lane's score), as float16 into pf
   auto exp_h = [&](const floatx16& o, int r, float& rs, f16x8 (&pf)[2]) {
-    const float pr = fast_exp2(fmaf(o[r], c, -m_run));
+    const float pr = fast_exp2(o[r]);
     rs += pr;
     pf[r >> 3][r & 7] = (_Float16)pr;
   };
 
-  auto fast_tile = [&](const uint16_t* Kd, const uint16_t* Vt, int jt_next, int stage_next) {
+  // bounded: no exponent of the tile can exceed m_run + kBoundMax (checked
+  // from the norms), so the maxima are not needed
+  // (The empty volatile asm keeps the maxima inside their branch: without it
+  // the compiler computes them unconditionally.)
+  auto fast_tile = [&](const uint16_t* Kd, const uint16_t* Vt, int jt_next, int stage_next,
+                       bool bounded) {
     // ---- A ----
     floatx16 s0, s1;
-    score_sub(s0, 0, Kd);
-    if (__builtin_amdgcn_ballot_w64(sub_max(s0) > m_run + kLazyMax)) return false;
+    score_sub(s0, 0, Kd, negm);
+    if (!bounded) {
+      asm volatile("");
+      if (__builtin_amdgcn_ballot_w64(sub_max(s0) > kLazyMax)) return false;
+    }
     // ---- B: scores(1) || softmax(0) ----
     f16x8 p0[2];
     float rs = 0.f;
     {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s1[r] = 0.f;
+      s1 = negm;
       bf16x8 ka[2][NP];
       ka_load(ka[0], 1, 0, Kd);
 #pragma unroll
@@ -627,14 +663,20 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       }
     }
     l_run += rs;
-    const float mt1 = sub_max(s1);
-    const bool up1 = mt1 > m_run + kLazyMax;
-    if (__builtin_amdgcn_ballot_w64(up1)) {
-      const float m_new = up1 ? mt1 : m_run;
-      rescale(fast_exp2(m_run - m_new));  // also rescales sub-tile 0's share of l
-      m_run = m_new;
+    if (!bounded) {
+      asm volatile("");
+      const float mt1 = sub_max(s1);  // largest t - m_run of sub-tile 1
+      const bool up1 = mt1 > kLazyMax;
+      if (__builtin_amdgcn_ballot_w64(up1)) {
+        const float dm = up1 ? mt1 : 0.f;
+        rescale(fast_exp2(-dm));  // also rescales sub-tile 0's share of l
+        set_m(m_run + dm);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) p0[r >> 3][r & 7] = (_Float16)fast_exp2(fmaf(s0[r], c, -m_run));
+        for (int r = 0; r < 16; ++r) {
+          p0[r >> 3][r & 7] = (_Float16)fast_exp2(s0[r] - dm);
+          s1[r] -= dm;
+        }
+      }
     }
     // ---- C: P.V(0) || softmax(1) ----
     f16x8 p1[2];
@@ -690,7 +732,13 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
                            __builtin_amdgcn_ballot_w64(!row_ok || m_run == -INFINITY) != 0;
     bool done = false;
     if constexpr (NS == 2 && VBF16 && !SAFE) {
-      if (act0 && act1 && !need_mask) done = fast_tile(Kd, (const uint16_t*)vt, jt_next, stage ^ 1);
+      if (act0 && act1 && !need_mask) {
+        // largest key norm of the tile, kept by the prepared image in the
+        // padding of key row 0
+        const float kn = *(const float*)(Kd + 2 * D);
+        const bool bounded = !__builtin_amdgcn_ballot_w64(!(qn * kn <= m_run + kBoundMax));
+        done = fast_tile(Kd, (const uint16_t*)vt, jt_next, stage ^ 1, bounded);
+      }
     }
     if (!done) {
       if (act0) generic_sub(j0, 0, Kd, vt);
@@ -700,7 +748,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     wait_dma();
     __syncthreads();
   }
-  l_run += swap_halves(l_run);  // lane-partial row sums -> row sums
+  l_run = pair_sum(l_run);  // lane-partial row sums -> row sums
 
   // ---------------- epilogue: O = acc / l, LSE = ln(l) + m ln 2 -------------
   if (row_ok) {
@@ -734,13 +782,14 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   // heads congruent to x, so one L2 serves all query blocks of a head, which
   // sweep its key tiles together.  Longest causal blocks first either way.
   const int nbh = (int)gridDim.y;
+  int qb = (int)blockIdx.x, bh = (int)blockIdx.y;
   if (nbh % 8 == 0) {
-    const int id = (int)blockIdx.x + (int)blockIdx.y * p.nqb;
+    const int id = qb + bh * p.nqb;
     const int xcd = id & 7, j = id >> 3;
-    fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - j % p.nqb, xcd + 8 * (j / p.nqb));
-  } else {
-    fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - (int)blockIdx.x, (int)blockIdx.y);
+    qb = j % p.nqb;
+    bh = xcd + 8 * (j / p.nqb);
   }
+  fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - qb, bh);
 }
 
 // Whether workgroup t = bh * nqb + qb was handed back (its first output
@@ -779,8 +828,10 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
 //   - the dense key tile [key][piece][coordinate] (pitch KR) with the codes'
 //     values as bf16 pieces x0 = bf16(x), x1 = bf16(x - x0) at their
 //     coordinates and zeros elsewhere;
-//   - V^T as float16, [dimension][key] (pitch kBC + 4).
-// Keys past n and all padding are zero.  flag t is set when a V value of the
+//   - V^T as float16, [dimension][key] (pitch kBC + 4);
+//   - in the padding of key row 0, the largest Euclidean norm of the tile's
+//     key codes (times 1 + 2^-8), which bounds the tile's scores.
+// Keys past n and the rest of the padding are zero.  flag t is set when a V value of the
 // tile lies outside the float16 range (|v| >= 65536, inf, NaN).  bf16 ->
 // float16 is exact for 2^-14 <= |v| <= 65504; below that it rounds to the
 // float16 subnormal grid (absolute error <= 2^-25).
@@ -804,6 +855,23 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
     const float x = load_val(k_val, c0 + e, vfmt);
     T[j * KR + f] = bf16_piece(x, 0);
     T[j * KR + D + f] = bf16_piece(x, 1);
+  }
+  // largest Euclidean norm of the tile's key codes (padding of key row 0)
+  __shared__ float kn2[kBC];
+  if (tid < kBC) {
+    float acc = 0.f;
+    if (j0 + tid < n)
+      for (int e = 0; e < k; ++e) {
+        const float x = load_val(k_val, c0 + (int64_t)tid * k + e, vfmt);
+        acc = fmaf(x, x, acc);
+      }
+    kn2[tid] = acc;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float mx = 0.f;
+    for (int j = 0; j < kBC; ++j) mx = fmaxf(mx, kn2[j]);
+    *(float*)(T + 2 * D) = sqrtf(mx) * (1.f + 1.f / 256.f);
   }
   const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
   bool over = false;

@@ -53,11 +53,11 @@ def check_o(o_gpu: torch.Tensor, o_ref: np.ndarray, tol: float, what: str):
     return err
 
 
-def check_lse(lse_gpu: torch.Tensor, lse_ref: np.ndarray, what: str):
+def check_lse(lse_gpu: torch.Tensor, lse_ref: np.ndarray, what: str, tol: float = TOL_LSE):
     got = np_f64(lse_gpu)
     err = np.abs(got - lse_ref).max() if got.size else 0.0
-    print(f"[parity] {what}: max|LSE-LSE_oracle| = {err:.3e} (tol {TOL_LSE:.0e})", flush=True)
-    assert err <= TOL_LSE, f"{what}: max |LSE - LSE_oracle| = {err:.3e} > {TOL_LSE:.1e}"
+    print(f"[parity] {what}: max|LSE-LSE_oracle| = {err:.3e} (tol {tol:.0e})", flush=True)
+    assert err <= tol, f"{what}: max |LSE - LSE_oracle| = {err:.3e} > {tol:.1e}"
     return err
 
 

@@ -13,7 +13,8 @@ import torch
 import oracle
 import paper_2603_22300_amd as sfa
 import sfa_inputs as si
-from helpers import (TOL_O_BF16V, TOL_O_F32, check_lse, check_o, np_vals, sample_rows)
+from helpers import (TOL_LSE, TOL_O_BF16V, TOL_O_F32, check_lse, check_o, np_vals,
+                     sample_rows)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -24,7 +25,7 @@ def _gpu_codes(x, k, idx_dtype=torch.int32, val_dtype=torch.float32):
 
 
 def _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, idx_dtype=torch.int32,
-              val_dtype=torch.float32, zipf_s=0.0, fwd=None):
+              val_dtype=torch.float32, zipf_s=0.0, fwd=None, scale=None, lse_tol=TOL_LSE):
     fwd = fwd or sfa.sfa_attn_fwd
     q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed,
                             v_dtype=torch.bfloat16 if v_bf16 else torch.float32, device=DEV)
@@ -40,7 +41,7 @@ def _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, idx_dtype=torch.int32,
                 kk[b, h] = si.dense_from_codes(i_, v_, d)
     qi, qv = _gpu_codes(q, k, idx_dtype, val_dtype)
     ki, kv = _gpu_codes(kk, k, idx_dtype, val_dtype)
-    scale = 1.0 / math.sqrt(d)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
     o32, lse = fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=torch.float32)
     ob16 = None
     if v_bf16:
@@ -58,7 +59,7 @@ def _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, idx_dtype=torch.int32,
     O, L = oracle.attn_fwd(oqi, oqv, oki, okv, vn, d, scale, causal)
     tol = TOL_O_BF16V if v_bf16 else TOL_O_F32
     eo = check_o(o32, O, tol, "O (float32 output)")
-    el = check_lse(lse, L, "LSE")
+    el = check_lse(lse, L, "LSE", lse_tol)
     if ob16 is not None:
         check_o(ob16, O, tol, "O (bf16 output)")
     return eo, el
@@ -104,6 +105,20 @@ def test_shapes(B, Hq, Hkv, n, d, k, causal, v_bf16):
 def test_index_variant(B, Hq, Hkv, n, d, k, causal, v_bf16):
     _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=B * 1000 + Hq * 100 + n + 7,
               fwd=sfa.sfa_attn_fwd_index)
+
+
+@pytest.mark.parametrize("scale,v_bf16", [(1.0, True), (-0.5, True), (0.0, True), (1.0, False),
+                                           (-1.0 / 128, True)])
+def test_scales(scale, v_bf16):
+    """Scales other than 1/sqrt(d), of either sign and zero.  At |scale| = 1
+    the exponents reach ~50 (base 2), far above the first tiles' maxima: the
+    lazily raised maximum and its rescaling run on most rows.  The score
+    error of the split products is proportional to |scale| * sum |q_u k_u|,
+    so the LSE bound, 1e-4 at scale 1/sqrt(d), is taken times
+    max(1, |scale| sqrt(d))."""
+    d = 128
+    _run_case(1, 4, 1, 1100, d, 16, True, v_bf16, seed=31 + int(8 * abs(scale)), scale=scale,
+              lse_tol=TOL_LSE * max(1.0, abs(scale) * math.sqrt(d)))
 
 
 def test_int16_indices_bf16_values():
