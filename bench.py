@@ -146,6 +146,8 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     ws = torch.empty(sfa.sfa_attn_fwd_workspace(B, Hkv, n, d, v.dtype), dtype=torch.uint8, device=DEV)
 
     def step(ev=None):
+        if ev is not None:
+            ev[2].record()
         sfa.sfa_topk_encode(q, kk, idx=qi, val=qv)
         sfa.sfa_topk_encode(k, kk, idx=ki, val=kv)
         if ev is not None:
@@ -158,8 +160,7 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(steps)]
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(steps)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -171,8 +172,9 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_step = t0.elapsed_time(t1) / steps
-    fwd_ms = [a.elapsed_time(b_) for a, b_ in evs]
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
     fwd_avg = float(np.mean(fwd_ms))
+    enc_avg = float(np.mean([e[2].elapsed_time(e[0]) for e in evs]))
 
     pairs = B * Hq * _allowed_pairs(n, w.causal, window, n_global)
     pv_flops = 2.0 * d * pairs          # P.V: 2 d flops per allowed pair
@@ -217,6 +219,14 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
             "overlap_products_E": E,
             "algorithmic_hbm_bytes_per_launch": _fwd_bytes(w),
             "hbm_frac": _fwd_bytes(w) / (fwd_avg * 1e-3) / PEAK_HBM,
+        },
+        # the two parts of the step: encoding Q and K, and the forward on
+        # codes already in HBM
+        "split": {
+            "encode_ms": enc_avg,
+            "encode_rows_per_s": B * (Hq + Hkv) * n / (enc_avg * 1e-3),
+            "fwd_ms": fwd_avg,
+            "fwd_tokens_per_s": tokens / (fwd_avg * 1e-3),
         },
         "wall_s_timed": wall,
     }

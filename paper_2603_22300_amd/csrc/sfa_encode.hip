@@ -11,10 +11,12 @@
 
 namespace sfa {
 
-template <int E>  // coordinates per lane: d <= 64 * E
+// E: coordinates per lane (d <= 64 * E); IF, VF: output formats (compile-time,
+// so the stores carry no format dispatch)
+template <int E, int IF, int VF>
 __global__ __launch_bounds__(256) void topk_encode_kernel(
     const float* __restrict__ x, int64_t rows, int d, int k,
-    void* __restrict__ idx_out, int ifmt, void* __restrict__ val_out, int vfmt) {
+    void* __restrict__ idx_out, void* __restrict__ val_out) {
   const int lane = threadIdx.x & 63;
   const int64_t nwaves = (int64_t)gridDim.x * 4;
   // the wave index is made visibly uniform so that the row walk and the
@@ -49,8 +51,27 @@ __global__ __launch_bounds__(256) void topk_encode_kernel(
 #pragma unroll
     for (int e = 0; e < E; ++e)
       if (sel[e] && slot[e] < k)  // exactly k are kept; the bound only hardens the store
-        store_code(idx_out, val_out, o0 + slot[e], lane + 64 * e, bits[e], ifmt, vfmt);
+        store_code(idx_out, val_out, o0 + slot[e], lane + 64 * e, bits[e], IF, VF);
   }
+}
+
+template <int E, int IF>
+static void launch_vf(dim3 grid, const float* x, int64_t rows, int d, int k, void* idx, void* val,
+                      int vfmt, hipStream_t stream) {
+  if (vfmt == kValBF16)
+    hipLaunchKernelGGL((topk_encode_kernel<E, IF, kValBF16>), grid, dim3(256), 0, stream, x, rows, d, k, idx, val);
+  else if (vfmt == kValF16)
+    hipLaunchKernelGGL((topk_encode_kernel<E, IF, kValF16>), grid, dim3(256), 0, stream, x, rows, d, k, idx, val);
+  else
+    hipLaunchKernelGGL((topk_encode_kernel<E, IF, kValF32>), grid, dim3(256), 0, stream, x, rows, d, k, idx, val);
+}
+
+template <int E>
+static void launch_if(dim3 grid, const float* x, int64_t rows, int d, int k, void* idx, int ifmt,
+                      void* val, int vfmt, hipStream_t stream) {
+  if (ifmt == kIdxI16) launch_vf<E, kIdxI16>(grid, x, rows, d, k, idx, val, vfmt, stream);
+  else if (ifmt == kIdxU8) launch_vf<E, kIdxU8>(grid, x, rows, d, k, idx, val, vfmt, stream);
+  else launch_vf<E, kIdxI32>(grid, x, rows, d, k, idx, val, vfmt, stream);
 }
 
 hipError_t launch_topk_encode(const float* x, int64_t rows, int d, int k, void* idx,
@@ -58,13 +79,10 @@ hipError_t launch_topk_encode(const float* x, int64_t rows, int d, int k, void* 
   // persistent waves: up to 32 per compute unit, 4 per workgroup
   const int64_t need = (rows + 3) / 4;
   const int64_t cap = 256 * 8;
-  dim3 grid((unsigned)(need < cap ? need : cap)), block(256);
-  if (d <= 64)
-    hipLaunchKernelGGL(topk_encode_kernel<1>, grid, block, 0, stream, x, rows, d, k, idx, ifmt, val, vfmt);
-  else if (d <= 128)
-    hipLaunchKernelGGL(topk_encode_kernel<2>, grid, block, 0, stream, x, rows, d, k, idx, ifmt, val, vfmt);
-  else
-    hipLaunchKernelGGL(topk_encode_kernel<4>, grid, block, 0, stream, x, rows, d, k, idx, ifmt, val, vfmt);
+  const dim3 grid((unsigned)(need < cap ? need : cap));
+  if (d <= 64) launch_if<1>(grid, x, rows, d, k, idx, ifmt, val, vfmt, stream);
+  else if (d <= 128) launch_if<2>(grid, x, rows, d, k, idx, ifmt, val, vfmt, stream);
+  else launch_if<4>(grid, x, rows, d, k, idx, ifmt, val, vfmt, stream);
   return hipGetLastError();
 }
 

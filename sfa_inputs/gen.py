@@ -119,6 +119,17 @@ def tie_rows(d: int, seed: int) -> np.ndarray:
     r = np.ldexp(np.ones(d, np.float32), rng.integers(-149, 127, size=d)).astype(np.float32)
     r[::3] *= -1; rows.append(r)
     r = np.full(d, np.finfo(np.float32).max, np.float32); r[1::2] *= -1; rows.append(r)
+    # magnitudes at and just below powers of two (4, 2, 1.99999988, 1,
+    # 0.99999994): the k-th largest lands on an exponent boundary
+    for _ in range(2):
+        levels = np.array([4.0, 2.0, np.float32(np.nextafter(np.float32(2), np.float32(0))),
+                           np.float32(np.nextafter(np.float32(1), np.float32(0)))], np.float32)
+        r = np.ones(d, np.float32)
+        r[: 4 * (d // 8)] = np.repeat(levels, d // 8)
+        r = r[rng.permutation(d)] * np.where(rng.integers(0, 2, size=d) == 1, -1, 1)
+        rows.append(r.astype(np.float32))
+    # one huge magnitude above ordinary ones
+    r = rng.standard_normal(d).astype(np.float32); r[rng.integers(0, d)] = 3e30; rows.append(r)
     # ascending and descending magnitude ramps
     rows.append(np.arange(d, dtype=np.float32))
     rows.append(-np.arange(d, 0, -1, dtype=np.float32))
