@@ -29,9 +29,14 @@ __device__ __forceinline__ int appended_count(const int32_t* n_new, int b, int T
 // loads in flight while the current one is selected and stored.  Everything
 // that depends only on the pair (its length, count, capacity) is read once;
 // a token's page and slot are a shift and a mask (power-of-two pages).
-template <int E>  // coordinates per lane: d <= 64 * E
+// E: coordinates per lane (d <= 64 * E).  COMMON: int16 / bf16 codes, bf16
+// values in and in the cache, as compile-time constants (the stores then
+// carry no format dispatch); else the formats are read from the arguments.
+template <int E, bool COMMON>
 __global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
   const int lane = threadIdx.x & 63;
+  const int ifmt = COMMON ? (int)kIdxI16 : a.ifmt, vfmt = COMMON ? (int)kValBF16 : a.vfmt;
+  const bool vin_bf16 = COMMON || a.vin_bf16, vc_bf16 = COMMON || a.vc_bf16;
   const int tw = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int tstride = gridDim.x * 4;
   const int64_t cap = a.table ? (int64_t)a.max_pages * a.page_size : a.page_size;
@@ -44,17 +49,21 @@ __global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
     if (tw >= tend) continue;  // uniform per wave
     const float* kbase = a.k_new + (int64_t)bh * a.T * a.d;
     const unsigned char* vbase =
-        (const unsigned char*)a.v_new + (int64_t)bh * a.T * a.d * (a.vin_bf16 ? 2 : 4);
+        (const unsigned char*)a.v_new + (int64_t)bh * a.T * a.d * (vin_bf16 ? 2 : 4);
 
-    // raw 32-bit words: key bits, and value bits (bf16 zero-extended or float)
+    // raw 32-bit words: key bits, and value bits (bf16 zero-extended or
+    // float); and the row's page, loaded with them so that the wait for it
+    // does not also wait for the next row's loads (loads retire in order)
     uint32_t nk[E], nv[E];
+    int npage = 0;
     auto load_row = [&](int t) {
+      if (a.table) npage = a.table[(int64_t)b * a.max_pages + ((L0 + t) >> a.log2P)];
       const int64_t o = (int64_t)t * a.d;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int c = min(lane + 64 * e, a.d - 1);
         nk[e] = __float_as_uint(kbase[o + c]);
-        nv[e] = a.vin_bf16 ? (uint32_t)((const uint16_t*)vbase)[o + c]
+        nv[e] = vin_bf16 ? (uint32_t)((const uint16_t*)vbase)[o + c]
                            : ((const uint32_t*)vbase)[o + c];
       }
     };
@@ -67,11 +76,12 @@ __global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
         vb[e] = nv[e];
         key[e] = topk_key(bits[e], lane + 64 * e < a.d);
       }
+      const int row_page = __builtin_amdgcn_readfirstlane(npage);
       if (t + tstride < tend) load_row(t + tstride);
       const int64_t pos = L0 + t;
       int64_t page = b, slot = pos;
       if (a.table) {
-        page = a.table[(int64_t)b * a.max_pages + (pos >> a.log2P)];
+        page = row_page;
         slot = pos & (a.page_size - 1);
         if (page < 0 || page >= a.num_pages) continue;  // uniform per wave
       }
@@ -84,19 +94,19 @@ __global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
 #pragma unroll
       for (int e = 0; e < E; ++e)
         if (sel[e] && sl[e] < a.k)
-          store_code(a.kc_idx, a.kc_val, crow * a.k + sl[e], lane + 64 * e, bits[e], a.ifmt,
-                     a.vfmt);
+          store_code(a.kc_idx, a.kc_val, crow * a.k + sl[e], lane + 64 * e, bits[e], ifmt,
+                     vfmt);
       // value row (bf16 cache from float32 values: round to nearest even)
       const int64_t vo = crow * a.d;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int c = lane + 64 * e;
         if (c < a.d) {
-          if (a.vc_bf16)
+          if (vc_bf16)
             ((uint16_t*)a.v_cache)[vo + c] =
-                a.vin_bf16 ? (uint16_t)vb[e] : (uint16_t)f32_to_bf16_rne(__uint_as_float(vb[e]));
+                vin_bf16 ? (uint16_t)vb[e] : (uint16_t)f32_to_bf16_rne(__uint_as_float(vb[e]));
           else
-            ((uint32_t*)a.v_cache)[vo + c] = a.vin_bf16 ? vb[e] << 16 : vb[e];
+            ((uint32_t*)a.v_cache)[vo + c] = vin_bf16 ? vb[e] << 16 : vb[e];
         }
       }
     }
@@ -123,12 +133,11 @@ hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
     const int gx_need = (a.T + 3) / 4;
     if (gx > gx_need) gx = gx_need;
     dim3 grid(gx, gy), block(256);
-    if (a.d <= 64)
-      hipLaunchKernelGGL(sfa_kv_append_kernel<1>, grid, block, 0, stream, a);
-    else if (a.d <= 128)
-      hipLaunchKernelGGL(sfa_kv_append_kernel<2>, grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL(sfa_kv_append_kernel<4>, grid, block, 0, stream, a);
+    const bool common = a.ifmt == kIdxI16 && a.vfmt == kValBF16 && a.vin_bf16 && a.vc_bf16;
+    auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, block, 0, stream, a); };
+    if (a.d <= 64) common ? go(sfa_kv_append_kernel<1, true>) : go(sfa_kv_append_kernel<1, false>);
+    else if (a.d <= 128) common ? go(sfa_kv_append_kernel<2, true>) : go(sfa_kv_append_kernel<2, false>);
+    else common ? go(sfa_kv_append_kernel<4, true>) : go(sfa_kv_append_kernel<4, false>);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
