@@ -111,7 +111,8 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * lse           [B, Hq, n] float32 natural-log LSE, or NULL to skip it.
  * ws, ws_bytes  caller-owned device workspace of at least
  *               sfa_attn_fwd_workspace(B, Hkv, n, d, v_t) bytes (0 for float32
- *               V, where ws may be NULL).  With bf16 V it receives, on the
+ *               V and for head dims other than 64 and 128, where ws may be
+ *               NULL).  With bf16 V it receives, on the
  *               stream, V converted once to float16 and laid out as the
  *               kernel's key tiles, and a range flag per tile.  Calls that
  *               overlap in time need separate workspaces.
@@ -126,9 +127,13 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * recomputed by a second kernel launched on the same stream, with bf16 V and
  * the probabilities split into two bfloat16 terms (~2^-17).  With float32 V
  * the P.V product is float32.
- * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0 with Hq / Hkv a power of two
- *         <= 128; d in {64, 128}; 1 <= k <= d; B * Hkv <= 65535;
- *         n * d <= 2^29 and n * k <= 2^29 (SFA_ENOTSUP otherwise);
+ * Other head dims (d <= 256 except 64 and 128) run on a float32 vector-unit
+ * kernel: overlap sums by code lookups, exact running maximum, float32
+ * probabilities and P.V; any group size, no workspace.
+ * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0; 1 <= k <= d <= 256;
+ *         B * Hkv <= 65535; n * d <= 2^29 and n * k <= 2^29;
+ *         d in {64, 128}: Hq / Hkv a power of two <= 128;
+ *         other d: B * Hq <= 65535 (SFA_ENOTSUP otherwise);
  *         window, n_global >= 0.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (workspace missing or too
  *         small), SFA_EHIP.
@@ -144,7 +149,8 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val,
 
 /*
  * Bytes of device workspace sfa_attn_fwd needs for these sizes: 0 for
- * float32 V (v_t == SFA_F32), and for an unsupported d or invalid sizes.
+ * float32 V (v_t == SFA_F32), for head dims other than 64 and 128 (no
+ * workspace), and for invalid sizes.
  */
 size_t sfa_attn_fwd_workspace(int B, int Hkv, int n, int d, int v_t);
 
@@ -158,8 +164,8 @@ size_t sfa_attn_fwd_workspace(int B, int Hkv, int n, int d, int v_t);
  * V the probabilities enter P.V as a single bfloat16 (relative rounding 2^-9
  * per weight).  Slower on this hardware; kept as the direct realisation of
  * the overlap formulation.
- * Limits: as sfa_attn_fwd, plus k <= 64, Hq / Hkv <= 128, and the per-tile
- * tables must fit LDS (SFA_ENOTSUP otherwise).
+ * Limits: as sfa_attn_fwd with d in {64, 128}, plus k <= 64, Hq / Hkv <= 128,
+ * and the per-tile tables must fit LDS (SFA_ENOTSUP otherwise).
  */
 sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
                               const void* k_idx, const void* k_val,
@@ -200,7 +206,8 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
  * into two bfloat16 pieces and three piece products kept (relative error
  * ~2^-16 of the sum of |terms|), float32 accumulation; P recomputed as
  * exp2(s log2(e) - LSE log2(e)) in float32.
- * Limits: as sfa_attn_fwd, plus Hq / Hkv a power of two <= 8.
+ * Limits: as sfa_attn_fwd with d in {64, 128}, plus Hq / Hkv a power of two
+ * <= 8.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC, SFA_EHIP.
  */
 sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val,

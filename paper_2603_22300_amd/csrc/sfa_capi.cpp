@@ -62,7 +62,7 @@ sfa_status check_fwd(const void* q_idx, const void* q_val, const void* k_idx, co
   if (Hq % Hkv != 0) return SFA_EINVAL;
   if (!is_idx(idx_t) || !is_cval(qk_val_t) || !is_val(v_t) || !is_val(o_t)) return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
-  if (d != 64 && d != 128) return SFA_ENOTSUP;
+  if (d > 256) return SFA_ENOTSUP;  // callers with matrix-core kernels only also require 64 or 128
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
   // per-head code and value offsets are 32-bit byte offsets in the kernels
   if ((long long)n * d > (1LL << 29) || (long long)n * k > (1LL << 29)) return SFA_ENOTSUP;
@@ -85,6 +85,17 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                             qk_val_t, v_t, o_t, o);
   if (st != SFA_OK) return st;
   if (window < 0 || n_global < 0) return SFA_EINVAL;
+  if (d != 64 && d != 128) {
+    // head dimensions without a matrix-core kernel: the float32 vector-unit
+    // forward (no workspace)
+    if (!sfa::fwd_generic_supported(d, k) || (long long)B * Hq > 65535) return SFA_ENOTSUP;
+    return from_hip(sfa::launch_attn_fwd_generic(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d,
+                                                 k, causal != 0, window,
+                                                 window > 0 ? n_global : 0, scale,
+                                                 ifmt_of(idx_t), vfmt_of(qk_val_t),
+                                                 v_t == SFA_BF16, o_t == SFA_BF16, o, lse,
+                                                 (hipStream_t)stream));
+  }
   if (!pow2_le(Hq / Hkv, sfa::fwd_max_group())) return SFA_ENOTSUP;
   const size_t need = sfa::fwd_workspace_bytes(B, Hkv, n, d, v_t == SFA_BF16);
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return SFA_ENOSPC;
@@ -111,6 +122,7 @@ sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
   if (st != SFA_OK) return st;
   if (!lse || !dout || !dq_val || !dk_val || !dv) return SFA_EINVAL;
   if (window < 0 || n_global < 0) return SFA_EINVAL;
+  if (d != 64 && d != 128) return SFA_ENOTSUP;
   if (!pow2_le(Hq / Hkv, sfa::bwd_max_group())) return SFA_ENOTSUP;
   if (ws == nullptr || ws_bytes < sfa::bwd_workspace_bytes(B, Hq, Hkv, n, d)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n,
@@ -127,6 +139,7 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val, const void* 
   sfa_status st = check_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k, scale, idx_t,
                             qk_val_t, v_t, o_t, o);
   if (st != SFA_OK) return st;
+  if (d != 64 && d != 128) return SFA_ENOTSUP;
   if (!pow2_le(Hq / Hkv, sfa::fwd_index_rows_per_block())) return SFA_ENOTSUP;
   if (k > sfa::fwd_index_max_k()) return SFA_ENOTSUP;
   if (sfa::fwd_index_lds_bytes(d, k, v_t == SFA_BF16) > kMaxLds) return SFA_ENOTSUP;

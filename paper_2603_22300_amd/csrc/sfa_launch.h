@@ -19,6 +19,15 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
 int fwd_max_group();
 size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16);
 
+// float32 vector-unit forward for head dimensions without a matrix-core
+// kernel (d <= 256); no workspace, any group size
+hipError_t launch_attn_fwd_generic(const void* q_idx, const void* q_val, const void* k_idx,
+                                   const void* k_val, const void* v, int B, int Hq, int Hkv,
+                                   int n, int d, int k, int causal, int window, int n_global,
+                                   float scale, int ifmt, int vfmt, int vbf16, int obf16, void* o,
+                                   float* lse, hipStream_t stream);
+bool fwd_generic_supported(int d, int k);
+
 hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
                            const void* k_val, const void* v, const void* o, const float* lse,
                            const void* dout, int B, int Hq, int Hkv, int n, int d, int k,

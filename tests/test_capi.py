@@ -69,7 +69,13 @@ def test_fwd_validation(L, fn):
     assert _fwd(L, fn, idx_t=2) == 1            # a value dtype as index dtype
     assert _fwd(L, fn, v_t=0) == 1
     assert _fwd(L, fn, scale=float("nan")) == 1
-    assert _fwd(L, fn, d=96, k=8) == 2           # no kernel for this head dim
+    assert _fwd(L, fn, d=300, k=8) == 2          # beyond the largest head dim, 256
+    if fn == "sfa_attn_fwd_index":
+        assert _fwd(L, fn, d=96, k=8) == 2       # the index variant: d in {64, 128}
+    else:
+        # other head dims take the float32 vector kernel, one query head per
+        # grid row: B * Hq is bounded by the grid
+        assert _fwd(L, fn, d=96, k=8, B=40000, Hq=2, Hkv=1) == 2
     assert _fwd(L, fn, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
     assert _fwd(L, fn, B=70000, Hkv=1, Hq=1) == 2  # grid limit
     assert _fwd(L, fn, n=(1 << 22) + 1, d=128, k=16) == 2  # 32-bit per-head offsets

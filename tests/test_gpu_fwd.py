@@ -107,6 +107,23 @@ def test_index_variant(B, Hq, Hkv, n, d, k, causal, v_bf16):
               fwd=sfa.sfa_attn_fwd_index)
 
 
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,v_bf16",
+    [
+        (1, 2, 1, 150, 32, 4, True, False),    # d = 32
+        (1, 3, 1, 97, 80, 8, True, True),      # d = 80, three query heads per KV head
+        (2, 2, 2, 70, 96, 12, False, False),   # d = 96, non-causal
+        (1, 2, 2, 65, 256, 16, True, True),    # d = 256, the largest
+        (1, 1, 1, 40, 200, 200, True, False),  # k = d = 200
+        (1, 2, 1, 35, 16, 1, True, True),      # d = 16, k = 1
+        (1, 6, 2, 300, 192, 24, True, True),   # d = 192, ten key tiles
+    ])
+def test_other_head_dims(B, Hq, Hkv, n, d, k, causal, v_bf16):
+    """Head dimensions other than 64 and 128 run on the float32 vector-unit
+    forward; any group size."""
+    _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=d * 10 + n)
+
+
 @pytest.mark.parametrize("scale,v_bf16", [(1.0, True), (-0.5, True), (0.0, True), (1.0, False),
                                            (-1.0 / 128, True)])
 def test_scales(scale, v_bf16):

@@ -27,6 +27,8 @@ DEV = "cuda"
     (1, 2, 1, 260, 128, 4, True, True, 1, 0),        # window 1: each query alone
     (1, 4, 4, 300, 64, 16, True, True, 1000, 0),     # window beyond n: plain causal
     (1, 4, 2, 1500, 128, 16, True, True, 257, 64),   # tile-aligned globals, odd window
+    (1, 3, 1, 400, 96, 8, True, True, 45, 5),        # head dim 96: float32 vector kernel
+    (1, 2, 2, 300, 48, 6, False, False, 33, 0),      # head dim 48, non-causal
 ])
 def test_fwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
     seed = n + w + g
