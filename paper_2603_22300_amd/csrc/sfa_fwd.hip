@@ -16,26 +16,28 @@
 // score keeps the terms q0k0 + q0k1 + q1k0 (relative error ~2^-16 of
 // sum|q_u k_u|); with float32 V it keeps every term of order <= 2
 // (q0k0 + q0k1 + q1k0 + q0k2 + q1k1 + q2k0, ~2^-24).
-// P.V with bf16 V: V is staged into LDS as float16 (exact for normal values up
-// to 65504) and P enters as float16 (P < 2^15, relative rounding 2^-11), one
-// MFMA per block.  A tile holding a V value outside the float16 range is
-// flagged while staged and runs with V read as bf16 from global memory and
-// P = Ph + Pl in bf16.  With float32 V, P.V runs on the float32 MFMA.
+// P.V with bf16 V: V is converted to float16 (exact for normal values up to
+// 65504) and P enters as float16 (P < 2^15, relative rounding 2^-11), one
+// MFMA per block.  A workgroup whose keys hold a V value outside the float16
+// range hands its rows to a rerun kernel that reads V as bf16 and splits P
+// into Ph + Pl in bf16.  With float32 V, P.V runs on the float32 MFMA.
 //
 // Workgroup = NW wavefronts = 32*NW query rows: the G query heads of one KV
 // head times BR = 32*NW/G positions, so all G heads share each key tile.
 // Per tile of 64 keys:
-//   [A] each wave zeroes its 64/NW rows of a dense LDS key tile
-//       Kd[key][piece][coordinate] and scatters those keys' codes (bf16
-//       pieces) into them; V is staged, transposed, beside it;
+//   [A] the tile's LDS image: the dense key tile Kd[key][piece][coordinate]
+//       (bf16 pieces of the codes, zeros elsewhere) and V^T beside it.  With
+//       bf16 V the image is prepared once per call by sfa_fwd_prep_kernel and
+//       copied global -> LDS by direct-to-LDS loads; otherwise (float32 V,
+//       the rerun) each wave zeroes and fills its 64/NW key rows itself;
 //   [B] per wavefront, two 32-key sub-tiles: S^T = K~ Q~^T on
 //       v_mfma_f32_32x32x16_bf16 (the query pieces live in registers for the
-//       whole kernel), leaving each lane with one query row and 16 keys;
-//       scale, causal mask and the online-softmax update (base 2) run on those
-//       registers; the bf16 probabilities are already in the B-operand layout
-//       of O^T += V^T P^T, the second MFMA.
-// The next tile is loaded into registers during the current one and written
-// to the other LDS stage, with one barrier per tile.
+//       whole kernel), leaving each lane with one query row and 16 keys; the
+//       causal mask and the online-softmax update (base 2) run on those
+//       registers; the probabilities are already in the B-operand layout of
+//       O^T += V^T P^T, the second MFMA.
+// The next tile's image is in flight during the current one, into the other
+// LDS stage, with one barrier per tile.
 // Keys whose support does not overlap a query keep score 0 and still enter
 // the softmax: the result is exactly softmax(Q~ K~^T * scale) V.
 #include "sfa_device.h"
