@@ -251,8 +251,11 @@ size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d);
  *                 sfa_attn_decode_workspace(B, Hq, Lmax, d) bytes; its
  *                 contents need no initialisation and are scratch after the
  *                 call.  Concurrent calls must use distinct workspaces.
+ * d in {64, 128} runs the tuned kernel (16-byte aligned cache arrays, Hq /
+ * Hkv a power of two); other d <= 256 run a float32 kernel with the same
+ * chunks and merge (any Hq / Hkv <= 8, no alignment needs).
  * Limits: B, Hq, Hkv, Lmax >= 1; Lmax <= 2^30; Hq % Hkv == 0; Hq / Hkv <= 8;
- *         d in {64, 128}; 1 <= k <= d; window, n_global >= 0.
+ *         B * Hkv <= 65535; 1 <= k <= d <= 256; window, n_global >= 0.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (ws_bytes too small), SFA_EHIP.
  */
 sfa_status sfa_attn_decode(const void* q_idx, const void* q_val,

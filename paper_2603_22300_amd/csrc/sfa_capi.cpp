@@ -170,10 +170,14 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
       !is_val(v_t) || !is_val(o_t))
     return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
-  if (d != 64 && d != 128) return SFA_ENOTSUP;
-  if (!pow2_le(Hq / Hkv, sfa::decode_max_group())) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
-  if (((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0) return SFA_EINVAL;
+  // head dims without the tuned kernel: the float32 decode (no alignment needs)
+  const bool generic = d != 64 && d != 128;
+  if (generic ? (d > 256 || Hq / Hkv > sfa::decode_generic_max_group())
+              : !pow2_le(Hq / Hkv, sfa::decode_max_group()))
+    return SFA_ENOTSUP;
+  if (!generic && ((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0)
+    return SFA_EINVAL;
   if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
   sfa::DecodeArgs a = {};
   a.q_idx = q_idx; a.q_val = q_val; a.kc_idx = kc_idx; a.kc_val = kc_val; a.v = v_cache;
@@ -184,7 +188,8 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
   a.kifmt = ifmt_of(kc_idx_t); a.kvfmt = vfmt_of(kc_val_t);
   a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;
   a.o = o; a.lse = lse; a.ws = ws;
-  return from_hip(sfa::launch_attn_decode(a, (hipStream_t)stream));
+  return from_hip(generic ? sfa::launch_attn_decode_generic(a, (hipStream_t)stream)
+                          : sfa::launch_attn_decode(a, (hipStream_t)stream));
 }
 
 sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* q_val,
@@ -208,11 +213,14 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
       !is_cval(kc_val_t) || !is_val(v_t) || !is_val(o_t))
     return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
-  if (d != 64 && d != 128) return SFA_ENOTSUP;
-  if (!pow2_le(Hq / Hkv, sfa::decode_max_group())) return SFA_ENOTSUP;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  const bool generic = d != 64 && d != 128;
+  if (generic ? (d > 256 || Hq / Hkv > sfa::decode_generic_max_group())
+              : !pow2_le(Hq / Hkv, sfa::decode_max_group()))
+    return SFA_ENOTSUP;
   const int Lmax = max_pages * page_size;
-  if (((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0) return SFA_EINVAL;
+  if (!generic && ((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0)
+    return SFA_EINVAL;
   if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
   int log2P = 0;
   while ((1 << log2P) < page_size) ++log2P;
@@ -227,7 +235,8 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
   a.kifmt = ifmt_of(kc_idx_t); a.kvfmt = vfmt_of(kc_val_t);
   a.vbf16 = v_t == SFA_BF16; a.obf16 = o_t == SFA_BF16;
   a.o = o; a.lse = lse; a.ws = ws;
-  return from_hip(sfa::launch_attn_decode(a, (hipStream_t)stream));
+  return from_hip(generic ? sfa::launch_attn_decode_generic(a, (hipStream_t)stream)
+                          : sfa::launch_attn_decode(a, (hipStream_t)stream));
 }
 
 sfa_status sfa_kv_append(const float* k_new, const void* v_new, const int32_t* n_new,

@@ -65,6 +65,10 @@ struct DecodeArgs {
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream);
 size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d);
 int decode_max_group();
+// float32 decode for head dimensions without the tuned kernel (d <= 256);
+// same workspace and partial layout, Hq / Hkv <= decode_generic_max_group()
+hipError_t launch_attn_decode_generic(const DecodeArgs& a, hipStream_t stream);
+int decode_generic_max_group();
 
 // KV-cache append: Top-k coding of new keys and copy of their values into a
 // contiguous (table == nullptr: [B, Hkv, P, ...]) or paged cache, then

@@ -133,7 +133,10 @@ def test_decode_validation_and_workspace(L):
     assert _dec(L, ws=None) == 1
     assert _dec(L, Hq=6, Hkv=4) == 1
     assert _dec(L, Hq=32, Hkv=2) == 2       # group of 16 heads: unsupported
-    assert _dec(L, d=80, k=8) == 2
+    assert _dec(L, d=300, k=8) == 2          # beyond the largest head dim, 256
+    # other head dims run the float32 decode: group size up to 8, any value
+    assert _dec(L, d=80, k=8, Hq=18, Hkv=2) == 2
+    assert _dec(L, d=80, k=8, ws_bytes=L.sfa_attn_decode_workspace(2, 8, 100, 80) - 1) == 4
     assert _dec(L, kc_idx_t=3) == 1
 
 
@@ -187,7 +190,8 @@ def test_decode_paged_validation(L):
     assert _paged(L, max_pages=1 << 25, page_size=64, **ok) == 1  # capacity beyond 2^30
     assert _paged(L, Hq=6, Hkv=4, **ok) == 1
     assert _paged(L, Hq=32, Hkv=2, **ok) == 2
-    assert _paged(L, d=96, k=8, **ok) == 2
+    assert _paged(L, d=300, k=8, **ok) == 2
+    assert _paged(L, d=96, k=8, Hq=18, Hkv=2, **ok) == 2   # float32 decode: group <= 8
     assert _paged(L, kc_val_t=1, **ok) == 1
     assert _paged(L, q=FAKE, q_idx=None, q_val=None, q_idx_t=7, o=None, **ok) == 1  # o missing
 

@@ -118,6 +118,8 @@ def _paged_copy(ci, cv, vc, P, rng, spare=3):
     (2, 4, 1, 3000, 128, 8, 1024, True, [3000, 0]),   # an empty sequence; page > wave range
     (1, 8, 4, 2500, 64, 32, 32, True, [2500]),
     (3, 2, 2, 777, 128, 1, 16, True, [5, 777, 64]),   # k = 1, generic code path
+    (2, 6, 2, 2300, 96, 12, 64, True, [2300, 0]),     # d = 96: float32 decode
+    (2, 2, 1, 500, 200, 8, 16, False, [500, 333]),    # d = 200, float32 V
 ])
 def test_paged_decode(B, Hq, Hkv, Lmax, d, k, P, v_bf16, seq):
     seed = Lmax + P

@@ -59,6 +59,20 @@ def test_shapes(B, Hq, Hkv, Lmax, d, k, v_bf16, seq):
     _case(B, Hq, Hkv, Lmax, d, k, v_bf16, seq, seed=Lmax + k)
 
 
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,Lmax,d,k,v_bf16,seq",
+    [
+        (2, 3, 1, 300, 80, 8, True, [300, 37]),          # three query heads per KV head
+        (2, 8, 1, 4500, 96, 12, False, [4500, 2049]),    # chunks, 8:1 groups, float32 V
+        (1, 2, 2, 100, 256, 16, True, None),             # d = 256
+        (2, 4, 2, 129, 32, 32, True, [129, 1]),          # k = d = 32
+        (1, 6, 2, 2100, 200, 10, True, [2100]),          # d = 200, group of 3
+    ])
+def test_other_head_dims(B, Hq, Hkv, Lmax, d, k, v_bf16, seq):
+    """Head dimensions other than 64 and 128 run the float32 decode."""
+    _case(B, Hq, Hkv, Lmax, d, k, v_bf16, seq, seed=d + Lmax)
+
+
 def test_float32_cache_values():
     _case(2, 4, 1, 700, 128, 16, True, [700, 333], seed=3, cache_bf16=False)
 

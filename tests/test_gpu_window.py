@@ -77,10 +77,13 @@ def test_fwd_window_qwen3_32k_sampled():
         check_lse(lse[0, h, sel], ref[1], f"qwen3_32k window head {h} LSE")
 
 
-@pytest.mark.parametrize("w,g,seq", [(700, 0, [5000, 2500, 700]), (512, 4, [5000, 4097, 3]),
-                                     (1, 0, [5000, 10, 1]), (3000, 2049, [5000, 2100, 4999])])
-def test_decode_window(w, g, seq):
-    B, Hq, Hkv, L, d, k, P = 3, 8, 2, 5000, 128, 16, 64
+@pytest.mark.parametrize("w,g,seq,d", [(700, 0, [5000, 2500, 700], 128),
+                                       (512, 4, [5000, 4097, 3], 128),
+                                       (1, 0, [5000, 10, 1], 128),
+                                       (3000, 2049, [5000, 2100, 4999], 128),
+                                       (600, 3, [5000, 2100, 7], 96)])  # float32 decode
+def test_decode_window(w, g, seq, d):
+    B, Hq, Hkv, L, k, P = 3, 8, 2, 5000, 16, 64
     seed = w + g
     kd = torch.empty((B, Hkv, L, d), device=DEV)
     vc = torch.empty((B, Hkv, L, d), device=DEV, dtype=torch.bfloat16)
