@@ -77,6 +77,36 @@ def test_fwd_window_qwen3_32k_sampled():
         check_lse(lse[0, h, sel], ref[1], f"qwen3_32k window head {h} LSE")
 
 
+def test_fwd_longest_sequence_window_sampled():
+    """The longest sequence the forward takes at d = 128: n = 2^22, so that
+    n * d = 2^29, the limit of the kernels' 32-bit per-head offsets.  A
+    4096-token window with 4 global tokens keeps the run short; every tile
+    image up to the last is read.  Sampled rows are checked against the
+    oracle's plain softmax attention over the keys the row may see, gathered
+    by hand (no mask): the global tokens and the window."""
+    n, d, k, w, g = 1 << 22, 128, 16, 4096, 4
+    q = si.normal((1, 1, n, d), 11, "q", device=DEV)
+    kk = si.normal((1, 1, n, d), 11, "k", device=DEV)
+    v = si.normal((1, 1, n, d), 11, "v", device=DEV).to(torch.bfloat16)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    del q, kk
+    scale = 1 / math.sqrt(d)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=scale,
+                              o_dtype=torch.float32, window=w, n_global=g)
+    torch.cuda.synchronize()
+    rows = [0, 1, 3, 4, w - 1, w, w + 63, 1 << 21, n - w, n - 65, n - 64, n - 2, n - 1]
+    for i in rows:
+        keys = sorted(set(range(min(g, i + 1))) | set(range(max(0, i - w + 1), i + 1)))
+        kx = torch.tensor(keys, device=DEV)
+        qd = oracle.densify(qi[0, 0, i:i + 1].cpu().numpy(), qv[0, 0, i:i + 1].cpu().numpy(), d)
+        kd = oracle.densify(ki[0, 0, kx].cpu().numpy(), kv[0, 0, kx].cpu().numpy(), d)
+        O, L = oracle.softmax_attention(qd, kd, oracle.widen(np_vals(v[0, 0, kx])), scale,
+                                        causal=False)
+        check_o(o[0, 0, i:i + 1], O, TOL_O_BF16V, f"n = 2^22 row {i} O")
+        check_lse(lse[0, 0, i:i + 1], L, f"n = 2^22 row {i} LSE")
+
+
 @pytest.mark.parametrize("w,g,seq,d", [(700, 0, [5000, 2500, 700], 128),
                                        (512, 4, [5000, 4097, 3], 128),
                                        (1, 0, [5000, 10, 1], 128),
