@@ -642,8 +642,13 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   auto fast_tile = [&](const uint16_t* Kd, const uint16_t* Vt, int jt_next, int stage_next,
                        bool bounded) {
     // ---- A ----
+    // The phases that are matrix-core work only (A and D) run at raised wave
+    // priority, so that the other wavefront of the SIMD, in its softmax,
+    // does not hold back their MFMA issue (measured: -3% per tile).
     floatx16 s0, s1;
+    __builtin_amdgcn_s_setprio(1);
     score_sub(s0, 0, Kd, negm);
+    __builtin_amdgcn_s_setprio(0);
     if (!bounded) {
       asm volatile("");
       if (__builtin_amdgcn_ballot_w64(sub_max(s0) > kLazyMax)) return false;
@@ -693,12 +698,14 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       for (int q = 0; q < 8; ++q) exp_h(s1, 8 * kk + q, rs, p1);
     }
     l_run += rs;
+    __builtin_amdgcn_s_setprio(1);
     // ---- D: P.V(1) || next tile's LDS writes ----
     va_load(va[1], 1, 1, Vt);
     pv_terms(va[0], p1[0]);
     write_tile_keys(stage_next, jt_next);
     pv_terms(va[1], p1[1]);
     write_tile_v(stage_next, jt_next);
+    __builtin_amdgcn_s_setprio(0);
     return true;
   };
 
