@@ -200,14 +200,18 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
  * dv            [B, Hkv, n, d] float32 out
  * ws, ws_bytes  caller-owned device workspace of at least
  *               sfa_attn_bwd_workspace(B, Hq, Hkv, n, d) bytes: tile images of
- *               the codes, V and dO written and read on the stream.  Calls
+ *               the codes, V and dO written and read on the stream (0 bytes
+ *               and ws unused for head dims other than 64 and 128).  Calls
  *               that overlap in time need separate workspaces.
  * Arithmetic: every product on the matrix cores with both operands split
  * into two bfloat16 pieces and three piece products kept (relative error
  * ~2^-16 of the sum of |terms|), float32 accumulation; P recomputed as
  * exp2(s log2(e) - LSE log2(e)) in float32.
- * Limits: as sfa_attn_fwd with d in {64, 128}, plus Hq / Hkv a power of two
- * <= 8.
+ * Other head dims (d <= 256 except 64 and 128) run a float32 vector-unit
+ * backward: the same formulas, scores and P recomputed in float32, no
+ * workspace (ws may be NULL), any group size.
+ * Limits: as sfa_attn_fwd; d in {64, 128}: Hq / Hkv a power of two <= 8;
+ *         other d: B * Hq <= 65535.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC, SFA_EHIP.
  */
 sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val,

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsfa.so")
-SOURCES = ["sfa_encode.hip", "sfa_fwd.hip", "sfa_fwd_generic.hip", "sfa_fwd_index.hip", "sfa_bwd.hip", "sfa_decode.hip",
+SOURCES = ["sfa_encode.hip", "sfa_fwd.hip", "sfa_fwd_generic.hip", "sfa_fwd_index.hip", "sfa_bwd.hip", "sfa_bwd_generic.hip", "sfa_decode.hip",
            "sfa_decode_generic.hip",
            "sfa_cache.hip", "sfa_format.hip", "sfa_capi.cpp"]
 ARCH = "gfx950"

@@ -122,7 +122,15 @@ sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
   if (st != SFA_OK) return st;
   if (!lse || !dout || !dq_val || !dk_val || !dv) return SFA_EINVAL;
   if (window < 0 || n_global < 0) return SFA_EINVAL;
-  if (d != 64 && d != 128) return SFA_ENOTSUP;
+  if (d != 64 && d != 128) {
+    // head dimensions without the matrix-core kernels: the float32 backward
+    // (no workspace)
+    if (!sfa::bwd_generic_supported(d, k) || (long long)B * Hq > 65535) return SFA_ENOTSUP;
+    return from_hip(sfa::launch_attn_bwd_generic(
+        q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n, d, k, causal != 0, window,
+        window > 0 ? n_global : 0, scale, ifmt_of(idx_t), vfmt_of(qk_val_t), v_t == SFA_BF16,
+        o_t == SFA_BF16, dq_val, dk_val, dv, (hipStream_t)stream));
+  }
   if (!pow2_le(Hq / Hkv, sfa::bwd_max_group())) return SFA_ENOTSUP;
   if (ws == nullptr || ws_bytes < sfa::bwd_workspace_bytes(B, Hq, Hkv, n, d)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n,

@@ -37,6 +37,16 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
 size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d);
 int bwd_max_group();
 
+// float32 backward for head dimensions without the matrix-core kernels
+// (d <= 256); no workspace, any group size
+hipError_t launch_attn_bwd_generic(const void* q_idx, const void* q_val, const void* k_idx,
+                                   const void* k_val, const void* v, const void* o,
+                                   const float* lse, const void* dout, int B, int Hq, int Hkv,
+                                   int n, int d, int k, int causal, int window, int n_global,
+                                   float scale, int ifmt, int vfmt, int vbf16, int obf16,
+                                   float* dq, float* dk, float* dv, hipStream_t stream);
+bool bwd_generic_supported(int d, int k);
+
 hipError_t launch_attn_fwd_index(const void* q_idx, const void* q_val, const void* k_idx,
                                  const void* k_val, const void* v, int B, int Hq, int Hkv, int n,
                                  int d, int k, int causal, float scale, int ifmt, int vfmt,

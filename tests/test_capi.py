@@ -162,7 +162,8 @@ def test_bwd_validation_and_workspace(L):
     assert _bwd(L, k=0) == 1
     assert _bwd(L, Hq=3, Hkv=2) == 1
     assert _bwd(L, Hq=32, Hkv=2) == 2      # group of 16 heads: not supported by the backward
-    assert _bwd(L, d=96, k=8) == 2
+    assert _bwd(L, d=300, k=8) == 2                 # beyond the largest head dim, 256
+    assert _bwd(L, d=96, k=8, B=40000, Hq=2, Hkv=1) == 2  # float32 backward: grid bound on B * Hq
 
 
 def _paged(L, **kw):

@@ -65,6 +65,20 @@ def test_shapes(B, Hq, Hkv, n, d, k, causal, v_bf16):
     _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=7 * n + k + Hq)
 
 
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,v_bf16,o_bf16",
+    [
+        (1, 3, 1, 70, 80, 8, True, True, False),     # d = 80, group of 3
+        (1, 2, 2, 100, 96, 12, False, False, False),  # d = 96, non-causal
+        (1, 2, 1, 45, 256, 16, True, True, True),    # d = 256, bf16 O and dO
+        (2, 1, 1, 33, 32, 32, True, False, False),   # k = d = 32
+        (1, 4, 2, 130, 200, 20, True, True, False),  # d = 200, several blocks
+    ])
+def test_other_head_dims(B, Hq, Hkv, n, d, k, causal, v_bf16, o_bf16):
+    """Head dimensions other than 64 and 128 run the float32 backward."""
+    _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=d + n, o_bf16=o_bf16)
+
+
 def test_bf16_output_and_grad():
     _run(1, 4, 2, 150, 128, 16, True, True, seed=21, o_bf16=True)
 

@@ -156,6 +156,7 @@ def test_decode_window(w, g, seq, d):
     (1, 2, 2, 400, 64, 8, False, False, 60, 40),
     (1, 8, 1, 600, 128, 16, True, True, 1, 0),
     (2, 2, 1, 333, 128, 16, False, True, 45, 0),
+    (1, 3, 1, 300, 96, 8, True, True, 40, 3),      # head dim 96: float32 backward
 ])
 def test_bwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
     seed = 3 * n + w + g
