@@ -15,7 +15,7 @@
 // Cache layouts: contiguous [B, Hkv, Lmax, ...], or paged -- a pool of pages
 // [num_pages, Hkv, P, ...] with a block table mapping each run of P
 // positions of a sequence to a page (P a power of two >= 16).  A wave's
-// 512-position range spans at most 32 pages; their ids are loaded once into
+// 1024-position range spans at most 64 pages; their ids are loaded once into
 // one register (lane l: the range's l-th page) and read back by lane shuffle
 // for the codes (lane = key) and by readlane for V, whose keys within one
 // wide load always share a page.
@@ -29,7 +29,7 @@ namespace sfa {
 
 constexpr int kDecWaves = 4;
 constexpr int kDecThreads = 64 * kDecWaves;
-constexpr int kDecChunk = 2048;  // keys per workgroup
+constexpr int kDecChunk = kDecodeChunk;  // keys per workgroup
 constexpr int kDecMaxG = 8;
 
 struct DecParams {
@@ -154,7 +154,8 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   const int pg0 = PAGED ? (w0 >> p.log2P) : 0;
   if constexpr (PAGED) {
     if (w0 < w1) {
-      const int npg = ((w1 - 1) >> p.log2P) - pg0 + 1;  // <= 32 (P >= 16)
+      // <= 64 (P >= 16; w0 is 1024-aligned, or 64-aligned at a window start)
+      const int npg = ((w1 - 1) >> p.log2P) - pg0 + 1;
       if (lane < npg) {
         const int pg = p.table[(int64_t)b * p.max_pages + pg0 + lane];
         tblv = min(max(pg, 0), p.num_pages - 1);

@@ -2,7 +2,7 @@
 // the tuned kernel: any d <= 256 other than 64 and 128, float32 arithmetic.
 //
 // Same split of the context as the tuned decode: a workgroup takes one chunk
-// of 2048 cached keys of one (sequence, KV head) for all G query heads and
+// of cached keys of one (sequence, KV head) for all G query heads and
 // writes a partial (m, l, o) per head; a combine kernel merges the chunks by
 // their log-sum-exp.  Inside a chunk, sub-blocks of 256 keys: thread = key
 // for the scores (s_h = sum_t kval_t * qd[kidx_t][h], the query codes
@@ -17,7 +17,7 @@
 namespace sfa {
 namespace {
 
-constexpr int kGdChunk = 2048;  // keys per workgroup: the tuned decode's partial slots
+constexpr int kGdChunk = kDecodeChunk;  // keys per workgroup: the workspace's partial slots
 constexpr int kGdT = 256;       // threads; keys per sub-block
 constexpr int kGdW = kGdT / 64;
 constexpr int kGdMaxG = 8;

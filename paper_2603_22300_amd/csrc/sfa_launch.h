@@ -72,6 +72,9 @@ struct DecodeArgs {
   float* lse;
   void* ws;
 };
+// Keys per decode workgroup (one context chunk); the workspace holds one
+// partial (m, l, o) per chunk, query head and sequence.
+constexpr int kDecodeChunk = 4096;
 hipError_t launch_attn_decode(const DecodeArgs& a, hipStream_t stream);
 size_t decode_workspace_bytes(int B, int Hq, int Lmax, int d);
 int decode_max_group();
