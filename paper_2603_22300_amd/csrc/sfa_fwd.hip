@@ -102,10 +102,17 @@ __host__ __device__ constexpr int n_stages() {
   return 2 * stage_bytes<D, VBF16>() <= 160 * 1024 ? 2 : 1;
 }
 
+// The densified query rows of the prologue sit past stage 0 with bf16 V, so
+// that the first tile's copy into stage 0 overlaps the prologue.
+template <int D, bool VBF16>
+__host__ __device__ constexpr int qs_offset() {
+  return VBF16 ? stage_bytes<D, VBF16>() : 0;
+}
+
 template <int D, bool VBF16, int NW>
 __host__ __device__ constexpr int lds_bytes() {
   constexpr int st = n_stages<D, VBF16>() * stage_bytes<D, VBF16>();
-  constexpr int qs = NW * 32 * Geo<D, 2>::QP * 2;
+  constexpr int qs = qs_offset<D, VBF16>() + NW * 32 * Geo<D, 2>::QP * 2;
   return st > qs ? st : qs;
 }
 
@@ -167,7 +174,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   constexpr int VI = (VITEMS + NT - 1) / NT;   // V items per thread and tile
   constexpr int VW = VBF16 ? 8 : 4;            // registers per V item
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t* Qs = (uint16_t*)smem;              // setup only: [R][QP]
+  uint16_t* Qs = (uint16_t*)(smem + qs_offset<D, VBF16>());  // setup only: [R][QP]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -206,12 +213,100 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // key tile of list position t (t == ntiles gives ntiles_all: past the end)
   auto tile_at = [&](int t) { return t < gt_end ? t : wt_begin + (t - gt_end); };
 
-  if constexpr (VBF16 && !SAFE) {
+  // bf16 V: key tiles arrive as prepared stage images, copied global -> LDS
+  // by the memory unit (16 bytes per lane, 1 KB per wave instruction);
+  // completion is awaited with vmcnt before the barrier that publishes them.
+  constexpr bool kDMA = VBF16 && !SAFE;
+  auto dma_stage = [&](int stage, int jt) {
+    static_assert(SB % 1024 == 0, "stage images are whole 1 KB blocks");
+    constexpr int NB = SB / 1024, NJ = (NB + NW - 1) / NW;
+    // wave-uniform base + 32-bit lane offset: the scalar-base address form
+    const unsigned char* src = p.ws_tiles + ((int64_t)bh * p.vtiles + jt) * SB;
+    unsigned char* dst = smem + stage * SB;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = wave + j * NW;  // 1 KB block of the image
+      if (j + 1 < NJ || i < NB)
+        __builtin_amdgcn_global_load_lds(src + (uint32_t)(i * 1024 + lane * 16),
+                                         (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                         16, 0, 0);
+    }
+  };
+  auto wait_dma = [&]() {
+    if constexpr (kDMA) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+  };
+
+  // V range flags of the workgroup's key tiles (thread tid: list positions
+  // tid, tid + NT, ...): the first is loaded now, all are tested once the
+  // query operand is built (a flagged workgroup writes nothing before that).
+  int vflag = 0;
+  if constexpr (kDMA) {
+    if (tid < ntiles) vflag = p.ws_flag[(int64_t)bh * p.vtiles + tile_at(tid)];
+  }
+
+  // ---------------- query operand: NP bf16 pieces of the densified rows ----
+  // The query values carry scale * log2(e): the score tiles come out as the
+  // base-2 exponents t = s * scale * log2(e) of the softmax, sign included.
+  // Code entry e of the block is term e % k of row r = e / k, the query head
+  // hkv*G + r / BR at position i0 + r % BR (BR is a power of two).
+  const int lbr = __builtin_ctz(p.BR);
+  auto q_entry = [&](int e, int& at, float& x) {
+    const int r = (int)(((float)e + 0.5f) * p.inv_k);
+    const int i = i0 + (r & (p.BR - 1));
+    at = -1;
+    x = 0.f;
+    if (e < R * k && i < n) {
+      const int hq = hkv * p.G + (r >> lbr);
+      const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + (e - r * k);
+      at = r * QP + load_idx(p.q_idx, gi, p.ifmt, dmask);
+      x = p.scale_log2 * load_val(p.q_val, gi, p.vfmt);
+    }
+  };
+  // With k <= 16 every thread's entries fit in registers: they are loaded
+  // once, ahead of the first tile's copy, and serve all pieces.
+  constexpr int QE = KM <= 16 ? R * KM / NT : 1;
+  int q_at[QE];
+  float q_x[QE];
+  if constexpr (KM <= 16) {
+#pragma unroll
+    for (int u = 0; u < QE; ++u) q_entry(tid + NT * u, q_at[u], q_x[u]);
+  }
+  if constexpr (kDMA && NS == 2) {
+    if (ntiles > 0) dma_stage(0, tile_at(0));  // stage 0; Qs lies past it
+  }
+
+  // Pieces are scattered into the same coordinates, so the rows are zeroed
+  // once and each piece overwrites the previous one.
+  for (int x = tid; x < R * QP / 8; x += NT) ((uint4*)Qs)[x] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  bf16x8 qB[NP][NKB];
+#pragma unroll
+  for (int pc = 0; pc < NP; ++pc) {
+    if (pc > 0) __syncthreads();  // the previous piece is read
+    if constexpr (KM <= 16) {
+#pragma unroll
+      for (int u = 0; u < QE; ++u)
+        if (q_at[u] >= 0) Qs[q_at[u]] = bf16_piece(q_x[u], pc);
+    } else {
+      for (int e = tid; e < R * k; e += NT) {
+        int at;
+        float x;
+        q_entry(e, at, x);
+        if (at >= 0) Qs[at] = bf16_piece(x, pc);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) qB[pc][kb] = *(const bf16x8*)(Qs + rho * QP + kb * 16 + 8 * hh);
+  }
+
+  if constexpr (kDMA) {
     // A V tile of this workgroup's key range outside the float16 range: hand
     // the rows back to the bf16 rerun before doing any work.
-    bool over = false;
-    for (int t = tid; t < ntiles; t += NT) over |= p.ws_flag[(int64_t)bh * p.vtiles + tile_at(t)] != 0;
-    if (__syncthreads_or(over)) {
+    for (int t = tid + NT; t < ntiles; t += NT)
+      vflag |= p.ws_flag[(int64_t)bh * p.vtiles + tile_at(t)];
+    if (__syncthreads_or(vflag != 0)) {
+      wait_dma();  // the stage copy lands before the workgroup's LDS is released
       if (tid == 0) {
         const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;  // row rho = 0
         if (p.obf16) ((uint16_t*)p.o)[orow0 * D] = kHandBack16;
@@ -219,31 +314,6 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       }
       return;
     }
-  }
-
-  // ---------------- query operand: NP bf16 pieces of the densified rows ----
-  // The query values carry scale * log2(e): the score tiles come out as the
-  // base-2 exponents t = s * scale * log2(e) of the softmax, sign included.
-  bf16x8 qB[NP][NKB];
-#pragma unroll
-  for (int pc = 0; pc < NP; ++pc) {
-    for (int x = tid; x < R * QP / 8; x += NT) ((uint4*)Qs)[x] = make_uint4(0u, 0u, 0u, 0u);
-    __syncthreads();
-    for (int e = tid; e < R * k; e += NT) {
-      const int r = (int)(((float)e + 0.5f) * p.inv_k);
-      const int t = e - r * k;
-      const int i = i0 + r % p.BR;
-      if (i < n) {
-        const int hq = hkv * p.G + r / p.BR;
-        const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
-        const int f = load_idx(p.q_idx, gi, p.ifmt, dmask);
-        Qs[r * QP + f] = bf16_piece(p.scale_log2 * load_val(p.q_val, gi, p.vfmt), pc);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) qB[pc][kb] = *(const bf16x8*)(Qs + rho * QP + kb * 16 + 8 * hh);
-    __syncthreads();
   }
 
   // Cauchy-Schwarz bound on this row's exponents: |t_ij| <= qn * |k_j| (the
@@ -309,8 +379,6 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   const unsigned char* kidx_b = (const unsigned char*)p.k_idx + kv_base * k * isz;
   const unsigned char* kval_b = (const unsigned char*)p.k_val + kv_base * k * ksz;
   const unsigned char* v_b = (const unsigned char*)p.v + kv_base * D * (VBF16 ? 2 : 4);
-  // bf16 V: key tiles arrive as prepared stage images (dma_stage below)
-  constexpr bool kDMA = VBF16 && !SAFE;
   auto load_tile = [&](int jt) {
     if constexpr (kDMA) return;
     const int j0 = jt * kBC;
@@ -434,30 +502,9 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     write_tile_keys(stage, jt);
     write_tile_v(stage, jt);
   };
-  // bf16 V: the prepared stage image of a key tile is copied global -> LDS
-  // by the memory unit (16 bytes per lane, 1 KB per wave instruction);
-  // completion is awaited with vmcnt before the barrier that publishes it.
-  auto dma_stage = [&](int stage, int jt) {
-    static_assert(SB % 1024 == 0, "stage images are whole 1 KB blocks");
-    constexpr int NB = SB / 1024, NJ = (NB + NW - 1) / NW;
-    // wave-uniform base + 32-bit lane offset: the scalar-base address form
-    const unsigned char* src = p.ws_tiles + ((int64_t)bh * p.vtiles + jt) * SB;
-    unsigned char* dst = smem + stage * SB;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int i = wave + j * NW;  // 1 KB block of the image
-      if (j + 1 < NJ || i < NB)
-        __builtin_amdgcn_global_load_lds(src + (uint32_t)(i * 1024 + lane * 16),
-                                         (__attribute__((address_space(3))) void*)(dst + i * 1024),
-                                         16, 0, 0);
-    }
-  };
-  auto wait_dma = [&]() {
-    if constexpr (kDMA) __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
-  };
+  // the first tile in stage 0 (bf16 V: its copy was issued with the query loads)
   if (ntiles > 0 && NS == 2) {
     if constexpr (kDMA) {
-      dma_stage(0, tile_at(0));
       wait_dma();
     } else {
       load_tile(tile_at(0));
