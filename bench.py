@@ -134,13 +134,14 @@ def _overlap_count(qi: torch.Tensor, ki: torch.Tensor, d: int, G: int, causal: b
     return E
 
 
-def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
+def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
     q, k, v = _fwd_inputs(w)
     B, Hq, Hkv, n, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
-    qi = torch.empty((B, Hq, n, kk), dtype=torch.int32, device=DEV)
-    qv = torch.empty((B, Hq, n, kk), dtype=torch.float32, device=DEV)
-    ki = torch.empty((B, Hkv, n, kk), dtype=torch.int32, device=DEV)
-    kv = torch.empty((B, Hkv, n, kk), dtype=torch.float32, device=DEV)
+    idt, vdt = FWD_CODE_FORMATS[codes]
+    qi = torch.empty((B, Hq, n, kk), dtype=idt, device=DEV)
+    qv = torch.empty((B, Hq, n, kk), dtype=vdt, device=DEV)
+    ki = torch.empty((B, Hkv, n, kk), dtype=idt, device=DEV)
+    kv = torch.empty((B, Hkv, n, kk), dtype=vdt, device=DEV)
     o = torch.empty((B, Hq, n, d), dtype=torch.bfloat16, device=DEV)
     lse = torch.empty((B, Hq, n), dtype=torch.float32, device=DEV)
     ws = torch.empty(sfa.sfa_attn_fwd_workspace(B, Hkv, n, d, v.dtype), dtype=torch.uint8, device=DEV)
@@ -182,9 +183,18 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     algo_flops = pv_flops + 2.0 * E     # + one multiply-add per overlapping coordinate
     achieved = algo_flops / (fwd_avg * 1e-3)
     tokens = B * n
+    metric = METRIC if window == 0 else METRIC + f"; sliding window {window} + {n_global} global tokens"
+    if codes != "i32f32":
+        metric += f"; codes stored as {_CODE_NAMES[codes]}"
+        precision = (f"codes {_CODE_NAMES[codes]}; scores fp32 (one exact {vdt_name(vdt)} MFMA product "
+                     "per coordinate block, scale applied in fp32); softmax fp32; P.V fp16 MFMA on V "
+                     "converted exactly to fp16, fp32 accumulate; O bf16")
+    else:
+        precision = ("codes fp32; scores fp32 (three bf16 piece products on MFMA); softmax fp32; "
+                     "P.V fp16 MFMA on V converted exactly to fp16, fp32 accumulate; O bf16")
+    hbm = _fwd_bytes(w, idt, vdt)
     out = {
-        "metric": METRIC if window == 0 else
-        METRIC + f"; sliding window {window} + {n_global} global tokens",
+        "metric": metric,
         "value": tokens / (ms_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -200,8 +210,8 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
             "workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "n": n, "d": d, "k": kk,
             "causal": w.causal, "seed": w.seed, "window": window, "n_global": n_global,
             "step": "sfa_topk_encode(Q) + sfa_topk_encode(K) + sfa_attn_fwd",
-            "precision": ("codes fp32; scores fp32 (three bf16 piece products on MFMA); softmax fp32; "
-                          "P.V fp16 MFMA on V converted exactly to fp16, fp32 accumulate; O bf16"),
+            "codes": codes,
+            "precision": precision,
         },
         "roofline": {
             "kernel": "sfa_fwd_kernel",
@@ -210,15 +220,16 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
             "peak": PEAK_MFMA_BF16 / 1e12,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_MFMA_BF16,
-            "traffic": _traffic("sfa_fwd.hip", w.name),
+            # the committed counter summary is of the fp32-code forward
+            "traffic": _traffic("sfa_fwd.hip", w.name) if codes == "i32f32" and window == 0 else None,
             "algorithmic_flops_per_launch": algo_flops,
             "pv_flops_per_launch": pv_flops,
             "fwd_ms_avg": fwd_avg,
             "fwd_ms_min": float(np.min(fwd_ms)),
             "allowed_pairs": pairs,
             "overlap_products_E": E,
-            "algorithmic_hbm_bytes_per_launch": _fwd_bytes(w),
-            "hbm_frac": _fwd_bytes(w) / (fwd_avg * 1e-3) / PEAK_HBM,
+            "algorithmic_hbm_bytes_per_launch": hbm,
+            "hbm_frac": hbm / (fwd_avg * 1e-3) / PEAK_HBM,
         },
         # the two parts of the step: encoding Q and K, and the forward on
         # codes already in HBM
@@ -230,7 +241,7 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0):
         },
         "wall_s_timed": wall,
     }
-    if want_cpu and window == 0:
+    if want_cpu and window == 0 and codes == "i32f32":
         out["cpu_baseline"] = cpu_baseline_fwd(w, q, k, v)
     return out
 
@@ -348,10 +359,12 @@ def cpu_baseline_bwd(w, q, k, v, dout, n_sub=3072):
     }
 
 
-def _fwd_bytes(w):
-    """Compulsory HBM bytes of one forward launch: codes in (int32 + fp32),
-    V in (bf16), O out (bf16), LSE out (fp32)."""
-    codes = (w.B * w.Hq * w.n + w.B * w.Hkv * w.n) * w.k * 8
+def _fwd_bytes(w, idt=torch.int32, vdt=torch.float32):
+    """Compulsory HBM bytes of one forward launch: codes in (index + value
+    bytes per entry; int32 + fp32 by default), V in (bf16), O out (bf16), LSE
+    out (fp32)."""
+    entry = torch.empty((), dtype=idt).element_size() + torch.empty((), dtype=vdt).element_size()
+    codes = (w.B * w.Hq * w.n + w.B * w.Hkv * w.n) * w.k * entry
     return codes + w.B * w.Hkv * w.n * w.d * 2 + w.B * w.Hq * w.n * w.d * 2 + w.B * w.Hq * w.n * 4
 
 
@@ -418,7 +431,12 @@ def cpu_baseline_fwd(w, q, k, v, budget_rows=1536, seed=0):
 # ----------------------------------------------------------------------------
 
 CODE_FORMATS = {"i16bf16": (torch.int16, torch.bfloat16), "u8f16": (torch.uint8, torch.float16)}
-_CODE_NAMES = {"i16bf16": "int16/bf16", "u8f16": "uint8/float16"}
+FWD_CODE_FORMATS = dict(CODE_FORMATS, i32f32=(torch.int32, torch.float32))
+_CODE_NAMES = {"i16bf16": "int16/bf16", "u8f16": "uint8/float16", "i32f32": "int32/float32"}
+
+
+def vdt_name(vdt) -> str:
+    return {torch.bfloat16: "bf16", torch.float16: "float16"}.get(vdt, str(vdt))
 
 
 def _decode_keys(L: int, window: int, n_global: int) -> int:
@@ -591,9 +609,10 @@ def main():
     ap.add_argument("--cache", default="contiguous", choices=["contiguous", "paged"],
                     help="decode workloads: contiguous cache (decode only) or paged cache "
                          "(append of the new token + decode with in-kernel query coding)")
-    ap.add_argument("--codes", default="i16bf16", choices=sorted(CODE_FORMATS),
-                    help="decode workloads: cache code storage (int16 indices + bf16 values, or "
-                         "the paper's compact uint8 indices + float16 values)")
+    ap.add_argument("--codes", default=None, choices=sorted(FWD_CODE_FORMATS),
+                    help="code storage: int32 indices + fp32 values (forward default), int16 + "
+                         "bf16 (decode default), or the paper's compact uint8 + float16; decode "
+                         "takes the two 16-bit formats")
     ap.add_argument("--window", type=int, default=0,
                     help="token sparsity composed with SFA: sliding window (0: none)")
     ap.add_argument("--n-global", type=int, default=0,
@@ -612,17 +631,21 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     w = si.workload(args.workload)
+    codes = args.codes or ("i16bf16" if w.kind == "decode" else "i32f32")
+    if (w.kind == "decode" and codes not in CODE_FORMATS) or (args.which == "bwd" and codes != "i32f32"):
+        print(f"--codes {codes} is not measured for this workload / pass", file=sys.stderr)
+        sys.exit(2)
     if w.kind == "decode" and args.cache == "paged":
-        out = bench_decode_paged(w, args.steps, args.warmup, args.codes)
+        out = bench_decode_paged(w, args.steps, args.warmup, codes)
     elif w.kind == "decode":
-        out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline, args.codes,
+        out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline, codes,
                            args.window, args.n_global)
     elif args.which == "bwd":
         out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
                         args.n_global)
     else:
         out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
-                        args.n_global)
+                        args.n_global, codes)
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device=DEV)
         dst = torch.empty_like(src)

@@ -16,6 +16,12 @@
 // score keeps the terms q0k0 + q0k1 + q1k0 (relative error ~2^-16 of
 // sum|q_u k_u|); with float32 V it keeps every term of order <= 2
 // (q0k0 + q0k1 + q1k0 + q0k2 + q1k1 + q2k0, ~2^-24).
+// 16-bit codes (bf16 or float16 values) with bf16 V and k <= 16: the raw
+// values are already MFMA operands, so each 16-coordinate block of the score
+// is one exact product on the matrix cores (bf16 or float16 MFMA), and the
+// float32 score is multiplied by |scale| * log2(e) before exp2 (the sign of
+// scale flips the query values' sign bits).  Per 64-key tile a wavefront then
+// issues 16 score MFMAs instead of 48.
 // P.V with bf16 V: V is converted to float16 (exact for normal values up to
 // 65504) and P enters as float16 (P < 2^15, relative rounding 2^-11), one
 // MFMA per block.  A workgroup whose keys hold a V value outside the float16
@@ -59,6 +65,10 @@ struct FwdParams {
   int Hq, Hkv, n, k, causal;
   int window, n_global;  // token pattern: |i - j| < window or a global token (window 0: none)
   float scale_log2;  // scale * log2(e)
+  // 16-bit codes: |scale| * log2(e), and the sign of scale as a 16-bit sign bit
+  float kx_scale;
+  uint32_t qsign;
+  int kx;  // 0, or the 16-bit code value type taking the one-product path
   int ifmt, vfmt, obf16;
   int G, BR, nqb;
   float inv_k;
@@ -89,30 +99,37 @@ __host__ __device__ constexpr int vtile_bytes() {
   return (D * (kBC + 4) * 2 + 1023) / 1024 * 1024;
 }
 
-template <int D, bool VBF16>
+// bf16 pieces per key value: two (bf16 V) or three (float32 V) pieces of a
+// float32 value; one raw value for 16-bit codes (KX = kValBF16 / kValF16).
+template <bool VBF16, int KX>
+__host__ __device__ constexpr int n_pieces() {
+  return KX ? 1 : (VBF16 ? 2 : 3);
+}
+
+template <int D, bool VBF16, int KX = 0>
 __host__ __device__ constexpr int stage_bytes() {
-  constexpr int NP = VBF16 ? 2 : 3;
+  constexpr int NP = n_pieces<VBF16, KX>();
   return kBC * Geo<D, NP>::KR * 2 + (VBF16 ? vtile_bytes<D>() : kBC * D * 4);
 }
 
 // Two LDS stages (next tile written while the current one is read) when they
 // fit; the float32-V path (three pieces, float32 V tile) uses one.
-template <int D, bool VBF16>
+template <int D, bool VBF16, int KX = 0>
 __host__ __device__ constexpr int n_stages() {
-  return 2 * stage_bytes<D, VBF16>() <= 160 * 1024 ? 2 : 1;
+  return 2 * stage_bytes<D, VBF16, KX>() <= 160 * 1024 ? 2 : 1;
 }
 
 // The densified query rows of the prologue sit past stage 0 with bf16 V, so
 // that the first tile's copy into stage 0 overlaps the prologue.
-template <int D, bool VBF16>
+template <int D, bool VBF16, int KX = 0>
 __host__ __device__ constexpr int qs_offset() {
-  return VBF16 ? stage_bytes<D, VBF16>() : 0;
+  return VBF16 ? stage_bytes<D, VBF16, KX>() : 0;
 }
 
-template <int D, bool VBF16, int NW>
+template <int D, bool VBF16, int NW, int KX = 0>
 __host__ __device__ constexpr int lds_bytes() {
-  constexpr int st = n_stages<D, VBF16>() * stage_bytes<D, VBF16>();
-  constexpr int qs = qs_offset<D, VBF16>() + NW * 32 * Geo<D, 2>::QP * 2;
+  constexpr int st = n_stages<D, VBF16, KX>() * stage_bytes<D, VBF16, KX>();
+  constexpr int qs = qs_offset<D, VBF16, KX>() + NW * 32 * Geo<D, 2>::QP * 2;
   return st > qs ? st : qs;
 }
 
@@ -157,16 +174,20 @@ constexpr uint32_t kHandBack32 = 0x7fa5a5a5u;
 // SAFE (bf16 V only): V is staged as bf16 and P.V uses P = Ph + Pl on the
 // bf16 MFMA, every tile on the generic path; it reruns the workgroups that the
 // float16 path handed back.
-template <int D, bool VBF16, int NW, int KM, bool SAFE>
+// KX (bf16 V, 16-bit codes): kValBF16 or kValF16, the code values' type.  The
+// raw query and key values are the MFMA operands (bf16 or float16), so each
+// score is one exact product sum; the scale is applied to the float32 scores.
+template <int D, bool VBF16, int NW, int KM, bool SAFE, int KX = 0>
 __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, const int bh) {
   static_assert(VBF16 || !SAFE, "the rerun is for bf16 V");
+  static_assert(KX == 0 || (VBF16 && !SAFE && KM <= 16), "16-bit codes: bf16 V, k <= 16");
   constexpr int NT = NW * 64;
   constexpr int R = NW * 32;
-  constexpr int NP = VBF16 ? 2 : 3;
+  constexpr int NP = n_pieces<VBF16, KX>();
   using Gm = Geo<D, NP>;
   constexpr int QP = Gm::QP, KR = Gm::KR, VP = Gm::VP, NKB = Gm::NKB, NDB = Gm::NDB;
-  constexpr int NS = n_stages<D, VBF16>();
-  constexpr int SB = stage_bytes<D, VBF16>();
+  constexpr int NS = n_stages<D, VBF16, KX>();
+  constexpr int SB = stage_bytes<D, VBF16, KX>();
   constexpr int KW = kBC / NW;                 // key rows owned (zeroed, filled) by a wave
   constexpr int KEL = (KW * KM + 63) / 64;     // key-code entries per lane and tile
   constexpr int NDP = D / 2;
@@ -174,7 +195,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   constexpr int VI = (VITEMS + NT - 1) / NT;   // V items per thread and tile
   constexpr int VW = VBF16 ? 8 : 4;            // registers per V item
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t* Qs = (uint16_t*)(smem + qs_offset<D, VBF16>());  // setup only: [R][QP]
+  uint16_t* Qs = (uint16_t*)(smem + qs_offset<D, VBF16, KX>());  // setup only: [R][QP]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -247,6 +268,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // ---------------- query operand: NP bf16 pieces of the densified rows ----
   // The query values carry scale * log2(e): the score tiles come out as the
   // base-2 exponents t = s * scale * log2(e) of the softmax, sign included.
+  // With 16-bit codes the operand is the raw value (sign of scale folded in)
+  // and the scores are multiplied by cs = |scale| * log2(e) after the MFMA.
   // Code entry e of the block is term e % k of row r = e / k, the query head
   // hkv*G + r / BR at position i0 + r % BR (BR is a power of two).
   const int lbr = __builtin_ctz(p.BR);
@@ -259,7 +282,10 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       const int hq = hkv * p.G + (r >> lbr);
       const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + (e - r * k);
       at = r * QP + load_idx(p.q_idx, gi, p.ifmt, dmask);
-      x = p.scale_log2 * load_val(p.q_val, gi, p.vfmt);
+      if constexpr (KX != 0)  // the 16-bit pattern, carried in a float register
+        x = __uint_as_float((uint32_t)((const uint16_t*)p.q_val)[gi] ^ p.qsign);
+      else
+        x = p.scale_log2 * load_val(p.q_val, gi, p.vfmt);
     }
   };
   // With k <= 16 every thread's entries fit in registers: they are loaded
@@ -286,13 +312,14 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     if constexpr (KM <= 16) {
 #pragma unroll
       for (int u = 0; u < QE; ++u)
-        if (q_at[u] >= 0) Qs[q_at[u]] = bf16_piece(q_x[u], pc);
+        if (q_at[u] >= 0)
+          Qs[q_at[u]] = KX ? (uint16_t)__float_as_uint(q_x[u]) : bf16_piece(q_x[u], pc);
     } else {
       for (int e = tid; e < R * k; e += NT) {
         int at;
         float x;
         q_entry(e, at, x);
-        if (at >= 0) Qs[at] = bf16_piece(x, pc);
+        if (at >= 0) Qs[at] = KX ? (uint16_t)__float_as_uint(x) : bf16_piece(x, pc);
       }
     }
     __syncthreads();
@@ -319,8 +346,19 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // Cauchy-Schwarz bound on this row's exponents: |t_ij| <= qn * |k_j| (the
   // overlap sum runs over a subset of the coordinates), with a margin for the
   // bf16 pieces and float32 rounding.
+  const float cs = KX ? p.kx_scale : 1.f;  // score units -> base-2 exponent units
   float qn = 0.f;
-  if constexpr (NP == 2) {
+  if constexpr (KX != 0) {
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint16_t bits = __builtin_bit_cast(uint16_t, qB[0][kb][e]);
+        const float x = KX == kValF16 ? f16_bits_to_f32(bits) : bf16_bits_to_f32(bits);
+        qn = fmaf(x, x, qn);
+      }
+    qn = sqrtf(pair_sum(qn)) * cs * (1.f + 1.f / 256.f);
+  } else if constexpr (NP == 2) {
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
@@ -333,7 +371,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
 
   float m_run = -INFINITY, l_run = 0.f;
   // Interior tiles start their score accumulators at -m_run (the C operand of
-  // the first MFMA), so they come out as t - m_run, the argument of exp2.
+  // the first MFMA), so they come out as t - m_run, the argument of exp2
+  // (16-bit codes: at -m_run / cs, giving (t - m_run) / cs).
   constexpr bool kFast = NS == 2 && VBF16 && !SAFE;
   floatx16 negm, zero16;
 #pragma unroll
@@ -341,8 +380,9 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   auto set_m = [&](float m) {
     m_run = m;
     if constexpr (kFast) {
+      const float c0 = KX ? -m / cs : -m;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) negm[r] = -m;
+      for (int r = 0; r < 16; ++r) negm[r] = c0;
     }
   };
   floatx16 acc[NDB];
@@ -524,6 +564,14 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
 #pragma unroll
       for (int pc = 0; pc < NP; ++pc)
         ka[pc] = *(const bf16x8*)(Kd + (s * 32 + l32) * KR + pc * D + kb * 16 + 8 * hh);
+      if constexpr (KX == kValF16) {
+        o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[0]),
+                                                   __builtin_bit_cast(f16x8, qB[0][kb]), o, 0, 0, 0);
+        continue;
+      } else if constexpr (KX == kValBF16) {
+        o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
+        continue;
+      }
       // smaller terms first
       if constexpr (NP == 3) {
         o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[2], qB[0][kb], o, 0, 0, 0);
@@ -617,6 +665,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     float mt = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
+      if constexpr (KX != 0) sc[r] *= cs;
       const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
       const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
                       (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
@@ -671,13 +720,20 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       ka[pc] = *(const bf16x8*)(Kd + (s * 32 + l32) * KR + pc * D + kb * 16 + 8 * hh);
   };
   auto score_terms = [&](floatx16& o, const bf16x8 (&ka)[NP], int kb) {
-    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[0][kb], o, 0, 0, 0);
-    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[1][kb], o, 0, 0, 0);
-    o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
+    if constexpr (KX == kValF16) {
+      o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[0]),
+                                                 __builtin_bit_cast(f16x8, qB[0][kb]), o, 0, 0, 0);
+    } else if constexpr (KX == kValBF16) {
+      o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
+    } else {
+      o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[0][kb], o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[1][kb], o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
+    }
   };
   // probability of value r (exp of the lane's score), as float16 into pf
   auto exp_h = [&](const floatx16& o, int r, float& rs, f16x8 (&pf)[2]) {
-    const float pr = fast_exp2(o[r]);
+    const float pr = fast_exp2(KX ? o[r] * cs : o[r]);
     rs += pr;
     pf[r >> 3][r & 7] = (_Float16)pr;
   };
@@ -698,7 +754,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     __builtin_amdgcn_s_setprio(0);
     if (!bounded) {
       asm volatile("");
-      if (__builtin_amdgcn_ballot_w64(sub_max(s0) > kLazyMax)) return false;
+      if (__builtin_amdgcn_ballot_w64(sub_max(s0) * cs > kLazyMax)) return false;
     }
     // ---- B: scores(1) || softmax(0) ----
     f16x8 p0[2];
@@ -719,7 +775,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     l_run += rs;
     if (!bounded) {
       asm volatile("");
-      const float mt1 = sub_max(s1);  // largest t - m_run of sub-tile 1
+      const float mt1 = sub_max(s1) * cs;  // largest t - m_run of sub-tile 1
       const bool up1 = mt1 > kLazyMax;
       if (__builtin_amdgcn_ballot_w64(up1)) {
         const float dm = up1 ? mt1 : 0.f;
@@ -727,8 +783,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
         set_m(m_run + dm);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          p0[r >> 3][r & 7] = (_Float16)fast_exp2(s0[r] - dm);
-          s1[r] -= dm;
+          p0[r >> 3][r & 7] = (_Float16)fast_exp2((KX ? s0[r] * cs : s0[r]) - dm);
+          s1[r] -= KX ? dm / cs : dm;
         }
       }
     }
@@ -791,7 +847,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
       if (act0 && act1 && !need_mask) {
         // largest key norm of the tile, kept by the prepared image in the
         // padding of key row 0
-        const float kn = *(const float*)(Kd + 2 * D);
+        const float kn = *(const float*)(Kd + NP * D);
         const bool bounded = !__builtin_amdgcn_ballot_w64(!(qn * kn <= m_run + kBoundMax));
         done = fast_tile(Kd, (const uint16_t*)vt, jt_next, stage ^ 1, bounded);
       }
@@ -830,7 +886,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   }
 }
 
-template <int D, bool VBF16, int NW, int KM>
+template <int D, bool VBF16, int NW, int KM, int KX>
 __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
   // longest causal blocks first
   // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
@@ -845,7 +901,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     qb = j % p.nqb;
     bh = xcd + 8 * (j / p.nqb);
   }
-  fwd_block<D, VBF16, NW, KM, false>(p, p.nqb - 1 - qb, bh);
+  fwd_block<D, VBF16, NW, KM, false, KX>(p, p.nqb - 1 - qb, bh);
 }
 
 // Whether workgroup t = bh * nqb + qb was handed back (its first output
@@ -883,7 +939,8 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
 // is exactly what the forward kernel holds in LDS for keys 64t .. 64t+63:
 //   - the dense key tile [key][piece][coordinate] (pitch KR) with the codes'
 //     values as bf16 pieces x0 = bf16(x), x1 = bf16(x - x0) at their
-//     coordinates and zeros elsewhere;
+//     coordinates and zeros elsewhere (KX: 16-bit codes, the raw values,
+//     one piece);
 //   - V^T as float16, [dimension][key] (pitch kBC + 4);
 //   - in the padding of key row 0, the largest Euclidean norm of the tile's
 //     key codes (times 1 + 2^-8), which bounds the tile's scores.
@@ -891,12 +948,13 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
 // tile lies outside the float16 range (|v| >= 65536, inf, NaN).  bf16 ->
 // float16 is exact for 2^-14 <= |v| <= 65504; below that it rounds to the
 // float16 subnormal grid (absolute error <= 2^-25).
-template <int D>
+template <int D, int KX>
 __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
     const void* __restrict__ k_idx, const void* __restrict__ k_val, const uint16_t* __restrict__ v,
     int n, int k, int ifmt, int vfmt, int vtiles, unsigned char* __restrict__ ws_tiles,
     int* __restrict__ ws_flag) {
-  constexpr int KR = Geo<D, 2>::KR, VP = kBC + 4, SB = stage_bytes<D, true>();
+  constexpr int NP = n_pieces<true, KX>();
+  constexpr int KR = Geo<D, NP>::KR, VP = kBC + 4, SB = stage_bytes<D, true, KX>();
   __shared__ __attribute__((aligned(16))) uint16_t T[SB / 2];
   uint16_t* Vt = T + kBC * KR;
   const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
@@ -908,9 +966,13 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
     const int j = e / k;
     if (j0 + j >= n) break;
     const int f = load_idx(k_idx, c0 + e, ifmt, D - 1);
-    const float x = load_val(k_val, c0 + e, vfmt);
-    T[j * KR + f] = bf16_piece(x, 0);
-    T[j * KR + D + f] = bf16_piece(x, 1);
+    if constexpr (KX != 0) {
+      T[j * KR + f] = ((const uint16_t*)k_val)[c0 + e];
+    } else {
+      const float x = load_val(k_val, c0 + e, vfmt);
+      T[j * KR + f] = bf16_piece(x, 0);
+      T[j * KR + D + f] = bf16_piece(x, 1);
+    }
   }
   // largest Euclidean norm of the tile's key codes (padding of key row 0)
   __shared__ float kn2[kBC];
@@ -927,7 +989,7 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
   if (tid == 0) {
     float mx = 0.f;
     for (int j = 0; j < kBC; ++j) mx = fmaxf(mx, kn2[j]);
-    *(float*)(T + 2 * D) = sqrtf(mx) * (1.f + 1.f / 256.f);
+    *(float*)(T + NP * D) = sqrtf(mx) * (1.f + 1.f / 256.f);
   }
   const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
   bool over = false;
@@ -949,26 +1011,29 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
   if (tid == 0) ws_flag[(int64_t)bh * vtiles + t] = any ? 1 : 0;
 }
 
-template <int D, bool VBF16, int NW, int KM>
+template <int D, bool VBF16, int NW, int KM, int KX>
 hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
-  constexpr int bytes = lds_bytes<D, VBF16, NW>();
+  constexpr int bytes = lds_bytes<D, VBF16, NW, KX>();
+  constexpr int rbytes = lds_bytes<D, true, NW>();  // the rerun: two bf16 pieces
   static bool configured = false;  // per instantiation
-  if (bytes > 65536 && !configured) {
-    hipError_t e = hipFuncSetAttribute((const void*)sfa_fwd_kernel<D, VBF16, NW, KM>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-    if (e == hipSuccess && VBF16)
-      e = hipFuncSetAttribute((const void*)sfa_fwd_rerun_kernel<D, NW, KM>,
+  if (!configured) {
+    hipError_t e = hipSuccess;
+    if (bytes > 65536)
+      e = hipFuncSetAttribute((const void*)sfa_fwd_kernel<D, VBF16, NW, KM, KX>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess && VBF16 && rbytes > 65536)
+      e = hipFuncSetAttribute((const void*)sfa_fwd_rerun_kernel<D, NW, KM>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, rbytes);
     if (e != hipSuccess) return e;
     configured = true;
   }
   dim3 grid(p.nqb, B * p.Hkv), block(NW * 64);
-  hipLaunchKernelGGL((sfa_fwd_kernel<D, VBF16, NW, KM>), grid, block, bytes, stream, p);
+  hipLaunchKernelGGL((sfa_fwd_kernel<D, VBF16, NW, KM, KX>), grid, block, bytes, stream, p);
   if constexpr (VBF16) {
     // one resident workgroup per compute unit (LDS-bound)
     const int total = p.nqb * B * p.Hkv;
     dim3 rgrid(total < 256 ? total : 256);
-    hipLaunchKernelGGL((sfa_fwd_rerun_kernel<D, NW, KM>), rgrid, block, bytes, stream, p, B * p.Hkv);
+    hipLaunchKernelGGL((sfa_fwd_rerun_kernel<D, NW, KM>), rgrid, block, rbytes, stream, p, B * p.Hkv);
   }
   return hipGetLastError();
 }
@@ -977,8 +1042,12 @@ template <int D, bool VBF16, int NW>
 hipError_t launch_nw(FwdParams p, int B, hipStream_t stream) {
   p.BR = NW * 32 / p.G;
   p.nqb = (p.n + p.BR - 1) / p.BR;
-  return p.k <= 16 ? launch_km<D, VBF16, NW, 16>(p, B, stream)
-                   : launch_km<D, VBF16, NW, 128>(p, B, stream);
+  if constexpr (VBF16) {
+    if (p.kx == kValBF16) return launch_km<D, true, NW, 16, kValBF16>(p, B, stream);
+    if (p.kx == kValF16) return launch_km<D, true, NW, 16, kValF16>(p, B, stream);
+  }
+  return p.k <= 16 ? launch_km<D, VBF16, NW, 16, 0>(p, B, stream)
+                   : launch_km<D, VBF16, NW, 128, 0>(p, B, stream);
 }
 
 template <int D, bool VBF16>
@@ -1013,6 +1082,11 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
   p.window = window; p.n_global = n_global;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
   p.ifmt = ifmt; p.vfmt = vfmt; p.obf16 = obf16;
+  // 16-bit code values with bf16 V and k <= 16 take the one-product score
+  // path (a zero scale keeps the piece path: its scores are all zero)
+  p.kx = vbf16 && vfmt != kValF32 && k <= 16 && scale != 0.f ? vfmt : 0;
+  p.kx_scale = (float)(fabs((double)scale) * 1.4426950408889634);
+  p.qsign = scale < 0.f ? 0x8000u : 0u;
   p.G = Hq / Hkv;
   p.BR = 0; p.nqb = 0;
   p.inv_k = 1.0f / (float)k;
@@ -1024,14 +1098,22 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
     const size_t sb = d == 64 ? stage_bytes<64, true>() : stage_bytes<128, true>();
     p.ws_flag = (const int*)((unsigned char*)ws + tiles * sb);
     dim3 grid(p.vtiles, B * Hkv), block(256);
-    if (d == 64)
-      hipLaunchKernelGGL(sfa_fwd_prep_kernel<64>, grid, block, 0, stream, k_idx, k_val,
-                         (const uint16_t*)v, n, k, ifmt, vfmt, p.vtiles, (unsigned char*)ws,
-                         (int*)p.ws_flag);
-    else
-      hipLaunchKernelGGL(sfa_fwd_prep_kernel<128>, grid, block, 0, stream, k_idx, k_val,
-                         (const uint16_t*)v, n, k, ifmt, vfmt, p.vtiles, (unsigned char*)ws,
-                         (int*)p.ws_flag);
+    unsigned char* wt = (unsigned char*)ws;
+    int* wf = (int*)p.ws_flag;
+    const uint16_t* vb = (const uint16_t*)v;
+#define SFA_PREP(DD, KK)                                                                        \
+  hipLaunchKernelGGL((sfa_fwd_prep_kernel<DD, KK>), grid, block, 0, stream, k_idx, k_val, vb, n, \
+                     k, ifmt, vfmt, p.vtiles, wt, wf)
+    if (d == 64) {
+      if (p.kx == kValBF16) SFA_PREP(64, kValBF16);
+      else if (p.kx == kValF16) SFA_PREP(64, kValF16);
+      else SFA_PREP(64, 0);
+    } else {
+      if (p.kx == kValBF16) SFA_PREP(128, kValBF16);
+      else if (p.kx == kValF16) SFA_PREP(128, kValF16);
+      else SFA_PREP(128, 0);
+    }
+#undef SFA_PREP
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
