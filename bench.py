@@ -246,12 +246,13 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
     return out
 
 
-def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0):
+def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
     """One step = sfa_attn_bwd (codes, O, LSE and dO resident in HBM)."""
     q, k, v = _fwd_inputs(w)
     B, Hq, Hkv, n, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
-    qi, qv = sfa.sfa_topk_encode(q, kk)
-    ki, kv = sfa.sfa_topk_encode(k, kk)
+    idt, vdt = FWD_CODE_FORMATS[codes]
+    qi, qv = sfa.sfa_topk_encode(q, kk, idx_dtype=idt, val_dtype=vdt)
+    ki, kv = sfa.sfa_topk_encode(k, kk, idx_dtype=idt, val_dtype=vdt)
     o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale,
                               o_dtype=torch.bfloat16, window=window, n_global=n_global)
     dout = torch.empty((B, Hq, n, d), dtype=torch.bfloat16, device=DEV)
@@ -288,7 +289,8 @@ def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0):
     algo = 4.0 * d * pairs + 6.0 * E
     out = {
         "metric": "SFA bwd (straight-through estimator) tokens/s at n=32K,d=128,k=16" +
-                  (f"; sliding window {window} + {n_global} global tokens" if window else ""),
+                  (f"; sliding window {window} + {n_global} global tokens" if window else "") +
+                  (f"; codes stored as {_CODE_NAMES[codes]}" if codes != "i32f32" else ""),
         "value": B * n / (ms_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -304,8 +306,10 @@ def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0):
             "workload": w.name, "B": B, "Hq": Hq, "Hkv": Hkv, "n": n, "d": d, "k": kk,
             "causal": w.causal, "seed": w.seed, "window": window, "n_global": n_global,
             "step": "sfa_attn_bwd",
-            "precision": "O and dO bf16; products on MFMA with bf16 hi/lo pieces (3 terms), "
-                         "fp32 accumulate; gradients fp32",
+            "codes": codes,
+            "precision": "O and dO bf16; products on MFMA with bf16 hi/lo pieces (3 terms; "
+                         "pieces that are zero, as for bf16 values, left out), fp32 accumulate; "
+                         "gradients fp32",
         },
         "roofline": {
             "kernel": "sfa_bwd_dq_kernel + sfa_bwd_dkv_kernel (+ tile images)",
@@ -322,7 +326,7 @@ def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0):
         },
         "wall_s_timed": wall,
     }
-    if want_cpu and window == 0:
+    if want_cpu and window == 0 and codes == "i32f32":
         out["cpu_baseline"] = cpu_baseline_bwd(w, q, k, v, dout)
     return out
 
@@ -632,7 +636,7 @@ def main():
     torch.cuda.set_device(0)
     w = si.workload(args.workload)
     codes = args.codes or ("i16bf16" if w.kind == "decode" else "i32f32")
-    if (w.kind == "decode" and codes not in CODE_FORMATS) or (args.which == "bwd" and codes != "i32f32"):
+    if w.kind == "decode" and codes not in CODE_FORMATS:
         print(f"--codes {codes} is not measured for this workload / pass", file=sys.stderr)
         sys.exit(2)
     if w.kind == "decode" and args.cache == "paged":
@@ -642,7 +646,7 @@ def main():
                            args.window, args.n_global)
     elif args.which == "bwd":
         out = bench_bwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
-                        args.n_global)
+                        args.n_global, codes)
     else:
         out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
                         args.n_global, codes)

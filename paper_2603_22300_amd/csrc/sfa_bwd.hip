@@ -10,7 +10,9 @@
 // the products run on the matrix cores on densified codes; every operand is
 // split into two bf16 pieces x = x0 + x1 and each product keeps the three
 // terms a0 b0 + a0 b1 + a1 b0 (relative error ~2^-16 of sum |a b|), with
-// float32 accumulation.
+// float32 accumulation.  An operand stored in bf16 (V, dO, and the code
+// values when they are bf16: CEX) has a zero low piece, so the products with
+// that piece are left out; the sums are unchanged (they only added zeros).
 //
 // Kernels (all on the caller's stream):
 //   sfa_bwd_qprep_kernel  per (batch, query head, 32-row tile): an image of
@@ -279,8 +281,9 @@ __device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, i
 // dq: query-parallel
 // ---------------------------------------------------------------------------
 
-// VEX / OEX: V / dO are stored in bf16, so their low pieces are zero.
-template <int D, bool VEX, bool OEX>
+// VEX / OEX / CEX: V / dO / the code values are stored in bf16, so their
+// low pieces are zero.
+template <int D, bool VEX, bool OEX, bool CEX>
 __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
   using I = Img<D>;
   constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
@@ -374,7 +377,7 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
         }
         const bf16x8 qq[2] = {qB[0][kb], qB[1][kb]};
         const bf16x8 gg[2] = {dB[0][kb], dB[1][kb]};
-        mfma3(s, a, qq);               // S^T = K~ Q~^T   (keys x queries)
+        mfma3<!CEX, !CEX>(s, a, qq);   // S^T = K~ Q~^T   (keys x queries)
         mfma3<!VEX, !OEX>(dp, v, gg);  // dP^T = V dO^T
       }
       // dS^T = P^T o (dP^T - D); lane = query my_i, register r = key j0 + 8(r/4) + 4hh + r%4
@@ -418,7 +421,7 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           const bf16x8 a[2] = {tr_load(trk, db * 32 + l32, kbase), tr_load(trk, D + db * 32 + l32, kbase)};
-          mfma3(acc[db], a, dsb[kk]);
+          mfma3<!CEX, true>(acc[db], a, dsb[kk]);
         }
       }
     }
@@ -461,7 +464,7 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
 // recompute S.
 constexpr int kDV = 0, kDK = 1;
 
-template <int D, bool VEX, bool OEX, int PART>
+template <int D, bool VEX, bool OEX, bool CEX, int PART>
 __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   using I = Img<D>;
   constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
@@ -565,7 +568,7 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
 #pragma unroll
         for (int pc = 0; pc < 2; ++pc) a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
         const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
-        mfma3(s, a, kk2);  // S = Q~ K~^T   (queries x keys)
+        mfma3<!CEX, !CEX>(s, a, kk2);  // S = Q~ K~^T   (queries x keys)
         if constexpr (PART == kDK) {
           bf16x8 g[2];
 #pragma unroll
@@ -629,7 +632,7 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
         for (int db = 0; db < NDB; ++db) {
           const bf16x8 at[2] = {tr_load(tra, db * 32 + l32, kbase), tr_load(tra, D + db * 32 + l32, kbase)};
           if constexpr (PART == kDV) mfma3<!OEX, true>(acc[db], at, xb[kk]);
-          else mfma3(acc[db], at, xb[kk]);
+          else mfma3<!CEX, true>(acc[db], at, xb[kk]);
         }
       }
     }
@@ -677,16 +680,16 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   }
 }
 
-template <int D, bool VEX, bool OEX>
+template <int D, bool VEX, bool OEX, bool CEX>
 hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   using I = Img<D>;
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipSuccess;
     const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
-                          (const void*)sfa_bwd_dq_kernel<D, VEX, OEX>,
-                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, kDV>,
-                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, kDK>};
+                          (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>,
+                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>,
+                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>};
     const int bytes[5] = {I::QB, I::KB, 2 * I::KB, kQS * I::DV_LEN, kQS * I::DK_LEN};
     for (int f = 0; f < 5 && e == hipSuccess; ++f)
       if (bytes[f] > 65536) e = hipFuncSetAttribute(fns[f], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[f]);
@@ -700,12 +703,12 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   const dim3 blk(256);
   hipLaunchKernelGGL(sfa_bwd_qprep_kernel<D>, dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
   hipLaunchKernelGGL(sfa_bwd_kprep_kernel<D>, dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
-  hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX>), dim3(p.nqb, B * p.Hkv), dim3(kNWQ * 64),
+  hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX, CEX>), dim3(p.nqb, B * p.Hkv), dim3(kNWQ * 64),
                      2 * I::KB, stream, p);
   const int nkb = (p.n + kNW * kT - 1) / (kNW * kT);
-  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, kDV>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
                      kQS * I::DV_LEN, stream, p);
-  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, kDK>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
                      kQS * I::DK_LEN, stream, p);
   return hipGetLastError();
 }
@@ -742,12 +745,16 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
   const size_t qbytes = (size_t)B * Hq * p.nt * (d == 64 ? Img<64>::QB : Img<128>::QB);
   p.qimg = (unsigned char*)ws;
   p.kimg = (unsigned char*)ws + qbytes;
+  // bf16 code values (exact in one bf16 piece) with bf16 V, O and dO
+  const bool cex = vfmt == kValBF16 && vbf16 && obf16;
   if (d == 64) {
-    if (vbf16) return obf16 ? launch_d<64, true, true>(p, B, stream) : launch_d<64, true, false>(p, B, stream);
-    return obf16 ? launch_d<64, false, true>(p, B, stream) : launch_d<64, false, false>(p, B, stream);
+    if (cex) return launch_d<64, true, true, true>(p, B, stream);
+    if (vbf16) return obf16 ? launch_d<64, true, true, false>(p, B, stream) : launch_d<64, true, false, false>(p, B, stream);
+    return obf16 ? launch_d<64, false, true, false>(p, B, stream) : launch_d<64, false, false, false>(p, B, stream);
   }
-  if (vbf16) return obf16 ? launch_d<128, true, true>(p, B, stream) : launch_d<128, true, false>(p, B, stream);
-  return obf16 ? launch_d<128, false, true>(p, B, stream) : launch_d<128, false, false>(p, B, stream);
+  if (cex) return launch_d<128, true, true, true>(p, B, stream);
+  if (vbf16) return obf16 ? launch_d<128, true, true, false>(p, B, stream) : launch_d<128, true, false, false>(p, B, stream);
+  return obf16 ? launch_d<128, false, true, false>(p, B, stream) : launch_d<128, false, false, false>(p, B, stream);
 }
 
 }  // namespace sfa

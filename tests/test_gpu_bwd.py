@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
-def _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, o_bf16=False):
+def _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, o_bf16=False, val_dtype=torch.float32):
     q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed,
                             v_dtype=torch.bfloat16 if v_bf16 else torch.float32, device=DEV)
     odt = torch.bfloat16 if o_bf16 else torch.float32
@@ -30,14 +30,15 @@ def _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, o_bf16=False):
         for h in range(Hq):
             dout[b, h] = si.normal((n, d), seed, "dout", b, h, device=DEV)
     dout = dout.to(odt)
-    qi, qv = sfa.sfa_topk_encode(q, k)
-    ki, kv = sfa.sfa_topk_encode(kk, k)
+    qi, qv = sfa.sfa_topk_encode(q, k, val_dtype=val_dtype)
+    ki, kv = sfa.sfa_topk_encode(kk, k, val_dtype=val_dtype)
     scale = 1.0 / math.sqrt(d)
     o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=odt)
     dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale)
     torch.cuda.synchronize()
-    oqi, oqv = oracle.topk_encode(q.cpu().numpy(), k)
-    oki, okv = oracle.topk_encode(kk.cpu().numpy(), k)
+    enc = oracle.topk_encode_bf16 if val_dtype == torch.bfloat16 else oracle.topk_encode
+    oqi, oqv = enc(q.cpu().numpy(), k)
+    oki, okv = enc(kk.cpu().numpy(), k)
     # the GPU and oracle codes are bit-identical (encoder parity), so the
     # gradients line up entry by entry
     assert np.array_equal(qi.cpu().numpy(), oqi) and np.array_equal(ki.cpu().numpy(), oki)
@@ -81,6 +82,37 @@ def test_other_head_dims(B, Hq, Hkv, n, d, k, causal, v_bf16, o_bf16):
 
 def test_bf16_output_and_grad():
     _run(1, 4, 2, 150, 128, 16, True, True, seed=21, o_bf16=True)
+
+
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,o_bf16",
+    [
+        (1, 4, 2, 150, 128, 16, True, True),   # bf16 codes, V, O, dO: one-piece code products
+        (2, 4, 1, 161, 64, 16, True, True),
+        (1, 2, 2, 130, 128, 32, False, True),
+        (1, 4, 2, 150, 128, 16, True, False),  # float32 O and dO: the piece path
+    ])
+def test_bf16_codes(B, Hq, Hkv, n, d, k, causal, o_bf16):
+    _run(B, Hq, Hkv, n, d, k, causal, True, seed=3 * n + d, o_bf16=o_bf16,
+         val_dtype=torch.bfloat16)
+
+
+def test_bf16_codes_match_widened_codes():
+    """bf16 code values have a zero low bf16 piece, so the backward leaves
+    their piece products out.  The same values widened to float32 take the
+    general path, which adds those products as exact zeros: every gradient
+    must be bitwise the same."""
+    B, Hq, Hkv, n, d, k = 1, 8, 2, 300, 128, 16
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, 17, v_dtype=torch.bfloat16, device=DEV)
+    dout = si.normal((B, Hq, n, d), 17, "dout", device=DEV).to(torch.bfloat16)
+    qi, qv = sfa.sfa_topk_encode(q, k, val_dtype=torch.bfloat16)
+    ki, kv = sfa.sfa_topk_encode(kk, k, val_dtype=torch.bfloat16)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.bfloat16)
+    a = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout)
+    b = sfa.sfa_attn_bwd(qi, qv.float(), ki, kv.float(), v, o, lse, dout)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
 
 
 def test_deterministic():
