@@ -120,8 +120,8 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * matrix cores, each value split into bfloat16 pieces whose products are
  * exact in float32 (bf16 V: three piece products, relative error ~2^-16 of
  * sum |q_u k_u|; float32 V: six, ~2^-24); softmax and accumulation in
- * float32.  16-bit code values (SFA_BF16 or SFA_F16) with bf16 V, k <= 16
- * and a nonzero scale: the raw query and key values are the matrix-core
+ * float32.  16-bit code values (SFA_BF16 or SFA_F16) with bf16 V and a
+ * nonzero scale: the raw query and key values are the matrix-core
  * operands (bf16 or float16 products, exact in float32, one per coordinate
  * block), the sign of scale is folded into the query values and |scale| is
  * applied to the float32 scores.  With bf16 V, V is converted to float16

@@ -16,7 +16,7 @@
 // score keeps the terms q0k0 + q0k1 + q1k0 (relative error ~2^-16 of
 // sum|q_u k_u|); with float32 V it keeps every term of order <= 2
 // (q0k0 + q0k1 + q1k0 + q0k2 + q1k1 + q2k0, ~2^-24).
-// 16-bit codes (bf16 or float16 values) with bf16 V and k <= 16: the raw
+// 16-bit codes (bf16 or float16 values) with bf16 V: the raw
 // values are already MFMA operands, so each 16-coordinate block of the score
 // is one exact product on the matrix cores (bf16 or float16 MFMA), and the
 // float32 score is multiplied by |scale| * log2(e) before exp2 (the sign of
@@ -180,7 +180,7 @@ constexpr uint32_t kHandBack32 = 0x7fa5a5a5u;
 template <int D, bool VBF16, int NW, int KM, bool SAFE, int KX = 0>
 __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, const int bh) {
   static_assert(VBF16 || !SAFE, "the rerun is for bf16 V");
-  static_assert(KX == 0 || (VBF16 && !SAFE && KM <= 16), "16-bit codes: bf16 V, k <= 16");
+  static_assert(KX == 0 || (VBF16 && !SAFE), "16-bit codes: bf16 V");
   constexpr int NT = NW * 64;
   constexpr int R = NW * 32;
   constexpr int NP = n_pieces<VBF16, KX>();
@@ -1043,8 +1043,12 @@ hipError_t launch_nw(FwdParams p, int B, hipStream_t stream) {
   p.BR = NW * 32 / p.G;
   p.nqb = (p.n + p.BR - 1) / p.BR;
   if constexpr (VBF16) {
-    if (p.kx == kValBF16) return launch_km<D, true, NW, 16, kValBF16>(p, B, stream);
-    if (p.kx == kValF16) return launch_km<D, true, NW, 16, kValF16>(p, B, stream);
+    if (p.kx == kValBF16)
+      return p.k <= 16 ? launch_km<D, true, NW, 16, kValBF16>(p, B, stream)
+                       : launch_km<D, true, NW, 128, kValBF16>(p, B, stream);
+    if (p.kx == kValF16)
+      return p.k <= 16 ? launch_km<D, true, NW, 16, kValF16>(p, B, stream)
+                       : launch_km<D, true, NW, 128, kValF16>(p, B, stream);
   }
   return p.k <= 16 ? launch_km<D, VBF16, NW, 16, 0>(p, B, stream)
                    : launch_km<D, VBF16, NW, 128, 0>(p, B, stream);
@@ -1082,9 +1086,9 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
   p.window = window; p.n_global = n_global;
   p.scale_log2 = (float)((double)scale * 1.4426950408889634);
   p.ifmt = ifmt; p.vfmt = vfmt; p.obf16 = obf16;
-  // 16-bit code values with bf16 V and k <= 16 take the one-product score
-  // path (a zero scale keeps the piece path: its scores are all zero)
-  p.kx = vbf16 && vfmt != kValF32 && k <= 16 && scale != 0.f ? vfmt : 0;
+  // 16-bit code values with bf16 V take the one-product score path (a zero
+  // scale keeps the piece path: its scores are all zero)
+  p.kx = vbf16 && vfmt != kValF32 && scale != 0.f ? vfmt : 0;
   p.kx_scale = (float)(fabs((double)scale) * 1.4426950408889634);
   p.qsign = scale < 0.f ? 0x8000u : 0u;
   p.G = Hq / Hkv;

@@ -1,9 +1,8 @@
 """GPU parity of the forward on 16-bit codes (bfloat16 or float16 values, the
 code storage of App. J and of the decode cache) with bf16 V.
 
-With k <= 16 these take the one-product score path: the raw query and key
-values are the matrix-core operands and the scale is applied to the float32
-scores.  The oracle codes the same dense inputs with its own Top-k, rounds the
+These take the one-product score path: the raw query and key values are the
+matrix-core operands and the scale is applied to the float32 scores.  The oracle codes the same dense inputs with its own Top-k, rounds the
 kept values to the same 16-bit type and evaluates the plain definition in
 float64.  Tolerances as for every bf16-V forward: O 5e-3, LSE 1e-4."""
 import math
@@ -60,7 +59,9 @@ def _case(B, Hq, Hkv, n, d, k, causal, val_dtype, seed, idx_dtype=torch.int32, s
         (1, 16, 1, 70, 64, 8, True, F16),      # 16 heads per KV head
         (1, 8, 2, 700, 128, 16, True, BF16),   # GQA 4:1 over eleven key tiles
         (1, 8, 2, 700, 128, 16, True, F16),
-        (1, 2, 2, 140, 128, 32, True, F16),    # k > 16: the piece path
+        (1, 2, 2, 140, 128, 32, True, F16),    # k > 16
+        (1, 4, 1, 333, 128, 128, True, BF16),  # k = d: dense attention
+        (1, 2, 2, 200, 64, 40, False, F16),    # d = 64, k = 40, non-causal
     ])
 def test_shapes(B, Hq, Hkv, n, d, k, causal, val_dtype):
     _case(B, Hq, Hkv, n, d, k, causal, val_dtype, seed=B * 1000 + Hq * 100 + n + 5)
