@@ -46,9 +46,11 @@ def test_fwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
     check_lse(lse, L, f"fwd window {w} global {g} LSE")
 
 
-def test_fwd_window_qwen3_32k_sampled():
+@pytest.mark.parametrize("val_dtype", [torch.float32, torch.bfloat16])
+def test_fwd_window_qwen3_32k_sampled(val_dtype):
     """The 32K GQA workload with a 4096-token window and 4 global tokens: all
-    rows on the GPU, sampled rows of two heads by the oracle."""
+    rows on the GPU, sampled rows of two heads by the oracle (32-bit codes, and
+    bf16 codes on the one-product score path)."""
     w_ = si.workload("qwen3_32k")
     B, Hq, Hkv, n, d, k, G = w_.B, w_.Hq, w_.Hkv, w_.n, w_.d, w_.k, w_.G
     win, ng = 4096, 4
@@ -60,16 +62,16 @@ def test_fwd_window_qwen3_32k_sampled():
     for h in range(Hkv):
         kk[0, h] = si.normal((n, d), w_.seed, "k", 0, h, device=DEV)
         v[0, h] = si.normal((n, d), w_.seed, "v", 0, h, device=DEV).to(torch.bfloat16)
-    qi, qv = sfa.sfa_topk_encode(q, k)
-    ki, kv = sfa.sfa_topk_encode(kk, k)
+    qi, qv = sfa.sfa_topk_encode(q, k, val_dtype=val_dtype)
+    ki, kv = sfa.sfa_topk_encode(kk, k, val_dtype=val_dtype)
     o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=w_.scale,
                               o_dtype=torch.float32, window=win, n_global=ng)
     torch.cuda.synchronize()
     rows = sample_rows(n, extra=[3, 4, win - 1, win, win + 63, 20000], count=12, seed=4)
     for h in (0, 13):
         g = h // G
-        ref = oracle.attn_fwd_rows(qi[0, h].cpu().numpy(), qv[0, h].cpu().numpy(),
-                                   ki[0, g].cpu().numpy(), kv[0, g].cpu().numpy(),
+        ref = oracle.attn_fwd_rows(qi[0, h].cpu().numpy(), np_vals(qv[0, h]),
+                                   ki[0, g].cpu().numpy(), np_vals(kv[0, g]),
                                    np_vals(v[0, g]), d, w_.scale, True, rows, window=win,
                                    n_global=ng)
         sel = torch.from_numpy(rows).to(DEV)
