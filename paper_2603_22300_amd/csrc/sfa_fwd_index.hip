@@ -6,12 +6,15 @@
 // Workgroup = 4 wavefronts = 128 query rows: the G query heads of one KV
 // head times BR = 128 / G positions, so all G heads share every key tile.
 // Per key tile of BC = 64 keys:
-//   1. the tile's BC*k key codes are counting-sorted by coordinate into an
-//      LDS inverted index (koff[u] .. koff[u+1] lists the keys holding u);
-//   2. every query nonzero (u, q_u) -- the workgroup's query codes were
-//      bucketed by coordinate once, at the start -- walks the keys of its
-//      coordinate's bucket and adds q_u * k_u into the LDS score tile with a
-//      float atomic (ds_add_f32), so only overlapping coordinates cost work;
+//   1. the tile's BC*k key codes are counting-sorted into an LDS inverted
+//      index by (coordinate u, key parity): bucket 2u + p lists the keys of
+//      parity p that hold u;
+//   2. thread (row r, parity p) walks, for each nonzero (u, q_u) of row r,
+//      bucket 2u + p and adds q_u * k_u into the score tile's entry
+//      (key, r), so only overlapping coordinates cost work.  Each score entry
+//      has one owner thread: the adds are plain LDS read-modify-writes, in
+//      program order, with no atomics (LDS float atomics run at a fraction
+//      of a lane per clock);
 //   3. each wavefront reads its 32 rows of the score tile in the register
 //      layout of the MFMA B operand, applies scale and the causal mask, runs
 //      the online-softmax update (base-2 exponent, scale * log2(e) folded),
@@ -30,7 +33,7 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRows = 32 * kWaves;  // query rows per workgroup
 constexpr int kBC = 64;             // keys per tile
-constexpr int kSP = kBC + 4;        // score-tile row pitch (floats)
+constexpr int kSP = kRows + 4;      // score tile [key][row]: key pitch (floats)
 constexpr int kVP = kBC + 8;        // transposed-V row pitch (bf16)
 constexpr int kMaxK = 64;           // largest supported k
 
@@ -57,11 +60,11 @@ template <int D, bool VBF16>
 __host__ __device__ inline FwdLds fwd_lds_layout(int k) {
   FwdLds L;
   int off = 0;
-  L.s_off = off;    off += kRows * kSP * 4;
+  L.s_off = off;    off += kBC * kSP * 4;
   L.qent_off = off; off += kRows * k * 8;
   L.kent_off = off; off += kBC * k * 8;
-  L.cnt_off = off;  off += (D + 1) * 4;
-  L.koff_off = off; off += (D + 1) * 4;
+  L.cnt_off = off;  off += (2 * D + 1) * 4;
+  L.koff_off = off; off += (2 * D + 1) * 4;
   off = (off + 15) & ~15;
   L.v_off = off;    off += VBF16 ? D * kVP * 2 : kBC * D * 4;
   L.total = off;
@@ -112,55 +115,33 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
   const int i0 = qb * p.BR;
   const int n = p.n;
 
-  // ---------------- bucket the workgroup's query codes by coordinate -------
-  // row rho in [0, kRows): query head hkv*G + rho / BR, position i0 + rho % BR
-  for (int f = tid; f <= D; f += kThreads) cnt[f] = 0;
-  __syncthreads();
+  // ---------------- the workgroup's query codes, per row -------------------
+  // row rho in [0, kRows): query head hkv*G + rho / BR, position i0 + rho % BR;
+  // qent[rho * k + t] = (coordinate, value) of its t-th nonzero (rows past n:
+  // value 0)
   const int nqe = kRows * k;
-  // first pass: count; remember (slot) in registers for the second pass
-  constexpr int kQE = kRows * KM / kThreads;
-  constexpr int kKE = kBC * KM / kThreads;
-  int q_slot[kQE];
-  int q_f[kQE];
-#pragma unroll
-  for (int r = 0; r < kQE; ++r) {
-    const int e = tid + r * kThreads;
-    q_slot[r] = -1;
-    q_f[r] = 0;
-    if (e < nqe) {
-      const int rho = (int)(((float)e + 0.5f) * p.inv_k);
-      const int t = e - rho * k;
-      const int hq = hkv * p.G + rho / p.BR;
-      const int i = i0 + rho % p.BR;
-      if (i < n) {
-        const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
-        const int f = load_idx(p.q_idx, gi, p.ifmt, dmask);
-        q_f[r] = f;
-        q_slot[r] = (int)atomicAdd(&cnt[f], 1u);
-      }
-    }
-  }
-  __syncthreads();
-  if (wave == 0) bucket_offsets<D>(cnt, koff, lane);
-  __syncthreads();
-  const int nq_total = (int)koff[D];
-#pragma unroll
-  for (int r = 0; r < kQE; ++r) {
-    const int e = tid + r * kThreads;
-    if (e < nqe && q_slot[r] >= 0) {
-      const int rho = (int)(((float)e + 0.5f) * p.inv_k);
-      const int t = e - rho * k;
-      const int hq = hkv * p.G + rho / p.BR;
-      const int i = i0 + rho % p.BR;
+  for (int e = tid; e < nqe; e += kThreads) {
+    const int rho = (int)(((float)e + 0.5f) * p.inv_k);
+    const int t = e - rho * k;
+    const int hq = hkv * p.G + rho / p.BR;
+    const int i = i0 + rho % p.BR;
+    uint2 qe = make_uint2(0u, 0u);
+    if (i < n) {
       const int64_t gi = (((int64_t)b * p.Hq + hq) * n + i) * k + t;
-      const float qv = load_val(p.q_val, gi, p.vfmt);
-      const uint32_t rowbyte = (uint32_t)(rho * kSP * 4);
-      qent[koff[q_f[r]] + q_slot[r]] = make_uint2(rowbyte | ((uint32_t)q_f[r] << 16), __float_as_uint(qv));
+      qe = make_uint2((uint32_t)load_idx(p.q_idx, gi, p.ifmt, dmask),
+                      __float_as_uint(load_val(p.q_val, gi, p.vfmt)));
     }
+    qent[e] = qe;
   }
   // zero the score tile
-  for (int x = tid; x < kRows * kSP; x += kThreads) S[x] = 0.f;
+  for (int x = tid; x < kBC * kSP; x += kThreads) S[x] = 0.f;
   __syncthreads();
+  static_assert(kThreads == 2 * kRows, "two threads (key parities) per row");
+  constexpr int kKE = kBC * KM / kThreads;  // key code entries per thread and tile
+  // score-phase ownership: row sr, key parity spar
+  const int sr = tid & (kRows - 1);
+  const int spar = tid / kRows;
+  float* Scol = S + sr;  // entry (key c, row sr) at Scol[c * kSP]
 
   // ---------------- per-wave row state (MFMA B-operand layout) ------------
   const int hh = lane >> 5;               // which 8-key half of each 16-key block
@@ -224,8 +205,8 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
       }
     }
 
-    // ---- inverted index of the key tile: count ----
-    for (int f = tid; f <= D; f += kThreads) cnt[f] = 0;
+    // ---- inverted index of the key tile by (coordinate, key parity): count ----
+    for (int f = tid; f <= 2 * D; f += kThreads) cnt[f] = 0;
     __syncthreads();
     int k_slot[kKE], k_f[kKE];
     float k_v[kKE];
@@ -242,14 +223,14 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
         const int j = j0 + c;
         if (j < n) {
           const int64_t gi = (kv_base + j) * k + t;
-          k_f[r] = load_idx(p.k_idx, gi, p.ifmt, dmask);
+          k_f[r] = 2 * load_idx(p.k_idx, gi, p.ifmt, dmask) + (c & 1);
           k_v[r] = load_val(p.k_val, gi, p.vfmt);
           k_slot[r] = (int)atomicAdd(&cnt[k_f[r]], 1u);
         }
       }
     }
     __syncthreads();
-    if (wave == 0) bucket_offsets<D>(cnt, koff + 0, lane);
+    if (wave == 0) bucket_offsets<2 * D>(cnt, koff, lane);
     __syncthreads();
     // ---- place entries: (column byte offset, value) ----
 #pragma unroll
@@ -257,37 +238,43 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
       const int e = tid + r * kThreads;
       if (k_slot[r] >= 0) {
         const int c = (int)(((float)e + 0.5f) * p.inv_k);
-        kent[koff[k_f[r]] + k_slot[r]] = make_uint2((uint32_t)(c * 4), __float_as_uint(k_v[r]));
+        kent[koff[k_f[r]] + k_slot[r]] = make_uint2((uint32_t)(c * kSP), __float_as_uint(k_v[r]));
       }
     }
     __syncthreads();
 
-    // ---- overlap scores: query nonzero x keys of its coordinate ----
-    for (int e = tid; e < nq_total; e += kThreads) {
-      const uint2 qe = qent[e];
-      const int f = (int)(qe.x >> 16) & 0xff;
-      const uint32_t rowbyte = qe.x & 0xffffu;
+    // ---- overlap scores: each (row, parity) thread walks its row's buckets ----
+    // A bucket holds a key at most once, so its four reads and four writes
+    // touch distinct entries; a key met again under a later coordinate is
+    // read after the earlier write (LDS operations of a wave run in order).
+    for (int t = 0; t < k; ++t) {
+      const uint2 qe = qent[sr * k + t];
       const float qv = __uint_as_float(qe.y);
-      const int p0 = (int)koff[f], p1 = (int)koff[f + 1];
-      for (int q = p0; q < p1; ++q) {
-        const uint2 ke = kent[q];
-        atomicAdd((float*)((unsigned char*)S + rowbyte + ke.x), qv * __uint_as_float(ke.y));
+      const int bk = 2 * (int)qe.x + spar;
+      const int p0 = (int)koff[bk], p1 = (int)koff[bk + 1];
+      for (int q = p0; q < p1; q += 4) {
+        uint2 ke[4];
+        float sv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) ke[u] = kent[min(q + u, p1 - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) sv[u] = Scol[ke[u].x];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (q + u < p1) Scol[ke[u].x] = fmaf(qv, __uint_as_float(ke[u].y), sv[u]);
       }
     }
     __syncthreads();
 
     // ---- online softmax on this wave's 32 rows, then P.V ----
-    float* Srow = S + rho * kSP;
+    float* Srow = S + rho;  // entry (key c, row rho) at Srow[c * kSP]
     const bool wave_active = !p.causal || wave_i_max >= j0;
     if (wave_active) {
       float t[4][8];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        float4 a = *(float4*)(Srow + kb * 16 + 8 * hh);
-        float4 c = *(float4*)(Srow + kb * 16 + 8 * hh + 4);
-        t[kb][0] = a.x; t[kb][1] = a.y; t[kb][2] = a.z; t[kb][3] = a.w;
-        t[kb][4] = c.x; t[kb][5] = c.y; t[kb][6] = c.z; t[kb][7] = c.w;
-      }
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t[kb][e] = Srow[(kb * 16 + 8 * hh + e) * kSP];
       float mt = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
@@ -348,10 +335,9 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
     }
     // clear this wave's rows of the score tile for the next key tile
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      *(float4*)(Srow + kb * 16 + 8 * hh) = make_float4(0.f, 0.f, 0.f, 0.f);
-      *(float4*)(Srow + kb * 16 + 8 * hh + 4) = make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Srow[(kb * 16 + 8 * hh + e) * kSP] = 0.f;
     __syncthreads();  // V tile and score tile are reused by the next key tile
   }
 

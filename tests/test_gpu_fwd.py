@@ -260,13 +260,14 @@ def test_deterministic():
 
 
 def test_index_variant_repeatable():
-    # the inverted-index variant accumulates with LDS float atomics, whose
-    # order may vary between runs; two runs agree far inside the tolerance
+    # the inverted-index variant: the order of keys inside a bucket may vary
+    # between runs (the counting sort takes slots with atomics), but every
+    # score entry has one owner that adds its overlaps in the row's code
+    # order, so the results are bitwise repeatable
     q, kk, v = si.dense_qkv(1, 4, 1, 500, 128, 9, device=DEV)
     qi, qv = _gpu_codes(q, 16)
     ki, kv = _gpu_codes(kk, 16)
     o1, l1 = sfa.sfa_attn_fwd_index(qi, qv, ki, kv, v, o_dtype=torch.float32)
     o2, l2 = sfa.sfa_attn_fwd_index(qi, qv, ki, kv, v, o_dtype=torch.float32)
     torch.cuda.synchronize()
-    assert (o1 - o2).abs().max().item() < 1e-5
-    assert (l1 - l2).abs().max().item() < 1e-5
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
