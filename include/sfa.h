@@ -162,13 +162,14 @@ size_t sfa_attn_fwd_workspace(int B, int Hkv, int n, int d, int v_t);
 /*
  * The same forward with the overlap scores accumulated through a per-key-tile
  * inverted index in LDS (Sec. 3.2's feature-intersection formulation): the
- * tile's key codes are counting-sorted by coordinate and each query nonzero
- * adds q_u * k_u into the score tile for exactly the keys holding its
- * coordinate.  Same arguments (without the workspace) and definitions as
- * sfa_attn_fwd; the scores agree up to float32 summation order, and with bf16
- * V the probabilities enter P.V as a single bfloat16 (relative rounding 2^-9
- * per weight).  Slower on this hardware; kept as the direct realisation of
- * the overlap formulation.
+ * tile's key codes are counting-sorted by (coordinate, key parity), and for
+ * each nonzero (u, q_u) of a query row the row's two owner threads add
+ * q_u * k_u into the score tile for exactly the keys holding u.  Same
+ * arguments (without the workspace) and definitions as sfa_attn_fwd; the
+ * scores agree up to float32 summation order, and with bf16 V the
+ * probabilities enter P.V as a single bfloat16 (relative rounding 2^-9 per
+ * weight).  Results are bitwise repeatable.  Slower on this hardware than
+ * sfa_attn_fwd; kept as the direct realisation of the overlap formulation.
  * Limits: as sfa_attn_fwd with d in {64, 128}, plus k <= 64, Hq / Hkv <= 128,
  * and the per-tile tables must fit LDS (SFA_ENOTSUP otherwise).
  */
