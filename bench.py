@@ -24,6 +24,7 @@ Prints ONE JSON line.  Besides the contract fields it carries
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -134,7 +135,7 @@ def _overlap_count(qi: torch.Tensor, ki: torch.Tensor, d: int, G: int, causal: b
     return E
 
 
-def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
+def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32", fwd="default"):
     q, k, v = _fwd_inputs(w)
     B, Hq, Hkv, n, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
     idt, vdt = FWD_CODE_FORMATS[codes]
@@ -153,8 +154,11 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
         sfa.sfa_topk_encode(k, kk, idx=ki, val=kv)
         if ev is not None:
             ev[0].record()
-        sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse, ws=ws,
-                         window=window, n_global=n_global)
+        if fwd == "index":
+            sfa.sfa_attn_fwd_index(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse)
+        else:
+            sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=w.causal, scale=w.scale, o=o, lse=lse,
+                             ws=ws, window=window, n_global=n_global)
         if ev is not None:
             ev[1].record()
 
@@ -176,6 +180,7 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
     fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
     fwd_avg = float(np.mean(fwd_ms))
     enc_avg = float(np.mean([e[2].elapsed_time(e[0]) for e in evs]))
+    step_ms = [e[2].elapsed_time(e[1]) for e in evs]
 
     pairs = B * Hq * _allowed_pairs(n, w.causal, window, n_global)
     pv_flops = 2.0 * d * pairs          # P.V: 2 d flops per allowed pair
@@ -184,6 +189,10 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
     achieved = algo_flops / (fwd_avg * 1e-3)
     tokens = B * n
     metric = METRIC if window == 0 else METRIC + f"; sliding window {window} + {n_global} global tokens"
+    if kk != 16 and w.name == "qwen3_32k":
+        metric = metric.replace("k=16", f"k={kk}")
+    if fwd == "index":
+        metric += "; inverted-index forward (sfa_attn_fwd_index)"
     if codes != "i32f32":
         metric += f"; codes stored as {_CODE_NAMES[codes]}"
         precision = (f"codes {_CODE_NAMES[codes]}; scores fp32 (one exact {vdt_name(vdt)} MFMA product "
@@ -214,14 +223,16 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
             "precision": precision,
         },
         "roofline": {
-            "kernel": "sfa_fwd_kernel",
+            "kernel": "sfa_fwd_index_kernel" if fwd == "index" else "sfa_fwd_kernel",
             "bound": "mfma",
             "achieved": achieved / 1e12,
             "peak": PEAK_MFMA_BF16 / 1e12,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_MFMA_BF16,
             # the committed counter summary is of the fp32-code forward
-            "traffic": _traffic("sfa_fwd.hip", w.name) if codes == "i32f32" and window == 0 else None,
+            "traffic": (_traffic("sfa_fwd.hip", w.name)
+                        if codes == "i32f32" and window == 0 and fwd == "default" and kk == 16
+                        else None),
             "algorithmic_flops_per_launch": algo_flops,
             "pv_flops_per_launch": pv_flops,
             "fwd_ms_avg": fwd_avg,
@@ -239,9 +250,11 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
             "fwd_ms": fwd_avg,
             "fwd_tokens_per_s": tokens / (fwd_avg * 1e-3),
         },
+        # per-step distribution (each step bracketed by its own events)
+        "timing": {"step": _pstats(step_ms), "fwd_call": _pstats(fwd_ms)},
         "wall_s_timed": wall,
     }
-    if want_cpu and window == 0 and codes == "i32f32":
+    if want_cpu and window == 0 and codes == "i32f32" and fwd == "default":
         out["cpu_baseline"] = cpu_baseline_fwd(w, q, k, v)
     return out
 
@@ -324,6 +337,7 @@ def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
             "overlap_products_E": E,
             "ms_min": float(np.min(ms)),
         },
+        "timing": {"step": _pstats(ms)},
         "wall_s_timed": wall,
     }
     if want_cpu and window == 0 and codes == "i32f32":
@@ -370,6 +384,13 @@ def _fwd_bytes(w, idt=torch.int32, vdt=torch.float32):
     entry = torch.empty((), dtype=idt).element_size() + torch.empty((), dtype=vdt).element_size()
     codes = (w.B * w.Hq * w.n + w.B * w.Hkv * w.n) * w.k * entry
     return codes + w.B * w.Hkv * w.n * w.d * 2 + w.B * w.Hq * w.n * w.d * 2 + w.B * w.Hq * w.n * 4
+
+
+def _pstats(ms) -> dict:
+    """Median, 10th and 90th percentile of per-step times (ms)."""
+    a = np.asarray(ms, dtype=np.float64)
+    return {"median_ms": float(np.median(a)), "p10_ms": float(np.percentile(a, 10)),
+            "p90_ms": float(np.percentile(a, 90)), "mean_ms": float(a.mean()), "n": int(a.size)}
 
 
 def _blas_threads():
@@ -479,12 +500,17 @@ def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16", window=0, n_global
     torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
     t0.record()
-    for _ in range(steps):
+    for s_ in range(steps):
+        evs[s_][0].record()
         step()
+        evs[s_][1].record()
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
+    step_ms = [a.elapsed_time(b_) for a, b_ in evs]
     algo_bytes = B * Hkv * _decode_keys(L, window, n_global) * (cbytes + d * 2) + \
         B * Hq * (kk * 8 + d * 2 + 4)
     achieved = algo_bytes / (ms * 1e-3)
@@ -503,6 +529,7 @@ def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16", window=0, n_global
                      "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM, "traffic": _traffic("sfa_decode.hip", w.name),
                      "algorithmic_bytes_per_launch": algo_bytes},
+        "timing": {"step": _pstats(step_ms)},
     }
     return out
 
@@ -576,7 +603,8 @@ def bench_decode_paged(w, steps, warmup, codes="i16bf16"):
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
-    dec_ms = sum(a.elapsed_time(b) for a, b in evs) / steps
+    dec_list = [a.elapsed_time(b) for a, b in evs]
+    dec_ms = sum(dec_list) / steps
     ctx = L + warmup + (steps + 1) / 2.0  # mean context length over the timed steps
     dec_bytes = B * Hkv * ctx * (cbytes + d * 2) + B * Hq * (d * 4 + d * 2 + 4)
     achieved = dec_bytes / (dec_ms * 1e-3)
@@ -599,14 +627,15 @@ def bench_decode_paged(w, steps, warmup, codes="i16bf16"):
         "append_prefill": {"kernel": "sfa_kv_append_kernel", "tokens_per_call": L,
                            "ms_per_call": app_ms / (B - 1), "bytes_per_call": app_bytes,
                            "achieved_GBps": app_rate / 1e9, "frac": app_rate / PEAK_HBM},
+        "timing": {"decode_call": _pstats(dec_list)},
     }
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="qwen3_32k", choices=sorted(si.WORKLOADS))
     ap.add_argument("--pass", dest="which", default="fwd", choices=["fwd", "bwd"],
                     help="forward (default, the headline metric) or the backward")
@@ -621,6 +650,10 @@ def main():
                     help="token sparsity composed with SFA: sliding window (0: none)")
     ap.add_argument("--n-global", type=int, default=0,
                     help="leading global tokens with --window")
+    ap.add_argument("--k", type=int, default=0,
+                    help="forward workloads: nonzeros per code other than the workload's")
+    ap.add_argument("--fwd", default="default", choices=["default", "index"],
+                    help="forward entry point: sfa_attn_fwd, or the inverted-index forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 1 GiB device copy twice (reference for "
@@ -635,6 +668,11 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     w = si.workload(args.workload)
+    if args.k:
+        if w.kind != "fwd" or not 1 <= args.k <= w.d:
+            print("--k applies to forward workloads, 1 <= k <= d", file=sys.stderr)
+            sys.exit(2)
+        w = dataclasses.replace(w, k=args.k)
     codes = args.codes or ("i16bf16" if w.kind == "decode" else "i32f32")
     if w.kind == "decode" and codes not in CODE_FORMATS:
         print(f"--codes {codes} is not measured for this workload / pass", file=sys.stderr)
@@ -649,7 +687,7 @@ def main():
                         args.n_global, codes)
     else:
         out = bench_fwd(w, args.steps, args.warmup, not args.no_cpu_baseline, args.window,
-                        args.n_global, codes)
+                        args.n_global, codes, args.fwd)
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device=DEV)
         dst = torch.empty_like(src)

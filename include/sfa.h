@@ -167,8 +167,8 @@ size_t sfa_attn_fwd_workspace(int B, int Hkv, int n, int d, int v_t);
  * q_u * k_u into the score tile for exactly the keys holding u.  Same
  * arguments (without the workspace) and definitions as sfa_attn_fwd; the
  * scores agree up to float32 summation order, and with bf16 V the
- * probabilities enter P.V as a single bfloat16 (relative rounding 2^-9 per
- * weight).  Results are bitwise repeatable.  Slower on this hardware than
+ * probabilities enter P.V as two bfloat16 pieces, hi + lo (relative rounding
+ * ~2^-17 per weight).  Results are bitwise repeatable.  Slower on this hardware than
  * sfa_attn_fwd; kept as the direct realisation of the overlap formulation.
  * Limits: as sfa_attn_fwd with d in {64, 128}, plus k <= 64, Hq / Hkv <= 128,
  * and the per-tile tables must fit LDS (SFA_ENOTSUP otherwise).

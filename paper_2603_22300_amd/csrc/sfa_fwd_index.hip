@@ -20,7 +20,8 @@
 //      the online-softmax update (base-2 exponent, scale * log2(e) folded),
 //      and clears the tile for the next key tile;
 //   4. O^T += V^T P^T on the matrix cores: bf16 V (transposed into LDS while
-//      staging) x bf16 P with float32 accumulation, or float32 x float32.
+//      staging) x P split into two bf16 pieces (hi + lo, ~2^-17 relative) with
+//      float32 accumulation, or float32 x float32.
 // Keys that share no coordinate with a query keep score 0 and still enter
 // the softmax, so the result is exactly softmax(Q~ K~^T * scale) V.
 #include "sfa_device.h"
@@ -309,13 +310,20 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
         const uint16_t* Vt = (const uint16_t*)(smem + L.v_off);
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
-          bf16x8 pb;
+          // P as two bfloat16 pieces, hi = bf16(p) and lo = bf16(p - hi): the
+          // pair carries p to ~2^-17 relative (a single bf16 P would carry
+          // 2^-8, which can exceed the output tolerance by itself)
+          bf16x8 ph, pl;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) pb[e] = (__bf16)t[kb][e];
+          for (int e = 0; e < 8; ++e) {
+            ph[e] = (__bf16)t[kb][e];
+            pl[e] = (__bf16)(t[kb][e] - (float)ph[e]);
+          }
 #pragma unroll
           for (int db = 0; db < NDB; ++db) {
             const bf16x8 va = *(const bf16x8*)(Vt + (db * 32 + (lane & 31)) * kVP + kb * 16 + 8 * hh);
-            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc[db], 0, 0, 0);
+            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ph, acc[db], 0, 0, 0);
+            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pl, acc[db], 0, 0, 0);
           }
         }
       } else {

@@ -80,3 +80,86 @@ def check_grad(g_gpu: torch.Tensor, g_ref: np.ndarray, tol: float, what: str):
     assert np.isfinite(got).all(), f"{what}: non-finite gradient"
     assert rel <= tol, f"{what}: max |g - g_oracle| / max |g| = {rel:.3e} > {tol:.1e}"
     return rel
+
+
+# ---------------------------------------------------------------------------
+# Running the oracle over many independent rows: the oracle's rows do not
+# depend on each other (each query row's softmax is its own), so large
+# samples are split across a thread pool.  The arithmetic is the oracle's;
+# only the scheduling is here.  numpy's sorts and elementwise kernels release
+# the GIL; BLAS is held to one thread per worker to avoid oversubscription.
+# ---------------------------------------------------------------------------
+
+import os as _os
+from concurrent.futures import ThreadPoolExecutor as _Pool
+
+
+def pool_size() -> int:
+    try:
+        n = len(_os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = _os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def par_map(fn, items):
+    from threadpoolctl import threadpool_limits
+    items = list(items)
+    with threadpool_limits(1):
+        with _Pool(pool_size()) as ex:
+            return list(ex.map(fn, items))
+
+
+def oracle_topk_rows(x: np.ndarray, k: int, chunk: int = 8192):
+    """oracle.topk_encode of every row of x [rows, d], in parallel chunks."""
+    import oracle
+    x = np.ascontiguousarray(x).reshape(-1, x.shape[-1])
+    parts = [x[s:s + chunk] for s in range(0, x.shape[0], chunk)]
+    res = par_map(lambda c: oracle.topk_encode(c, k), parts)
+    if not res:
+        return np.zeros((0, k), np.int64), np.zeros((0, k), np.float32)
+    return np.concatenate([r[0] for r in res]), np.concatenate([r[1] for r in res])
+
+
+def oracle_attn_rows(qd: np.ndarray, kd: np.ndarray, vv: np.ndarray, scale: float, causal: bool,
+                     pos: np.ndarray, parts: int = 0, **kw):
+    """oracle.softmax_attention of the query rows qd [r, d] at positions pos,
+    split into interleaved parts that run in parallel; (O [r, dv], LSE [r])."""
+    import oracle
+    parts = parts or pool_size()
+    pos = np.asarray(pos, dtype=np.int64)
+    sl = [np.arange(s, len(pos), parts) for s in range(parts)]
+    sl = [s for s in sl if s.size]
+    res = par_map(lambda s: oracle.softmax_attention(qd[s], kd, vv, scale, causal, pos=pos[s],
+                                                     row_chunk=256, **kw), sl)
+    O = np.empty((len(pos), vv.shape[1]))
+    L = np.empty(len(pos))
+    for s, (o_, l_) in zip(sl, res):
+        O[s], L[s] = o_, l_
+    return O, L
+
+
+def boundary_tie_rows(x: np.ndarray, k: int) -> np.ndarray:
+    """Rows of x whose k-th and (k+1)-th largest magnitudes are equal (the
+    Top-k tie rule decides which coordinate is kept)."""
+    d = x.shape[-1]
+    if k >= d:
+        return np.zeros(0, np.int64)
+    a = np.abs(x.reshape(-1, d).astype(np.float64))
+    part = -np.partition(-a, [k - 1, k], axis=1)
+    return np.flatnonzero(part[:, k - 1] == part[:, k])
+
+
+def full_size_rows(n: int, seed: int, target: int = 4096, tile: int = 64) -> np.ndarray:
+    """Query rows for full-size parity: 0, 1, n-1, both sides of every
+    tile boundary (64m - 1, 64m), then random rows until `target`."""
+    rows = {0, 1, n - 1}
+    for m in range(1, (n + tile - 1) // tile):
+        rows |= {tile * m - 1, tile * m}
+    rng = np.random.default_rng(seed)
+    extra = max(1024, target - len(rows)) if n > target else 0
+    while extra > 0 and len(rows) < min(n, len(rows) + extra):
+        before = len(rows)
+        rows |= set(rng.integers(0, n, size=extra).tolist())
+        extra -= len(rows) - before
+    return np.array(sorted(r for r in rows if 0 <= r < n), dtype=np.int64)

@@ -101,6 +101,11 @@ def test_shapes(B, Hq, Hkv, n, d, k, causal, v_bf16):
         (1, 2, 1, 257, 128, 8, False, True),
         (1, 2, 2, 150, 64, 64, True, False),
         (1, 16, 1, 70, 64, 8, True, True),
+        (1, 2, 1, 300, 128, 32, True, True),   # d = 128, 16 < k <= 64 (the k <= 64 tables)
+        (1, 2, 2, 200, 128, 64, True, True),   # d = 128, k = 64, the largest supported
+        (1, 32, 1, 150, 128, 16, True, True),  # 32 heads per KV head (4 rows per head and block)
+        (1, 128, 1, 70, 128, 8, True, True),   # 128 heads per KV head (1 row per head and block)
+        (1, 4, 2, 1000, 128, 4, True, True),   # small k over 16 key tiles
     ])
 def test_index_variant(B, Hq, Hkv, n, d, k, causal, v_bf16):
     _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=B * 1000 + Hq * 100 + n + 7,
@@ -264,7 +269,7 @@ def test_index_variant_repeatable():
     # between runs (the counting sort takes slots with atomics), but every
     # score entry has one owner that adds its overlaps in the row's code
     # order, so the results are bitwise repeatable
-    q, kk, v = si.dense_qkv(1, 4, 1, 500, 128, 9, device=DEV)
+    q, kk, v = si.dense_qkv(1, 4, 1, 2100, 128, 9, device=DEV)
     qi, qv = _gpu_codes(q, 16)
     ki, kv = _gpu_codes(kk, 16)
     o1, l1 = sfa.sfa_attn_fwd_index(qi, qv, ki, kv, v, o_dtype=torch.float32)
