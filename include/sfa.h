@@ -279,6 +279,37 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val,
                            void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * sfa_attn_decode without a caller workspace and without any allocation, for
+ * callers that cannot allocate device memory around the call (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ *
+ * Same arguments, definitions, kernels and results (bit for bit) as
+ * sfa_attn_decode, minus ws / ws_bytes.  The partial (max, sum, output)
+ * triples of the context chunks go to a static device scratch array of the
+ * library, SFA_DECODE_NOALLOC_MAX_BYTES per GPU, which each GPU the library
+ * runs on holds until the process ends; its device address is looked up
+ * once per device, on the first call with that device current.  The call
+ * allocates nothing and calls no allocating routine.  Every call on one GPU
+ * shares that GPU's scratch: calls that overlap in time on one GPU (other
+ * streams, other threads) race on it and must not be issued.  No part of the
+ * scratch needs to start at zero: each partial is written before it is read.
+ * Errors: as sfa_attn_decode; SFA_ENOSPC when the partials,
+ * sfa_attn_decode_workspace(B, Hq, Lmax, d) bytes, exceed
+ * SFA_DECODE_NOALLOC_MAX_BYTES (at d = 128 and 4096-key chunks: B * Hq *
+ * ceil(Lmax / 4096) <= 64,527 query-head chunks, e.g. 64 sequences x 32
+ * heads x 64K keys); SFA_EHIP if the scratch address cannot be looked up.
+ */
+#define SFA_DECODE_NOALLOC_MAX_BYTES ((size_t)32 << 20)
+sfa_status sfa_attn_decode_noalloc(const void* q_idx, const void* q_val,
+                                   const void* kc_idx, const void* kc_val,
+                                   const void* v_cache, const int32_t* seq_len,
+                                   int B, int Hq, int Hkv, int Lmax, int d, int k,
+                                   float scale, int window, int n_global,
+                                   int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t,
+                                   int v_t, int o_t,
+                                   void* o, float* lse, void* stream);
+
+/*
  * CSR code storage to fixed-width codes (Sec. 2, sparse formats; App. J: the
  * paper stores codes as CSR with int32 indptr, int8 indices, fp16 values).
  *

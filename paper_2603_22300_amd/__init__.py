@@ -18,7 +18,8 @@ __all__ = [
     "SfaError", "lib", "library_path", "sfa_abi_version", "sfa_strerror",
     "sfa_topk_encode", "sfa_attn_fwd_workspace", "sfa_attn_fwd", "sfa_attn_fwd_index",
     "sfa_attn_bwd_workspace", "sfa_attn_bwd",
-    "sfa_attn_decode_workspace", "sfa_attn_decode", "sfa_attn_decode_paged", "sfa_kv_append",
+    "sfa_attn_decode_workspace", "sfa_attn_decode", "sfa_attn_decode_noalloc",
+    "sfa_attn_decode_paged", "sfa_kv_append",
     "sfa_csr_to_codes",
     "SFA_OK", "SFA_EINVAL", "SFA_ENOTSUP", "SFA_EHIP", "SFA_ENOSPC",
     "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16", "SFA_U8", "SFA_F16",
@@ -72,6 +73,10 @@ def lib() -> ctypes.CDLL:
         L.sfa_attn_decode.restype = i32
         L.sfa_attn_decode.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, f32,
                                       i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, sz, vp]
+        L.sfa_attn_decode_noalloc.restype = i32
+        L.sfa_attn_decode_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                              f32, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp,
+                                              vp]
         L.sfa_attn_decode_paged.restype = i32
         L.sfa_attn_decode_paged.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, i32, i32,
                                             i32, i32, i32, f32, i32, i32, i32, i32, i32, i32,
@@ -306,6 +311,43 @@ def sfa_attn_decode(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len=None, scale: 
                                 ot, o.data_ptr(), lp,
                                 ws.data_ptr(), ws.numel() * ws.element_size(), _stream(v_cache)),
           "sfa_attn_decode")
+    return o, lse
+
+
+def sfa_attn_decode_noalloc(q_idx, q_val, kc_idx, kc_val, v_cache, o, lse=None, seq_len=None,
+                            scale: float | None = None, window: int = 0, n_global: int = 0):
+    """sfa_attn_decode on the library's static device scratch: no workspace and
+    no allocation, so the outputs o [B, Hq, d] (and lse [B, Hq] float32, or
+    None) are the caller's.  Calls that overlap in time on one GPU race on the
+    scratch."""
+    B, Hq, k = q_idx.shape
+    Hkv, Lmax, d = kc_idx.shape[1], kc_idx.shape[2], v_cache.shape[-1]
+    if tuple(q_val.shape) != (B, Hq, k) or tuple(kc_idx.shape) != (B, Hkv, Lmax, k) \
+            or tuple(kc_val.shape) != (B, Hkv, Lmax, k) or tuple(v_cache.shape) != (B, Hkv, Lmax, d) \
+            or tuple(o.shape) != (B, Hq, d):
+        raise ValueError("inconsistent shapes")
+    qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _CVAL)
+    cit = _check(kc_idx, "kc_idx", _IDX); cvt = _check(kc_val, "kc_val", _CVAL)
+    vt = _check(v_cache, "v_cache", _VAL); ot = _check(o, "o", _VAL)
+    sp = 0
+    if seq_len is not None:
+        _check(seq_len, "seq_len", {torch.int32: SFA_I32})
+        if seq_len.numel() != B:
+            raise ValueError("seq_len must hold B entries")
+        sp = seq_len.data_ptr()
+    lp = 0
+    if lse is not None:
+        _check(lse, "lse", {torch.float32: SFA_F32})
+        if lse.numel() != B * Hq:
+            raise ValueError("lse must hold B * Hq entries")
+        lp = lse.data_ptr()
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _call(lib().sfa_attn_decode_noalloc(q_idx.data_ptr(), q_val.data_ptr(), kc_idx.data_ptr(),
+                                        kc_val.data_ptr(), v_cache.data_ptr(), sp, B, Hq, Hkv,
+                                        Lmax, d, k, float(scale), int(window), int(n_global), qit,
+                                        qvt, cit, cvt, vt, ot, o.data_ptr(), lp, _stream(v_cache)),
+          "sfa_attn_decode_noalloc")
     return o, lse
 
 

@@ -162,14 +162,21 @@ size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d) {
   return sfa::decode_workspace_bytes(B, Hq, Lmax, d);
 }
 
-sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
-                           const void* kc_val, const void* v_cache, const int32_t* seq_len,
-                           int B, int Hq, int Hkv, int Lmax, int d, int k, float scale,
-                           int window, int n_global,
-                           int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t, int v_t,
-                           int o_t, void* o, float* lse, void* ws, size_t ws_bytes,
-                           void* stream) {
-  if (!q_idx || !q_val || !kc_idx || !kc_val || !v_cache || !o || !ws) return SFA_EINVAL;
+}  // extern "C"
+
+namespace {
+
+// Contiguous-cache decode behind sfa_attn_decode and sfa_attn_decode_noalloc.
+// ws == nullptr selects the library's static device scratch (after every
+// argument check, and only if the partials fit it).
+sfa_status decode_contiguous(const void* q_idx, const void* q_val, const void* kc_idx,
+                             const void* kc_val, const void* v_cache, const int32_t* seq_len,
+                             int B, int Hq, int Hkv, int Lmax, int d, int k, float scale,
+                             int window, int n_global, int q_idx_t, int q_val_t, int kc_idx_t,
+                             int kc_val_t, int v_t, int o_t, void* o, float* lse, void* ws,
+                             size_t ws_bytes, bool use_scratch, void* stream) {
+  if (!q_idx || !q_val || !kc_idx || !kc_val || !v_cache || !o) return SFA_EINVAL;
+  if (!use_scratch && !ws) return SFA_EINVAL;
   if (B < 1 || Hq < 1 || Hkv < 1 || Lmax < 1 || d < 1 || k < 1 || k > d) return SFA_EINVAL;
   if (window < 0 || n_global < 0) return SFA_EINVAL;
   if (Lmax > (1 << 30)) return SFA_ENOTSUP;
@@ -186,7 +193,13 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
     return SFA_ENOTSUP;
   if (!generic && ((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0)
     return SFA_EINVAL;
-  if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
+  const size_t need = sfa::decode_workspace_bytes(B, Hq, Lmax, d);
+  if (use_scratch) {
+    if (need > sfa::noalloc_scratch_bytes()) return SFA_ENOSPC;
+    if (sfa::noalloc_scratch(&ws) != hipSuccess) return SFA_EHIP;
+  } else if (ws_bytes < need) {
+    return SFA_ENOSPC;
+  }
   sfa::DecodeArgs a = {};
   a.q_idx = q_idx; a.q_val = q_val; a.kc_idx = kc_idx; a.kc_val = kc_val; a.v = v_cache;
   a.seq_len = seq_len;
@@ -198,6 +211,33 @@ sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_
   a.o = o; a.lse = lse; a.ws = ws;
   return from_hip(generic ? sfa::launch_attn_decode_generic(a, (hipStream_t)stream)
                           : sfa::launch_attn_decode(a, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+sfa_status sfa_attn_decode(const void* q_idx, const void* q_val, const void* kc_idx,
+                           const void* kc_val, const void* v_cache, const int32_t* seq_len,
+                           int B, int Hq, int Hkv, int Lmax, int d, int k, float scale,
+                           int window, int n_global,
+                           int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t, int v_t,
+                           int o_t, void* o, float* lse, void* ws, size_t ws_bytes,
+                           void* stream) {
+  return decode_contiguous(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, B, Hq, Hkv, Lmax, d,
+                           k, scale, window, n_global, q_idx_t, q_val_t, kc_idx_t, kc_val_t, v_t,
+                           o_t, o, lse, ws, ws_bytes, false, stream);
+}
+
+sfa_status sfa_attn_decode_noalloc(const void* q_idx, const void* q_val, const void* kc_idx,
+                                   const void* kc_val, const void* v_cache,
+                                   const int32_t* seq_len, int B, int Hq, int Hkv, int Lmax,
+                                   int d, int k, float scale, int window, int n_global,
+                                   int q_idx_t, int q_val_t, int kc_idx_t, int kc_val_t, int v_t,
+                                   int o_t, void* o, float* lse, void* stream) {
+  return decode_contiguous(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, B, Hq, Hkv, Lmax, d,
+                           k, scale, window, n_global, q_idx_t, q_val_t, kc_idx_t, kc_val_t, v_t,
+                           o_t, o, lse, nullptr, 0, true, stream);
 }
 
 sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* q_val,

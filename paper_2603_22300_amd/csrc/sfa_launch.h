@@ -83,6 +83,12 @@ int decode_max_group();
 hipError_t launch_attn_decode_generic(const DecodeArgs& a, hipStream_t stream);
 int decode_generic_max_group();
 
+// Static device scratch of the allocation-free decode (one copy per GPU):
+// its size, and its device address on the current device (looked up once per
+// device).
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(void** out);
+
 // KV-cache append: Top-k coding of new keys and copy of their values into a
 // contiguous (table == nullptr: [B, Hkv, P, ...]) or paged cache, then
 // seq_len[b] += the appended count (clamped to the capacity).

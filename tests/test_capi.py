@@ -248,3 +248,16 @@ def test_compact_dtypes_accepted_for_codes_only(L):
     assert _fwd(L, o_t=5) == 1
     assert _dec(L, kc_idx_t=4, kc_val_t=5, ws_bytes=1) == 4
     assert _dec(L, v_t=5) == 1
+
+
+def test_decode_noalloc_host_checks(L):
+    # the allocation-free decode rejects, before any HIP call: partials beyond
+    # its static scratch (SFA_ENOSPC) and null pointers (SFA_EINVAL)
+    B, Hq, Hkv, Lmax, d, k = 64, 32, 8, 1 << 17, 128, 16
+    assert L.sfa_attn_decode_workspace(B, Hq, Lmax, d) > 32 << 20
+    args = [FAKE, FAKE, FAKE, FAKE, FAKE, None, B, Hq, Hkv, Lmax, d, k, ctypes.c_float(0.088), 0,
+            0, 0, 2, 1, 3, 3, 2, FAKE, None, None]
+    assert L.sfa_attn_decode_noalloc(*args) == 4
+    args[6], args[9] = 1, 4096
+    args[0] = None
+    assert L.sfa_attn_decode_noalloc(*args) == 1
