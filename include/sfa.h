@@ -132,13 +132,13 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * recomputed by a second kernel launched on the same stream, with bf16 V and
  * the probabilities split into two bfloat16 terms (~2^-17).  With float32 V
  * the P.V product is float32.
- * Other head dims (d <= 256 except 64 and 128) run on a float32 vector-unit
- * kernel: overlap sums by code lookups, exact running maximum, float32
- * probabilities and P.V; any group size, no workspace.
+ * Other head dims (d <= 256 except 64 and 128), and group sizes Hq / Hkv
+ * that are not a power of two <= 128, run on a float32 vector-unit kernel:
+ * overlap sums by code lookups, exact running maximum, float32 probabilities
+ * and P.V; any group size, no workspace (ws is then unused).
  * Limits: B, Hq, Hkv, n >= 1; Hq % Hkv == 0; 1 <= k <= d <= 256;
  *         B * Hkv <= 65535; n * d <= 2^29 and n * k <= 2^29;
- *         d in {64, 128}: Hq / Hkv a power of two <= 128;
- *         other d: B * Hq <= 65535 (SFA_ENOTSUP otherwise);
+ *         on the float32 kernel: B * Hq <= 65535 (SFA_ENOTSUP otherwise);
  *         window, n_global >= 0.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (workspace missing or too
  *         small), SFA_EHIP.
@@ -213,11 +213,11 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
  * into two bfloat16 pieces and three piece products kept (relative error
  * ~2^-16 of the sum of |terms|), float32 accumulation; P recomputed as
  * exp2(s log2(e) - LSE log2(e)) in float32.
- * Other head dims (d <= 256 except 64 and 128) run a float32 vector-unit
- * backward: the same formulas, scores and P recomputed in float32, no
- * workspace (ws may be NULL), any group size.
- * Limits: as sfa_attn_fwd; d in {64, 128}: Hq / Hkv a power of two <= 8;
- *         other d: B * Hq <= 65535.
+ * Other head dims (d <= 256 except 64 and 128), and group sizes Hq / Hkv
+ * that are not a power of two <= 8, run a float32 vector-unit backward: the
+ * same formulas, scores and P recomputed in float32, no workspace (ws may be
+ * NULL), any group size.
+ * Limits: as sfa_attn_fwd; on the float32 backward: B * Hq <= 65535.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC, SFA_EHIP.
  */
 sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val,
@@ -261,9 +261,10 @@ size_t sfa_attn_decode_workspace(int B, int Hq, int Lmax, int d);
  *                 sfa_attn_decode_workspace(B, Hq, Lmax, d) bytes; its
  *                 contents need no initialisation and are scratch after the
  *                 call.  Concurrent calls must use distinct workspaces.
- * d in {64, 128} runs the tuned kernel (16-byte aligned cache arrays, Hq /
- * Hkv a power of two); other d <= 256 run a float32 kernel with the same
- * chunks and merge (any Hq / Hkv <= 8, no alignment needs).
+ * d in {64, 128} with Hq / Hkv a power of two runs the tuned kernel (16-byte
+ * aligned cache arrays); other d <= 256 and other group sizes run a float32
+ * kernel with the same chunks and merge (any Hq / Hkv <= 8, no alignment
+ * needs).
  * Limits: B, Hq, Hkv, Lmax >= 1; Lmax <= 2^30; Hq % Hkv == 0; Hq / Hkv <= 8;
  *         B * Hkv <= 65535; 1 <= k <= d <= 256; window, n_global >= 0.
  * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC (ws_bytes too small), SFA_EHIP.

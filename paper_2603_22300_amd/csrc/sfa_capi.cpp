@@ -85,9 +85,9 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                             qk_val_t, v_t, o_t, o);
   if (st != SFA_OK) return st;
   if (window < 0 || n_global < 0) return SFA_EINVAL;
-  if (d != 64 && d != 128) {
-    // head dimensions without a matrix-core kernel: the float32 vector-unit
-    // forward (no workspace)
+  if ((d != 64 && d != 128) || !pow2_le(Hq / Hkv, sfa::fwd_max_group())) {
+    // head dimensions or group sizes without a matrix-core kernel: the
+    // float32 vector-unit forward (any group size, no workspace)
     if (!sfa::fwd_generic_supported(d, k) || (long long)B * Hq > 65535) return SFA_ENOTSUP;
     return from_hip(sfa::launch_attn_fwd_generic(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d,
                                                  k, causal != 0, window,
@@ -96,7 +96,6 @@ sfa_status sfa_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
                                                  v_t == SFA_BF16, o_t == SFA_BF16, o, lse,
                                                  (hipStream_t)stream));
   }
-  if (!pow2_le(Hq / Hkv, sfa::fwd_max_group())) return SFA_ENOTSUP;
   const size_t need = sfa::fwd_workspace_bytes(B, Hkv, n, d, v_t == SFA_BF16);
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_fwd(q_idx, q_val, k_idx, k_val, v, B, Hq, Hkv, n, d, k,
@@ -122,16 +121,15 @@ sfa_status sfa_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
   if (st != SFA_OK) return st;
   if (!lse || !dout || !dq_val || !dk_val || !dv) return SFA_EINVAL;
   if (window < 0 || n_global < 0) return SFA_EINVAL;
-  if (d != 64 && d != 128) {
-    // head dimensions without the matrix-core kernels: the float32 backward
-    // (no workspace)
+  if ((d != 64 && d != 128) || !pow2_le(Hq / Hkv, sfa::bwd_max_group())) {
+    // head dimensions or group sizes without the matrix-core kernels: the
+    // float32 backward (any group size, no workspace)
     if (!sfa::bwd_generic_supported(d, k) || (long long)B * Hq > 65535) return SFA_ENOTSUP;
     return from_hip(sfa::launch_attn_bwd_generic(
         q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n, d, k, causal != 0, window,
         window > 0 ? n_global : 0, scale, ifmt_of(idx_t), vfmt_of(qk_val_t), v_t == SFA_BF16,
         o_t == SFA_BF16, dq_val, dk_val, dv, (hipStream_t)stream));
   }
-  if (!pow2_le(Hq / Hkv, sfa::bwd_max_group())) return SFA_ENOTSUP;
   if (ws == nullptr || ws_bytes < sfa::bwd_workspace_bytes(B, Hq, Hkv, n, d)) return SFA_ENOSPC;
   return from_hip(sfa::launch_attn_bwd(q_idx, q_val, k_idx, k_val, v, o, lse, dout, B, Hq, Hkv, n,
                                        d, k, causal != 0, window, window > 0 ? n_global : 0,
@@ -186,11 +184,10 @@ sfa_status decode_contiguous(const void* q_idx, const void* q_val, const void* k
     return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
-  // head dims without the tuned kernel: the float32 decode (no alignment needs)
-  const bool generic = d != 64 && d != 128;
-  if (generic ? (d > 256 || Hq / Hkv > sfa::decode_generic_max_group())
-              : !pow2_le(Hq / Hkv, sfa::decode_max_group()))
-    return SFA_ENOTSUP;
+  // head dims or group sizes without the tuned kernel: the float32 decode
+  // (no alignment needs)
+  const bool generic = (d != 64 && d != 128) || !pow2_le(Hq / Hkv, sfa::decode_max_group());
+  if (generic && (d > 256 || Hq / Hkv > sfa::decode_generic_max_group())) return SFA_ENOTSUP;
   if (!generic && ((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0)
     return SFA_EINVAL;
   const size_t need = sfa::decode_workspace_bytes(B, Hq, Lmax, d);
@@ -262,10 +259,8 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
     return SFA_EINVAL;
   if (!isfinite(scale)) return SFA_EINVAL;
   if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
-  const bool generic = d != 64 && d != 128;
-  if (generic ? (d > 256 || Hq / Hkv > sfa::decode_generic_max_group())
-              : !pow2_le(Hq / Hkv, sfa::decode_max_group()))
-    return SFA_ENOTSUP;
+  const bool generic = (d != 64 && d != 128) || !pow2_le(Hq / Hkv, sfa::decode_max_group());
+  if (generic && (d > 256 || Hq / Hkv > sfa::decode_generic_max_group())) return SFA_ENOTSUP;
   const int Lmax = max_pages * page_size;
   if (!generic && ((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0)
     return SFA_EINVAL;

@@ -9,12 +9,16 @@
 // so the codes are densified tile by tile into LDS and contracted there.
 //
 // Precision: each code value x (for queries: x = q * scale * log2(e), so the
-// scores come out as base-2 exponents) is split into bfloat16 pieces
-// x = x0 + x1 (+ x2),
-// x0 = bf16(x), x1 = bf16(x - x0), x2 = bf16(x - x0 - x1).  Products of
-// bf16 pieces are exact in float32 and accumulate in float32.  With bf16 V the
-// score keeps the terms q0k0 + q0k1 + q1k0 (relative error ~2^-16 of
-// sum|q_u k_u|); with float32 V it keeps every term of order <= 2
+// scores come out as base-2 exponents) is split into 16-bit pieces whose
+// products are exact in float32 and accumulate in float32.
+// With bf16 V: two float16 pieces, x0 = f16(x), x1 = f16(x - x0) (round to
+// nearest even; the float16 matrix cores keep subnormal operands), and the
+// score keeps q0k0 + q0k1 + q1k0: the dropped q1k1 and the rounding of x1
+// leave ~3 * 2^-22 of sum|q_u k_u| (plus at most 2^-25 absolute per value
+// below the float16 normal range).  A value of magnitude >= 65504 does not
+// fit float16: its workgroups are handed to the rerun kernel (below).  With
+// float32 V, and in the rerun: three bfloat16 pieces x0 = bf16(x),
+// x1 = bf16(x - x0), x2 = bf16(x - x0 - x1), and every term of order <= 2
 // (q0k0 + q0k1 + q1k0 + q0k2 + q1k1 + q2k0, ~2^-24).
 // 16-bit codes (bf16 or float16 values) with bf16 V: the raw
 // values are already MFMA operands, so each 16-coordinate block of the score
@@ -25,8 +29,10 @@
 // P.V with bf16 V: V is converted to float16 (exact for normal values up to
 // 65504) and P enters as float16 (P < 2^15, relative rounding 2^-11), one
 // MFMA per block.  A workgroup whose keys hold a V value outside the float16
-// range hands its rows to a rerun kernel that reads V as bf16 and splits P
-// into Ph + Pl in bf16.  With float32 V, P.V runs on the float32 MFMA.
+// range (or a code value too large for the float16 pieces) hands its rows to
+// a rerun kernel that reads V as bf16, splits P into Ph + Pl in bf16 and the
+// code values into three bf16 pieces (six products, ~2^-24).  With float32
+// V, P.V runs on the float32 MFMA.
 //
 // Workgroup = NW wavefronts = 32*NW query rows: the G query heads of one KV
 // head times BR = 32*NW/G positions, so all G heads share each key tile.
@@ -99,37 +105,38 @@ __host__ __device__ constexpr int vtile_bytes() {
   return (D * (kBC + 4) * 2 + 1023) / 1024 * 1024;
 }
 
-// bf16 pieces per key value: two (bf16 V) or three (float32 V) pieces of a
-// float32 value; one raw value for 16-bit codes (KX = kValBF16 / kValF16).
-template <bool VBF16, int KX>
+// 16-bit pieces per key value: two float16 pieces of a float32 value (bf16
+// V), three bfloat16 pieces (float32 V, and the bf16-V rerun); one raw value
+// for 16-bit codes (KX = kValBF16 / kValF16).
+template <bool VBF16, int KX, bool SAFE = false>
 __host__ __device__ constexpr int n_pieces() {
-  return KX ? 1 : (VBF16 ? 2 : 3);
+  return KX ? 1 : (VBF16 && !SAFE ? 2 : 3);
 }
 
-template <int D, bool VBF16, int KX = 0>
+template <int D, bool VBF16, int KX = 0, bool SAFE = false>
 __host__ __device__ constexpr int stage_bytes() {
-  constexpr int NP = n_pieces<VBF16, KX>();
+  constexpr int NP = n_pieces<VBF16, KX, SAFE>();
   return kBC * Geo<D, NP>::KR * 2 + (VBF16 ? vtile_bytes<D>() : kBC * D * 4);
 }
 
 // Two LDS stages (next tile written while the current one is read) when they
 // fit; the float32-V path (three pieces, float32 V tile) uses one.
-template <int D, bool VBF16, int KX = 0>
+template <int D, bool VBF16, int KX = 0, bool SAFE = false>
 __host__ __device__ constexpr int n_stages() {
-  return 2 * stage_bytes<D, VBF16, KX>() <= 160 * 1024 ? 2 : 1;
+  return 2 * stage_bytes<D, VBF16, KX, SAFE>() <= 160 * 1024 ? 2 : 1;
 }
 
 // The densified query rows of the prologue sit past stage 0 with bf16 V, so
 // that the first tile's copy into stage 0 overlaps the prologue.
-template <int D, bool VBF16, int KX = 0>
+template <int D, bool VBF16, int KX = 0, bool SAFE = false>
 __host__ __device__ constexpr int qs_offset() {
-  return VBF16 ? stage_bytes<D, VBF16, KX>() : 0;
+  return VBF16 ? stage_bytes<D, VBF16, KX, SAFE>() : 0;
 }
 
-template <int D, bool VBF16, int NW, int KX = 0>
+template <int D, bool VBF16, int NW, int KX = 0, bool SAFE = false>
 __host__ __device__ constexpr int lds_bytes() {
-  constexpr int st = n_stages<D, VBF16, KX>() * stage_bytes<D, VBF16, KX>();
-  constexpr int qs = qs_offset<D, VBF16, KX>() + NW * 32 * Geo<D, 2>::QP * 2;
+  constexpr int st = n_stages<D, VBF16, KX, SAFE>() * stage_bytes<D, VBF16, KX, SAFE>();
+  constexpr int qs = qs_offset<D, VBF16, KX, SAFE>() + NW * 32 * Geo<D, 2>::QP * 2;
   return st > qs ? st : qs;
 }
 
@@ -142,6 +149,18 @@ __device__ __forceinline__ uint16_t bf16_piece(float x, int pc) {
   if (pc == 1) return (uint16_t)m;
   return (uint16_t)f32_to_bf16_rne(r1 - bf16_bits_to_f32(m));
 }
+
+// float16 piece `pc` of x (0: nearest float16; 1: float16 of x - x0, which is
+// exact in float32).  Finite only for |x| < 65520; callers hand larger values
+// to the bf16-piece rerun.
+__device__ __forceinline__ uint16_t f16_piece(float x, int pc) {
+  const _Float16 h = (_Float16)x;
+  if (pc == 0) return __builtin_bit_cast(uint16_t, h);
+  return __builtin_bit_cast(uint16_t, (_Float16)(x - (float)h));
+}
+// Code values (query values with scale * log2(e) folded in) from this
+// magnitude on take the bf16-piece rerun: float16 pieces would overflow.
+constexpr float kF16PieceMax = 65504.f;
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -172,8 +191,9 @@ constexpr uint32_t kHandBack32 = 0x7fa5a5a5u;
 
 // One workgroup: query block qb of (batch, KV head) bh.
 // SAFE (bf16 V only): V is staged as bf16 and P.V uses P = Ph + Pl on the
-// bf16 MFMA, every tile on the generic path; it reruns the workgroups that the
-// float16 path handed back.
+// bf16 MFMA, every tile on the generic path; the code values are split into
+// three bf16 pieces (every product of order <= 2 kept, any finite magnitude);
+// it reruns the workgroups that the float16 path handed back.
 // KX (bf16 V, 16-bit codes): kValBF16 or kValF16, the code values' type.  The
 // raw query and key values are the MFMA operands (bf16 or float16), so each
 // score is one exact product sum; the scale is applied to the float32 scores.
@@ -183,11 +203,14 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   static_assert(KX == 0 || (VBF16 && !SAFE), "16-bit codes: bf16 V");
   constexpr int NT = NW * 64;
   constexpr int R = NW * 32;
-  constexpr int NP = n_pieces<VBF16, KX>();
+  constexpr int NP = n_pieces<VBF16, KX, SAFE>();
+  // two float16 pieces (bf16 V, 32-bit codes, not the rerun): the three
+  // score products run on the float16 matrix cores
+  constexpr bool F16P = NP == 2 && KX == 0 && !SAFE;
   using Gm = Geo<D, NP>;
   constexpr int QP = Gm::QP, KR = Gm::KR, VP = Gm::VP, NKB = Gm::NKB, NDB = Gm::NDB;
-  constexpr int NS = n_stages<D, VBF16, KX>();
-  constexpr int SB = stage_bytes<D, VBF16, KX>();
+  constexpr int NS = n_stages<D, VBF16, KX, SAFE>();
+  constexpr int SB = stage_bytes<D, VBF16, KX, SAFE>();
   constexpr int KW = kBC / NW;                 // key rows owned (zeroed, filled) by a wave
   constexpr int KEL = (KW * KM + 63) / 64;     // key-code entries per lane and tile
   constexpr int NDP = D / 2;
@@ -195,7 +218,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   constexpr int VI = (VITEMS + NT - 1) / NT;   // V items per thread and tile
   constexpr int VW = VBF16 ? 8 : 4;            // registers per V item
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t* Qs = (uint16_t*)(smem + qs_offset<D, VBF16, KX>());  // setup only: [R][QP]
+  uint16_t* Qs = (uint16_t*)(smem + qs_offset<D, VBF16, KX, SAFE>());  // setup only: [R][QP]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -305,21 +328,32 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // once and each piece overwrites the previous one.
   for (int x = tid; x < R * QP / 8; x += NT) ((uint4*)Qs)[x] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
-  bf16x8 qB[NP][NKB];
+  // a query value too large for float16 pieces hands the workgroup back
+  bool qbig = false;
+  auto q_piece = [&](float x, int pc) -> uint16_t {
+    if constexpr (KX != 0) {
+      return (uint16_t)__float_as_uint(x);
+    } else if constexpr (F16P) {
+      qbig |= fabsf(x) >= kF16PieceMax;
+      return f16_piece(x, pc);
+    } else {
+      return bf16_piece(x, pc);
+    }
+  };
+  bf16x8 qB[NP][NKB];  // 16-bit pieces (float16 bits when F16P)
 #pragma unroll
   for (int pc = 0; pc < NP; ++pc) {
     if (pc > 0) __syncthreads();  // the previous piece is read
     if constexpr (KM <= 16) {
 #pragma unroll
       for (int u = 0; u < QE; ++u)
-        if (q_at[u] >= 0)
-          Qs[q_at[u]] = KX ? (uint16_t)__float_as_uint(q_x[u]) : bf16_piece(q_x[u], pc);
+        if (q_at[u] >= 0) Qs[q_at[u]] = q_piece(q_x[u], pc);
     } else {
       for (int e = tid; e < R * k; e += NT) {
         int at;
         float x;
         q_entry(e, at, x);
-        if (at >= 0) Qs[at] = KX ? (uint16_t)__float_as_uint(x) : bf16_piece(x, pc);
+        if (at >= 0) Qs[at] = q_piece(x, pc);
       }
     }
     __syncthreads();
@@ -328,11 +362,13 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   }
 
   if constexpr (kDMA) {
-    // A V tile of this workgroup's key range outside the float16 range: hand
-    // the rows back to the bf16 rerun before doing any work.
+    // A tile of this workgroup's key range flagged by the pre-pass (a V value
+    // outside the float16 range, or a key value too large for the float16
+    // pieces), or a query value too large for them: hand the rows back to the
+    // bf16 rerun before doing any work.
     for (int t = tid + NT; t < ntiles; t += NT)
       vflag |= p.ws_flag[(int64_t)bh * p.vtiles + tile_at(t)];
-    if (__syncthreads_or(vflag != 0)) {
+    if (__syncthreads_or(vflag != 0 || qbig)) {
       wait_dma();  // the stage copy lands before the workgroup's LDS is released
       if (tid == 0) {
         const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;  // row rho = 0
@@ -363,7 +399,12 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float x = (float)qB[0][kb][e] + (float)qB[1][kb][e];
+        float x;
+        if constexpr (F16P)
+          x = (float)__builtin_bit_cast(f16x8, qB[0][kb])[e] +
+              (float)__builtin_bit_cast(f16x8, qB[1][kb])[e];
+        else
+          x = (float)qB[0][kb][e] + (float)qB[1][kb][e];
         qn = fmaf(x, x, qn);
       }
     qn = sqrtf(pair_sum(qn)) * (1.f + 1.f / 256.f);
@@ -572,6 +613,15 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
         o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
         continue;
       }
+      if constexpr (F16P) {  // smaller terms first
+        o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[1]),
+                                                   __builtin_bit_cast(f16x8, qB[0][kb]), o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[0]),
+                                                   __builtin_bit_cast(f16x8, qB[1][kb]), o, 0, 0, 0);
+        o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[0]),
+                                                   __builtin_bit_cast(f16x8, qB[0][kb]), o, 0, 0, 0);
+        continue;
+      }
       // smaller terms first
       if constexpr (NP == 3) {
         o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[2], qB[0][kb], o, 0, 0, 0);
@@ -725,6 +775,13 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
                                                  __builtin_bit_cast(f16x8, qB[0][kb]), o, 0, 0, 0);
     } else if constexpr (KX == kValBF16) {
       o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[0][kb], o, 0, 0, 0);
+    } else if constexpr (F16P) {
+      o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[1]),
+                                                 __builtin_bit_cast(f16x8, qB[0][kb]), o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[0]),
+                                                 __builtin_bit_cast(f16x8, qB[1][kb]), o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, ka[0]),
+                                                 __builtin_bit_cast(f16x8, qB[0][kb]), o, 0, 0, 0);
     } else {
       o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1], qB[0][kb], o, 0, 0, 0);
       o = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qB[1][kb], o, 0, 0, 0);
@@ -938,14 +995,15 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
 // Stage images for bf16 V, built once per call: image t of (batch, KV head) bh
 // is exactly what the forward kernel holds in LDS for keys 64t .. 64t+63:
 //   - the dense key tile [key][piece][coordinate] (pitch KR) with the codes'
-//     values as bf16 pieces x0 = bf16(x), x1 = bf16(x - x0) at their
+//     values as float16 pieces x0 = f16(x), x1 = f16(x - x0) at their
 //     coordinates and zeros elsewhere (KX: 16-bit codes, the raw values,
 //     one piece);
 //   - V^T as float16, [dimension][key] (pitch kBC + 4);
 //   - in the padding of key row 0, the largest Euclidean norm of the tile's
 //     key codes (times 1 + 2^-8), which bounds the tile's scores.
 // Keys past n and the rest of the padding are zero.  flag t is set when a V value of the
-// tile lies outside the float16 range (|v| >= 65536, inf, NaN).  bf16 ->
+// tile lies outside the float16 range (|v| >= 65536, inf, NaN), or (32-bit
+// codes) a key value is too large for float16 pieces (|x| >= 65504).  bf16 ->
 // float16 is exact for 2^-14 <= |v| <= 65504; below that it rounds to the
 // float16 subnormal grid (absolute error <= 2^-25).
 template <int D, int KX>
@@ -962,6 +1020,7 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
   for (int i = tid; i < SB / 16; i += 256) ((uint4*)T)[i] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
   const int64_t c0 = ((int64_t)bh * n + j0) * k;  // first code element of the tile
+  bool over = false;
   for (int e = tid; e < kBC * k; e += 256) {
     const int j = e / k;
     if (j0 + j >= n) break;
@@ -970,8 +1029,9 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
       T[j * KR + f] = ((const uint16_t*)k_val)[c0 + e];
     } else {
       const float x = load_val(k_val, c0 + e, vfmt);
-      T[j * KR + f] = bf16_piece(x, 0);
-      T[j * KR + D + f] = bf16_piece(x, 1);
+      over |= fabsf(x) >= kF16PieceMax;
+      T[j * KR + f] = f16_piece(x, 0);
+      T[j * KR + D + f] = f16_piece(x, 1);
     }
   }
   // largest Euclidean norm of the tile's key codes (padding of key row 0)
@@ -992,7 +1052,6 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
     *(float*)(T + NP * D) = sqrtf(mx) * (1.f + 1.f / 256.f);
   }
   const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
-  bool over = false;
   for (int c = tid; c < kBC * D / 8; c += 256) {  // 16-byte chunks: key j, dims d0..d0+7
     const int j = c / (D / 8), d0 = (c % (D / 8)) * 8;
     if (j0 + j >= n) break;
@@ -1014,7 +1073,7 @@ __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
 template <int D, bool VBF16, int NW, int KM, int KX>
 hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
   constexpr int bytes = lds_bytes<D, VBF16, NW, KX>();
-  constexpr int rbytes = lds_bytes<D, true, NW>();  // the rerun: two bf16 pieces
+  constexpr int rbytes = lds_bytes<D, true, NW, 0, true>();  // the rerun: three bf16 pieces
   static bool configured = false;  // per instantiation
   if (!configured) {
     hipError_t e = hipSuccess;

@@ -15,10 +15,14 @@ TOL_LSE = 1e-4
 # Backward (no tolerance is fixed by the method): max |g - g_oracle| as a
 # fraction of max |g_oracle| of the same tensor, keyed by (bf16 V, bf16 O and
 # dO).  The products themselves carry ~2^-16; the error that dominates enters
-# through D_i = dO_i . O_i, computed from the forward's O: ~1e-6 relative on
-# the float32 path, ~1e-4 with bf16 V (float16 P in the forward), 2^-9 when
-# O and dO are stored in bf16.  Each bound leaves a factor of ~10 over that.
-TOL_GRAD = {(False, False): 1e-4, (True, False): 2e-3, (True, True): 2e-2}
+# through D_i = dO_i . O_i, computed from the O the caller passes (the
+# oracle's D is exact): ~1e-6 relative on the float32 path, ~1e-4 with bf16 V
+# (float16 P in the forward), and with O stored in bf16 its rounding, unit
+# roundoff 2^-8 (8 significant bits): D_i moves by up to 2^-8 sum_c |dO_ic
+# O_ic|, which shifts dS_ij by P_ij times that and dq, dk by about 2^-8 of
+# max |g| (measured <= 3.2e-3).  The float32 paths keep a factor of ~10 over
+# their error; the bf16-O bound is 1.3 * 2^-8.
+TOL_GRAD = {(False, False): 1e-4, (True, False): 2e-3, (True, True): 5e-3}
 
 
 def np_vals(t: torch.Tensor) -> np.ndarray:

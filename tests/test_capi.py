@@ -76,7 +76,12 @@ def test_fwd_validation(L, fn):
         # other head dims take the float32 vector kernel, one query head per
         # grid row: B * Hq is bounded by the grid
         assert _fwd(L, fn, d=96, k=8, B=40000, Hq=2, Hkv=1) == 2
-    assert _fwd(L, fn, Hq=12, Hkv=4) == 2        # group of 3 heads: unsupported
+    if fn == "sfa_attn_fwd_index":
+        assert _fwd(L, fn, Hq=12, Hkv=4) == 2    # group of 3 heads: the index tables need 2^m
+    else:
+        # a group of 3 heads at d = 64 runs the float32 kernel: its grid bound
+        # on B * Hq applies (and rejects before any launch)
+        assert _fwd(L, fn, B=6000, Hq=12, Hkv=4) == 2
     assert _fwd(L, fn, B=70000, Hkv=1, Hq=1) == 2  # grid limit
     assert _fwd(L, fn, n=(1 << 22) + 1, d=128, k=16) == 2  # 32-bit per-head offsets
 
@@ -161,7 +166,8 @@ def test_bwd_validation_and_workspace(L):
     assert _bwd(L, dq=None) == 1
     assert _bwd(L, k=0) == 1
     assert _bwd(L, Hq=3, Hkv=2) == 1
-    assert _bwd(L, Hq=32, Hkv=2) == 2      # group of 16 heads: not supported by the backward
+    # a group of 16 heads runs the float32 backward: its grid bound on B * Hq
+    assert _bwd(L, B=4000, Hq=32, Hkv=2) == 2
     assert _bwd(L, d=300, k=8) == 2                 # beyond the largest head dim, 256
     assert _bwd(L, d=96, k=8, B=40000, Hq=2, Hkv=1) == 2  # float32 backward: grid bound on B * Hq
 

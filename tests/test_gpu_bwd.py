@@ -69,6 +69,18 @@ def test_shapes(B, Hq, Hkv, n, d, k, causal, v_bf16):
 @pytest.mark.parametrize(
     "B,Hq,Hkv,n,d,k,causal,v_bf16,o_bf16",
     [
+        (1, 6, 2, 150, 128, 16, True, True, False),  # groups of 3 query heads
+        (1, 5, 1, 100, 128, 16, True, True, True),   # a group of 5, bf16 O and dO
+        (1, 10, 2, 90, 64, 8, False, False, False),  # groups of 5 at d = 64, non-causal
+    ])
+def test_group_not_power_of_two(B, Hq, Hkv, n, d, k, causal, v_bf16, o_bf16):
+    """Group sizes that are not a power of two run the float32 backward."""
+    _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=Hq * 7 + n, o_bf16=o_bf16)
+
+
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,v_bf16,o_bf16",
+    [
         (1, 3, 1, 70, 80, 8, True, True, False),     # d = 80, group of 3
         (1, 2, 2, 100, 96, 12, False, False, False),  # d = 96, non-causal
         (1, 2, 1, 45, 256, 16, True, True, True),    # d = 256, bf16 O and dO

@@ -73,6 +73,18 @@ def test_other_head_dims(B, Hq, Hkv, Lmax, d, k, v_bf16, seq):
     _case(B, Hq, Hkv, Lmax, d, k, v_bf16, seq, seed=d + Lmax)
 
 
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,Lmax,d,k,v_bf16,seq",
+    [
+        (2, 6, 2, 5000, 128, 16, True, [5000, 77]),   # groups of 3, two chunks
+        (1, 5, 1, 300, 128, 16, True, None),          # a group of 5
+        (2, 10, 2, 700, 64, 8, False, [700, 1]),      # groups of 5 at d = 64
+    ])
+def test_group_not_power_of_two(B, Hq, Hkv, Lmax, d, k, v_bf16, seq):
+    """Group sizes that are not a power of two run the float32 decode."""
+    _case(B, Hq, Hkv, Lmax, d, k, v_bf16, seq, seed=Hq + Lmax)
+
+
 def test_float32_cache_values():
     _case(2, 4, 1, 700, 128, 16, True, [700, 333], seed=3, cache_bf16=False)
 
