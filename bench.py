@@ -191,6 +191,8 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32", 
     metric = METRIC if window == 0 else METRIC + f"; sliding window {window} + {n_global} global tokens"
     if kk != 16 and w.name == "qwen3_32k":
         metric = metric.replace("k=16", f"k={kk}")
+    if n != 32768 and w.name == "qwen3_32k":
+        metric = metric.replace("n=32K", f"n={n}")
     if fwd == "index":
         metric += "; inverted-index forward (sfa_attn_fwd_index)"
     if codes != "i32f32":
@@ -652,6 +654,8 @@ def main():
                     help="leading global tokens with --window")
     ap.add_argument("--k", type=int, default=0,
                     help="forward workloads: nonzeros per code other than the workload's")
+    ap.add_argument("--n", type=int, default=0,
+                    help="forward workloads: sequence length other than the workload's")
     ap.add_argument("--fwd", default="default", choices=["default", "index"],
                     help="forward entry point: sfa_attn_fwd, or the inverted-index forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -673,6 +677,11 @@ def main():
             print("--k applies to forward workloads, 1 <= k <= d", file=sys.stderr)
             sys.exit(2)
         w = dataclasses.replace(w, k=args.k)
+    if args.n:
+        if w.kind != "fwd" or args.n < 1:
+            print("--n applies to forward workloads, n >= 1", file=sys.stderr)
+            sys.exit(2)
+        w = dataclasses.replace(w, n=args.n)
     codes = args.codes or ("i16bf16" if w.kind == "decode" else "i32f32")
     if w.kind == "decode" and codes not in CODE_FORMATS:
         print(f"--codes {codes} is not measured for this workload / pass", file=sys.stderr)

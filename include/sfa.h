@@ -114,7 +114,8 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  *               V and for head dims other than 64 and 128, where ws may be
  *               NULL).  With bf16 V it receives, on the
  *               stream, V converted once to float16 and laid out as the
- *               kernel's key tiles, and a range flag per tile.  Calls that
+ *               kernel's key tiles, and a range flag per tile (at d = 128
+ *               also the per-tile inverted indexes below).  Calls that
  *               overlap in time need separate workspaces.
  * Arithmetic: the scores are the product of the densified codes on the
  * matrix cores, each value split into bfloat16 pieces whose products are
@@ -132,6 +133,15 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * recomputed by a second kernel launched on the same stream, with bf16 V and
  * the probabilities split into two bfloat16 terms (~2^-17).  With float32 V
  * the P.V product is float32.
+ * Inverted-index scores (Sec. 3.2: intersect the supports through the keys'
+ * active features): at d = 128, k <= 2, bf16 V, each key tile's codes are
+ * bucketed once per call by (coordinate, key parity), and each query
+ * nonzero (u, q_u) adds q_u * k_u into the scores of exactly the keys of the
+ * tile that hold u (float32 products and sums).  This is chosen on the device
+ * from the data: if the tiles' longest buckets average at most 6 entries
+ * (near-uniform supports); skewed supports (long buckets) take the matrix-core
+ * product instead.  The results agree with the matrix-core path up to float32
+ * summation order.
  * Other head dims (d <= 256 except 64 and 128), and group sizes Hq / Hkv
  * that are not a power of two <= 128, run on a float32 vector-unit kernel:
  * overlap sums by code lookups, exact running maximum, float32 probabilities

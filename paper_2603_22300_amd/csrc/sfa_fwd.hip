@@ -52,6 +52,8 @@
 // LDS stage, with one barrier per tile.
 // Keys whose support does not overlap a query keep score 0 and still enter
 // the softmax: the result is exactly softmax(Q~ K~^T * scale) V.
+#include <algorithm>
+
 #include "sfa_device.h"
 #include "sfa_launch.h"
 
@@ -75,6 +77,15 @@ struct FwdParams {
   float kx_scale;
   uint32_t qsign;
   int kx;  // 0, or the 16-bit code value type taking the one-product path
+  // Inverted-index score mode (k <= kIxMaxK, bf16 V): its tile images, and
+  // the data-dependent choice between it and the dense product.  The index
+  // pre-pass adds every tile's longest bucket into *ix_stat; the index mode
+  // runs if the sum is <= ix_thresh, else the dense mode (each launch of the
+  // other mode returns at once).  ix == 0: dense mode only.
+  int ix;
+  const unsigned char* ix_tiles;
+  const uint32_t* ix_stat;
+  uint32_t ix_thresh;
   int ifmt, vfmt, obf16;
   int G, BR, nqb;
   float inv_k;
@@ -958,6 +969,7 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
     qb = j % p.nqb;
     bh = xcd + 8 * (j / p.nqb);
   }
+  if (p.ix && *p.ix_stat <= p.ix_thresh) return;  // the index mode takes this call
   fwd_block<D, VBF16, NW, KM, false, KX>(p, p.nqb - 1 - qb, bh);
 }
 
@@ -992,6 +1004,409 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int
   }
 }
 
+// ---------------------------------------------------------------------------
+// Inverted-index score mode (Sec. 3.2: intersect the supports through the
+// keys' active features), for small k.
+//
+// Each key tile's inverted index is built once per call by
+// sfa_fwd_ix_prep_kernel into the forward's workspace: bucket b = 2u + p
+// lists the tile's keys of parity p that hold coordinate u, as (key, value)
+// entries sorted by bucket, with the bucket bounds, the tile's largest key
+// norm and the float16 V^T tile of the dense image beside them.  The forward
+// copies a tile's index into LDS with direct-to-LDS loads (the next tile in
+// flight).  The two lanes of a query row (key parities p = 0, 1) walk the
+// buckets of the row's nonzeros (u, q_u): for each entry (key c, k_cu) of
+// bucket 2u + p they add q_u * k_cu into S[row][c] of the wave's private
+// score block.  Only overlapping coordinates cost work; every score entry
+// has one owner lane (the key's parity), so the adds are plain
+// read-modify-writes, and each entry sums its overlaps in the row's code
+// order (float32 products and sums).  The wave reads its scores back in the
+// P.V operand layout, clears the entries it touched by a second walk, and
+// runs the online softmax and float16 P.V of the dense mode.
+// ---------------------------------------------------------------------------
+// Largest k of the index mode, which runs at d = 128 only: beyond k = 2, and
+// at d = 64 (half the dense score work), the dense product on the matrix
+// cores is faster on every input measured.
+constexpr int kIxMaxK = 2;
+constexpr int kIxD = 128;
+
+template <int D, int KM>
+struct IxGeo {
+  static constexpr int NBND = 2 * D + 2;                        // bucket bounds 0..2D (+1 pad)
+  static constexpr int ENT = (NBND * 2 + 15) / 16 * 16;          // entries (uint2) start, bytes
+  static constexpr int NORM = ENT + kBC * KM * 8;                // largest key norm (float)
+  static constexpr int VT = (NORM + 16 + 1023) / 1024 * 1024;    // float16 V^T tile
+  static constexpr int SB = VT + vtile_bytes<D>();               // image bytes (whole KB)
+  static constexpr int SPK = kBC + 4;                            // score block row pitch (floats)
+};
+
+template <int D, int NW, int KM>
+__host__ __device__ constexpr int ix_lds_bytes() {
+  return 2 * IxGeo<D, KM>::SB + NW * 32 * IxGeo<D, KM>::SPK * 4;
+}
+
+// Index images: image t of (batch, KV head) bh holds keys 64t .. 64t+63.
+// The bucket order within a bucket follows the counting sort's atomics; it
+// does not change any result (a key enters a bucket once, and a score entry
+// sums its coordinates in the query row's order).  flag t as for the dense
+// images (a V value outside the float16 range).
+template <int D, int KM>
+__global__ __launch_bounds__(256) void sfa_fwd_ix_prep_kernel(
+    const void* __restrict__ k_idx, const void* __restrict__ k_val, const uint16_t* __restrict__ v,
+    int n, int k, int ifmt, int vfmt, int vtiles, unsigned char* __restrict__ ws_tiles,
+    int* __restrict__ ws_flag, uint32_t* __restrict__ ix_stat) {
+  using Gx = IxGeo<D, KM>;
+  constexpr int VP = kBC + 4;
+  __shared__ __attribute__((aligned(16))) unsigned char T[Gx::SB];
+  __shared__ uint32_t cnt[2 * D];
+  __shared__ float kn2[kBC];
+  uint16_t* off = (uint16_t*)T;
+  uint2* ent = (uint2*)(T + Gx::ENT);
+  uint16_t* Vt = (uint16_t*)(T + Gx::VT);
+  const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int j0 = t * kBC;
+  const int nk = min(kBC, n - j0);  // keys of the tile
+  for (int i = tid; i < Gx::SB / 16; i += 256) ((uint4*)T)[i] = make_uint4(0u, 0u, 0u, 0u);
+  for (int i = tid; i < 2 * D; i += 256) cnt[i] = 0u;
+  __syncthreads();
+  const int64_t c0 = ((int64_t)bh * n + j0) * k;  // first code element of the tile
+  constexpr int EPT = (kBC * KM + 255) / 256;     // code entries per thread
+  int eb[EPT], es[EPT], ec[EPT];
+  float ev[EPT];
+#pragma unroll
+  for (int r = 0; r < EPT; ++r) {
+    const int e = tid + 256 * r;
+    eb[r] = -1;
+    if (e < nk * k) {
+      const int c = e / k;
+      ec[r] = c;
+      eb[r] = 2 * load_idx(k_idx, c0 + e, ifmt, D - 1) + (c & 1);
+      ev[r] = load_val(k_val, c0 + e, vfmt);
+      es[r] = (int)atomicAdd(&cnt[eb[r]], 1u);
+    }
+  }
+  __syncthreads();
+  if (tid < 64) {  // exclusive scan of the 2D bucket counts, F consecutive per lane
+    constexpr int F = 2 * D / 64;
+    uint32_t c[F], local = 0;
+#pragma unroll
+    for (int f = 0; f < F; ++f) { c[f] = cnt[tid * F + f]; local += c[f]; }
+    uint32_t incl = local;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o, 64);
+      if (tid >= o) incl += y;
+    }
+    uint32_t run = incl - local, big = 0;
+#pragma unroll
+    for (int f = 0; f < F; ++f) { off[tid * F + f] = (uint16_t)run; run += c[f]; big = max(big, c[f]); }
+    if (tid == 63) off[2 * D] = (uint16_t)incl;
+    big = wave_umax(big);  // the tile's longest bucket
+    if (tid == 0) atomicAdd(ix_stat, big);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < EPT; ++r)
+    if (eb[r] >= 0) ent[off[eb[r]] + es[r]] = make_uint2((uint32_t)ec[r], __float_as_uint(ev[r]));
+  // largest Euclidean norm of the tile's key codes (times 1 + 2^-8)
+  if (tid < kBC) {
+    float acc = 0.f;
+    if (tid < nk)
+      for (int e = 0; e < k; ++e) {
+        const float x = load_val(k_val, c0 + (int64_t)tid * k + e, vfmt);
+        acc = fmaf(x, x, acc);
+      }
+    kn2[tid] = acc;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float mx = 0.f;
+    for (int j = 0; j < kBC; ++j) mx = fmaxf(mx, kn2[j]);
+    *(float*)(T + Gx::NORM) = sqrtf(mx) * (1.f + 1.f / 256.f);
+  }
+  // V^T as float16, [dimension][key], and the V range flag (as the dense image)
+  const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
+  bool over = false;
+  for (int c = tid; c < kBC * D / 8; c += 256) {
+    const int j = c / (D / 8), d0 = (c % (D / 8)) * 8;
+    if (j >= nk) break;
+    const uint4 w4 = *(const uint4*)(src + (int64_t)j * D + d0);
+    const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      over |= (w[e] & 0x7fffu) >= 0x4780u || ((w[e] >> 16) & 0x7fffu) >= 0x4780u;
+      Vt[(d0 + 2 * e) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] & 0xffffu));
+      Vt[(d0 + 2 * e + 1) * VP + j] = __builtin_bit_cast(uint16_t, (_Float16)bf16_bits_to_f32(w[e] >> 16));
+    }
+  }
+  const int any = __syncthreads_or(over);
+  uint4* dst = (uint4*)(ws_tiles + ((int64_t)bh * vtiles + t) * Gx::SB);
+  for (int i = tid; i < Gx::SB / 16; i += 256) dst[i] = ((const uint4*)T)[i];
+  if (tid == 0) ws_flag[(int64_t)bh * vtiles + t] = any ? 1 : 0;
+}
+
+// One workgroup of the index mode: query block qb of (batch, KV head) bh.
+template <int D, int NW, int KM>
+__device__ __forceinline__ void fwd_block_ix(const FwdParams& p, const int qb, const int bh) {
+  using Gx = IxGeo<D, KM>;
+  constexpr int NT = NW * 64, SB = Gx::SB, SPK = Gx::SPK, NDB = D / 32, VP = kBC + 4;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int hh = lane >> 5;  // P.V operand half; in the walks, the key parity
+  const int l32 = lane & 31;
+  const int k = p.k;
+  const int n = p.n;
+  const int b = bh / p.Hkv;
+  const int hkv = bh - b * p.Hkv;
+  const int i0 = qb * p.BR;
+  const int rho = wave * 32 + l32;
+  const int my_i = i0 + rho % p.BR;
+  const int my_hq = hkv * p.G + rho / p.BR;
+  const bool row_ok = my_i < n;
+  float* Srow = (float*)(smem + 2 * SB) + (wave * 32 + l32) * SPK;  // S[row][key]
+
+  const int blk_last = min(n, i0 + p.BR) - 1;
+  const bool win = p.window > 0;
+  int n_keys = p.causal ? blk_last + 1 : n;
+  int gt_end = 0, wt_begin = 0;
+  if (win && i0 >= p.n_global) {
+    if (!p.causal) n_keys = min(n, blk_last + p.window);
+    gt_end = (p.n_global + kBC - 1) / kBC;
+    wt_begin = max(0, i0 - p.window + 1) / kBC;
+    if (wt_begin <= gt_end) gt_end = wt_begin = 0;
+  }
+  const int ntiles_all = (n_keys + kBC - 1) / kBC;
+  const int ntiles = gt_end + ntiles_all - wt_begin;
+  auto tile_at = [&](int t) { return t < gt_end ? t : wt_begin + (t - gt_end); };
+  auto dma_stage = [&](int stage, int jt) {
+    constexpr int NB = SB / 1024, NJ = (NB + NW - 1) / NW;
+    const unsigned char* src = p.ix_tiles + ((int64_t)bh * p.vtiles + jt) * SB;
+    unsigned char* dst = smem + stage * SB;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = wave + j * NW;
+      if (j + 1 < NJ || i < NB)
+        __builtin_amdgcn_global_load_lds(src + (uint32_t)(i * 1024 + lane * 16),
+                                         (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                         16, 0, 0);
+    }
+  };
+  auto wait_dma = [&]() { __builtin_amdgcn_s_waitcnt(0x0f70); };  // vmcnt(0)
+
+  int vflag = 0;
+  if (tid < ntiles) vflag = p.ws_flag[(int64_t)bh * p.vtiles + tile_at(tid)];
+  // the row's nonzeros: bucket 2u + (this lane's key parity) and q_u * scale * log2(e)
+  int qbk[KM];
+  float qx[KM];
+  float qn = 0.f;
+#pragma unroll
+  for (int t = 0; t < KM; ++t) {
+    qbk[t] = -1;
+    qx[t] = 0.f;
+    if (t < k && row_ok) {
+      const int64_t gi = (((int64_t)b * p.Hq + my_hq) * n + my_i) * k + t;
+      qbk[t] = 2 * load_idx(p.q_idx, gi, p.ifmt, D - 1) + hh;
+      qx[t] = p.scale_log2 * load_val(p.q_val, gi, p.vfmt);
+      qn = fmaf(qx[t], qx[t], qn);
+    }
+  }
+  qn = sqrtf(qn) * (1.f + 1.f / 256.f);  // Cauchy-Schwarz bound of the row's exponents per unit key norm
+  if (ntiles > 0) dma_stage(0, tile_at(0));
+  // the wave's score block starts at zero; the walks leave it at zero
+  for (int x = lane; x < 32 * SPK / 4; x += 64)
+    ((float4*)((float*)(smem + 2 * SB) + wave * 32 * SPK))[x] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int t = tid + NT; t < ntiles; t += NT) vflag |= p.ws_flag[(int64_t)bh * p.vtiles + tile_at(t)];
+  if (__syncthreads_or(vflag != 0)) {
+    wait_dma();
+    if (tid == 0) {
+      const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;
+      if (p.obf16) ((uint16_t*)p.o)[orow0 * D] = kHandBack16;
+      else ((uint32_t*)p.o)[orow0 * D] = kHandBack32;
+    }
+    return;
+  }
+
+  float m_run = -INFINITY, l_run = 0.f;
+  floatx16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
+  const int wave_i_max = i0 + (wave * 32 + 31) % p.BR;
+  const int wave_i_min = p.BR >= 32 ? i0 + (wave * 32) % p.BR : i0;
+  auto in_window = [&](int a) {
+    return !win || a < p.n_global || wave_i_min < p.n_global ||
+           (a + 31 > wave_i_min - p.window && a < wave_i_max + p.window);
+  };
+  // Walk the row's buckets: add q_u k_cu into S[row][c] (zero: clear the
+  // entries instead).  The bucket bounds of all the row's terms are read
+  // first; a bucket holds a key at most once, so its entries go four at a
+  // time (four reads, then four read-modify-writes); a key met again under a
+  // later term is read after the earlier write (a wave's LDS operations run
+  // in order).
+  auto walk = [&](const uint16_t* off, const uint2* ent, bool zero) {
+    int e0[KM], e1[KM];
+#pragma unroll
+    for (int t = 0; t < KM; ++t) {
+      const int bk = qbk[t] < 0 ? 0 : qbk[t];
+      e0[t] = off[bk];
+      e1[t] = qbk[t] < 0 ? e0[t] : off[bk + 1];
+    }
+#pragma unroll
+    for (int t = 0; t < KM; ++t) {
+      for (int e = e0[t]; e < e1[t]; e += 4) {
+        uint2 en[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) en[u] = ent[min(e + u, e1[t] - 1)];
+        if (zero) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) Srow[en[u].x] = 0.f;
+        } else {
+          float sv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) sv[u] = Srow[en[u].x];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (e + u < e1[t]) Srow[en[u].x] = fmaf(qx[t], __uint_as_float(en[u].y), sv[u]);
+        }
+      }
+    }
+  };
+  auto pv_sub = [&](int s, const floatx16& pr, const uint16_t* Vt) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      f16x8 pf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = (_Float16)pr[8 * kk + e];
+      const int kbase = 32 * s + 16 * kk + 4 * hh;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const uint16_t* row = Vt + (db * 32 + l32) * VP + kbase;
+        const uint2 v0 = *(const uint2*)row;
+        const uint2 v1 = *(const uint2*)(row + 8);
+        const u32x4 vw = {v0.x, v0.y, v1.x, v1.y};
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, vw), pf,
+                                                         acc[db], 0, 0, 0);
+      }
+    }
+  };
+
+  wait_dma();
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int jt = tile_at(t), jt_next = tile_at(t + 1);
+    const int j0 = jt * kBC;
+    const int stage = t & 1;
+    if (t + 1 < ntiles) dma_stage(stage ^ 1, jt_next);
+    const unsigned char* img = smem + stage * SB;
+    const uint16_t* off = (const uint16_t*)img;
+    const uint2* ent = (const uint2*)(img + Gx::ENT);
+    const uint16_t* Vt = (const uint16_t*)(img + Gx::VT);
+    const bool act0 = (!p.causal || wave_i_max >= j0) && in_window(j0);
+    const bool act1 = (!p.causal || wave_i_max >= j0 + 32) && in_window(j0 + 32);
+    if (act0 || act1) {
+      walk(off, ent, false);
+      floatx16 sc[2];
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const float4 x = *(const float4*)(Srow + 32 * s + 8 * g + 4 * hh);
+          sc[s][4 * g + 0] = x.x; sc[s][4 * g + 1] = x.y; sc[s][4 * g + 2] = x.z; sc[s][4 * g + 3] = x.w;
+        }
+      walk(off, ent, true);
+      const bool wcut = win && j0 + kBC > p.n_global &&
+                        (wave_i_min < p.n_global || wave_i_max - j0 >= p.window ||
+                         j0 + kBC - 1 - wave_i_min >= p.window);
+      const bool need_mask = j0 + kBC > n || (p.causal && j0 + kBC - 1 > wave_i_min) || wcut ||
+                             __builtin_amdgcn_ballot_w64(!row_ok || m_run == -INFINITY) != 0;
+      const float kn = *(const float*)(img + Gx::NORM);
+      // every exponent of the tile is below m_run + kBoundMax: no maxima needed
+      const bool bounded =
+          !need_mask && !__builtin_amdgcn_ballot_w64(!(qn * kn <= m_run + kBoundMax));
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        if (!(s == 0 ? act0 : act1)) continue;
+        floatx16 x = sc[s];
+        float m_use = m_run;
+        if (!bounded) {
+          float mt = -INFINITY;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int j = j0 + 32 * s + 8 * (r >> 2) + 4 * hh + (r & 3);
+            const bool ok = !need_mask ||
+                            (row_ok && j < n && (!p.causal || j <= my_i) &&
+                             (!win || abs(my_i - j) < p.window || j < p.n_global ||
+                              my_i < p.n_global));
+            x[r] = ok ? x[r] : -INFINITY;
+            mt = fmaxf(mt, x[r]);
+          }
+          mt = pair_max(mt);
+          const bool upd = mt > m_run + kLazyMax;
+          const float m_new = upd ? mt : m_run;
+          m_use = (m_new == -INFINITY) ? 0.f : m_new;
+          if (__builtin_amdgcn_ballot_w64(upd)) {
+            const float alpha = upd ? fast_exp2(m_run - m_use) : 1.f;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < NDB; ++db)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
+            m_run = m_new;
+          }
+        }
+        float rs = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) { x[r] = fast_exp2(x[r] - m_use); rs += x[r]; }
+        l_run += rs;
+        pv_sub(s, x, Vt);
+      }
+    }
+    wait_dma();
+    __syncthreads();
+  }
+  l_run = pair_sum(l_run);
+
+  if (row_ok) {
+    const float inv = 1.f / l_run;
+    const int64_t orow = ((int64_t)b * p.Hq + my_hq) * n + my_i;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int dim = db * 32 + 8 * g + 4 * hh;
+        const float o0 = acc[db][4 * g + 0] * inv, o1 = acc[db][4 * g + 1] * inv;
+        const float o2 = acc[db][4 * g + 2] * inv, o3 = acc[db][4 * g + 3] * inv;
+        if (p.obf16) {
+          uint2 w;
+          w.x = f32_to_bf16_rne(o0) | (f32_to_bf16_rne(o1) << 16);
+          w.y = f32_to_bf16_rne(o2) | (f32_to_bf16_rne(o3) << 16);
+          *(uint2*)((uint16_t*)p.o + orow * D + dim) = w;
+        } else {
+          *(float4*)((float*)p.o + orow * D + dim) = make_float4(o0, o1, o2, o3);
+        }
+      }
+    if (p.lse && hh == 0) p.lse[orow] = (m_run + __log2f(l_run)) * kLn2;
+  }
+}
+
+template <int D, int NW, int KM>
+__global__ __launch_bounds__(NW * 64) void sfa_fwd_ix_kernel(FwdParams p) {
+  // workgroup placement as sfa_fwd_kernel (XCD-aware, longest causal blocks first)
+  const int nbh = (int)gridDim.y;
+  int qb = (int)blockIdx.x, bh = (int)blockIdx.y;
+  if (nbh % 8 == 0) {
+    const int id = qb + bh * p.nqb;
+    const int xcd = id & 7, j = id >> 3;
+    qb = j % p.nqb;
+    bh = xcd + 8 * (j / p.nqb);
+  }
+  if (*p.ix_stat > p.ix_thresh) return;  // skewed buckets: the dense mode takes this call
+  fwd_block_ix<D, NW, KM>(p, p.nqb - 1 - qb, bh);
+}
+
 // Stage images for bf16 V, built once per call: image t of (batch, KV head) bh
 // is exactly what the forward kernel holds in LDS for keys 64t .. 64t+63:
 //   - the dense key tile [key][piece][coordinate] (pitch KR) with the codes'
@@ -1010,7 +1425,8 @@ template <int D, int KX>
 __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
     const void* __restrict__ k_idx, const void* __restrict__ k_val, const uint16_t* __restrict__ v,
     int n, int k, int ifmt, int vfmt, int vtiles, unsigned char* __restrict__ ws_tiles,
-    int* __restrict__ ws_flag) {
+    int* __restrict__ ws_flag, const uint32_t* __restrict__ ix_stat, uint32_t ix_thresh) {
+  if (ix_stat && *ix_stat <= ix_thresh) return;  // the index mode takes this call
   constexpr int NP = n_pieces<true, KX>();
   constexpr int KR = Geo<D, NP>::KR, VP = kBC + 4, SB = stage_bytes<D, true, KX>();
   __shared__ __attribute__((aligned(16))) uint16_t T[SB / 2];
@@ -1097,10 +1513,33 @@ hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Index score mode: its forward (returning at once when the dense mode was
+// chosen); the dense forward and the rerun follow on the stream.
+template <int D, int NW, int KM>
+hipError_t launch_ix(const FwdParams& p, int B, hipStream_t stream) {
+  constexpr int bytes = ix_lds_bytes<D, NW, KM>();
+  static bool configured = false;  // per instantiation
+  if (!configured) {
+    hipError_t e = hipFuncSetAttribute((const void*)sfa_fwd_ix_kernel<D, NW, KM>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  dim3 grid(p.nqb, B * p.Hkv), block(NW * 64);
+  hipLaunchKernelGGL((sfa_fwd_ix_kernel<D, NW, KM>), grid, block, bytes, stream, p);
+  return hipGetLastError();
+}
+
 template <int D, bool VBF16, int NW>
 hipError_t launch_nw(FwdParams p, int B, hipStream_t stream) {
   p.BR = NW * 32 / p.G;
   p.nqb = (p.n + p.BR - 1) / p.BR;
+  if constexpr (VBF16 && D == kIxD) {
+    if (p.ix) {
+      const hipError_t e = launch_ix<D, NW, kIxMaxK>(p, B, stream);
+      if (e != hipSuccess) return e;
+    }
+  }
   if constexpr (VBF16) {
     if (p.kx == kValBF16)
       return p.k <= 16 ? launch_km<D, true, NW, 16, kValBF16>(p, B, stream)
@@ -1124,13 +1563,22 @@ hipError_t launch_t(const FwdParams& p, int B, hipStream_t stream) {
 
 }  // namespace
 
+// The index mode's choice: mean longest bucket per tile at most this (the
+// walks of a wave last as long as its longest bucket).
+constexpr uint32_t kIxMeanLongest = 6;
+
+__global__ void sfa_fwd_ix_stat_zero_kernel(uint32_t* stat) { stat[threadIdx.x] = 0u; }
+
 int fwd_max_group() { return 128; }
 
+// Workspace (bf16 V): the dense tile images, one V range flag per tile, the
+// index-mode tile images and the index mode's statistic.
 size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16) {
   if (!vbf16) return 0;
   const size_t tiles = (size_t)B * Hkv * (size_t)((n + kBC - 1) / kBC);
   const size_t sb = d == 64 ? stage_bytes<64, true>() : stage_bytes<128, true>();
-  return tiles * sb + (tiles * 4 + 255) / 256 * 256;
+  const size_t ix = d == kIxD ? tiles * IxGeo<kIxD, kIxMaxK>::SB + 256 : 0;
+  return tiles * sb + (tiles * 4 + 255) / 256 * 256 + ix;
 }
 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
@@ -1149,6 +1597,10 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
   // scale keeps the piece path: its scores are all zero)
   p.kx = vbf16 && vfmt != kValF32 && scale != 0.f ? vfmt : 0;
   p.kx_scale = (float)(fabs((double)scale) * 1.4426950408889634);
+  p.ix = vbf16 && k <= kIxMaxK && d == kIxD;
+  p.ix_tiles = nullptr;
+  p.ix_stat = nullptr;
+  p.ix_thresh = 0;
   p.qsign = scale < 0.f ? 0x8000u : 0u;
   p.G = Hq / Hkv;
   p.BR = 0; p.nqb = 0;
@@ -1159,14 +1611,27 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
   if (vbf16) {
     const size_t tiles = (size_t)B * Hkv * p.vtiles;
     const size_t sb = d == 64 ? stage_bytes<64, true>() : stage_bytes<128, true>();
+    const size_t sbx = IxGeo<kIxD, kIxMaxK>::SB;
     p.ws_flag = (const int*)((unsigned char*)ws + tiles * sb);
+    unsigned char* wx = (unsigned char*)ws + tiles * sb + (tiles * 4 + 255) / 256 * 256;
+    uint32_t* stat = (uint32_t*)(wx + tiles * sbx);
     dim3 grid(p.vtiles, B * Hkv), block(256);
     unsigned char* wt = (unsigned char*)ws;
     int* wf = (int*)p.ws_flag;
     const uint16_t* vb = (const uint16_t*)v;
+    const uint32_t* gstat = nullptr;  // the dense pre-pass skips itself if the index mode runs
+    if (p.ix) {
+      p.ix_tiles = wx;
+      p.ix_stat = stat;
+      p.ix_thresh = (uint32_t)std::min<size_t>(tiles * kIxMeanLongest, 0xffffffffu);
+      gstat = stat;
+      hipLaunchKernelGGL(sfa_fwd_ix_stat_zero_kernel, dim3(1), dim3(1), 0, stream, stat);
+      hipLaunchKernelGGL((sfa_fwd_ix_prep_kernel<kIxD, kIxMaxK>), grid, block, 0, stream, k_idx,
+                         k_val, vb, n, k, ifmt, vfmt, p.vtiles, wx, wf, stat);
+    }
 #define SFA_PREP(DD, KK)                                                                        \
   hipLaunchKernelGGL((sfa_fwd_prep_kernel<DD, KK>), grid, block, 0, stream, k_idx, k_val, vb, n, \
-                     k, ifmt, vfmt, p.vtiles, wt, wf)
+                     k, ifmt, vfmt, p.vtiles, wt, wf, gstat, p.ix_thresh)
     if (d == 64) {
       if (p.kx == kValBF16) SFA_PREP(64, kValBF16);
       else if (p.kx == kValF16) SFA_PREP(64, kValF16);

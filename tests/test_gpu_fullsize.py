@@ -1,8 +1,9 @@
 """Full-size parity on the long workloads, against the oracle.
 
 * Forward (Sec. 3.1 Eqs. (3)-(5), Sec. 3.2): qwen3_32k (32 query heads over 8
-  KV heads, n = 32768) with float32 codes and with int16/bf16 codes, and
-  zipf_128k (8 heads, n = 131072, Zipf supports), run whole on the GPU; every
+  KV heads, n = 32768) with float32 codes, with int16/bf16 codes and with
+  k = 2 (scores through the per-tile inverted indexes), and zipf_128k (8
+  heads, n = 131072, Zipf supports), run whole on the GPU; every
   query head is compared with the oracle on >= 4096 rows: rows 0, 1, n-1,
   both sides of every 64-row tile boundary, and random rows.  The float32 and
   bf16 outputs of sfa_attn_fwd and the output of the inverted-index forward
@@ -18,6 +19,8 @@ The oracle codes the same dense inputs with its own Top-k; nothing it reads
 comes from the GPU path.  Its rows are independent and are run in parallel
 (tests/helpers.py).
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -57,10 +60,12 @@ def _dense_inputs(w):
     return q, kk, v
 
 
-def _run_workload(name, codes16=False, index=True):
+def _run_workload(name, codes16=False, index=True, k=0):
     """Encode + forward on the GPU at full size; keep the dense inputs, the
     GPU codes and the outputs at the sampled rows on the host."""
     w = si.workload(name)
+    if k:
+        w = dataclasses.replace(w, k=k)
     print(f"[fullsize] {name} codes16={codes16}: GPU encode + forward", flush=True)
     q, kk, v = _dense_inputs(w)
     idt, vdt = (torch.int16, torch.bfloat16) if codes16 else (torch.int32, torch.float32)
@@ -106,6 +111,12 @@ def zipf():
     return _run_workload("zipf_128k")
 
 
+@pytest.fixture(scope="module")
+def qwen3_k2():
+    # k = 2: the forward scores through the per-tile inverted indexes
+    return _run_workload("qwen3_32k", index=False, k=2)
+
+
 def _oracle_codes(x, k, bf16):
     i_, v_ = oracle_topk_rows(x, k)
     return (i_, oracle.bf16_rne(v_)) if bf16 else (i_, v_)
@@ -143,6 +154,11 @@ def test_qwen3_32k_codes16_every_head(qwen3_codes16, g):
 @pytest.mark.parametrize("h", range(8))
 def test_zipf_128k_every_head(zipf, h):
     _check_kv_group(zipf, h, bf16_codes=False)
+
+
+@pytest.mark.parametrize("g", range(8))
+def test_qwen3_32k_k2_index_scores_every_head(qwen3_k2, g):
+    _check_kv_group(qwen3_k2, g, bf16_codes=False)
 
 
 def _check_topk_all(x, gi, gv, k, bf16, what):

@@ -184,6 +184,65 @@ def test_group_not_power_of_two(B, Hq, Hkv, n, d, k, causal, v_bf16):
     _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=Hq * 10 + n)
 
 
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,v_bf16",
+    [
+        (1, 4, 1, 700, 128, 2, True, True),    # k = 2, eleven key tiles
+        (1, 8, 2, 300, 128, 1, True, True),    # k = 1, GQA 4:1
+        (2, 2, 2, 257, 128, 2, False, True),   # non-causal, ragged
+        (1, 1, 1, 200, 64, 1, True, True),     # d = 64: the dense product (faster there)
+        (1, 16, 1, 130, 128, 2, True, True),   # 16 heads per KV head
+        (1, 128, 1, 40, 128, 2, True, True),   # 128 heads per KV head (one row per head)
+        (1, 2, 1, 1, 128, 2, True, True),      # n = 1
+        (1, 6, 2, 300, 128, 2, True, True),    # groups of 3: the float32 kernel
+    ])
+def test_index_scores_small_k(B, Hq, Hkv, n, d, k, causal, v_bf16):
+    """k <= 2 at d = 128 with bf16 V and near-uniform supports: sfa_attn_fwd
+    scores through the per-tile inverted indexes (bucket walks) instead of the
+    dense product."""
+    _run_case(B, Hq, Hkv, n, d, k, causal, v_bf16, seed=k * 100 + n + Hq)
+
+
+def test_index_scores_skewed_supports():
+    """Zipf-skewed supports at k = 2 make long buckets: the data-dependent
+    choice may take either mode; the result must match either way."""
+    _run_case(1, 4, 2, 1500, 128, 2, True, True, seed=14, zipf_s=1.1)
+
+
+def test_index_scores_deterministic():
+    q, kk, v = si.dense_qkv(1, 4, 1, 2100, 128, 19, device=DEV)
+    qi, qv = _gpu_codes(q, 2)
+    ki, kv = _gpu_codes(kk, 2)
+    o1, l1 = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.float32)
+    o2, l2 = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, o_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_index_scores_v_beyond_float16_range():
+    """The index mode hands workgroups whose keys reach a V value outside the
+    float16 range to the bf16 rerun, like the dense mode."""
+    B, Hq, Hkv, n, d, k = 1, 8, 2, 700, 128, 2
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, 97, v_dtype=torch.bfloat16, device=DEV)
+    v[0, 0, 70, 5] = 65536.0
+    v[0, 1, 650, 100] = -3.0e5
+    qi, qv = _gpu_codes(q, k)
+    ki, kv = _gpu_codes(kk, k)
+    scale = 1.0 / math.sqrt(d)
+    o32, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=scale, o_dtype=torch.float32)
+    torch.cuda.synchronize()
+    oqi, oqv = oracle.topk_encode(q.cpu().numpy(), k)
+    oki, okv = oracle.topk_encode(kk.cpu().numpy(), k)
+    vn = np_vals(v)
+    O, L = oracle.attn_fwd(oqi, oqv, oki, okv, vn, d, scale, True)
+    tol = TOL_O_BF16V + 2.0 ** -16 * float(np.abs(oracle.widen(vn)).max())
+    got = o32.double().cpu().numpy()
+    err = np.abs(got - O).max()
+    print(f"[parity] index mode, large V: max|O-O_oracle| = {err:.3e} (bound {tol:.3e})", flush=True)
+    assert np.isfinite(got).all() and err <= tol
+    check_lse(lse, L, "LSE (index mode, large V)")
+
+
 def test_int16_indices_bf16_values():
     _run_case(1, 4, 2, 190, 128, 16, True, True, seed=77, idx_dtype=torch.int16,
               val_dtype=torch.bfloat16)

@@ -29,6 +29,9 @@ DEV = "cuda"
     (1, 4, 2, 1500, 128, 16, True, True, 257, 64),   # tile-aligned globals, odd window
     (1, 3, 1, 400, 96, 8, True, True, 45, 5),        # head dim 96: float32 vector kernel
     (1, 2, 2, 300, 48, 6, False, False, 33, 0),      # head dim 48, non-causal
+    (1, 4, 2, 900, 128, 2, True, True, 128, 3),      # index scores (k <= 2): globals, gap
+    (1, 8, 1, 517, 128, 1, False, True, 50, 2),      # index scores, non-causal window
+    (1, 4, 1, 1500, 128, 2, True, True, 257, 64),    # index scores, tile-aligned globals
 ])
 def test_fwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
     seed = n + w + g
