@@ -38,6 +38,9 @@ out in float64 with numpy:
   for the KV-cache codes and the compact format of App. J (8-bit indices,
   fp16 values), and CSR rows of variable length (Sec. 2 sparse formats)
   brought to fixed width.
+* The 8-bit cache of "SFA (quant)" (App. E: SFA with 8-bit activations):
+  symmetric per-row int8 codes with a float32 scale per row, for the key
+  codes' values and the value rows; attention reads their values q * s.
 
 Parity pins for every function live in tests/test_oracle_*.py.
 """
@@ -455,6 +458,69 @@ def attn_decode_paged(q_idx, q_val, kc_idx, kc_val, v_cache, seq_len, d: int, sc
                               n_global=n_global)
         O[b], L[b] = Ob[0], Lsb[0]
     return O, L
+
+
+# --------------------------------------------------------------------------
+# 8-bit cache (App. E, "SFA (quant)": SFA combined with 8-bit quantisation
+# of the activations; with a KV cache, the cached keys and values are those
+# activations): symmetric per-row int8 with one float32 scale per row
+# --------------------------------------------------------------------------
+
+
+def quant_q8(x: np.ndarray):
+    """Symmetric 8-bit quantisation of each row of x [..., m] (float32).
+
+    Per row: a = max |x_u|, s = a / 127 as a float32 division, and
+    q_u = x_u / s as a float32 division, rounded to the nearest integer with
+    ties to even, limited to [-127, 127].  A row of zeros has s = 0 and
+    q = 0.  The value code q_u stands for is q_u * s.
+    Returns (q int8 [..., m], s float32 [...])."""
+    x = np.asarray(x, dtype=np.float32)
+    a = np.abs(x).max(axis=-1)
+    s = (a / np.float32(127)).astype(np.float32)
+    safe = np.where(s > 0, s, np.float32(1)).astype(np.float32)
+    r = (x / safe[..., None]).astype(np.float32)
+    q = np.clip(np.rint(r), -127, 127)
+    q = np.where(s[..., None] > 0, q, 0).astype(np.int8)
+    return q, s
+
+
+def dequant_q8(q, s) -> np.ndarray:
+    """float64 values q * s of int8 codes with their row scales."""
+    return np.asarray(q).astype(np.float64) * np.asarray(s).astype(np.float64)[..., None]
+
+
+def kv_append_q8(kc_idx, kc_val, kc_scale, v_cache, v_scale, k_new, v_new, seq_len, k: int,
+                 n_new=None):
+    """Append to a contiguous 8-bit cache, in place: kc_idx [B, Hkv, Lmax, k],
+    kc_val int8 [B, Hkv, Lmax, k], kc_scale float32 [B, Hkv, Lmax], v_cache int8
+    [B, Hkv, Lmax, d], v_scale float32 [B, Hkv, Lmax].
+
+    For each sequence b and t < n_new[b] (all T when None), the key row
+    k_new[b, h, t] (float32) is coded by Top-k (Sec. 3.1; float32 values) and
+    its k kept values quantised as one row (quant_q8); the value row
+    v_new[b, h, t] (float32, or uint16 bf16 bits widened exactly) is
+    quantised as one row.  Both go to position seq_len[b] + t; positions at
+    or past Lmax are not written.  Returns the new lengths."""
+    k_new = np.asarray(k_new, dtype=np.float32)
+    B, Hkv, T, _ = k_new.shape
+    Lmax = np.shape(kc_idx)[2]
+    lens = np.asarray(seq_len).astype(np.int64)
+    cnt = np.full(B, T) if n_new is None else np.clip(np.asarray(n_new), 0, T)
+    vv = np.asarray(v_new)
+    vv = widen(vv).astype(np.float32) if vv.dtype == np.uint16 else vv.astype(np.float32)
+    for b in range(B):
+        for t in range(int(cnt[b])):
+            j = int(lens[b]) + t
+            if j >= Lmax:
+                break
+            for h in range(Hkv):
+                ci, cv = topk_encode(k_new[b, h, t], k)
+                q, sc = quant_q8(cv)
+                kc_idx[b, h, j], kc_val[b, h, j], kc_scale[b, h, j] = ci, q, sc
+                q, sc = quant_q8(vv[b, h, t])
+                v_cache[b, h, j], v_scale[b, h, j] = q, sc
+    return np.minimum(lens + cnt, Lmax)
 
 
 # --------------------------------------------------------------------------
