@@ -536,6 +536,89 @@ def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16", window=0, n_global
     return out
 
 
+def bench_decode_q8(w, steps, warmup, window=0, n_global=0):
+    """Decode step over the 8-bit cache of SFA (quant): int16 indices, int8
+    code values and int8 value rows with a float32 scale per row, filled by
+    sfa_kv_append_q8 from the same dense keys and values as the bf16 cache."""
+    B, Hq, Hkv, L, d, kk = w.B, w.Hq, w.Hkv, w.n, w.d, w.k
+    ci = torch.empty((B, Hkv, L, kk), dtype=torch.int16, device=DEV)
+    cv = torch.empty((B, Hkv, L, kk), dtype=torch.int8, device=DEV)
+    cs = torch.empty((B, Hkv, L), dtype=torch.float32, device=DEV)
+    vc = torch.empty((B, Hkv, L, d), dtype=torch.int8, device=DEV)
+    vs = torch.empty((B, Hkv, L), dtype=torch.float32, device=DEV)
+    kb = torch.empty((1, Hkv, L, d), device=DEV)
+    vb = torch.empty((1, Hkv, L, d), device=DEV, dtype=torch.bfloat16)
+    zero = torch.zeros(1, dtype=torch.int32, device=DEV)
+    app_ms = 0.0
+    for b in range(B):
+        for h in range(Hkv):
+            kb[0, h] = si.normal((L, d), w.seed, "k", b, h, device=DEV)
+            vb[0, h] = si.normal((L, d), w.seed, "v", b, h, device=DEV).to(torch.bfloat16)
+        zero.zero_()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        sfa.sfa_kv_append_q8(kb, vb, zero, ci[b:b + 1], cv[b:b + 1], cs[b:b + 1], vc[b:b + 1],
+                             vs[b:b + 1], k=kk)
+        e1.record()
+        torch.cuda.synchronize()
+        if b > 0:
+            app_ms += e0.elapsed_time(e1)
+    del kb, vb
+    qd = si.normal((B, Hq, d), w.seed, "q", device=DEV)
+    qi, qv = sfa.sfa_topk_encode(qd, kk)
+    o = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=DEV)
+    ws = torch.empty(sfa.sfa_attn_decode_workspace(B, Hq, L, d), dtype=torch.uint8, device=DEV)
+
+    def step():
+        sfa.sfa_attn_decode_q8(ci, cv, cs, vc, vs, q_idx=qi, q_val=qv, scale=w.scale, o=o,
+                               lse=lse, ws=ws, window=window, n_global=n_global)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    t0.record()
+    for s_ in range(steps):
+        evs[s_][0].record()
+        step()
+        evs[s_][1].record()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    step_ms = [a.elapsed_time(b_) for a, b_ in evs]
+    key_bytes = kk * 2 + kk + 4 + d + 4  # int16 indices, int8 values, scale, int8 V, scale
+    algo_bytes = B * Hkv * _decode_keys(L, window, n_global) * key_bytes + \
+        B * Hq * (kk * 8 + d * 2 + 4)
+    achieved = algo_bytes / (ms * 1e-3)
+    app_bytes = Hkv * L * (d * 4 + d * 2 + key_bytes)
+    return {
+        "metric": "SFA decode tokens/s, 64 seqs x 64K 8-bit cache (SFA (quant): k=16 int16 "
+                  "indices + int8 values, int8 V, float32 scale per row; d=128), 32/8 heads",
+        "value": B / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int8", "data": "synthetic",
+        "config": {"workload": w.name + "_q8", "B": B, "Hq": Hq, "Hkv": Hkv, "L": L, "d": d,
+                   "k": kk, "cache": "int16 idx + int8 values + int8 V, float32 scale per row",
+                   "window": window, "n_global": n_global,
+                   "step": "sfa_attn_decode_q8 (split context + LSE merge)"},
+        "roofline": {"kernel": "sfa_decode_kernel (8-bit) + combine", "bound": "hbm",
+                     "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM, "traffic": None,
+                     "algorithmic_bytes_per_launch": algo_bytes,
+                     "bytes_per_cached_key": key_bytes},
+        "append_prefill": {"kernel": "sfa_kv_append_kernel (8-bit)", "tokens_per_call": L,
+                           "ms_per_call": app_ms / (B - 1), "bytes_per_call": app_bytes,
+                           "achieved_GBps": app_bytes / (app_ms / (B - 1) * 1e-3) / 1e9},
+        "timing": {"step": _pstats(step_ms)},
+    }
+
+
 def bench_decode_paged(w, steps, warmup, codes="i16bf16"):
     """Serving step over a paged cache: append each sequence's new key (coded on
     append) and value, then decode the new dense query (coded inside the decode
@@ -644,10 +727,10 @@ def main():
     ap.add_argument("--cache", default="contiguous", choices=["contiguous", "paged"],
                     help="decode workloads: contiguous cache (decode only) or paged cache "
                          "(append of the new token + decode with in-kernel query coding)")
-    ap.add_argument("--codes", default=None, choices=sorted(FWD_CODE_FORMATS),
+    ap.add_argument("--codes", default=None, choices=sorted(FWD_CODE_FORMATS) + ["q8"],
                     help="code storage: int32 indices + fp32 values (forward default), int16 + "
                          "bf16 (decode default), or the paper's compact uint8 + float16; decode "
-                         "takes the two 16-bit formats")
+                         "takes the two 16-bit formats, and q8: the 8-bit cache of SFA (quant)")
     ap.add_argument("--window", type=int, default=0,
                     help="token sparsity composed with SFA: sliding window (0: none)")
     ap.add_argument("--n-global", type=int, default=0,
@@ -683,10 +766,15 @@ def main():
             sys.exit(2)
         w = dataclasses.replace(w, n=args.n)
     codes = args.codes or ("i16bf16" if w.kind == "decode" else "i32f32")
-    if w.kind == "decode" and codes not in CODE_FORMATS:
+    if codes == "q8" and w.kind != "decode":
+        print("--codes q8 (the 8-bit cache) is a decode format", file=sys.stderr)
+        sys.exit(2)
+    if w.kind == "decode" and codes not in CODE_FORMATS and codes != "q8":
         print(f"--codes {codes} is not measured for this workload / pass", file=sys.stderr)
         sys.exit(2)
-    if w.kind == "decode" and args.cache == "paged":
+    if codes == "q8":
+        out = bench_decode_q8(w, args.steps, args.warmup, args.window, args.n_global)
+    elif w.kind == "decode" and args.cache == "paged":
         out = bench_decode_paged(w, args.steps, args.warmup, codes)
     elif w.kind == "decode":
         out = bench_decode(w, args.steps, args.warmup, not args.no_cpu_baseline, codes,

@@ -425,6 +425,65 @@ sfa_status sfa_attn_decode_paged(const float* q, const void* q_idx, const void* 
                                  int kc_idx_t, int kc_val_t, int v_t, int o_t, void* o,
                                  float* lse, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * 8-bit KV cache ("SFA (quant)", App. E comparison table: SFA combined with
+ * 8-bit quantisation of the activations; with a KV cache, the cached keys
+ * and values are those activations).  Every cached key code and every value
+ * row is one int8 row with its float32 scale (symmetric, per row):
+ *     s = max_u |x_u| / 127,   q_u = round-half-even(x_u / s) in [-127, 127]
+ * (both float32 divisions correctly rounded; a zero row has s = 0, q = 0).
+ * The cache then stands for the values q_u * s, and the attention computed
+ * over it is the plain SFA decode of those values.
+ *
+ * Layout (contiguous: rows (b, h, j) of [B, Hkv, Lmax]; paged: rows
+ * (page, h, slot) of [num_pages, Hkv, page_size], as for sfa_kv_append):
+ *     kc_idx   [rows, k] indices (kc_idx_t)      kc_val [rows, k] int8
+ *     kc_scale [rows] float32                    v_cache [rows, d] int8
+ *     v_scale  [rows] float32
+ * 184 bytes per cached key and KV head at d = 128, k = 16 with int16
+ * indices, against 320 with int16 / bf16 codes and bf16 V.
+ */
+
+/*
+ * Append to an 8-bit cache: as sfa_kv_append (Top-k coding of k_new, the
+ * same positions, capacity and page rules, seq_len advanced), with the kept
+ * code values quantised as one row (its scale to kc_scale) and the value
+ * row v_new (v_new_t SFA_F32 or SFA_BF16, widened exactly) quantised as one
+ * row (its scale to v_scale).  Indices are stored as kc_idx_t (SFA_I32,
+ * SFA_I16 or SFA_U8).
+ * Limits and errors: as sfa_kv_append.
+ */
+sfa_status sfa_kv_append_q8(const float* k_new, const void* v_new, const int32_t* n_new,
+                            int32_t* seq_len, int B, int Hkv, int T, int d, int k,
+                            const int32_t* block_table, int max_pages, int page_size,
+                            int num_pages, void* kc_idx, int8_t* kc_val, float* kc_scale,
+                            int8_t* v_cache, float* v_scale, int kc_idx_t, int v_new_t,
+                            void* stream);
+
+/*
+ * Decode step over an 8-bit cache: sfa_attn_decode (or, with block_table
+ * non-NULL, sfa_attn_decode_paged, including the dense query q coded in the
+ * kernel) with key j's code values q_ju * ks_j and value row v_j = qv_j * vs_j.
+ * The score is the integer-coded overlap sum times scale * ks_j (float32);
+ * the probability enters P.V times vs_j, the int8 values widened exactly.
+ * block_table NULL: contiguous cache [B, Hkv, page_size, ...] (page_size =
+ * Lmax; max_pages and num_pages ignored).  seq_len, window, n_global, o,
+ * lse, ws (sized by sfa_attn_decode_workspace(B, Hq, capacity, d)) as
+ * sfa_attn_decode.
+ * Limits: kc_idx_t SFA_I16, k in {8, 16, 32}, d in {64, 128}, Hq / Hkv a
+ * power of two <= 8 (SFA_ENOTSUP otherwise); 16-byte aligned cache arrays;
+ * paged: page_size a power of two >= 16.
+ * Errors: SFA_EINVAL, SFA_ENOTSUP, SFA_ENOSPC, SFA_EHIP.
+ */
+sfa_status sfa_attn_decode_q8(const float* q, const void* q_idx, const void* q_val,
+                              const void* kc_idx, const int8_t* kc_val, const float* kc_scale,
+                              const int8_t* v_cache, const float* v_scale,
+                              const int32_t* block_table, int max_pages, int page_size,
+                              int num_pages, const int32_t* seq_len, int B, int Hq, int Hkv,
+                              int d, int k, float scale, int window, int n_global, int q_idx_t,
+                              int q_val_t, int kc_idx_t, int o_t, void* o, float* lse, void* ws,
+                              size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

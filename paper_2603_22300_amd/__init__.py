@@ -19,7 +19,7 @@ __all__ = [
     "sfa_topk_encode", "sfa_attn_fwd_workspace", "sfa_attn_fwd", "sfa_attn_fwd_index",
     "sfa_attn_bwd_workspace", "sfa_attn_bwd",
     "sfa_attn_decode_workspace", "sfa_attn_decode", "sfa_attn_decode_noalloc",
-    "sfa_attn_decode_paged", "sfa_kv_append",
+    "sfa_attn_decode_paged", "sfa_kv_append", "sfa_kv_append_q8", "sfa_attn_decode_q8",
     "sfa_csr_to_codes",
     "SFA_OK", "SFA_EINVAL", "SFA_ENOTSUP", "SFA_EHIP", "SFA_ENOSPC",
     "SFA_I32", "SFA_I16", "SFA_F32", "SFA_BF16", "SFA_U8", "SFA_F16",
@@ -84,6 +84,13 @@ def lib() -> ctypes.CDLL:
         L.sfa_kv_append.restype = i32
         L.sfa_kv_append.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp, i32, i32, i32,
                                     vp, vp, vp, i32, i32, i32, i32, vp]
+        L.sfa_kv_append_q8.restype = i32
+        L.sfa_kv_append_q8.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp, i32, i32, i32,
+                                       vp, vp, vp, vp, vp, i32, i32, vp]
+        L.sfa_attn_decode_q8.restype = i32
+        L.sfa_attn_decode_q8.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp,
+                                         i32, i32, i32, i32, i32, f32, i32, i32, i32, i32, i32,
+                                         i32, vp, vp, vp, sz, vp]
         L.sfa_csr_to_codes.restype = i32
         L.sfa_csr_to_codes.argtypes = [vp, vp, i32, vp, i32, i64, i32, i32, vp, i32, vp, vp]
         _lib = L
@@ -454,6 +461,92 @@ def sfa_attn_decode_paged(kc_idx, kc_val, v_cache, block_table, seq_len=None, q=
                                       ot, o.data_ptr(), lp, ws.data_ptr(),
                                       ws.numel() * ws.element_size(), _stream(v_cache)),
           "sfa_attn_decode_paged")
+    return o, lse
+
+
+def sfa_kv_append_q8(k_new, v_new, seq_len, kc_idx, kc_val, kc_scale, v_cache, v_scale, k: int,
+                     block_table=None, n_new=None):
+    """Append to an 8-bit cache (int8 code values and value rows, a float32
+    scale per row).  k_new [B, Hkv, T, d] float32, v_new [B, Hkv, T, d] float32
+    or bf16; contiguous cache kc_idx [B, Hkv, Lmax, k], kc_val int8 [B, Hkv,
+    Lmax, k], kc_scale [B, Hkv, Lmax], v_cache int8 [B, Hkv, Lmax, d], v_scale
+    [B, Hkv, Lmax]; or paged [num_pages, Hkv, P, ...] with block_table [B,
+    max_pages].  seq_len int32 [B] on the GPU is advanced in place."""
+    B, Hkv, T, d = k_new.shape
+    _check(k_new, "k_new", {torch.float32: SFA_F32})
+    vt = _check(v_new, "v_new", _VAL)
+    cit = _check(kc_idx, "kc_idx", _IDX)
+    _check(kc_val, "kc_val", {torch.int8: 0}); _check(v_cache, "v_cache", {torch.int8: 0})
+    _check(kc_scale, "kc_scale", {torch.float32: SFA_F32})
+    _check(v_scale, "v_scale", {torch.float32: SFA_F32})
+    P = kc_idx.shape[2]
+    if tuple(kc_val.shape) != tuple(kc_idx.shape) or kc_idx.shape[3] != k \
+            or tuple(v_cache.shape) != tuple(kc_idx.shape[:3]) + (d,) \
+            or tuple(kc_scale.shape) != tuple(kc_idx.shape[:3]) \
+            or tuple(v_scale.shape) != tuple(kc_idx.shape[:3]):
+        raise ValueError("inconsistent cache shapes")
+    sp = _i32_vec(seq_len, "seq_len", B)
+    np_ = _i32_vec(n_new, "n_new", B) if n_new is not None else 0
+    tp, max_pages, num_pages = 0, 0, 0
+    if block_table is not None:
+        _check(block_table, "block_table", {torch.int32: SFA_I32})
+        tp, max_pages, num_pages = block_table.data_ptr(), block_table.shape[1], kc_idx.shape[0]
+    elif kc_idx.shape[0] != B:
+        raise ValueError("contiguous cache: first dimension must be B")
+    _call(lib().sfa_kv_append_q8(k_new.data_ptr(), v_new.data_ptr(), np_, sp, B, Hkv, T, d, k, tp,
+                                 max_pages, P, num_pages, kc_idx.data_ptr(), kc_val.data_ptr(),
+                                 kc_scale.data_ptr(), v_cache.data_ptr(), v_scale.data_ptr(), cit,
+                                 vt, _stream(k_new)), "sfa_kv_append_q8")
+
+
+def sfa_attn_decode_q8(kc_idx, kc_val, kc_scale, v_cache, v_scale, block_table=None, seq_len=None,
+                       q=None, q_idx=None, q_val=None, Hq=None, scale: float | None = None,
+                       o_dtype=torch.float32, o=None, lse=None, want_lse: bool = True, ws=None,
+                       window: int = 0, n_global: int = 0):
+    """Decode over an 8-bit cache (contiguous, or paged with block_table), with
+    query codes q_idx / q_val [B, Hq, k] or a dense float32 query q [B, Hq, d]
+    coded in the kernel.  Returns (o [B, Hq, d], lse [B, Hq] or None)."""
+    Hkv, P, k = kc_idx.shape[1], kc_idx.shape[2], kc_idx.shape[3]
+    d = v_cache.shape[-1]
+    if q is not None:
+        B, Hq, _ = q.shape
+        _check(q, "q", {torch.float32: SFA_F32})
+        qp, qip, qvp, qit, qvt = q.data_ptr(), 0, 0, 0, 0
+    else:
+        B, Hq, _ = q_idx.shape
+        qit = _check(q_idx, "q_idx", _IDX); qvt = _check(q_val, "q_val", _CVAL)
+        qp, qip, qvp = 0, q_idx.data_ptr(), q_val.data_ptr()
+    cit = _check(kc_idx, "kc_idx", _IDX)
+    _check(kc_val, "kc_val", {torch.int8: 0}); _check(v_cache, "v_cache", {torch.int8: 0})
+    _check(kc_scale, "kc_scale", {torch.float32: SFA_F32})
+    _check(v_scale, "v_scale", {torch.float32: SFA_F32})
+    tp, max_pages, num_pages = 0, 0, 0
+    if block_table is not None:
+        _check(block_table, "block_table", {torch.int32: SFA_I32})
+        tp, max_pages, num_pages = block_table.data_ptr(), block_table.shape[1], kc_idx.shape[0]
+        cap = max_pages * P
+    else:
+        if kc_idx.shape[0] != B:
+            raise ValueError("contiguous cache: first dimension must be B")
+        cap = P
+    sp = _i32_vec(seq_len, "seq_len", B) if seq_len is not None else 0
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if o is None:
+        o = torch.empty((B, Hq, d), dtype=o_dtype, device=v_cache.device)
+    ot = _check(o, "o", _VAL)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=v_cache.device)
+    lp = lse.data_ptr() if lse is not None else 0
+    if ws is None:
+        ws = torch.empty(sfa_attn_decode_workspace(B, Hq, cap, d), dtype=torch.uint8,
+                         device=v_cache.device)
+    _call(lib().sfa_attn_decode_q8(qp, qip, qvp, kc_idx.data_ptr(), kc_val.data_ptr(),
+                                   kc_scale.data_ptr(), v_cache.data_ptr(), v_scale.data_ptr(), tp,
+                                   max_pages, P, num_pages, sp, B, Hq, Hkv, d, k, float(scale),
+                                   int(window), int(n_global), qit, qvt, cit, ot, o.data_ptr(), lp,
+                                   ws.data_ptr(), ws.numel() * ws.element_size(), _stream(v_cache)),
+          "sfa_attn_decode_q8")
     return o, lse
 
 

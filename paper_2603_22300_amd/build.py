@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsfa.so")
 SOURCES = ["sfa_encode.hip", "sfa_fwd.hip", "sfa_fwd_generic.hip", "sfa_fwd_index.hip", "sfa_bwd.hip", "sfa_bwd_generic.hip", "sfa_decode.hip",
-           "sfa_decode_generic.hip",
+           "sfa_decode_generic.hip", "sfa_decode_q8.hip",
            "sfa_cache.hip", "sfa_format.hip", "sfa_noalloc.hip", "sfa_capi.cpp"]
 ARCH = "gfx950"
 

@@ -12,6 +12,10 @@
 // sfa_kv_advance_kernel: seq_len[b] += appended count, clamped to the
 // capacity; it runs after the append on the same stream, so every append
 // wave reads the old length.
+// 8-bit cache (SFA with 8-bit activations, App. E "SFA (quant)"): the kept
+// code values and the value row are each quantised as one row, s = max|x| /
+// 127 and q = round-half-even(x / s) in [-127, 127] (float32 divisions,
+// correctly rounded), stored as int8 with s per row.
 #include "sfa_device.h"
 #include "sfa_launch.h"
 #include "sfa_topk.h"
@@ -32,8 +36,10 @@ __device__ __forceinline__ int appended_count(const int32_t* n_new, int b, int T
 // E: coordinates per lane (d <= 64 * E).  COMMON: int16 / bf16 codes, bf16
 // values in and in the cache, as compile-time constants (the stores then
 // carry no format dispatch); else the formats are read from the arguments.
-template <int E, bool COMMON>
+// Q8: the 8-bit cache (index format from the arguments).
+template <int E, bool COMMON, bool Q8 = false>
 __global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
+  static_assert(!(COMMON && Q8), "the 8-bit cache has its own formats");
   const int lane = threadIdx.x & 63;
   const int ifmt = COMMON ? (int)kIdxI16 : a.ifmt, vfmt = COMMON ? (int)kValBF16 : a.vfmt;
   const bool vin_bf16 = COMMON || a.vin_bf16, vc_bf16 = COMMON || a.vc_bf16;
@@ -91,6 +97,47 @@ __global__ __launch_bounds__(256) void sfa_kv_append_kernel(AppendArgs a) {
       topk_select<E>(key, a.k, sel);
       int sl[E];
       topk_slots<E>(sel, sl);
+      if constexpr (Q8) {
+        // the kept values' largest magnitude is the row's largest: the
+        // largest key, |bits| + 1
+        uint32_t km = 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) km = max(km, key[e]);
+        const float ks = __uint_as_float(wave_umax(km) - 1u) / 127.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          if (sel[e] && sl[e] < a.k) {
+            const int64_t at = crow * a.k + sl[e];
+            const int u = lane + 64 * e;
+            if (ifmt == kIdxI16) ((int16_t*)a.kc_idx)[at] = (int16_t)u;
+            else if (ifmt == kIdxU8) ((uint8_t*)a.kc_idx)[at] = (uint8_t)u;
+            else ((int32_t*)a.kc_idx)[at] = u;
+            const float qf = ks > 0.f ? rintf(__uint_as_float(bits[e]) / ks) : 0.f;
+            ((int8_t*)a.kc_val)[at] = (int8_t)(int)fminf(fmaxf(qf, -127.f), 127.f);
+          }
+        if (lane == 0) a.kc_scale[crow] = ks;
+        // the value row
+        float vf[E];
+        uint32_t vm = 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const bool in = lane + 64 * e < a.d;
+          vf[e] = in ? (vin_bf16 ? bf16_bits_to_f32(vb[e]) : __uint_as_float(vb[e])) : 0.f;
+          vm = max(vm, __float_as_uint(vf[e]) & 0x7fffffffu);
+        }
+        const float vs = __uint_as_float(wave_umax(vm)) / 127.f;
+        const int64_t vo = crow * a.d;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int c = lane + 64 * e;
+          if (c < a.d) {
+            const float qf = vs > 0.f ? rintf(vf[e] / vs) : 0.f;
+            ((int8_t*)a.v_cache)[vo + c] = (int8_t)(int)fminf(fmaxf(qf, -127.f), 127.f);
+          }
+        }
+        if (lane == 0) a.v_scale[crow] = vs;
+        continue;
+      }
 #pragma unroll
       for (int e = 0; e < E; ++e)
         if (sel[e] && sl[e] < a.k)
@@ -133,11 +180,20 @@ hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
     const int gx_need = (a.T + 3) / 4;
     if (gx > gx_need) gx = gx_need;
     dim3 grid(gx, gy), block(256);
-    const bool common = a.ifmt == kIdxI16 && a.vfmt == kValBF16 && a.vin_bf16 && a.vc_bf16;
+    const bool common =
+        !a.q8 && a.ifmt == kIdxI16 && a.vfmt == kValBF16 && a.vin_bf16 && a.vc_bf16;
     auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, block, 0, stream, a); };
-    if (a.d <= 64) common ? go(sfa_kv_append_kernel<1, true>) : go(sfa_kv_append_kernel<1, false>);
-    else if (a.d <= 128) common ? go(sfa_kv_append_kernel<2, true>) : go(sfa_kv_append_kernel<2, false>);
-    else common ? go(sfa_kv_append_kernel<4, true>) : go(sfa_kv_append_kernel<4, false>);
+    if (a.q8) {
+      if (a.d <= 64) go(sfa_kv_append_kernel<1, false, true>);
+      else if (a.d <= 128) go(sfa_kv_append_kernel<2, false, true>);
+      else go(sfa_kv_append_kernel<4, false, true>);
+    } else if (a.d <= 64) {
+      common ? go(sfa_kv_append_kernel<1, true>) : go(sfa_kv_append_kernel<1, false>);
+    } else if (a.d <= 128) {
+      common ? go(sfa_kv_append_kernel<2, true>) : go(sfa_kv_append_kernel<2, false>);
+    } else {
+      common ? go(sfa_kv_append_kernel<4, true>) : go(sfa_kv_append_kernel<4, false>);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

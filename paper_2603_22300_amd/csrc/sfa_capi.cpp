@@ -325,4 +325,77 @@ sfa_status sfa_csr_to_codes(const int32_t* indptr, const void* indices, int indi
   return from_hip(sfa::launch_csr_to_codes(a, (hipStream_t)stream));
 }
 
+sfa_status sfa_kv_append_q8(const float* k_new, const void* v_new, const int32_t* n_new,
+                            int32_t* seq_len, int B, int Hkv, int T, int d, int k,
+                            const int32_t* block_table, int max_pages, int page_size,
+                            int num_pages, void* kc_idx, int8_t* kc_val, float* kc_scale,
+                            int8_t* v_cache, float* v_scale, int kc_idx_t, int v_new_t,
+                            void* stream) {
+  if (!seq_len || !kc_idx || !kc_val || !kc_scale || !v_cache || !v_scale) return SFA_EINVAL;
+  if (B < 1 || Hkv < 1 || T < 0 || d < 1 || k < 1 || k > d || page_size < 1) return SFA_EINVAL;
+  if (T > 0 && (!k_new || !v_new)) return SFA_EINVAL;
+  if (block_table && (max_pages < 1 || num_pages < 1)) return SFA_EINVAL;
+  if (block_table && (long long)max_pages * page_size > (1LL << 30)) return SFA_EINVAL;
+  if (block_table && (page_size & (page_size - 1)) != 0) return SFA_EINVAL;
+  if (!is_idx(kc_idx_t) || !is_val(v_new_t)) return SFA_EINVAL;
+  if (d > 256) return SFA_ENOTSUP;
+  if ((long long)B * Hkv * T > (1LL << 31)) return SFA_ENOTSUP;
+  sfa::AppendArgs a = {};
+  a.k_new = k_new; a.v_new = v_new; a.n_new = n_new; a.seq_len = seq_len;
+  a.table = block_table; a.kc_idx = kc_idx; a.kc_val = kc_val; a.v_cache = v_cache;
+  a.B = B; a.Hkv = Hkv; a.T = T; a.d = d; a.k = k;
+  a.page_size = page_size; a.max_pages = max_pages; a.num_pages = num_pages;
+  while ((1 << a.log2P) < page_size) ++a.log2P;
+  a.ifmt = ifmt_of(kc_idx_t); a.vfmt = sfa::kValF32;
+  a.vin_bf16 = v_new_t == SFA_BF16; a.vc_bf16 = 0;
+  a.q8 = 1; a.kc_scale = kc_scale; a.v_scale = v_scale;
+  return from_hip(sfa::launch_kv_append(a, (hipStream_t)stream));
+}
+
+sfa_status sfa_attn_decode_q8(const float* q, const void* q_idx, const void* q_val,
+                              const void* kc_idx, const int8_t* kc_val, const float* kc_scale,
+                              const int8_t* v_cache, const float* v_scale,
+                              const int32_t* block_table, int max_pages, int page_size,
+                              int num_pages, const int32_t* seq_len, int B, int Hq, int Hkv,
+                              int d, int k, float scale, int window, int n_global, int q_idx_t,
+                              int q_val_t, int kc_idx_t, int o_t, void* o, float* lse, void* ws,
+                              size_t ws_bytes, void* stream) {
+  const bool dense_q = q != nullptr;
+  if (dense_q ? (q_idx || q_val) : (!q_idx || !q_val)) return SFA_EINVAL;
+  if (!kc_idx || !kc_val || !kc_scale || !v_cache || !v_scale || !o || !ws) return SFA_EINVAL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || d < 1 || k < 1 || k > d || page_size < 1) return SFA_EINVAL;
+  if (block_table && (max_pages < 1 || num_pages < 1)) return SFA_EINVAL;
+  if (block_table && (page_size < 16 || (page_size & (page_size - 1)) != 0)) return SFA_EINVAL;
+  if (window < 0 || n_global < 0) return SFA_EINVAL;
+  if (Hq % Hkv != 0) return SFA_EINVAL;
+  if ((!dense_q && (!is_idx(q_idx_t) || !is_cval(q_val_t))) || !is_idx(kc_idx_t) || !is_val(o_t))
+    return SFA_EINVAL;
+  if (!isfinite(scale)) return SFA_EINVAL;
+  const long long cap = block_table ? (long long)max_pages * page_size : page_size;
+  if (cap > (1LL << 30)) return SFA_ENOTSUP;
+  if ((long long)B * Hkv > 65535) return SFA_ENOTSUP;
+  // the 8-bit cache runs the vector decode: int16 indices, k in {8, 16, 32},
+  // d in {64, 128}, a power-of-two group <= 8
+  if (kc_idx_t != SFA_I16 || !sfa::decode_q8_supported(d, k, Hq / Hkv)) return SFA_ENOTSUP;
+  if (((uintptr_t)v_cache | (uintptr_t)kc_idx | (uintptr_t)kc_val) % 16 != 0) return SFA_EINVAL;
+  const int Lmax = (int)cap;
+  if (ws_bytes < sfa::decode_workspace_bytes(B, Hq, Lmax, d)) return SFA_ENOSPC;
+  int log2P = 0;
+  if (block_table)
+    while ((1 << log2P) < page_size) ++log2P;
+  sfa::DecodeArgs a = {};
+  a.q_dense = q; a.q_idx = q_idx; a.q_val = q_val;
+  a.kc_idx = kc_idx; a.kc_val = kc_val; a.v = v_cache;
+  a.kc_scale = kc_scale; a.v_scale = v_scale;
+  a.seq_len = seq_len; a.table = block_table;
+  a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lmax = Lmax; a.d = d; a.k = k; a.scale = scale;
+  a.max_pages = max_pages; a.log2P = log2P; a.num_pages = num_pages;
+  a.window = window; a.n_global = window > 0 ? n_global : 0;
+  a.qifmt = dense_q ? 0 : ifmt_of(q_idx_t); a.qvfmt = dense_q ? 0 : vfmt_of(q_val_t);
+  a.kifmt = sfa::kIdxI16; a.kvfmt = sfa::kValF32;
+  a.vbf16 = 0; a.obf16 = o_t == SFA_BF16;
+  a.o = o; a.lse = lse; a.ws = ws;
+  return from_hip(sfa::launch_attn_decode_q8(a, (hipStream_t)stream));
+}
+
 }  // extern "C"

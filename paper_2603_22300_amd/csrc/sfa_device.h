@@ -67,6 +67,27 @@ __device__ __forceinline__ uint32_t wave_umax(uint32_t x) {
   return max(max(r0, r1), max(r2, r3));
 }
 
+// Float maximum over the wavefront (all 64 lanes active), wave-uniform
+// result, without LDS: the DPP steps of wave_umax make each 16-lane row hold
+// its maximum, and the four row maxima are read by readlane.
+template <int CTRL>
+__device__ __forceinline__ float dpp_max_step(float v) {
+  return fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v),
+                                                             CTRL, 0xf, 0xf, false)));
+}
+
+__device__ __forceinline__ float wave_max_dpp(float x) {
+  x = dpp_max_step<0xb1>(x);   // quad_perm 1,0,3,2
+  x = dpp_max_step<0x4e>(x);   // quad_perm 2,3,0,1
+  x = dpp_max_step<0x141>(x);  // row_half_mirror
+  x = dpp_max_step<0x140>(x);  // row_mirror
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));

@@ -71,6 +71,9 @@ struct DecodeArgs {
   void* o;
   float* lse;
   void* ws;
+  // 8-bit cache (launch_attn_decode_q8): float32 scale per key row / value row
+  const float* kc_scale;
+  const float* v_scale;
 };
 // Keys per decode workgroup (one context chunk); the workspace holds one
 // partial (m, l, o) per chunk, query head and sequence.
@@ -89,6 +92,12 @@ int decode_generic_max_group();
 size_t noalloc_scratch_bytes();
 hipError_t noalloc_scratch(void** out);
 
+// Decode over the 8-bit cache: int8 code values (int16 indices, k in
+// {8, 16, 32}) and int8 value rows with their scales; d in {64, 128}, Hq /
+// Hkv a power of two <= 8.
+hipError_t launch_attn_decode_q8(const DecodeArgs& a, hipStream_t stream);
+bool decode_q8_supported(int d, int k, int G);
+
 // KV-cache append: Top-k coding of new keys and copy of their values into a
 // contiguous (table == nullptr: [B, Hkv, P, ...]) or paged cache, then
 // seq_len[b] += the appended count (clamped to the capacity).
@@ -103,6 +112,11 @@ struct AppendArgs {
   int page_size, max_pages, num_pages;
   int log2P;  // paged: page_size == 1 << log2P
   int ifmt, vfmt, vin_bf16, vc_bf16;
+  // 8-bit cache: kc_val and v_cache hold int8, with one float32 scale per
+  // key row (kc_scale) and value row (v_scale)
+  int q8;
+  float* kc_scale;
+  float* v_scale;
 };
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
 

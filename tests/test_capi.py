@@ -267,3 +267,29 @@ def test_decode_noalloc_host_checks(L):
     args[6], args[9] = 1, 4096
     args[0] = None
     assert L.sfa_attn_decode_noalloc(*args) == 1
+
+
+def test_q8_cache_host_checks(L):
+    # 8-bit cache entry points: rejections before any launch
+    app = [FAKE, FAKE, None, FAKE, 2, 2, 3, 128, 16, None, 0, 100, 0, FAKE, FAKE, FAKE, FAKE, FAKE,
+           1, 3, None]
+    a = list(app); a[13] = None                    # kc_idx missing
+    assert L.sfa_kv_append_q8(*a) == 1
+    a = list(app); a[8] = 129                      # k > d
+    assert L.sfa_kv_append_q8(*a) == 1
+    a = list(app); a[7], a[8] = 300, 8             # d beyond 256
+    assert L.sfa_kv_append_q8(*a) == 2
+    dec = [None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, 4096, 0, None, 2, 8, 2, 128, 16,
+           ctypes.c_float(0.088), 0, 0, 0, 2, 1, 2, FAKE, None, FAKE, ctypes.c_size_t(1 << 40), None]
+    a = list(dec); a[0] = FAKE                     # dense query and codes together
+    assert L.sfa_attn_decode_q8(*a) == 1
+    a = list(dec); a[17] = 12                      # k without the vector path
+    assert L.sfa_attn_decode_q8(*a) == 2
+    a = list(dec); a[16], a[17] = 96, 8            # head dim without the tuned kernel
+    assert L.sfa_attn_decode_q8(*a) == 2
+    a = list(dec); a[23] = 0                       # int32 cache indices
+    assert L.sfa_attn_decode_q8(*a) == 2
+    a = list(dec); a[14] = 12                      # group of 6
+    assert L.sfa_attn_decode_q8(*a) == 2
+    a = list(dec); a[28] = ctypes.c_size_t(16)     # workspace too small
+    assert L.sfa_attn_decode_q8(*a) == 4
