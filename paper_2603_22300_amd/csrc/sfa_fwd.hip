@@ -954,8 +954,13 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   }
 }
 
+// d = 64, bf16 V, 4 wavefronts: at most 168 VGPRs, so that three
+// workgroups (three waves per SIMD) share a compute unit, as their LDS
+// allows; with two, short sequences were latency-bound (measured: the gpt2s
+// shape's forward kernel 77 -> 54 us).
 template <int D, bool VBF16, int NW, int KM, int KX>
-__global__ __launch_bounds__(NW * 64) void sfa_fwd_kernel(FwdParams p) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64 && VBF16 && NW == 4 ? 3 : 1)))
+void sfa_fwd_kernel(FwdParams p) {
   // longest causal blocks first
   // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
   // L2): with the (batch, KV head) count a multiple of 8, XCD x runs the KV
@@ -1555,9 +1560,12 @@ hipError_t launch_nw(FwdParams p, int B, hipStream_t stream) {
 template <int D, bool VBF16>
 hipError_t launch_t(const FwdParams& p, int B, hipStream_t stream) {
   // 8 wavefronts (256 rows) per workgroup when that still gives >= 4
-  // workgroups per compute unit; else 4 wavefronts.
+  // workgroups per compute unit; else 4 wavefronts.  d = 64 with bf16 V
+  // always takes 4: three such workgroups fit a compute unit (12 waves,
+  // against 8 for one 8-wave workgroup), faster at every length measured
+  // (n = 1024, 4096, 16384).
   const long long wg8 = (long long)((p.n + 256 / p.G - 1) / (256 / p.G)) * B * p.Hkv;
-  if (p.G <= 8 && wg8 >= 4LL * 256) return launch_nw<D, VBF16, 8>(p, B, stream);
+  if (!(D == 64 && VBF16) && p.G <= 8 && wg8 >= 4LL * 256) return launch_nw<D, VBF16, 8>(p, B, stream);
   return launch_nw<D, VBF16, 4>(p, B, stream);
 }
 
