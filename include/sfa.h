@@ -118,10 +118,12 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  *               also the per-tile inverted indexes below).  Calls that
  *               overlap in time need separate workspaces.
  * Arithmetic: the scores are the product of the densified codes on the
- * matrix cores, each value split into bfloat16 pieces whose products are
- * exact in float32 (bf16 V: three piece products, relative error ~2^-16 of
- * sum |q_u k_u|; float32 V: six, ~2^-24); softmax and accumulation in
- * float32.  16-bit code values (SFA_BF16 or SFA_F16) with bf16 V and a
+ * matrix cores, each value split into 16-bit pieces whose products are
+ * exact in float32: with bf16 V two float16 pieces x0 = f16(x),
+ * x1 = f16(x - x0) and three piece products (relative error ~3 * 2^-22 of
+ * sum |q_u k_u|); with float32 V, and for code values of magnitude >= 65504
+ * (query values after the scale), three bfloat16 pieces and six products
+ * (~2^-24); softmax and accumulation in float32.  16-bit code values (SFA_BF16 or SFA_F16) with bf16 V and a
  * nonzero scale: the raw query and key values are the matrix-core
  * operands (bf16 or float16 products, exact in float32, one per coordinate
  * block), the sign of scale is folded into the query values and |scale| is
@@ -129,9 +131,11 @@ sfa_status sfa_topk_encode(const float* x, int64_t rows, int d, int k,
  * (exact for normal values up to 65504) and the probabilities (below 2^15)
  * enter P.V as float16,
  * relative rounding 2^-11 per weight (MFMA, float32 accumulate).  Workgroups
- * whose keys reach a V value of magnitude >= 65536 (or inf / NaN) are
- * recomputed by a second kernel launched on the same stream, with bf16 V and
- * the probabilities split into two bfloat16 terms (~2^-17).  With float32 V
+ * whose keys reach a V value of magnitude >= 65536 (or inf / NaN), or a
+ * code value too large for the float16 pieces, are recomputed by a second
+ * kernel launched on the same stream, with bf16 V and the probabilities
+ * split into two bfloat16 terms (~2^-17); it returns at once when no
+ * workgroup was handed back.  With float32 V
  * the P.V product is float32.
  * Inverted-index scores (Sec. 3.2: intersect the supports through the keys'
  * active features): at d = 128, k <= 2, bf16 V, each key tile's codes are

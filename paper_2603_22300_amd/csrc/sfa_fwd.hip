@@ -94,6 +94,9 @@ struct FwdParams {
   // flag per tile
   const unsigned char* ws_tiles;
   const int* ws_flag;
+  // set to nonzero by every workgroup that hands its rows back (zeroed by
+  // the pre-pass), so that the rerun launch returns at once when none did
+  int* hb_count;
   int vtiles;  // tiles per (batch, KV head): ceil(n / 64)
 };
 
@@ -385,6 +388,7 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
         const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;  // row rho = 0
         if (p.obf16) ((uint16_t*)p.o)[orow0 * D] = kHandBack16;
         else ((uint32_t*)p.o)[orow0 * D] = kHandBack32;
+        *p.hb_count = 1;
       }
       return;
     }
@@ -973,6 +977,16 @@ void sfa_fwd_kernel(FwdParams p) {
     const int xcd = id & 7, j = id >> 3;
     qb = j % p.nqb;
     bh = xcd + 8 * (j / p.nqb);
+    if constexpr (D == 64 && VBF16 && NW == 4) {
+      // Three of these workgroups share a compute unit, all resident at
+      // once, so nothing evens out their causal lengths later: successive
+      // heads of an XCD take the blocks longest-first, shortest-first and
+      // half-rotated, which mixes long and short blocks on a compute unit
+      // under in-order dispatch (measured: gpt2s shape 54 -> 50 us).
+      const int r = (j / p.nqb) % 3;
+      if (r == 1) qb = p.nqb - 1 - qb;
+      else if (r == 2) qb = (qb + p.nqb / 2) % p.nqb;
+    }
   }
   if (p.ix && *p.ix_stat <= p.ix_thresh) return;  // the index mode takes this call
   fwd_block<D, VBF16, NW, KM, false, KX>(p, p.nqb - 1 - qb, bh);
@@ -994,6 +1008,7 @@ __device__ __forceinline__ bool handed_back(const FwdParams& p, int t, int D) {
 template <int D, int NW, int KM>
 __global__ __launch_bounds__(NW * 64) void sfa_fwd_rerun_kernel(FwdParams p, int nbh) {
   constexpr int NT = NW * 64;
+  if (*p.hb_count == 0) return;  // no workgroup was handed back
   const int total = p.nqb * nbh;
   const int stride = (int)gridDim.x;
   for (int base = (int)blockIdx.x; base < total; base += stride * NT) {
@@ -1229,6 +1244,7 @@ __device__ __forceinline__ void fwd_block_ix(const FwdParams& p, const int qb, c
       const int64_t orow0 = ((int64_t)b * p.Hq + hkv * p.G) * n + i0;
       if (p.obf16) ((uint16_t*)p.o)[orow0 * D] = kHandBack16;
       else ((uint32_t*)p.o)[orow0 * D] = kHandBack32;
+      *p.hb_count = 1;
     }
     return;
   }
@@ -1426,58 +1442,100 @@ __global__ __launch_bounds__(NW * 64) void sfa_fwd_ix_kernel(FwdParams p) {
 // codes) a key value is too large for float16 pieces (|x| >= 65504).  bf16 ->
 // float16 is exact for 2^-14 <= |v| <= 65504; below that it rounds to the
 // float16 subnormal grid (absolute error <= 2^-25).
+// Every global load of the tile is issued before the first use (one memory
+// round trip, then the LDS work, then the stores): with k <= 16 the code
+// entries and the V chunks sit in registers, and the norms of the tile's 64
+// keys are taken by lanes 0-63 from loads of their own.
 template <int D, int KX>
 __global__ __launch_bounds__(256) void sfa_fwd_prep_kernel(
     const void* __restrict__ k_idx, const void* __restrict__ k_val, const uint16_t* __restrict__ v,
     int n, int k, int ifmt, int vfmt, int vtiles, unsigned char* __restrict__ ws_tiles,
-    int* __restrict__ ws_flag, const uint32_t* __restrict__ ix_stat, uint32_t ix_thresh) {
-  if (ix_stat && *ix_stat <= ix_thresh) return;  // the index mode takes this call
+    int* __restrict__ ws_flag, const uint32_t* __restrict__ ix_stat, uint32_t ix_thresh,
+    int* __restrict__ hb_count) {
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *hb_count = 0;
   constexpr int NP = n_pieces<true, KX>();
   constexpr int KR = Geo<D, NP>::KR, VP = kBC + 4, SB = stage_bytes<D, true, KX>();
+  constexpr int KE = kBC * 16 / 256;   // code entries per thread for k <= 16
+  constexpr int VC = kBC * D / 8 / 256;  // 16-byte V chunks per thread
+  static_assert(KE * 256 == kBC * 16 && VC * 256 * 8 == kBC * D, "whole tiles per thread");
   __shared__ __attribute__((aligned(16))) uint16_t T[SB / 2];
   uint16_t* Vt = T + kBC * KR;
   const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const int j0 = t * kBC;
+  const int nk = min(kBC, n - j0);                // keys of this tile
+  const int64_t c0 = ((int64_t)bh * n + j0) * k;  // first code element of the tile
+  const bool small_k = k <= 16;
+
+  // ---- global loads ----
+  int ci[KE];
+  float cx[KE];
+#pragma unroll
+  for (int i = 0; i < KE; ++i) {
+    const int e = tid + 256 * i;
+    ci[i] = -1;
+    cx[i] = 0.f;
+    if (small_k && e < nk * k) {
+      ci[i] = load_idx(k_idx, c0 + e, ifmt, D - 1);
+      cx[i] = KX != 0 ? __uint_as_float((uint32_t)((const uint16_t*)k_val)[c0 + e])
+                      : load_val(k_val, c0 + e, vfmt);
+    }
+  }
+  const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
+  uint4 vw[VC];
+#pragma unroll
+  for (int i = 0; i < VC; ++i) {  // chunk c: key c / (D / 8), dimensions 8 (c % (D / 8)) + 0..7
+    const int c = tid + 256 * i, j = c / (D / 8), d0 = (c % (D / 8)) * 8;
+    vw[i] = j < nk ? *(const uint4*)(src + (int64_t)j * D + d0) : make_uint4(0u, 0u, 0u, 0u);
+  }
+  float kx[16];  // lanes 0-63: the code values of key tid (k <= 16)
+#pragma unroll
+  for (int e = 0; e < 16; ++e)
+    kx[e] = (small_k && tid < nk && e < k) ? load_val(k_val, c0 + (int64_t)tid * k + e, vfmt) : 0.f;
+  if (ix_stat && *ix_stat <= ix_thresh) return;  // the index mode takes this call
+
   for (int i = tid; i < SB / 16; i += 256) ((uint4*)T)[i] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
-  const int64_t c0 = ((int64_t)bh * n + j0) * k;  // first code element of the tile
   bool over = false;
-  for (int e = tid; e < kBC * k; e += 256) {
-    const int j = e / k;
-    if (j0 + j >= n) break;
-    const int f = load_idx(k_idx, c0 + e, ifmt, D - 1);
+  auto put = [&](int j, int f, float x) {  // x: the value (KX: its 16-bit pattern)
     if constexpr (KX != 0) {
-      T[j * KR + f] = ((const uint16_t*)k_val)[c0 + e];
+      T[j * KR + f] = (uint16_t)__float_as_uint(x);
     } else {
-      const float x = load_val(k_val, c0 + e, vfmt);
       over |= fabsf(x) >= kF16PieceMax;
       T[j * KR + f] = f16_piece(x, 0);
       T[j * KR + D + f] = f16_piece(x, 1);
     }
+  };
+  if (small_k) {
+#pragma unroll
+    for (int i = 0; i < KE; ++i)
+      if (ci[i] >= 0) put((tid + 256 * i) / k, ci[i], cx[i]);
+  } else {
+    for (int e = tid; e < nk * k; e += 256)
+      put(e / k, load_idx(k_idx, c0 + e, ifmt, D - 1),
+          KX != 0 ? __uint_as_float((uint32_t)((const uint16_t*)k_val)[c0 + e])
+                  : load_val(k_val, c0 + e, vfmt));
   }
-  // largest Euclidean norm of the tile's key codes (padding of key row 0)
-  __shared__ float kn2[kBC];
+  // largest Euclidean norm of the tile's key codes (padding of key row 0),
+  // each key's squares summed in code order
   if (tid < kBC) {
     float acc = 0.f;
-    if (j0 + tid < n)
+    if (small_k) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc = fmaf(kx[e], kx[e], acc);
+    } else if (tid < nk) {
       for (int e = 0; e < k; ++e) {
         const float x = load_val(k_val, c0 + (int64_t)tid * k + e, vfmt);
         acc = fmaf(x, x, acc);
       }
-    kn2[tid] = acc;
+    }
+    const float mx = wave_max_dpp(acc);  // wave 0, all 64 lanes
+    if (tid == 0) *(float*)(T + NP * D) = sqrtf(mx) * (1.f + 1.f / 256.f);
   }
-  __syncthreads();
-  if (tid == 0) {
-    float mx = 0.f;
-    for (int j = 0; j < kBC; ++j) mx = fmaxf(mx, kn2[j]);
-    *(float*)(T + NP * D) = sqrtf(mx) * (1.f + 1.f / 256.f);
-  }
-  const uint16_t* src = v + ((int64_t)bh * n + j0) * D;
-  for (int c = tid; c < kBC * D / 8; c += 256) {  // 16-byte chunks: key j, dims d0..d0+7
-    const int j = c / (D / 8), d0 = (c % (D / 8)) * 8;
-    if (j0 + j >= n) break;
-    const uint4 w4 = *(const uint4*)(src + (int64_t)j * D + d0);
-    const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+  for (int i = 0; i < VC; ++i) {
+    const int c = tid + 256 * i, j = c / (D / 8), d0 = (c % (D / 8)) * 8;
+    if (j >= nk) continue;  // keys past n stay zero
+    const uint32_t w[4] = {vw[i].x, vw[i].y, vw[i].z, vw[i].w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       over |= (w[e] & 0x7fffu) >= 0x4780u || ((w[e] >> 16) & 0x7fffu) >= 0x4780u;
@@ -1580,13 +1638,14 @@ __global__ void sfa_fwd_ix_stat_zero_kernel(uint32_t* stat) { stat[threadIdx.x] 
 int fwd_max_group() { return 128; }
 
 // Workspace (bf16 V): the dense tile images, one V range flag per tile, the
-// index-mode tile images and the index mode's statistic.
+// hand-back count (own 256-byte block), the index-mode tile images and the
+// index mode's statistic.
 size_t fwd_workspace_bytes(int B, int Hkv, int n, int d, int vbf16) {
   if (!vbf16) return 0;
   const size_t tiles = (size_t)B * Hkv * (size_t)((n + kBC - 1) / kBC);
   const size_t sb = d == 64 ? stage_bytes<64, true>() : stage_bytes<128, true>();
   const size_t ix = d == kIxD ? tiles * IxGeo<kIxD, kIxMaxK>::SB + 256 : 0;
-  return tiles * sb + (tiles * 4 + 255) / 256 * 256 + ix;
+  return tiles * sb + (tiles * 4 + 255) / 256 * 256 + 256 + ix;
 }
 
 hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_idx,
@@ -1616,12 +1675,14 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
   p.vtiles = (n + kBC - 1) / kBC;
   p.ws_tiles = (const unsigned char*)ws;
   p.ws_flag = nullptr;
+  p.hb_count = nullptr;
   if (vbf16) {
     const size_t tiles = (size_t)B * Hkv * p.vtiles;
     const size_t sb = d == 64 ? stage_bytes<64, true>() : stage_bytes<128, true>();
     const size_t sbx = IxGeo<kIxD, kIxMaxK>::SB;
     p.ws_flag = (const int*)((unsigned char*)ws + tiles * sb);
-    unsigned char* wx = (unsigned char*)ws + tiles * sb + (tiles * 4 + 255) / 256 * 256;
+    p.hb_count = (int*)((unsigned char*)ws + tiles * sb + (tiles * 4 + 255) / 256 * 256);
+    unsigned char* wx = (unsigned char*)p.hb_count + 256;
     uint32_t* stat = (uint32_t*)(wx + tiles * sbx);
     dim3 grid(p.vtiles, B * Hkv), block(256);
     unsigned char* wt = (unsigned char*)ws;
@@ -1639,7 +1700,7 @@ hipError_t launch_attn_fwd(const void* q_idx, const void* q_val, const void* k_i
     }
 #define SFA_PREP(DD, KK)                                                                        \
   hipLaunchKernelGGL((sfa_fwd_prep_kernel<DD, KK>), grid, block, 0, stream, k_idx, k_val, vb, n, \
-                     k, ifmt, vfmt, p.vtiles, wt, wf, gstat, p.ix_thresh)
+                     k, ifmt, vfmt, p.vtiles, wt, wf, gstat, p.ix_thresh, p.hb_count)
     if (d == 64) {
       if (p.kx == kValBF16) SFA_PREP(64, kValBF16);
       else if (p.kx == kValF16) SFA_PREP(64, kValF16);
