@@ -201,8 +201,9 @@ def bench_fwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32", 
                      "per coordinate block, scale applied in fp32); softmax fp32; P.V fp16 MFMA on V "
                      "converted exactly to fp16, fp32 accumulate; O bf16")
     else:
-        precision = ("codes fp32; scores fp32 (three bf16 piece products on MFMA); softmax fp32; "
-                     "P.V fp16 MFMA on V converted exactly to fp16, fp32 accumulate; O bf16")
+        precision = ("codes fp32; scores fp32 (three products of float16 pieces on MFMA, ~3*2^-22 "
+                     "relative); softmax fp32; P.V fp16 MFMA on V converted exactly to fp16, fp32 "
+                     "accumulate; O bf16")
     hbm = _fwd_bytes(w, idt, vdt)
     out = {
         "metric": metric,
