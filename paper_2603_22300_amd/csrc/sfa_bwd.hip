@@ -24,7 +24,9 @@
 //       dP^T = V dO^T, dS^T, dQ~^T += K~^T dS^T over the allowed key tiles;
 //   sfa_bwd_dkv_kernel    key-parallel: S = Q~ K~^T, dP = dO V^T, dS,
 //       dV^T += dO^T P and dK~^T += Q~^T dS over the query tiles of every
-//       query head of the KV head.
+//       query head of the KV head;
+//   sfa_bwd_dkvf_kernel   both products from one S, P, dP, dS per tile pair
+//       (d = 64, bf16 V and O, in place of the two above).
 // Every output element is owned by one wavefront: no atomics.  The tile
 // images are copied global -> LDS with direct-to-LDS loads.
 #include "sfa_device.h"
@@ -680,18 +682,226 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// dk and dv fused: key-parallel, with S, P, dP and dS computed once per
+// (query tile, key tile) for both products (72 MFMAs per 32 x 32 tile pair
+// with 32-bit codes and bf16 V / dO at d = 128, against 96 in the two
+// kernels above).  A wave's state (K~ and V operands of its 32 keys, the dV
+// and dK~ accumulators) takes more registers than two waves per SIMD allow,
+// so a workgroup is four waves over 128 keys, at one or two waves per SIMD.
+// LDS holds two stages of the whole query image.  Used at d = 64 with bf16 V
+// and O (gpt2s shape: 0.46 -> 0.38 ms per backward); at d = 128 the single
+// wave per SIMD leaves the dependency chain of a tile (S -> P -> dV, dK)
+// exposed and the two kernels above are faster (66.8 against 82.5 ms on
+// qwen3_32k).
+// ---------------------------------------------------------------------------
+constexpr int kNWF = 4;
+
+template <int D, bool VEX, bool OEX>
+constexpr bool fused_dkv() { return D == 64 && VEX && OEX; }
+
+template <int D, bool VEX, bool OEX, bool CEX>
+__global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
+  using I = Img<D>;
+  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, QB = I::QB;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = p.n;
+  int xb, bh;
+  xcd_map((int)gridDim.x, xb, bh);
+  const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+  const int j0b = xb * (kNWF * kT);  // most query tiles first: smallest j0 first
+  const int jw0 = j0b + wave * kT;
+  const int my_j = jw0 + l32;
+  const bool wave_ok = jw0 < n;
+  const bool key_ok = my_j < n;
+
+  bf16x8 kB[2][NKB], vB[2][NKB];
+  if (wave_ok) {
+    const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
+    load_rows_b<D>(kimg, I::K_RMK, l32, hh, kB);
+    load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
+  } else {
+#pragma unroll
+    for (int pc = 0; pc < 2; ++pc)
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        kB[pc][kb] = bf16x8{};
+        vB[pc][kb] = bf16x8{};
+      }
+  }
+  floatx16 accV[NDB], accK[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      accV[db][r] = 0.f;
+      accK[db][r] = 0.f;
+    }
+
+  // query tiles that see a key of the block, swept from the highest down,
+  // the G heads of a tile together (as in sfa_bwd_dkv_kernel)
+  const bool win = p.window > 0;
+  int t_lo = p.causal ? j0b / kT : 0, t_hi = p.nt - 1, gq_end = 0;
+  if (win && j0b >= p.n_global) {
+    const int jlast = min(n, j0b + kNWF * kT) - 1;
+    t_hi = min(p.nt - 1, (jlast + p.window - 1) / kT);
+    if (!p.causal) {
+      t_lo = max(0, j0b - p.window + 1) / kT;
+      gq_end = min(t_lo, (p.n_global + kT - 1) / kT);
+    }
+  }
+  const int nrange = t_hi - t_lo + 1;
+  const int total = p.G * (nrange + gq_end);
+  auto tile_of = [&](int it) {
+    const int x = it / p.G;
+    return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
+  };
+  auto in_window = [&](int q0) {
+    return !win || q0 < p.n_global || jw0 < p.n_global ||
+           (q0 < jw0 + kT - 1 + p.window && q0 + kT - 1 > jw0 - p.window);
+  };
+  auto qimg_of = [&](int it) {
+    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + it % p.G) * p.nt + tile_of(it)) * QB;
+  };
+  if (total > 0) dma<kNWF>(qimg_of(0), smem, QB, wave, lane);
+  wait_vm();
+  __syncthreads();
+  for (int it = 0; it < total; ++it) {
+    // reads through `cur`, the copy of the next image through `nxt`
+    auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
+    if (it + 1 < total) dma<kNWF>(qimg_of(it + 1), nxt, QB, wave, lane);
+    const int q0 = tile_of(it) * kT;
+    if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
+      const uint16_t* rmq = (const uint16_t*)(cur + I::Q_RMQ);
+      const uint16_t* trq = (const uint16_t*)(cur + I::Q_TRQ);
+      const uint16_t* rmo = (const uint16_t*)(cur + I::Q_RMO);
+      const uint16_t* tro = (const uint16_t*)(cur + I::Q_TRO);
+      const float* l2 = (const float*)(cur + I::Q_L2);
+      const float* dd = (const float*)(cur + I::Q_D);
+      floatx16 s, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        bf16x8 a[2], g[2];
+#pragma unroll
+        for (int pc = 0; pc < 2; ++pc) {
+          a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
+        }
+        const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
+        const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
+        mfma3<!CEX, !CEX>(s, a, kk2);   // S = Q~ K~^T   (queries x keys)
+        mfma3<!OEX, !VEX>(dp, g, vv2);  // dP = dO V^T
+      }
+      // lane = key my_j; register r = query row q0 + 8(r/4) + 4hh + r%4.
+      // Every (query, key) pair of a full tile is allowed: no element mask
+      // (queries past n have L2 = +inf, hence P = 0, either way).
+      const bool wcut = win && q0 + kT > p.n_global && jw0 + kT > p.n_global &&
+                        (q0 < p.n_global || jw0 < p.n_global || q0 + kT - 1 - jw0 >= p.window ||
+                         jw0 + kT - 1 - q0 >= p.window);
+      const bool full = jw0 + kT <= n && (!p.causal || q0 >= jw0 + kT - 1) && !wcut;
+      u32x4 pw[2][2], sw[2][2];  // [kk][piece]: P and dS as bf16 pairs
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
+        const float4 d4 = *(const float4*)(dd + 8 * g4 + 4 * hh);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        const float dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+        float pv[4], sv[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const int r = 4 * g4 + x;
+          const int i = q0 + 8 * g4 + 4 * hh + x;
+          float pr;
+          if (full) {
+            pr = __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x]));
+          } else {
+            const bool ok = key_ok && (!p.causal || i >= my_j) &&
+                            (!win || abs(i - my_j) < p.window || i < p.n_global || my_j < p.n_global);
+            pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x])) : 0.f;
+          }
+          pv[x] = pr;
+          sv[x] = pr * (dp[r] - dv4[x]);
+        }
+#pragma unroll
+        for (int x = 0; x < 4; x += 2) {
+          const int r = 4 * g4 + x;
+          uint32_t hw, lw;
+          split2_pair(pv[x], pv[x + 1], hw, lw);
+          pw[r >> 3][0][(r & 7) >> 1] = hw;
+          pw[r >> 3][1][(r & 7) >> 1] = lw;
+          split2_pair(sv[x], sv[x + 1], hw, lw);
+          sw[r >> 3][0][(r & 7) >> 1] = hw;
+          sw[r >> 3][1][(r & 7) >> 1] = lw;
+        }
+      }
+      // dV^T += dO^T P  and  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int kbase = 16 * kk + 4 * hh;
+        const bf16x8 pb[2] = {__builtin_bit_cast(bf16x8, pw[kk][0]), __builtin_bit_cast(bf16x8, pw[kk][1])};
+        const bf16x8 sb[2] = {__builtin_bit_cast(bf16x8, sw[kk][0]), __builtin_bit_cast(bf16x8, sw[kk][1])};
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8 ao[2] = {tr_load(tro, db * 32 + l32, kbase), tr_load(tro, D + db * 32 + l32, kbase)};
+          mfma3<!OEX, true>(accV[db], ao, pb);
+          const bf16x8 aq[2] = {tr_load(trq, db * 32 + l32, kbase), tr_load(trq, D + db * 32 + l32, kbase)};
+          mfma3<!CEX, true>(accK[db], aq, sb);
+        }
+      }
+    }
+    };
+    tile(smem + (it & 1) * QB, smem + ((it + 1) & 1) * QB);
+    wait_vm();  // the next image has landed
+    __syncthreads();
+  }
+
+  // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
+  if (key_ok) {
+    float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *(float4*)(dvr + db * 32 + 8 * g4 + 4 * hh) =
+            make_float4(accV[db][4 * g4], accV[db][4 * g4 + 1], accV[db][4 * g4 + 2], accV[db][4 * g4 + 3]);
+  }
+  // dk_val = scale * dK~ at the key's support, through LDS (the stages are
+  // free): [wave][key][coordinate], pitch D + 4
+  float* L = (float*)smem + wave * kT * (D + 4);
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = accK[db][r];
+  __syncthreads();
+  if (key_ok) {
+    const int64_t row = (int64_t)bh * n + my_j;
+    for (int t = hh; t < p.k; t += 2) {
+      const int u = load_idx(p.k_idx, row * p.k + t, p.ifmt, D - 1);
+      p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+    }
+  }
+}
+
 template <int D, bool VEX, bool OEX, bool CEX>
 hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   using I = Img<D>;
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipSuccess;
-    const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
+    const void* fns[6] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
                           (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>,
                           (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>,
-                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>};
-    const int bytes[5] = {I::QB, I::KB, 2 * I::KB, kQS * I::DV_LEN, kQS * I::DK_LEN};
-    for (int f = 0; f < 5 && e == hipSuccess; ++f)
+                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>,
+                          (const void*)sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>};
+    const int bytes[6] = {I::QB, I::KB, 2 * I::KB, kQS * I::DV_LEN, kQS * I::DK_LEN, 2 * I::QB};
+    // (the fused kernel is instantiated for every type combination, launched
+    // only where fused_dkv holds)
+    for (int f = 0; f < 6 && e == hipSuccess; ++f)
       if (bytes[f] > 65536) e = hipFuncSetAttribute(fns[f], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[f]);
     if (e != hipSuccess) return e;
     configured = true;
@@ -705,6 +915,13 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   hipLaunchKernelGGL(sfa_bwd_kprep_kernel<D>, dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
   hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX, CEX>), dim3(p.nqb, B * p.Hkv), dim3(kNWQ * 64),
                      2 * I::KB, stream, p);
+  static_assert(2 * I::QB <= 160 * 1024 && 2 * I::QB >= kNWF * kT * (D + 4) * 4, "fused dk/dv stages");
+  if constexpr (fused_dkv<D, VEX, OEX>()) {
+    const int nkf = (p.n + kNWF * kT - 1) / (kNWF * kT);
+    hipLaunchKernelGGL((sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>), dim3(nkf, B * p.Hkv), dim3(kNWF * 64),
+                       2 * I::QB, stream, p);
+    return hipGetLastError();
+  }
   const int nkb = (p.n + kNW * kT - 1) / (kNW * kT);
   hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
                      kQS * I::DV_LEN, stream, p);

@@ -97,6 +97,44 @@ def test_bf16_output_and_grad():
 
 
 @pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal",
+    [
+        (1, 4, 1, 300, 64, 16, True),     # three 128-key blocks, ragged, GQA 4:1
+        (2, 2, 2, 129, 64, 8, False),     # one key past a block, non-causal
+        (1, 8, 2, 256, 64, 1, True),      # k = 1, whole blocks
+        (1, 2, 1, 200, 64, 64, True),     # k = d: dense attention gradients
+        (1, 12, 12, 1024, 64, 16, True),  # the gpt2s head shape, one sequence
+    ])
+def test_d64_bf16_fused(B, Hq, Hkv, n, d, k, causal):
+    """d = 64 with bf16 V, O and dO and 32-bit codes: dk and dv come from
+    one S, P, dP, dS per tile pair (the fused key-parallel kernel)."""
+    _run(B, Hq, Hkv, n, d, k, causal, True, seed=5 * n + k, o_bf16=True)
+
+
+def test_d64_bf16_fused_window():
+    """The fused d = 64 kernel under a token window with global tokens."""
+    B, Hq, Hkv, n, d, k, w, g = 1, 4, 2, 700, 64, 16, 150, 3
+    seed = 11
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed, v_dtype=torch.bfloat16, device=DEV)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    scale = 1 / math.sqrt(d)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=True, scale=scale, o_dtype=torch.bfloat16,
+                              window=w, n_global=g)
+    dout = si.normal((B, Hq, n, d), seed, "dout", device=DEV).to(torch.bfloat16)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=True, scale=scale,
+                                  window=w, n_global=g)
+    torch.cuda.synchronize()
+    gq, gk, gv = oracle.attn_bwd(qi.cpu().numpy(), qv.cpu().numpy(), ki.cpu().numpy(),
+                                 kv.cpu().numpy(), np_vals(v), np_vals(dout), d, scale, True,
+                                 window=w, n_global=g)
+    tol = TOL_GRAD[(True, True)]
+    check_grad(dq, gq, tol, "dq_val (fused d = 64, window)")
+    check_grad(dk, gk, tol, "dk_val (fused d = 64, window)")
+    check_grad(dv, gv, tol, "dv (fused d = 64, window)")
+
+
+@pytest.mark.parametrize(
     "B,Hq,Hkv,n,d,k,causal,o_bf16",
     [
         (1, 4, 2, 150, 128, 16, True, True),   # bf16 codes, V, O, dO: one-piece code products
