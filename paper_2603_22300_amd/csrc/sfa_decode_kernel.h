@@ -87,7 +87,12 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   constexpr int KPL = 64 / DL;  // keys per wave-wide V load
   constexpr int NR = 64 / KPL;  // V loads per lane per 64-key sub-block
   __shared__ float qd[D][G];
+  // P of the wave's 64 keys, [key][head] in float32; the 8-bit cache keeps
+  // them as float16 pairs instead, in the order its P.V loop reads them:
+  // slot (r / 2) * KPL + ksub holds keys r * KPL + ksub (low half) and
+  // (r + 1) * KPL + ksub (high half), r even, one pair per head.
   __shared__ float pbuf[kDecWaves][64][G];
+  uint32_t* pb2 = (uint32_t*)&pbuf[0][0][0];  // 8-bit cache: [wave][32 slots][G]
   __shared__ float red_m[kDecWaves][G], red_l[kDecWaves][G];
   __shared__ float red_o[kDecWaves][G][D];
 
@@ -211,7 +216,13 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
       m_run[h] = m_new;
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[h][e] *= alpha;
-      pbuf[wave][lane][h] = pj * pfac;
+      if constexpr (Q8) {
+        const int r = lane / KPL;
+        _Float16* dst = (_Float16*)&pb2[(wave * 32 + (r >> 1) * KPL + lane % KPL) * G + h];
+        dst[r & 1] = (_Float16)(pj * pfac);
+      } else {
+        pbuf[wave][lane][h] = pj * pfac;
+      }
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -232,13 +243,17 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
     uint32_t cidx[NIW], cval[NVW];
     float ksc = 1.f, vsc = 1.f;  // 8-bit cache: the key's code and value-row scales
     auto load_codes = [&](int sb) {
-      const int64_t row = row_of(min(sb + lane, w1 - 1));
+      // contiguous cache: a wave-uniform base row and 32-bit lane offsets
+      const int64_t row = PAGED ? row_of(min(sb + lane, w1 - 1)) : kv_row0 + sb;
+      const int lo = PAGED ? 0 : min(lane, w1 - 1 - sb);
       if constexpr (Q8) {
-        ksc = p.kc_scale[row];
-        vsc = p.v_scale[row];
+        ksc = (p.kc_scale + row)[lo];
+        vsc = (p.v_scale + row)[lo];
       }
-      const uint32_t* pi = (const uint32_t*)((const unsigned char*)p.kc_idx + row * (4 * NIW));
-      const uint32_t* pv = (const uint32_t*)((const unsigned char*)p.kc_val + row * (4 * NVW));
+      const uint32_t* pi = (const uint32_t*)((const unsigned char*)p.kc_idx + row * (4 * NIW) +
+                                             (uint32_t)lo * (4 * NIW));
+      const uint32_t* pv = (const uint32_t*)((const unsigned char*)p.kc_val + row * (4 * NVW) +
+                                             (uint32_t)lo * (4 * NVW));
       if constexpr (NIW % 4 == 0) {
 #pragma unroll
         for (int c = 0; c < NIW / 4; ++c) {
@@ -266,14 +281,29 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
       // key per lane: 16 bytes of bf16, or 8 bytes of int8)
       uint4 vraw[Q8 ? 1 : NR];
       uint2 vraw8[Q8 ? NR : 1];
+      constexpr int VB = Q8 ? 1 : 2;  // bytes per V value
+      if constexpr (!PAGED) {
+        // a wave-uniform base row and 32-bit lane offsets (keys clamped
+        // into the range)
+        const unsigned char* vb = (const unsigned char*)p.v + (kv_row0 + sb) * (int64_t)(D * VB);
+        const int jlast = w1 - 1 - sb;
 #pragma unroll
-      for (int r = 0; r < NR; ++r) {
-        const int jg = min(sb + r * KPL + ksub, w1 - 1);
-        const int64_t row = row_near(min(sb + r * KPL, w1 - 1), jg);
-        if constexpr (Q8)
-          vraw8[r] = *(const uint2*)((const int8_t*)p.v + row * D + dsub * 8);
-        else
-          vraw[r] = *(const uint4*)((const uint16_t*)p.v + row * D + dsub * 8);
+        for (int r = 0; r < NR; ++r) {
+          const int jj = min(r * KPL + ksub, jlast);
+          const unsigned char* src = vb + (uint32_t)((jj * D + dsub * 8) * VB);
+          if constexpr (Q8) vraw8[r] = *(const uint2*)src;
+          else vraw[r] = *(const uint4*)src;
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+          const int jg = min(sb + r * KPL + ksub, w1 - 1);
+          const int64_t row = row_near(min(sb + r * KPL, w1 - 1), jg);
+          if constexpr (Q8)
+            vraw8[r] = *(const uint2*)((const int8_t*)p.v + row * D + dsub * 8);
+          else
+            vraw[r] = *(const uint4*)((const uint16_t*)p.v + row * D + dsub * 8);
+        }
       }
       // scores, lane = key
       float s[G];
@@ -309,10 +339,11 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
 #pragma unroll
         for (int r = 0; r < NR; r += 2) {
           const int j0 = r * KPL + ksub, j1 = j0 + KPL;
+          (void)j1;
           h2 pp[G];
+          const uint32_t* ps = &pb2[(wave * 32 + (r >> 1) * KPL + ksub) * G];
 #pragma unroll
-          for (int h = 0; h < G; ++h)
-            pp[h] = (h2){(_Float16)pbuf[wave][j0][h], (_Float16)pbuf[wave][j1][h]};
+          for (int h = 0; h < G; ++h) pp[h] = __builtin_bit_cast(h2, ps[h]);
 #pragma unroll
           for (int half = 0; half < 2; ++half) {  // dims 4 half .. 4 half + 3
             const uint32_t x0 = (half ? vraw8[r].y : vraw8[r].x) ^ 0x80808080u;
