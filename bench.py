@@ -44,12 +44,18 @@ import sfa_inputs as si  # noqa: E402
 METRIC = "SFA fwd tokens/s at n=32K,d=128,k=16; % of HBM/MFMA roofline"
 PEAK_MFMA_BF16 = 2.5e15      # dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12            # bytes/s
+# the decode kernel: its launcher and the header holding the kernel template
+DECODE_SRC = "sfa_decode.hip+sfa_decode_kernel.h"
 DEV = "cuda"
 
 
 def _src_hash(name: str) -> str:
-    p = os.path.join(ROOT, "paper_2603_22300_amd", "csrc", name)
-    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+    """sha256[:16] of a kernel source, or of several joined by '+' (a source
+    and the header that holds its kernel template)."""
+    h = hashlib.sha256()
+    for part in name.split("+"):
+        h.update(open(os.path.join(ROOT, "paper_2603_22300_amd", "csrc", part), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def _traffic(kernel_file: str, workload: str):
@@ -530,7 +536,7 @@ def bench_decode(w, steps, warmup, want_cpu, codes="i16bf16", window=0, n_global
                    "step": "sfa_attn_decode (split context + LSE merge)"},
         "roofline": {"kernel": "sfa_decode_kernel + combine", "bound": "hbm",
                      "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM, "traffic": _traffic("sfa_decode.hip", w.name),
+                     "frac": achieved / PEAK_HBM, "traffic": _traffic(DECODE_SRC, w.name),
                      "algorithmic_bytes_per_launch": algo_bytes},
         "timing": {"step": _pstats(step_ms)},
     }
