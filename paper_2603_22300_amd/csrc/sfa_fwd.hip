@@ -775,8 +775,8 @@ __device__ __forceinline__ void fwd_block(const FwdParams& p, const int qb, cons
   // A: scores(0)  B: scores(1) || softmax(0)  C: P.V(0) || softmax(1)
   // D: P.V(1) || next tile's LDS writes.  Within B, C and D the source is
   // sliced by hand (one MFMA group plus its share of independent VALU work,
-  // operands read one slice ahead) and sched_barrier fences keep that order,
-  // so the matrix pipe and the VALU work side by side.  The maximum stays
+  // operands read one slice ahead), so that the matrix pipe and the VALU
+  // work side by side.  The maximum stays
   // fixed unless a sub-tile exceeds it by 2^kLazyMax: after A that hands the
   // tile to generic_tile (returns false); after B it is fixed up in place.
   auto ka_load = [&](bf16x8 (&ka)[NP], int s, int kb, const uint16_t* Kd) {
