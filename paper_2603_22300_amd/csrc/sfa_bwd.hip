@@ -893,16 +893,18 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipSuccess;
-    const void* fns[6] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
+    const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
                           (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>,
                           (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>,
-                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>,
-                          (const void*)sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>};
-    const int bytes[6] = {I::QB, I::KB, 2 * I::KB, kQS * I::DV_LEN, kQS * I::DK_LEN, 2 * I::QB};
-    // (the fused kernel is instantiated for every type combination, launched
-    // only where fused_dkv holds)
-    for (int f = 0; f < 6 && e == hipSuccess; ++f)
+                          (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>};
+    const int bytes[5] = {I::QB, I::KB, 2 * I::KB, kQS * I::DV_LEN, kQS * I::DK_LEN};
+    for (int f = 0; f < 5 && e == hipSuccess; ++f)
       if (bytes[f] > 65536) e = hipFuncSetAttribute(fns[f], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[f]);
+    if constexpr (fused_dkv<D, VEX, OEX>()) {
+      if (e == hipSuccess && 2 * I::QB > 65536)
+        e = hipFuncSetAttribute((const void*)sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, 2 * I::QB);
+    }
     if (e != hipSuccess) return e;
     configured = true;
   }
