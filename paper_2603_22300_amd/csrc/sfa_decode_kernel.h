@@ -96,7 +96,8 @@ __global__ __launch_bounds__(kDecThreads) void sfa_decode_kernel(DecParams p) {
   __shared__ float red_m[kDecWaves][G], red_l[kDecWaves][G];
   __shared__ float red_o[kDecWaves][G][D];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: per-wave values stay scalar
   const int bh = blockIdx.y;
   const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
   const int L = seq_len_of(p.seq_len, b, p.Lmax);
