@@ -29,6 +29,8 @@
 //       (d = 64, bf16 V and O, in place of the two above).
 // Every output element is owned by one wavefront: no atomics.  The tile
 // images are copied global -> LDS with direct-to-LDS loads.
+#include <type_traits>
+
 #include "sfa_device.h"
 #include "sfa_launch.h"
 
@@ -390,27 +392,32 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
                          j0 + kT - 1 - pos0 >= p.window);
       const bool full = j0 + kT <= n && (!p.causal || j0 + kT - 1 <= pos0) && !wcut;
       u32x4 dsw[2][2];  // [kk][piece], as bf16 pairs
+      // one straight-line body per case (FULL: no element mask), chosen once
+      // per tile: a mask test per element would become a branch per element
+      auto ds_tile = [&](auto full_c) {
+        constexpr bool FULL = decltype(full_c)::value;
 #pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        float ds[2];
+        for (int r = 0; r < 16; r += 2) {
+          float ds[2];
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
-          const int j = j0 + 8 * ((r + x) >> 2) + 4 * hh + ((r + x) & 3);
-          float pr;
-          if (full) {
-            pr = __builtin_amdgcn_exp2f(fmaf(s[r + x], p.c, -L2));
-          } else {
-            const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
-                            (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
-            pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r + x], p.c, -L2)) : 0.f;
+          for (int x = 0; x < 2; ++x) {
+            float pr = __builtin_amdgcn_exp2f(fmaf(s[r + x], p.c, -L2));
+            if constexpr (!FULL) {
+              const int j = j0 + 8 * ((r + x) >> 2) + 4 * hh + ((r + x) & 3);
+              const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
+                              (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
+              pr = ok ? pr : 0.f;
+            }
+            ds[x] = pr * (dp[r + x] - Dq);
           }
-          ds[x] = pr * (dp[r + x] - Dq);
+          uint32_t hw, lw;
+          split2_pair(ds[0], ds[1], hw, lw);
+          dsw[r >> 3][0][(r & 7) >> 1] = hw;
+          dsw[r >> 3][1][(r & 7) >> 1] = lw;
         }
-        uint32_t hw, lw;
-        split2_pair(ds[0], ds[1], hw, lw);
-        dsw[r >> 3][0][(r & 7) >> 1] = hw;
-        dsw[r >> 3][1][(r & 7) >> 1] = lw;
-      }
+      };
+      if (full) ds_tile(std::true_type{});
+      else ds_tile(std::false_type{});
       bf16x8 dsb[2][2];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
@@ -587,6 +594,10 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
                          jw0 + kT - 1 - q0 >= p.window);
       const bool full = jw0 + kT <= n && (!p.causal || q0 >= jw0 + kT - 1) && !wcut;
       u32x4 xw[2][2];  // [kk][piece]: P (dV) or dS (dK), as bf16 pairs
+      // one straight-line body per case (FULL: no element mask), chosen once
+      // per tile
+      auto px_tile = [&](auto full_c) {
+      constexpr bool FULL = decltype(full_c)::value;
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
@@ -600,14 +611,12 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
           const int r = 4 * g4 + x;
-          const int i = q0 + 8 * g4 + 4 * hh + x;
-          float pr;
-          if (full) {
-            pr = __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x]));
-          } else {
+          float pr = __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x]));
+          if constexpr (!FULL) {
+            const int i = q0 + 8 * g4 + 4 * hh + x;
             const bool ok = key_ok && (!p.causal || i >= my_j) &&
                             (!win || abs(i - my_j) < p.window || i < p.n_global || my_j < p.n_global);
-            pr = ok ? __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x])) : 0.f;
+            pr = ok ? pr : 0.f;
           }
           val[x] = PART == kDV ? pr : pr * (dp[r] - dv4[x]);
         }
@@ -620,6 +629,9 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
           xw[r >> 3][1][(r & 7) >> 1] = lw;
         }
       }
+      };
+      if (full) px_tile(std::true_type{});
+      else px_tile(std::false_type{});
       bf16x8 xb[2][2];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
@@ -804,6 +816,8 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
                          jw0 + kT - 1 - q0 >= p.window);
       const bool full = jw0 + kT <= n && (!p.causal || q0 >= jw0 + kT - 1) && !wcut;
       u32x4 pw[2][2], sw[2][2];  // [kk][piece]: P and dS as bf16 pairs
+      // (one body with the mask test per element: the two-body form of the
+      // kernels above costs this kernel its second wave per SIMD)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
