@@ -83,6 +83,7 @@ struct BwdParams {
   int nt;    // tiles per head: ceil(n / 32)
   int BR;    // query positions per dq workgroup: 256 / G
   int nqb;   // dq workgroups per (batch, KV head)
+  int lg;    // log2(G): the matrix-core kernels run power-of-two groups
   float scale, c;  // c = scale * log2(e)
 };
 
@@ -530,7 +531,7 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   const int nrange = t_hi - t_lo + 1;
   const int total = p.G * (nrange + gq_end);
   auto tile_of = [&](int it) {
-    const int x = it / p.G;
+    const int x = it >> p.lg;
     return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
   };
   // a query tile from q0 on meets the window of some key of this wave
@@ -543,7 +544,7 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   constexpr int ROFF = PART == kDV ? I::DV_OFF : I::DK_OFF;
   constexpr int RLEN = PART == kDV ? I::DV_LEN : I::DK_LEN;
   auto qimg_of = [&](int it) {
-    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + it % p.G) * p.nt + tile_of(it)) * I::QB + ROFF;
+    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + (it & (p.G - 1))) * p.nt + tile_of(it)) * I::QB + ROFF;
   };
   // three stages: the image two tiles ahead is in flight while a tile is
   // consumed (vmcnt waits only for the one needed next)
@@ -767,7 +768,7 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   const int nrange = t_hi - t_lo + 1;
   const int total = p.G * (nrange + gq_end);
   auto tile_of = [&](int it) {
-    const int x = it / p.G;
+    const int x = it >> p.lg;
     return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
   };
   auto in_window = [&](int q0) {
@@ -775,7 +776,7 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
            (q0 < jw0 + kT - 1 + p.window && q0 + kT - 1 > jw0 - p.window);
   };
   auto qimg_of = [&](int it) {
-    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + it % p.G) * p.nt + tile_of(it)) * QB;
+    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + (it & (p.G - 1))) * p.nt + tile_of(it)) * QB;
   };
   if (total > 0) dma<kNWF>(qimg_of(0), smem, QB, wave, lane);
   wait_vm();
@@ -973,6 +974,7 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
   p.nt = (n + kT - 1) / kT;
   p.BR = kNWQ * kT / p.G;
   p.nqb = (n + p.BR - 1) / p.BR;
+  p.lg = __builtin_ctz((unsigned)p.G);  // G is a power of two here (checked by the caller)
   p.scale = scale;
   p.c = (float)((double)scale * 1.4426950408889634);
   const size_t qbytes = (size_t)B * Hq * p.nt * (d == 64 ? Img<64>::QB : Img<128>::QB);
