@@ -28,7 +28,11 @@
 //   sfa_bwd_dkvf_kernel   both products from one S, P, dP, dS per tile pair
 //       (d = 64, bf16 V and O, in place of the two above).
 // Every output element is owned by one wavefront: no atomics.  The tile
-// images are copied global -> LDS with direct-to-LDS loads.
+// images are copied global -> LDS with direct-to-LDS loads.  When the
+// (batch, KV head) pairs split evenly over the 8 XCDs, the dq, dk and dv
+// kernels run persistent grids whose workgroups on one XCD sweep the same
+// tiles in step, so that each image comes from HBM about once per row of
+// blocks (qwen3_32k: 32 GB -> 16 GB of fetch per backward).
 #include <type_traits>
 
 #include "sfa_device.h"
@@ -84,6 +88,9 @@ struct BwdParams {
   int BR;    // query positions per dq workgroup: 256 / G
   int nqb;   // dq workgroups per (batch, KV head)
   int lg;    // log2(G): the matrix-core kernels run power-of-two groups
+  int nkb;   // dk / dv key blocks (256 keys) per (batch, KV head)
+  int pr;    // dk / dv persistent grid: workgroups per XCD (0: one workgroup per block)
+  int pm;    // dk / dv persistent grid: blocks per XCD
   float scale, c;  // c = scale * log2(e)
 };
 
@@ -296,174 +303,195 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = p.n;
-  int xb, bh;
-  xcd_map(p.nqb, xb, bh);
-  const int qb = p.nqb - 1 - xb;  // longest causal blocks first
-  const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
-  const int i0 = qb * p.BR;
-  // wave: 32 consecutive positions of one query head (BR is a multiple of 32)
-  const int hq = hkv * p.G + (wave * kT) / p.BR;
-  const int pos0 = i0 + (wave * kT) % p.BR;
-  const int my_i = pos0 + l32;
-  const bool wave_ok = pos0 < n;
-  const bool row_ok = my_i < n;
-  const int wave_i_max = min(pos0 + kT - 1, n - 1);
-
-  bf16x8 qB[2][NKB], dB[2][NKB];
-  float L2 = INFINITY, Dq = 0.f;
-  if (wave_ok) {
-    const unsigned char* qimg = p.qimg + ((int64_t)(b * p.Hq + hq) * p.nt + pos0 / kT) * I::QB;
-    load_rows_b<D>(qimg, I::Q_RMQ, l32, hh, qB);
-    load_rows_b<D>(qimg, I::Q_RMO, l32, hh, dB);
-    L2 = ((const float*)(qimg + I::Q_L2))[l32];
-    Dq = ((const float*)(qimg + I::Q_D))[l32];
-  } else {
-#pragma unroll
-    for (int pc = 0; pc < 2; ++pc)
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        qB[pc][kb] = bf16x8{};
-        dB[pc][kb] = bf16x8{};
-      }
-  }
-  floatx16 acc[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
-
-  const int blk_last = min(n, i0 + p.BR) - 1;
-  // Key tiles of the block: all up to the causal limit, or with a token
-  // window (and no global row here) the global tiles [0, gt_end) and the
-  // window tiles [wt_begin, nkt_all); the gap between them is skipped.
-  const bool win = p.window > 0;
-  int kend = p.causal ? blk_last + 1 : n;
-  int gt_end = 0, wt_begin = 0;
-  if (win && i0 >= p.n_global) {
-    if (!p.causal) kend = min(n, blk_last + p.window);
-    gt_end = (p.n_global + kT - 1) / kT;
-    wt_begin = max(0, i0 - p.window + 1) / kT;
-    if (wt_begin <= gt_end) gt_end = wt_begin = 0;  // no gap
-  }
-  const int nkt = gt_end + (kend + kT - 1) / kT - wt_begin;
-  auto tile_at = [&](int t) { return t < gt_end ? t : wt_begin + (t - gt_end); };
-  // a key tile from j0 on meets the window of some row of this wave
-  auto in_window = [&](int j0) {
-    return !win || j0 < p.n_global || pos0 < p.n_global ||
-           (j0 + kT - 1 > pos0 - p.window && j0 < wave_i_max + p.window);
-  };
-  const unsigned char* kimg0 = p.kimg + (int64_t)bh * p.nt * I::KB;
-  if (nkt > 0) dma<kNWQ>(kimg0 + (int64_t)tile_at(0) * I::KB, smem, I::KB, wave, lane);
-  wait_vm();
-  __syncthreads();
-  for (int t = 0; t < nkt; ++t) {
-    const int stage = t & 1;
-    const int jt = tile_at(t);
-    // reads through `cur`, the copy of the next tile through `nxt` (restrict:
-    // no compiler wait on the copy before the reads)
-    auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
-    if (t + 1 < nkt) dma<kNWQ>(kimg0 + (int64_t)tile_at(t + 1) * I::KB, nxt, I::KB, wave, lane);
-    const int j0 = jt * kT;
-    if (wave_ok && (!p.causal || wave_i_max >= j0) && in_window(j0)) {
-      const unsigned char* K = cur;
-      const uint16_t* rmk = (const uint16_t*)(K + I::K_RMK);
-      const uint16_t* trk = (const uint16_t*)(K + I::K_TRK);
-      const uint16_t* rmv = (const uint16_t*)(K + I::K_RMV);
-      floatx16 s, dp;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        bf16x8 a[2], v[2];
-#pragma unroll
-        for (int pc = 0; pc < 2; ++pc) {
-          a[pc] = *(const bf16x8*)(rmk + l32 * RP + pc * D + kb * 16 + 8 * hh);
-          v[pc] = *(const bf16x8*)(rmv + l32 * RP + pc * D + kb * 16 + 8 * hh);
-        }
-        const bf16x8 qq[2] = {qB[0][kb], qB[1][kb]};
-        const bf16x8 gg[2] = {dB[0][kb], dB[1][kb]};
-        mfma3<!CEX, !CEX>(s, a, qq);   // S^T = K~ Q~^T   (keys x queries)
-        mfma3<!VEX, !OEX>(dp, v, gg);  // dP^T = V dO^T
-      }
-      // dS^T = P^T o (dP^T - D); lane = query my_i, register r = key j0 + 8(r/4) + 4hh + r%4
-      // every (row, key) pair of the tile allowed: no element mask (rows past
-      // n have L2 = +inf, hence P = 0, either way)
-      const bool wcut = win && j0 + kT > p.n_global && wave_i_max >= p.n_global &&
-                        (pos0 < p.n_global || wave_i_max - j0 >= p.window ||
-                         j0 + kT - 1 - pos0 >= p.window);
-      const bool full = j0 + kT <= n && (!p.causal || j0 + kT - 1 <= pos0) && !wcut;
-      u32x4 dsw[2][2];  // [kk][piece], as bf16 pairs
-      // one straight-line body per case (FULL: no element mask), chosen once
-      // per tile: a mask test per element would become a branch per element
-      auto ds_tile = [&](auto full_c) {
-        constexpr bool FULL = decltype(full_c)::value;
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          float ds[2];
-#pragma unroll
-          for (int x = 0; x < 2; ++x) {
-            float pr = __builtin_amdgcn_exp2f(fmaf(s[r + x], p.c, -L2));
-            if constexpr (!FULL) {
-              const int j = j0 + 8 * ((r + x) >> 2) + 4 * hh + ((r + x) & 3);
-              const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
-                              (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
-              pr = ok ? pr : 0.f;
-            }
-            ds[x] = pr * (dp[r + x] - Dq);
-          }
-          uint32_t hw, lw;
-          split2_pair(ds[0], ds[1], hw, lw);
-          dsw[r >> 3][0][(r & 7) >> 1] = hw;
-          dsw[r >> 3][1][(r & 7) >> 1] = lw;
-        }
-      };
-      if (full) ds_tile(std::true_type{});
-      else ds_tile(std::false_type{});
-      bf16x8 dsb[2][2];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int pc = 0; pc < 2; ++pc) dsb[kk][pc] = __builtin_bit_cast(bf16x8, dsw[kk][pc]);
-      // dQ~^T += K~^T dS^T   (coordinates x queries)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const int kbase = 16 * kk + 4 * hh;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8 a[2] = {tr_load(trk, db * 32 + l32, kbase), tr_load(trk, D + db * 32 + l32, kbase)};
-          mfma3<!CEX, true>(acc[db], a, dsb[kk]);
-        }
-      }
+  // Work items: (batch x KV head, block of BR positions), the longest causal
+  // blocks first.  Persistent grid (p.pr > 0) as in the key-parallel kernels
+  // below, with the key tiles swept upward on even rows and downward on odd
+  // ones.
+  for (int prow = 0;; ++prow) {
+    int xb, bh;
+    bool down = false;
+    if (p.pr > 0) {
+      const int w = (int)blockIdx.x >> 3;
+      if (prow * p.pr >= p.pm) break;
+      const int idx = prow * p.pr + ((prow & 1) ? p.pr - 1 - w : w);
+      if (idx >= p.pm) continue;  // last row: the next one breaks
+      xb = idx % p.nqb;
+      bh = ((int)blockIdx.x & 7) + 8 * (idx / p.nqb);
+      down = prow & 1;
+    } else {
+      if (prow > 0) break;
+      xcd_map(p.nqb, xb, bh);
     }
+    const int qb = p.nqb - 1 - xb;  // longest causal blocks first
+    const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+    const int i0 = qb * p.BR;
+    // wave: 32 consecutive positions of one query head (BR is a multiple of 32)
+    const int hq = hkv * p.G + (wave * kT) / p.BR;
+    const int pos0 = i0 + (wave * kT) % p.BR;
+    const int my_i = pos0 + l32;
+    const bool wave_ok = pos0 < n;
+    const bool row_ok = my_i < n;
+    const int wave_i_max = min(pos0 + kT - 1, n - 1);
+
+    bf16x8 qB[2][NKB], dB[2][NKB];
+    float L2 = INFINITY, Dq = 0.f;
+    if (wave_ok) {
+      const unsigned char* qimg = p.qimg + ((int64_t)(b * p.Hq + hq) * p.nt + pos0 / kT) * I::QB;
+      load_rows_b<D>(qimg, I::Q_RMQ, l32, hh, qB);
+      load_rows_b<D>(qimg, I::Q_RMO, l32, hh, dB);
+      L2 = ((const float*)(qimg + I::Q_L2))[l32];
+      Dq = ((const float*)(qimg + I::Q_D))[l32];
+    } else {
+#pragma unroll
+      for (int pc = 0; pc < 2; ++pc)
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+          qB[pc][kb] = bf16x8{};
+          dB[pc][kb] = bf16x8{};
+        }
+    }
+    floatx16 acc[NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
+
+    const int blk_last = min(n, i0 + p.BR) - 1;
+    // Key tiles of the block: all up to the causal limit, or with a token
+    // window (and no global row here) the global tiles [0, gt_end) and the
+    // window tiles [wt_begin, nkt_all); the gap between them is skipped.
+    const bool win = p.window > 0;
+    int kend = p.causal ? blk_last + 1 : n;
+    int gt_end = 0, wt_begin = 0;
+    if (win && i0 >= p.n_global) {
+      if (!p.causal) kend = min(n, blk_last + p.window);
+      gt_end = (p.n_global + kT - 1) / kT;
+      wt_begin = max(0, i0 - p.window + 1) / kT;
+      if (wt_begin <= gt_end) gt_end = wt_begin = 0;  // no gap
+    }
+    const int nkt = gt_end + (kend + kT - 1) / kT - wt_begin;
+    auto tile_at = [&](int t) {
+      if (down) t = nkt - 1 - t;
+      return t < gt_end ? t : wt_begin + (t - gt_end);
     };
-    tile(smem + stage * I::KB, smem + (stage ^ 1) * I::KB);
+    // a key tile from j0 on meets the window of some row of this wave
+    auto in_window = [&](int j0) {
+      return !win || j0 < p.n_global || pos0 < p.n_global ||
+             (j0 + kT - 1 > pos0 - p.window && j0 < wave_i_max + p.window);
+    };
+    const unsigned char* kimg0 = p.kimg + (int64_t)bh * p.nt * I::KB;
+    if (nkt > 0) dma<kNWQ>(kimg0 + (int64_t)tile_at(0) * I::KB, smem, I::KB, wave, lane);
     wait_vm();
     __syncthreads();
-  }
-
-  // dq_val = scale * dQ~ at the row's support: stage dQ~ through LDS
-  // (the key stages are free now), four waves at a time:
-  // [wave % 4][query][coordinate], pitch D + 4.
-  float* L = (float*)smem + (wave & 3) * kT * (D + 4);
+    for (int t = 0; t < nkt; ++t) {
+      const int stage = t & 1;
+      const int jt = tile_at(t);
+      // reads through `cur`, the copy of the next tile through `nxt` (restrict:
+      // no compiler wait on the copy before the reads)
+      auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
+      if (t + 1 < nkt) dma<kNWQ>(kimg0 + (int64_t)tile_at(t + 1) * I::KB, nxt, I::KB, wave, lane);
+      const int j0 = jt * kT;
+      if (wave_ok && (!p.causal || wave_i_max >= j0) && in_window(j0)) {
+        const unsigned char* K = cur;
+        const uint16_t* rmk = (const uint16_t*)(K + I::K_RMK);
+        const uint16_t* trk = (const uint16_t*)(K + I::K_TRK);
+        const uint16_t* rmv = (const uint16_t*)(K + I::K_RMV);
+        floatx16 s, dp;
 #pragma unroll
-  for (int round = 0; round < kNWQ / 4; ++round) {
-    if (wave / 4 == round) {
+        for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+        for (int kb = 0; kb < NKB; ++kb) {
+          bf16x8 a[2], v[2];
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
-    }
-    __syncthreads();
-    if (wave / 4 == round && row_ok) {
-      const int64_t row = ((int64_t)b * p.Hq + hq) * n + my_i;
-      for (int t = hh; t < p.k; t += 2) {
-        const int u = load_idx(p.q_idx, row * p.k + t, p.ifmt, D - 1);
-        p.dq[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+          for (int pc = 0; pc < 2; ++pc) {
+            a[pc] = *(const bf16x8*)(rmk + l32 * RP + pc * D + kb * 16 + 8 * hh);
+            v[pc] = *(const bf16x8*)(rmv + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          }
+          const bf16x8 qq[2] = {qB[0][kb], qB[1][kb]};
+          const bf16x8 gg[2] = {dB[0][kb], dB[1][kb]};
+          mfma3<!CEX, !CEX>(s, a, qq);   // S^T = K~ Q~^T   (keys x queries)
+          mfma3<!VEX, !OEX>(dp, v, gg);  // dP^T = V dO^T
+        }
+        // dS^T = P^T o (dP^T - D); lane = query my_i, register r = key j0 + 8(r/4) + 4hh + r%4
+        // every (row, key) pair of the tile allowed: no element mask (rows past
+        // n have L2 = +inf, hence P = 0, either way)
+        const bool wcut = win && j0 + kT > p.n_global && wave_i_max >= p.n_global &&
+                          (pos0 < p.n_global || wave_i_max - j0 >= p.window ||
+                           j0 + kT - 1 - pos0 >= p.window);
+        const bool full = j0 + kT <= n && (!p.causal || j0 + kT - 1 <= pos0) && !wcut;
+        u32x4 dsw[2][2];  // [kk][piece], as bf16 pairs
+        // one straight-line body per case (FULL: no element mask), chosen once
+        // per tile: a mask test per element would become a branch per element
+        auto ds_tile = [&](auto full_c) {
+          constexpr bool FULL = decltype(full_c)::value;
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            float ds[2];
+#pragma unroll
+            for (int x = 0; x < 2; ++x) {
+              float pr = __builtin_amdgcn_exp2f(fmaf(s[r + x], p.c, -L2));
+              if constexpr (!FULL) {
+                const int j = j0 + 8 * ((r + x) >> 2) + 4 * hh + ((r + x) & 3);
+                const bool ok = row_ok && j < n && (!p.causal || j <= my_i) &&
+                                (!win || abs(my_i - j) < p.window || j < p.n_global || my_i < p.n_global);
+                pr = ok ? pr : 0.f;
+              }
+              ds[x] = pr * (dp[r + x] - Dq);
+            }
+            uint32_t hw, lw;
+            split2_pair(ds[0], ds[1], hw, lw);
+            dsw[r >> 3][0][(r & 7) >> 1] = hw;
+            dsw[r >> 3][1][(r & 7) >> 1] = lw;
+          }
+        };
+        if (full) ds_tile(std::true_type{});
+        else ds_tile(std::false_type{});
+        bf16x8 dsb[2][2];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int pc = 0; pc < 2; ++pc) dsb[kk][pc] = __builtin_bit_cast(bf16x8, dsw[kk][pc]);
+        // dQ~^T += K~^T dS^T   (coordinates x queries)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int kbase = 16 * kk + 4 * hh;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) {
+            const bf16x8 a[2] = {tr_load(trk, db * 32 + l32, kbase), tr_load(trk, D + db * 32 + l32, kbase)};
+            mfma3<!CEX, true>(acc[db], a, dsb[kk]);
+          }
+        }
       }
+      };
+      tile(smem + stage * I::KB, smem + (stage ^ 1) * I::KB);
+      wait_vm();
+      __syncthreads();
     }
-    __syncthreads();
-  }
+
+    // dq_val = scale * dQ~ at the row's support: stage dQ~ through LDS
+    // (the key stages are free now), four waves at a time:
+    // [wave % 4][query][coordinate], pitch D + 4.
+    float* L = (float*)smem + (wave & 3) * kT * (D + 4);
+#pragma unroll
+    for (int round = 0; round < kNWQ / 4; ++round) {
+      if (wave / 4 == round) {
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
+      }
+      __syncthreads();
+      if (wave / 4 == round && row_ok) {
+        const int64_t row = ((int64_t)b * p.Hq + hq) * n + my_i;
+        for (int t = hh; t < p.k; t += 2) {
+          const int u = load_idx(p.q_idx, row * p.k + t, p.ifmt, D - 1);
+          p.dq[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+        }
+      }
+      __syncthreads();
+    }
+  }  // work items
 }
 
 // ---------------------------------------------------------------------------
@@ -482,217 +510,241 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = p.n;
-  int xb, bh;
-  xcd_map((int)gridDim.x, xb, bh);
-  const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
-  const int j0b = xb * (kNW * kT);  // most key tiles first: smallest j0 first
-  const int jw0 = j0b + wave * kT;
-  const int my_j = jw0 + l32;
-  const bool wave_ok = jw0 < n;
-  const bool key_ok = my_j < n;
-
-  bf16x8 kB[2][NKB], vB[2][NKB];
-  if (wave_ok) {
-    const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
-    load_rows_b<D>(kimg, I::K_RMK, l32, hh, kB);
-    if constexpr (PART == kDK) load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
-  } else {
-#pragma unroll
-    for (int pc = 0; pc < 2; ++pc)
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        kB[pc][kb] = bf16x8{};
-        vB[pc][kb] = bf16x8{};
-      }
-  }
-  floatx16 acc[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
-
-  // Query tiles of all G heads that see some key of the block, swept from
-  // the last tile down, the G heads of a tile together: every workgroup of a
-  // KV head starts on the same tile and moves at the same rate, so the
-  // resident workgroups read each tile image while it is in L2.
-  // Query tiles that see a key of the block, swept from the highest down: the
-  // range [t_lo, t_hi], and (non-causal window) the global query tiles below
-  // it, [0, gq_end).  Without a window t_hi is the last tile.
-  const bool win = p.window > 0;
-  int t_lo = p.causal ? j0b / kT : 0, t_hi = p.nt - 1, gq_end = 0;
-  if (win && j0b >= p.n_global) {
-    const int jlast = min(n, j0b + kNW * kT) - 1;
-    t_hi = min(p.nt - 1, (jlast + p.window - 1) / kT);
-    if (!p.causal) {
-      t_lo = max(0, j0b - p.window + 1) / kT;
-      gq_end = min(t_lo, (p.n_global + kT - 1) / kT);
+  // Work items: (batch x KV head, block of 256 keys).  Without the persistent
+  // grid a workgroup runs one item, placed by xcd_map.  With it (p.pr > 0,
+  // B * Hkv a multiple of 8) the grid is 8 x pr workgroups, all resident:
+  // workgroup id runs on XCD id & 7 (round-robin dispatch) in slot id >> 3,
+  // and XCD c takes the KV heads congruent to c, their blocks in rows of pr,
+  // slots reversed on every other row, query tiles swept downward on even
+  // rows and upward on odd ones.  Under causal masking a block's sweep
+  // shortens as its first key grows; with this order the workgroups of an
+  // XCD start each row together or end it together, and in between stay on
+  // the same query tile, so one L2 fetch of an image serves all of them.
+  for (int prow = 0;; ++prow) {
+    int xb, bh;
+    bool up = false;
+    if (p.pr > 0) {
+      const int w = (int)blockIdx.x >> 3;
+      if (prow * p.pr >= p.pm) break;
+      const int idx = prow * p.pr + ((prow & 1) ? p.pr - 1 - w : w);
+      if (idx >= p.pm) continue;  // last row: the next one breaks
+      xb = idx % p.nkb;
+      bh = ((int)blockIdx.x & 7) + 8 * (idx / p.nkb);
+      up = prow & 1;
+    } else {
+      if (prow > 0) break;
+      xcd_map((int)gridDim.x, xb, bh);
     }
-  }
-  const int nrange = t_hi - t_lo + 1;
-  const int total = p.G * (nrange + gq_end);
-  auto tile_of = [&](int it) {
-    const int x = it >> p.lg;
-    return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
-  };
-  // a query tile from q0 on meets the window of some key of this wave
-  auto in_window = [&](int q0) {
-    return !win || q0 < p.n_global || jw0 < p.n_global ||
-           (q0 < jw0 + kT - 1 + p.window && q0 + kT - 1 > jw0 - p.window);
-  };
-  // only this kernel's part of each image is copied; LDS holds it from
-  // image offset ROFF on
-  constexpr int ROFF = PART == kDV ? I::DV_OFF : I::DK_OFF;
-  constexpr int RLEN = PART == kDV ? I::DV_LEN : I::DK_LEN;
-  auto qimg_of = [&](int it) {
-    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + (it & (p.G - 1))) * p.nt + tile_of(it)) * I::QB + ROFF;
-  };
-  // three stages: the image two tiles ahead is in flight while a tile is
-  // consumed (vmcnt waits only for the one needed next)
-  // every wave copies at least RLEN / 1024 / kNW blocks of an image
-  constexpr int kMinCopies = RLEN / 1024 / kNW;
-  if (total > 0) dma<kNW>(qimg_of(0), smem, RLEN, wave, lane);
-  if (total > 1) dma<kNW>(qimg_of(1), smem + RLEN, RLEN, wave, lane);
-  if (total > 1) wait_vm_n<kMinCopies>(); else wait_vm();
-  __syncthreads();
-  for (int it = 0; it < total; ++it) {
-    // The tile's LDS reads go through `cur` and the copy two tiles ahead
-    // through `nxt`, both restrict: the compiler then knows the copy cannot
-    // alias those reads and does not wait for it before them.
-    auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
-    if (it + 2 < total) dma<kNW>(qimg_of(it + 2), nxt, RLEN, wave, lane);
-    const int q0 = tile_of(it) * kT;
-    if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
-      const unsigned char* Q = cur - ROFF;  // image offsets apply as is
-      const uint16_t* rmq = (const uint16_t*)(Q + I::Q_RMQ);
-      const uint16_t* trq = (const uint16_t*)(Q + I::Q_TRQ);
-      const uint16_t* rmo = (const uint16_t*)(Q + I::Q_RMO);
-      const uint16_t* tro = (const uint16_t*)(Q + I::Q_TRO);
-      const float* l2 = (const float*)(Q + I::Q_L2);
-      const float* dd = (const float*)(Q + I::Q_D);
-      floatx16 s, dp;
+    const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
+    const int j0b = xb * (kNW * kT);  // most key tiles first: smallest j0 first
+    const int jw0 = j0b + wave * kT;
+    const int my_j = jw0 + l32;
+    const bool wave_ok = jw0 < n;
+    const bool key_ok = my_j < n;
+
+    bf16x8 kB[2][NKB], vB[2][NKB];
+    if (wave_ok) {
+      const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
+      load_rows_b<D>(kimg, I::K_RMK, l32, hh, kB);
+      if constexpr (PART == kDK) load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
+    } else {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
+      for (int pc = 0; pc < 2; ++pc)
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        bf16x8 a[2];
-#pragma unroll
-        for (int pc = 0; pc < 2; ++pc) a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
-        const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
-        mfma3<!CEX, !CEX>(s, a, kk2);  // S = Q~ K~^T   (queries x keys)
-        if constexpr (PART == kDK) {
-          bf16x8 g[2];
-#pragma unroll
-          for (int pc = 0; pc < 2; ++pc) g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
-          const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
-          mfma3<!OEX, !VEX>(dp, g, vv2);  // dP = dO V^T
+        for (int kb = 0; kb < NKB; ++kb) {
+          kB[pc][kb] = bf16x8{};
+          vB[pc][kb] = bf16x8{};
         }
+    }
+    floatx16 acc[NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
+
+    // Query tiles of all G heads that see some key of the block, the G heads
+    // of a tile together, in the downward order: the range [t_lo, t_hi] from
+    // the highest tile, then (non-causal window) the global query tiles below
+    // it, [0, gq_end).  Without a window t_hi is the last tile.  `up` runs
+    // the same order backwards.
+    const bool win = p.window > 0;
+    int t_lo = p.causal ? j0b / kT : 0, t_hi = p.nt - 1, gq_end = 0;
+    if (win && j0b >= p.n_global) {
+      const int jlast = min(n, j0b + kNW * kT) - 1;
+      t_hi = min(p.nt - 1, (jlast + p.window - 1) / kT);
+      if (!p.causal) {
+        t_lo = max(0, j0b - p.window + 1) / kT;
+        gq_end = min(t_lo, (p.n_global + kT - 1) / kT);
       }
-      // lane = key my_j; register r = query row q0 + 8(r/4) + 4hh + r%4
-      // every (query, key) pair of the tile allowed: no element mask (queries
-      // past n have L2 = +inf, hence P = 0, either way)
-      const bool wcut = win && q0 + kT > p.n_global && jw0 + kT > p.n_global &&
-                        (q0 < p.n_global || jw0 < p.n_global || q0 + kT - 1 - jw0 >= p.window ||
-                         jw0 + kT - 1 - q0 >= p.window);
-      const bool full = jw0 + kT <= n && (!p.causal || q0 >= jw0 + kT - 1) && !wcut;
-      u32x4 xw[2][2];  // [kk][piece]: P (dV) or dS (dK), as bf16 pairs
-      // one straight-line body per case (FULL: no element mask), chosen once
-      // per tile
-      auto px_tile = [&](auto full_c) {
-      constexpr bool FULL = decltype(full_c)::value;
+    }
+    const int nrange = t_hi - t_lo + 1;
+    const int total = p.G * (nrange + gq_end);
+    // step it of the sweep -> position in the downward order
+    auto ord = [&](int it) { return up ? total - 1 - it : it; };
+    auto tile_of = [&](int it) {
+      const int x = ord(it) >> p.lg;
+      return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
+    };
+    // a query tile from q0 on meets the window of some key of this wave
+    auto in_window = [&](int q0) {
+      return !win || q0 < p.n_global || jw0 < p.n_global ||
+             (q0 < jw0 + kT - 1 + p.window && q0 + kT - 1 > jw0 - p.window);
+    };
+    // only this kernel's part of each image is copied; LDS holds it from
+    // image offset ROFF on
+    constexpr int ROFF = PART == kDV ? I::DV_OFF : I::DK_OFF;
+    constexpr int RLEN = PART == kDV ? I::DV_LEN : I::DK_LEN;
+    auto qimg_of = [&](int it) {
+      return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + (ord(it) & (p.G - 1))) * p.nt + tile_of(it)) * I::QB + ROFF;
+    };
+    // three stages: the image two tiles ahead is in flight while a tile is
+    // consumed (vmcnt waits only for the one needed next)
+    // every wave copies at least RLEN / 1024 / kNW blocks of an image
+    constexpr int kMinCopies = RLEN / 1024 / kNW;
+    if (total > 0) dma<kNW>(qimg_of(0), smem, RLEN, wave, lane);
+    if (total > 1) dma<kNW>(qimg_of(1), smem + RLEN, RLEN, wave, lane);
+    if (total > 1) wait_vm_n<kMinCopies>(); else wait_vm();
+    __syncthreads();
+    for (int it = 0; it < total; ++it) {
+      // The tile's LDS reads go through `cur` and the copy two tiles ahead
+      // through `nxt`, both restrict: the compiler then knows the copy cannot
+      // alias those reads and does not wait for it before them.
+      auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
+      if (it + 2 < total) dma<kNW>(qimg_of(it + 2), nxt, RLEN, wave, lane);
+      const int q0 = tile_of(it) * kT;
+      if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
+        const unsigned char* Q = cur - ROFF;  // image offsets apply as is
+        const uint16_t* rmq = (const uint16_t*)(Q + I::Q_RMQ);
+        const uint16_t* trq = (const uint16_t*)(Q + I::Q_TRQ);
+        const uint16_t* rmo = (const uint16_t*)(Q + I::Q_RMO);
+        const uint16_t* tro = (const uint16_t*)(Q + I::Q_TRO);
+        const float* l2 = (const float*)(Q + I::Q_L2);
+        const float* dd = (const float*)(Q + I::Q_D);
+        floatx16 s, dp;
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-        float dv4[4] = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (PART == kDK) {
-          const float4 d4 = *(const float4*)(dd + 8 * g4 + 4 * hh);
-          dv4[0] = d4.x; dv4[1] = d4.y; dv4[2] = d4.z; dv4[3] = d4.w;
-        }
-        float val[4];
+        for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          const int r = 4 * g4 + x;
-          float pr = __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x]));
-          if constexpr (!FULL) {
-            const int i = q0 + 8 * g4 + 4 * hh + x;
-            const bool ok = key_ok && (!p.causal || i >= my_j) &&
-                            (!win || abs(i - my_j) < p.window || i < p.n_global || my_j < p.n_global);
-            pr = ok ? pr : 0.f;
+        for (int kb = 0; kb < NKB; ++kb) {
+          bf16x8 a[2];
+#pragma unroll
+          for (int pc = 0; pc < 2; ++pc) a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
+          mfma3<!CEX, !CEX>(s, a, kk2);  // S = Q~ K~^T   (queries x keys)
+          if constexpr (PART == kDK) {
+            bf16x8 g[2];
+#pragma unroll
+            for (int pc = 0; pc < 2; ++pc) g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
+            const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
+            mfma3<!OEX, !VEX>(dp, g, vv2);  // dP = dO V^T
           }
-          val[x] = PART == kDV ? pr : pr * (dp[r] - dv4[x]);
         }
+        // lane = key my_j; register r = query row q0 + 8(r/4) + 4hh + r%4
+        // every (query, key) pair of the tile allowed: no element mask (queries
+        // past n have L2 = +inf, hence P = 0, either way)
+        const bool wcut = win && q0 + kT > p.n_global && jw0 + kT > p.n_global &&
+                          (q0 < p.n_global || jw0 < p.n_global || q0 + kT - 1 - jw0 >= p.window ||
+                           jw0 + kT - 1 - q0 >= p.window);
+        const bool full = jw0 + kT <= n && (!p.causal || q0 >= jw0 + kT - 1) && !wcut;
+        u32x4 xw[2][2];  // [kk][piece]: P (dV) or dS (dK), as bf16 pairs
+        // one straight-line body per case (FULL: no element mask), chosen once
+        // per tile
+        auto px_tile = [&](auto full_c) {
+        constexpr bool FULL = decltype(full_c)::value;
 #pragma unroll
-        for (int x = 0; x < 4; x += 2) {
-          const int r = 4 * g4 + x;
-          uint32_t hw, lw;
-          split2_pair(val[x], val[x + 1], hw, lw);
-          xw[r >> 3][0][(r & 7) >> 1] = hw;
-          xw[r >> 3][1][(r & 7) >> 1] = lw;
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const float4 l4 = *(const float4*)(l2 + 8 * g4 + 4 * hh);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+          float dv4[4] = {0.f, 0.f, 0.f, 0.f};
+          if constexpr (PART == kDK) {
+            const float4 d4 = *(const float4*)(dd + 8 * g4 + 4 * hh);
+            dv4[0] = d4.x; dv4[1] = d4.y; dv4[2] = d4.z; dv4[3] = d4.w;
+          }
+          float val[4];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            const int r = 4 * g4 + x;
+            float pr = __builtin_amdgcn_exp2f(fmaf(s[r], p.c, -lv[x]));
+            if constexpr (!FULL) {
+              const int i = q0 + 8 * g4 + 4 * hh + x;
+              const bool ok = key_ok && (!p.causal || i >= my_j) &&
+                              (!win || abs(i - my_j) < p.window || i < p.n_global || my_j < p.n_global);
+              pr = ok ? pr : 0.f;
+            }
+            val[x] = PART == kDV ? pr : pr * (dp[r] - dv4[x]);
+          }
+#pragma unroll
+          for (int x = 0; x < 4; x += 2) {
+            const int r = 4 * g4 + x;
+            uint32_t hw, lw;
+            split2_pair(val[x], val[x + 1], hw, lw);
+            xw[r >> 3][0][(r & 7) >> 1] = hw;
+            xw[r >> 3][1][(r & 7) >> 1] = lw;
+          }
+        }
+        };
+        if (full) px_tile(std::true_type{});
+        else px_tile(std::false_type{});
+        bf16x8 xb[2][2];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int pc = 0; pc < 2; ++pc) xb[kk][pc] = __builtin_bit_cast(bf16x8, xw[kk][pc]);
+        // dV^T += dO^T P  or  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
+        const uint16_t* tra = PART == kDV ? tro : trq;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int kbase = 16 * kk + 4 * hh;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) {
+            const bf16x8 at[2] = {tr_load(tra, db * 32 + l32, kbase), tr_load(tra, D + db * 32 + l32, kbase)};
+            if constexpr (PART == kDV) mfma3<!OEX, true>(acc[db], at, xb[kk]);
+            else mfma3<!CEX, true>(acc[db], at, xb[kk]);
+          }
         }
       }
       };
-      if (full) px_tile(std::true_type{});
-      else px_tile(std::false_type{});
-      bf16x8 xb[2][2];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int pc = 0; pc < 2; ++pc) xb[kk][pc] = __builtin_bit_cast(bf16x8, xw[kk][pc]);
-      // dV^T += dO^T P  or  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
-      const uint16_t* tra = PART == kDV ? tro : trq;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const int kbase = 16 * kk + 4 * hh;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8 at[2] = {tr_load(tra, db * 32 + l32, kbase), tr_load(tra, D + db * 32 + l32, kbase)};
-          if constexpr (PART == kDV) mfma3<!OEX, true>(acc[db], at, xb[kk]);
-          else mfma3<!CEX, true>(acc[db], at, xb[kk]);
-        }
-      }
+      tile(smem + (it % kQS) * RLEN, smem + ((it + 2) % kQS) * RLEN);
+      // the next tile's copies must be complete; the one after may still run
+      if (it + 2 < total) wait_vm_n<kMinCopies>(); else wait_vm();
+      __syncthreads();
     }
-    };
-    tile(smem + (it % kQS) * RLEN, smem + ((it + 2) % kQS) * RLEN);
-    // the next tile's copies must be complete; the one after may still run
-    if (it + 2 < total) wait_vm_n<kMinCopies>(); else wait_vm();
-    __syncthreads();
-  }
 
-  if constexpr (PART == kDV) {
-    // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
-    if (key_ok) {
-      float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4)
-          *(float4*)(dvr + db * 32 + 8 * g4 + 4 * hh) =
-              make_float4(acc[db][4 * g4], acc[db][4 * g4 + 1], acc[db][4 * g4 + 2], acc[db][4 * g4 + 3]);
-    }
-  } else {
-    // dk_val = scale * dK~ at the key's support, through LDS, four waves at
-    // a time: [wave % 4][key][coordinate], pitch D + 4
-    float* L = (float*)smem + (wave & 3) * kT * (D + 4);
-#pragma unroll
-    for (int round = 0; round < kNW / 4; ++round) {
-      if (wave / 4 == round) {
+    if constexpr (PART == kDV) {
+      // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
+      if (key_ok) {
+        float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
+          for (int g4 = 0; g4 < 4; ++g4)
+            *(float4*)(dvr + db * 32 + 8 * g4 + 4 * hh) =
+                make_float4(acc[db][4 * g4], acc[db][4 * g4 + 1], acc[db][4 * g4 + 2], acc[db][4 * g4 + 3]);
       }
-      __syncthreads();
-      if (wave / 4 == round && key_ok) {
-        const int64_t row = (int64_t)bh * n + my_j;
-        for (int t = hh; t < p.k; t += 2) {
-          const int u = load_idx(p.k_idx, row * p.k + t, p.ifmt, D - 1);
-          p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+    } else {
+      // dk_val = scale * dK~ at the key's support, through LDS, four waves at
+      // a time: [wave % 4][key][coordinate], pitch D + 4
+      float* L = (float*)smem + (wave & 3) * kT * (D + 4);
+#pragma unroll
+      for (int round = 0; round < kNW / 4; ++round) {
+        if (wave / 4 == round) {
+#pragma unroll
+          for (int db = 0; db < NDB; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              L[l32 * (D + 4) + db * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[db][r];
         }
+        __syncthreads();
+        if (wave / 4 == round && key_ok) {
+          const int64_t row = (int64_t)bh * n + my_j;
+          for (int t = hh; t < p.k; t += 2) {
+            const int u = load_idx(p.k_idx, row * p.k + t, p.ifmt, D - 1);
+            p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+          }
+        }
+        __syncthreads();
       }
-      __syncthreads();
     }
-  }
+  }  // work items
 }
 
 // ---------------------------------------------------------------------------
@@ -906,6 +958,7 @@ template <int D, bool VEX, bool OEX, bool CEX>
 hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   using I = Img<D>;
   static bool configured = false;
+  static int res_dq = 0, res_dv = 0, res_dk = 0;  // resident workgroups per XCD
   if (!configured) {
     hipError_t e = hipSuccess;
     const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
@@ -920,7 +973,23 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
         e = hipFuncSetAttribute((const void*)sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, 2 * I::QB);
     }
+    // persistent dk / dv grids: resident workgroups per CU x CUs / 8
+    int dev = 0, cus = 0, nb_dq = 0, nb_dv = 0, nb_dk = 0;
+    if (e == hipSuccess) e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &nb_dq, (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>, kNWQ * 64, 2 * I::KB);
+    if (e == hipSuccess)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &nb_dv, (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>, kNW * 64, kQS * I::DV_LEN);
+    if (e == hipSuccess)
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &nb_dk, (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>, kNW * 64, kQS * I::DK_LEN);
     if (e != hipSuccess) return e;
+    res_dq = nb_dq * cus / 8;
+    res_dv = nb_dv * cus / 8;
+    res_dk = nb_dk * cus / 8;
     configured = true;
   }
   static_assert(2 * I::KB >= 4 * kT * (D + 4) * 4, "dq gather (four waves at a time) fits the stages");
@@ -930,8 +999,15 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   const dim3 blk(256);
   hipLaunchKernelGGL(sfa_bwd_qprep_kernel<D>, dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
   hipLaunchKernelGGL(sfa_bwd_kprep_kernel<D>, dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
-  hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX, CEX>), dim3(p.nqb, B * p.Hkv), dim3(kNWQ * 64),
-                     2 * I::KB, stream, p);
+  // persistent grids when the KV heads split evenly over the 8 XCDs
+  const bool pers = (B * p.Hkv) % 8 == 0;
+  {
+    BwdParams pq = p;
+    pq.pm = B * p.Hkv / 8 * p.nqb;
+    pq.pr = pers ? max(1, min(res_dq, pq.pm)) : 0;
+    const dim3 gq = pers ? dim3(8 * pq.pr) : dim3(p.nqb, B * p.Hkv);
+    hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX, CEX>), gq, dim3(kNWQ * 64), 2 * I::KB, stream, pq);
+  }
   static_assert(2 * I::QB <= 160 * 1024 && 2 * I::QB >= kNWF * kT * (D + 4) * 4, "fused dk/dv stages");
   if constexpr (fused_dkv<D, VEX, OEX>()) {
     const int nkf = (p.n + kNWF * kT - 1) / (kNWF * kT);
@@ -939,11 +1015,17 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
                        2 * I::QB, stream, p);
     return hipGetLastError();
   }
-  const int nkb = (p.n + kNW * kT - 1) / (kNW * kT);
-  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
-                     kQS * I::DV_LEN, stream, p);
-  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>), dim3(nkb, B * p.Hkv), dim3(kNW * 64),
-                     kQS * I::DK_LEN, stream, p);
+  p.nkb = (p.n + kNW * kT - 1) / (kNW * kT);
+  p.pm = B * p.Hkv / 8 * p.nkb;
+  BwdParams pv = p, pk = p;
+  pv.pr = pers ? max(1, min(res_dv, p.pm)) : 0;
+  pk.pr = pers ? max(1, min(res_dk, p.pm)) : 0;
+  const dim3 gv = pers ? dim3(8 * pv.pr) : dim3(p.nkb, B * p.Hkv);
+  const dim3 gk = pers ? dim3(8 * pk.pr) : dim3(p.nkb, B * p.Hkv);
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>), gv, dim3(kNW * 64), kQS * I::DV_LEN,
+                     stream, pv);
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>), gk, dim3(kNW * 64), kQS * I::DK_LEN,
+                     stream, pk);
   return hipGetLastError();
 }
 
@@ -975,6 +1057,7 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
   p.BR = kNWQ * kT / p.G;
   p.nqb = (n + p.BR - 1) / p.BR;
   p.lg = __builtin_ctz((unsigned)p.G);  // G is a power of two here (checked by the caller)
+  p.nkb = p.pr = p.pm = 0;  // set by launch_d for the dk / dv kernels
   p.scale = scale;
   p.c = (float)((double)scale * 1.4426950408889634);
   const size_t qbytes = (size_t)B * Hq * p.nt * (d == 64 ? Img<64>::QB : Img<128>::QB);

@@ -219,3 +219,50 @@ def test_qwen3_32k_full_size_sampled():
     sel = torch.from_numpy(cols).to(DEV)
     check_grad(dk[0, g, sel], gk, tol, f"dk_val KV head {g}")
     check_grad(dv[0, g, sel], gv, tol, f"dv KV head {g}")
+
+
+@pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal,bf16",
+    [
+        (2, 16, 8, 4500, 128, 16, True, True),  # dq: 3 rows of blocks per XCD, dk / dv: 2
+        (1, 8, 8, 9000, 64, 8, False, False),   # G = 1, non-causal, float32 V, O and dO
+    ])
+def test_persistent_grid_sampled(B, Hq, Hkv, n, d, k, causal, bf16):
+    """With B * Hkv a multiple of 8 the dq, dk and dv kernels run persistent
+    grids; with more blocks than resident workgroups each workgroup takes
+    several, in reversed slot order and sweep direction on every other row.
+    Sampled query rows and keys from blocks of every row, in the first and
+    the last KV head, against the oracle."""
+    seed = 77
+    dt = torch.bfloat16 if bf16 else torch.float32
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed, v_dtype=dt, device=DEV)
+    dout = torch.empty((B, Hq, n, d), device=DEV)
+    for b in range(B):
+        for h in range(Hq):
+            dout[b, h] = si.normal((n, d), seed, "dout", b, h, device=DEV)
+    dout = dout.to(dt)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    scale = 1.0 / math.sqrt(d)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=dt)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    tol = TOL_GRAD[(bf16, bf16)]
+    G = Hq // Hkv
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([[0, 255, 256, n // 2, n - 1], rng.integers(0, n, 10)]))
+    cols = np.unique(np.concatenate([[0, 255, 256, n - 300, n - 1], rng.integers(0, n, 10)]))
+    for b, g in ((0, 0), (B - 1, Hkv - 1)):
+        oki, okv = oracle.topk_encode(kk[b, g].cpu().numpy(), k)
+        vn, dn = np_vals(v[b, g]), np_vals(dout[b])
+        qc = [oracle.topk_encode(q[b, h].cpu().numpy(), k) for h in range(G * g, G * g + G)]
+        for h in sorted({0, G - 1}):
+            ref = oracle.attn_bwd_rows(qc[h][0], qc[h][1], oki, okv, vn, dn[G * g + h], d, scale,
+                                       causal, rows)
+            check_grad(dq[b, G * g + h, torch.from_numpy(rows).to(DEV)], ref, tol,
+                       f"dq_val batch {b} head {G * g + h}")
+        gk, gv = oracle.attn_bwd_cols(np.stack([c[0] for c in qc]), np.stack([c[1] for c in qc]),
+                                      oki, okv, vn, dn[G * g:G * g + G], d, scale, causal, cols)
+        sel = torch.from_numpy(cols).to(DEV)
+        check_grad(dk[b, g, sel], gk, tol, f"dk_val batch {b} KV head {g}")
+        check_grad(dv[b, g, sel], gv, tol, f"dv batch {b} KV head {g}")
