@@ -47,23 +47,32 @@ constexpr int kNWQ = 8;        // dq: wavefronts per workgroup (two per SIMD)
 constexpr int kTP = kT + 4;    // bf16 pitch of a transposed row: 72 B, conflict-free 8-byte reads
 constexpr float kLog2e = 1.44269504088896340736f;
 
-template <int D>
+// Tile images.  OEX / VEX: dO / V are stored in bf16, so their low pieces
+// are zero and only the high piece is kept (the query image's layout does
+// not depend on VEX, the key image's not on OEX).
+template <int D, bool OEX = false, bool VEX = false>
 struct Img {
+  static constexpr int PO = OEX ? 1 : 2, PV = VEX ? 1 : 2;  // pieces kept of dO and V
   static constexpr int RP = 2 * D + 8;                 // bf16 pitch of a row-major row: [piece][col]
+  static constexpr int RPO = PO * D + 8, RPV = PV * D + 8;  // the same for dO and V rows
   static constexpr int RMB = kT * RP * 2;              // row-major array bytes
+  static constexpr int RMBO = kT * RPO * 2, RMBV = kT * RPV * 2;
   static constexpr int TRB = 2 * D * kTP * 2;          // transposed array bytes: [piece][col][row]
+  static constexpr int TRBO = PO * D * kTP * 2;
   // query image: dO tr | Q~ rm | L2[32] | D[32] | Q~ tr | dO rm, ordered so
   // that the dV kernel's part (dO tr, Q~ rm, L2) and the dK kernel's part
   // (Q~ rm .. dO rm) are each one contiguous range of whole 1 KB blocks
-  static constexpr int Q_TRO = 0, Q_RMQ = TRB, Q_L2 = TRB + RMB, Q_D = Q_L2 + kT * 4;
+  static constexpr int Q_TRO = 0, Q_RMQ = (TRBO + 1023) / 1024 * 1024, Q_L2 = Q_RMQ + RMB;
+  static constexpr int Q_D = Q_L2 + kT * 4;
   static constexpr int Q_TRQ = Q_D + kT * 4, Q_RMO = Q_TRQ + TRB;
-  static constexpr int QB = (Q_RMO + RMB + 1023) / 1024 * 1024;
+  static constexpr int QB = (Q_RMO + RMBO + 1023) / 1024 * 1024;
   static constexpr int DV_OFF = 0, DV_LEN = (Q_D + 1023) / 1024 * 1024;
   static constexpr int DK_OFF = Q_RMQ, DK_LEN = QB - Q_RMQ;
   static_assert(Q_RMQ % 1024 == 0, "the dK range starts on a 1 KB block");
+  static_assert(Q_L2 % 16 == 0 && Q_RMO % 16 == 0, "16-byte reads of L2, D and dO rows");
   // key image: K~ rm | K~ tr | V rm
   static constexpr int K_RMK = 0, K_TRK = RMB, K_RMV = RMB + TRB;
-  static constexpr int KB = (2 * RMB + TRB + 1023) / 1024 * 1024;
+  static constexpr int KB = (RMB + TRB + RMBV + 1023) / 1024 * 1024;
   static constexpr int NKB = D / 16, NDB = D / 32;
 };
 
@@ -180,9 +189,9 @@ __device__ __forceinline__ bf16x8 tr_load(const uint16_t* tr, int row, int kbase
 // images
 // ---------------------------------------------------------------------------
 
-template <int D>
+template <int D, bool OEX>
 __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
-  using I = Img<D>;
+  using I = Img<D, OEX>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* rmq = (uint16_t*)(smem + I::Q_RMQ);
   uint16_t* trq = (uint16_t*)(smem + I::Q_TRQ);
@@ -221,10 +230,12 @@ __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
       acc = fmaf(g, o, acc);
       uint16_t h, l;
       split2(g, h, l);
-      rmo[r * I::RP + dim] = h;
-      rmo[r * I::RP + D + dim] = l;
+      rmo[r * I::RPO + dim] = h;
       tro[dim * kTP + r] = h;
-      tro[(D + dim) * kTP + r] = l;
+      if constexpr (!OEX) {  // (bf16 dO: l = 0)
+        rmo[r * I::RPO + D + dim] = l;
+        tro[(D + dim) * kTP + r] = l;
+      }
     }
     acc += __shfl_xor(acc, 1, 64);
     acc += __shfl_xor(acc, 2, 64);
@@ -240,9 +251,9 @@ __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
   for (int i = tid; i < I::QB / 16; i += 256) dst[i] = ((const uint4*)smem)[i];
 }
 
-template <int D>
+template <int D, bool VEX>
 __global__ __launch_bounds__(256) void sfa_bwd_kprep_kernel(BwdParams p) {
-  using I = Img<D>;
+  using I = Img<D, false, VEX>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* rmk = (uint16_t*)(smem + I::K_RMK);
   uint16_t* trk = (uint16_t*)(smem + I::K_TRK);
@@ -268,17 +279,18 @@ __global__ __launch_bounds__(256) void sfa_bwd_kprep_kernel(BwdParams p) {
     if (t * kT + r >= n) break;
     uint16_t h, l;
     split2(load_f(p.v, (r0 + r) * D + dim, p.vbf16), h, l);
-    rmv[r * I::RP + dim] = h;
-    rmv[r * I::RP + D + dim] = l;
+    rmv[r * I::RPV + dim] = h;
+    if constexpr (!VEX) rmv[r * I::RPV + D + dim] = l;  // (bf16 V: l = 0)
   }
   __syncthreads();
   uint4* dst = (uint4*)(p.kimg + ((int64_t)bh * p.nt + t) * I::KB);
   for (int i = tid; i < I::KB / 16; i += 256) dst[i] = ((const uint4*)smem)[i];
 }
 
-// Row-major B operand (lane = row l32, coordinates 16 kb + 8 hh ..) of both
-// pieces, straight from an image in global memory.
-template <int D>
+// Row-major B operand (lane = row l32, coordinates 16 kb + 8 hh ..) of the
+// NP pieces stored at bf16 pitch RP, straight from an image in global memory
+// (a piece not stored is zero).
+template <int D, int RP, int NP>
 __device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, int l32, int hh,
                                             bf16x8 (&b)[2][D / 16]) {
   const uint16_t* rm = (const uint16_t*)(img + off);
@@ -286,7 +298,7 @@ __device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, i
   for (int pc = 0; pc < 2; ++pc)
 #pragma unroll
     for (int kb = 0; kb < D / 16; ++kb)
-      b[pc][kb] = *(const bf16x8*)(rm + l32 * Img<D>::RP + pc * D + kb * 16 + 8 * hh);
+      b[pc][kb] = pc < NP ? *(const bf16x8*)(rm + l32 * RP + pc * D + kb * 16 + 8 * hh) : bf16x8{};
 }
 
 // ---------------------------------------------------------------------------
@@ -297,8 +309,8 @@ __device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, i
 // low pieces are zero.
 template <int D, bool VEX, bool OEX, bool CEX>
 __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
-  using I = Img<D>;
-  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
+  using I = Img<D, OEX, VEX>;
+  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, RPO = I::RPO, RPV = I::RPV;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -337,8 +349,8 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
     float L2 = INFINITY, Dq = 0.f;
     if (wave_ok) {
       const unsigned char* qimg = p.qimg + ((int64_t)(b * p.Hq + hq) * p.nt + pos0 / kT) * I::QB;
-      load_rows_b<D>(qimg, I::Q_RMQ, l32, hh, qB);
-      load_rows_b<D>(qimg, I::Q_RMO, l32, hh, dB);
+      load_rows_b<D, RP, 2>(qimg, I::Q_RMQ, l32, hh, qB);
+      load_rows_b<D, RPO, I::PO>(qimg, I::Q_RMO, l32, hh, dB);
       L2 = ((const float*)(qimg + I::Q_L2))[l32];
       Dq = ((const float*)(qimg + I::Q_D))[l32];
     } else {
@@ -405,7 +417,7 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
           for (int pc = 0; pc < 2; ++pc) {
             a[pc] = *(const bf16x8*)(rmk + l32 * RP + pc * D + kb * 16 + 8 * hh);
-            v[pc] = *(const bf16x8*)(rmv + l32 * RP + pc * D + kb * 16 + 8 * hh);
+            v[pc] = pc < I::PV ? *(const bf16x8*)(rmv + l32 * RPV + pc * D + kb * 16 + 8 * hh) : bf16x8{};
           }
           const bf16x8 qq[2] = {qB[0][kb], qB[1][kb]};
           const bf16x8 gg[2] = {dB[0][kb], dB[1][kb]};
@@ -504,8 +516,8 @@ constexpr int kDV = 0, kDK = 1;
 
 template <int D, bool VEX, bool OEX, bool CEX, int PART>
 __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
-  using I = Img<D>;
-  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP;
+  using I = Img<D, OEX, VEX>;
+  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, RPO = I::RPO, RPV = I::RPV;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -545,8 +557,8 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
     bf16x8 kB[2][NKB], vB[2][NKB];
     if (wave_ok) {
       const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
-      load_rows_b<D>(kimg, I::K_RMK, l32, hh, kB);
-      if constexpr (PART == kDK) load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
+      load_rows_b<D, RP, 2>(kimg, I::K_RMK, l32, hh, kB);
+      if constexpr (PART == kDK) load_rows_b<D, RPV, I::PV>(kimg, I::K_RMV, l32, hh, vB);
     } else {
 #pragma unroll
       for (int pc = 0; pc < 2; ++pc)
@@ -633,7 +645,8 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
           if constexpr (PART == kDK) {
             bf16x8 g[2];
 #pragma unroll
-            for (int pc = 0; pc < 2; ++pc) g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
+            for (int pc = 0; pc < 2; ++pc)
+              g[pc] = pc < I::PO ? *(const bf16x8*)(rmo + l32 * RPO + pc * D + kb * 16 + 8 * hh) : bf16x8{};
             const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
             mfma3<!OEX, !VEX>(dp, g, vv2);  // dP = dO V^T
           }
@@ -696,7 +709,10 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
           const int kbase = 16 * kk + 4 * hh;
 #pragma unroll
           for (int db = 0; db < NDB; ++db) {
-            const bf16x8 at[2] = {tr_load(tra, db * 32 + l32, kbase), tr_load(tra, D + db * 32 + l32, kbase)};
+            // (dO^T with bf16 dO: the high piece only)
+            const bool lo = PART == kDK || I::PO == 2;
+            const bf16x8 at[2] = {tr_load(tra, db * 32 + l32, kbase),
+                                  lo ? tr_load(tra, D + db * 32 + l32, kbase) : bf16x8{}};
             if constexpr (PART == kDV) mfma3<!OEX, true>(acc[db], at, xb[kk]);
             else mfma3<!CEX, true>(acc[db], at, xb[kk]);
           }
@@ -767,8 +783,8 @@ constexpr bool fused_dkv() { return D == 64 && VEX && OEX; }
 
 template <int D, bool VEX, bool OEX, bool CEX>
 __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
-  using I = Img<D>;
-  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, QB = I::QB;
+  using I = Img<D, OEX, VEX>;
+  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, RPO = I::RPO, QB = I::QB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -785,8 +801,8 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   bf16x8 kB[2][NKB], vB[2][NKB];
   if (wave_ok) {
     const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
-    load_rows_b<D>(kimg, I::K_RMK, l32, hh, kB);
-    load_rows_b<D>(kimg, I::K_RMV, l32, hh, vB);
+    load_rows_b<D, RP, 2>(kimg, I::K_RMK, l32, hh, kB);
+    load_rows_b<D, I::RPV, I::PV>(kimg, I::K_RMV, l32, hh, vB);
   } else {
 #pragma unroll
     for (int pc = 0; pc < 2; ++pc)
@@ -854,7 +870,7 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
 #pragma unroll
         for (int pc = 0; pc < 2; ++pc) {
           a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
-          g[pc] = *(const bf16x8*)(rmo + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          g[pc] = pc < I::PO ? *(const bf16x8*)(rmo + l32 * RPO + pc * D + kb * 16 + 8 * hh) : bf16x8{};
         }
         const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
         const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
@@ -913,7 +929,8 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
         const bf16x8 sb[2] = {__builtin_bit_cast(bf16x8, sw[kk][0]), __builtin_bit_cast(bf16x8, sw[kk][1])};
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const bf16x8 ao[2] = {tr_load(tro, db * 32 + l32, kbase), tr_load(tro, D + db * 32 + l32, kbase)};
+          const bf16x8 ao[2] = {tr_load(tro, db * 32 + l32, kbase),
+                                I::PO == 2 ? tr_load(tro, D + db * 32 + l32, kbase) : bf16x8{}};
           mfma3<!OEX, true>(accV[db], ao, pb);
           const bf16x8 aq[2] = {tr_load(trq, db * 32 + l32, kbase), tr_load(trq, D + db * 32 + l32, kbase)};
           mfma3<!CEX, true>(accK[db], aq, sb);
@@ -956,12 +973,12 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
 
 template <int D, bool VEX, bool OEX, bool CEX>
 hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
-  using I = Img<D>;
+  using I = Img<D, OEX, VEX>;
   static bool configured = false;
   static int res_dq = 0, res_dv = 0, res_dk = 0;  // resident workgroups per XCD
   if (!configured) {
     hipError_t e = hipSuccess;
-    const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D>, (const void*)sfa_bwd_kprep_kernel<D>,
+    const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D, OEX>, (const void*)sfa_bwd_kprep_kernel<D, VEX>,
                           (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>,
                           (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>,
                           (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>};
@@ -996,9 +1013,11 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   static_assert(kQS * I::DK_LEN >= 4 * kT * (D + 4) * 4, "dk gather (four waves at a time) fits the stages");
   static_assert(kQS * I::DK_LEN <= 160 * 1024 - 512, "three dK stages fit LDS");
   static_assert(I::DV_LEN / 1024 / kNW >= 1 && I::DK_LEN / 1024 / kNW >= 1, "each wave copies part of each image");
+  // the key images follow the query images in the workspace
+  p.kimg = p.qimg + (size_t)B * p.Hq * p.nt * I::QB;
   const dim3 blk(256);
-  hipLaunchKernelGGL(sfa_bwd_qprep_kernel<D>, dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
-  hipLaunchKernelGGL(sfa_bwd_kprep_kernel<D>, dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
+  hipLaunchKernelGGL((sfa_bwd_qprep_kernel<D, OEX>), dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
+  hipLaunchKernelGGL((sfa_bwd_kprep_kernel<D, VEX>), dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
   // persistent grids when the KV heads split evenly over the 8 XCDs
   const bool pers = (B * p.Hkv) % 8 == 0;
   {
@@ -1060,9 +1079,9 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
   p.nkb = p.pr = p.pm = 0;  // set by launch_d for the dk / dv kernels
   p.scale = scale;
   p.c = (float)((double)scale * 1.4426950408889634);
-  const size_t qbytes = (size_t)B * Hq * p.nt * (d == 64 ? Img<64>::QB : Img<128>::QB);
+  // (images of the bf16 dO / V layouts are smaller than the workspace's)
   p.qimg = (unsigned char*)ws;
-  p.kimg = (unsigned char*)ws + qbytes;
+  p.kimg = nullptr;  // set by launch_d
   // bf16 code values (exact in one bf16 piece) with bf16 V, O and dO
   const bool cex = vfmt == kValBF16 && vbf16 && obf16;
   if (d == 64) {
