@@ -135,6 +135,19 @@ def test_d64_bf16_fused_window():
 
 
 @pytest.mark.parametrize(
+    "B,Hq,Hkv,n,d,k,causal",
+    [
+        (1, 4, 2, 150, 128, 16, True),   # GQA 2:1, ragged
+        (2, 4, 1, 161, 64, 16, True),    # GQA 4:1, d = 64
+        (1, 2, 2, 130, 64, 8, False),    # non-causal
+    ])
+def test_float32_v_bf16_o(B, Hq, Hkv, n, d, k, causal):
+    """float32 V with bf16 O and dO: the tile images keep both pieces of V
+    and the high piece of dO only."""
+    _run(B, Hq, Hkv, n, d, k, causal, False, seed=13 * n + k, o_bf16=True)
+
+
+@pytest.mark.parametrize(
     "B,Hq,Hkv,n,d,k,causal,o_bf16",
     [
         (1, 4, 2, 150, 128, 16, True, True),   # bf16 codes, V, O, dO: one-piece code products
@@ -222,12 +235,13 @@ def test_qwen3_32k_full_size_sampled():
 
 
 @pytest.mark.parametrize(
-    "B,Hq,Hkv,n,d,k,causal,bf16",
+    "B,Hq,Hkv,n,d,k,causal,bf16,win,ng",
     [
-        (2, 16, 8, 4500, 128, 16, True, True),  # dq: 3 rows of blocks per XCD, dk / dv: 2
-        (1, 8, 8, 9000, 64, 8, False, False),   # G = 1, non-causal, float32 V, O and dO
+        (2, 16, 8, 4500, 128, 16, True, True, 0, 0),    # dq: 3 rows of blocks per XCD, dk / dv: 2
+        (1, 8, 8, 9000, 64, 8, False, False, 0, 0),     # G = 1, non-causal, float32 V, O and dO
+        (1, 16, 8, 9000, 128, 16, False, True, 700, 3),  # non-causal token window, global tokens
     ])
-def test_persistent_grid_sampled(B, Hq, Hkv, n, d, k, causal, bf16):
+def test_persistent_grid_sampled(B, Hq, Hkv, n, d, k, causal, bf16, win, ng):
     """With B * Hkv a multiple of 8 the dq, dk and dv kernels run persistent
     grids; with more blocks than resident workgroups each workgroup takes
     several, in reversed slot order and sweep direction on every other row.
@@ -244,8 +258,10 @@ def test_persistent_grid_sampled(B, Hq, Hkv, n, d, k, causal, bf16):
     qi, qv = sfa.sfa_topk_encode(q, k)
     ki, kv = sfa.sfa_topk_encode(kk, k)
     scale = 1.0 / math.sqrt(d)
-    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=dt)
-    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale)
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=dt,
+                              window=win, n_global=ng)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale,
+                                  window=win, n_global=ng)
     torch.cuda.synchronize()
     tol = TOL_GRAD[(bf16, bf16)]
     G = Hq // Hkv
@@ -258,11 +274,12 @@ def test_persistent_grid_sampled(B, Hq, Hkv, n, d, k, causal, bf16):
         qc = [oracle.topk_encode(q[b, h].cpu().numpy(), k) for h in range(G * g, G * g + G)]
         for h in sorted({0, G - 1}):
             ref = oracle.attn_bwd_rows(qc[h][0], qc[h][1], oki, okv, vn, dn[G * g + h], d, scale,
-                                       causal, rows)
+                                       causal, rows, window=win, n_global=ng)
             check_grad(dq[b, G * g + h, torch.from_numpy(rows).to(DEV)], ref, tol,
                        f"dq_val batch {b} head {G * g + h}")
         gk, gv = oracle.attn_bwd_cols(np.stack([c[0] for c in qc]), np.stack([c[1] for c in qc]),
-                                      oki, okv, vn, dn[G * g:G * g + G], d, scale, causal, cols)
+                                      oki, okv, vn, dn[G * g:G * g + G], d, scale, causal, cols,
+                                      window=win, n_global=ng)
         sel = torch.from_numpy(cols).to(DEV)
         check_grad(dk[b, g, sel], gk, tol, f"dk_val batch {b} KV head {g}")
         check_grad(dv[b, g, sel], gv, tol, f"dv batch {b} KV head {g}")
