@@ -340,7 +340,8 @@ def bench_bwd(w, steps, warmup, want_cpu, window=0, n_global=0, codes="i32f32"):
             "peak": PEAK_MFMA_BF16 / 1e12,
             "unit": "TFLOP/s",
             "frac": algo / (ms_step * 1e-3) / PEAK_MFMA_BF16,
-            "traffic": None,
+            "traffic": (_traffic("sfa_bwd.hip", f"bwd_{w.name}")
+                        if codes == "i32f32" and window == 0 else None),
             "algorithmic_flops_per_launch": algo,
             "allowed_pairs": pairs,
             "overlap_products_E": E,
