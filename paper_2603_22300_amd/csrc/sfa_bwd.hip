@@ -98,8 +98,8 @@ struct BwdParams {
   int nqb;   // dq workgroups per (batch, KV head)
   int lg;    // log2(G): the matrix-core kernels run power-of-two groups
   int nkb;   // dk / dv key blocks (256 keys) per (batch, KV head)
-  int pr;    // dk / dv persistent grid: workgroups per XCD (0: one workgroup per block)
-  int pm;    // dk / dv persistent grid: blocks per XCD
+  int pr;    // persistent grid of the launch: workgroups per XCD (0: one workgroup per block)
+  int pm;    // persistent grid of the launch: blocks per XCD
   float scale, c;  // c = scale * log2(e)
 };
 
