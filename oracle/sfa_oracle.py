@@ -608,33 +608,41 @@ def attn_bwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, do_bh, d: int, s
 
 
 def attn_bwd_cols(q_idx_bg, q_val_bg, k_idx_bg, k_val_bg, v_bg, do_bg, d: int, scale: float,
-                  causal: bool, cols, row_chunk: int = 1024, window: int = 0, n_global: int = 0):
+                  causal: bool, cols, row_chunk: int = 1024, window: int = 0, n_global: int = 0,
+                  row_from: int = 0):
     """dk_val and dv (Eq. (6)) of the selected keys of one KV head, summed
     over its query heads: q_*_bg [G, n, k], do_bg [G, n, dv].  Each query
     row's LSE_i and D_i = dO_i . O_i come from the plain forward
     (softmax_attention); then for key j and every query i that sees it,
     P_ij = exp(s_ij - LSE_i), dS_ij = P_ij (dO_i . v_j - D_i),
     dv_j = sum_i P_ij dO_i and dk~_j = scale sum_i dS_ij q~_i.
+    row_from > 0 (causal, no window, every column >= row_from): only query
+    rows from row_from on are evaluated; the rows below see none of the
+    columns (j <= i fails), so they would add only zeros.
     Returns (dk [len(cols), k], dv [len(cols), dv]), float64."""
     kd = densify(k_idx_bg, k_val_bg, d)
     vv, dd = widen(v_bg), widen(do_bg)
     n = kd.shape[0]
     cols = np.asarray(cols, dtype=np.int64)
+    if row_from > 0:
+        assert causal and window == 0 and int(cols.min()) >= row_from
+    pos = np.arange(row_from, n)
     dk = np.zeros((len(cols), np.shape(k_idx_bg)[1]), dtype=np.float64)
     dv = np.zeros((len(cols), vv.shape[1]), dtype=np.float64)
     dkd = np.zeros((len(cols), d), dtype=np.float64)
     for h in range(np.shape(q_idx_bg)[0]):
-        qd = densify(q_idx_bg[h], q_val_bg[h], d)
-        O, L = softmax_attention(qd, kd, vv, scale, causal, row_chunk=row_chunk, window=window,
-                                 n_global=n_global)
-        D = (dd[h] * O).sum(axis=1)
-        S = scale * (qd @ kd[cols].T)                      # [n, len(cols)]
+        qd = densify(q_idx_bg[h], q_val_bg[h], d)[row_from:]
+        do_h = dd[h][row_from:]
+        O, L = softmax_attention(qd, kd, vv, scale, causal, pos=pos, row_chunk=row_chunk,
+                                 window=window, n_global=n_global)
+        D = (do_h * O).sum(axis=1)
+        S = scale * (qd @ kd[cols].T)                      # [rows, len(cols)]
         if causal or window > 0:
-            allowed = token_mask(np.arange(n), n, causal, window, n_global)[:, cols]
+            allowed = token_mask(pos, n, causal, window, n_global)[:, cols]
             S = np.where(allowed, S, -np.inf)
         P = np.exp(S - L[:, None])
-        dS = P * (dd[h] @ vv[cols].T - D[:, None])
-        dv += P.T @ dd[h]
+        dS = P * (do_h @ vv[cols].T - D[:, None])
+        dv += P.T @ do_h
         dkd += scale * (dS.T @ qd)
     for c, j in enumerate(cols):
         dk[c] = dkd[c][np.asarray(k_idx_bg[j], dtype=np.int64)]

@@ -197,7 +197,10 @@ def test_qwen3_32k_full_size_sampled():
     """The 32K GQA workload in the bench's configuration (bf16 V, O and dO):
     all gradients computed on the GPU; the oracle rebuilds dq for sampled
     query rows of two heads and dk, dv for sampled keys of one KV head (its
-    forward over all 32768 rows of the four query heads supplies LSE and O)."""
+    forward over all 32768 rows of the four query heads supplies LSE and O).
+    Then every KV head (each runs on its own XCD in the persistent schedule):
+    dq for sampled rows of one of its query heads, and dk, dv for sampled
+    keys among the last 512, whose causal rows are the last 512."""
     w = si.workload("qwen3_32k")
     B, Hq, Hkv, n, d, k, G = w.B, w.Hq, w.Hkv, w.n, w.d, w.k, w.G
     q = torch.empty((B, Hq, n, d), device=DEV)
@@ -232,6 +235,27 @@ def test_qwen3_32k_full_size_sampled():
     sel = torch.from_numpy(cols).to(DEV)
     check_grad(dk[0, g, sel], gk, tol, f"dk_val KV head {g}")
     check_grad(dv[0, g, sel], gv, tol, f"dv KV head {g}")
+    tail = n - 512
+    for g2 in range(Hkv):
+        oki2, okv2 = oracle.topk_encode(kk[0, g2].cpu().numpy(), k)
+        vn2 = np_vals(v[0, g2])
+        qc2 = [oracle.topk_encode(q[0, h].cpu().numpy(), k) for h in range(G * g2, G * g2 + G)]
+        hq = g2 % G  # one query head of the group
+        rows2 = np.unique(np.concatenate([[0, 255, 256, n - 1], rng.integers(0, n, 4)]))
+        ref = oracle.attn_bwd_rows(qc2[hq][0], qc2[hq][1], oki2, okv2, vn2, dn[G * g2 + hq], d,
+                                   w.scale, True, rows2)
+        check_grad(dq[0, G * g2 + hq, torch.from_numpy(rows2).to(DEV)], ref, tol,
+                   f"dq_val head {G * g2 + hq}")
+        cols2 = np.unique(np.concatenate([[tail, n - 257, n - 256, n - 1],
+                                          rng.integers(tail, n, 4)]))
+        gk2, gv2 = oracle.attn_bwd_cols(np.stack([c[0] for c in qc2]), np.stack([c[1] for c in qc2]),
+                                        oki2, okv2, vn2, dn[G * g2:G * g2 + G], d, w.scale, True,
+                                        cols2, row_from=tail)
+        sel2 = torch.from_numpy(cols2).to(DEV)
+        check_grad(dk[0, g2, sel2], gk2, tol, f"dk_val KV head {g2} (last keys)")
+        check_grad(dv[0, g2, sel2], gv2, tol, f"dv KV head {g2} (last keys)")
+    print(f"[parity] qwen3_32k backward: dq rows of 2 + {Hkv} heads, dk / dv keys of every KV head",
+          flush=True)
 
 
 @pytest.mark.parametrize(

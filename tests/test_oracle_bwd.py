@@ -152,3 +152,11 @@ def test_rows_and_cols_match_the_full_backward():
                                           do[0, hs], d, 0.25, causal, cols, row_chunk=7)
             assert np.abs(gk - dk[0, g, cols]).max() < 1e-12
             assert np.abs(gv - dvv[0, g, cols]).max() < 1e-12
+            if causal:
+                # rows below the first selected key add nothing under the causal mask
+                late = [20, 38, 39]
+                gk2, gv2 = oracle.attn_bwd_cols(qi[0, hs], qv[0, hs], ki[0, g], kv[0, g], v[0, g],
+                                                do[0, hs], d, 0.25, causal, late, row_chunk=7,
+                                                row_from=17)
+                assert np.abs(gk2 - dk[0, g, late]).max() < 1e-12
+                assert np.abs(gv2 - dvv[0, g, late]).max() < 1e-12
