@@ -29,10 +29,11 @@
 //       (d = 64, bf16 V and O, in place of the two above).
 // Every output element is owned by one wavefront: no atomics.  The tile
 // images are copied global -> LDS with direct-to-LDS loads.  When the
-// (batch, KV head) pairs split evenly over the 8 XCDs, the dq, dk and dv
-// kernels run persistent grids whose workgroups on one XCD sweep the same
-// tiles in step, so that each image comes from HBM about once per row of
-// blocks (qwen3_32k: 32 GB -> 16 GB of fetch per backward).
+// (batch, KV head) pairs split evenly over the 8 XCDs and there is no token
+// window, the dq, dk and dv kernels run persistent grids whose workgroups on
+// one XCD sweep the same tiles in step, so that each image comes from HBM
+// about once per row of blocks (qwen3_32k: 32 GB -> 16 GB of traffic per
+// backward).
 #include <type_traits>
 
 #include "sfa_device.h"
@@ -1019,7 +1020,9 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   hipLaunchKernelGGL((sfa_bwd_qprep_kernel<D, OEX>), dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
   hipLaunchKernelGGL((sfa_bwd_kprep_kernel<D, VEX>), dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
   // persistent grids when the KV heads split evenly over the 8 XCDs
-  const bool pers = (B * p.Hkv) % 8 == 0;
+  // (not under a token window: there every block sweeps the same number of
+  // tiles, and the one-workgroup-per-block grid measured faster)
+  const bool pers = (B * p.Hkv) % 8 == 0 && p.window == 0;
   {
     BwdParams pq = p;
     pq.pm = B * p.Hkv / 8 * p.nqb;

@@ -263,14 +263,15 @@ def test_qwen3_32k_full_size_sampled():
     [
         (2, 16, 8, 4500, 128, 16, True, True, 0, 0),    # dq: 3 rows of blocks per XCD, dk / dv: 2
         (1, 8, 8, 9000, 64, 8, False, False, 0, 0),     # G = 1, non-causal, float32 V, O and dO
-        (1, 16, 8, 9000, 128, 16, False, True, 700, 3),  # non-causal token window, global tokens
+        (1, 16, 8, 9000, 128, 16, False, True, 700, 3),  # token window: one workgroup per block
     ])
 def test_persistent_grid_sampled(B, Hq, Hkv, n, d, k, causal, bf16, win, ng):
-    """With B * Hkv a multiple of 8 the dq, dk and dv kernels run persistent
-    grids; with more blocks than resident workgroups each workgroup takes
-    several, in reversed slot order and sweep direction on every other row.
-    Sampled query rows and keys from blocks of every row, in the first and
-    the last KV head, against the oracle."""
+    """With B * Hkv a multiple of 8 (and no token window) the dq, dk and dv
+    kernels run persistent grids; with more blocks than resident workgroups
+    each workgroup takes several, in reversed slot order and sweep direction
+    on every other row.  Sampled query rows and keys from blocks of every
+    row, in the first and the last KV head, against the oracle; the windowed
+    case checks the one-workgroup-per-block grid at the same shape."""
     seed = 77
     dt = torch.bfloat16 if bf16 else torch.float32
     q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed, v_dtype=dt, device=DEV)
