@@ -975,10 +975,16 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
 template <int D, bool VEX, bool OEX, bool CEX>
 hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   using I = Img<D, OEX, VEX>;
-  static bool configured = false;
-  static int res_dq = 0, res_dv = 0, res_dk = 0;  // resident workgroups per XCD
-  if (!configured) {
-    hipError_t e = hipSuccess;
+  // once per instantiation (a function-local static: initialised once, also
+  // under concurrent first calls): kernel attributes, and the resident
+  // workgroups per XCD of the persistent grids (per CU x CUs / 8)
+  struct Cfg {
+    hipError_t e;
+    int res_dq, res_dv, res_dk;
+  };
+  static const Cfg cfg = [] {
+    Cfg c{hipSuccess, 0, 0, 0};
+    hipError_t& e = c.e;
     const void* fns[5] = {(const void*)sfa_bwd_qprep_kernel<D, OEX>, (const void*)sfa_bwd_kprep_kernel<D, VEX>,
                           (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>,
                           (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>,
@@ -991,7 +997,6 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
         e = hipFuncSetAttribute((const void*)sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, 2 * I::QB);
     }
-    // persistent dk / dv grids: resident workgroups per CU x CUs / 8
     int dev = 0, cus = 0, nb_dq = 0, nb_dv = 0, nb_dk = 0;
     if (e == hipSuccess) e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -1004,12 +1009,13 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
     if (e == hipSuccess)
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
           &nb_dk, (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>, kNW * 64, kQS * I::DK_LEN);
-    if (e != hipSuccess) return e;
-    res_dq = nb_dq * cus / 8;
-    res_dv = nb_dv * cus / 8;
-    res_dk = nb_dk * cus / 8;
-    configured = true;
-  }
+    c.res_dq = nb_dq * cus / 8;
+    c.res_dv = nb_dv * cus / 8;
+    c.res_dk = nb_dk * cus / 8;
+    return c;
+  }();
+  if (cfg.e != hipSuccess) return cfg.e;
+  const int res_dq = cfg.res_dq, res_dv = cfg.res_dv, res_dk = cfg.res_dk;
   static_assert(2 * I::KB >= 4 * kT * (D + 4) * 4, "dq gather (four waves at a time) fits the stages");
   static_assert(kQS * I::DK_LEN >= 4 * kT * (D + 4) * 4, "dk gather (four waves at a time) fits the stages");
   static_assert(kQS * I::DK_LEN <= 160 * 1024 - 512, "three dK stages fit LDS");

@@ -1553,8 +1553,9 @@ template <int D, bool VBF16, int NW, int KM, int KX>
 hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
   constexpr int bytes = lds_bytes<D, VBF16, NW, KX>();
   constexpr int rbytes = lds_bytes<D, true, NW, 0, true>();  // the rerun: three bf16 pieces
-  static bool configured = false;  // per instantiation
-  if (!configured) {
+  // once per instantiation (a function-local static: initialised once, also
+  // under concurrent first calls)
+  static const hipError_t configured = [] {
     hipError_t e = hipSuccess;
     if (bytes > 65536)
       e = hipFuncSetAttribute((const void*)sfa_fwd_kernel<D, VBF16, NW, KM, KX>,
@@ -1562,9 +1563,9 @@ hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
     if (e == hipSuccess && VBF16 && rbytes > 65536)
       e = hipFuncSetAttribute((const void*)sfa_fwd_rerun_kernel<D, NW, KM>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, rbytes);
-    if (e != hipSuccess) return e;
-    configured = true;
-  }
+    return e;
+  }();
+  if (configured != hipSuccess) return configured;
   dim3 grid(p.nqb, B * p.Hkv), block(NW * 64);
   hipLaunchKernelGGL((sfa_fwd_kernel<D, VBF16, NW, KM, KX>), grid, block, bytes, stream, p);
   if constexpr (VBF16) {
@@ -1581,13 +1582,11 @@ hipError_t launch_km(const FwdParams& p, int B, hipStream_t stream) {
 template <int D, int NW, int KM>
 hipError_t launch_ix(const FwdParams& p, int B, hipStream_t stream) {
   constexpr int bytes = ix_lds_bytes<D, NW, KM>();
-  static bool configured = false;  // per instantiation
-  if (!configured) {
-    hipError_t e = hipFuncSetAttribute((const void*)sfa_fwd_ix_kernel<D, NW, KM>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-    if (e != hipSuccess) return e;
-    configured = true;
-  }
+  static const hipError_t configured = [] {  // once per instantiation
+    return hipFuncSetAttribute((const void*)sfa_fwd_ix_kernel<D, NW, KM>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  }();
+  if (configured != hipSuccess) return configured;
   dim3 grid(p.nqb, B * p.Hkv), block(NW * 64);
   hipLaunchKernelGGL((sfa_fwd_ix_kernel<D, NW, KM>), grid, block, bytes, stream, p);
   return hipGetLastError();

@@ -24,6 +24,8 @@
 //      float32 accumulation, or float32 x float32.
 // Keys that share no coordinate with a query keep score 0 and still enter
 // the softmax, so the result is exactly softmax(Q~ K~^T * scale) V.
+#include <mutex>
+
 #include "sfa_device.h"
 #include "sfa_launch.h"
 
@@ -376,12 +378,17 @@ __global__ __launch_bounds__(kThreads, 2) void sfa_fwd_index_kernel(FwdParams p)
 template <int D, bool VBF16, int KM>
 static hipError_t launch_fwd_km(const FwdParams& p, int B, hipStream_t stream) {
   const FwdLds L = fwd_lds_layout<D, VBF16>(p.k);
-  static int configured_bytes = 0;  // per instantiation
-  if (L.total > 65536 && L.total > configured_bytes) {
-    hipError_t e = hipFuncSetAttribute((const void*)sfa_fwd_index_kernel<D, VBF16, KM>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, L.total);
-    if (e != hipSuccess) return e;
-    configured_bytes = L.total;
+  // the largest dynamic LDS size set so far, per instantiation (it grows with k)
+  static std::mutex mu;
+  static int configured_bytes = 0;
+  if (L.total > 65536) {
+    std::lock_guard<std::mutex> lock(mu);
+    if (L.total > configured_bytes) {
+      hipError_t e = hipFuncSetAttribute((const void*)sfa_fwd_index_kernel<D, VBF16, KM>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, L.total);
+      if (e != hipSuccess) return e;
+      configured_bytes = L.total;
+    }
   }
   dim3 grid(p.nqb, B * p.Hkv), block(kThreads);
   hipLaunchKernelGGL((sfa_fwd_index_kernel<D, VBF16, KM>), grid, block, L.total, stream, p);
