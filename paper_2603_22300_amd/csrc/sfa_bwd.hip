@@ -16,10 +16,9 @@
 //
 // Kernels (all on the caller's stream):
 //   sfa_bwd_qprep_kernel  per (batch, query head, 32-row tile): an image of
-//       Q~ and dO as bf16 pieces, row-major and transposed, plus
-//       log2(e) * LSE and D for the 32 rows;
-//   sfa_bwd_kprep_kernel  per (batch, KV head, 32-key tile): K~ row-major and
-//       transposed, V row-major;
+//       Q~ and dO as bf16 pieces, plus log2(e) * LSE and D for the 32 rows;
+//   sfa_bwd_kprep_kernel  per (batch, KV head, 32-key tile): an image of K~
+//       and V;
 //   sfa_bwd_dq_kernel     query-parallel (like the forward): S^T = K~ Q~^T,
 //       dP^T = V dO^T, dS^T, dQ~^T += K~^T dS^T over the allowed key tiles;
 //   sfa_bwd_dkv_kernel    key-parallel: S = Q~ K~^T, dP = dO V^T, dS,
@@ -32,8 +31,8 @@
 // (batch, KV head) pairs split evenly over the 8 XCDs and there is no token
 // window, the dq, dk and dv kernels run persistent grids whose workgroups on
 // one XCD sweep the same tiles in step, so that each image comes from HBM
-// about once per row of blocks (qwen3_32k: 32 GB -> 16 GB of traffic per
-// backward).
+// about once per row of blocks.
+#include <algorithm>
 #include <type_traits>
 
 #include "sfa_device.h"
@@ -45,37 +44,37 @@ namespace {
 constexpr int kT = 32;         // rows (queries or keys) per tile image
 constexpr int kNW = 8;         // dk, dv: wavefronts per workgroup (two per SIMD)
 constexpr int kNWQ = 8;        // dq: wavefronts per workgroup (two per SIMD)
-constexpr int kTP = kT + 4;    // bf16 pitch of a transposed row: 72 B, conflict-free 8-byte reads
 constexpr float kLog2e = 1.44269504088896340736f;
 
-// Tile images.  OEX / VEX: dO / V are stored in bf16, so their low pieces
-// are zero and only the high piece is kept (the query image's layout does
-// not depend on VEX, the key image's not on OEX).
+// Tile images: 32 rows, each row the bf16 pieces of two arrays side by side,
+// [Q~ piece 0 | Q~ piece 1 | dO pieces] in the query image and
+// [K~ piece 0 | K~ piece 1 | V pieces] in the key image.  OEX / VEX: dO / V
+// are stored in bf16, so their low pieces are zero and only the high piece
+// is kept.  A row is a run of 16-byte chunks, padded by 64 bytes (a pitch of
+// 16 or 48 banks modulo the 64 LDS banks), and chunk c of row r is stored at
+// chunk c ^ ((r / 4) % 4).  The one layout then serves, free of LDS bank
+// conflicts, both the row operands (16-byte reads, a row per lane) and the
+// transposed operands (ds_read_b64_tr_b16: 8 bytes of a row per lane, four
+// consecutive rows per 16 lanes): no transposed copy is stored.  The query image ends with log2(e) * LSE and D of its 32
+// rows.
 template <int D, bool OEX = false, bool VEX = false>
 struct Img {
   static constexpr int PO = OEX ? 1 : 2, PV = VEX ? 1 : 2;  // pieces kept of dO and V
-  static constexpr int RP = 2 * D + 8;                 // bf16 pitch of a row-major row: [piece][col]
-  static constexpr int RPO = PO * D + 8, RPV = PV * D + 8;  // the same for dO and V rows
-  static constexpr int RMB = kT * RP * 2;              // row-major array bytes
-  static constexpr int RMBO = kT * RPO * 2, RMBV = kT * RPV * 2;
-  static constexpr int TRB = 2 * D * kTP * 2;          // transposed array bytes: [piece][col][row]
-  static constexpr int TRBO = PO * D * kTP * 2;
-  // query image: dO tr | Q~ rm | L2[32] | D[32] | Q~ tr | dO rm, ordered so
-  // that the dV kernel's part (dO tr, Q~ rm, L2) and the dK kernel's part
-  // (Q~ rm .. dO rm) are each one contiguous range of whole 1 KB blocks
-  static constexpr int Q_TRO = 0, Q_RMQ = (TRBO + 1023) / 1024 * 1024, Q_L2 = Q_RMQ + RMB;
-  static constexpr int Q_D = Q_L2 + kT * 4;
-  static constexpr int Q_TRQ = Q_D + kT * 4, Q_RMO = Q_TRQ + TRB;
-  static constexpr int QB = (Q_RMO + RMBO + 1023) / 1024 * 1024;
-  static constexpr int DV_OFF = 0, DV_LEN = (Q_D + 1023) / 1024 * 1024;
-  static constexpr int DK_OFF = Q_RMQ, DK_LEN = QB - Q_RMQ;
-  static_assert(Q_RMQ % 1024 == 0, "the dK range starts on a 1 KB block");
-  static_assert(Q_L2 % 16 == 0 && Q_RMO % 16 == 0, "16-byte reads of L2, D and dO rows");
-  // key image: K~ rm | K~ tr | V rm
-  static constexpr int K_RMK = 0, K_TRK = RMB, K_RMV = RMB + TRB;
-  static constexpr int KB = (RMB + TRB + RMBV + 1023) / 1024 * 1024;
+  static constexpr int C2 = 2 * D / 8;                       // first chunk of dO / V in a row
+  static constexpr int QRB = (2 + PO) * D * 2 + 64, KRB = (2 + PV) * D * 2 + 64;  // row pitches, bytes
+  static_assert((QRB / 4) % 64 == 16 || (QRB / 4) % 64 == 48, "query rows: conflict-free pitch");
+  static_assert((KRB / 4) % 64 == 16 || (KRB / 4) % 64 == 48, "key rows: conflict-free pitch");
+  static constexpr int Q_L2 = kT * QRB, Q_D = Q_L2 + kT * 4;
+  static constexpr int QB = (Q_D + kT * 4 + 1023) / 1024 * 1024;
+  static constexpr int KB = (kT * KRB + 1023) / 1024 * 1024;
   static constexpr int NKB = D / 16, NDB = D / 32;
 };
+
+// Byte offset of bf16 column `col` of row r in an image of row pitch RB.
+template <int RB>
+__device__ __forceinline__ int img_pos(int r, int col) {
+  return r * RB + 16 * ((col >> 3) ^ ((r >> 2) & 3)) + 2 * (col & 7);
+}
 
 struct BwdParams {
   const void* q_idx;
@@ -160,9 +159,6 @@ __device__ __forceinline__ void wait_vm_n() {
   __builtin_amdgcn_s_waitcnt(0x0f70 | N);
 }
 
-// A-operand slice of a transposed array: row `row` (a coordinate / dimension),
-// columns kbase + 0..3 and kbase + 8..11 (the key / query order of the MFMA
-// output layout).
 // Workgroup (x, y) of a grid (nx, nbh) -> (block, bh): workgroups go
 // round-robin over the 8 XCDs, each with its own L2; with nbh a multiple of 8,
 // XCD c runs the (batch, KV head) pairs congruent to c, so one L2 serves every
@@ -178,12 +174,53 @@ __device__ __forceinline__ void xcd_map(int nx, int& x, int& bh) {
   }
 }
 
-__device__ __forceinline__ bf16x8 tr_load(const uint16_t* tr, int row, int kbase) {
-  const uint16_t* p = tr + row * kTP + kbase;
-  const uint2 v0 = *(const uint2*)p;
-  const uint2 v1 = *(const uint2*)(p + 8);
-  const u32x4 w = {v0.x, v0.y, v1.x, v1.y};
+// Per-lane byte offsets into a tile image of row pitch RB (see Img).
+//   Row operand (B of 32x32x16): lane (l32, hh) reads row l32, columns
+//   8 (c0 + 2 kb + hh) .. + 7 for a chunk c0 that is a multiple of 4:
+//   row[kb & 1] + 16 (c0 + 4 (kb / 2)).
+//   Transposed operand (A of 32x32x16, the image's rows as its k index in
+//   the order of the MFMA output layout): lane (l32, hh) needs columns
+//   8 c0 + l32 of rows 16 kk + 4 hh + (0..3) and 16 kk + 4 hh + 8 + (0..3).
+//   A transposing read hands lane i of a 16-lane group element i % 4 of
+//   the 8 bytes addressed by lane 4 e + i / 4 of the group, as its element
+//   e; so lane j of group g addresses row 4 hh + j / 4 (+ 8), columns
+//   8 c0 + 16 (g % 2) + 4 (j % 4) + (0..3): tr[0] / tr[1] + (16 kk) RB + 16 c0.
+template <int RB>
+struct LaneOff {
+  int row[2], tr[2];
+  __device__ __forceinline__ explicit LaneOff(int lane) {
+    const int l32 = lane & 31, hh = lane >> 5, g = lane >> 4, j = lane & 15;
+    row[0] = l32 * RB + 16 * (hh ^ ((l32 >> 2) & 3));
+    row[1] = row[0] ^ 32;
+    tr[0] = (4 * hh + (j >> 2)) * RB + 8 * (j & 1) + 16 * ((2 * (g & 1) + ((j >> 1) & 1)) ^ hh);
+    tr[1] = (tr[0] ^ 32) + 8 * RB;
+  }
+};
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ i16x4 lds_read_tr(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
+}
+
+// Transposed operand of 32 columns from chunk c0 on, rows from 16 kk on.
+template <int RB>
+__device__ __forceinline__ bf16x8 tr_operand(const unsigned char* img, const LaneOff<RB>& o, int kk,
+                                             int c0) {
+  const int off = 16 * kk * RB + 16 * c0;
+  const i16x4 a = lds_read_tr(img + o.tr[0] + off);
+  const i16x4 b = lds_read_tr(img + o.tr[1] + off);
+  const u32x2 x = __builtin_bit_cast(u32x2, a), y = __builtin_bit_cast(u32x2, b);
+  const u32x4 w = {x.x, x.y, y.x, y.y};
   return __builtin_bit_cast(bf16x8, w);
+}
+
+// Row operand: chunk c0 + 2 kb + hh of the lane's row.
+template <int RB>
+__device__ __forceinline__ bf16x8 row_operand(const unsigned char* img, const LaneOff<RB>& o, int kb,
+                                              int c0) {
+  return *(const bf16x8*)(img + o.row[kb & 1] + 16 * (c0 + 4 * (kb >> 1)));
 }
 
 // ---------------------------------------------------------------------------
@@ -193,11 +230,9 @@ __device__ __forceinline__ bf16x8 tr_load(const uint16_t* tr, int row, int kbase
 template <int D, bool OEX>
 __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
   using I = Img<D, OEX>;
+  constexpr int RB = I::QRB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t* rmq = (uint16_t*)(smem + I::Q_RMQ);
-  uint16_t* trq = (uint16_t*)(smem + I::Q_TRQ);
-  uint16_t* rmo = (uint16_t*)(smem + I::Q_RMO);
-  uint16_t* tro = (uint16_t*)(smem + I::Q_TRO);
+  unsigned char* img = smem;
   float* l2 = (float*)(smem + I::Q_L2);
   float* dd = (float*)(smem + I::Q_D);
   const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;  // bh = b * Hq + hq
@@ -211,10 +246,8 @@ __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
     const int f = load_idx(p.q_idx, r0 * k + e, p.ifmt, D - 1);
     uint16_t h, l;
     split2(load_val(p.q_val, r0 * k + e, p.vfmt), h, l);
-    rmq[r * I::RP + f] = h;
-    rmq[r * I::RP + D + f] = l;
-    trq[f * kTP + r] = h;
-    trq[(D + f) * kTP + r] = l;
+    *(uint16_t*)(img + img_pos<RB>(r, f)) = h;
+    *(uint16_t*)(img + img_pos<RB>(r, D + f)) = l;
   }
   // dO pieces, and D = dO . O with 8 threads per row (fixed reduction order)
   {
@@ -231,12 +264,8 @@ __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
       acc = fmaf(g, o, acc);
       uint16_t h, l;
       split2(g, h, l);
-      rmo[r * I::RPO + dim] = h;
-      tro[dim * kTP + r] = h;
-      if constexpr (!OEX) {  // (bf16 dO: l = 0)
-        rmo[r * I::RPO + D + dim] = l;
-        tro[(D + dim) * kTP + r] = l;
-      }
+      *(uint16_t*)(img + img_pos<RB>(r, 2 * D + dim)) = h;
+      if constexpr (!OEX) *(uint16_t*)(img + img_pos<RB>(r, 3 * D + dim)) = l;  // (bf16 dO: l = 0)
     }
     acc += __shfl_xor(acc, 1, 64);
     acc += __shfl_xor(acc, 2, 64);
@@ -255,10 +284,9 @@ __global__ __launch_bounds__(256) void sfa_bwd_qprep_kernel(BwdParams p) {
 template <int D, bool VEX>
 __global__ __launch_bounds__(256) void sfa_bwd_kprep_kernel(BwdParams p) {
   using I = Img<D, false, VEX>;
+  constexpr int RB = I::KRB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t* rmk = (uint16_t*)(smem + I::K_RMK);
-  uint16_t* trk = (uint16_t*)(smem + I::K_TRK);
-  uint16_t* rmv = (uint16_t*)(smem + I::K_RMV);
+  unsigned char* img = smem;
   const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;  // bh = b * Hkv + hkv
   const int n = p.n, k = p.k;
   const int64_t r0 = (int64_t)bh * n + (int64_t)t * kT;
@@ -270,36 +298,33 @@ __global__ __launch_bounds__(256) void sfa_bwd_kprep_kernel(BwdParams p) {
     const int f = load_idx(p.k_idx, r0 * k + e, p.ifmt, D - 1);
     uint16_t h, l;
     split2(load_val(p.k_val, r0 * k + e, p.vfmt), h, l);
-    rmk[r * I::RP + f] = h;
-    rmk[r * I::RP + D + f] = l;
-    trk[f * kTP + r] = h;
-    trk[(D + f) * kTP + r] = l;
+    *(uint16_t*)(img + img_pos<RB>(r, f)) = h;
+    *(uint16_t*)(img + img_pos<RB>(r, D + f)) = l;
   }
   for (int e = tid; e < kT * D; e += 256) {
     const int r = e / D, dim = e - r * D;
     if (t * kT + r >= n) break;
     uint16_t h, l;
     split2(load_f(p.v, (r0 + r) * D + dim, p.vbf16), h, l);
-    rmv[r * I::RPV + dim] = h;
-    if constexpr (!VEX) rmv[r * I::RPV + D + dim] = l;  // (bf16 V: l = 0)
+    *(uint16_t*)(img + img_pos<RB>(r, 2 * D + dim)) = h;
+    if constexpr (!VEX) *(uint16_t*)(img + img_pos<RB>(r, 3 * D + dim)) = l;  // (bf16 V: l = 0)
   }
   __syncthreads();
   uint4* dst = (uint4*)(p.kimg + ((int64_t)bh * p.nt + t) * I::KB);
   for (int i = tid; i < I::KB / 16; i += 256) dst[i] = ((const uint4*)smem)[i];
 }
 
-// Row-major B operand (lane = row l32, coordinates 16 kb + 8 hh ..) of the
-// NP pieces stored at bf16 pitch RP, straight from an image in global memory
-// (a piece not stored is zero).
-template <int D, int RP, int NP>
-__device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, int l32, int hh,
+// Row operands (lane = row l32, columns 8 c0 + 16 kb + 8 hh ..) of the NP
+// pieces from chunk c0 on, straight from an image in global memory (a piece
+// not stored is zero); two per-lane offsets and immediate ones, as in LDS.
+template <int D, int RB, int NP>
+__device__ __forceinline__ void load_rows_b(const unsigned char* img, int c0, int lane,
                                             bf16x8 (&b)[2][D / 16]) {
-  const uint16_t* rm = (const uint16_t*)(img + off);
+  const LaneOff<RB> o(lane);
 #pragma unroll
   for (int pc = 0; pc < 2; ++pc)
 #pragma unroll
-    for (int kb = 0; kb < D / 16; ++kb)
-      b[pc][kb] = pc < NP ? *(const bf16x8*)(rm + l32 * RP + pc * D + kb * 16 + 8 * hh) : bf16x8{};
+    for (int kb = 0; kb < D / 16; ++kb) b[pc][kb] = pc < NP ? row_operand(img, o, kb, c0 + pc * D / 8) : bf16x8{};
 }
 
 // ---------------------------------------------------------------------------
@@ -311,11 +336,12 @@ __device__ __forceinline__ void load_rows_b(const unsigned char* img, int off, i
 template <int D, bool VEX, bool OEX, bool CEX>
 __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
   using I = Img<D, OEX, VEX>;
-  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, RPO = I::RPO, RPV = I::RPV;
+  constexpr int NKB = I::NKB, NDB = I::NDB, QRB = I::QRB, KRB = I::KRB, C2 = I::C2;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = p.n;
+  const LaneOff<KRB> ko(lane);
   // Work items: (batch x KV head, block of BR positions), the longest causal
   // blocks first.  Persistent grid (p.pr > 0) as in the key-parallel kernels
   // below, with the key tiles swept upward on even rows and downward on odd
@@ -350,8 +376,8 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
     float L2 = INFINITY, Dq = 0.f;
     if (wave_ok) {
       const unsigned char* qimg = p.qimg + ((int64_t)(b * p.Hq + hq) * p.nt + pos0 / kT) * I::QB;
-      load_rows_b<D, RP, 2>(qimg, I::Q_RMQ, l32, hh, qB);
-      load_rows_b<D, RPO, I::PO>(qimg, I::Q_RMO, l32, hh, dB);
+      load_rows_b<D, QRB, 2>(qimg, 0, lane, qB);
+      load_rows_b<D, QRB, I::PO>(qimg, C2, lane, dB);
       L2 = ((const float*)(qimg + I::Q_L2))[l32];
       Dq = ((const float*)(qimg + I::Q_D))[l32];
     } else {
@@ -406,9 +432,6 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
       const int j0 = jt * kT;
       if (wave_ok && (!p.causal || wave_i_max >= j0) && in_window(j0)) {
         const unsigned char* K = cur;
-        const uint16_t* rmk = (const uint16_t*)(K + I::K_RMK);
-        const uint16_t* trk = (const uint16_t*)(K + I::K_TRK);
-        const uint16_t* rmv = (const uint16_t*)(K + I::K_RMV);
         floatx16 s, dp;
 #pragma unroll
         for (int r = 0; r < 16; ++r) { s[r] = 0.f; dp[r] = 0.f; }
@@ -417,8 +440,8 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
           bf16x8 a[2], v[2];
 #pragma unroll
           for (int pc = 0; pc < 2; ++pc) {
-            a[pc] = *(const bf16x8*)(rmk + l32 * RP + pc * D + kb * 16 + 8 * hh);
-            v[pc] = pc < I::PV ? *(const bf16x8*)(rmv + l32 * RPV + pc * D + kb * 16 + 8 * hh) : bf16x8{};
+            a[pc] = row_operand(K, ko, kb, pc * D / 8);
+            v[pc] = pc < I::PV ? row_operand(K, ko, kb, C2 + pc * D / 8) : bf16x8{};
           }
           const bf16x8 qq[2] = {qB[0][kb], qB[1][kb]};
           const bf16x8 gg[2] = {dB[0][kb], dB[1][kb]};
@@ -467,10 +490,9 @@ __global__ __launch_bounds__(kNWQ * 64) void sfa_bwd_dq_kernel(BwdParams p) {
         // dQ~^T += K~^T dS^T   (coordinates x queries)
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          const int kbase = 16 * kk + 4 * hh;
 #pragma unroll
           for (int db = 0; db < NDB; ++db) {
-            const bf16x8 a[2] = {tr_load(trk, db * 32 + l32, kbase), tr_load(trk, D + db * 32 + l32, kbase)};
+            const bf16x8 a[2] = {tr_operand(K, ko, kk, 4 * db), tr_operand(K, ko, kk, D / 8 + 4 * db)};
             mfma3<!CEX, true>(acc[db], a, dsb[kk]);
           }
         }
@@ -518,11 +540,12 @@ constexpr int kDV = 0, kDK = 1;
 template <int D, bool VEX, bool OEX, bool CEX, int PART>
 __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   using I = Img<D, OEX, VEX>;
-  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, RPO = I::RPO, RPV = I::RPV;
+  constexpr int NKB = I::NKB, NDB = I::NDB, QRB = I::QRB, KRB = I::KRB, C2 = I::C2, QB = I::QB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = p.n;
+  const LaneOff<QRB> qo(lane);
   // Work items: (batch x KV head, block of 256 keys).  Without the persistent
   // grid a workgroup runs one item, placed by xcd_map.  With it (p.pr > 0,
   // B * Hkv a multiple of 8) the grid is 8 x pr workgroups, all resident:
@@ -558,8 +581,8 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
     bf16x8 kB[2][NKB], vB[2][NKB];
     if (wave_ok) {
       const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
-      load_rows_b<D, RP, 2>(kimg, I::K_RMK, l32, hh, kB);
-      if constexpr (PART == kDK) load_rows_b<D, RPV, I::PV>(kimg, I::K_RMV, l32, hh, vB);
+      load_rows_b<D, KRB, 2>(kimg, 0, lane, kB);
+      if constexpr (PART == kDK) load_rows_b<D, KRB, I::PV>(kimg, C2, lane, vB);
     } else {
 #pragma unroll
       for (int pc = 0; pc < 2; ++pc)
@@ -603,19 +626,15 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
       return !win || q0 < p.n_global || jw0 < p.n_global ||
              (q0 < jw0 + kT - 1 + p.window && q0 + kT - 1 > jw0 - p.window);
     };
-    // only this kernel's part of each image is copied; LDS holds it from
-    // image offset ROFF on
-    constexpr int ROFF = PART == kDV ? I::DV_OFF : I::DK_OFF;
-    constexpr int RLEN = PART == kDV ? I::DV_LEN : I::DK_LEN;
     auto qimg_of = [&](int it) {
-      return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + (ord(it) & (p.G - 1))) * p.nt + tile_of(it)) * I::QB + ROFF;
+      return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + (ord(it) & (p.G - 1))) * p.nt + tile_of(it)) * QB;
     };
     // three stages: the image two tiles ahead is in flight while a tile is
     // consumed (vmcnt waits only for the one needed next)
-    // every wave copies at least RLEN / 1024 / kNW blocks of an image
-    constexpr int kMinCopies = RLEN / 1024 / kNW;
-    if (total > 0) dma<kNW>(qimg_of(0), smem, RLEN, wave, lane);
-    if (total > 1) dma<kNW>(qimg_of(1), smem + RLEN, RLEN, wave, lane);
+    // every wave copies at least QB / 1024 / kNW blocks of an image
+    constexpr int kMinCopies = QB / 1024 / kNW;
+    if (total > 0) dma<kNW>(qimg_of(0), smem, QB, wave, lane);
+    if (total > 1) dma<kNW>(qimg_of(1), smem + QB, QB, wave, lane);
     if (total > 1) wait_vm_n<kMinCopies>(); else wait_vm();
     __syncthreads();
     for (int it = 0; it < total; ++it) {
@@ -623,14 +642,10 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
       // through `nxt`, both restrict: the compiler then knows the copy cannot
       // alias those reads and does not wait for it before them.
       auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
-      if (it + 2 < total) dma<kNW>(qimg_of(it + 2), nxt, RLEN, wave, lane);
+      if (it + 2 < total) dma<kNW>(qimg_of(it + 2), nxt, QB, wave, lane);
       const int q0 = tile_of(it) * kT;
       if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
-        const unsigned char* Q = cur - ROFF;  // image offsets apply as is
-        const uint16_t* rmq = (const uint16_t*)(Q + I::Q_RMQ);
-        const uint16_t* trq = (const uint16_t*)(Q + I::Q_TRQ);
-        const uint16_t* rmo = (const uint16_t*)(Q + I::Q_RMO);
-        const uint16_t* tro = (const uint16_t*)(Q + I::Q_TRO);
+        const unsigned char* Q = cur;
         const float* l2 = (const float*)(Q + I::Q_L2);
         const float* dd = (const float*)(Q + I::Q_D);
         floatx16 s, dp;
@@ -640,14 +655,14 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
         for (int kb = 0; kb < NKB; ++kb) {
           bf16x8 a[2];
 #pragma unroll
-          for (int pc = 0; pc < 2; ++pc) a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
+          for (int pc = 0; pc < 2; ++pc) a[pc] = row_operand(Q, qo, kb, pc * D / 8);
           const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
           mfma3<!CEX, !CEX>(s, a, kk2);  // S = Q~ K~^T   (queries x keys)
           if constexpr (PART == kDK) {
             bf16x8 g[2];
 #pragma unroll
             for (int pc = 0; pc < 2; ++pc)
-              g[pc] = pc < I::PO ? *(const bf16x8*)(rmo + l32 * RPO + pc * D + kb * 16 + 8 * hh) : bf16x8{};
+              g[pc] = pc < I::PO ? row_operand(Q, qo, kb, C2 + pc * D / 8) : bf16x8{};
             const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
             mfma3<!OEX, !VEX>(dp, g, vv2);  // dP = dO V^T
           }
@@ -704,23 +719,22 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
 #pragma unroll
           for (int pc = 0; pc < 2; ++pc) xb[kk][pc] = __builtin_bit_cast(bf16x8, xw[kk][pc]);
         // dV^T += dO^T P  or  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
-        const uint16_t* tra = PART == kDV ? tro : trq;
+        constexpr int ca = PART == kDV ? C2 : 0;  // dO or Q~
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-          const int kbase = 16 * kk + 4 * hh;
 #pragma unroll
           for (int db = 0; db < NDB; ++db) {
             // (dO^T with bf16 dO: the high piece only)
             const bool lo = PART == kDK || I::PO == 2;
-            const bf16x8 at[2] = {tr_load(tra, db * 32 + l32, kbase),
-                                  lo ? tr_load(tra, D + db * 32 + l32, kbase) : bf16x8{}};
+            const bf16x8 at[2] = {tr_operand(Q, qo, kk, ca + 4 * db),
+                                  lo ? tr_operand(Q, qo, kk, ca + D / 8 + 4 * db) : bf16x8{}};
             if constexpr (PART == kDV) mfma3<!OEX, true>(acc[db], at, xb[kk]);
             else mfma3<!CEX, true>(acc[db], at, xb[kk]);
           }
         }
       }
       };
-      tile(smem + (it % kQS) * RLEN, smem + ((it + 2) % kQS) * RLEN);
+      tile(smem + (it % kQS) * QB, smem + ((it + 2) % kQS) * QB);
       // the next tile's copies must be complete; the one after may still run
       if (it + 2 < total) wait_vm_n<kMinCopies>(); else wait_vm();
       __syncthreads();
@@ -785,11 +799,12 @@ constexpr bool fused_dkv() { return D == 64 && VEX && OEX; }
 template <int D, bool VEX, bool OEX, bool CEX>
 __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   using I = Img<D, OEX, VEX>;
-  constexpr int NKB = I::NKB, NDB = I::NDB, RP = I::RP, RPO = I::RPO, QB = I::QB;
+  constexpr int NKB = I::NKB, NDB = I::NDB, QRB = I::QRB, KRB = I::KRB, C2 = I::C2, QB = I::QB;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = p.n;
+  const LaneOff<QRB> qo(lane);
   int xb, bh;
   xcd_map((int)gridDim.x, xb, bh);
   const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
@@ -802,8 +817,8 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   bf16x8 kB[2][NKB], vB[2][NKB];
   if (wave_ok) {
     const unsigned char* kimg = p.kimg + ((int64_t)bh * p.nt + jw0 / kT) * I::KB;
-    load_rows_b<D, RP, 2>(kimg, I::K_RMK, l32, hh, kB);
-    load_rows_b<D, I::RPV, I::PV>(kimg, I::K_RMV, l32, hh, vB);
+    load_rows_b<D, KRB, 2>(kimg, 0, lane, kB);
+    load_rows_b<D, KRB, I::PV>(kimg, C2, lane, vB);
   } else {
 #pragma unroll
     for (int pc = 0; pc < 2; ++pc)
@@ -856,10 +871,6 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
     if (it + 1 < total) dma<kNWF>(qimg_of(it + 1), nxt, QB, wave, lane);
     const int q0 = tile_of(it) * kT;
     if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
-      const uint16_t* rmq = (const uint16_t*)(cur + I::Q_RMQ);
-      const uint16_t* trq = (const uint16_t*)(cur + I::Q_TRQ);
-      const uint16_t* rmo = (const uint16_t*)(cur + I::Q_RMO);
-      const uint16_t* tro = (const uint16_t*)(cur + I::Q_TRO);
       const float* l2 = (const float*)(cur + I::Q_L2);
       const float* dd = (const float*)(cur + I::Q_D);
       floatx16 s, dp;
@@ -870,8 +881,8 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
         bf16x8 a[2], g[2];
 #pragma unroll
         for (int pc = 0; pc < 2; ++pc) {
-          a[pc] = *(const bf16x8*)(rmq + l32 * RP + pc * D + kb * 16 + 8 * hh);
-          g[pc] = pc < I::PO ? *(const bf16x8*)(rmo + l32 * RPO + pc * D + kb * 16 + 8 * hh) : bf16x8{};
+          a[pc] = row_operand(cur, qo, kb, pc * D / 8);
+          g[pc] = pc < I::PO ? row_operand(cur, qo, kb, C2 + pc * D / 8) : bf16x8{};
         }
         const bf16x8 kk2[2] = {kB[0][kb], kB[1][kb]};
         const bf16x8 vv2[2] = {vB[0][kb], vB[1][kb]};
@@ -925,15 +936,14 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
       // dV^T += dO^T P  and  dK~^T += Q~^T dS   (dimensions / coordinates x keys)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        const int kbase = 16 * kk + 4 * hh;
         const bf16x8 pb[2] = {__builtin_bit_cast(bf16x8, pw[kk][0]), __builtin_bit_cast(bf16x8, pw[kk][1])};
         const bf16x8 sb[2] = {__builtin_bit_cast(bf16x8, sw[kk][0]), __builtin_bit_cast(bf16x8, sw[kk][1])};
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const bf16x8 ao[2] = {tr_load(tro, db * 32 + l32, kbase),
-                                I::PO == 2 ? tr_load(tro, D + db * 32 + l32, kbase) : bf16x8{}};
+          const bf16x8 ao[2] = {tr_operand(cur, qo, kk, C2 + 4 * db),
+                                I::PO == 2 ? tr_operand(cur, qo, kk, C2 + D / 8 + 4 * db) : bf16x8{}};
           mfma3<!OEX, true>(accV[db], ao, pb);
-          const bf16x8 aq[2] = {tr_load(trq, db * 32 + l32, kbase), tr_load(trq, D + db * 32 + l32, kbase)};
+          const bf16x8 aq[2] = {tr_operand(cur, qo, kk, 4 * db), tr_operand(cur, qo, kk, D / 8 + 4 * db)};
           mfma3<!CEX, true>(accK[db], aq, sb);
         }
       }
@@ -975,6 +985,11 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
 template <int D, bool VEX, bool OEX, bool CEX>
 hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   using I = Img<D, OEX, VEX>;
+  // LDS of the dq kernel (two key-image stages, or the gather of dQ~ that
+  // follows, four waves at a time) and of the fused dk / dv kernel (two
+  // query-image stages, or its gather)
+  constexpr int kDqLds = std::max(2 * I::KB, 4 * kT * (D + 4) * 4);
+  constexpr int kFLds = std::max(2 * I::QB, kNWF * kT * (D + 4) * 4);
   // once per instantiation (a function-local static: initialised once, also
   // under concurrent first calls): kernel attributes, and the resident
   // workgroups per XCD of the persistent grids (per CU x CUs / 8)
@@ -989,26 +1004,26 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
                           (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>,
                           (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>,
                           (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>};
-    const int bytes[5] = {I::QB, I::KB, 2 * I::KB, kQS * I::DV_LEN, kQS * I::DK_LEN};
+    const int bytes[5] = {I::QB, I::KB, kDqLds, kQS * I::QB, kQS * I::QB};
     for (int f = 0; f < 5 && e == hipSuccess; ++f)
       if (bytes[f] > 65536) e = hipFuncSetAttribute(fns[f], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[f]);
     if constexpr (fused_dkv<D, VEX, OEX>()) {
-      if (e == hipSuccess && 2 * I::QB > 65536)
+      if (e == hipSuccess && kFLds > 65536)
         e = hipFuncSetAttribute((const void*)sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, 2 * I::QB);
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kFLds);
     }
     int dev = 0, cus = 0, nb_dq = 0, nb_dv = 0, nb_dk = 0;
     if (e == hipSuccess) e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &nb_dq, (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>, kNWQ * 64, 2 * I::KB);
+          &nb_dq, (const void*)sfa_bwd_dq_kernel<D, VEX, OEX, CEX>, kNWQ * 64, kDqLds);
     if (e == hipSuccess)
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &nb_dv, (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>, kNW * 64, kQS * I::DV_LEN);
+          &nb_dv, (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>, kNW * 64, kQS * I::QB);
     if (e == hipSuccess)
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &nb_dk, (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>, kNW * 64, kQS * I::DK_LEN);
+          &nb_dk, (const void*)sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>, kNW * 64, kQS * I::QB);
     c.res_dq = nb_dq * cus / 8;
     c.res_dv = nb_dv * cus / 8;
     c.res_dk = nb_dk * cus / 8;
@@ -1016,10 +1031,9 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   }();
   if (cfg.e != hipSuccess) return cfg.e;
   const int res_dq = cfg.res_dq, res_dv = cfg.res_dv, res_dk = cfg.res_dk;
-  static_assert(2 * I::KB >= 4 * kT * (D + 4) * 4, "dq gather (four waves at a time) fits the stages");
-  static_assert(kQS * I::DK_LEN >= 4 * kT * (D + 4) * 4, "dk gather (four waves at a time) fits the stages");
-  static_assert(kQS * I::DK_LEN <= 160 * 1024 - 512, "three dK stages fit LDS");
-  static_assert(I::DV_LEN / 1024 / kNW >= 1 && I::DK_LEN / 1024 / kNW >= 1, "each wave copies part of each image");
+  static_assert(kQS * I::QB >= 4 * kT * (D + 4) * 4, "dk gather (four waves at a time) fits the stages");
+  static_assert(kQS * I::QB <= 160 * 1024 - 512, "the query-image stages fit LDS");
+  static_assert(I::QB / 1024 / kNW >= 1, "each wave copies part of each image");
   // the key images follow the query images in the workspace
   p.kimg = p.qimg + (size_t)B * p.Hq * p.nt * I::QB;
   const dim3 blk(256);
@@ -1034,13 +1048,13 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
     pq.pm = B * p.Hkv / 8 * p.nqb;
     pq.pr = pers ? max(1, min(res_dq, pq.pm)) : 0;
     const dim3 gq = pers ? dim3(8 * pq.pr) : dim3(p.nqb, B * p.Hkv);
-    hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX, CEX>), gq, dim3(kNWQ * 64), 2 * I::KB, stream, pq);
+    hipLaunchKernelGGL((sfa_bwd_dq_kernel<D, VEX, OEX, CEX>), gq, dim3(kNWQ * 64), kDqLds, stream, pq);
   }
-  static_assert(2 * I::QB <= 160 * 1024 && 2 * I::QB >= kNWF * kT * (D + 4) * 4, "fused dk/dv stages");
+  static_assert(kFLds <= 160 * 1024, "fused dk/dv stages");
   if constexpr (fused_dkv<D, VEX, OEX>()) {
     const int nkf = (p.n + kNWF * kT - 1) / (kNWF * kT);
     hipLaunchKernelGGL((sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>), dim3(nkf, B * p.Hkv), dim3(kNWF * 64),
-                       2 * I::QB, stream, p);
+                       kFLds, stream, p);
     return hipGetLastError();
   }
   p.nkb = (p.n + kNW * kT - 1) / (kNW * kT);
@@ -1050,9 +1064,9 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   pk.pr = pers ? max(1, min(res_dk, p.pm)) : 0;
   const dim3 gv = pers ? dim3(8 * pv.pr) : dim3(p.nkb, B * p.Hkv);
   const dim3 gk = pers ? dim3(8 * pk.pr) : dim3(p.nkb, B * p.Hkv);
-  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>), gv, dim3(kNW * 64), kQS * I::DV_LEN,
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>), gv, dim3(kNW * 64), kQS * I::QB,
                      stream, pv);
-  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>), gk, dim3(kNW * 64), kQS * I::DK_LEN,
+  hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>), gk, dim3(kNW * 64), kQS * I::QB,
                      stream, pk);
   return hipGetLastError();
 }
