@@ -220,9 +220,11 @@ sfa_status sfa_attn_fwd_index(const void* q_idx, const void* q_val,
  * dv            [B, Hkv, n, d] float32 out
  * ws, ws_bytes  caller-owned device workspace of at least
  *               sfa_attn_bwd_workspace(B, Hq, Hkv, n, d) bytes: tile images of
- *               the codes, V and dO written and read on the stream (0 bytes
- *               and ws unused for head dims other than 64 and 128).  Calls
- *               that overlap in time need separate workspaces.
+ *               the codes, V and dO, and partial gradients of the keys that
+ *               global tokens make every query see, written and read on the
+ *               stream (0 bytes and ws unused for head dims other than 64
+ *               and 128).  Calls that overlap in time need separate
+ *               workspaces.
  * Arithmetic: every product on the matrix cores with both operands split
  * into two bfloat16 pieces and three piece products kept (relative error
  * ~2^-16 of the sum of |terms|), float32 accumulation; P recomputed as

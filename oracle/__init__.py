@@ -9,5 +9,5 @@ from .sfa_oracle import (  # noqa: F401
     csr_bytes, softmax_attention_grad, attn_bwd, attn_bwd_rows, attn_bwd_cols,
     cache_location, cache_capacity, kv_append, cache_gather, attn_decode_paged,
     f16_rne, widen_f16, topk_encode_f16, csr_densify, csr_to_fixed, token_mask,
-    quant_q8, dequant_q8, kv_append_q8,
+    quant_q8, dequant_q8, kv_append_q8, stored_output,
 )

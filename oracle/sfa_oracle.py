@@ -533,14 +533,27 @@ def kv_append_q8(kc_idx, kc_val, kc_scale, v_cache, v_scale, k_new, v_new, seq_l
 # --------------------------------------------------------------------------
 
 
+def stored_output(o: np.ndarray, o_store) -> np.ndarray:
+    """The forward's output O as the backward receives it: o_store None keeps
+    it exact, "bf16" rounds it to the nearest bfloat16 (ties to even) through
+    float32, as a forward that writes O in bfloat16 stores it."""
+    if o_store is None:
+        return o
+    assert o_store == "bf16", o_store
+    return widen(bf16_rne(np.asarray(o, dtype=np.float64).astype(np.float32)))
+
+
 def softmax_attention_grad(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, do: np.ndarray,
-                           scale: float, causal: bool, window: int = 0, n_global: int = 0):
+                           scale: float, causal: bool, window: int = 0, n_global: int = 0,
+                           o_store=None):
     """Gradients of O = softmax(scale * qd kd^T, mask) v for one head, dense
     float64, queries at positions 0..r-1 and keys at 0..n_k-1; the mask is
     token_mask (causal, window, global tokens).
 
     With P the row-normalised weights: dV = P^T dO, dP = dO V^T,
-    dS = P * (dP - rowsum(dP * P)), dQ = scale dS K, dK = scale dS^T Q.
+    dS = P * (dP - D), dQ = scale dS K, dK = scale dS^T Q, where
+    D_i = dO_i . O_i = rowsum(dP * P)_i.  With o_store the backward takes O
+    as the forward stored it (stored_output), and D_i = dO_i . O_i uses that.
     Returns (dQ [r, d], dK [n_k, d], dV [n_k, dv])."""
     S = scale * (qd @ kd.T)
     if causal or window > 0:
@@ -550,12 +563,16 @@ def softmax_attention_grad(qd: np.ndarray, kd: np.ndarray, v: np.ndarray, do: np
     P /= P.sum(axis=1, keepdims=True)
     dV = P.T @ do
     dP = do @ v.T
-    dS = P * (dP - (dP * P).sum(axis=1, keepdims=True))
+    if o_store is None:
+        D = (dP * P).sum(axis=1, keepdims=True)
+    else:
+        D = (do * stored_output(P @ v, o_store)).sum(axis=1, keepdims=True)
+    dS = P * (dP - D)
     return scale * (dS @ kd), scale * (dS.T @ qd), dV
 
 
 def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bool,
-             window: int = 0, n_global: int = 0):
+             window: int = 0, n_global: int = 0, o_store=None):
     """SFA backward on codes (Sec. 3.1, Eq. (6)).
 
     Inputs as attn_fwd, plus do [B, Hq, n, dv] (float32, or uint16 bf16
@@ -563,7 +580,9 @@ def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bo
     its support and 0 elsewhere, so it is returned in code form:
     dq_val [B, Hq, n, k] with dq_val[..., t] the gradient at q_idx[..., t];
     likewise dk_val [B, Hkv, n, k].  dv [B, Hkv, n, dv].  A KV head's
-    gradients sum over the query heads that read it.  float64."""
+    gradients sum over the query heads that read it.  o_store: the stored
+    form of the forward's output that D_i = dO_i . O_i uses (stored_output).
+    float64."""
     B, Hq, n, k = np.shape(q_idx)
     Hkv = np.shape(k_idx)[1]
     G = Hq // Hkv
@@ -578,7 +597,7 @@ def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bo
             for h in range(g * G, (g + 1) * G):
                 qd = densify(q_idx[b, h], q_val[b, h], d)
                 gq, gk, gv = softmax_attention_grad(qd, kd, vv[b, g], dd[b, h], scale, causal,
-                                                    window, n_global)
+                                                    window, n_global, o_store)
                 dq[b, h] = np.take_along_axis(gq, np.asarray(q_idx[b, h], dtype=np.int64), 1)
                 dkd += gk
                 dv[b, g] += gv
@@ -587,10 +606,11 @@ def attn_bwd(q_idx, q_val, k_idx, k_val, v, do, d: int, scale: float, causal: bo
 
 
 def attn_bwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, do_bh, d: int, scale: float,
-                  causal: bool, rows, window: int = 0, n_global: int = 0):
+                  causal: bool, rows, window: int = 0, n_global: int = 0, o_store=None):
     """dq_val (Eq. (6)) of the selected query rows of one head, each row on
     its own: p = softmax over the row's allowed keys, dp = V do_i,
-    ds = p * (dp - p.dp), dq~ = scale ds K~, read at the row's support.
+    ds = p * (dp - D_i) with D_i = p.dp = do_i . o_i (o_i = p V, in its stored
+    form with o_store), dq~ = scale ds K~, read at the row's support.
     Returns [len(rows), k], float64."""
     kd = densify(k_idx_bg, k_val_bg, d)
     vv, dd = widen(v_bg), widen(do_bh)
@@ -602,20 +622,22 @@ def attn_bwd_rows(q_idx_bh, q_val_bh, k_idx_bg, k_val_bg, v_bg, do_bh, d: int, s
         p = np.exp(s - s.max())
         p /= p.sum()
         dp = vv[keys] @ dd[i]
-        ds = p * (dp - p @ dp)
+        Di = p @ dp if o_store is None else dd[i] @ stored_output(p @ vv[keys], o_store)
+        ds = p * (dp - Di)
         out[r] = (scale * (ds @ kd[keys]))[np.asarray(q_idx_bh[i], dtype=np.int64)]
     return out
 
 
 def attn_bwd_cols(q_idx_bg, q_val_bg, k_idx_bg, k_val_bg, v_bg, do_bg, d: int, scale: float,
                   causal: bool, cols, row_chunk: int = 1024, window: int = 0, n_global: int = 0,
-                  row_from: int = 0):
+                  row_from: int = 0, o_store=None):
     """dk_val and dv (Eq. (6)) of the selected keys of one KV head, summed
     over its query heads: q_*_bg [G, n, k], do_bg [G, n, dv].  Each query
     row's LSE_i and D_i = dO_i . O_i come from the plain forward
     (softmax_attention); then for key j and every query i that sees it,
     P_ij = exp(s_ij - LSE_i), dS_ij = P_ij (dO_i . v_j - D_i),
-    dv_j = sum_i P_ij dO_i and dk~_j = scale sum_i dS_ij q~_i.
+    dv_j = sum_i P_ij dO_i and dk~_j = scale sum_i dS_ij q~_i; with o_store,
+    D_i takes O in its stored form (stored_output).
     row_from > 0 (causal, no window, every column >= row_from): only query
     rows from row_from on are evaluated; the rows below see none of the
     columns (j <= i fails), so they would add only zeros.
@@ -635,7 +657,7 @@ def attn_bwd_cols(q_idx_bg, q_val_bg, k_idx_bg, k_val_bg, v_bg, do_bg, d: int, s
         do_h = dd[h][row_from:]
         O, L = softmax_attention(qd, kd, vv, scale, causal, pos=pos, row_chunk=row_chunk,
                                  window=window, n_global=n_global)
-        D = (do_h * O).sum(axis=1)
+        D = (do_h * stored_output(O, o_store)).sum(axis=1)
         S = scale * (qd @ kd[cols].T)                      # [rows, len(cols)]
         if causal or window > 0:
             allowed = token_mask(pos, n, causal, window, n_global)[:, cols]

@@ -25,8 +25,12 @@
 //       dV^T += dO^T P and dK~^T += Q~^T dS over the query tiles of every
 //       query head of the KV head;
 //   sfa_bwd_dkvf_kernel   both products from one S, P, dP, dS per tile pair
-//       (d = 64, bf16 V and O, in place of the two above).
-// Every output element is owned by one wavefront: no atomics.  The tile
+//       (d = 64, bf16 V and O, in place of the two above);
+//   sfa_bwd_split_sum_kernel  under a token window with global tokens, the
+//       sum of the partial dv, dk_val of key block 0, whose sweep over every
+//       query tile is split over several work items.
+// Every output element is owned by one wavefront (or, for a split block, by
+// the sum kernel, which adds the parts in a fixed order): no atomics.  The tile
 // images are copied global -> LDS with direct-to-LDS loads.  When the
 // (batch, KV head) pairs split evenly over the 8 XCDs and there is no token
 // window, the dq, dk and dv kernels run persistent grids whose workgroups on
@@ -100,6 +104,15 @@ struct BwdParams {
   int nkb;   // dk / dv key blocks (256 keys) per (batch, KV head)
   int pr;    // persistent grid of the launch: workgroups per XCD (0: one workgroup per block)
   int pm;    // persistent grid of the launch: blocks per XCD
+  // Token window with global tokens: key block 0 holds the global keys, which
+  // every query sees, so its sweep is far longer than any other block's; it
+  // is split over nsplit work items (1: no split), which write partial dv and
+  // dk_val for the block's keys ([nsplit][B * Hkv][kSplitKeys][d] floats
+  // each, dk_val rows k long) for sfa_bwd_split_sum_kernel to add up.
+  int nsplit;
+  int bhkv;  // B * Hkv
+  float* part_dv;
+  float* part_dk;
   float scale, c;  // c = scale * log2(e)
 };
 
@@ -149,6 +162,15 @@ __device__ __forceinline__ void dma(const unsigned char* src, unsigned char* dst
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
 
 constexpr int kQS = 3;  // query-image stages of the key-parallel kernels
+
+// Split of key block 0's sweep under a token window with global tokens.
+constexpr int kMaxSplit = 16;         // most work items sharing the sweep
+constexpr int kSplitKeys = kNW * kT;  // keys of a split block (the fused kernel's 128 fit)
+
+// Bytes of the partial dv and dk_val of the split blocks (dk_val rows are k <= d long).
+inline size_t split_part_bytes(int bhkv, int d) {
+  return (size_t)2 * kMaxSplit * bhkv * kSplitKeys * d * sizeof(float);
+}
 
 // vmcnt(N): at most N of this wave's loads outstanding.  Loads retire in issue
 // order, so with N no larger than the number of copies this wave issued for
@@ -556,8 +578,10 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
   // shortens as its first key grows; with this order the workgroups of an
   // XCD start each row together or end it together, and in between stay on
   // the same query tile, so one L2 fetch of an image serves all of them.
+  // With p.nsplit > 1 (one workgroup per block only) the first p.nsplit
+  // items of a head are the parts of key block 0's sweep.
   for (int prow = 0;; ++prow) {
-    int xb, bh;
+    int xb, bh, seg = 0;
     bool up = false;
     if (p.pr > 0) {
       const int w = (int)blockIdx.x >> 3;
@@ -570,7 +594,10 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
     } else {
       if (prow > 0) break;
       xcd_map((int)gridDim.x, xb, bh);
+      seg = xb < p.nsplit ? xb : 0;
+      xb = xb < p.nsplit ? 0 : xb - p.nsplit + 1;
     }
+    const bool part = p.nsplit > 1 && xb == 0;  // a part of block 0's sweep: partial results
     const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
     const int j0b = xb * (kNW * kT);  // most key tiles first: smallest j0 first
     const int jw0 = j0b + wave * kT;
@@ -615,8 +642,11 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
     }
     const int nrange = t_hi - t_lo + 1;
     const int total = p.G * (nrange + gq_end);
-    // step it of the sweep -> position in the downward order
-    auto ord = [&](int it) { return up ? total - 1 - it : it; };
+    // this item's steps of the sweep: [it_lo, it_lo + cnt)
+    const int it_lo = part ? (int)((int64_t)total * seg / p.nsplit) : 0;
+    const int cnt = part ? (int)((int64_t)total * (seg + 1) / p.nsplit) - it_lo : total;
+    // step it of the item -> position in the downward order
+    auto ord = [&](int it) { return up ? total - 1 - (it_lo + it) : it_lo + it; };
     auto tile_of = [&](int it) {
       const int x = ord(it) >> p.lg;
       return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
@@ -633,16 +663,16 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
     // consumed (vmcnt waits only for the one needed next)
     // every wave copies at least QB / 1024 / kNW blocks of an image
     constexpr int kMinCopies = QB / 1024 / kNW;
-    if (total > 0) dma<kNW>(qimg_of(0), smem, QB, wave, lane);
-    if (total > 1) dma<kNW>(qimg_of(1), smem + QB, QB, wave, lane);
-    if (total > 1) wait_vm_n<kMinCopies>(); else wait_vm();
+    if (cnt > 0) dma<kNW>(qimg_of(0), smem, QB, wave, lane);
+    if (cnt > 1) dma<kNW>(qimg_of(1), smem + QB, QB, wave, lane);
+    if (cnt > 1) wait_vm_n<kMinCopies>(); else wait_vm();
     __syncthreads();
-    for (int it = 0; it < total; ++it) {
+    for (int it = 0; it < cnt; ++it) {
       // The tile's LDS reads go through `cur` and the copy two tiles ahead
       // through `nxt`, both restrict: the compiler then knows the copy cannot
       // alias those reads and does not wait for it before them.
       auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
-      if (it + 2 < total) dma<kNW>(qimg_of(it + 2), nxt, QB, wave, lane);
+      if (it + 2 < cnt) dma<kNW>(qimg_of(it + 2), nxt, QB, wave, lane);
       const int q0 = tile_of(it) * kT;
       if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
         const unsigned char* Q = cur;
@@ -736,14 +766,15 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
       };
       tile(smem + (it % kQS) * QB, smem + ((it + 2) % kQS) * QB);
       // the next tile's copies must be complete; the one after may still run
-      if (it + 2 < total) wait_vm_n<kMinCopies>(); else wait_vm();
+      if (it + 2 < cnt) wait_vm_n<kMinCopies>(); else wait_vm();
       __syncthreads();
     }
 
     if constexpr (PART == kDV) {
       // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
       if (key_ok) {
-        float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
+        float* dvr = part ? p.part_dv + (((int64_t)seg * p.bhkv + bh) * kSplitKeys + my_j) * D
+                          : p.dv + ((int64_t)bh * n + my_j) * D;
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -767,9 +798,11 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
         __syncthreads();
         if (wave / 4 == round && key_ok) {
           const int64_t row = (int64_t)bh * n + my_j;
+          float* dkr = part ? p.part_dk + (((int64_t)seg * p.bhkv + bh) * kSplitKeys + my_j) * p.k
+                            : p.dk + row * p.k;
           for (int t = hh; t < p.k; t += 2) {
             const int u = load_idx(p.k_idx, row * p.k + t, p.ifmt, D - 1);
-            p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+            dkr[t] = p.scale * L[l32 * (D + 4) + u];
           }
         }
         __syncthreads();
@@ -792,6 +825,7 @@ __global__ __launch_bounds__(kNW * 64) void sfa_bwd_dkv_kernel(BwdParams p) {
 // qwen3_32k).
 // ---------------------------------------------------------------------------
 constexpr int kNWF = 4;
+static_assert(kNWF * kT <= kSplitKeys, "a split fused block fits the partial results");
 
 template <int D, bool VEX, bool OEX>
 constexpr bool fused_dkv() { return D == 64 && VEX && OEX; }
@@ -807,6 +841,10 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   const LaneOff<QRB> qo(lane);
   int xb, bh;
   xcd_map((int)gridDim.x, xb, bh);
+  // the first p.nsplit items of a head are the parts of key block 0's sweep
+  const int seg = xb < p.nsplit ? xb : 0;
+  xb = xb < p.nsplit ? 0 : xb - p.nsplit + 1;
+  const bool part = p.nsplit > 1 && xb == 0;  // partial results
   const int b = bh / p.Hkv, hkv = bh - b * p.Hkv;
   const int j0b = xb * (kNWF * kT);  // most query tiles first: smallest j0 first
   const int jw0 = j0b + wave * kT;
@@ -851,8 +889,11 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   }
   const int nrange = t_hi - t_lo + 1;
   const int total = p.G * (nrange + gq_end);
+  // this item's steps of the sweep: [it_lo, it_lo + cnt)
+  const int it_lo = part ? (int)((int64_t)total * seg / p.nsplit) : 0;
+  const int cnt = part ? (int)((int64_t)total * (seg + 1) / p.nsplit) - it_lo : total;
   auto tile_of = [&](int it) {
-    const int x = it >> p.lg;
+    const int x = (it_lo + it) >> p.lg;
     return x < nrange ? t_hi - x : gq_end - 1 - (x - nrange);
   };
   auto in_window = [&](int q0) {
@@ -860,15 +901,15 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
            (q0 < jw0 + kT - 1 + p.window && q0 + kT - 1 > jw0 - p.window);
   };
   auto qimg_of = [&](int it) {
-    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + (it & (p.G - 1))) * p.nt + tile_of(it)) * QB;
+    return p.qimg + ((int64_t)(b * p.Hq + hkv * p.G + ((it_lo + it) & (p.G - 1))) * p.nt + tile_of(it)) * QB;
   };
-  if (total > 0) dma<kNWF>(qimg_of(0), smem, QB, wave, lane);
+  if (cnt > 0) dma<kNWF>(qimg_of(0), smem, QB, wave, lane);
   wait_vm();
   __syncthreads();
-  for (int it = 0; it < total; ++it) {
+  for (int it = 0; it < cnt; ++it) {
     // reads through `cur`, the copy of the next image through `nxt`
     auto tile = [&](const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt) {
-    if (it + 1 < total) dma<kNWF>(qimg_of(it + 1), nxt, QB, wave, lane);
+    if (it + 1 < cnt) dma<kNWF>(qimg_of(it + 1), nxt, QB, wave, lane);
     const int q0 = tile_of(it) * kT;
     if (wave_ok && (!p.causal || q0 + kT - 1 >= jw0) && in_window(q0)) {
       const float* l2 = (const float*)(cur + I::Q_L2);
@@ -956,7 +997,8 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
 
   // dv: lane = key my_j, register r of block db = dimension db*32 + 8(r/4) + 4hh + r%4
   if (key_ok) {
-    float* dvr = p.dv + ((int64_t)bh * n + my_j) * D;
+    float* dvr = part ? p.part_dv + (((int64_t)seg * p.bhkv + bh) * kSplitKeys + my_j) * D
+                      : p.dv + ((int64_t)bh * n + my_j) * D;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -975,10 +1017,36 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   __syncthreads();
   if (key_ok) {
     const int64_t row = (int64_t)bh * n + my_j;
+    float* dkr = part ? p.part_dk + (((int64_t)seg * p.bhkv + bh) * kSplitKeys + my_j) * p.k
+                      : p.dk + row * p.k;
     for (int t = hh; t < p.k; t += 2) {
       const int u = load_idx(p.k_idx, row * p.k + t, p.ifmt, D - 1);
-      p.dk[row * p.k + t] = p.scale * L[l32 * (D + 4) + u];
+      dkr[t] = p.scale * L[l32 * (D + 4) + u];
     }
+  }
+}
+
+// dv and dk_val of key block 0's keys after a split sweep: the sum of the
+// parts' partial results, in part order (the same on every run).  Workgroup
+// (x, bh) takes keys 16 x .. 16 x + 15 of head bh.
+__global__ __launch_bounds__(256) void sfa_bwd_split_sum_kernel(BwdParams p, int D) {
+  const int bh = blockIdx.y, j0 = blockIdx.x * 16;
+  const int nk = min(16, p.n - j0);
+  if (nk <= 0) return;
+  const size_t ps = (size_t)p.bhkv * kSplitKeys;  // keys between two parts
+  for (int e = threadIdx.x; e < nk * D; e += 256) {
+    const int j = j0 + e / D, c = e % D;
+    const float* src = p.part_dv + ((size_t)bh * kSplitKeys + j) * D + c;
+    float acc = 0.f;
+    for (int sg = 0; sg < p.nsplit; ++sg) acc += src[sg * ps * D];
+    p.dv[((int64_t)bh * p.n + j) * D + c] = acc;
+  }
+  for (int e = threadIdx.x; e < nk * p.k; e += 256) {
+    const int j = j0 + e / p.k, t = e % p.k;
+    const float* src = p.part_dk + ((size_t)bh * kSplitKeys + j) * p.k + t;
+    float acc = 0.f;
+    for (int sg = 0; sg < p.nsplit; ++sg) acc += src[sg * ps * p.k];
+    p.dk[((int64_t)bh * p.n + j) * p.k + t] = acc;
   }
 }
 
@@ -1034,8 +1102,23 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   static_assert(kQS * I::QB >= 4 * kT * (D + 4) * 4, "dk gather (four waves at a time) fits the stages");
   static_assert(kQS * I::QB <= 160 * 1024 - 512, "the query-image stages fit LDS");
   static_assert(I::QB / 1024 / kNW >= 1, "each wave copies part of each image");
-  // the key images follow the query images in the workspace
+  // the key images follow the query images in the workspace, then the
+  // partial results of a split block
   p.kimg = p.qimg + (size_t)B * p.Hq * p.nt * I::QB;
+  p.part_dv = (float*)(p.kimg + (size_t)B * p.Hkv * p.nt * I::KB);
+  p.part_dk = p.part_dv + (size_t)kMaxSplit * p.bhkv * kSplitKeys * D;
+  // Under a token window with global tokens, key block 0 (which holds them)
+  // sweeps every query tile, a windowed block about (its keys + the window)
+  // / 32 of them (twice the window without causal masking): block 0's sweep
+  // is split so that no part is much longer than a windowed block's.
+  // (Blocks past the first that hold global keys, n_global > their first
+  // key, keep their whole sweep.)
+  p.nsplit = 1;
+  if (p.window > 0 && p.n_global > 0) {
+    const int keys = fused_dkv<D, VEX, OEX>() ? kNWF * kT : kNW * kT;
+    const int typ = (keys + (p.causal ? 1 : 2) * p.window) / kT + 1;
+    p.nsplit = std::min(kMaxSplit, std::max(1, (p.nt + typ - 1) / typ));
+  }
   const dim3 blk(256);
   hipLaunchKernelGGL((sfa_bwd_qprep_kernel<D, OEX>), dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
   hipLaunchKernelGGL((sfa_bwd_kprep_kernel<D, VEX>), dim3(p.nt, B * p.Hkv), blk, I::KB, stream, p);
@@ -1053,8 +1136,10 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   static_assert(kFLds <= 160 * 1024, "fused dk/dv stages");
   if constexpr (fused_dkv<D, VEX, OEX>()) {
     const int nkf = (p.n + kNWF * kT - 1) / (kNWF * kT);
-    hipLaunchKernelGGL((sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>), dim3(nkf, B * p.Hkv), dim3(kNWF * 64),
-                       kFLds, stream, p);
+    hipLaunchKernelGGL((sfa_bwd_dkvf_kernel<D, VEX, OEX, CEX>), dim3(nkf + p.nsplit - 1, B * p.Hkv),
+                       dim3(kNWF * 64), kFLds, stream, p);
+    if (p.nsplit > 1)
+      hipLaunchKernelGGL(sfa_bwd_split_sum_kernel, dim3(kNWF * kT / 16, B * p.Hkv), dim3(256), 0, stream, p, D);
     return hipGetLastError();
   }
   p.nkb = (p.n + kNW * kT - 1) / (kNW * kT);
@@ -1062,12 +1147,15 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   BwdParams pv = p, pk = p;
   pv.pr = pers ? max(1, min(res_dv, p.pm)) : 0;
   pk.pr = pers ? max(1, min(res_dk, p.pm)) : 0;
-  const dim3 gv = pers ? dim3(8 * pv.pr) : dim3(p.nkb, B * p.Hkv);
-  const dim3 gk = pers ? dim3(8 * pk.pr) : dim3(p.nkb, B * p.Hkv);
+  // (a split sweep only with a token window, which has no persistent grid)
+  const dim3 gv = pers ? dim3(8 * pv.pr) : dim3(p.nkb + p.nsplit - 1, B * p.Hkv);
+  const dim3 gk = pers ? dim3(8 * pk.pr) : dim3(p.nkb + p.nsplit - 1, B * p.Hkv);
   hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDV>), gv, dim3(kNW * 64), kQS * I::QB,
                      stream, pv);
   hipLaunchKernelGGL((sfa_bwd_dkv_kernel<D, VEX, OEX, CEX, kDK>), gk, dim3(kNW * 64), kQS * I::QB,
                      stream, pk);
+  if (p.nsplit > 1)
+    hipLaunchKernelGGL(sfa_bwd_split_sum_kernel, dim3(kNW * kT / 16, B * p.Hkv), dim3(256), 0, stream, p, D);
   return hipGetLastError();
 }
 
@@ -1080,7 +1168,7 @@ size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d) {
   const size_t nt = (size_t)((n + kT - 1) / kT);
   const size_t qb = d == 64 ? Img<64>::QB : Img<128>::QB;
   const size_t kb = d == 64 ? Img<64>::KB : Img<128>::KB;
-  return (size_t)B * Hq * nt * qb + (size_t)B * Hkv * nt * kb;
+  return (size_t)B * Hq * nt * qb + (size_t)B * Hkv * nt * kb + split_part_bytes(B * Hkv, d);
 }
 
 hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,
@@ -1100,6 +1188,9 @@ hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_i
   p.nqb = (n + p.BR - 1) / p.BR;
   p.lg = __builtin_ctz((unsigned)p.G);  // G is a power of two here (checked by the caller)
   p.nkb = p.pr = p.pm = 0;  // set by launch_d for the dk / dv kernels
+  p.nsplit = 1;
+  p.bhkv = B * Hkv;
+  p.part_dv = p.part_dk = nullptr;  // set by launch_d
   p.scale = scale;
   p.c = (float)((double)scale * 1.4426950408889634);
   // (images of the bf16 dO / V layouts are smaller than the workspace's)

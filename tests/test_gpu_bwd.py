@@ -42,7 +42,8 @@ def _run(B, Hq, Hkv, n, d, k, causal, v_bf16, seed, o_bf16=False, val_dtype=torc
     # the GPU and oracle codes are bit-identical (encoder parity), so the
     # gradients line up entry by entry
     assert np.array_equal(qi.cpu().numpy(), oqi) and np.array_equal(ki.cpu().numpy(), oki)
-    gq, gk, gv = oracle.attn_bwd(oqi, oqv, oki, okv, np_vals(v), np_vals(dout), d, scale, causal)
+    gq, gk, gv = oracle.attn_bwd(oqi, oqv, oki, okv, np_vals(v), np_vals(dout), d, scale, causal,
+                                 o_store="bf16" if o_bf16 else None)
     tol = TOL_GRAD[(v_bf16, o_bf16)]
     e = (check_grad(dq, gq, tol, "dq_val"), check_grad(dk, gk, tol, "dk_val"),
          check_grad(dv, gv, tol, "dv"))
@@ -127,7 +128,7 @@ def test_d64_bf16_fused_window():
     torch.cuda.synchronize()
     gq, gk, gv = oracle.attn_bwd(qi.cpu().numpy(), qv.cpu().numpy(), ki.cpu().numpy(),
                                  kv.cpu().numpy(), np_vals(v), np_vals(dout), d, scale, True,
-                                 window=w, n_global=g)
+                                 window=w, n_global=g, o_store="bf16")
     tol = TOL_GRAD[(True, True)]
     check_grad(dq, gq, tol, "dq_val (fused d = 64, window)")
     check_grad(dk, gk, tol, "dk_val (fused d = 64, window)")
@@ -226,12 +227,14 @@ def test_qwen3_32k_full_size_sampled():
     rows = np.unique(np.concatenate([[0, 1, 31, 32, 4095, 16383, n - 1], rng.integers(0, n, 9)]))
     for h in (G * g, G * g + 3):
         oqi, oqv = oracle.topk_encode(q[0, h].cpu().numpy(), k)
-        ref = oracle.attn_bwd_rows(oqi, oqv, oki, okv, vn, dn[h], d, w.scale, True, rows)
+        ref = oracle.attn_bwd_rows(oqi, oqv, oki, okv, vn, dn[h], d, w.scale, True, rows,
+                                   o_store="bf16")
         check_grad(dq[0, h, torch.from_numpy(rows).to(DEV)], ref, tol, f"dq_val head {h}")
     cols = np.unique(np.concatenate([[0, 1, 63, 127, 128, 20000, n - 1], rng.integers(0, n, 9)]))
     qc = [oracle.topk_encode(q[0, h].cpu().numpy(), k) for h in range(G * g, G * g + G)]
     gk, gv = oracle.attn_bwd_cols(np.stack([c[0] for c in qc]), np.stack([c[1] for c in qc]),
-                                  oki, okv, vn, dn[G * g:G * g + G], d, w.scale, True, cols)
+                                  oki, okv, vn, dn[G * g:G * g + G], d, w.scale, True, cols,
+                                  o_store="bf16")
     sel = torch.from_numpy(cols).to(DEV)
     check_grad(dk[0, g, sel], gk, tol, f"dk_val KV head {g}")
     check_grad(dv[0, g, sel], gv, tol, f"dv KV head {g}")
@@ -243,14 +246,14 @@ def test_qwen3_32k_full_size_sampled():
         hq = g2 % G  # one query head of the group
         rows2 = np.unique(np.concatenate([[0, 255, 256, n - 1], rng.integers(0, n, 4)]))
         ref = oracle.attn_bwd_rows(qc2[hq][0], qc2[hq][1], oki2, okv2, vn2, dn[G * g2 + hq], d,
-                                   w.scale, True, rows2)
+                                   w.scale, True, rows2, o_store="bf16")
         check_grad(dq[0, G * g2 + hq, torch.from_numpy(rows2).to(DEV)], ref, tol,
                    f"dq_val head {G * g2 + hq}")
         cols2 = np.unique(np.concatenate([[tail, n - 257, n - 256, n - 1],
                                           rng.integers(tail, n, 4)]))
         gk2, gv2 = oracle.attn_bwd_cols(np.stack([c[0] for c in qc2]), np.stack([c[1] for c in qc2]),
                                         oki2, okv2, vn2, dn[G * g2:G * g2 + G], d, w.scale, True,
-                                        cols2, row_from=tail)
+                                        cols2, row_from=tail, o_store="bf16")
         sel2 = torch.from_numpy(cols2).to(DEV)
         check_grad(dk[0, g2, sel2], gk2, tol, f"dk_val KV head {g2} (last keys)")
         check_grad(dv[0, g2, sel2], gv2, tol, f"dv KV head {g2} (last keys)")
@@ -299,12 +302,13 @@ def test_persistent_grid_sampled(B, Hq, Hkv, n, d, k, causal, bf16, win, ng):
         qc = [oracle.topk_encode(q[b, h].cpu().numpy(), k) for h in range(G * g, G * g + G)]
         for h in sorted({0, G - 1}):
             ref = oracle.attn_bwd_rows(qc[h][0], qc[h][1], oki, okv, vn, dn[G * g + h], d, scale,
-                                       causal, rows, window=win, n_global=ng)
+                                       causal, rows, window=win, n_global=ng,
+                                       o_store="bf16" if bf16 else None)
             check_grad(dq[b, G * g + h, torch.from_numpy(rows).to(DEV)], ref, tol,
                        f"dq_val batch {b} head {G * g + h}")
         gk, gv = oracle.attn_bwd_cols(np.stack([c[0] for c in qc]), np.stack([c[1] for c in qc]),
                                       oki, okv, vn, dn[G * g:G * g + G], d, scale, causal, cols,
-                                      window=win, n_global=ng)
+                                      window=win, n_global=ng, o_store="bf16" if bf16 else None)
         sel = torch.from_numpy(cols).to(DEV)
         check_grad(dk[b, g, sel], gk, tol, f"dk_val batch {b} KV head {g}")
         check_grad(dv[b, g, sel], gv, tol, f"dv batch {b} KV head {g}")

@@ -185,6 +185,43 @@ def test_bwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
     check_grad(dv, gv, tol, f"dv window {w} global {g}")
 
 
+@pytest.mark.parametrize("Hq,Hkv,n,d,k,causal,v_bf16,o_bf16,w,g", [
+    (4, 1, 2048, 128, 16, True, True, False, 128, 4),     # dK / dV kernels, 5 parts
+    (2, 2, 2000, 128, 16, False, False, False, 100, 5),   # without causal masking
+    (4, 2, 2048, 64, 8, True, True, True, 64, 4),         # fused d = 64 kernel, 10 parts
+    (2, 1, 1500, 64, 8, False, True, True, 50, 33),       # fused, global keys in two tiles
+])
+def test_bwd_window_split(Hq, Hkv, n, d, k, causal, v_bf16, o_bf16, w, g):
+    """Token window with global tokens over sequences long enough that key
+    block 0's sweep (every query sees the global keys) is split over several
+    work items and their partial results summed: every gradient against the
+    oracle, and two runs bitwise identical."""
+    B = 1
+    seed = 7 * n + w + g
+    q, kk, v = si.dense_qkv(B, Hq, Hkv, n, d, seed, device=DEV,
+                            v_dtype=torch.bfloat16 if v_bf16 else torch.float32)
+    qi, qv = sfa.sfa_topk_encode(q, k)
+    ki, kv = sfa.sfa_topk_encode(kk, k)
+    scale = 1 / math.sqrt(d)
+    odt = torch.bfloat16 if o_bf16 else torch.float32
+    o, lse = sfa.sfa_attn_fwd(qi, qv, ki, kv, v, causal=causal, scale=scale, o_dtype=odt,
+                              window=w, n_global=g)
+    dout = si.normal((B, Hq, n, d), seed, "dout", device=DEV).to(odt)
+    dq, dk, dv = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale,
+                                  window=w, n_global=g)
+    dq2, dk2, dv2 = sfa.sfa_attn_bwd(qi, qv, ki, kv, v, o, lse, dout, causal=causal, scale=scale,
+                                     window=w, n_global=g)
+    torch.cuda.synchronize()
+    assert torch.equal(dq, dq2) and torch.equal(dk, dk2) and torch.equal(dv, dv2)
+    gq, gk, gv = oracle.attn_bwd(qi.cpu().numpy(), qv.cpu().numpy(), ki.cpu().numpy(),
+                                 kv.cpu().numpy(), np_vals(v), np_vals(dout), d, scale, causal,
+                                 window=w, n_global=g, o_store="bf16" if o_bf16 else None)
+    tol = TOL_GRAD[(v_bf16, o_bf16)]
+    check_grad(dq, gq, tol, f"dq_val window {w} global {g} (split)")
+    check_grad(dk, gk, tol, f"dk_val window {w} global {g} (split)")
+    check_grad(dv, gv, tol, f"dv window {w} global {g} (split)")
+
+
 def test_bwd_window_qwen3_32k_sampled():
     """Backward on the 32K GQA workload with a 4096-token window and 4 global
     tokens (bf16 V, O, dO): dq rows of one head and dk, dv keys of one KV head
@@ -216,12 +253,14 @@ def test_bwd_window_qwen3_32k_sampled():
     rows = np.array([0, 3, 4, 4095, 4096, 4160, 20000, n - 1])
     h = G * g + 1
     ref = oracle.attn_bwd_rows(qi[0, h].cpu().numpy(), qv[0, h].cpu().numpy(), oki, okv, vn,
-                               dn[h], d, w_.scale, True, rows, window=win, n_global=ng)
+                               dn[h], d, w_.scale, True, rows, window=win, n_global=ng,
+                               o_store="bf16")
     check_grad(dq[0, h, torch.from_numpy(rows).to(DEV)], ref, tol, f"dq_val window head {h}")
     cols = np.array([0, 3, 4, 100, 4095, 4096, 30000, n - 1])
     hs = slice(G * g, G * g + G)
     gk, gv = oracle.attn_bwd_cols(qi[0, hs].cpu().numpy(), qv[0, hs].cpu().numpy(), oki, okv, vn,
-                                  dn[hs], d, w_.scale, True, cols, window=win, n_global=ng)
+                                  dn[hs], d, w_.scale, True, cols, window=win, n_global=ng,
+                                  o_store="bf16")
     sel = torch.from_numpy(cols).to(DEV)
     check_grad(dk[0, g, sel], gk, tol, f"dk_val window KV head {g}")
     check_grad(dv[0, g, sel], gv, tol, f"dv window KV head {g}")

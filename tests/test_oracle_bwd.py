@@ -14,7 +14,10 @@ that do not share that derivation:
   * identities: sum_j dV_j = sum_i dO_i (each row of P sums to one), and
     the first query under the causal mask (its only key is key 0, weight 1
     whatever the score) has dq = 0;
-  * the sampled row / column forms agree with the full backward.
+  * the sampled row / column forms agree with the full backward;
+  * O in its stored (bf16) form: unchanged results when every O_i is exact
+    in bf16, and otherwise shifts of dq and dk that the forward oracle and
+    the D-free dV part give independently.
 """
 import math
 
@@ -160,3 +163,66 @@ def test_rows_and_cols_match_the_full_backward():
                                                 row_from=17)
                 assert np.abs(gk2 - dk[0, g, late]).max() < 1e-12
                 assert np.abs(gv2 - dvv[0, g, late]).max() < 1e-12
+
+
+def test_stored_output_exact_in_bf16_changes_nothing():
+    """V rows all equal to one bf16-exact vector: every O_i is that vector
+    (the weights sum to one), its bf16 form is exact, and D_i, hence every
+    gradient, is the same as with the exact output."""
+    rng = np.random.default_rng(21)
+    B, Hq, Hkv, n, d, k = 1, 4, 2, 24, 16, 4
+    qi, qv, ki, kv, _, do = _case(rng, B, Hq, Hkv, n, d, k)
+    row = rng.integers(-8, 9, size=d).astype(np.float32)
+    v = np.broadcast_to(row, (B, Hkv, n, d)).copy()
+    for causal in (True, False):
+        a = oracle.attn_bwd(qi, qv, ki, kv, v, do, d, 0.3, causal)
+        b = oracle.attn_bwd(qi, qv, ki, kv, v, do, d, 0.3, causal, o_store="bf16")
+        for x, y in zip(a, b):
+            assert np.abs(x - y).max() < 1e-12
+
+
+def test_stored_output_shifts_dq_dk_as_the_forward_predicts():
+    """With O rounded to bf16, D_i moves by dD_i = dO_i . (bf16(O_i) - O_i),
+    so dS_ij moves by -P_ij dD_i:
+      dq~_i moves by -scale dD_i sum_j P_ij k~_j, the forward's output with
+        V replaced by the dense key codes;
+      dk~_j moves by -scale sum_i P_ij dD_i q~_i, the backward's dV (which
+        has no D term) with dO_i replaced by dD_i q~_i;
+      dV does not move."""
+    rng = np.random.default_rng(23)
+    B, Hq, Hkv, n, d, k = 1, 4, 2, 28, 16, 4
+    G = Hq // Hkv
+    scale = 0.35
+    qi, qv, ki, kv, v, do = _case(rng, B, Hq, Hkv, n, d, k)
+    for causal in (True, False):
+        dq0, dk0, dv0 = oracle.attn_bwd(qi, qv, ki, kv, v, do, d, scale, causal)
+        dq1, dk1, dv1 = oracle.attn_bwd(qi, qv, ki, kv, v, do, d, scale, causal, o_store="bf16")
+        assert np.abs(dv1 - dv0).max() < 1e-12
+        O, _ = oracle.attn_fwd(qi, qv, ki, kv, v, d, scale, causal)
+        dD = (do.astype(np.float64) * (oracle.stored_output(O, "bf16") - O)).sum(axis=-1)
+        assert np.abs(dD).max() > 0  # the rounding does move D here
+        kd = np.stack([oracle.densify(ki[0, g], kv[0, g], d) for g in range(Hkv)])[None]
+        OK, _ = oracle.attn_fwd(qi, qv, ki, kv, kd, d, scale, causal)      # sum_j P_ij k~_j
+        shift_q = -scale * dD[..., None] * OK
+        want_q = dq0 + np.take_along_axis(shift_q, qi.astype(np.int64), -1)
+        assert np.abs(dq1 - want_q).max() < 1e-12
+        qd = np.stack([oracle.densify(qi[0, h], qv[0, h], d) for h in range(Hq)])[None]
+        _, _, pq = oracle.attn_bwd(qi, qv, ki, kv, np.zeros((B, Hkv, n, d)), dD[..., None] * qd,
+                                   d, scale, causal)                        # sum_i P_ij dD_i q~_i
+        shift_k = -scale * pq
+        want_k = dk0 + np.take_along_axis(shift_k, ki.astype(np.int64), -1)
+        assert np.abs(dk1 - want_k).max() < 1e-12
+        # the sampled forms take the same stored output
+        rows = [0, 9, 27]
+        for h in range(Hq):
+            g = h // G
+            got = oracle.attn_bwd_rows(qi[0, h], qv[0, h], ki[0, g], kv[0, g], v[0, g], do[0, h],
+                                       d, scale, causal, rows, o_store="bf16")
+            assert np.abs(got - dq1[0, h, rows]).max() < 1e-12
+        cols = [0, 13, 27]
+        for g in range(Hkv):
+            hs = slice(g * G, g * G + G)
+            gk, gv = oracle.attn_bwd_cols(qi[0, hs], qv[0, hs], ki[0, g], kv[0, g], v[0, g],
+                                          do[0, hs], d, scale, causal, cols, o_store="bf16")
+            assert np.abs(gk - dk1[0, g, cols]).max() < 1e-12
+            assert np.abs(gv - dv1[0, g, cols]).max() < 1e-12
