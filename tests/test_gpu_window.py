@@ -190,6 +190,8 @@ def test_bwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
     (2, 2, 2000, 128, 16, False, False, False, 100, 5),   # without causal masking
     (4, 2, 2048, 64, 8, True, True, True, 64, 4),         # fused d = 64 kernel, 10 parts
     (2, 1, 1500, 64, 8, False, True, True, 50, 33),       # fused, global keys in two tiles
+    (2, 1, 1200, 128, 16, True, True, False, 100, 300),   # global keys past block 0 (whole sweep)
+    (2, 2, 1200, 64, 8, True, True, True, 64, 300),       # the same with the fused kernel's blocks
 ])
 def test_bwd_window_split(Hq, Hkv, n, d, k, causal, v_bf16, o_bf16, w, g):
     """Token window with global tokens over sequences long enough that key
