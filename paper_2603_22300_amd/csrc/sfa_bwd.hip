@@ -167,9 +167,9 @@ constexpr int kQS = 3;  // query-image stages of the key-parallel kernels
 constexpr int kMaxSplit = 16;         // most work items sharing the sweep
 constexpr int kSplitKeys = kNW * kT;  // keys of a split block (the fused kernel's 128 fit)
 
-// Bytes of the partial dv and dk_val of the split blocks (dk_val rows are k <= d long).
+// Bytes of one part's partial dv and dk_val (dk_val rows are k <= d long).
 inline size_t split_part_bytes(int bhkv, int d) {
-  return (size_t)2 * kMaxSplit * bhkv * kSplitKeys * d * sizeof(float);
+  return (size_t)2 * bhkv * kSplitKeys * d * sizeof(float);
 }
 
 // vmcnt(N): at most N of this wave's loads outstanding.  Loads retire in issue
@@ -1026,6 +1026,23 @@ __global__ __launch_bounds__(kNWF * 64) void sfa_bwd_dkvf_kernel(BwdParams p) {
   }
 }
 
+// Workspace bytes of the tile images in the largest layout (float32 dO and V).
+inline size_t bwd_image_bytes(int B, int Hq, int Hkv, int n, int d) {
+  const size_t nt = (size_t)((n + kT - 1) / kT);
+  const size_t qb = d == 64 ? Img<64>::QB : Img<128>::QB;
+  const size_t kb = d == 64 ? Img<64>::KB : Img<128>::KB;
+  return (size_t)B * Hq * nt * qb + (size_t)B * Hkv * nt * kb;
+}
+
+// Parts a split sweep may use for these sizes: at most kMaxSplit, with their
+// partial results at most 1/8 of the tile images' bytes (short sequences
+// would otherwise pay more for them than for the images); 0 (no split) when
+// fewer than two fit.  The workspace holds this many parts' results.
+inline int split_parts_max(int B, int Hq, int Hkv, int n, int d) {
+  const size_t m = bwd_image_bytes(B, Hq, Hkv, n, d) / 8 / split_part_bytes(B * Hkv, d);
+  return m >= 2 ? (int)std::min<size_t>(m, kMaxSplit) : 0;
+}
+
 // dv and dk_val of key block 0's keys after a split sweep: the sum of the
 // parts' partial results, in part order (the same on every run).  Workgroup
 // (x, bh) takes keys 16 x .. 16 x + 15 of head bh.
@@ -1105,8 +1122,9 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   // the key images follow the query images in the workspace, then the
   // partial results of a split block
   p.kimg = p.qimg + (size_t)B * p.Hq * p.nt * I::QB;
+  const int parts = split_parts_max(B, p.Hq, p.Hkv, p.n, D);
   p.part_dv = (float*)(p.kimg + (size_t)B * p.Hkv * p.nt * I::KB);
-  p.part_dk = p.part_dv + (size_t)kMaxSplit * p.bhkv * kSplitKeys * D;
+  p.part_dk = p.part_dv + (size_t)parts * p.bhkv * kSplitKeys * D;
   // Under a token window with global tokens, key block 0 (which holds them)
   // sweeps every query tile, a windowed block about (its keys + the window)
   // / 32 of them (twice the window without causal masking): block 0's sweep
@@ -1114,10 +1132,10 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
   // (Blocks past the first that hold global keys, n_global > their first
   // key, keep their whole sweep.)
   p.nsplit = 1;
-  if (p.window > 0 && p.n_global > 0) {
+  if (p.window > 0 && p.n_global > 0 && parts >= 2) {
     const int keys = fused_dkv<D, VEX, OEX>() ? kNWF * kT : kNW * kT;
     const int typ = (keys + (p.causal ? 1 : 2) * p.window) / kT + 1;
-    p.nsplit = std::min(kMaxSplit, std::max(1, (p.nt + typ - 1) / typ));
+    p.nsplit = std::min(parts, std::max(1, (p.nt + typ - 1) / typ));
   }
   const dim3 blk(256);
   hipLaunchKernelGGL((sfa_bwd_qprep_kernel<D, OEX>), dim3(p.nt, B * p.Hq), blk, I::QB, stream, p);
@@ -1165,10 +1183,8 @@ hipError_t launch_d(BwdParams p, int B, hipStream_t stream) {
 int bwd_max_group() { return kNWQ; }
 
 size_t bwd_workspace_bytes(int B, int Hq, int Hkv, int n, int d) {
-  const size_t nt = (size_t)((n + kT - 1) / kT);
-  const size_t qb = d == 64 ? Img<64>::QB : Img<128>::QB;
-  const size_t kb = d == 64 ? Img<64>::KB : Img<128>::KB;
-  return (size_t)B * Hq * nt * qb + (size_t)B * Hkv * nt * kb + split_part_bytes(B * Hkv, d);
+  return bwd_image_bytes(B, Hq, Hkv, n, d) +
+         (size_t)split_parts_max(B, Hq, Hkv, n, d) * split_part_bytes(B * Hkv, d);
 }
 
 hipError_t launch_attn_bwd(const void* q_idx, const void* q_val, const void* k_idx,

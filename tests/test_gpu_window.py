@@ -187,11 +187,11 @@ def test_bwd_window(B, Hq, Hkv, n, d, k, causal, v_bf16, w, g):
 
 @pytest.mark.parametrize("Hq,Hkv,n,d,k,causal,v_bf16,o_bf16,w,g", [
     (4, 1, 2048, 128, 16, True, True, False, 128, 4),     # dK / dV kernels, 5 parts
-    (2, 2, 2000, 128, 16, False, False, False, 100, 5),   # without causal masking
-    (4, 2, 2048, 64, 8, True, True, True, 64, 4),         # fused d = 64 kernel, 10 parts
+    (2, 2, 2000, 128, 16, False, False, False, 100, 5),   # without causal masking, 2 parts
+    (4, 2, 2048, 64, 8, True, True, True, 64, 4),         # fused d = 64 kernel, 3 parts
     (2, 1, 1500, 64, 8, False, True, True, 50, 33),       # fused, global keys in two tiles
-    (2, 1, 1200, 128, 16, True, True, False, 100, 300),   # global keys past block 0 (whole sweep)
-    (2, 2, 1200, 64, 8, True, True, True, 64, 300),       # the same with the fused kernel's blocks
+    (4, 1, 1200, 128, 16, True, True, False, 100, 300),   # block 0 in 3 parts, block 1 (global
+    (8, 1, 1200, 64, 8, True, True, True, 64, 300),       # keys too) whole; fused: 6 parts
 ])
 def test_bwd_window_split(Hq, Hkv, n, d, k, causal, v_bf16, o_bf16, w, g):
     """Token window with global tokens over sequences long enough that key
