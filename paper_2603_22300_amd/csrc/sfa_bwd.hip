@@ -59,8 +59,8 @@ constexpr float kLog2e = 1.44269504088896340736f;
 // chunk c ^ ((r / 4) % 4).  The one layout then serves, free of LDS bank
 // conflicts, both the row operands (16-byte reads, a row per lane) and the
 // transposed operands (ds_read_b64_tr_b16: 8 bytes of a row per lane, four
-// consecutive rows per 16 lanes): no transposed copy is stored.  The query image ends with log2(e) * LSE and D of its 32
-// rows.
+// consecutive rows per 16 lanes): no transposed copy is stored.  The query
+// image ends with log2(e) * LSE and D of its 32 rows.
 template <int D, bool OEX = false, bool VEX = false>
 struct Img {
   static constexpr int PO = OEX ? 1 : 2, PV = VEX ? 1 : 2;  // pieces kept of dO and V
